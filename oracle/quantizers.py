@@ -1,0 +1,353 @@
+"""Gradient, activation and weight quantizers (oracle; test infrastructure only).
+
+Paper: Chen et al. 2020, "A Statistical Framework for Low-bitwidth Training of
+Deep Neural Networks".
+
+* PTQ, per-tensor quantizer, Sec. 3.3: Q(X) = SR(s (X - z)) / s + z with
+  z = min X, s = B / R(X), R(X) = max X - min X, B = 2^b - 1.  The deterministic
+  variant (nearest rounding) is the Q_f / Q_theta of App. E.
+* PSQ, per-sample quantizer, Sec. 4.1 and App. C.3: the same per row i with
+  s_i = B / R(row i) (the optimum of the per-sample problem); z_i = row min.
+* BHQ, block Householder quantizer, Sec. 4.2, App. C.4 and App. D: rows sorted
+  by their infinity norm; each group holds one large row and k-1 small rows;
+  the group's scale block is Q diag(s1, s2, ..., s2) with Q the Householder
+  reflection whose normal is 1/sqrt(k) - e_1, and s1, s2 the closed form of
+  App. C.4.
+
+Readings where the paper is silent (each is listed with its reason in the
+design notes of the repository):
+  * R = 0 gives s = 1; B/R beyond the float32 range saturates at FLT_MAX;
+  * a rounded code is clamped to [0, B];
+  * PSQ zero point is the row minimum (by analogy with PTQ);
+  * BHQ with a fixed block size k: G = ceil(N/k) groups; group g takes the
+    g-th largest row plus the next k-1 rows of the sorted tail, in order;
+  * BHQ zero point: one offset c_g per group in the transformed domain,
+    c_g = alpha s1 min(large row) - lambda2 s2 sqrt(k) / 2, which App. C.4's
+    range bound places at the bottom of the transformed values;
+  * lambda1 = 0 takes lambda2; lambda2 = 0 gives s2 = s1 = B sqrt(k)/lambda1;
+    both zero give s1 = s2 = 1; a one-row group is a PSQ row;
+  * cube roots are correctly rounded float32; the group column sum adds the
+    slots in aligned chunks of min(k, 16), each chunk left to right, then the
+    chunk sums left to right.
+
+Offset codes (what the int8 contractions consume) are code - 2^(b-1).
+"""
+from fractions import Fraction
+import math
+
+import numpy as np
+
+from . import sr
+
+FLT_MAX = float(np.finfo(np.float32).max)
+CHUNK = 16          # slots per partial column sum in the BHQ group sum
+
+
+def n_bins(bits):
+    """B = 2^b - 1 (Sec. 3.3)."""
+    return (1 << int(bits)) - 1
+
+
+def offset(bits):
+    return 1 << (int(bits) - 1)
+
+
+def to_f32_sat(v):
+    """Round a float64 to float32 (nearest even), saturating at FLT_MAX."""
+    f = np.float32(v)
+    if not np.isfinite(f):
+        f = np.float32(FLT_MAX)
+    return f
+
+
+def scale_from_range(R, B):
+    """s = B / R in float32 (one correctly rounded division); R = 0 gives 1."""
+    R = np.float32(R)
+    if R == 0:
+        return np.float32(1.0)
+    with np.errstate(over="ignore"):
+        s = np.float32(B) / R
+    return s if np.isfinite(s) else np.float32(FLT_MAX)
+
+
+def row_stats(x):
+    """Per-row min, max, range R (float32 subtraction) and infinity norm M."""
+    x = np.asarray(x, dtype=np.float32)
+    mn = x.min(axis=1)
+    mx = x.max(axis=1)
+    R = (mx - mn).astype(np.float32)
+    M = np.maximum(np.abs(mn), np.abs(mx)).astype(np.float32)
+    return mn, mx, R, M
+
+
+# ----------------------------------------------------------------------------
+# PTQ and PSQ
+# ----------------------------------------------------------------------------
+
+def _affine_codes(x, s, z, bits, stochastic, seed, stream, elem_index):
+    """y = s (x - z) in float32 (subtract, then multiply), then round."""
+    B = n_bins(bits)
+    t = (x - z).astype(np.float32)
+    y = (s * t).astype(np.float32)
+    if stochastic:
+        u = sr.uniform24(elem_index, seed, stream)
+        return sr.round_stochastic(y, u, B)
+    return sr.round_nearest_even(y, B)
+
+
+def quantize_ptq(x, bits, stochastic, seed=0, stream=0):
+    """Per-tensor quantizer of Sec. 3.3 on a 2-D float32 array.
+
+    Returns dict(code [rows, cols] int64 in [0, B], scale, zero, bits).  The
+    element index of the SR draw is the logical row-major index i*cols + j.
+    """
+    x = np.asarray(x, dtype=np.float32)
+    rows, cols = x.shape
+    B = n_bins(bits)
+    z = np.float32(x.min()) if x.size else np.float32(0)
+    R = np.float32(np.float32(x.max()) - z) if x.size else np.float32(0)
+    s = scale_from_range(R, B)
+    e = np.arange(rows * cols, dtype=np.uint64).reshape(rows, cols)
+    code = _affine_codes(x, s, z, bits, stochastic, seed, stream, e)
+    return dict(kind="ptq", code=code, scale=np.float32(s), zero=np.float32(z), bits=int(bits))
+
+
+def quantize_psq(x, bits, seed=0, stream=0):
+    """Per-sample quantizer of Sec. 4.1: one (s_i, z_i) per row, SR per element."""
+    x = np.asarray(x, dtype=np.float32)
+    rows, cols = x.shape
+    B = n_bins(bits)
+    mn, _, R, _ = row_stats(x)
+    s = np.array([scale_from_range(r, B) for r in R], dtype=np.float32)
+    e = np.arange(rows * cols, dtype=np.uint64).reshape(rows, cols)
+    code = _affine_codes(x, s[:, None], mn[:, None], bits, True, seed, stream, e)
+    return dict(kind="psq", code=code, scale=s, zero=mn.astype(np.float32), bits=int(bits))
+
+
+def dequantize_affine(q):
+    """Real value of each code, code / s + z, in float64 (Sec. 3.3 inverse map)."""
+    s = np.asarray(q["scale"], dtype=np.float64)
+    z = np.asarray(q["zero"], dtype=np.float64)
+    if s.ndim == 1:
+        s, z = s[:, None], z[:, None]
+    return q["code"].astype(np.float64) / s + z
+
+
+# ----------------------------------------------------------------------------
+# BHQ
+# ----------------------------------------------------------------------------
+
+def cbrt_rn(x):
+    """Correctly rounded float32 cube root of a non-negative finite float32.
+
+    A float64 estimate picks a candidate; exact rational comparisons against
+    the cubes of the midpoints to its float32 neighbours then move it to the
+    nearest float32.  A midpoint has 25 significant bits, so its cube is never
+    a float32 and ties cannot occur.
+    """
+    x = np.float32(x)
+    if x == 0:
+        return np.float32(0.0)
+    X = Fraction(float(x))
+    r = np.float32(np.cbrt(np.float64(x)))
+    while True:
+        up = np.nextafter(r, np.float32(np.inf))
+        dn = np.nextafter(r, np.float32(0))
+        mid_up = (Fraction(float(r)) + Fraction(float(up))) / 2
+        mid_dn = (Fraction(float(r)) + Fraction(float(dn))) / 2
+        if mid_up ** 3 < X:
+            r = up
+        elif mid_dn ** 3 > X:
+            r = dn
+        else:
+            assert mid_up ** 3 != X and mid_dn ** 3 != X
+            return np.float32(r)
+
+
+def bhq_groups(N, k):
+    """Row-slot layout of fixed-block BHQ: G = ceil(N/k) groups.
+
+    Returns (G, sizes) with sizes[g] = 1 + the number of sorted-tail rows that
+    group g takes (App. D builds groups of one large row plus small rows; the
+    paper leaves the fixed-size assignment open: contiguous chunks of k-1).
+    """
+    G = -(-N // k)
+    small = N - G
+    sizes = []
+    for g in range(G):
+        lo = min(small, g * (k - 1))
+        hi = min(small, (g + 1) * (k - 1))
+        sizes.append(1 + hi - lo)
+    return G, sizes
+
+
+def bhq_plan(x, bits, k):
+    """Sort, grouping and per-group scalars of the block Householder quantizer.
+
+    Sec. 4.2 / App. D: sort the row infinity norms M_i in descending order
+    (ties: lower row index first); the first G rows are the large rows.
+    App. C.4: s1 = B k^(1/6) lambda1^(-1/3) / (lambda1^(2/3) k^(-1/3) +
+    lambda2^(2/3) k^(2/3)) and likewise s2 with lambda2^(-1/3); multiplying
+    through by k^(1/3) gives the form evaluated here, s1 = B sqrt(k) /
+    (a (a^2 + c^2 k)), s2 = B sqrt(k) / (c (a^2 + c^2 k)), a = lambda1^(1/3),
+    c = lambda2^(1/3).
+    """
+    x = np.asarray(x, dtype=np.float32)
+    N, D = x.shape
+    B = n_bins(bits)
+    mn, mx, R, M = row_stats(x)
+    order = np.lexsort((np.arange(N), -M))          # M descending, index ascending
+    G, sizes = bhq_groups(N, k)
+    perm, group_off = [], [0]
+    scale = np.zeros(N, np.float32)
+    zero = np.zeros(N, np.float32)
+    groups = []
+    for g in range(G):
+        small = order[G + g * (k - 1): G + g * (k - 1) + sizes[g] - 1]
+        members = [int(order[g])] + [int(i) for i in small]
+        base = len(perm)
+        perm.extend(members)
+        group_off.append(len(perm))
+        kg = len(members)
+        info = dict(members=members, base=base, size=kg)
+        if kg == 1:
+            i = members[0]
+            scale[base] = scale_from_range(R[i], B)
+            zero[base] = mn[i]
+        else:
+            big = members[0]
+            lam1 = np.float32(R[big])
+            lam2 = np.float32(np.float32(2.0) * np.float32(M[members[1:]].max()))
+            if lam1 == 0:
+                lam1 = lam2
+            sk = math.sqrt(float(kg))
+            if lam1 == 0 and lam2 == 0:
+                s1 = s2 = np.float32(1.0)
+            elif lam2 == 0:
+                s1 = s2 = to_f32_sat((float(B) * sk) / float(lam1))
+            else:
+                a = float(cbrt_rn(lam1))
+                c = float(cbrt_rn(lam2))
+                t = a * a + (c * c) * float(kg)
+                num = float(B) * sk
+                s1 = to_f32_sat(num / (a * t))
+                s2 = to_f32_sat(num / (c * t))
+            alpha = np.float32(1.0 / sk)
+            oma = np.float32(np.float32(1.0) - alpha)
+            cg = np.float32(((float(alpha) * float(s1)) * float(mn[big]))
+                            - (((0.5 * float(lam2)) * float(s2)) * sk))
+            scale[base] = s1
+            scale[base + 1: base + kg] = s2
+            zero[base: base + kg] = cg
+            info.update(lam1=lam1, lam2=lam2, s1=s1, s2=s2, alpha=alpha, oma=oma, cg=cg, sk=sk)
+        groups.append(info)
+    return dict(perm=np.array(perm, np.int64), group_off=np.array(group_off, np.int64),
+                scale=scale, zero=zero, groups=groups, G=G, k=k, bits=int(bits), sorted=order)
+
+
+def group_column_sum(v, k):
+    """Column sums of a group's scaled rows v [k_g, D] (float32).
+
+    Slots are added in aligned chunks of min(k, 16): each chunk left to right,
+    then the chunk sums left to right.  Slots past k_g count as zero.
+    """
+    ch = min(k, CHUNK)
+    kg, D = v.shape
+    S = None
+    for c0 in range(0, max(kg, 1), ch):
+        P = np.zeros(D, np.float32)
+        for p in range(c0, min(kg, c0 + ch)):
+            P = (P + v[p]).astype(np.float32)
+        S = P if S is None else (S + P).astype(np.float32)
+    return S
+
+
+def bhq_transform(rows, info):
+    """y' = Q diag(s1, s2..s2) G_g - c_g for one group, float32 (Sec. 4.2).
+
+    v_p = d_p g_p; S = group column sum; tau = (alpha S - v_0) / (1 - alpha);
+    Y_0 = v_0 + (1 - alpha) tau, Y_p = v_p - alpha tau; then subtract c_g.
+    This is the reflection I - 2 n n^T / |n|^2 with n = alpha 1 - e_0 applied
+    as a rank-1 update (|n|^2 = 2 (1 - alpha)).
+    """
+    kg = info["size"]
+    d = np.array([info["s1"]] + [info["s2"]] * (kg - 1), np.float32)
+    v = (d[:, None] * rows).astype(np.float32)
+    S = group_column_sum(v, info["k"])
+    alpha, oma = np.float32(info["alpha"]), np.float32(info["oma"])
+    m = (alpha * S).astype(np.float32)
+    m = (m - v[0]).astype(np.float32)
+    tau = (m / oma).astype(np.float32)
+    Y = np.empty_like(v)
+    Y[0] = (v[0] + (oma * tau).astype(np.float32)).astype(np.float32)
+    if kg > 1:
+        Y[1:] = (v[1:] - (alpha * tau).astype(np.float32)[None, :]).astype(np.float32)
+    return (Y - np.float32(info["cg"])).astype(np.float32)
+
+
+def quantize_bhq(x, bits, k, seed=0, stream=0, plan=None):
+    """Block Householder quantizer with fixed block size k (Sec. 4.2).
+
+    Codes are returned in slot order (group by group); the SR draw of slot p,
+    column j uses element index perm[p] * cols + j (its original position).
+    """
+    x = np.asarray(x, dtype=np.float32)
+    N, D = x.shape
+    B = n_bins(bits)
+    if plan is None:
+        plan = bhq_plan(x, bits, k)
+    code = np.zeros((N, D), np.int64)
+    cols = np.arange(D, dtype=np.uint64)
+    for info in plan["groups"]:
+        info = dict(info, k=k)
+        mem = info["members"]
+        base, kg = info["base"], info["size"]
+        rows = x[mem]
+        e = np.asarray(mem, dtype=np.uint64)[:, None] * np.uint64(D) + cols[None, :]
+        if kg == 1:
+            s, z = plan["scale"][base], plan["zero"][base]
+            y = (s * (rows - z).astype(np.float32)).astype(np.float32)
+        else:
+            y = bhq_transform(rows, info)
+        u = sr.uniform24(e, seed, stream)
+        code[base: base + kg] = sr.round_stochastic(y, u, B)
+    return dict(kind="bhq", code=code, scale=plan["scale"], zero=plan["zero"], perm=plan["perm"],
+                group_off=plan["group_off"], bits=int(bits), plan=plan, k=k)
+
+
+def dequantize_bhq(q):
+    """Real values of a BHQ result in original row order, float64.
+
+    Inverse map of Eq. (matrix-quantizer): G~_g = diag(d)^-1 Q (code + c_g),
+    with the exact reflection (alpha = 1/sqrt(k_g) in float64); a one-row group
+    is a PSQ row, code / s + z.
+    """
+    code = q["code"].astype(np.float64)
+    N, D = code.shape
+    out = np.zeros((N, D), np.float64)
+    for info in q["plan"]["groups"]:
+        base, kg, mem = info["base"], info["size"], info["members"]
+        s = q["scale"][base: base + kg].astype(np.float64)
+        z = q["zero"][base: base + kg].astype(np.float64)
+        if kg == 1:
+            out[mem[0]] = code[base] / s[0] + z[0]
+            continue
+        w = code[base: base + kg] + z[0]
+        a = 1.0 / math.sqrt(kg)
+        tau = (a * w.sum(axis=0) - w[0]) / (1.0 - a)
+        Z = w - a * tau[None, :]
+        Z[0] = w[0] + (1.0 - a) * tau
+        out[mem] = Z / s[:, None]
+    return out
+
+
+def offset_codes(q):
+    """Signed codes code - 2^(b-1), the int8 operands of the contractions."""
+    return (q["code"] - offset(q["bits"])).astype(np.int64)
+
+
+def dequantize(q):
+    """Real values of any quantizer result, original row order, float64."""
+    if q["kind"] == "bhq":
+        return dequantize_bhq(q)
+    return dequantize_affine(q)
