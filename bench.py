@@ -1,0 +1,147 @@
+#!/usr/bin/env python3
+"""Benchmark: FQT backward of one Transformer-FFN shaped linear layer on one MI355X.
+
+Workload: X [8192, 1024], W [4096, 1024], G [8192, 4096] float32 (1% outlier
+gradient rows), grad_X quantizer BHQ 5-bit with block size 64, grad_W
+quantizer 8-bit stochastic PTQ, X and W 8-bit deterministic PTQ.  A step is
+one fqt_linear_backward call (statistics, BHQ plan, all quantizers, both int8
+contractions and their dequantizing epilogues) on inputs resident in HBM.
+
+Prints one JSON line: the int8 throughput of the whole layer backward
+(2 * 2 N d_in d_out ops per step / step time), per-phase times from HIP
+events recorded inside the timed steps, the roofline of the dominant kernel
+and the CPU oracle timed on a bounded sample of the same layer.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+N, D_IN, D_OUT = 8192, 1024, 4096
+QB_X = ("bhq", 5, 64)
+QB_W = ("ptq", 8, 0)
+HBM_PEAK_GBS = 8000.0            # MI355X HBM3E
+INT8_PEAK_TOPS = 5000.0          # MI355X dense int8 matrix cores
+CPU_SAMPLE_ROWS = 256
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    return ap.parse_args()
+
+
+def cpu_baseline(X, W, G):
+    """The oracle, as is, on the first CPU_SAMPLE_ROWS samples of the same layer."""
+    from oracle import backward as BW
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = 1
+    n = CPU_SAMPLE_ROWS
+    t0 = time.perf_counter()
+    BW.linear_backward(X[:n], W, G[:n], qb_x=QB_X, qb_w=QB_W, seed=0)
+    dt = time.perf_counter() - t0
+    ops = 2.0 * 2.0 * n * D_IN * D_OUT
+    return {"value": ops / dt / 1e12, "unit": "TOPS", "cores": int(threads), "kind": "oracle",
+            "sample": f"first {n} of {N} samples of the same layer (full d_in, d_out), BHQ-5 k=64; {dt:.1f} s"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported "
+              "(the layer backward runs on a single MI355X)", file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+    from paper_2010_14298_amd import fqt, synth
+
+    fqt.load()
+    X, W, G = synth.linear_outlier(seed=0, n=N, d_in=D_IN, d_out=D_OUT)
+    dX, dW, dG = (torch.from_numpy(a).cuda() for a in (X, W, G))
+    grad_W = torch.empty((D_OUT, D_IN), dtype=torch.float32, device="cuda")
+    grad_X = torch.empty((N, D_IN), dtype=torch.float32, device="cuda")
+    cfg = fqt.cfg_struct(QB_X, QB_W, 8, 8, 0)
+    ws = torch.empty(fqt.fqt_linear_backward_workspace(N, D_IN, D_OUT, cfg), dtype=torch.uint8, device="cuda")
+
+    def step(seed, trace=None):
+        fqt.fqt_linear_backward(dX, dW, dG, qb_x=QB_X, qb_w=QB_W, seed=seed, grad_W=grad_W, grad_X=grad_X,
+                                ws=ws, trace=trace)
+
+    for i in range(args.warmup):
+        step(1000 + i)
+    torch.cuda.synchronize()
+    if fqt.fqt_workspace_status(ws) != 0:
+        raise RuntimeError("non-finite data reported by the workspace status")
+    traces = [fqt.make_trace() for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(i, traces[i])
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms_step = (t1 - t0) * 1e3 / args.steps
+    phase_ms = np.mean([fqt.trace_ms(t) for t in traces], axis=0)
+    for t in traces:
+        fqt.free_trace(t)
+    phases = dict(zip(fqt.PHASE_NAMES, [round(float(v), 5) for v in phase_ms]))
+
+    gemm_ops = 2.0 * N * D_IN * D_OUT               # per contraction
+    value = 2.0 * gemm_ops / (ms_step * 1e-3) / 1e12
+    nd = float(N) * D_OUT
+    quant_bytes = 4 * nd + 2 * nd                   # read G, write Q_b2 and Q_b1 codes
+    t_quant_g = phases["quant_G"] * 1e-3
+    t_quantizer = (phases["stats"] + phases["scales_plan"] + phases["quant_G"]) * 1e-3
+    kernels = {
+        "gemm_gradX": {"bound": "mfma", "t": phases["gemm_gradX"] * 1e-3, "work": gemm_ops, "unit": "TFLOP/s",
+                       "peak": INT8_PEAK_TOPS, "scale": 1e12},
+        "gemm_gradW": {"bound": "mfma", "t": phases["gemm_gradW"] * 1e-3, "work": gemm_ops, "unit": "TFLOP/s",
+                       "peak": INT8_PEAK_TOPS, "scale": 1e12},
+        "quant_G": {"bound": "hbm", "t": t_quant_g, "work": quant_bytes, "unit": "GB/s", "peak": HBM_PEAK_GBS,
+                    "scale": 1e9},
+    }
+    per_kernel = {}
+    for name, k in kernels.items():
+        ach = k["work"] / k["t"] / k["scale"]
+        per_kernel[name] = {"bound": k["bound"], "achieved": round(ach, 2), "peak": k["peak"], "unit": k["unit"],
+                            "frac": round(ach / k["peak"], 4), "ms": round(k["t"] * 1e3, 4)}
+    dom = max(kernels, key=lambda n: kernels[n]["t"])
+    roof = dict(per_kernel[dom])
+    roof.pop("ms")
+    roof["kernel"] = dom
+    roof["traffic"] = None
+    out = {
+        "metric": "FQT layer-backward int8 TOPS + quantizer HBM GB/s (BHQ 5-bit) vs roofline",
+        "value": round(value, 3),
+        "unit": "TOPS",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int8 contractions, f32 quantizers, f64 epilogue",
+        "data": "synthetic",
+        "config": {"workload": "linear FQT backward, N=8192 tokens, d_in=1024, d_out=4096, 1% outlier gradient "
+                               "rows; Q_b2 = BHQ 5-bit block 64, Q_b1 = PTQ 8-bit, Q_f = Q_theta = PTQ 8-bit",
+                   "global_batch": N, "parallelism": "single GPU"},
+        "quantizer_GBps": round(quant_bytes / t_quantizer / 1e9, 2),
+        "quant_G_pass_GBps": round(quant_bytes / t_quant_g / 1e9, 2),
+        "phases_ms": phases,
+        "kernels": per_kernel,
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(X, W, G)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,202 @@
+/*
+ * fqt.h -- C ABI of libfqt.so: the fully-quantized-training (FQT) backward of
+ * one linear or conv layer on an MI355X (gfx950).
+ *
+ * Method: Chen, Gai, Yao, Mahoney, Gonzalez, "A Statistical Framework for
+ * Low-bitwidth Training of Deep Neural Networks" (NeurIPS 2020).
+ *   Sec. 2.2, Eq. (linear-sq-backprop):  grad_W = Q_b(G)^T Q_f(X),
+ *                                         grad_X = Q_b(G)   Q_theta(W)
+ *   Sec. 3.3  per-tensor quantizer (PTQ) with stochastic rounding SR
+ *   Sec. 4.1  per-sample quantizer (PSQ)
+ *   Sec. 4.2, App. C.4, App. D  block Householder quantizer (BHQ)
+ *   App. E    gradient bifurcation: Q_b1 (8-bit stochastic PTQ) feeds
+ *             grad_W, Q_b2 (PTQ / PSQ / BHQ, 4-8 bits) feeds grad_X;
+ *             Q_f and Q_theta are deterministic 8-bit PTQ.
+ *
+ * Conventions for every entry point
+ *   - Row-major; a row is a sample (or token).  PyTorch orientation:
+ *     X [N, d_in], W [d_out, d_in], G = dL/dY [N, d_out].
+ *   - All array pointers are DEVICE pointers owned by the caller; only the
+ *     small configuration structs (`cfg`, `shape`) are host memory.
+ *   - `ws` is a caller-owned device workspace of at least the size the
+ *     matching *_workspace() query returns; the library never allocates.
+ *   - Work is enqueued asynchronously on `stream` (0 = the null stream).
+ *     The library keeps no state between calls; calls on different
+ *     workspaces may run concurrently.
+ *   - Argument errors are reported synchronously, before anything is
+ *     enqueued.  Data errors (a NaN or Inf in an input, or a range that
+ *     overflows float32) are recorded in the workspace and returned by
+ *     fqt_workspace_status(); outputs are then unspecified.
+ *   - Stochastic rounding draw for logical element e (row-major index in the
+ *     quantized matrix) = Philox4x32-10 with key = seed, counter =
+ *     (e >> 2, stream, 0), word e & 3; the upper 24 bits are the uniform.
+ *     Results are a deterministic function of (inputs, seed, stream).
+ *   - Codes are stored as int8 offset codes q = code - 2^(bits-1), where code
+ *     in [0, 2^bits - 1] is the quantization bin of Sec. 3.3.
+ */
+#ifndef FQT_H_
+#define FQT_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct ihipStream_t* fqt_stream_t; /* same object as hipStream_t */
+
+typedef enum {
+  FQT_OK = 0,
+  FQT_EINVAL = 1,        /* bad argument (NULL, size <= 0, bits outside 1..8, ...) */
+  FQT_EUNSUPPORTED = 2,  /* valid per the paper but not implemented here */
+  FQT_ENONFINITE = 3,    /* NaN / Inf input or float32 range overflow */
+  FQT_EWORKSPACE = 4,    /* ws NULL or ws_bytes below the query */
+  FQT_EDEVICE = 5        /* a HIP runtime call failed */
+} fqt_status;
+
+typedef enum { FQT_PTQ = 0, FQT_PSQ = 1, FQT_BHQ = 2 } fqt_kind;
+
+/* One quantized matrix (Sec. 3.3 / Eq. matrix-quantizer).  Every pointer is
+ * caller-owned device memory; a NULL optional pointer is skipped.
+ *   q         codes, offset form.  Natural layout [rows, cols]; for BHQ the
+ *             rows are in slot order (grouped, see perm).  Transposed layout
+ *             [cols, rows] where the entry point says so.
+ *   scale     PTQ: [1] s.  PSQ: [rows] s_i.  BHQ: [rows] per slot d_p
+ *             (s1 for a group's first slot, s2 for the others; a one-row
+ *             group holds its PSQ scale).
+ *   zero      PTQ: [1] z.  PSQ: [rows] z_i = row min.  BHQ: [rows] per slot:
+ *             the group's transformed-domain offset c_g (one-row group: its
+ *             row min, as PSQ).
+ *   perm      BHQ only: [rows] slot -> original row.
+ *   group_off BHQ only, optional: [rows + 1]; the first G + 1 entries are
+ *             the group boundaries in slot order (G = ceil(rows / k)).
+ *   code_sum  optional int32 sums of q along the contiguous axis of the
+ *             stored layout: [rows] for natural, [cols] for transposed.
+ * Dequantized value: PTQ/PSQ code / s + z.  BHQ group of k_g > 1 slots:
+ * diag(d)^-1 H (code + c_g), H the k_g x k_g Householder reflection with
+ * normal 1/sqrt(k_g) - e_1 (Sec. 4.2).                                      */
+typedef struct {
+  int8_t* q;
+  float* scale;
+  float* zero;
+  int32_t* perm;
+  int32_t* group_off;
+  int32_t* code_sum;
+} fqt_qtensor;
+
+/* Per-tensor quantizer, Sec. 3.3: z = min x, s = B / (max x - min x),
+ * code = SR(s (x - z)) (stochastic != 0) or round-half-even (stochastic == 0),
+ * clamped to [0, B], B = 2^bits - 1.  transpose != 0 stores q as [cols, rows].
+ * Needs out->q, out->scale, out->zero.  bits in 1..8.                        */
+fqt_status fqt_quantize_ptq(const float* x, int64_t rows, int64_t cols, int bits, int stochastic,
+                            uint64_t seed, uint32_t stream, int transpose, const fqt_qtensor* out,
+                            void* ws, size_t ws_bytes, fqt_stream_t s);
+
+/* Per-sample quantizer, Sec. 4.1: per row z_i = min, s_i = B / R_i, SR.
+ * Natural layout.  Needs out->q, out->scale [rows], out->zero [rows].       */
+fqt_status fqt_quantize_psq(const float* x, int64_t rows, int64_t cols, int bits, uint64_t seed,
+                            uint32_t stream, const fqt_qtensor* out, void* ws, size_t ws_bytes,
+                            fqt_stream_t s);
+
+/* Block Householder quantizer, Sec. 4.2 / App. C.4 / App. D, fixed block
+ * size k = block_size (a power of two, 1..64; 0, the adaptive grouping,
+ * returns FQT_EUNSUPPORTED).  Rows are sorted by infinity norm (descending,
+ * ties by row index); G = ceil(rows / k) groups each take one of the G
+ * largest rows plus the next k - 1 rows of the sorted tail.  Codes are in
+ * slot order, natural layout.  Needs out->q, scale, zero, perm.            */
+fqt_status fqt_quantize_bhq(const float* x, int64_t rows, int64_t cols, int bits, int block_size,
+                            uint64_t seed, uint32_t stream, const fqt_qtensor* out, void* ws,
+                            size_t ws_bytes, fqt_stream_t s);
+
+size_t fqt_quantize_workspace(fqt_kind kind, int64_t rows, int64_t cols, int block_size);
+
+/* Quantizer choice for one gradient quantizer. */
+typedef struct {
+  fqt_kind kind;   /* FQT_PTQ, FQT_PSQ or FQT_BHQ */
+  int bits;        /* 1..8 */
+  int block_size;  /* BHQ only: power of two in 1..64 */
+} fqt_qspec;
+
+/* Optional per-phase timing: when fqt_bwd_cfg.trace is non-NULL, the layer
+ * backward records start[i] / stop[i] (caller-created hipEvent_t handles)
+ * around phase i on `stream`, for i < count.  Phases of the layer backward:
+ *   0 workspace init   1 stats X, W, G   2 scales / BHQ plan
+ *   3 quantize X       4 quantize W      5 quantize G (Q_b1 and Q_b2)
+ *   6 grad_W contraction (with any split-K reduction)
+ *   7 grad_X contraction                                                    */
+#define FQT_TRACE_PHASES 8
+typedef struct {
+  void* start[FQT_TRACE_PHASES];
+  void* stop[FQT_TRACE_PHASES];
+  int count;
+} fqt_trace;
+
+/* Layer backward configuration (App. E).  qb_w feeds grad_W and must be PTQ
+ * (per-row scales lie on grad_W's contraction axis; anything else returns
+ * FQT_EUNSUPPORTED).  qb_x feeds grad_X.  f_bits / theta_bits are the
+ * deterministic PTQ widths of X and W.  Q_b1 draws from stream 0 and Q_b2
+ * from stream 1 of `seed`.                                                  */
+typedef struct {
+  fqt_qspec qb_w;
+  fqt_qspec qb_x;
+  int f_bits;
+  int theta_bits;
+  uint64_t seed;
+  const fqt_trace* trace; /* optional, NULL for none */
+} fqt_bwd_cfg;
+
+/* Linear layer FQT backward, Eq. (linear-sq-backprop) with bifurcation:
+ *   grad_W [d_out, d_in] = Q_b1(G)^T Q_f(X)
+ *   grad_X [N, d_in]     = Q_b2(G)   Q_theta(W)
+ * both contracted on int8 matrix cores with exact int32 accumulators
+ * (int64 across K-splits) and dequantized in float64, rounded to float32.
+ * Outputs are overwritten.  N, d_in, d_out >= 1.                            */
+fqt_status fqt_linear_backward(const float* X, const float* W, const float* G, int64_t N, int64_t d_in,
+                               int64_t d_out, const fqt_bwd_cfg* cfg, float* grad_W, float* grad_X,
+                               void* ws, size_t ws_bytes, fqt_stream_t s);
+
+size_t fqt_linear_backward_workspace(int64_t N, int64_t d_in, int64_t d_out, const fqt_bwd_cfg* cfg);
+
+/* Conv geometry: X NHWC [n, h, w, c], W [o, kh, kw, c], G NHWC [n, ho, wo, o],
+ * ho = (h + 2 pad - kh) / stride + 1 (likewise wo); zero padding.           */
+typedef struct {
+  int n, c, h, w, o, kh, kw, stride, pad, ho, wo;
+} fqt_conv_shape;
+
+/* Conv layer FQT backward as implicit-im2col contractions: the conv is the
+ * linear layer Y = im2col(X) W^T, so grad_W = Q_b1(G)^T im2col(Q_f(X)) and
+ * grad_X = col2im(Q_b2(G) Q_theta(W)).  Quantizer rows are samples
+ * (Sec. 4.1): X and W per tensor, G [n, ho*wo*o] per sample / group.
+ * Padding taps contribute exactly zero.  Outputs grad_W [o, kh, kw, c] and
+ * grad_X [n, h, w, c] are overwritten.                                      */
+fqt_status fqt_conv_backward_im2col(const float* X, const float* W, const float* G,
+                                    const fqt_conv_shape* shape, const fqt_bwd_cfg* cfg, float* grad_W,
+                                    float* grad_X, void* ws, size_t ws_bytes, fqt_stream_t s);
+
+size_t fqt_conv_backward_workspace(const fqt_conv_shape* shape, const fqt_bwd_cfg* cfg);
+
+/* Exact int8 contraction C[m, n] = sum_k A[m, k] B[n, k] (both K-contiguous,
+ * row strides lda, ldb in bytes >= K), int64 output [M, N].  int32
+ * accumulation over K-chunks of at most 65536, summed in int64.  The same
+ * kernels as the layer backward; exported to test accumulators bit-exactly. */
+fqt_status fqt_gemm_s8s8_s64(const int8_t* A, const int8_t* B, int64_t M, int64_t N, int64_t K, int64_t lda,
+                             int64_t ldb, int64_t* C, void* ws, size_t ws_bytes, fqt_stream_t s);
+
+size_t fqt_gemm_workspace(int64_t M, int64_t N, int64_t K);
+
+/* Waits for `s`, then reports the data status recorded in `ws` by the last
+ * call that used it: FQT_OK or FQT_ENONFINITE (FQT_EDEVICE if the wait or
+ * copy fails).                                                              */
+fqt_status fqt_workspace_status(const void* ws, fqt_stream_t s);
+
+const char* fqt_status_str(fqt_status st);
+
+/* Library version string. */
+const char* fqt_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FQT_H_ */

@@ -1,0 +1,534 @@
+// C ABI of libfqt.so (declared in include/fqt.h): argument checks, workspace
+// carving and the launch sequence of each entry point.
+#include <string.h>
+
+#include "../../include/fqt.h"
+#include "fqt_device.h"
+#include "fqt_kernels.h"
+
+namespace fqt {
+namespace {
+
+constexpr int64_t MAX_K_CHUNK = 65536;  // int32-exact K per contraction split
+constexpr int64_t MAX_ROWS = 65535LL * 64;  // quantizer grid limit (64 slots per tile row)
+
+// Bump allocator over the caller's workspace; with base == nullptr it only
+// measures.  Every block is 256-byte aligned.
+struct Carver {
+  char* base;
+  size_t off = 0;
+  explicit Carver(void* b) : base(static_cast<char*>(b)) {}
+  template <class T>
+  T* take(int64_t count) {
+    off = (off + 255) & ~(size_t)255;
+    T* p = base ? reinterpret_cast<T*>(base + off) : nullptr;
+    off += (size_t)count * sizeof(T);
+    return p;
+  }
+};
+
+// Fixed header at the start of every workspace.
+struct Header {
+  uint32_t* status;   // [1]
+  uint32_t* gminmax;  // [8]: X, W, G (min, max) + spare
+};
+Header take_header(Carver& c) {
+  uint32_t* h = c.take<uint32_t>(64);
+  return Header{h, h ? h + 1 : nullptr};
+}
+
+struct FillSeg {
+  uint32_t* p;
+  int64_t n;
+  uint32_t v;
+};
+struct FillList {
+  FillSeg seg[8];
+  int count;
+};
+
+__global__ void fill_segments_kernel(FillList fl) {
+  for (int s = 0; s < fl.count; ++s) {
+    const FillSeg g = fl.seg[s];
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < g.n; i += (int64_t)gridDim.x * blockDim.x)
+      g.p[i] = g.v;
+  }
+}
+
+hipError_t fill_segments(const FillList& fl, hipStream_t s) {
+  int64_t total = 0;
+  for (int i = 0; i < fl.count; ++i) total += fl.seg[i].n;
+  int64_t blocks = (total + 255) / 256;
+  if (blocks < 1) blocks = 1;
+  if (blocks > 1024) blocks = 1024;
+  hipLaunchKernelGGL(fill_segments_kernel, dim3((unsigned)blocks), dim3(256), 0, s, fl);
+  return hipGetLastError();
+}
+
+void add_fill(FillList& fl, void* p, int64_t n, uint32_t v) {
+  if (p && n > 0) fl.seg[fl.count++] = FillSeg{static_cast<uint32_t*>(p), n, v};
+}
+
+bool valid_bits(int b) { return b >= 1 && b <= 8; }
+
+// Optional phase markers of fqt_bwd_cfg.trace.
+struct Tracer {
+  const fqt_trace* t;
+  hipStream_t s;
+  void begin(int i) const {
+    if (t && i < t->count && t->start[i]) (void)hipEventRecord(static_cast<hipEvent_t>(t->start[i]), s);
+  }
+  void end(int i) const {
+    if (t && i < t->count && t->stop[i]) (void)hipEventRecord(static_cast<hipEvent_t>(t->stop[i]), s);
+  }
+};
+bool valid_block(int k) { return k >= 1 && k <= 64 && (k & (k - 1)) == 0; }
+
+fqt_status from_hip(hipError_t e) { return e == hipSuccess ? FQT_OK : FQT_EDEVICE; }
+
+#define FQT_TRY(expr)                              \
+  do {                                             \
+    const hipError_t e_ = (expr);                  \
+    if (e_ != hipSuccess) return FQT_EDEVICE;      \
+  } while (0)
+
+// ---------------------------------------------------------------------------
+// standalone quantizers
+// ---------------------------------------------------------------------------
+struct QuantWs {
+  Header h;
+  uint32_t* rmin;
+  uint32_t* rmax;
+  void* plan;
+};
+
+QuantWs carve_quant(Carver& c, fqt_kind kind, int64_t rows) {
+  QuantWs w{};
+  w.h = take_header(c);
+  if (kind != FQT_PTQ) {
+    w.rmin = c.take<uint32_t>(rows);
+    w.rmax = c.take<uint32_t>(rows);
+  }
+  if (kind == FQT_BHQ) w.plan = c.take<char>((int64_t)bhq_plan_workspace(rows));
+  return w;
+}
+
+fqt_status check_quant_args(const float* x, int64_t rows, int64_t cols, int bits, const fqt_qtensor* out) {
+  if (!x || !out || !out->q || !out->scale || !out->zero) return FQT_EINVAL;
+  if (rows < 1 || cols < 1 || !valid_bits(bits)) return FQT_EINVAL;
+  if (rows > MAX_ROWS || cols > ((int64_t)1 << 40) / rows) return FQT_EUNSUPPORTED;
+  return FQT_OK;
+}
+
+fqt_status quantize_common(fqt_kind kind, const float* x, int64_t rows, int64_t cols, int bits, int stochastic,
+                           uint64_t seed, uint32_t stream, int transpose, int block_size, const fqt_qtensor* out,
+                           void* ws, size_t ws_bytes, hipStream_t s) {
+  fqt_status st = check_quant_args(x, rows, cols, bits, out);
+  if (st != FQT_OK) return st;
+  if (kind == FQT_BHQ) {
+    if (block_size == 0) return FQT_EUNSUPPORTED;
+    if (!valid_block(block_size) || !out->perm) return FQT_EINVAL;
+  }
+  if (!ws) return FQT_EWORKSPACE;
+  Carver cs(nullptr);
+  carve_quant(cs, kind, rows);
+  if (ws_bytes < cs.off) return FQT_EWORKSPACE;
+  Carver c(ws);
+  QuantWs w = carve_quant(c, kind, rows);
+
+  FillList fl{};
+  add_fill(fl, w.h.status, 1, 0u);
+  add_fill(fl, w.h.gminmax, 1, ORD_POS_INF);
+  add_fill(fl, w.h.gminmax + 1, 1, ORD_NEG_INF);
+  add_fill(fl, w.rmin, rows, ORD_POS_INF);
+  add_fill(fl, w.rmax, rows, ORD_NEG_INF);
+  add_fill(fl, out->code_sum, transpose ? cols : rows, 0u);
+  FQT_TRY(fill_segments(fl, s));
+
+  QuantParams p{};
+  p.x = x;
+  p.rows = rows;
+  p.cols = cols;
+  p.bits = bits;
+  p.stoch = stochastic;
+  p.seed = seed;
+  p.stream = stream;
+  p.scale = out->scale;
+  p.zero = out->zero;
+  if (transpose) {
+    p.q_t = out->q;
+    p.sum_t = out->code_sum;
+  } else {
+    p.q_nat = out->q;
+    p.sum_nat = out->code_sum;
+  }
+  int mode = QM_TENSOR;
+  if (kind == FQT_PTQ) {
+    FQT_TRY(launch_stats_flat(x, rows * cols, w.h.gminmax, w.h.status, s));
+    FQT_TRY(launch_ptq_finalize(w.h.gminmax, bits, out->scale, out->zero, w.h.status, s));
+  } else {
+    FQT_TRY(launch_stats_rows(x, rows, cols, w.rmin, w.rmax, w.h.gminmax, w.h.status, s));
+    if (kind == FQT_PSQ) {
+      FQT_TRY(launch_psq_finalize(w.rmin, w.rmax, rows, bits, out->scale, out->zero, w.h.status, s));
+      mode = QM_ROW;
+    } else {
+      p.L = bhq_layout(rows, block_size);
+      FQT_TRY(launch_bhq_plan(w.rmin, w.rmax, p.L, bits, w.plan, out->perm, out->scale, out->zero, out->group_off,
+                              s));
+      p.perm = out->perm;
+      mode = QM_BHQ;
+    }
+  }
+  FQT_TRY(launch_quant(p, mode, s));
+  return FQT_OK;
+}
+
+// ---------------------------------------------------------------------------
+// linear backward
+// ---------------------------------------------------------------------------
+struct LinearWs {
+  Header h;
+  uint32_t *rmin, *rmax;
+  int8_t *qx_t, *qw_t, *qg1_t, *qg2;
+  int32_t *sum_x, *sum_w, *sum_g1, *sum_g2;
+  float *sx, *zx, *sw, *zw, *sg1, *zg1, *sg2, *zg2;
+  int32_t* perm;
+  void* plan;
+  int32_t* part;
+  int splits;
+};
+
+int linear_splits(int64_t N) { return (int)((N + MAX_K_CHUNK - 1) / MAX_K_CHUNK); }
+
+LinearWs carve_linear(Carver& c, int64_t N, int64_t d_in, int64_t d_out, const fqt_bwd_cfg& cfg) {
+  LinearWs w{};
+  w.h = take_header(c);
+  w.rmin = c.take<uint32_t>(N);
+  w.rmax = c.take<uint32_t>(N);
+  w.qx_t = c.take<int8_t>(d_in * N);
+  w.qw_t = c.take<int8_t>(d_in * d_out);
+  w.qg1_t = c.take<int8_t>(d_out * N);
+  w.qg2 = c.take<int8_t>(N * d_out);
+  w.sum_x = c.take<int32_t>(d_in);
+  w.sum_w = c.take<int32_t>(d_in);
+  w.sum_g1 = c.take<int32_t>(d_out);
+  w.sum_g2 = c.take<int32_t>(N);
+  w.sx = c.take<float>(1);
+  w.zx = c.take<float>(1);
+  w.sw = c.take<float>(1);
+  w.zw = c.take<float>(1);
+  w.sg1 = c.take<float>(1);
+  w.zg1 = c.take<float>(1);
+  w.sg2 = c.take<float>(N);
+  w.zg2 = c.take<float>(N);
+  if (cfg.qb_x.kind == FQT_BHQ) {
+    w.perm = c.take<int32_t>(N);
+    w.plan = c.take<char>((int64_t)bhq_plan_workspace(N));
+  }
+  w.splits = linear_splits(N);
+  if (w.splits > 1) w.part = c.take<int32_t>((int64_t)w.splits * d_out * d_in);
+  return w;
+}
+
+fqt_status check_cfg(const fqt_bwd_cfg* cfg) {
+  if (!cfg) return FQT_EINVAL;
+  if (!valid_bits(cfg->f_bits) || !valid_bits(cfg->theta_bits) || !valid_bits(cfg->qb_w.bits) ||
+      !valid_bits(cfg->qb_x.bits))
+    return FQT_EINVAL;
+  if (cfg->qb_x.kind < FQT_PTQ || cfg->qb_x.kind > FQT_BHQ || cfg->qb_w.kind < FQT_PTQ || cfg->qb_w.kind > FQT_BHQ)
+    return FQT_EINVAL;
+  if (cfg->qb_w.kind != FQT_PTQ) return FQT_EUNSUPPORTED;
+  if (cfg->qb_x.kind == FQT_BHQ) {
+    if (cfg->qb_x.block_size == 0) return FQT_EUNSUPPORTED;
+    if (!valid_block(cfg->qb_x.block_size)) return FQT_EINVAL;
+  }
+  return FQT_OK;
+}
+
+}  // namespace
+}  // namespace fqt
+
+using namespace fqt;
+
+extern "C" {
+
+fqt_status fqt_quantize_ptq(const float* x, int64_t rows, int64_t cols, int bits, int stochastic, uint64_t seed,
+                            uint32_t stream, int transpose, const fqt_qtensor* out, void* ws, size_t ws_bytes,
+                            fqt_stream_t s) {
+  return quantize_common(FQT_PTQ, x, rows, cols, bits, stochastic ? 1 : 0, seed, stream, transpose ? 1 : 0, 0, out,
+                         ws, ws_bytes, s);
+}
+
+fqt_status fqt_quantize_psq(const float* x, int64_t rows, int64_t cols, int bits, uint64_t seed, uint32_t stream,
+                            const fqt_qtensor* out, void* ws, size_t ws_bytes, fqt_stream_t s) {
+  return quantize_common(FQT_PSQ, x, rows, cols, bits, 1, seed, stream, 0, 0, out, ws, ws_bytes, s);
+}
+
+fqt_status fqt_quantize_bhq(const float* x, int64_t rows, int64_t cols, int bits, int block_size, uint64_t seed,
+                            uint32_t stream, const fqt_qtensor* out, void* ws, size_t ws_bytes, fqt_stream_t s) {
+  return quantize_common(FQT_BHQ, x, rows, cols, bits, 1, seed, stream, 0, block_size, out, ws, ws_bytes, s);
+}
+
+size_t fqt_quantize_workspace(fqt_kind kind, int64_t rows, int64_t cols, int block_size) {
+  (void)cols;
+  (void)block_size;
+  if (rows < 1) return 0;
+  Carver c(nullptr);
+  carve_quant(c, kind, rows);
+  return c.off;
+}
+
+size_t fqt_linear_backward_workspace(int64_t N, int64_t d_in, int64_t d_out, const fqt_bwd_cfg* cfg) {
+  if (!cfg || N < 1 || d_in < 1 || d_out < 1) return 0;
+  Carver c(nullptr);
+  carve_linear(c, N, d_in, d_out, *cfg);
+  return c.off;
+}
+
+fqt_status fqt_linear_backward(const float* X, const float* W, const float* G, int64_t N, int64_t d_in,
+                               int64_t d_out, const fqt_bwd_cfg* cfg, float* grad_W, float* grad_X, void* ws,
+                               size_t ws_bytes, fqt_stream_t s) {
+  if (!X || !W || !G || !grad_W || !grad_X) return FQT_EINVAL;
+  if (N < 1 || d_in < 1 || d_out < 1) return FQT_EINVAL;
+  fqt_status st = check_cfg(cfg);
+  if (st != FQT_OK) return st;
+  if (N > MAX_ROWS || d_out > MAX_ROWS || d_out > MAX_K_CHUNK || N > 0x7FFFFFFF / 2) return FQT_EUNSUPPORTED;
+  if (!ws) return FQT_EWORKSPACE;
+  if (ws_bytes < fqt_linear_backward_workspace(N, d_in, d_out, cfg)) return FQT_EWORKSPACE;
+  Carver c(ws);
+  LinearWs w = carve_linear(c, N, d_in, d_out, *cfg);
+  const fqt_qspec qx = cfg->qb_x;
+  const bool bhq = qx.kind == FQT_BHQ;
+
+  const Tracer tr{cfg->trace, s};
+  tr.begin(0);
+  FillList fl{};
+  add_fill(fl, w.h.status, 1, 0u);
+  add_fill(fl, w.h.gminmax, 8, ORD_POS_INF);
+  add_fill(fl, w.rmin, N, ORD_POS_INF);
+  add_fill(fl, w.rmax, N, ORD_NEG_INF);
+  add_fill(fl, w.sum_x, d_in, 0u);
+  add_fill(fl, w.sum_w, d_in, 0u);
+  add_fill(fl, w.sum_g1, d_out, 0u);
+  add_fill(fl, w.sum_g2, N, 0u);
+  FQT_TRY(fill_segments(fl, s));
+  // the max slots of gminmax start at -inf
+  FillList fm{};
+  add_fill(fm, w.h.gminmax + 1, 1, ORD_NEG_INF);
+  add_fill(fm, w.h.gminmax + 3, 1, ORD_NEG_INF);
+  add_fill(fm, w.h.gminmax + 5, 1, ORD_NEG_INF);
+  FQT_TRY(fill_segments(fm, s));
+  tr.end(0);
+
+  uint32_t* gX = w.h.gminmax;
+  uint32_t* gW = w.h.gminmax + 2;
+  uint32_t* gG = w.h.gminmax + 4;
+  tr.begin(1);
+  FQT_TRY(launch_stats_flat(X, N * d_in, gX, w.h.status, s));
+  FQT_TRY(launch_stats_flat(W, d_out * d_in, gW, w.h.status, s));
+  FQT_TRY(launch_stats_rows(G, N, d_out, w.rmin, w.rmax, gG, w.h.status, s));
+  tr.end(1);
+  tr.begin(2);
+  FQT_TRY(launch_ptq_finalize(gX, cfg->f_bits, w.sx, w.zx, w.h.status, s));
+  FQT_TRY(launch_ptq_finalize(gW, cfg->theta_bits, w.sw, w.zw, w.h.status, s));
+  FQT_TRY(launch_ptq_finalize(gG, cfg->qb_w.bits, w.sg1, w.zg1, w.h.status, s));
+  BhqLayout L{};
+  int mode = QM_TENSOR;
+  if (qx.kind == FQT_PTQ) {
+    FQT_TRY(launch_ptq_finalize(gG, qx.bits, w.sg2, w.zg2, w.h.status, s));
+  } else if (qx.kind == FQT_PSQ) {
+    FQT_TRY(launch_psq_finalize(w.rmin, w.rmax, N, qx.bits, w.sg2, w.zg2, w.h.status, s));
+    mode = QM_ROW;
+  } else {
+    L = bhq_layout(N, qx.block_size);
+    FQT_TRY(launch_bhq_plan(w.rmin, w.rmax, L, qx.bits, w.plan, w.perm, w.sg2, w.zg2, nullptr, s));
+    mode = QM_BHQ;
+  }
+  tr.end(2);
+
+  // Q_f(X): deterministic PTQ, codes [d_in, N] in slot order (rows through perm)
+  QuantParams px{};
+  px.x = X;
+  px.rows = N;
+  px.cols = d_in;
+  px.perm = w.perm;
+  px.bits = cfg->f_bits;
+  px.scale = w.sx;
+  px.zero = w.zx;
+  px.q_t = w.qx_t;
+  px.sum_t = w.sum_x;
+  tr.begin(3);
+  FQT_TRY(launch_quant(px, QM_TENSOR, s));
+  tr.end(3);
+  // Q_theta(W): deterministic PTQ, codes [d_in, d_out]
+  QuantParams pw{};
+  pw.x = W;
+  pw.rows = d_out;
+  pw.cols = d_in;
+  pw.bits = cfg->theta_bits;
+  pw.scale = w.sw;
+  pw.zero = w.zw;
+  pw.q_t = w.qw_t;
+  pw.sum_t = w.sum_w;
+  tr.begin(4);
+  FQT_TRY(launch_quant(pw, QM_TENSOR, s));
+  tr.end(4);
+  // Q_b2(G) [N, d_out] slot order (stream 1) and Q_b1(G) [d_out, N] (stream 0), one read of G
+  QuantParams pg{};
+  pg.x = G;
+  pg.rows = N;
+  pg.cols = d_out;
+  pg.perm = w.perm;
+  pg.bits = qx.bits;
+  pg.stoch = 1;
+  pg.seed = cfg->seed;
+  pg.stream = 1;
+  pg.scale = w.sg2;
+  pg.zero = w.zg2;
+  pg.q_nat = w.qg2;
+  pg.sum_nat = w.sum_g2;
+  pg.bits2 = cfg->qb_w.bits;
+  pg.stream2 = 0;
+  pg.scale2 = w.sg1;
+  pg.zero2 = w.zg1;
+  pg.q2_t = w.qg1_t;
+  pg.sum2_t = w.sum_g1;
+  pg.L = L;
+  tr.begin(5);
+  FQT_TRY(launch_quant(pg, mode, s));
+  tr.end(5);
+
+  // grad_W [d_out, d_in] = Q_b1(G)^T Q_f(X): contraction over the N samples
+  GemmParams gw{};
+  gw.A = w.qg1_t;
+  gw.B = w.qx_t;
+  gw.M = d_out;
+  gw.N = d_in;
+  gw.K = N;
+  gw.lda = N;
+  gw.ldb = N;
+  gw.splits = w.splits;
+  gw.kchunk = w.splits > 1 ? MAX_K_CHUNK : N;
+  gw.part = w.part;
+  gw.out = grad_W;
+  gw.ldo = d_in;
+  gw.sumA = w.sum_g1;
+  gw.sumB = w.sum_x;
+  gw.scaleA = w.sg1;
+  gw.zeroA = w.zg1;
+  gw.halfA = 1 << (cfg->qb_w.bits - 1);
+  gw.scaleB = w.sx;
+  gw.zeroB = w.zx;
+  gw.halfB = 1 << (cfg->f_bits - 1);
+  tr.begin(6);
+  if (w.splits > 1) {
+    FQT_TRY(launch_gemm(gw, EPI_RAW_I32, s));
+    FQT_TRY(launch_splitk_reduce(gw, nullptr, EPI_TENSOR, s));
+  } else {
+    FQT_TRY(launch_gemm(gw, EPI_TENSOR, s));
+  }
+  tr.end(6);
+  // grad_X [N, d_in] = Q_b2(G) Q_theta(W): contraction over d_out
+  GemmParams gx{};
+  gx.A = w.qg2;
+  gx.B = w.qw_t;
+  gx.M = N;
+  gx.N = d_in;
+  gx.K = d_out;
+  gx.lda = d_out;
+  gx.ldb = d_out;
+  gx.splits = 1;
+  gx.kchunk = d_out;
+  gx.out = grad_X;
+  gx.ldo = d_in;
+  gx.perm = w.perm;
+  gx.sumA = w.sum_g2;
+  gx.sumB = w.sum_w;
+  gx.scaleA = w.sg2;
+  gx.zeroA = w.zg2;
+  gx.rowwiseA = qx.kind != FQT_PTQ;
+  gx.halfA = 1 << (qx.bits - 1);
+  gx.scaleB = w.sw;
+  gx.zeroB = w.zw;
+  gx.halfB = 1 << (cfg->theta_bits - 1);
+  gx.L = L;
+  tr.begin(7);
+  FQT_TRY(launch_gemm(gx, bhq ? EPI_BHQ : EPI_ROW, s));
+  tr.end(7);
+  return FQT_OK;
+}
+
+size_t fqt_gemm_workspace(int64_t M, int64_t N, int64_t K) {
+  if (M < 1 || N < 1 || K < 1) return 0;
+  const int64_t splits = (K + MAX_K_CHUNK - 1) / MAX_K_CHUNK;
+  return (size_t)(splits * M * N * 4) + 256;
+}
+
+fqt_status fqt_gemm_s8s8_s64(const int8_t* A, const int8_t* B, int64_t M, int64_t N, int64_t K, int64_t lda,
+                             int64_t ldb, int64_t* C, void* ws, size_t ws_bytes, fqt_stream_t s) {
+  if (!A || !B || !C) return FQT_EINVAL;
+  if (M < 1 || N < 1 || K < 1 || lda < K || ldb < K) return FQT_EINVAL;
+  if (M > 65535LL * 128 || (K + MAX_K_CHUNK - 1) / MAX_K_CHUNK > 65535) return FQT_EUNSUPPORTED;
+  if (!ws) return FQT_EWORKSPACE;
+  if (ws_bytes < fqt_gemm_workspace(M, N, K)) return FQT_EWORKSPACE;
+  GemmParams g{};
+  g.A = A;
+  g.B = B;
+  g.M = M;
+  g.N = N;
+  g.K = K;
+  g.lda = lda;
+  g.ldb = ldb;
+  g.splits = (int)((K + MAX_K_CHUNK - 1) / MAX_K_CHUNK);
+  g.kchunk = g.splits > 1 ? MAX_K_CHUNK : K;
+  g.part = static_cast<int32_t*>(ws);
+  FQT_TRY(launch_gemm(g, EPI_RAW_I32, s));
+  FQT_TRY(launch_splitk_reduce(g, C, EPI_RAW_I32, s));
+  return FQT_OK;
+}
+
+fqt_status fqt_conv_backward_im2col(const float* X, const float* W, const float* G, const fqt_conv_shape* shape,
+                                    const fqt_bwd_cfg* cfg, float* grad_W, float* grad_X, void* ws,
+                                    size_t ws_bytes, fqt_stream_t s) {
+  (void)X;
+  (void)W;
+  (void)G;
+  (void)shape;
+  (void)cfg;
+  (void)grad_W;
+  (void)grad_X;
+  (void)ws;
+  (void)ws_bytes;
+  (void)s;
+  return FQT_EUNSUPPORTED;
+}
+
+size_t fqt_conv_backward_workspace(const fqt_conv_shape* shape, const fqt_bwd_cfg* cfg) {
+  (void)shape;
+  (void)cfg;
+  return 0;
+}
+
+fqt_status fqt_workspace_status(const void* ws, fqt_stream_t s) {
+  if (!ws) return FQT_EINVAL;
+  if (hipStreamSynchronize(s) != hipSuccess) return FQT_EDEVICE;
+  uint32_t word = 0;
+  if (hipMemcpy(&word, ws, sizeof(word), hipMemcpyDeviceToHost) != hipSuccess) return FQT_EDEVICE;
+  return (word & STATUS_NONFINITE) ? FQT_ENONFINITE : FQT_OK;
+}
+
+const char* fqt_status_str(fqt_status st) {
+  switch (st) {
+    case FQT_OK: return "ok";
+    case FQT_EINVAL: return "invalid argument";
+    case FQT_EUNSUPPORTED: return "unsupported configuration";
+    case FQT_ENONFINITE: return "non-finite input or range overflow";
+    case FQT_EWORKSPACE: return "workspace missing or too small";
+    case FQT_EDEVICE: return "HIP runtime error";
+  }
+  return "unknown status";
+}
+
+const char* fqt_version(void) { return "fqt-mi355x 0.1 (gfx950)"; }
+
+}  // extern "C"

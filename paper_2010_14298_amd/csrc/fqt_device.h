@@ -1,0 +1,98 @@
+// Device helpers shared by the FQT kernels: Philox4x32-10, stochastic
+// rounding, order-preserving float encodings for atomic min / max.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace fqt {
+
+// ---------------------------------------------------------------------------
+// Philox4x32-10 (Salmon et al., SC'11): four 32-bit words from a 128-bit
+// counter under a 64-bit key.  Ten rounds; the key is advanced by the two
+// Weyl increments between rounds.
+// ---------------------------------------------------------------------------
+struct u32x4 {
+  uint32_t x, y, z, w;
+};
+
+__device__ __forceinline__ u32x4 philox10(uint32_t c0, uint32_t c1, uint32_t c2, uint32_t c3, uint32_t k0,
+                                          uint32_t k1) {
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    const uint64_t p0 = (uint64_t)0xD2511F53u * c0;
+    const uint64_t p1 = (uint64_t)0xCD9E8D57u * c2;
+    const uint32_t n0 = (uint32_t)(p1 >> 32) ^ c1 ^ k0;
+    const uint32_t n2 = (uint32_t)(p0 >> 32) ^ c3 ^ k1;
+    c1 = (uint32_t)p1;
+    c3 = (uint32_t)p0;
+    c0 = n0;
+    c2 = n2;
+    k0 += 0x9E3779B9u;
+    k1 += 0xBB67AE85u;
+  }
+  return u32x4{c0, c1, c2, c3};
+}
+
+// Philox block holding logical element e (e multiple of 4 gives words for
+// e..e+3 in order).
+__device__ __forceinline__ u32x4 philox_block(uint64_t e, uint64_t seed, uint32_t stream) {
+  const uint64_t blk = e >> 2;
+  return philox10((uint32_t)blk, (uint32_t)(blk >> 32), stream, 0u, (uint32_t)seed, (uint32_t)(seed >> 32));
+}
+
+__device__ __forceinline__ uint32_t philox_word(const u32x4& o, int i) {
+  return i == 0 ? o.x : (i == 1 ? o.y : (i == 2 ? o.z : o.w));
+}
+
+// ---------------------------------------------------------------------------
+// Stochastic rounding with a 24-bit uniform (Sec. 3.3):
+//   fl = floor(y); frac = y - fl; round up iff float(word >> 8) < frac * 2^24;
+//   code clamped to [0, B].
+// fl is clamped to [-1, B] first, which leaves the clamped code unchanged and
+// keeps the integer conversion in range.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ int sr_code(float y, uint32_t word, int B) {
+  float fl = floorf(y);
+  const float frac = y - fl;
+  const float thr = frac * 16777216.0f;
+  const float u = (float)(word >> 8);
+  fl = fminf(fmaxf(fl, -1.0f), (float)B);
+  int c = (int)fl + (u < thr ? 1 : 0);
+  return min(max(c, 0), B);
+}
+
+// Deterministic round-half-to-even, clamped to [0, B] (Q_f, Q_theta).
+__device__ __forceinline__ int rne_code(float y, int B) {
+  float r = rintf(y);
+  r = fminf(fmaxf(r, 0.0f), (float)B);
+  return (int)r;
+}
+
+// ---------------------------------------------------------------------------
+// Order-preserving uint32 encoding of float32 (for unsigned atomic min/max).
+// ---------------------------------------------------------------------------
+__host__ __device__ __forceinline__ uint32_t f2ord(float f) {
+  uint32_t u = __float_as_uint(f);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+__host__ __device__ __forceinline__ float ord2f(uint32_t u) {
+  return __uint_as_float((u & 0x80000000u) ? (u & 0x7FFFFFFFu) : ~u);
+}
+constexpr uint32_t ORD_POS_INF = 0xFF800000u;  // f2ord(+inf): identity of min
+constexpr uint32_t ORD_NEG_INF = 0x007FFFFFu;  // f2ord(-inf): identity of max
+
+constexpr float FLT_MAX_F = 3.402823466e+38f;
+
+// s = B / R (one correctly rounded float32 division); R = 0 gives 1;
+// overflow saturates at FLT_MAX.
+__device__ __forceinline__ float scale_from_range(float R, int B) {
+  if (!(R > 0.0f)) return 1.0f;
+  float s = __fdiv_rn((float)B, R);
+  return (s > FLT_MAX_F) ? FLT_MAX_F : s;
+}
+
+// Status word bits (first word of every workspace).
+constexpr uint32_t STATUS_NONFINITE = 1u;
+
+}  // namespace fqt

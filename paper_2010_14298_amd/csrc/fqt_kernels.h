@@ -1,0 +1,120 @@
+// Internal launch interface between the FQT host layer (api.hip) and the
+// kernels (quant.hip, gemm.hip, conv.hip).  Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace fqt {
+
+// ---- quantizer front end -------------------------------------------------
+
+hipError_t launch_fill_u32(uint32_t* p, uint32_t v, int64_t n, hipStream_t s);
+
+// Global min / max (order-encoded) of a flat tensor; sets STATUS_NONFINITE.
+hipError_t launch_stats_flat(const float* x, int64_t n, uint32_t* gminmax, uint32_t* status, hipStream_t s);
+
+// Per-row min / max (order-encoded) plus the global min / max.
+hipError_t launch_stats_rows(const float* x, int64_t rows, int64_t cols, uint32_t* rmin, uint32_t* rmax,
+                             uint32_t* gminmax, uint32_t* status, hipStream_t s);
+
+// Per-tensor scale and zero point from a global min / max (Sec. 3.3).
+hipError_t launch_ptq_finalize(const uint32_t* gminmax, int bits, float* scale, float* zero, uint32_t* status,
+                               hipStream_t s);
+
+// Per-row scale and zero point (Sec. 4.1).
+hipError_t launch_psq_finalize(const uint32_t* rmin, const uint32_t* rmax, int64_t rows, int bits, float* scale,
+                               float* zero, uint32_t* status, hipStream_t s);
+
+// Fixed-block BHQ layout, all data independent (see bhq_layout()).
+struct BhqLayout {
+  int64_t rows;
+  int k;        // block size
+  int64_t G;    // number of groups
+  int64_t full; // groups of exactly k rows (first in slot order)
+  int part;     // size of the one partial group after them (0: none)
+  double sk_k, sk_p;        // sqrt(k), sqrt(part)
+  double inv_sk_k, inv_sk_p;  // 1/sqrt(k), 1/sqrt(part) in float64 (dequantization)
+  float a_k, oma_k, a_p, oma_p;  // float32(1/sqrt(size)) and float32(1 - that)
+};
+BhqLayout bhq_layout(int64_t rows, int k);
+
+// Slot kind under a fixed-block layout: 0 = one-row group, 1 = full group,
+// 2 = the partial group.  Groups are stored full ones first, then the
+// partial one, then the one-row groups, each full / partial group starting
+// at a multiple of k.
+__device__ __forceinline__ int bhq_slot_kind(const BhqLayout& L, int64_t slot) {
+  if (slot < L.full * L.k) return 1;
+  if (L.part > 0 && slot < L.full * L.k + L.part) return 2;
+  return 0;
+}
+
+// Workspace for the BHQ plan: keys, sorted chunks, rank, sigma.
+size_t bhq_plan_workspace(int64_t rows);
+hipError_t launch_bhq_plan(const uint32_t* rmin, const uint32_t* rmax, const BhqLayout& L, int bits, void* plan_ws,
+                           int32_t* perm, float* scale, float* zero, int32_t* group_off, hipStream_t s);
+
+struct QuantParams {
+  const float* x;
+  int64_t rows, cols;
+  const int32_t* perm;  // slot -> source row; nullptr = identity
+  int bits;
+  int stoch;
+  uint64_t seed;
+  uint32_t stream;
+  const float* scale;  // per tensor: [1]; per row / BHQ: [rows] per slot
+  const float* zero;
+  int8_t* q_nat;       // [rows, cols] slot order, or nullptr
+  int32_t* sum_nat;    // [rows] row sums, or nullptr
+  int8_t* q_t;         // [cols, rows] slot order, or nullptr
+  int32_t* sum_t;      // [cols] column sums, or nullptr
+  // second, per-tensor stochastic quantizer of the same rows (Q_b1); transposed only
+  int bits2;
+  uint32_t stream2;
+  const float* scale2;
+  const float* zero2;
+  int8_t* q2_t;
+  int32_t* sum2_t;
+  BhqLayout L;
+};
+enum QuantMode { QM_TENSOR = 0, QM_ROW = 1, QM_BHQ = 2 };
+hipError_t launch_quant(const QuantParams& p, int mode, hipStream_t s);
+
+// ---- int8 contractions ---------------------------------------------------
+
+enum Epilogue {
+  EPI_RAW_I32 = 0,   // int32 partials [splits][M][N] (caller reduces)
+  EPI_TENSOR = 1,    // per-tensor A, per-tensor B: grad_W
+  EPI_ROW = 2,       // per-row A (PTQ broadcasts), per-tensor B: grad_X
+  EPI_BHQ = 3        // per-group Householder on A rows, per-tensor B: grad_X
+};
+
+struct GemmParams {
+  const int8_t* A;  // [M, K] row stride lda
+  const int8_t* B;  // [N, K] row stride ldb
+  int64_t M, N, K, lda, ldb;
+  int64_t kchunk;   // K per split (multiple of 64, <= 65536)
+  int splits;
+  int32_t* part;    // EPI_RAW_I32 output [splits][M][N]
+  // epilogue data (float64 arithmetic, float32 result)
+  float* out;       // [M, N] (row index remapped through perm when given)
+  int64_t ldo;
+  const int32_t* perm;   // A row (slot) -> output row; nullptr = identity
+  const int32_t* sumA;   // [M] sum over K of A's codes
+  const int32_t* sumB;   // [N] sum over K of B's codes
+  const float* scaleA;   // [1] or [M]
+  const float* zeroA;
+  int rowwiseA;          // scaleA / zeroA indexed per row
+  int halfA;             // 2^(bitsA - 1)
+  const float* scaleB;   // [1]
+  const float* zeroB;
+  int halfB;
+  BhqLayout L;           // EPI_BHQ group structure
+};
+hipError_t launch_gemm(const GemmParams& p, int epi, hipStream_t s);
+
+// Sum int32 split partials in int64; either store int64 (out64) or apply the
+// per-tensor epilogue (EPI_TENSOR) into p.out.
+hipError_t launch_splitk_reduce(const GemmParams& p, int64_t* out64, int epi, hipStream_t s);
+
+}  // namespace fqt

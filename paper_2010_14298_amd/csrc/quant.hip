@@ -1,0 +1,795 @@
+// Gradient / activation / weight quantizers of the FQT backward on gfx950.
+//
+//   stats      per-row and per-tensor min / max by wavefront shuffles and
+//              order-preserving atomics (exact in any order)
+//   finalize   PTQ scale s = B / R, zero z = min (Sec. 3.3); PSQ per row
+//              (Sec. 4.1)
+//   bhq plan   sort by row infinity norm, grouping and per-group scalars of
+//              the block Householder quantizer (Sec. 4.2, App. C.4, App. D)
+//   quant      one pass over the matrix: affine map or block Householder
+//              transform, stochastic rounding from a Philox stream, int8
+//              offset codes in natural and / or transposed layout with code
+//              sums; optionally a second per-tensor quantizer (the
+//              bifurcated Q_b1 of App. E) from the same read.
+#include <math.h>
+
+#include "fqt_device.h"
+#include "fqt_kernels.h"
+
+namespace fqt {
+
+// ---------------------------------------------------------------------------
+// small utilities
+// ---------------------------------------------------------------------------
+__global__ void fill_u32_kernel(uint32_t* p, uint32_t v, int64_t n) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+    p[i] = v;
+}
+
+hipError_t launch_fill_u32(uint32_t* p, uint32_t v, int64_t n, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  int64_t blocks = (n + 255) / 256;
+  if (blocks > 4096) blocks = 4096;
+  hipLaunchKernelGGL(fill_u32_kernel, dim3((unsigned)blocks), dim3(256), 0, s, p, v, n);
+  return hipGetLastError();
+}
+
+__device__ __forceinline__ float wave_min(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fminf(v, __shfl_xor(v, o));
+  return v;
+}
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+  return v;
+}
+__device__ __forceinline__ int wave_sum_i(int v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
+// Block-wide min / max / non-finite flag; thread 0 publishes by atomics.
+__device__ __forceinline__ void block_publish(float mn, float mx, bool bad, uint32_t* amin, uint32_t* amax,
+                                              uint32_t* gminmax, uint32_t* status) {
+  __shared__ float smn[16], smx[16];
+  __shared__ int sbad;
+  if (threadIdx.x == 0) sbad = 0;
+  __syncthreads();
+  mn = wave_min(mn);
+  mx = wave_max(mx);
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  if (bad) atomicOr(&sbad, 1);
+  if (lane == 0) {
+    smn[w] = mn;
+    smx[w] = mx;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const int nw = (blockDim.x + 63) >> 6;
+    for (int i = 1; i < nw; ++i) {
+      mn = fminf(mn, smn[i]);
+      mx = fmaxf(mx, smx[i]);
+    }
+    if (amin) atomicMin(amin, f2ord(mn));
+    if (amax) atomicMax(amax, f2ord(mx));
+    if (gminmax) {
+      atomicMin(gminmax + 0, f2ord(mn));
+      atomicMax(gminmax + 1, f2ord(mx));
+    }
+    if (sbad) atomicOr(status, STATUS_NONFINITE);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// stats
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void stats_flat_kernel(const float* __restrict__ x, int64_t n,
+                                                         uint32_t* gminmax, uint32_t* status) {
+  float mn = INFINITY, mx = -INFINITY;
+  bool bad = false;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  const int64_t tid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if ((n & 3) == 0 && ((uintptr_t)x & 15) == 0) {
+    const float4* x4 = reinterpret_cast<const float4*>(x);
+    for (int64_t i = tid; i < (n >> 2); i += stride) {
+      const float4 v = x4[i];
+      mn = fminf(fminf(mn, v.x), fminf(v.y, fminf(v.z, v.w)));
+      mx = fmaxf(fmaxf(mx, v.x), fmaxf(v.y, fmaxf(v.z, v.w)));
+      bad |= !(isfinite(v.x) && isfinite(v.y) && isfinite(v.z) && isfinite(v.w));
+    }
+  } else {
+    for (int64_t i = tid; i < n; i += stride) {
+      const float v = x[i];
+      mn = fminf(mn, v);
+      mx = fmaxf(mx, v);
+      bad |= !isfinite(v);
+    }
+  }
+  block_publish(mn, mx, bad, nullptr, nullptr, gminmax, status);
+}
+
+hipError_t launch_stats_flat(const float* x, int64_t n, uint32_t* gminmax, uint32_t* status, hipStream_t s) {
+  int64_t blocks = (n / 4 + 255) / 256;
+  if (blocks < 1) blocks = 1;
+  if (blocks > 2048) blocks = 2048;
+  hipLaunchKernelGGL(stats_flat_kernel, dim3((unsigned)blocks), dim3(256), 0, s, x, n, gminmax, status);
+  return hipGetLastError();
+}
+
+constexpr int64_t STATS_CHUNK = 8192;  // columns per block of stats_rows
+
+__global__ __launch_bounds__(256) void stats_rows_kernel(const float* __restrict__ x, int64_t rows, int64_t cols,
+                                                         uint32_t* rmin, uint32_t* rmax, uint32_t* gminmax,
+                                                         uint32_t* status) {
+  const int64_t row = blockIdx.x;
+  const int64_t c_begin = (int64_t)blockIdx.y * STATS_CHUNK;
+  const int64_t c_end = (c_begin + STATS_CHUNK < cols) ? c_begin + STATS_CHUNK : cols;
+  const float* xr = x + row * cols;
+  float mn = INFINITY, mx = -INFINITY;
+  bool bad = false;
+  if ((cols & 3) == 0 && ((uintptr_t)x & 15) == 0) {
+    const float4* x4 = reinterpret_cast<const float4*>(xr);
+    for (int64_t i = (c_begin >> 2) + threadIdx.x; i < (c_end >> 2); i += blockDim.x) {
+      const float4 v = x4[i];
+      mn = fminf(fminf(mn, v.x), fminf(v.y, fminf(v.z, v.w)));
+      mx = fmaxf(fmaxf(mx, v.x), fmaxf(v.y, fmaxf(v.z, v.w)));
+      bad |= !(isfinite(v.x) && isfinite(v.y) && isfinite(v.z) && isfinite(v.w));
+    }
+  } else {
+    for (int64_t i = c_begin + threadIdx.x; i < c_end; i += blockDim.x) {
+      const float v = xr[i];
+      mn = fminf(mn, v);
+      mx = fmaxf(mx, v);
+      bad |= !isfinite(v);
+    }
+  }
+  block_publish(mn, mx, bad, rmin + row, rmax + row, gminmax, status);
+}
+
+hipError_t launch_stats_rows(const float* x, int64_t rows, int64_t cols, uint32_t* rmin, uint32_t* rmax,
+                             uint32_t* gminmax, uint32_t* status, hipStream_t s) {
+  const int64_t chunks = (cols + STATS_CHUNK - 1) / STATS_CHUNK;
+  if (rows > 0x7FFFFFFF || chunks > 65535) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(stats_rows_kernel, dim3((unsigned)rows, (unsigned)chunks), dim3(256), 0, s, x, rows, cols,
+                     rmin, rmax, gminmax, status);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// finalize: PTQ and PSQ scalars
+// ---------------------------------------------------------------------------
+__global__ void ptq_finalize_kernel(const uint32_t* gminmax, int B, float* scale, float* zero, uint32_t* status) {
+  const float z = ord2f(gminmax[0]);
+  const float mx = ord2f(gminmax[1]);
+  const float R = mx - z;
+  if (!isfinite(R)) atomicOr(status, STATUS_NONFINITE);
+  scale[0] = scale_from_range(R, B);
+  zero[0] = z;
+}
+
+hipError_t launch_ptq_finalize(const uint32_t* gminmax, int bits, float* scale, float* zero, uint32_t* status,
+                               hipStream_t s) {
+  hipLaunchKernelGGL(ptq_finalize_kernel, dim3(1), dim3(1), 0, s, gminmax, (1 << bits) - 1, scale, zero, status);
+  return hipGetLastError();
+}
+
+__global__ void psq_finalize_kernel(const uint32_t* rmin, const uint32_t* rmax, int64_t rows, int B, float* scale,
+                                    float* zero, uint32_t* status) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= rows) return;
+  const float z = ord2f(rmin[i]);
+  const float R = ord2f(rmax[i]) - z;
+  if (!isfinite(R)) atomicOr(status, STATUS_NONFINITE);
+  scale[i] = scale_from_range(R, B);
+  zero[i] = z;
+}
+
+hipError_t launch_psq_finalize(const uint32_t* rmin, const uint32_t* rmax, int64_t rows, int bits, float* scale,
+                               float* zero, uint32_t* status, hipStream_t s) {
+  hipLaunchKernelGGL(psq_finalize_kernel, dim3((unsigned)((rows + 255) / 256)), dim3(256), 0, s, rmin, rmax, rows,
+                     (1 << bits) - 1, scale, zero, status);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// BHQ plan
+// ---------------------------------------------------------------------------
+BhqLayout bhq_layout(int64_t rows, int k) {
+  BhqLayout L{};
+  L.rows = rows;
+  L.k = k;
+  L.G = (rows + k - 1) / k;
+  const int64_t small = rows - L.G;
+  if (k > 1) {
+    L.full = small / (k - 1);
+    const int64_t rem = small % (k - 1);
+    L.part = rem > 0 ? (int)(1 + rem) : 0;
+  } else {
+    L.full = 0;
+    L.part = 0;
+  }
+  // Per-size scalars, IEEE double on the host: sqrt(size), float32(1/sqrt)
+  // and the float32 difference 1 - alpha.
+  L.sk_k = sqrt((double)k);
+  L.a_k = (float)(1.0 / L.sk_k);
+  L.oma_k = 1.0f - L.a_k;
+  const int ps = L.part > 0 ? L.part : 1;
+  L.sk_p = sqrt((double)ps);
+  L.a_p = (float)(1.0 / L.sk_p);
+  L.oma_p = 1.0f - L.a_p;
+  L.inv_sk_k = 1.0 / L.sk_k;
+  L.inv_sk_p = 1.0 / L.sk_p;
+  return L;
+}
+
+constexpr int SORT_CH = 1024;  // keys per sorted chunk
+
+static int64_t sort_pad(int64_t rows) { return (rows + SORT_CH - 1) / SORT_CH * SORT_CH; }
+
+size_t bhq_plan_workspace(int64_t rows) {
+  const int64_t np = sort_pad(rows);
+  // keys, sorted chunks (uint64 each), rank and sigma (int32 each)
+  return (size_t)np * 8 * 2 + (size_t)rows * 4 * 2 + 256;
+}
+
+// key = (~bits(M_i) << 32) | i: ascending order = M descending, index ascending.
+__global__ void bhq_keys_kernel(const uint32_t* rmin, const uint32_t* rmax, int64_t rows, int64_t npad,
+                                uint64_t* keys, int32_t* rank) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= npad) return;
+  if (i < rows) {
+    const float M = fmaxf(fabsf(ord2f(rmin[i])), fabsf(ord2f(rmax[i])));
+    keys[i] = ((uint64_t)(~__float_as_uint(M)) << 32) | (uint64_t)(uint32_t)i;
+    rank[i] = 0;
+  } else {
+    keys[i] = ~0ull;
+  }
+}
+
+// Bitonic sort of one 1024-key chunk in LDS.
+__global__ __launch_bounds__(512) void bhq_sort_chunks_kernel(const uint64_t* keys, uint64_t* sorted) {
+  __shared__ uint64_t sk[SORT_CH];
+  const int t = threadIdx.x;
+  const int64_t base = (int64_t)blockIdx.x * SORT_CH;
+  sk[t] = keys[base + t];
+  sk[t + 512] = keys[base + t + 512];
+  for (int size = 2; size <= SORT_CH; size <<= 1) {
+    for (int stride = size >> 1; stride > 0; stride >>= 1) {
+      __syncthreads();
+      const int i = (t / stride) * 2 * stride + (t % stride);
+      const int j = i + stride;
+      const bool asc = (i & size) == 0;
+      const uint64_t a = sk[i], b = sk[j];
+      if ((a > b) == asc) {
+        sk[i] = b;
+        sk[j] = a;
+      }
+    }
+  }
+  __syncthreads();
+  sorted[base + t] = sk[t];
+  sorted[base + t + 512] = sk[t + 512];
+}
+
+// rank(key) = number of keys below it, summed over every sorted chunk.
+__global__ __launch_bounds__(256) void bhq_rank_kernel(const uint64_t* sorted, int32_t* rank) {
+  __shared__ uint64_t sk[SORT_CH];
+  const int t = threadIdx.x;
+  const int64_t cbase = (int64_t)blockIdx.x * SORT_CH;
+  const int64_t sbase = (int64_t)blockIdx.y * SORT_CH;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) sk[t + 256 * e] = sorted[sbase + t + 256 * e];
+  __syncthreads();
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const uint64_t key = sorted[cbase + t + 256 * e];
+    if (key == ~0ull) continue;
+    int lo = 0, hi = SORT_CH;  // first index with sk[idx] >= key
+    while (lo < hi) {
+      const int mid = (lo + hi) >> 1;
+      if (sk[mid] < key)
+        lo = mid + 1;
+      else
+        hi = mid;
+    }
+    if (lo > 0) atomicAdd(&rank[(uint32_t)key], lo);
+  }
+}
+
+__global__ void bhq_scatter_kernel(const int32_t* rank, int64_t rows, int32_t* sigma) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < rows) sigma[rank[i]] = (int32_t)i;
+}
+
+// Correctly rounded float32 cube root of a positive finite float: a float64
+// estimate, then exact comparisons of x with the cubes of the midpoints to
+// the float32 neighbours.  mid^2 is exact in float64 (25-bit mid); mid^3 =
+// p + e exactly with p = fl(mid^2 mid), e = fma(mid^2, mid, -p); p - x is
+// exact (Sterbenz), so mid^3 > x iff (p - x) > -e.
+__device__ bool cube_gt(double mid, double x) {
+  const double m2 = mid * mid;
+  const double p = m2 * mid;
+  const double e = fma(m2, mid, -p);
+  return (p - x) > -e;
+}
+__device__ bool cube_lt(double mid, double x) {
+  const double m2 = mid * mid;
+  const double p = m2 * mid;
+  const double e = fma(m2, mid, -p);
+  return (p - x) < -e;
+}
+__device__ float cbrt_rn(float x) {
+  if (!(x > 0.0f)) return 0.0f;
+  float r = (float)cbrt((double)x);
+  const double xd = (double)x;
+  for (int it = 0; it < 8; ++it) {
+    const uint32_t b = __float_as_uint(r);
+    const float up = __uint_as_float(b + 1);
+    const float dn = __uint_as_float(b - 1);
+    const double mid_up = 0.5 * ((double)r + (double)up);
+    const double mid_dn = 0.5 * ((double)r + (double)dn);
+    if (cube_lt(mid_up, xd)) {
+      r = up;
+    } else if (cube_gt(mid_dn, xd)) {
+      r = dn;
+    } else {
+      break;
+    }
+  }
+  return r;
+}
+
+__device__ __forceinline__ float to_f32_sat(double v) {
+  float f = (float)v;
+  return (f > FLT_MAX_F) ? FLT_MAX_F : f;
+}
+
+// One thread per group: perm, per-slot scale d_p and zero (c_g or row min).
+__global__ void bhq_groups_kernel(const uint32_t* rmin, const uint32_t* rmax, const int32_t* sigma, BhqLayout L,
+                                  int B, int32_t* perm, float* scale, float* zero, int32_t* group_off) {
+  const int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (g >= L.G) return;
+  const int k = L.k;
+  int kg;
+  int64_t base;
+  if (g < L.full) {
+    kg = k;
+    base = g * k;
+  } else if (g == L.full && L.part > 0) {
+    kg = L.part;
+    base = L.full * k;
+  } else {
+    kg = 1;
+    base = L.full * k + L.part + (g - L.full - (L.part > 0 ? 1 : 0));
+  }
+  if (group_off) {
+    group_off[g] = (int32_t)base;
+    if (g == L.G - 1) group_off[L.G] = (int32_t)L.rows;
+  }
+  const int32_t big = sigma[g];
+  perm[base] = big;
+  const float mn0 = ord2f(rmin[big]);
+  const float mx0 = ord2f(rmax[big]);
+  if (kg == 1) {
+    scale[base] = scale_from_range(mx0 - mn0, B);
+    zero[base] = mn0;
+    return;
+  }
+  const int64_t tail = L.G + g * (int64_t)(k - 1);
+  float m2 = 0.0f;
+  for (int j = 0; j < kg - 1; ++j) {
+    const int32_t r = sigma[tail + j];
+    perm[base + 1 + j] = r;
+    const float M = fmaxf(fabsf(ord2f(rmin[r])), fabsf(ord2f(rmax[r])));
+    m2 = fmaxf(m2, M);
+  }
+  float lam1 = mx0 - mn0;
+  const float lam2 = 2.0f * m2;
+  if (lam1 == 0.0f) lam1 = lam2;
+  const double sk = (kg == k) ? L.sk_k : L.sk_p;
+  const float alpha = (kg == k) ? L.a_k : L.a_p;
+  float s1, s2;
+  if (lam1 == 0.0f && lam2 == 0.0f) {
+    s1 = s2 = 1.0f;
+  } else if (lam2 == 0.0f) {
+    s1 = s2 = to_f32_sat(((double)B * sk) / (double)lam1);
+  } else {
+    const double a = (double)cbrt_rn(lam1);
+    const double c = (double)cbrt_rn(lam2);
+    const double aa = a * a;
+    const double cc = c * c;
+    const double cck = cc * (double)kg;
+    const double t = aa + cck;
+    const double num = (double)B * sk;
+    s1 = to_f32_sat(num / (a * t));
+    s2 = to_f32_sat(num / (c * t));
+  }
+  const double t1 = ((double)alpha * (double)s1) * (double)mn0;
+  const double t2 = ((0.5 * (double)lam2) * (double)s2) * sk;
+  const float cg = (float)(t1 - t2);
+  scale[base] = s1;
+  zero[base] = cg;
+  for (int j = 1; j < kg; ++j) {
+    scale[base + j] = s2;
+    zero[base + j] = cg;
+  }
+}
+
+hipError_t launch_bhq_plan(const uint32_t* rmin, const uint32_t* rmax, const BhqLayout& L, int bits, void* plan_ws,
+                           int32_t* perm, float* scale, float* zero, int32_t* group_off, hipStream_t s) {
+  const int64_t rows = L.rows;
+  const int64_t np = sort_pad(rows);
+  const int64_t nch = np / SORT_CH;
+  if (nch > 65535) return hipErrorInvalidValue;
+  char* w = static_cast<char*>(plan_ws);
+  uint64_t* keys = reinterpret_cast<uint64_t*>(w);
+  uint64_t* sorted = keys + np;
+  int32_t* rank = reinterpret_cast<int32_t*>(sorted + np);
+  int32_t* sigma = rank + rows;
+  hipLaunchKernelGGL(bhq_keys_kernel, dim3((unsigned)((np + 255) / 256)), dim3(256), 0, s, rmin, rmax, rows, np, keys,
+                     rank);
+  hipLaunchKernelGGL(bhq_sort_chunks_kernel, dim3((unsigned)nch), dim3(512), 0, s, keys, sorted);
+  hipLaunchKernelGGL(bhq_rank_kernel, dim3((unsigned)nch, (unsigned)nch), dim3(256), 0, s, sorted, rank);
+  hipLaunchKernelGGL(bhq_scatter_kernel, dim3((unsigned)((rows + 255) / 256)), dim3(256), 0, s, rank, rows, sigma);
+  hipLaunchKernelGGL(bhq_groups_kernel, dim3((unsigned)((L.G + 63) / 64)), dim3(64), 0, s, rmin, rmax, sigma, L,
+                     (1 << bits) - 1, perm, scale, zero, group_off);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// quant: tile = 64 slots x 256 columns, 4 waves of 16 slots, 4 columns / lane
+// ---------------------------------------------------------------------------
+constexpr int QT_SLOTS = 64;
+constexpr int QT_COLS = 256;
+constexpr int QT_ROWS_PER_WAVE = 16;
+
+__device__ __forceinline__ uint32_t pack4(int a, int b, int c, int d) {
+  return (uint32_t)(a & 255) | ((uint32_t)(b & 255) << 8) | ((uint32_t)(c & 255) << 16) | ((uint32_t)(d & 255) << 24);
+}
+
+template <int MODE, int K, bool HAS2>
+__global__ __launch_bounds__(256) void quant_tile_kernel(QuantParams p) {
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int64_t tile0 = (int64_t)blockIdx.y * QT_SLOTS;
+  const int64_t slot0 = tile0 + wave * QT_ROWS_PER_WAVE;
+  const int64_t c0 = (int64_t)blockIdx.x * QT_COLS + lane * 4;
+  const int64_t rows = p.rows, cols = p.cols;
+  const bool vec = (cols & 3) == 0;
+  const int B = (1 << p.bits) - 1;
+  const int half = 1 << (p.bits - 1);
+
+  __shared__ float s_part[4][QT_COLS];   // per-wave partial group sums (BHQ, K >= 16)
+  __shared__ float s_v0[4][QT_COLS];     // v of a group's first slot (BHQ, K >= 16)
+  __shared__ int s_csum[2][4][QT_COLS];  // per-wave column code sums (transposed outputs)
+
+  // ---- load 16 rows x 4 columns
+  float g[QT_ROWS_PER_WAVE][4];
+  int32_t srow[QT_ROWS_PER_WAVE];
+#pragma unroll
+  for (int r = 0; r < QT_ROWS_PER_WAVE; ++r) {
+    const int64_t slot = slot0 + r;
+    const bool ok = slot < rows;
+    const int32_t row = ok ? (p.perm ? p.perm[slot] : (int32_t)slot) : 0;
+    srow[r] = row;
+    const float* xr = p.x + (int64_t)row * cols;
+    if (ok && vec && c0 + 3 < cols) {
+      const float4 v = *reinterpret_cast<const float4*>(xr + c0);
+      g[r][0] = v.x;
+      g[r][1] = v.y;
+      g[r][2] = v.z;
+      g[r][3] = v.w;
+    } else {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) g[r][j] = (ok && c0 + j < cols) ? xr[c0 + j] : 0.0f;
+    }
+  }
+
+  // ---- primary transformed values y (in place in g -> y)
+  float y[QT_ROWS_PER_WAVE][4];
+  if constexpr (MODE == QM_TENSOR || MODE == QM_ROW) {
+    const float s_t = p.scale[0], z_t = p.zero[0];
+#pragma unroll
+    for (int r = 0; r < QT_ROWS_PER_WAVE; ++r) {
+      const int64_t slot = slot0 + r;
+      const bool ok = slot < rows;
+      const float s = (MODE == QM_ROW) ? (ok ? p.scale[slot] : 1.0f) : s_t;
+      const float z = (MODE == QM_ROW) ? (ok ? p.zero[slot] : 0.0f) : z_t;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) y[r][j] = s * (g[r][j] - z);
+    }
+  } else {
+    // block Householder: v = d * g; group sums; Y = v - alpha tau (first
+    // slot: v + (1 - alpha) tau); y' = Y - c_g.  One-row groups use the
+    // per-sample map s (g - z).
+    const BhqLayout& L = p.L;
+    float v[QT_ROWS_PER_WAVE][4];
+    int kind[QT_ROWS_PER_WAVE];
+#pragma unroll
+    for (int r = 0; r < QT_ROWS_PER_WAVE; ++r) {
+      const int64_t slot = slot0 + r;
+      const bool ok = slot < rows;
+      kind[r] = ok ? bhq_slot_kind(L, slot) : 0;
+      const float d = ok ? p.scale[slot] : 1.0f;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) v[r][j] = d * g[r][j];
+    }
+    if constexpr (K >= 16) {
+      // per-wave partial sums over the wave's 16 slots, slot order
+      float P[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+      for (int r = 0; r < QT_ROWS_PER_WAVE; ++r)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) P[j] = P[j] + (kind[r] != 0 ? v[r][j] : 0.0f);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        s_part[wave][lane * 4 + j] = P[j];
+        s_v0[wave][lane * 4 + j] = v[0][j];
+      }
+      __syncthreads();
+      const int nw = K / 16;                       // waves per group
+      const int w0 = (wave / nw) * nw;             // first wave of this wave's group
+      float S[4], v0[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        S[j] = s_part[w0][lane * 4 + j];
+        for (int i = 1; i < nw; ++i) S[j] = S[j] + s_part[w0 + i][lane * 4 + j];
+        v0[j] = s_v0[w0][lane * 4 + j];
+      }
+      // the group's first slot decides full / partial (one-row slots skip)
+      const int64_t gfirst = tile0 + w0 * 16;
+      const int gkind = gfirst < rows ? bhq_slot_kind(L, gfirst) : 0;
+      const float alpha = gkind == 2 ? L.a_p : L.a_k;
+      const float oma = gkind == 2 ? L.oma_p : L.oma_k;
+      float tau[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const float m = alpha * S[j] - v0[j];
+        tau[j] = __fdiv_rn(m, oma);
+      }
+#pragma unroll
+      for (int r = 0; r < QT_ROWS_PER_WAVE; ++r) {
+        const int64_t slot = slot0 + r;
+        const bool ok = slot < rows;
+        const float c = ok ? p.zero[slot] : 0.0f;
+        const bool first = (slot % K) == 0;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          if (kind[r] != 0) {
+            const float Y = first ? v[r][j] + oma * tau[j] : v[r][j] - alpha * tau[j];
+            y[r][j] = Y - c;
+          } else {
+            const float s = ok ? p.scale[slot] : 1.0f;
+            y[r][j] = s * (g[r][j] - c);
+          }
+        }
+      }
+    } else {
+      // K < 16: each group lies inside this wave's 16 slots
+      static_assert(K >= 1 && K < 16, "block size");
+#pragma unroll
+      for (int gi = 0; gi < QT_ROWS_PER_WAVE / K; ++gi) {
+        const int r0 = gi * K;
+        const int64_t gfirst = slot0 + r0;
+        const int gkind = (K > 1 && gfirst < rows) ? bhq_slot_kind(L, gfirst) : 0;
+        const float alpha = gkind == 2 ? L.a_p : L.a_k;
+        const float oma = gkind == 2 ? L.oma_p : L.oma_k;
+        float tau[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+        if constexpr (K > 1) {
+          float S[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+          for (int rr = 0; rr < K; ++rr)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) S[j] = S[j] + (kind[r0 + rr] != 0 ? v[r0 + rr][j] : 0.0f);
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const float m = alpha * S[j] - v[r0][j];
+            tau[j] = __fdiv_rn(m, oma);
+          }
+        }
+#pragma unroll
+        for (int rr = 0; rr < K; ++rr) {
+          const int r = r0 + rr;
+          const int64_t slot = slot0 + r;
+          const bool ok = slot < rows;
+          const float c = ok ? p.zero[slot] : 0.0f;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            if (K > 1 && kind[r] != 0) {
+              const float Y = rr == 0 ? v[r][j] + oma * tau[j] : v[r][j] - alpha * tau[j];
+              y[r][j] = Y - c;
+            } else {
+              const float s = ok ? p.scale[slot] : 1.0f;
+              y[r][j] = s * (g[r][j] - c);
+            }
+          }
+        }
+      }
+    }
+  }
+
+  // ---- rounding, stores, code sums
+  const bool full_vec = vec && c0 + 3 < cols;
+  int csum[4] = {0, 0, 0, 0};
+  uint32_t tcodes[4][4];  // transposed: [column][4 words of 16 slots]
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+#pragma unroll
+    for (int w = 0; w < 4; ++w) tcodes[j][w] = 0u;
+
+#pragma unroll
+  for (int r = 0; r < QT_ROWS_PER_WAVE; ++r) {
+    const int64_t slot = slot0 + r;
+    const bool ok = slot < rows;
+    const uint64_t ebase = (uint64_t)srow[r] * (uint64_t)cols + (uint64_t)c0;
+    int code[4];
+    if (p.stoch) {
+      if (full_vec) {
+        const u32x4 o = philox_block(ebase, p.seed, p.stream);
+        code[0] = sr_code(y[r][0], o.x, B);
+        code[1] = sr_code(y[r][1], o.y, B);
+        code[2] = sr_code(y[r][2], o.z, B);
+        code[3] = sr_code(y[r][3], o.w, B);
+      } else {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const uint64_t e = ebase + j;
+          const u32x4 o = philox_block(e, p.seed, p.stream);
+          code[j] = sr_code(y[r][j], philox_word(o, (int)(e & 3)), B);
+        }
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) code[j] = rne_code(y[r][j], B);
+    }
+    int q[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const bool cok = ok && (c0 + j < cols);
+      q[j] = cok ? code[j] - half : 0;
+    }
+    if (p.q_nat && ok) {
+      int8_t* dst = p.q_nat + slot * cols + c0;
+      if (full_vec) {
+        *reinterpret_cast<uint32_t*>(dst) = pack4(q[0], q[1], q[2], q[3]);
+      } else {
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          if (c0 + j < cols) dst[j] = (int8_t)q[j];
+      }
+    }
+    if (p.sum_nat) {
+      const int t = wave_sum_i(q[0] + q[1] + q[2] + q[3]);
+      if (lane == 0 && ok) atomicAdd(p.sum_nat + slot, t);
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      csum[j] += q[j];
+      tcodes[j][r >> 2] |= (uint32_t)(q[j] & 255) << (8 * (r & 3));
+    }
+  }
+  if (p.q_t) {
+    const bool tvec = ((rows & 15) == 0) && (slot0 + 15 < rows);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int64_t col = c0 + j;
+      if (col >= cols) continue;
+      int8_t* dst = p.q_t + col * rows + slot0;
+      if (tvec) {
+        *reinterpret_cast<uint4*>(dst) = make_uint4(tcodes[j][0], tcodes[j][1], tcodes[j][2], tcodes[j][3]);
+      } else {
+#pragma unroll
+        for (int r = 0; r < QT_ROWS_PER_WAVE; ++r)
+          if (slot0 + r < rows) dst[r] = (int8_t)((tcodes[j][r >> 2] >> (8 * (r & 3))) & 255);
+      }
+    }
+  }
+
+  // ---- second quantizer (per tensor, stochastic, transposed) on the same rows
+  int csum2[4] = {0, 0, 0, 0};
+  if (HAS2) {
+    const int B2 = (1 << p.bits2) - 1;
+    const int half2 = 1 << (p.bits2 - 1);
+    const float s2 = p.scale2[0], z2 = p.zero2[0];
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int w = 0; w < 4; ++w) tcodes[j][w] = 0u;
+#pragma unroll
+    for (int r = 0; r < QT_ROWS_PER_WAVE; ++r) {
+      const int64_t slot = slot0 + r;
+      const bool ok = slot < rows;
+      const uint64_t ebase = (uint64_t)srow[r] * (uint64_t)cols + (uint64_t)c0;
+      int code[4];
+      if (full_vec) {
+        const u32x4 o = philox_block(ebase, p.seed, p.stream2);
+        code[0] = sr_code(s2 * (g[r][0] - z2), o.x, B2);
+        code[1] = sr_code(s2 * (g[r][1] - z2), o.y, B2);
+        code[2] = sr_code(s2 * (g[r][2] - z2), o.z, B2);
+        code[3] = sr_code(s2 * (g[r][3] - z2), o.w, B2);
+      } else {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const uint64_t e = ebase + j;
+          const u32x4 o = philox_block(e, p.seed, p.stream2);
+          code[j] = sr_code(s2 * (g[r][j] - z2), philox_word(o, (int)(e & 3)), B2);
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const bool cok = ok && (c0 + j < cols);
+        const int q = cok ? code[j] - half2 : 0;
+        csum2[j] += q;
+        tcodes[j][r >> 2] |= (uint32_t)(q & 255) << (8 * (r & 3));
+      }
+    }
+    const bool tvec = ((rows & 15) == 0) && (slot0 + 15 < rows);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int64_t col = c0 + j;
+      if (col >= cols) continue;
+      int8_t* dst = p.q2_t + col * rows + slot0;
+      if (tvec) {
+        *reinterpret_cast<uint4*>(dst) = make_uint4(tcodes[j][0], tcodes[j][1], tcodes[j][2], tcodes[j][3]);
+      } else {
+#pragma unroll
+        for (int r = 0; r < QT_ROWS_PER_WAVE; ++r)
+          if (slot0 + r < rows) dst[r] = (int8_t)((tcodes[j][r >> 2] >> (8 * (r & 3))) & 255);
+      }
+    }
+  }
+
+  // ---- column sums of the transposed outputs: reduce the 4 waves in LDS
+  if (p.sum_t || (HAS2 && p.sum2_t)) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      s_csum[0][wave][lane * 4 + j] = csum[j];
+      s_csum[1][wave][lane * 4 + j] = csum2[j];
+    }
+    __syncthreads();
+    const int c = threadIdx.x;  // 256 threads = 256 columns of the tile
+    const int64_t col = (int64_t)blockIdx.x * QT_COLS + c;
+    if (col < cols) {
+      if (p.sum_t) {
+        const int t = s_csum[0][0][c] + s_csum[0][1][c] + s_csum[0][2][c] + s_csum[0][3][c];
+        atomicAdd(p.sum_t + col, t);
+      }
+      if (HAS2 && p.sum2_t) {
+        const int t = s_csum[1][0][c] + s_csum[1][1][c] + s_csum[1][2][c] + s_csum[1][3][c];
+        atomicAdd(p.sum2_t + col, t);
+      }
+    }
+  }
+}
+
+template <int MODE, int K>
+static hipError_t launch_quant_k(const QuantParams& p, hipStream_t s) {
+  const int64_t ct = (p.cols + QT_COLS - 1) / QT_COLS;
+  const int64_t rt = (p.rows + QT_SLOTS - 1) / QT_SLOTS;
+  if (ct > 0x7FFFFFFF || rt > 65535) return hipErrorInvalidValue;
+  const dim3 grid((unsigned)ct, (unsigned)rt);
+  if (p.q2_t)
+    hipLaunchKernelGGL((quant_tile_kernel<MODE, K, true>), grid, dim3(256), 0, s, p);
+  else
+    hipLaunchKernelGGL((quant_tile_kernel<MODE, K, false>), grid, dim3(256), 0, s, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_quant(const QuantParams& p, int mode, hipStream_t s) {
+  if (mode == QM_TENSOR) return launch_quant_k<QM_TENSOR, 0>(p, s);
+  if (mode == QM_ROW) return launch_quant_k<QM_ROW, 0>(p, s);
+  switch (p.L.k) {
+    case 1: return launch_quant_k<QM_BHQ, 1>(p, s);
+    case 2: return launch_quant_k<QM_BHQ, 2>(p, s);
+    case 4: return launch_quant_k<QM_BHQ, 4>(p, s);
+    case 8: return launch_quant_k<QM_BHQ, 8>(p, s);
+    case 16: return launch_quant_k<QM_BHQ, 16>(p, s);
+    case 32: return launch_quant_k<QM_BHQ, 32>(p, s);
+    case 64: return launch_quant_k<QM_BHQ, 64>(p, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace fqt

@@ -1,0 +1,328 @@
+"""ctypes binding of libfqt.so (C ABI in include/fqt.h).
+
+Argument marshalling only: every step of the FQT backward runs in the HIP
+library.  Tensors are torch CUDA (ROCm) tensors; the binding passes their
+device pointers and the current HIP stream, allocates outputs and the
+workspace with torch, and raises on any non-OK status.  There is no CPU
+fallback: if the library is not built or cannot load, every call raises.
+"""
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libfqt.so")
+
+FQT_PTQ, FQT_PSQ, FQT_BHQ = 0, 1, 2
+KINDS = {"ptq": FQT_PTQ, "psq": FQT_PSQ, "bhq": FQT_BHQ}
+STATUS = {0: "FQT_OK", 1: "FQT_EINVAL", 2: "FQT_EUNSUPPORTED", 3: "FQT_ENONFINITE", 4: "FQT_EWORKSPACE",
+          5: "FQT_EDEVICE"}
+
+
+class FqtError(RuntimeError):
+    def __init__(self, fn, code):
+        super().__init__(f"{fn} returned {STATUS.get(code, code)}")
+        self.code = code
+
+
+class QTensor(ctypes.Structure):
+    _fields_ = [("q", ctypes.c_void_p), ("scale", ctypes.c_void_p), ("zero", ctypes.c_void_p),
+                ("perm", ctypes.c_void_p), ("group_off", ctypes.c_void_p), ("code_sum", ctypes.c_void_p)]
+
+
+class QSpec(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int), ("bits", ctypes.c_int), ("block_size", ctypes.c_int)]
+
+
+TRACE_PHASES = 8
+PHASE_NAMES = ["init", "stats", "scales_plan", "quant_X", "quant_W", "quant_G", "gemm_gradW", "gemm_gradX"]
+
+
+class Trace(ctypes.Structure):
+    _fields_ = [("start", ctypes.c_void_p * TRACE_PHASES), ("stop", ctypes.c_void_p * TRACE_PHASES),
+                ("count", ctypes.c_int)]
+
+
+class BwdCfg(ctypes.Structure):
+    _fields_ = [("qb_w", QSpec), ("qb_x", QSpec), ("f_bits", ctypes.c_int), ("theta_bits", ctypes.c_int),
+                ("seed", ctypes.c_uint64), ("trace", ctypes.POINTER(Trace))]
+
+
+class ConvShape(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int) for n in ("n", "c", "h", "w", "o", "kh", "kw", "stride", "pad", "ho", "wo")]
+
+
+EXPORTS = [
+    "fqt_quantize_ptq", "fqt_quantize_psq", "fqt_quantize_bhq", "fqt_quantize_workspace",
+    "fqt_linear_backward", "fqt_linear_backward_workspace",
+    "fqt_conv_backward_im2col", "fqt_conv_backward_workspace",
+    "fqt_gemm_s8s8_s64", "fqt_gemm_workspace",
+    "fqt_workspace_status", "fqt_status_str", "fqt_version",
+]
+
+_lib = None
+
+
+def load(path=LIB_PATH):
+    """Load libfqt.so once and declare its signatures."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with paper_2010_14298_amd.build (no CPU fallback)")
+    lib = ctypes.CDLL(path)
+    vp, i64, i32, u32, u64, sz = (ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_uint32,
+                                  ctypes.c_uint64, ctypes.c_size_t)
+    qtp = ctypes.POINTER(QTensor)
+    cfgp = ctypes.POINTER(BwdCfg)
+    shp = ctypes.POINTER(ConvShape)
+    sig = {
+        "fqt_quantize_ptq": ([vp, i64, i64, i32, i32, u64, u32, i32, qtp, vp, sz, vp], i32),
+        "fqt_quantize_psq": ([vp, i64, i64, i32, u64, u32, qtp, vp, sz, vp], i32),
+        "fqt_quantize_bhq": ([vp, i64, i64, i32, i32, u64, u32, qtp, vp, sz, vp], i32),
+        "fqt_quantize_workspace": ([i32, i64, i64, i32], sz),
+        "fqt_linear_backward": ([vp, vp, vp, i64, i64, i64, cfgp, vp, vp, vp, sz, vp], i32),
+        "fqt_linear_backward_workspace": ([i64, i64, i64, cfgp], sz),
+        "fqt_conv_backward_im2col": ([vp, vp, vp, shp, cfgp, vp, vp, vp, sz, vp], i32),
+        "fqt_conv_backward_workspace": ([shp, cfgp], sz),
+        "fqt_gemm_s8s8_s64": ([vp, vp, i64, i64, i64, i64, i64, vp, vp, sz, vp], i32),
+        "fqt_gemm_workspace": ([i64, i64, i64], sz),
+        "fqt_workspace_status": ([vp, vp], i32),
+        "fqt_status_str": ([i32], ctypes.c_char_p),
+        "fqt_version": ([], ctypes.c_char_p),
+    }
+    for name, (args, res) in sig.items():
+        f = getattr(lib, name)
+        f.argtypes = args
+        f.restype = res
+    _lib = lib
+    return lib
+
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None else ctypes.c_void_p(0)
+
+
+def _stream():
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _check(fn, code):
+    if code != 0:
+        raise FqtError(fn, code)
+
+
+def _f32(x, name):
+    if not (x.is_cuda and x.dtype == torch.float32 and x.is_contiguous()):
+        raise ValueError(f"{name} must be a contiguous float32 CUDA tensor")
+    return x
+
+
+def _workspace(nbytes, device):
+    return torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=device)
+
+
+def cfg_struct(qb_x=("psq", 8, 0), qb_w=("ptq", 8, 0), f_bits=8, theta_bits=8, seed=0, trace=None):
+    return BwdCfg(QSpec(KINDS[qb_w[0]], int(qb_w[1]), int(qb_w[2])),
+                  QSpec(KINDS[qb_x[0]], int(qb_x[1]), int(qb_x[2])), int(f_bits), int(theta_bits), int(seed),
+                  ctypes.pointer(trace) if trace is not None else None)
+
+
+# ----------------------------------------------------------------------------
+# entry points (same names as the C ABI)
+# ----------------------------------------------------------------------------
+
+def fqt_quantize_workspace(kind, rows, cols, block_size=0):
+    return load().fqt_quantize_workspace(KINDS.get(kind, kind), rows, cols, block_size)
+
+
+def _quant_outputs(x, rows, cols, kind, transpose, code_sum):
+    dev = x.device
+    shape = (cols, rows) if transpose else (rows, cols)
+    n_scale = 1 if kind == "ptq" else rows
+    out = dict(q=torch.empty(shape, dtype=torch.int8, device=dev),
+               scale=torch.empty(n_scale, dtype=torch.float32, device=dev),
+               zero=torch.empty(n_scale, dtype=torch.float32, device=dev))
+    if kind == "bhq":
+        out["perm"] = torch.empty(rows, dtype=torch.int32, device=dev)
+        out["group_off"] = torch.empty(rows + 1, dtype=torch.int32, device=dev)
+    if code_sum:
+        out["code_sum"] = torch.empty(cols if transpose else rows, dtype=torch.int32, device=dev)
+    qt = QTensor(out["q"].data_ptr(), out["scale"].data_ptr(), out["zero"].data_ptr(),
+                 out["perm"].data_ptr() if "perm" in out else 0,
+                 out["group_off"].data_ptr() if "group_off" in out else 0,
+                 out["code_sum"].data_ptr() if "code_sum" in out else 0)
+    return out, qt
+
+
+def fqt_quantize_ptq(x, bits, stochastic, seed=0, stream=0, transpose=False, code_sum=False, ws=None):
+    x = _f32(x, "x")
+    rows, cols = x.shape
+    out, qt = _quant_outputs(x, rows, cols, "ptq", transpose, code_sum)
+    if ws is None:
+        ws = _workspace(fqt_quantize_workspace("ptq", rows, cols), x.device)
+    rc = load().fqt_quantize_ptq(_ptr(x), rows, cols, bits, int(bool(stochastic)), seed, stream,
+                                 int(bool(transpose)), ctypes.byref(qt), _ptr(ws), ws.numel(), _stream())
+    _check("fqt_quantize_ptq", rc)
+    out["ws"] = ws
+    return out
+
+
+def fqt_quantize_psq(x, bits, seed=0, stream=0, code_sum=False, ws=None):
+    x = _f32(x, "x")
+    rows, cols = x.shape
+    out, qt = _quant_outputs(x, rows, cols, "psq", False, code_sum)
+    if ws is None:
+        ws = _workspace(fqt_quantize_workspace("psq", rows, cols), x.device)
+    rc = load().fqt_quantize_psq(_ptr(x), rows, cols, bits, seed, stream, ctypes.byref(qt), _ptr(ws), ws.numel(),
+                                 _stream())
+    _check("fqt_quantize_psq", rc)
+    out["ws"] = ws
+    return out
+
+
+def fqt_quantize_bhq(x, bits, block_size, seed=0, stream=0, code_sum=False, ws=None):
+    x = _f32(x, "x")
+    rows, cols = x.shape
+    out, qt = _quant_outputs(x, rows, cols, "bhq", False, code_sum)
+    if ws is None:
+        ws = _workspace(fqt_quantize_workspace("bhq", rows, cols, block_size), x.device)
+    rc = load().fqt_quantize_bhq(_ptr(x), rows, cols, bits, block_size, seed, stream, ctypes.byref(qt), _ptr(ws),
+                                 ws.numel(), _stream())
+    _check("fqt_quantize_bhq", rc)
+    out["ws"] = ws
+    return out
+
+
+def fqt_linear_backward_workspace(N, d_in, d_out, cfg):
+    return load().fqt_linear_backward_workspace(N, d_in, d_out, ctypes.byref(cfg))
+
+
+def fqt_linear_backward(X, W, G, qb_x=("psq", 8, 0), qb_w=("ptq", 8, 0), f_bits=8, theta_bits=8, seed=0,
+                        grad_W=None, grad_X=None, ws=None, trace=None):
+    X, W, G = _f32(X, "X"), _f32(W, "W"), _f32(G, "G")
+    N, d_in = X.shape
+    d_out = W.shape[0]
+    if W.shape != (d_out, d_in) or G.shape != (N, d_out):
+        raise ValueError("shapes: X [N, d_in], W [d_out, d_in], G [N, d_out]")
+    cfg = cfg_struct(qb_x, qb_w, f_bits, theta_bits, seed, trace)
+    if grad_W is None:
+        grad_W = torch.empty((d_out, d_in), dtype=torch.float32, device=X.device)
+    if grad_X is None:
+        grad_X = torch.empty((N, d_in), dtype=torch.float32, device=X.device)
+    if ws is None:
+        ws = _workspace(fqt_linear_backward_workspace(N, d_in, d_out, cfg), X.device)
+    rc = load().fqt_linear_backward(_ptr(X), _ptr(W), _ptr(G), N, d_in, d_out, ctypes.byref(cfg), _ptr(grad_W),
+                                    _ptr(grad_X), _ptr(ws), ws.numel(), _stream())
+    _check("fqt_linear_backward", rc)
+    return grad_W, grad_X, ws
+
+
+def conv_shape(n, c, h, w, o, kh, kw, stride, pad):
+    ho = (h + 2 * pad - kh) // stride + 1
+    wo = (w + 2 * pad - kw) // stride + 1
+    return ConvShape(n, c, h, w, o, kh, kw, stride, pad, ho, wo)
+
+
+def fqt_conv_backward_workspace(shape, cfg):
+    return load().fqt_conv_backward_workspace(ctypes.byref(shape), ctypes.byref(cfg))
+
+
+def fqt_conv_backward_im2col(X, W, G, stride, pad, qb_x=("bhq", 5, 64), qb_w=("ptq", 8, 0), f_bits=8,
+                             theta_bits=8, seed=0, grad_W=None, grad_X=None, ws=None, trace=None):
+    X, W, G = _f32(X, "X"), _f32(W, "W"), _f32(G, "G")
+    n, h, w, c = X.shape
+    o, kh, kw, _ = W.shape
+    sh = conv_shape(n, c, h, w, o, kh, kw, stride, pad)
+    if tuple(G.shape) != (n, sh.ho, sh.wo, o) or W.shape[3] != c:
+        raise ValueError("shapes: X [n,h,w,c], W [o,kh,kw,c], G [n,ho,wo,o]")
+    cfg = cfg_struct(qb_x, qb_w, f_bits, theta_bits, seed, trace)
+    if grad_W is None:
+        grad_W = torch.empty(W.shape, dtype=torch.float32, device=X.device)
+    if grad_X is None:
+        grad_X = torch.empty(X.shape, dtype=torch.float32, device=X.device)
+    if ws is None:
+        ws = _workspace(fqt_conv_backward_workspace(sh, cfg), X.device)
+    rc = load().fqt_conv_backward_im2col(_ptr(X), _ptr(W), _ptr(G), ctypes.byref(sh), ctypes.byref(cfg),
+                                         _ptr(grad_W), _ptr(grad_X), _ptr(ws), ws.numel(), _stream())
+    _check("fqt_conv_backward_im2col", rc)
+    return grad_W, grad_X, ws
+
+
+def fqt_gemm_workspace(M, N, K):
+    return load().fqt_gemm_workspace(M, N, K)
+
+
+def fqt_gemm_s8s8_s64(A, B, ws=None):
+    """C [M, N] int64 = A [M, K] int8 . B [N, K]^T int8 (exact)."""
+    if not (A.is_cuda and B.is_cuda and A.dtype == torch.int8 and B.dtype == torch.int8):
+        raise ValueError("A, B must be int8 CUDA tensors")
+    M, K = A.shape
+    N = B.shape[0]
+    if B.shape[1] != K or A.stride(1) != 1 or B.stride(1) != 1:
+        raise ValueError("A [M, K], B [N, K], K contiguous")
+    C = torch.empty((M, N), dtype=torch.int64, device=A.device)
+    if ws is None:
+        ws = _workspace(fqt_gemm_workspace(M, N, K), A.device)
+    rc = load().fqt_gemm_s8s8_s64(_ptr(A), _ptr(B), M, N, K, A.stride(0), B.stride(0), _ptr(C), _ptr(ws),
+                                  ws.numel(), _stream())
+    _check("fqt_gemm_s8s8_s64", rc)
+    return C
+
+
+def fqt_workspace_status(ws):
+    return load().fqt_workspace_status(_ptr(ws), _stream())
+
+
+def fqt_version():
+    return load().fqt_version().decode()
+
+
+# ----------------------------------------------------------------------------
+# HIP events for fqt_trace (profiling only)
+# ----------------------------------------------------------------------------
+_hip = None
+
+
+def _hiprt():
+    global _hip
+    if _hip is None:
+        _hip = ctypes.CDLL("libamdhip64.so")
+        _hip.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        _hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
+        _hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+    return _hip
+
+
+def make_trace():
+    """A Trace with freshly created HIP events for every phase."""
+    hip = _hiprt()
+    t = Trace()
+    for i in range(TRACE_PHASES):
+        for arr in (t.start, t.stop):
+            ev = ctypes.c_void_p()
+            if hip.hipEventCreate(ctypes.byref(ev)) != 0:
+                raise RuntimeError("hipEventCreate failed")
+            arr[i] = ev
+    t.count = TRACE_PHASES
+    return t
+
+
+def trace_ms(t):
+    """Milliseconds of each phase of a completed traced call."""
+    hip = _hiprt()
+    out = []
+    for i in range(t.count):
+        ms = ctypes.c_float()
+        if hip.hipEventElapsedTime(ctypes.byref(ms), t.start[i], t.stop[i]) != 0:
+            raise RuntimeError("hipEventElapsedTime failed")
+        out.append(ms.value)
+    return out
+
+
+def free_trace(t):
+    hip = _hiprt()
+    for i in range(t.count):
+        hip.hipEventDestroy(t.start[i])
+        hip.hipEventDestroy(t.stop[i])

@@ -1,0 +1,81 @@
+"""Host-side checks of libfqt.so: it loads, exports every function include/fqt.h
+declares, sizes workspaces, and rejects bad arguments before any launch.
+No GPU work is started here: every call below returns during validation."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "fqt.h")
+LIB = os.path.join(ROOT, "paper_2010_14298_amd", "libfqt.so")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(LIB), reason="libfqt.so not built")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(fqt_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_header_declares_the_paper_entry_points():
+    names = declared_functions()
+    for n in ("fqt_quantize_ptq", "fqt_quantize_psq", "fqt_quantize_bhq", "fqt_linear_backward",
+              "fqt_conv_backward_im2col"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol():
+    lib = ctypes.CDLL(LIB)
+    missing = [n for n in declared_functions() if not hasattr(lib, n)]
+    assert not missing, missing
+
+
+def test_binding_exports_match_header():
+    from paper_2010_14298_amd import fqt
+    assert sorted(fqt.EXPORTS) == declared_functions()
+
+
+def test_workspace_queries_and_argument_errors():
+    from paper_2010_14298_amd import fqt
+    lib = fqt.load()
+    cfg = fqt.cfg_struct(qb_x=("bhq", 5, 64))
+    n = lib.fqt_linear_backward_workspace(8192, 1024, 4096, ctypes.byref(cfg))
+    # codes of X, W, G twice, plus stats and plan: at least the code bytes
+    assert n >= 8192 * 1024 + 1024 * 4096 + 2 * 8192 * 4096
+    assert lib.fqt_linear_backward_workspace(0, 1, 1, ctypes.byref(cfg)) == 0
+    assert lib.fqt_quantize_workspace(fqt.FQT_BHQ, 128, 10, 64) > lib.fqt_quantize_workspace(fqt.FQT_PTQ, 128, 10, 0)
+    null = ctypes.c_void_p(0)
+    fake = ctypes.c_void_p(0x1000)      # never dereferenced: validation fails first
+    # NULL inputs
+    rc = lib.fqt_linear_backward(null, fake, fake, 4, 4, 4, ctypes.byref(cfg), fake, fake, fake, 1 << 30, null)
+    assert rc == 1
+    # bits out of range
+    bad = fqt.cfg_struct(qb_x=("psq", 9, 0))
+    rc = lib.fqt_linear_backward(fake, fake, fake, 4, 4, 4, ctypes.byref(bad), fake, fake, fake, 1 << 30, null)
+    assert rc == 1
+    # grad_W quantizer other than PTQ is unsupported (per-row scales lie on its contraction axis)
+    unsup = fqt.cfg_struct(qb_w=("psq", 8, 0))
+    rc = lib.fqt_linear_backward(fake, fake, fake, 4, 4, 4, ctypes.byref(unsup), fake, fake, fake, 1 << 30, null)
+    assert rc == 2
+    # adaptive BHQ grouping (block size 0) is not built; block sizes must be powers of two <= 64
+    rc = lib.fqt_linear_backward(fake, fake, fake, 4, 4, 4, ctypes.byref(fqt.cfg_struct(qb_x=("bhq", 5, 0))),
+                                 fake, fake, fake, 1 << 30, null)
+    assert rc == 2
+    rc = lib.fqt_linear_backward(fake, fake, fake, 4, 4, 4, ctypes.byref(fqt.cfg_struct(qb_x=("bhq", 5, 48))),
+                                 fake, fake, fake, 1 << 30, null)
+    assert rc == 1
+    # workspace too small / missing
+    rc = lib.fqt_linear_backward(fake, fake, fake, 4, 4, 4, ctypes.byref(cfg), fake, fake, fake, 16, null)
+    assert rc == 4
+    rc = lib.fqt_linear_backward(fake, fake, fake, 4, 4, 4, ctypes.byref(cfg), fake, fake, null, 1 << 30, null)
+    assert rc == 4
+    # quantizer arguments
+    qt = fqt.QTensor(0x1000, 0x1000, 0x1000, 0, 0, 0)
+    assert lib.fqt_quantize_psq(fake, 0, 4, 8, 0, 0, ctypes.byref(qt), fake, 1 << 30, null) == 1
+    assert lib.fqt_quantize_psq(fake, 4, 4, 0, 0, 0, ctypes.byref(qt), fake, 1 << 30, null) == 1
+    assert lib.fqt_quantize_bhq(fake, 4, 4, 5, 64, 0, 0, ctypes.byref(qt), fake, 1 << 30, null) == 1   # no perm
+    assert lib.fqt_gemm_s8s8_s64(fake, fake, 4, 4, 8, 4, 8, fake, fake, 1 << 30, null) == 1            # lda < K
+    assert lib.fqt_status_str(3) == b"non-finite input or range overflow"
