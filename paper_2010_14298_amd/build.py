@@ -33,16 +33,30 @@ def hipcc():
     raise RuntimeError("hipcc not found: the FQT library needs ROCm's hipcc")
 
 
-def build(verbose=False):
-    srcs = sorted(glob.glob(os.path.join(HERE, "csrc", "*.hip")))
-    tmp = LIB + ".tmp"
-    cmd = [hipcc()] + HIP_FLAGS + ["-I", os.path.join(ROOT, "include")] + srcs + ["-o", tmp]
+def _run(cmd, verbose):
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         sys.stderr.write(res.stdout + res.stderr)
-        raise RuntimeError("libfqt.so build failed")
+        raise RuntimeError("libfqt.so build failed: " + " ".join(cmd[-3:]))
+
+
+def build(verbose=False):
+    """Compile every csrc/*.hip to an object in parallel, then link libfqt.so."""
+    from concurrent.futures import ThreadPoolExecutor
+    srcs = sorted(glob.glob(os.path.join(HERE, "csrc", "*.hip")))
+    objdir = os.path.join(HERE, "_build")
+    os.makedirs(objdir, exist_ok=True)
+    cc = hipcc()
+    inc = ["-I", os.path.join(ROOT, "include")]
+    objs = [os.path.join(objdir, os.path.basename(s)[:-4] + ".o") for s in srcs]
+    jobs = [[cc] + [f for f in HIP_FLAGS if f != "-shared"] + inc + ["-c", s, "-o", o] for s, o in zip(srcs, objs)]
+    workers = max(1, min(len(jobs), int(os.environ.get("MAX_JOBS", os.cpu_count() or 4))))
+    with ThreadPoolExecutor(workers) as ex:
+        list(ex.map(lambda c: _run(c, verbose), jobs))
+    tmp = LIB + ".tmp"
+    _run([cc, "-shared", "-fPIC", "--offload-arch=" + ARCH] + objs + ["-o", tmp], verbose)
     os.replace(tmp, LIB)
     return LIB
 

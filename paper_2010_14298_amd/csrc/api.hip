@@ -27,47 +27,11 @@ struct Carver {
   }
 };
 
-// Fixed header at the start of every workspace.
+// Fixed header at the start of every workspace: the status word.
 struct Header {
-  uint32_t* status;   // [1]
-  uint32_t* gminmax;  // [8]: X, W, G (min, max) + spare
+  uint32_t* status;
 };
-Header take_header(Carver& c) {
-  uint32_t* h = c.take<uint32_t>(64);
-  return Header{h, h ? h + 1 : nullptr};
-}
-
-struct FillSeg {
-  uint32_t* p;
-  int64_t n;
-  uint32_t v;
-};
-struct FillList {
-  FillSeg seg[8];
-  int count;
-};
-
-__global__ void fill_segments_kernel(FillList fl) {
-  for (int s = 0; s < fl.count; ++s) {
-    const FillSeg g = fl.seg[s];
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < g.n; i += (int64_t)gridDim.x * blockDim.x)
-      g.p[i] = g.v;
-  }
-}
-
-hipError_t fill_segments(const FillList& fl, hipStream_t s) {
-  int64_t total = 0;
-  for (int i = 0; i < fl.count; ++i) total += fl.seg[i].n;
-  int64_t blocks = (total + 255) / 256;
-  if (blocks < 1) blocks = 1;
-  if (blocks > 1024) blocks = 1024;
-  hipLaunchKernelGGL(fill_segments_kernel, dim3((unsigned)blocks), dim3(256), 0, s, fl);
-  return hipGetLastError();
-}
-
-void add_fill(FillList& fl, void* p, int64_t n, uint32_t v) {
-  if (p && n > 0) fl.seg[fl.count++] = FillSeg{static_cast<uint32_t*>(p), n, v};
-}
+Header take_header(Carver& c) { return Header{c.take<uint32_t>(64)}; }
 
 bool valid_bits(int b) { return b >= 1 && b <= 8; }
 
@@ -84,8 +48,6 @@ struct Tracer {
 };
 bool valid_block(int k) { return k >= 1 && k <= 64 && (k & (k - 1)) == 0; }
 
-fqt_status from_hip(hipError_t e) { return e == hipSuccess ? FQT_OK : FQT_EDEVICE; }
-
 #define FQT_TRY(expr)                              \
   do {                                             \
     const hipError_t e_ = (expr);                  \
@@ -97,20 +59,31 @@ fqt_status from_hip(hipError_t e) { return e == hipSuccess ? FQT_OK : FQT_EDEVIC
 // ---------------------------------------------------------------------------
 struct QuantWs {
   Header h;
-  uint32_t* rmin;
-  uint32_t* rmax;
+  StatsSeg seg;
+  float* rmin;
+  float* rmax;
   void* plan;
 };
 
-QuantWs carve_quant(Carver& c, fqt_kind kind, int64_t rows) {
+QuantWs carve_quant(Carver& c, fqt_kind kind, const float* x, int64_t rows, int64_t cols) {
   QuantWs w{};
   w.h = take_header(c);
+  w.seg = kind == FQT_PTQ ? stats_flat_seg(x, rows * cols) : stats_rows_seg(x, rows, cols);
+  w.seg.part = c.take<float2>(stats_partials(w.seg));
   if (kind != FQT_PTQ) {
-    w.rmin = c.take<uint32_t>(rows);
-    w.rmax = c.take<uint32_t>(rows);
+    w.rmin = c.take<float>(rows);
+    w.rmax = c.take<float>(rows);
   }
   if (kind == FQT_BHQ) w.plan = c.take<char>((int64_t)bhq_plan_workspace(rows));
   return w;
+}
+
+void add_zero(FinalizePlan& fp, int32_t* p, int64_t n) {
+  if (p && n > 0) {
+    fp.zero_i32[fp.nzero] = p;
+    fp.zero_n[fp.nzero] = n;
+    ++fp.nzero;
+  }
 }
 
 fqt_status check_quant_args(const float* x, int64_t rows, int64_t cols, int bits, const fqt_qtensor* out) {
@@ -131,19 +104,29 @@ fqt_status quantize_common(fqt_kind kind, const float* x, int64_t rows, int64_t 
   }
   if (!ws) return FQT_EWORKSPACE;
   Carver cs(nullptr);
-  carve_quant(cs, kind, rows);
+  carve_quant(cs, kind, x, rows, cols);
   if (ws_bytes < cs.off) return FQT_EWORKSPACE;
   Carver c(ws);
-  QuantWs w = carve_quant(c, kind, rows);
+  QuantWs w = carve_quant(c, kind, x, rows, cols);
 
-  FillList fl{};
-  add_fill(fl, w.h.status, 1, 0u);
-  add_fill(fl, w.h.gminmax, 1, ORD_POS_INF);
-  add_fill(fl, w.h.gminmax + 1, 1, ORD_NEG_INF);
-  add_fill(fl, w.rmin, rows, ORD_POS_INF);
-  add_fill(fl, w.rmax, rows, ORD_NEG_INF);
-  add_fill(fl, out->code_sum, transpose ? cols : rows, 0u);
-  FQT_TRY(fill_segments(fl, s));
+  StatsPlan sp{};
+  sp.seg[0] = w.seg;
+  sp.nseg = 1;
+  FQT_TRY(launch_stats(sp, s));
+  FinalizePlan fp{};
+  fp.seg[0] = w.seg;
+  fp.nseg = 1;
+  fp.row_seg = kind == FQT_PTQ ? -1 : 0;
+  fp.rmin = w.rmin;
+  fp.rmax = w.rmax;
+  fp.status = w.h.status;
+  if (kind != FQT_BHQ) {
+    fp.out[0] = ScaleOut{0, bits, kind == FQT_PSQ ? 1 : 0, out->scale, out->zero};
+    fp.nout = 1;
+  }
+  add_zero(fp, out->code_sum, transpose ? cols : rows);
+  if (kind == FQT_BHQ) add_zero(fp, bhq_plan_carve(w.plan, rows).rank, rows);
+  FQT_TRY(launch_finalize(fp, s));
 
   QuantParams p{};
   p.x = x;
@@ -163,21 +146,13 @@ fqt_status quantize_common(fqt_kind kind, const float* x, int64_t rows, int64_t 
     p.sum_nat = out->code_sum;
   }
   int mode = QM_TENSOR;
-  if (kind == FQT_PTQ) {
-    FQT_TRY(launch_stats_flat(x, rows * cols, w.h.gminmax, w.h.status, s));
-    FQT_TRY(launch_ptq_finalize(w.h.gminmax, bits, out->scale, out->zero, w.h.status, s));
-  } else {
-    FQT_TRY(launch_stats_rows(x, rows, cols, w.rmin, w.rmax, w.h.gminmax, w.h.status, s));
-    if (kind == FQT_PSQ) {
-      FQT_TRY(launch_psq_finalize(w.rmin, w.rmax, rows, bits, out->scale, out->zero, w.h.status, s));
-      mode = QM_ROW;
-    } else {
-      p.L = bhq_layout(rows, block_size);
-      FQT_TRY(launch_bhq_plan(w.rmin, w.rmax, p.L, bits, w.plan, out->perm, out->scale, out->zero, out->group_off,
-                              s));
-      p.perm = out->perm;
-      mode = QM_BHQ;
-    }
+  if (kind == FQT_PSQ) {
+    mode = QM_ROW;
+  } else if (kind == FQT_BHQ) {
+    p.L = bhq_layout(rows, block_size);
+    FQT_TRY(launch_bhq_plan(w.rmin, w.rmax, p.L, bits, w.plan, out->perm, out->scale, out->zero, out->group_off, s));
+    p.perm = out->perm;
+    mode = QM_BHQ;
   }
   FQT_TRY(launch_quant(p, mode, s));
   return FQT_OK;
@@ -188,7 +163,8 @@ fqt_status quantize_common(fqt_kind kind, const float* x, int64_t rows, int64_t 
 // ---------------------------------------------------------------------------
 struct LinearWs {
   Header h;
-  uint32_t *rmin, *rmax;
+  StatsSeg sx_seg, sw_seg, sg_seg;
+  float *rmin, *rmax;
   int8_t *qx_t, *qw_t, *qg1_t, *qg2;
   int32_t *sum_x, *sum_w, *sum_g1, *sum_g2;
   float *sx, *zx, *sw, *zw, *sg1, *zg1, *sg2, *zg2;
@@ -200,11 +176,18 @@ struct LinearWs {
 
 int linear_splits(int64_t N) { return (int)((N + MAX_K_CHUNK - 1) / MAX_K_CHUNK); }
 
-LinearWs carve_linear(Carver& c, int64_t N, int64_t d_in, int64_t d_out, const fqt_bwd_cfg& cfg) {
+LinearWs carve_linear(Carver& c, const float* X, const float* W, const float* G, int64_t N, int64_t d_in,
+                      int64_t d_out, const fqt_bwd_cfg& cfg) {
   LinearWs w{};
   w.h = take_header(c);
-  w.rmin = c.take<uint32_t>(N);
-  w.rmax = c.take<uint32_t>(N);
+  w.sx_seg = stats_flat_seg(X, N * d_in);
+  w.sw_seg = stats_flat_seg(W, d_out * d_in);
+  w.sg_seg = stats_rows_seg(G, N, d_out);
+  w.sx_seg.part = c.take<float2>(stats_partials(w.sx_seg));
+  w.sw_seg.part = c.take<float2>(stats_partials(w.sw_seg));
+  w.sg_seg.part = c.take<float2>(stats_partials(w.sg_seg));
+  w.rmin = c.take<float>(N);
+  w.rmax = c.take<float>(N);
   w.qx_t = c.take<int8_t>(d_in * N);
   w.qw_t = c.take<int8_t>(d_in * d_out);
   w.qg1_t = c.take<int8_t>(d_out * N);
@@ -270,18 +253,17 @@ fqt_status fqt_quantize_bhq(const float* x, int64_t rows, int64_t cols, int bits
 }
 
 size_t fqt_quantize_workspace(fqt_kind kind, int64_t rows, int64_t cols, int block_size) {
-  (void)cols;
   (void)block_size;
-  if (rows < 1) return 0;
+  if (rows < 1 || cols < 1) return 0;
   Carver c(nullptr);
-  carve_quant(c, kind, rows);
+  carve_quant(c, kind, nullptr, rows, cols);
   return c.off;
 }
 
 size_t fqt_linear_backward_workspace(int64_t N, int64_t d_in, int64_t d_out, const fqt_bwd_cfg* cfg) {
   if (!cfg || N < 1 || d_in < 1 || d_out < 1) return 0;
   Carver c(nullptr);
-  carve_linear(c, N, d_in, d_out, *cfg);
+  carve_linear(c, nullptr, nullptr, nullptr, N, d_in, d_out, *cfg);
   return c.off;
 }
 
@@ -296,50 +278,47 @@ fqt_status fqt_linear_backward(const float* X, const float* W, const float* G, i
   if (!ws) return FQT_EWORKSPACE;
   if (ws_bytes < fqt_linear_backward_workspace(N, d_in, d_out, cfg)) return FQT_EWORKSPACE;
   Carver c(ws);
-  LinearWs w = carve_linear(c, N, d_in, d_out, *cfg);
+  LinearWs w = carve_linear(c, X, W, G, N, d_in, d_out, *cfg);
   const fqt_qspec qx = cfg->qb_x;
   const bool bhq = qx.kind == FQT_BHQ;
-
   const Tracer tr{cfg->trace, s};
-  tr.begin(0);
-  FillList fl{};
-  add_fill(fl, w.h.status, 1, 0u);
-  add_fill(fl, w.h.gminmax, 8, ORD_POS_INF);
-  add_fill(fl, w.rmin, N, ORD_POS_INF);
-  add_fill(fl, w.rmax, N, ORD_NEG_INF);
-  add_fill(fl, w.sum_x, d_in, 0u);
-  add_fill(fl, w.sum_w, d_in, 0u);
-  add_fill(fl, w.sum_g1, d_out, 0u);
-  add_fill(fl, w.sum_g2, N, 0u);
-  FQT_TRY(fill_segments(fl, s));
-  // the max slots of gminmax start at -inf
-  FillList fm{};
-  add_fill(fm, w.h.gminmax + 1, 1, ORD_NEG_INF);
-  add_fill(fm, w.h.gminmax + 3, 1, ORD_NEG_INF);
-  add_fill(fm, w.h.gminmax + 5, 1, ORD_NEG_INF);
-  FQT_TRY(fill_segments(fm, s));
-  tr.end(0);
 
-  uint32_t* gX = w.h.gminmax;
-  uint32_t* gW = w.h.gminmax + 2;
-  uint32_t* gG = w.h.gminmax + 4;
+  // statistics of X, W (per tensor) and G (per row), one launch
+  tr.begin(0);
+  tr.end(0);
   tr.begin(1);
-  FQT_TRY(launch_stats_flat(X, N * d_in, gX, w.h.status, s));
-  FQT_TRY(launch_stats_flat(W, d_out * d_in, gW, w.h.status, s));
-  FQT_TRY(launch_stats_rows(G, N, d_out, w.rmin, w.rmax, gG, w.h.status, s));
+  StatsPlan sp{};
+  sp.seg[0] = w.sx_seg;
+  sp.seg[1] = w.sw_seg;
+  sp.seg[2] = w.sg_seg;
+  sp.nseg = 3;
+  FQT_TRY(launch_stats(sp, s));
   tr.end(1);
+  // scales: Q_f, Q_theta, Q_b1 per tensor; Q_b2 per tensor / per row / BHQ plan
   tr.begin(2);
-  FQT_TRY(launch_ptq_finalize(gX, cfg->f_bits, w.sx, w.zx, w.h.status, s));
-  FQT_TRY(launch_ptq_finalize(gW, cfg->theta_bits, w.sw, w.zw, w.h.status, s));
-  FQT_TRY(launch_ptq_finalize(gG, cfg->qb_w.bits, w.sg1, w.zg1, w.h.status, s));
+  FinalizePlan fp{};
+  fp.seg[0] = w.sx_seg;
+  fp.seg[1] = w.sw_seg;
+  fp.seg[2] = w.sg_seg;
+  fp.nseg = 3;
+  fp.row_seg = 2;
+  fp.rmin = w.rmin;
+  fp.rmax = w.rmax;
+  fp.status = w.h.status;
+  fp.out[0] = ScaleOut{0, cfg->f_bits, 0, w.sx, w.zx};
+  fp.out[1] = ScaleOut{1, cfg->theta_bits, 0, w.sw, w.zw};
+  fp.out[2] = ScaleOut{2, cfg->qb_w.bits, 0, w.sg1, w.zg1};
+  fp.nout = 3;
+  if (qx.kind != FQT_BHQ) fp.out[fp.nout++] = ScaleOut{2, qx.bits, qx.kind == FQT_PSQ ? 1 : 0, w.sg2, w.zg2};
+  add_zero(fp, w.sum_x, d_in);
+  add_zero(fp, w.sum_w, d_in);
+  add_zero(fp, w.sum_g1, d_out);
+  add_zero(fp, w.sum_g2, N);
+  if (bhq) add_zero(fp, bhq_plan_carve(w.plan, N).rank, N);
+  FQT_TRY(launch_finalize(fp, s));
   BhqLayout L{};
-  int mode = QM_TENSOR;
-  if (qx.kind == FQT_PTQ) {
-    FQT_TRY(launch_ptq_finalize(gG, qx.bits, w.sg2, w.zg2, w.h.status, s));
-  } else if (qx.kind == FQT_PSQ) {
-    FQT_TRY(launch_psq_finalize(w.rmin, w.rmax, N, qx.bits, w.sg2, w.zg2, w.h.status, s));
-    mode = QM_ROW;
-  } else {
+  int mode = qx.kind == FQT_PSQ ? QM_ROW : QM_TENSOR;
+  if (bhq) {
     L = bhq_layout(N, qx.block_size);
     FQT_TRY(launch_bhq_plan(w.rmin, w.rmax, L, qx.bits, w.plan, w.perm, w.sg2, w.zg2, nullptr, s));
     mode = QM_BHQ;

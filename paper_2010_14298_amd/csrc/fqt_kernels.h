@@ -9,22 +9,50 @@ namespace fqt {
 
 // ---- quantizer front end -------------------------------------------------
 
-hipError_t launch_fill_u32(uint32_t* p, uint32_t v, int64_t n, hipStream_t s);
+// Statistics: each block reduces one chunk of a flat tensor (rows = 1) or
+// of one row, into part[row * chunks + chunk] = (min, max); min is NaN when
+// the chunk holds a non-finite value.
+struct StatsSeg {
+  const float* x;
+  int64_t rows, cols;
+  int64_t chunk;   // columns per block
+  int64_t chunks;  // blocks per row
+  float2* part;
+};
+StatsSeg stats_flat_seg(const float* x, int64_t n);
+StatsSeg stats_rows_seg(const float* x, int64_t rows, int64_t cols);
+__host__ __device__ inline int64_t stats_partials(const StatsSeg& g) { return g.rows * g.chunks; }
+struct StatsPlan {
+  StatsSeg seg[3];
+  int nseg;
+  int64_t block_start[4];
+};
+hipError_t launch_stats(StatsPlan sp, hipStream_t s);
 
-// Global min / max (order-encoded) of a flat tensor; sets STATUS_NONFINITE.
-hipError_t launch_stats_flat(const float* x, int64_t n, uint32_t* gminmax, uint32_t* status, hipStream_t s);
-
-// Per-row min / max (order-encoded) plus the global min / max.
-hipError_t launch_stats_rows(const float* x, int64_t rows, int64_t cols, uint32_t* rmin, uint32_t* rmax,
-                             uint32_t* gminmax, uint32_t* status, hipStream_t s);
-
-// Per-tensor scale and zero point from a global min / max (Sec. 3.3).
-hipError_t launch_ptq_finalize(const uint32_t* gminmax, int bits, float* scale, float* zero, uint32_t* status,
-                               hipStream_t s);
-
-// Per-row scale and zero point (Sec. 4.1).
-hipError_t launch_psq_finalize(const uint32_t* rmin, const uint32_t* rmax, int64_t rows, int bits, float* scale,
-                               float* zero, uint32_t* status, hipStream_t s);
+// One finalize block: per-tensor PTQ scale / zero (Sec. 3.3), per-row PSQ
+// scale / zero (Sec. 4.1), per-row min / max of the row segment, cleared
+// int32 arrays and the status word.
+struct ScaleOut {
+  int seg;
+  int bits;
+  int per_row;
+  float* scale;
+  float* zero;
+};
+struct FinalizePlan {
+  StatsSeg seg[3];
+  int nseg;
+  int row_seg;       // index of the per-row segment, -1 if none
+  float* rmin;       // [rows] of the row segment
+  float* rmax;
+  ScaleOut out[4];
+  int nout;
+  int32_t* zero_i32[6];
+  int64_t zero_n[6];
+  int nzero;
+  uint32_t* status;
+};
+hipError_t launch_finalize(const FinalizePlan& fp, hipStream_t s);
 
 // Fixed-block BHQ layout, all data independent (see bhq_layout()).
 struct BhqLayout {
@@ -49,9 +77,16 @@ __device__ __forceinline__ int bhq_slot_kind(const BhqLayout& L, int64_t slot) {
   return 0;
 }
 
-// Workspace for the BHQ plan: keys, sorted chunks, rank, sigma.
+// Workspace for the BHQ plan: sorted chunk keys, rank (must be zero before
+// the plan runs), sigma = rows in sorted order.
 size_t bhq_plan_workspace(int64_t rows);
-hipError_t launch_bhq_plan(const uint32_t* rmin, const uint32_t* rmax, const BhqLayout& L, int bits, void* plan_ws,
+struct BhqPlanWs {
+  uint64_t* sorted;
+  int32_t* rank;
+  int32_t* sigma;
+};
+BhqPlanWs bhq_plan_carve(void* plan_ws, int64_t rows);
+hipError_t launch_bhq_plan(const float* rmin, const float* rmax, const BhqLayout& L, int bits, void* plan_ws,
                            int32_t* perm, float* scale, float* zero, int32_t* group_off, hipStream_t s);
 
 struct QuantParams {

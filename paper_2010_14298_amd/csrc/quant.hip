@@ -19,21 +19,8 @@
 namespace fqt {
 
 // ---------------------------------------------------------------------------
-// small utilities
+// reductions
 // ---------------------------------------------------------------------------
-__global__ void fill_u32_kernel(uint32_t* p, uint32_t v, int64_t n) {
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
-    p[i] = v;
-}
-
-hipError_t launch_fill_u32(uint32_t* p, uint32_t v, int64_t n, hipStream_t s) {
-  if (n <= 0) return hipSuccess;
-  int64_t blocks = (n + 255) / 256;
-  if (blocks > 4096) blocks = 4096;
-  hipLaunchKernelGGL(fill_u32_kernel, dim3((unsigned)blocks), dim3(256), 0, s, p, v, n);
-  return hipGetLastError();
-}
-
 __device__ __forceinline__ float wave_min(float v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v = fminf(v, __shfl_xor(v, o));
@@ -50,86 +37,53 @@ __device__ __forceinline__ int wave_sum_i(int v) {
   return v;
 }
 
-// Block-wide min / max / non-finite flag; thread 0 publishes by atomics.
-__device__ __forceinline__ void block_publish(float mn, float mx, bool bad, uint32_t* amin, uint32_t* amax,
-                                              uint32_t* gminmax, uint32_t* status) {
-  __shared__ float smn[16], smx[16];
-  __shared__ int sbad;
-  if (threadIdx.x == 0) sbad = 0;
-  __syncthreads();
+// Block-wide (min, max, any-bad); every thread gets the result.
+struct MinMax {
+  float mn, mx;
+  int bad;
+};
+template <int NW>
+__device__ __forceinline__ MinMax block_minmax(float mn, float mx, int bad) {
+  __shared__ float smn[NW], smx[NW];
+  __shared__ int sbad[NW];
   mn = wave_min(mn);
   mx = wave_max(mx);
+  bad = __any(bad) ? 1 : 0;
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  if (bad) atomicOr(&sbad, 1);
+  __syncthreads();
   if (lane == 0) {
     smn[w] = mn;
     smx[w] = mx;
+    sbad[w] = bad;
   }
   __syncthreads();
-  if (threadIdx.x == 0) {
-    const int nw = (blockDim.x + 63) >> 6;
-    for (int i = 1; i < nw; ++i) {
-      mn = fminf(mn, smn[i]);
-      mx = fmaxf(mx, smx[i]);
-    }
-    if (amin) atomicMin(amin, f2ord(mn));
-    if (amax) atomicMax(amax, f2ord(mx));
-    if (gminmax) {
-      atomicMin(gminmax + 0, f2ord(mn));
-      atomicMax(gminmax + 1, f2ord(mx));
-    }
-    if (sbad) atomicOr(status, STATUS_NONFINITE);
+  MinMax r{smn[0], smx[0], sbad[0]};
+  for (int i = 1; i < NW; ++i) {
+    r.mn = fminf(r.mn, smn[i]);
+    r.mx = fmaxf(r.mx, smx[i]);
+    r.bad |= sbad[i];
   }
+  return r;
 }
 
 // ---------------------------------------------------------------------------
-// stats
+// stats: one launch over up to three tensors.  Every block reduces its chunk
+// (a piece of a flat tensor, or a piece of one row) and stores the partial
+// (min, max); a non-finite element turns the partial's min into NaN.  No
+// atomics: the finalize block combines the partials.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void stats_flat_kernel(const float* __restrict__ x, int64_t n,
-                                                         uint32_t* gminmax, uint32_t* status) {
+__global__ __launch_bounds__(256) void stats_kernel(StatsPlan sp) {
+  int si = 0;
+  while (si + 1 < sp.nseg && (int64_t)blockIdx.x >= sp.block_start[si + 1]) ++si;
+  const StatsSeg g = sp.seg[si];
+  const int64_t b = (int64_t)blockIdx.x - sp.block_start[si];
+  const int64_t row = b / g.chunks;
+  const int64_t c_begin = (b % g.chunks) * g.chunk;
+  const int64_t c_end = (c_begin + g.chunk < g.cols) ? c_begin + g.chunk : g.cols;
+  const float* xr = g.x + row * g.cols;
   float mn = INFINITY, mx = -INFINITY;
-  bool bad = false;
-  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  const int64_t tid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if ((n & 3) == 0 && ((uintptr_t)x & 15) == 0) {
-    const float4* x4 = reinterpret_cast<const float4*>(x);
-    for (int64_t i = tid; i < (n >> 2); i += stride) {
-      const float4 v = x4[i];
-      mn = fminf(fminf(mn, v.x), fminf(v.y, fminf(v.z, v.w)));
-      mx = fmaxf(fmaxf(mx, v.x), fmaxf(v.y, fmaxf(v.z, v.w)));
-      bad |= !(isfinite(v.x) && isfinite(v.y) && isfinite(v.z) && isfinite(v.w));
-    }
-  } else {
-    for (int64_t i = tid; i < n; i += stride) {
-      const float v = x[i];
-      mn = fminf(mn, v);
-      mx = fmaxf(mx, v);
-      bad |= !isfinite(v);
-    }
-  }
-  block_publish(mn, mx, bad, nullptr, nullptr, gminmax, status);
-}
-
-hipError_t launch_stats_flat(const float* x, int64_t n, uint32_t* gminmax, uint32_t* status, hipStream_t s) {
-  int64_t blocks = (n / 4 + 255) / 256;
-  if (blocks < 1) blocks = 1;
-  if (blocks > 2048) blocks = 2048;
-  hipLaunchKernelGGL(stats_flat_kernel, dim3((unsigned)blocks), dim3(256), 0, s, x, n, gminmax, status);
-  return hipGetLastError();
-}
-
-constexpr int64_t STATS_CHUNK = 8192;  // columns per block of stats_rows
-
-__global__ __launch_bounds__(256) void stats_rows_kernel(const float* __restrict__ x, int64_t rows, int64_t cols,
-                                                         uint32_t* rmin, uint32_t* rmax, uint32_t* gminmax,
-                                                         uint32_t* status) {
-  const int64_t row = blockIdx.x;
-  const int64_t c_begin = (int64_t)blockIdx.y * STATS_CHUNK;
-  const int64_t c_end = (c_begin + STATS_CHUNK < cols) ? c_begin + STATS_CHUNK : cols;
-  const float* xr = x + row * cols;
-  float mn = INFINITY, mx = -INFINITY;
-  bool bad = false;
-  if ((cols & 3) == 0 && ((uintptr_t)x & 15) == 0) {
+  int bad = 0;
+  if ((g.cols & 3) == 0 && ((uintptr_t)g.x & 15) == 0) {
     const float4* x4 = reinterpret_cast<const float4*>(xr);
     for (int64_t i = (c_begin >> 2) + threadIdx.x; i < (c_end >> 2); i += blockDim.x) {
       const float4 v = x4[i];
@@ -145,51 +99,113 @@ __global__ __launch_bounds__(256) void stats_rows_kernel(const float* __restrict
       bad |= !isfinite(v);
     }
   }
-  block_publish(mn, mx, bad, rmin + row, rmax + row, gminmax, status);
+  const MinMax r = block_minmax<4>(mn, mx, bad);
+  if (threadIdx.x == 0) g.part[b] = make_float2(r.bad ? NAN : r.mn, r.mx);
 }
 
-hipError_t launch_stats_rows(const float* x, int64_t rows, int64_t cols, uint32_t* rmin, uint32_t* rmax,
-                             uint32_t* gminmax, uint32_t* status, hipStream_t s) {
-  const int64_t chunks = (cols + STATS_CHUNK - 1) / STATS_CHUNK;
-  if (rows > 0x7FFFFFFF || chunks > 65535) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(stats_rows_kernel, dim3((unsigned)rows, (unsigned)chunks), dim3(256), 0, s, x, rows, cols,
-                     rmin, rmax, gminmax, status);
+StatsSeg stats_flat_seg(const float* x, int64_t n) {
+  StatsSeg g{};
+  g.x = x;
+  g.rows = 1;
+  g.cols = n;
+  g.chunk = 16384;
+  g.chunks = (n + g.chunk - 1) / g.chunk;
+  return g;
+}
+
+StatsSeg stats_rows_seg(const float* x, int64_t rows, int64_t cols) {
+  StatsSeg g{};
+  g.x = x;
+  g.rows = rows;
+  g.cols = cols;
+  g.chunk = 8192;
+  g.chunks = (cols + g.chunk - 1) / g.chunk;
+  return g;
+}
+
+
+hipError_t launch_stats(StatsPlan sp, hipStream_t s) {
+  int64_t total = 0;
+  for (int i = 0; i < sp.nseg; ++i) {
+    sp.block_start[i] = total;
+    total += stats_partials(sp.seg[i]);
+  }
+  sp.block_start[sp.nseg] = total;
+  if (total > 0x7FFFFFFF) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(stats_kernel, dim3((unsigned)total), dim3(256), 0, s, sp);
   return hipGetLastError();
 }
 
 // ---------------------------------------------------------------------------
-// finalize: PTQ and PSQ scalars
+// finalize: one 1024-thread block.  Combines the partials into per-tensor and
+// per-row ranges, writes the PTQ scale / zero (Sec. 3.3) and PSQ per-row
+// scales / zeros (Sec. 4.1), clears the code-sum and rank arrays, and sets
+// the status word (non-finite input, or a range beyond float32).
 // ---------------------------------------------------------------------------
-__global__ void ptq_finalize_kernel(const uint32_t* gminmax, int B, float* scale, float* zero, uint32_t* status) {
-  const float z = ord2f(gminmax[0]);
-  const float mx = ord2f(gminmax[1]);
-  const float R = mx - z;
-  if (!isfinite(R)) atomicOr(status, STATUS_NONFINITE);
-  scale[0] = scale_from_range(R, B);
-  zero[0] = z;
+__global__ __launch_bounds__(1024) void finalize_kernel(FinalizePlan fp) {
+  const int t = threadIdx.x;
+  for (int z = 0; z < fp.nzero; ++z)
+    for (int64_t i = t; i < fp.zero_n[z]; i += blockDim.x) fp.zero_i32[z][i] = 0;
+  __shared__ float seg_mn[3], seg_mx[3];
+  __shared__ int seg_bad[3];
+  for (int si = 0; si < fp.nseg; ++si) {
+    const StatsSeg& g = fp.seg[si];
+    float mn = INFINITY, mx = -INFINITY;
+    int bad = 0;
+    if (si == fp.row_seg) {
+      for (int64_t r = t; r < g.rows; r += blockDim.x) {
+        float rmn = INFINITY, rmx = -INFINITY;
+        for (int64_t c = 0; c < g.chunks; ++c) {
+          const float2 p = g.part[r * g.chunks + c];
+          if (isnan(p.x)) bad = 1;
+          rmn = fminf(rmn, p.x);
+          rmx = fmaxf(rmx, p.y);
+        }
+        fp.rmin[r] = rmn;
+        fp.rmax[r] = rmx;
+        if (!isfinite(rmx - rmn)) bad = 1;
+        mn = fminf(mn, rmn);
+        mx = fmaxf(mx, rmx);
+      }
+    } else {
+      for (int64_t i = t; i < stats_partials(g); i += blockDim.x) {
+        const float2 p = g.part[i];
+        if (isnan(p.x)) bad = 1;
+        mn = fminf(mn, p.x);
+        mx = fmaxf(mx, p.y);
+      }
+    }
+    const MinMax r = block_minmax<16>(mn, mx, bad);
+    if (t == 0) {
+      seg_mn[si] = r.mn;
+      seg_mx[si] = r.mx;
+      seg_bad[si] = r.bad || !isfinite(r.mx - r.mn);
+    }
+  }
+  __syncthreads();
+  for (int o = 0; o < fp.nout; ++o) {
+    const ScaleOut& so = fp.out[o];
+    const int B = (1 << so.bits) - 1;
+    if (so.per_row) {
+      const int64_t rows = fp.seg[so.seg].rows;
+      for (int64_t r = t; r < rows; r += blockDim.x) {
+        so.scale[r] = scale_from_range(fp.rmax[r] - fp.rmin[r], B);
+        so.zero[r] = fp.rmin[r];
+      }
+    } else if (t == 0) {
+      so.scale[0] = scale_from_range(seg_mx[so.seg] - seg_mn[so.seg], B);
+      so.zero[0] = seg_mn[so.seg];
+    }
+  }
+  if (t == 0) {
+    int bad = 0;
+    for (int si = 0; si < fp.nseg; ++si) bad |= seg_bad[si];
+    *fp.status = bad ? STATUS_NONFINITE : 0u;
+  }
 }
 
-hipError_t launch_ptq_finalize(const uint32_t* gminmax, int bits, float* scale, float* zero, uint32_t* status,
-                               hipStream_t s) {
-  hipLaunchKernelGGL(ptq_finalize_kernel, dim3(1), dim3(1), 0, s, gminmax, (1 << bits) - 1, scale, zero, status);
-  return hipGetLastError();
-}
-
-__global__ void psq_finalize_kernel(const uint32_t* rmin, const uint32_t* rmax, int64_t rows, int B, float* scale,
-                                    float* zero, uint32_t* status) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= rows) return;
-  const float z = ord2f(rmin[i]);
-  const float R = ord2f(rmax[i]) - z;
-  if (!isfinite(R)) atomicOr(status, STATUS_NONFINITE);
-  scale[i] = scale_from_range(R, B);
-  zero[i] = z;
-}
-
-hipError_t launch_psq_finalize(const uint32_t* rmin, const uint32_t* rmax, int64_t rows, int bits, float* scale,
-                               float* zero, uint32_t* status, hipStream_t s) {
-  hipLaunchKernelGGL(psq_finalize_kernel, dim3((unsigned)((rows + 255) / 256)), dim3(256), 0, s, rmin, rmax, rows,
-                     (1 << bits) - 1, scale, zero, status);
+hipError_t launch_finalize(const FinalizePlan& fp, hipStream_t s) {
+  hipLaunchKernelGGL(finalize_kernel, dim3(1), dim3(1024), 0, s, fp);
   return hipGetLastError();
 }
 
@@ -230,31 +246,25 @@ static int64_t sort_pad(int64_t rows) { return (rows + SORT_CH - 1) / SORT_CH * 
 
 size_t bhq_plan_workspace(int64_t rows) {
   const int64_t np = sort_pad(rows);
-  // keys, sorted chunks (uint64 each), rank and sigma (int32 each)
-  return (size_t)np * 8 * 2 + (size_t)rows * 4 * 2 + 256;
+  // sorted chunk keys (uint64), rank and sigma (int32 each)
+  return (size_t)np * 8 + (size_t)rows * 4 * 2 + 256;
 }
 
 // key = (~bits(M_i) << 32) | i: ascending order = M descending, index ascending.
-__global__ void bhq_keys_kernel(const uint32_t* rmin, const uint32_t* rmax, int64_t rows, int64_t npad,
-                                uint64_t* keys, int32_t* rank) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= npad) return;
-  if (i < rows) {
-    const float M = fmaxf(fabsf(ord2f(rmin[i])), fabsf(ord2f(rmax[i])));
-    keys[i] = ((uint64_t)(~__float_as_uint(M)) << 32) | (uint64_t)(uint32_t)i;
-    rank[i] = 0;
-  } else {
-    keys[i] = ~0ull;
-  }
+__device__ __forceinline__ uint64_t bhq_key(const float* rmin, const float* rmax, int64_t rows, int64_t i) {
+  if (i >= rows) return ~0ull;
+  const float M = fmaxf(fabsf(rmin[i]), fabsf(rmax[i]));
+  return ((uint64_t)(~__float_as_uint(M)) << 32) | (uint64_t)(uint32_t)i;
 }
 
-// Bitonic sort of one 1024-key chunk in LDS.
-__global__ __launch_bounds__(512) void bhq_sort_chunks_kernel(const uint64_t* keys, uint64_t* sorted) {
+// Keys of one 1024-row chunk, bitonic-sorted in LDS.
+__global__ __launch_bounds__(512) void bhq_sort_chunks_kernel(const float* rmin, const float* rmax, int64_t rows,
+                                                              uint64_t* sorted) {
   __shared__ uint64_t sk[SORT_CH];
   const int t = threadIdx.x;
   const int64_t base = (int64_t)blockIdx.x * SORT_CH;
-  sk[t] = keys[base + t];
-  sk[t + 512] = keys[base + t + 512];
+  sk[t] = bhq_key(rmin, rmax, rows, base + t);
+  sk[t + 512] = bhq_key(rmin, rmax, rows, base + t + 512);
   for (int size = 2; size <= SORT_CH; size <<= 1) {
     for (int stride = size >> 1; stride > 0; stride >>= 1) {
       __syncthreads();
@@ -346,11 +356,13 @@ __device__ __forceinline__ float to_f32_sat(double v) {
   return (f > FLT_MAX_F) ? FLT_MAX_F : f;
 }
 
-// One thread per group: perm, per-slot scale d_p and zero (c_g or row min).
-__global__ void bhq_groups_kernel(const uint32_t* rmin, const uint32_t* rmax, const int32_t* sigma, BhqLayout L,
-                                  int B, int32_t* perm, float* scale, float* zero, int32_t* group_off) {
-  const int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (g >= L.G) return;
+// One wave per group: perm, per-slot scale d_p and zero (c_g, or the row min
+// for a one-row group).  Lane j handles the group's slot j + 1.
+__global__ __launch_bounds__(64) void bhq_groups_kernel(const float* rmin, const float* rmax, const int32_t* sigma,
+                                                        BhqLayout L, int B, int32_t* perm, float* scale, float* zero,
+                                                        int32_t* group_off) {
+  const int64_t g = blockIdx.x;
+  const int lane = threadIdx.x;
   const int k = L.k;
   int kg;
   int64_t base;
@@ -364,27 +376,29 @@ __global__ void bhq_groups_kernel(const uint32_t* rmin, const uint32_t* rmax, co
     kg = 1;
     base = L.full * k + L.part + (g - L.full - (L.part > 0 ? 1 : 0));
   }
-  if (group_off) {
+  if (group_off && lane == 0) {
     group_off[g] = (int32_t)base;
     if (g == L.G - 1) group_off[L.G] = (int32_t)L.rows;
   }
   const int32_t big = sigma[g];
-  perm[base] = big;
-  const float mn0 = ord2f(rmin[big]);
-  const float mx0 = ord2f(rmax[big]);
+  const float mn0 = rmin[big];
+  const float mx0 = rmax[big];
   if (kg == 1) {
-    scale[base] = scale_from_range(mx0 - mn0, B);
-    zero[base] = mn0;
+    if (lane == 0) {
+      perm[base] = big;
+      scale[base] = scale_from_range(mx0 - mn0, B);
+      zero[base] = mn0;
+    }
     return;
   }
   const int64_t tail = L.G + g * (int64_t)(k - 1);
-  float m2 = 0.0f;
-  for (int j = 0; j < kg - 1; ++j) {
-    const int32_t r = sigma[tail + j];
-    perm[base + 1 + j] = r;
-    const float M = fmaxf(fabsf(ord2f(rmin[r])), fabsf(ord2f(rmax[r])));
-    m2 = fmaxf(m2, M);
+  int32_t r = -1;
+  float M = 0.0f;
+  if (lane < kg - 1) {
+    r = sigma[tail + lane];
+    M = fmaxf(fabsf(rmin[r]), fabsf(rmax[r]));
   }
+  const float m2 = wave_max(M);
   float lam1 = mx0 - mn0;
   const float lam2 = 2.0f * m2;
   if (lam1 == 0.0f) lam1 = lam2;
@@ -409,31 +423,41 @@ __global__ void bhq_groups_kernel(const uint32_t* rmin, const uint32_t* rmax, co
   const double t1 = ((double)alpha * (double)s1) * (double)mn0;
   const double t2 = ((0.5 * (double)lam2) * (double)s2) * sk;
   const float cg = (float)(t1 - t2);
-  scale[base] = s1;
-  zero[base] = cg;
-  for (int j = 1; j < kg; ++j) {
-    scale[base + j] = s2;
-    zero[base + j] = cg;
+  if (lane == 0) {
+    perm[base] = big;
+    scale[base] = s1;
+    zero[base] = cg;
+  }
+  if (lane < kg - 1) {
+    perm[base + 1 + lane] = r;
+    scale[base + 1 + lane] = s2;
+    zero[base + 1 + lane] = cg;
   }
 }
 
-hipError_t launch_bhq_plan(const uint32_t* rmin, const uint32_t* rmax, const BhqLayout& L, int bits, void* plan_ws,
+BhqPlanWs bhq_plan_carve(void* plan_ws, int64_t rows) {
+  const int64_t np = sort_pad(rows);
+  char* w = static_cast<char*>(plan_ws);
+  BhqPlanWs p{};
+  p.sorted = reinterpret_cast<uint64_t*>(w);
+  p.rank = reinterpret_cast<int32_t*>(p.sorted + np);
+  p.sigma = p.rank + rows;
+  return p;
+}
+
+hipError_t launch_bhq_plan(const float* rmin, const float* rmax, const BhqLayout& L, int bits, void* plan_ws,
                            int32_t* perm, float* scale, float* zero, int32_t* group_off, hipStream_t s) {
   const int64_t rows = L.rows;
   const int64_t np = sort_pad(rows);
   const int64_t nch = np / SORT_CH;
-  if (nch > 65535) return hipErrorInvalidValue;
-  char* w = static_cast<char*>(plan_ws);
-  uint64_t* keys = reinterpret_cast<uint64_t*>(w);
-  uint64_t* sorted = keys + np;
-  int32_t* rank = reinterpret_cast<int32_t*>(sorted + np);
-  int32_t* sigma = rank + rows;
-  hipLaunchKernelGGL(bhq_keys_kernel, dim3((unsigned)((np + 255) / 256)), dim3(256), 0, s, rmin, rmax, rows, np, keys,
-                     rank);
-  hipLaunchKernelGGL(bhq_sort_chunks_kernel, dim3((unsigned)nch), dim3(512), 0, s, keys, sorted);
-  hipLaunchKernelGGL(bhq_rank_kernel, dim3((unsigned)nch, (unsigned)nch), dim3(256), 0, s, sorted, rank);
-  hipLaunchKernelGGL(bhq_scatter_kernel, dim3((unsigned)((rows + 255) / 256)), dim3(256), 0, s, rank, rows, sigma);
-  hipLaunchKernelGGL(bhq_groups_kernel, dim3((unsigned)((L.G + 63) / 64)), dim3(64), 0, s, rmin, rmax, sigma, L,
+  if (nch > 65535 || L.G > 0x7FFFFFFF) return hipErrorInvalidValue;
+  const BhqPlanWs w = bhq_plan_carve(plan_ws, rows);
+  // w.rank must be zero here (the finalize kernel clears it)
+  hipLaunchKernelGGL(bhq_sort_chunks_kernel, dim3((unsigned)nch), dim3(512), 0, s, rmin, rmax, rows, w.sorted);
+  hipLaunchKernelGGL(bhq_rank_kernel, dim3((unsigned)nch, (unsigned)nch), dim3(256), 0, s, w.sorted, w.rank);
+  hipLaunchKernelGGL(bhq_scatter_kernel, dim3((unsigned)((rows + 255) / 256)), dim3(256), 0, s, w.rank, rows,
+                     w.sigma);
+  hipLaunchKernelGGL(bhq_groups_kernel, dim3((unsigned)L.G), dim3(64), 0, s, rmin, rmax, w.sigma, L,
                      (1 << bits) - 1, perm, scale, zero, group_off);
   return hipGetLastError();
 }
