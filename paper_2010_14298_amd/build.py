@@ -21,6 +21,7 @@ HIP_FLAGS = [
     "-O3", "-std=c++17", "-fPIC", "-shared",
     "--offload-arch=" + ARCH,
     "-ffp-contract=off",
+    "-mllvm", "-disable-promote-alloca-to-lds",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-Wall", "-Wno-unused-function",
 ]

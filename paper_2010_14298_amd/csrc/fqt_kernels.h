@@ -128,7 +128,7 @@ struct GemmParams {
   const int8_t* A;  // [M, K] row stride lda
   const int8_t* B;  // [N, K] row stride ldb
   int64_t M, N, K, lda, ldb;
-  int64_t kchunk;   // K per split (multiple of 64, <= 65536)
+  int64_t kchunk;   // K per split (multiple of 128 when split, <= 65536)
   int splits;
   int32_t* part;    // EPI_RAW_I32 output [splits][M][N]
   // epilogue data (float64 arithmetic, float32 result)
