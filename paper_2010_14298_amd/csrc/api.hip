@@ -228,6 +228,99 @@ fqt_status check_cfg(const fqt_bwd_cfg* cfg) {
   return FQT_OK;
 }
 
+// ---------------------------------------------------------------------------
+// conv backward
+// ---------------------------------------------------------------------------
+fqt_status check_conv_shape(const fqt_conv_shape& sh) {
+  if (sh.n < 1 || sh.c < 1 || sh.h < 1 || sh.w < 1 || sh.o < 1 || sh.kh < 1 || sh.kw < 1 || sh.stride < 1 ||
+      sh.pad < 0)
+    return FQT_EINVAL;
+  if (sh.ho != (sh.h + 2 * sh.pad - sh.kh) / sh.stride + 1 || sh.wo != (sh.w + 2 * sh.pad - sh.kw) / sh.stride + 1 ||
+      sh.ho < 1 || sh.wo < 1)
+    return FQT_EINVAL;
+  // 16-channel gathers of the gradient codes; row / tap counts within grid limits
+  if (sh.o % 16 != 0 || (int64_t)sh.kh * sh.kw * sh.c > 65535 || sh.n > MAX_ROWS) return FQT_EUNSUPPORTED;
+  const int64_t P = (int64_t)sh.n * sh.ho * sh.wo;
+  if (P > 0x7FFFFFFF / 2 || (int64_t)sh.n * sh.h * sh.w > 0x7FFFFFFF / 2) return FQT_EUNSUPPORTED;
+  return FQT_OK;
+}
+
+ConvGeom conv_geom(const fqt_conv_shape& sh) {
+  ConvGeom g{sh.n, sh.c, sh.h, sh.w, sh.o, sh.kh, sh.kw, sh.stride, sh.pad, sh.ho, sh.wo, 0};
+  g.npad = ((int64_t)sh.n + 63) / 64 * 64;
+  return g;
+}
+
+struct ConvWs {
+  Header h;
+  StatsSeg sx_seg, sw_seg, sg_seg;
+  float *rmin, *rmax;
+  int8_t *xq_t, *wq_t, *q2, *q1_t, *bw;
+  int32_t *swq, *sumB, *qs, *sumA_tap, *count_tap, *sg, *ct, *cnt;
+  float *sx, *zx, *sw, *zw, *sg1, *zg1, *sg2, *zg2;
+  int32_t* perm;
+  void* plan;
+  int32_t* part;
+  int64_t ldq, kchunk;
+  int splits;
+};
+
+ConvWs carve_conv(Carver& c, const float* X, const float* W, const float* G, const ConvGeom& g,
+                  const fqt_bwd_cfg& cfg) {
+  ConvWs w{};
+  const int64_t N = g.n, hw = (int64_t)g.h * g.w, howo = (int64_t)g.ho * g.wo;
+  const int64_t taps = (int64_t)g.kh * g.kw;
+  const int64_t P = N * howo;
+  w.h = take_header(c);
+  w.sx_seg = stats_flat_seg(X, N * hw * g.c);
+  w.sw_seg = stats_flat_seg(W, (int64_t)g.o * taps * g.c);
+  w.sg_seg = stats_rows_seg(G, N, howo * g.o);
+  w.sx_seg.part = c.take<float2>(stats_partials(w.sx_seg));
+  w.sw_seg.part = c.take<float2>(stats_partials(w.sw_seg));
+  w.sg_seg.part = c.take<float2>(stats_partials(w.sg_seg));
+  w.rmin = c.take<float>(N);
+  w.rmax = c.take<float>(N);
+  w.ldq = (P + 127) / 128 * 128;
+  w.xq_t = c.take<int8_t>((int64_t)g.c * N * hw);
+  w.wq_t = c.take<int8_t>((int64_t)g.c * taps * g.o);
+  w.q2 = c.take<int8_t>(N * howo * g.o);
+  w.q1_t = c.take<int8_t>((int64_t)g.o * w.ldq);
+  w.bw = c.take<int8_t>(taps * g.c * w.ldq);
+  w.swq = c.take<int32_t>(taps * g.c);
+  w.sumB = c.take<int32_t>(taps * g.c);
+  w.qs = c.take<int32_t>((int64_t)g.o * howo);
+  w.sumA_tap = c.take<int32_t>((int64_t)g.o * taps);
+  w.count_tap = c.take<int32_t>(taps);
+  w.sg = c.take<int32_t>(N * howo);
+  w.ct = c.take<int32_t>(hw * g.c);
+  w.cnt = c.take<int32_t>(hw);
+  w.sx = c.take<float>(1);
+  w.zx = c.take<float>(1);
+  w.sw = c.take<float>(1);
+  w.zw = c.take<float>(1);
+  w.sg1 = c.take<float>(1);
+  w.zg1 = c.take<float>(1);
+  w.sg2 = c.take<float>(N);
+  w.zg2 = c.take<float>(N);
+  if (cfg.qb_x.kind == FQT_BHQ) {
+    w.perm = c.take<int32_t>(N);
+    w.plan = c.take<char>((int64_t)bhq_plan_workspace(N));
+  }
+  // grad_W: split the pixel contraction so that about 512 blocks run, each
+  // K chunk a whole number of 128-byte stages and at most 65536
+  const int64_t tiles = ((g.o + 127) / 128) * ((taps * g.c + 127) / 128);
+  int64_t want = (512 + tiles - 1) / tiles;
+  const int64_t stages = w.ldq / 128;
+  if (want > stages) want = stages;
+  if (want < 1) want = 1;
+  int64_t kchunk = (stages + want - 1) / want * 128;
+  if (kchunk > 65536) kchunk = 65536;
+  w.kchunk = kchunk;
+  w.splits = (int)((w.ldq + kchunk - 1) / kchunk);
+  w.part = c.take<int32_t>((int64_t)w.splits * g.o * taps * g.c);
+  return w;
+}
+
 }  // namespace
 }  // namespace fqt
 
@@ -469,23 +562,172 @@ fqt_status fqt_gemm_s8s8_s64(const int8_t* A, const int8_t* B, int64_t M, int64_
 fqt_status fqt_conv_backward_im2col(const float* X, const float* W, const float* G, const fqt_conv_shape* shape,
                                     const fqt_bwd_cfg* cfg, float* grad_W, float* grad_X, void* ws,
                                     size_t ws_bytes, fqt_stream_t s) {
-  (void)X;
-  (void)W;
-  (void)G;
-  (void)shape;
-  (void)cfg;
-  (void)grad_W;
-  (void)grad_X;
-  (void)ws;
-  (void)ws_bytes;
-  (void)s;
-  return FQT_EUNSUPPORTED;
+  if (!X || !W || !G || !grad_W || !grad_X || !shape) return FQT_EINVAL;
+  fqt_status st = check_conv_shape(*shape);
+  if (st != FQT_OK) return st;
+  st = check_cfg(cfg);
+  if (st != FQT_OK) return st;
+  if (!ws) return FQT_EWORKSPACE;
+  if (ws_bytes < fqt_conv_backward_workspace(shape, cfg)) return FQT_EWORKSPACE;
+  const ConvGeom g = conv_geom(*shape);
+  Carver c(ws);
+  ConvWs w = carve_conv(c, X, W, G, g, *cfg);
+  const fqt_qspec qx = cfg->qb_x;
+  const bool bhq = qx.kind == FQT_BHQ;
+  const Tracer tr{cfg->trace, s};
+  const int64_t N = g.n, D = (int64_t)g.ho * g.wo * g.o;
+  const int64_t hw = (int64_t)g.h * g.w, howo = (int64_t)g.ho * g.wo;
+  const int64_t taps = (int64_t)g.kh * g.kw;
+
+  tr.begin(0);
+  tr.end(0);
+  tr.begin(1);
+  StatsPlan sp{};
+  sp.seg[0] = w.sx_seg;
+  sp.seg[1] = w.sw_seg;
+  sp.seg[2] = w.sg_seg;
+  sp.nseg = 3;
+  FQT_TRY(launch_stats(sp, s));
+  tr.end(1);
+  tr.begin(2);
+  FinalizePlan fp{};
+  fp.seg[0] = w.sx_seg;
+  fp.seg[1] = w.sw_seg;
+  fp.seg[2] = w.sg_seg;
+  fp.nseg = 3;
+  fp.row_seg = 2;
+  fp.rmin = w.rmin;
+  fp.rmax = w.rmax;
+  fp.status = w.h.status;
+  fp.out[0] = ScaleOut{0, cfg->f_bits, 0, w.sx, w.zx};
+  fp.out[1] = ScaleOut{1, cfg->theta_bits, 0, w.sw, w.zw};
+  fp.out[2] = ScaleOut{2, cfg->qb_w.bits, 0, w.sg1, w.zg1};
+  fp.nout = 3;
+  if (!bhq) fp.out[fp.nout++] = ScaleOut{2, qx.bits, qx.kind == FQT_PSQ ? 1 : 0, w.sg2, w.zg2};
+  add_zero(fp, w.sumB, taps * g.c);
+  if (bhq) add_zero(fp, bhq_plan_carve(w.plan, N).rank, N);
+  FQT_TRY(launch_finalize(fp, s));
+  BhqLayout L{};
+  int mode = qx.kind == FQT_PSQ ? QM_ROW : QM_TENSOR;
+  if (bhq) {
+    L = bhq_layout(N, qx.block_size);
+    FQT_TRY(launch_bhq_plan(w.rmin, w.rmax, L, qx.bits, w.plan, w.perm, w.sg2, w.zg2, nullptr, s));
+    mode = QM_BHQ;
+  }
+  tr.end(2);
+
+  // Q_f(X): codes [c][pixels], samples in slot order
+  tr.begin(3);
+  NarrowQParams nx{};
+  nx.x = X;
+  nx.rows = N * hw;
+  nx.cols = g.c;
+  nx.perm = w.perm;
+  nx.blk = hw;
+  nx.bits = cfg->f_bits;
+  nx.scale = w.sx;
+  nx.zero = w.zx;
+  nx.q_t = w.xq_t;
+  nx.ldt = N * hw;
+  FQT_TRY(launch_quant_narrow_t(nx, s));
+  tr.end(3);
+  // Q_theta(W): codes [c][(r, s, o)] and their sums over o
+  tr.begin(4);
+  FQT_TRY(launch_conv_wq(W, g, cfg->theta_bits, w.sw, w.zw, w.wq_t, w.swq, s));
+  tr.end(4);
+  // Q_b2(G) [slot][(y, x, o)] (stream 1); Q_b1(G) [o][pixels] (stream 0)
+  tr.begin(5);
+  QuantParams pg{};
+  pg.x = G;
+  pg.rows = N;
+  pg.cols = D;
+  pg.perm = w.perm;
+  pg.bits = qx.bits;
+  pg.stoch = 1;
+  pg.seed = cfg->seed;
+  pg.stream = 1;
+  pg.scale = w.sg2;
+  pg.zero = w.zg2;
+  pg.q_nat = w.q2;
+  pg.L = L;
+  FQT_TRY(launch_quant(pg, mode, s));
+  NarrowQParams n1{};
+  n1.x = G;
+  n1.rows = N * howo;
+  n1.cols = g.o;
+  n1.perm = w.perm;
+  n1.blk = howo;
+  n1.bits = cfg->qb_w.bits;
+  n1.stoch = 1;
+  n1.seed = cfg->seed;
+  n1.stream = 0;
+  n1.scale = w.sg1;
+  n1.zero = w.zg1;
+  n1.q_t = w.q1_t;
+  n1.ldt = w.ldq;
+  FQT_TRY(launch_quant_narrow_t(n1, s));
+  tr.end(5);
+
+  // grad_W [o][(r, s, c)] = Q_b1(G)^T im2col(Q_f(X)), split over output pixels
+  tr.begin(6);
+  FQT_TRY(launch_conv_im2col_w(g, w.xq_t, w.bw, w.ldq, w.sumB, s));
+  FQT_TRY(launch_conv_tapsums(g, w.q1_t, w.ldq, w.qs, w.sumA_tap, w.count_tap, s));
+  GemmParams gw{};
+  gw.A = w.q1_t;
+  gw.B = w.bw;
+  gw.M = g.o;
+  gw.N = taps * g.c;
+  gw.K = w.ldq;
+  gw.lda = w.ldq;
+  gw.ldb = w.ldq;
+  gw.splits = w.splits;
+  gw.kchunk = w.kchunk;
+  gw.part = w.part;
+  gw.out = grad_W;
+  gw.ldo = taps * g.c;
+  gw.sumB = w.sumB;
+  gw.scaleA = w.sg1;
+  gw.zeroA = w.zg1;
+  gw.halfA = 1 << (cfg->qb_w.bits - 1);
+  gw.scaleB = w.sx;
+  gw.zeroB = w.zx;
+  gw.halfB = 1 << (cfg->f_bits - 1);
+  FQT_TRY(launch_gemm(gw, EPI_RAW_I32, s));
+  FQT_TRY(launch_conv_gradw_reduce(gw, g, w.sumA_tap, w.count_tap, s));
+  tr.end(6);
+
+  // grad_X [n][h][w][c] = col2im(Q_b2(G) Q_theta(W)), implicit im2col rows
+  tr.begin(7);
+  FQT_TRY(launch_conv_gradx_prep(g, w.q2, w.swq, w.sg, w.ct, w.cnt, s));
+  GemmParams gx{};
+  gx.B = w.wq_t;
+  gx.M = hw * g.npad;
+  gx.N = g.c;
+  gx.K = taps * g.o;
+  gx.ldb = taps * g.o;
+  gx.splits = 1;
+  gx.kchunk = gx.K;
+  gx.out = grad_X;
+  gx.ldo = g.c;
+  gx.perm = w.perm;
+  gx.scaleA = w.sg2;
+  gx.zeroA = w.zg2;
+  gx.rowwiseA = qx.kind != FQT_PTQ;
+  gx.halfA = 1 << (qx.bits - 1);
+  gx.scaleB = w.sw;
+  gx.zeroB = w.zw;
+  gx.halfB = 1 << (cfg->theta_bits - 1);
+  gx.L = L;
+  FQT_TRY(launch_conv_gradx(gx, bhq ? EPI_BHQ : EPI_ROW, g, w.q2, w.sg, w.ct, w.cnt, s));
+  tr.end(7);
+  return FQT_OK;
 }
 
 size_t fqt_conv_backward_workspace(const fqt_conv_shape* shape, const fqt_bwd_cfg* cfg) {
-  (void)shape;
-  (void)cfg;
-  return 0;
+  if (!shape || !cfg || check_conv_shape(*shape) != FQT_OK) return 0;
+  Carver c(nullptr);
+  carve_conv(c, nullptr, nullptr, nullptr, conv_geom(*shape), *cfg);
+  return c.off;
 }
 
 fqt_status fqt_workspace_status(const void* ws, fqt_stream_t s) {

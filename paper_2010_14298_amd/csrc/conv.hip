@@ -1,0 +1,515 @@
+// Conv layer FQT backward on gfx950 (NHWC tensors, rows = samples).
+//
+// The conv is the linear layer Y = im2col(X) W^T (Sec. 2.1 for linear layers),
+// so its backward is grad_W = Q_b1(G)^T im2col(Q_f(X)) and
+// grad_X = col2im(Q_b2(G) Q_theta(W)) (Sec. 2.2).  Layouts:
+//
+//   X codes    [c][pixels]           per-tensor PTQ, samples in slot order
+//   Q_b1(G)    [o][pixels (padded)]  per-tensor stochastic PTQ, slot order
+//   im2col     [(r, s, c)][pixels]   X codes per tap, zero codes on padding
+//   W codes    [c][(r, s, o)]        per-tensor PTQ
+//   Q_b2(G)    [slot][(y, x, o)]     PTQ / PSQ / BHQ, natural layout
+//
+// grad_W is a split-K int8 contraction over output pixels with per-tap
+// masked zero-point sums in its epilogue.  grad_X is an implicit-im2col
+// contraction: its A rows (input pixel, slot) are gathered 16 output
+// channels at a time from Q_b2(G); padded taps load zero codes and the
+// epilogue subtracts nothing for them (their zero-point sums are built from
+// the valid taps only).  A tile row block holds the slots of one input pixel,
+// so the block Householder inverse of a group runs inside the tile.
+#include "gemm_core.h"
+
+namespace fqt {
+
+// ---------------------------------------------------------------------------
+// narrow transposing per-tensor quantizer: logical [rows, cols] (cols small)
+// -> codes [cols][ldt], rows in slot order; rows in [rows, ldt) get code 0
+// ---------------------------------------------------------------------------
+template <int LPR>
+__global__ __launch_bounds__(256) void quant_narrow_t_kernel(NarrowQParams p) {
+  constexpr int RG = 64 / LPR;  // row groups of 16 per wave
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int q = lane / LPR, cl = lane % LPR;
+  const int64_t r0 = (int64_t)blockIdx.x * (4 * RG * 16) + wave * (RG * 16) + q * 16;
+  const int64_t c0 = (int64_t)cl * 4;
+  const int B = (1 << p.bits) - 1;
+  const int half = 1 << (p.bits - 1);
+  const float s = p.scale[0], z = p.zero[0];
+  const bool vec = (p.cols & 3) == 0;
+  uint32_t tcodes[4][4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+#pragma unroll
+    for (int w = 0; w < 4; ++w) tcodes[j][w] = 0u;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const int64_t row = r0 + r;
+    const bool ok = row < p.rows;
+    const int64_t src = ok ? (p.perm ? (int64_t)p.perm[row / p.blk] * p.blk + row % p.blk : row) : 0;
+    const float* xr = p.x + src * p.cols;
+    float g[4];
+    if (ok && vec && c0 + 3 < p.cols) {
+      const float4 v = *reinterpret_cast<const float4*>(xr + c0);
+      g[0] = v.x;
+      g[1] = v.y;
+      g[2] = v.z;
+      g[3] = v.w;
+    } else {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) g[j] = (ok && c0 + j < p.cols) ? xr[c0 + j] : 0.0f;
+    }
+    int code[4];
+    const uint64_t ebase = (uint64_t)src * (uint64_t)p.cols + (uint64_t)c0;
+    if (p.stoch) {
+      if (vec) {
+        const u32x4 o = philox_block(ebase, p.seed, p.stream);
+        code[0] = sr_code(s * (g[0] - z), o.x, B);
+        code[1] = sr_code(s * (g[1] - z), o.y, B);
+        code[2] = sr_code(s * (g[2] - z), o.z, B);
+        code[3] = sr_code(s * (g[3] - z), o.w, B);
+      } else {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const uint64_t e = ebase + j;
+          const u32x4 o = philox_block(e, p.seed, p.stream);
+          code[j] = sr_code(s * (g[j] - z), philox_word(o, (int)(e & 3)), B);
+        }
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) code[j] = rne_code(s * (g[j] - z), B);
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int qv = (ok && c0 + j < p.cols) ? code[j] - half : 0;
+      tcodes[j][r >> 2] |= (uint32_t)(qv & 255) << (8 * (r & 3));
+    }
+  }
+  const bool tvec = ((p.ldt & 15) == 0) && (r0 + 15 < p.ldt);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int64_t col = c0 + j;
+    if (col >= p.cols || r0 >= p.ldt) continue;
+    int8_t* dst = p.q_t + col * p.ldt + r0;
+    if (tvec) {
+      *reinterpret_cast<uint4*>(dst) = make_uint4(tcodes[j][0], tcodes[j][1], tcodes[j][2], tcodes[j][3]);
+    } else {
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        if (r0 + r < p.ldt) dst[r] = (int8_t)((tcodes[j][r >> 2] >> (8 * (r & 3))) & 255);
+    }
+  }
+}
+
+hipError_t launch_quant_narrow_t(const NarrowQParams& p, hipStream_t s) {
+  // lanes per row: the smallest power of two covering cols / 4 (at most 64)
+  const int64_t need = (p.cols + 3) / 4;
+  int lpr = 1;
+  while (lpr < need && lpr < 64) lpr <<= 1;
+  if (need > 64) return hipErrorInvalidValue;
+  const int64_t rows_per_block = 4 * (64 / lpr) * 16;
+  const int64_t blocks = (p.ldt + rows_per_block - 1) / rows_per_block;
+  if (blocks > 0x7FFFFFFF) return hipErrorInvalidValue;
+  const dim3 grid((unsigned)blocks);
+  switch (lpr) {
+    case 1: hipLaunchKernelGGL(quant_narrow_t_kernel<1>, grid, dim3(256), 0, s, p); break;
+    case 2: hipLaunchKernelGGL(quant_narrow_t_kernel<2>, grid, dim3(256), 0, s, p); break;
+    case 4: hipLaunchKernelGGL(quant_narrow_t_kernel<4>, grid, dim3(256), 0, s, p); break;
+    case 8: hipLaunchKernelGGL(quant_narrow_t_kernel<8>, grid, dim3(256), 0, s, p); break;
+    case 16: hipLaunchKernelGGL(quant_narrow_t_kernel<16>, grid, dim3(256), 0, s, p); break;
+    case 32: hipLaunchKernelGGL(quant_narrow_t_kernel<32>, grid, dim3(256), 0, s, p); break;
+    default: hipLaunchKernelGGL(quant_narrow_t_kernel<64>, grid, dim3(256), 0, s, p); break;
+  }
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// W codes [c][(r, s, o)] (deterministic PTQ) and their sums over o per (tap, c)
+// ---------------------------------------------------------------------------
+__global__ void conv_wq_kernel(const float* W, ConvGeom g, int bits, const float* scale, const float* zero,
+                               int8_t* wq_t, int32_t* swq) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int taps = g.kh * g.kw;
+  if (t >= (int64_t)taps * g.c) return;
+  const int tap = (int)(t / g.c), c = (int)(t % g.c);
+  const int B = (1 << bits) - 1, half = 1 << (bits - 1);
+  const float s = scale[0], z = zero[0];
+  const int64_t K = (int64_t)taps * g.o;
+  int sum = 0;
+  for (int o = 0; o < g.o; ++o) {
+    const float v = W[((int64_t)o * taps + tap) * g.c + c];
+    const int q = rne_code(s * (v - z), B) - half;
+    wq_t[(int64_t)c * K + (int64_t)tap * g.o + o] = (int8_t)q;
+    sum += q;
+  }
+  swq[(int64_t)tap * g.c + c] = sum;
+}
+
+// ---------------------------------------------------------------------------
+// im2col of the X codes for grad_W: B[(r, s, c)][p] over output pixels p in
+// slot order (zero codes on padded taps and for p >= P), plus row sums
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void conv_im2col_w_kernel(ConvGeom g, const int8_t* xq_t, int8_t* bw, int64_t ldb,
+                                                            int32_t* sumB) {
+  const int64_t row = blockIdx.y;
+  const int tap = (int)(row / g.c), c = (int)(row % g.c);
+  const int r = tap / g.kw, s = tap % g.kw;
+  const int64_t hw = (int64_t)g.h * g.w, howo = (int64_t)g.ho * g.wo;
+  const int64_t P = (int64_t)g.n * howo;
+  const int64_t p0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 16;
+  const int8_t* xc = xq_t + (int64_t)c * g.n * hw;
+  uint32_t w[4] = {0u, 0u, 0u, 0u};
+  int sum = 0;
+  if (p0 < ldb) {
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const int64_t p = p0 + i;
+      int v = 0;
+      if (p < P) {
+        const int64_t slot = p / howo, pix = p % howo;
+        const int y = (int)(pix / g.wo), x = (int)(pix % g.wo);
+        const int iy = y * g.stride - g.pad + r, ix = x * g.stride - g.pad + s;
+        if (iy >= 0 && iy < g.h && ix >= 0 && ix < g.w) v = xc[slot * hw + (int64_t)iy * g.w + ix];
+      }
+      sum += v;
+      w[i >> 2] |= (uint32_t)(v & 255) << (8 * (i & 3));
+    }
+    *reinterpret_cast<uint4*>(bw + row * ldb + p0) = make_uint4(w[0], w[1], w[2], w[3]);
+  }
+  // block sum -> one atomic per block
+  __shared__ int ssum[4];
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) sum += __shfl_xor(sum, o);
+  if ((threadIdx.x & 63) == 0) ssum[threadIdx.x >> 6] = sum;
+  __syncthreads();
+  if (threadIdx.x == 0) atomicAdd(sumB + row, ssum[0] + ssum[1] + ssum[2] + ssum[3]);
+}
+
+// ---------------------------------------------------------------------------
+// masked zero-point sums of Q_b1(G) per (o, tap) and the valid-pixel count of
+// each tap: Qs[o][y][x] = sum over samples, then rectangle sums per tap
+// ---------------------------------------------------------------------------
+__global__ void conv_qsum_kernel(ConvGeom g, const int8_t* q1_t, int64_t ldq, int32_t* qs) {
+  const int64_t howo = (int64_t)g.ho * g.wo;
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= (int64_t)g.o * howo) return;
+  const int64_t o = t / howo, pix = t % howo;
+  const int8_t* row = q1_t + o * ldq + pix;
+  int sum = 0;
+  for (int n = 0; n < g.n; ++n) sum += row[(int64_t)n * howo];
+  qs[t] = sum;
+}
+
+// valid output rows / columns of tap offset r: y with 0 <= y*stride - pad + r < h
+__device__ __forceinline__ void tap_range(int r, int stride, int pad, int h, int ho, int& lo, int& hi) {
+  lo = 0;
+  while (lo < ho && lo * stride - pad + r < 0) ++lo;
+  hi = ho;
+  while (hi > lo && (hi - 1) * stride - pad + r >= h) --hi;
+}
+
+__global__ void conv_tapsum_kernel(ConvGeom g, const int32_t* qs, int32_t* sumA_tap, int32_t* count_tap) {
+  const int taps = g.kh * g.kw;
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= (int64_t)g.o * taps) return;
+  const int o = (int)(t / taps), tap = (int)(t % taps);
+  const int r = tap / g.kw, s = tap % g.kw;
+  int ylo, yhi, xlo, xhi;
+  tap_range(r, g.stride, g.pad, g.h, g.ho, ylo, yhi);
+  tap_range(s, g.stride, g.pad, g.w, g.wo, xlo, xhi);
+  const int32_t* q = qs + (int64_t)o * g.ho * g.wo;
+  int sum = 0;
+  for (int y = ylo; y < yhi; ++y)
+    for (int x = xlo; x < xhi; ++x) sum += q[(int64_t)y * g.wo + x];
+  sumA_tap[t] = sum;
+  if (o == 0) count_tap[tap] = g.n * (yhi - ylo) * (xhi - xlo);
+}
+
+// split-K reduction of grad_W with the per-tap masked zero-point expansion:
+// out[o][(tap, c)] = dA dB acc + dA zB sumA_tap[o][tap] + zA dB sumB[(tap, c)] + count[tap] zA zB
+__global__ void conv_gradw_reduce_kernel(GemmParams p, ConvGeom g, const int32_t* sumA_tap, const int32_t* count_tap) {
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t MN = p.M * p.N;
+  if (idx >= MN) return;
+  int64_t sum = 0;
+  for (int s = 0; s < p.splits; ++s) sum += (int64_t)p.part[(int64_t)s * MN + idx];
+  const int64_t row = idx / p.N, col = idx % p.N;
+  const int taps = g.kh * g.kw;
+  const int tap = (int)(col / g.c);
+  const double dA = 1.0 / (double)p.scaleA[0];
+  const double zA = (double)p.zeroA[0] + (double)p.halfA * dA;
+  const double dB = 1.0 / (double)p.scaleB[0];
+  const double zB = (double)p.zeroB[0] + (double)p.halfB * dB;
+  const double v = dA * dB * (double)sum + dA * zB * (double)sumA_tap[row * taps + tap] +
+                   zA * dB * (double)p.sumB[col] + (double)count_tap[tap] * zA * zB;
+  p.out[row * p.ldo + col] = (float)v;
+}
+
+// ---------------------------------------------------------------------------
+// grad_X helpers: S_G[slot][pix] = sum_o Q_b2 codes; CT[pix_in][c] = sum of W
+// codes over the valid taps of an input pixel, cnt[pix_in] = their number
+// ---------------------------------------------------------------------------
+__global__ void conv_sg_kernel(ConvGeom g, const int8_t* q2, int32_t* sg) {
+  const int64_t howo = (int64_t)g.ho * g.wo;
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= (int64_t)g.n * howo) return;
+  const int8_t* src = q2 + t * g.o;  // slot-major [slot][(pix, o)] is contiguous in t * o
+  int sum = 0;
+  for (int o = 0; o < g.o; ++o) sum += src[o];
+  sg[t] = sum;
+}
+
+// taps (r, s) whose output pixel feeds input pixel (iy, ix)
+__device__ __forceinline__ bool tap_hits(const ConvGeom& g, int iy, int ix, int r, int s, int& y, int& x) {
+  const int ty = iy + g.pad - r, tx = ix + g.pad - s;
+  if (ty < 0 || tx < 0 || ty % g.stride || tx % g.stride) return false;
+  y = ty / g.stride;
+  x = tx / g.stride;
+  return y < g.ho && x < g.wo;
+}
+
+__global__ void conv_ct_kernel(ConvGeom g, const int32_t* swq, int32_t* ct, int32_t* cnt) {
+  const int64_t hw = (int64_t)g.h * g.w;
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= hw * g.c) return;
+  const int64_t pix = t / g.c;
+  const int c = (int)(t % g.c);
+  const int iy = (int)(pix / g.w), ix = (int)(pix % g.w);
+  int sum = 0, n = 0;
+  for (int r = 0; r < g.kh; ++r)
+    for (int s = 0; s < g.kw; ++s) {
+      int y, x;
+      if (tap_hits(g, iy, ix, r, s, y, x)) {
+        sum += swq[(int64_t)(r * g.kw + s) * g.c + c];
+        ++n;
+      }
+    }
+  ct[t] = sum;
+  if (c == 0) cnt[pix] = n;
+}
+
+// Implicit im2col rows of grad_X: row m = (input pixel m / npad, slot m % npad);
+// column k = (tap k / o, channel k % o).  16-byte chunks of 16 channels.
+struct ConvXLoader {
+  const int8_t* q2;
+  ConvGeom g;
+  int64_t M, K, D;
+  __device__ __forceinline__ Chunk16 operator()(int64_t m, int64_t k) const {
+    Chunk16 c{{0u, 0u, 0u, 0u}};
+    if (m >= M || k >= K) return c;
+    const int64_t slot = m % g.npad, pix = m / g.npad;
+    if (slot >= g.n) return c;
+    const int tap = (int)(k / g.o), o0 = (int)(k % g.o);
+    const int r = tap / g.kw, s = tap % g.kw;
+    const int iy = (int)(pix / g.w), ix = (int)(pix % g.w);
+    int y, x;
+    if (!tap_hits(g, iy, ix, r, s, y, x)) return c;
+    const uint4 v = *reinterpret_cast<const uint4*>(q2 + slot * D + ((int64_t)y * g.wo + x) * g.o + o0);
+    c.w[0] = v.x;
+    c.w[1] = v.y;
+    c.w[2] = v.z;
+    c.w[3] = v.w;
+    return c;
+  }
+};
+
+struct ConvRowStage {
+  double rterm;  // zW * (codes summed over the valid taps of the row)
+  double hz;     // BHQ group row: half + c_g;  affine row: z + half / s
+  double dq;     // 1 / s
+  int kind;      // BHQ slot kind (0 affine)
+  int orow;      // output pixel row (sample * h * w + pixel), -1 if none
+  int pix;       // input pixel
+};
+
+using CfgConvX = TileCfg<256, 64, 64, 64>;
+
+template <int EPI, int KG>
+__global__ __launch_bounds__(256) void conv_gradx_kernel(GemmParams p, ConvGeom g, const int8_t* q2, const int32_t* sg,
+                                                          const int32_t* ct, const int32_t* cnt) {
+  using C = CfgConvX;
+  constexpr int EP_BYTES = C::BM * C::BN * 4 + C::BM * (int)sizeof(ConvRowStage);
+  constexpr int BYTES = EP_BYTES > C::OP_BYTES ? EP_BYTES : C::OP_BYTES;
+  __shared__ __attribute__((aligned(16))) int8_t lds[BYTES];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int wm = wave / C::WAVES_N, wn = wave % C::WAVES_N;
+  const int64_t tiles_n = (p.N + C::BN - 1) / C::BN;
+  const int64_t tiles_m = (p.M + C::BM - 1) / C::BM;
+  const int64_t tile = xcd_tile(blockIdx.x, tiles_m * tiles_n);
+  const int64_t m0 = (tile / tiles_n) * C::BM;
+  const int64_t n0 = (tile % tiles_n) * C::BN;
+  const int lrow = lane & 31;
+  const int h = lane >> 5;
+  const int64_t D = (int64_t)g.ho * g.wo * g.o;
+
+  v16i acc[C::IT][C::JT];
+#pragma unroll
+  for (int i = 0; i < C::IT; ++i)
+#pragma unroll
+    for (int j = 0; j < C::JT; ++j) acc[i][j] = v16i{0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0};
+  const ConvXLoader aload{q2, g, p.M, p.K, D};
+  gemm_mainloop<C, false>(p, aload, lds, m0, n0, 0, p.K, acc);
+
+  int32_t* sacc = reinterpret_cast<int32_t*>(lds);
+  ConvRowStage* srow = reinterpret_cast<ConvRowStage*>(lds + C::BM * C::BN * 4);
+  const double dW = 1.0 / (double)p.scaleB[0];
+  const double zW = (double)p.zeroB[0] + (double)p.halfB * dW;
+#pragma unroll
+  for (int i = 0; i < C::IT; ++i)
+#pragma unroll
+    for (int j = 0; j < C::JT; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        sacc[(wm * C::WM + i * 32 + 8 * (r >> 2) + 4 * h + (r & 3)) * C::BN + wn * C::WN + j * 32 + lrow] =
+            acc[i][j][r];
+  const int64_t hw = (int64_t)g.h * g.w, howo = (int64_t)g.ho * g.wo;
+  for (int rr = tid; rr < C::BM; rr += C::THREADS) {
+    const int64_t m = m0 + rr;
+    ConvRowStage q{};
+    q.orow = -1;
+    const int64_t slot = m % g.npad, pix = m / g.npad;
+    if (m < p.M && slot < g.n) {
+      const float s = p.rowwiseA ? p.scaleA[slot] : p.scaleA[0];
+      const float z = p.rowwiseA ? p.zeroA[slot] : p.zeroA[0];
+      q.kind = (EPI == EPI_BHQ) ? bhq_slot_kind(p.L, slot) : 0;
+      const int iy = (int)(pix / g.w), ix = (int)(pix % g.w);
+      int rs = 0;
+      for (int r = 0; r < g.kh; ++r)
+        for (int s2 = 0; s2 < g.kw; ++s2) {
+          int y, x;
+          if (tap_hits(g, iy, ix, r, s2, y, x)) rs += sg[slot * howo + (int64_t)y * g.wo + x];
+        }
+      q.rterm = zW * (double)rs;
+      q.dq = 1.0 / (double)s;
+      q.hz = q.kind != 0 ? (double)p.halfA + (double)z : (double)z + (double)p.halfA * q.dq;
+      q.orow = (int)((p.perm ? (int64_t)p.perm[slot] : slot) * hw + pix);
+      q.pix = (int)pix;
+    }
+    srow[rr] = q;
+  }
+  __syncthreads();
+  constexpr int RUNS = C::THREADS / C::BN;
+  constexpr int RUN = C::BM / RUNS;  // 64 rows: the slots of one input pixel (npad % 64 == 0)
+  const int c = tid % C::BN;
+  const int rbase = (tid / C::BN) * RUN;
+  const int64_t col = n0 + c;
+  if (col >= p.N) return;
+  const double kz = (double)g.o * zW;
+  if constexpr (EPI == EPI_BHQ && KG > 1) {
+    for (int g0 = rbase; g0 < rbase + RUN; g0 += KG) {
+      const ConvRowStage& q0 = srow[g0];
+      if (q0.orow < 0 && q0.kind == 0) continue;
+      const int pix = q0.pix;
+      const double colterm = dW * (double)ct[(int64_t)pix * g.c + col] + (double)cnt[pix] * kz;
+      double S = 0.0, T0 = 0.0;
+      for (int t = 0; t < KG; ++t) {
+        const ConvRowStage& q = srow[g0 + t];
+        const double T = dW * (double)sacc[(g0 + t) * C::BN + c] + (q.rterm + q.hz * colterm);
+        if (q.kind != 0) S += T;
+        if (t == 0) T0 = T;
+      }
+      const double alpha = q0.kind == 2 ? p.L.inv_sk_p : p.L.inv_sk_k;
+      const double tau = (alpha * S - T0) / (1.0 - alpha);
+      for (int t = 0; t < KG; ++t) {
+        const ConvRowStage& q = srow[g0 + t];
+        if (q.orow < 0) continue;
+        const double a = (double)sacc[(g0 + t) * C::BN + c];
+        double v;
+        if (q.kind != 0) {
+          const double T = dW * a + (q.rterm + q.hz * colterm);
+          const double Z = (t == 0) ? T + (1.0 - alpha) * tau : T - alpha * tau;
+          v = Z * q.dq;
+        } else {
+          v = q.dq * (dW * a + q.rterm) + q.hz * colterm;
+        }
+        p.out[(int64_t)q.orow * p.ldo + col] = (float)v;
+      }
+    }
+  } else {
+    for (int t = rbase; t < rbase + RUN; ++t) {
+      const ConvRowStage& q = srow[t];
+      if (q.orow < 0) continue;
+      const double colterm = dW * (double)ct[(int64_t)q.pix * g.c + col] + (double)cnt[q.pix] * kz;
+      const double a = (double)sacc[t * C::BN + c];
+      p.out[(int64_t)q.orow * p.ldo + col] = (float)(q.dq * (dW * a + q.rterm) + q.hz * colterm);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// launchers
+// ---------------------------------------------------------------------------
+hipError_t launch_conv_wq(const float* W, const ConvGeom& g, int bits, const float* scale, const float* zero,
+                          int8_t* wq_t, int32_t* swq, hipStream_t s) {
+  const int64_t n = (int64_t)g.kh * g.kw * g.c;
+  hipLaunchKernelGGL(conv_wq_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, W, g, bits, scale, zero, wq_t,
+                     swq);
+  return hipGetLastError();
+}
+
+hipError_t launch_conv_im2col_w(const ConvGeom& g, const int8_t* xq_t, int8_t* bw, int64_t ldb, int32_t* sumB,
+                                hipStream_t s) {
+  const int64_t rows = (int64_t)g.kh * g.kw * g.c;
+  const int64_t chunks = (ldb + 16 * 256 - 1) / (16 * 256);
+  if (rows > 65535 || chunks > 0x7FFFFFFF) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(conv_im2col_w_kernel, dim3((unsigned)chunks, (unsigned)rows), dim3(256), 0, s, g, xq_t, bw, ldb,
+                     sumB);
+  return hipGetLastError();
+}
+
+hipError_t launch_conv_tapsums(const ConvGeom& g, const int8_t* q1_t, int64_t ldq, int32_t* qs, int32_t* sumA_tap,
+                               int32_t* count_tap, hipStream_t s) {
+  const int64_t n1 = (int64_t)g.o * g.ho * g.wo;
+  hipLaunchKernelGGL(conv_qsum_kernel, dim3((unsigned)((n1 + 255) / 256)), dim3(256), 0, s, g, q1_t, ldq, qs);
+  const int64_t n2 = (int64_t)g.o * g.kh * g.kw;
+  hipLaunchKernelGGL(conv_tapsum_kernel, dim3((unsigned)((n2 + 255) / 256)), dim3(256), 0, s, g, qs, sumA_tap,
+                     count_tap);
+  return hipGetLastError();
+}
+
+hipError_t launch_conv_gradw_reduce(const GemmParams& p, const ConvGeom& g, const int32_t* sumA_tap,
+                                    const int32_t* count_tap, hipStream_t s) {
+  const int64_t MN = p.M * p.N;
+  hipLaunchKernelGGL(conv_gradw_reduce_kernel, dim3((unsigned)((MN + 255) / 256)), dim3(256), 0, s, p, g, sumA_tap,
+                     count_tap);
+  return hipGetLastError();
+}
+
+hipError_t launch_conv_gradx_prep(const ConvGeom& g, const int8_t* q2, const int32_t* swq, int32_t* sg, int32_t* ct,
+                                  int32_t* cnt, hipStream_t s) {
+  const int64_t n1 = (int64_t)g.n * g.ho * g.wo;
+  hipLaunchKernelGGL(conv_sg_kernel, dim3((unsigned)((n1 + 255) / 256)), dim3(256), 0, s, g, q2, sg);
+  const int64_t n2 = (int64_t)g.h * g.w * g.c;
+  hipLaunchKernelGGL(conv_ct_kernel, dim3((unsigned)((n2 + 255) / 256)), dim3(256), 0, s, g, swq, ct, cnt);
+  return hipGetLastError();
+}
+
+template <int EPI, int KG>
+static hipError_t launch_conv_gradx_t(const GemmParams& p, const ConvGeom& g, const int8_t* q2, const int32_t* sg,
+                                      const int32_t* ct, const int32_t* cnt, hipStream_t s) {
+  const int64_t tiles = ((p.M + CfgConvX::BM - 1) / CfgConvX::BM) * ((p.N + CfgConvX::BN - 1) / CfgConvX::BN);
+  if (tiles > 0x7FFFFFFF) return hipErrorInvalidValue;
+  hipLaunchKernelGGL((conv_gradx_kernel<EPI, KG>), dim3((unsigned)tiles), dim3(CfgConvX::THREADS), 0, s, p, g, q2, sg,
+                     ct, cnt);
+  return hipGetLastError();
+}
+
+hipError_t launch_conv_gradx(const GemmParams& p, int epi, const ConvGeom& g, const int8_t* q2, const int32_t* sg,
+                             const int32_t* ct, const int32_t* cnt, hipStream_t s) {
+  if (epi == EPI_ROW) return launch_conv_gradx_t<EPI_ROW, 0>(p, g, q2, sg, ct, cnt, s);
+  switch (p.L.k) {
+    case 1: return launch_conv_gradx_t<EPI_BHQ, 1>(p, g, q2, sg, ct, cnt, s);
+    case 2: return launch_conv_gradx_t<EPI_BHQ, 2>(p, g, q2, sg, ct, cnt, s);
+    case 4: return launch_conv_gradx_t<EPI_BHQ, 4>(p, g, q2, sg, ct, cnt, s);
+    case 8: return launch_conv_gradx_t<EPI_BHQ, 8>(p, g, q2, sg, ct, cnt, s);
+    case 16: return launch_conv_gradx_t<EPI_BHQ, 16>(p, g, q2, sg, ct, cnt, s);
+    case 32: return launch_conv_gradx_t<EPI_BHQ, 32>(p, g, q2, sg, ct, cnt, s);
+    case 64: return launch_conv_gradx_t<EPI_BHQ, 64>(p, g, q2, sg, ct, cnt, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace fqt

@@ -115,6 +115,25 @@ struct QuantParams {
 enum QuantMode { QM_TENSOR = 0, QM_ROW = 1, QM_BHQ = 2 };
 hipError_t launch_quant(const QuantParams& p, int mode, hipStream_t s);
 
+// Narrow transposing per-tensor quantizer (conv activations and Q_b1 of a
+// conv gradient): logical [rows, cols], row r of the output taken from source
+// row perm[r / blk] * blk + r % blk; codes [cols][ldt], rows >= rows get 0.
+struct NarrowQParams {
+  const float* x;
+  int64_t rows, cols;
+  const int32_t* perm;
+  int64_t blk;
+  int bits;
+  int stoch;
+  uint64_t seed;
+  uint32_t stream;
+  const float* scale;
+  const float* zero;
+  int8_t* q_t;
+  int64_t ldt;
+};
+hipError_t launch_quant_narrow_t(const NarrowQParams& p, hipStream_t s);
+
 // ---- int8 contractions ---------------------------------------------------
 
 enum Epilogue {
@@ -151,5 +170,23 @@ hipError_t launch_gemm(const GemmParams& p, int epi, hipStream_t s);
 // Sum int32 split partials in int64; either store int64 (out64) or apply the
 // per-tensor epilogue (EPI_TENSOR) into p.out.
 hipError_t launch_splitk_reduce(const GemmParams& p, int64_t* out64, int epi, hipStream_t s);
+
+// ---- conv ----------------------------------------------------------------
+struct ConvGeom {
+  int n, c, h, w, o, kh, kw, stride, pad, ho, wo;
+  int64_t npad;  // slots per input pixel in the grad_X rows (multiple of 64)
+};
+hipError_t launch_conv_wq(const float* W, const ConvGeom& g, int bits, const float* scale, const float* zero,
+                          int8_t* wq_t, int32_t* swq, hipStream_t s);
+hipError_t launch_conv_im2col_w(const ConvGeom& g, const int8_t* xq_t, int8_t* bw, int64_t ldb, int32_t* sumB,
+                                hipStream_t s);
+hipError_t launch_conv_tapsums(const ConvGeom& g, const int8_t* q1_t, int64_t ldq, int32_t* qs, int32_t* sumA_tap,
+                               int32_t* count_tap, hipStream_t s);
+hipError_t launch_conv_gradw_reduce(const GemmParams& p, const ConvGeom& g, const int32_t* sumA_tap,
+                                    const int32_t* count_tap, hipStream_t s);
+hipError_t launch_conv_gradx_prep(const ConvGeom& g, const int8_t* q2, const int32_t* swq, int32_t* sg, int32_t* ct,
+                                  int32_t* cnt, hipStream_t s);
+hipError_t launch_conv_gradx(const GemmParams& p, int epi, const ConvGeom& g, const int8_t* q2, const int32_t* sg,
+                             const int32_t* ct, const int32_t* cnt, hipStream_t s);
 
 }  // namespace fqt

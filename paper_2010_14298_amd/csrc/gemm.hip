@@ -15,58 +15,9 @@
 // its L2).  Exact int32 accumulation over K-chunks of at most 65536 (|q| <=
 // 128, so 65536 * 2^14 < 2^31); longer K is split and the int32 partials
 // are summed in int64.
-#include "fqt_device.h"
-#include "fqt_kernels.h"
+#include "gemm_core.h"
 
 namespace fqt {
-
-typedef int v4i __attribute__((ext_vector_type(4)));
-typedef int v16i __attribute__((ext_vector_type(16)));
-
-constexpr int BK = 128;          // K bytes per pipeline stage
-constexpr int KCH = BK / 16;     // 16-byte chunks per row per stage
-constexpr int LDS_STRIDE = 144;  // bytes per tile row in LDS: 128 + 16 (conflict-free 8- and 16-lane phases)
-constexpr int NUM_XCD = 8;
-
-template <int BM_, int BN_, int WM_, int WN_>
-struct TileCfg {
-  static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_;
-  static constexpr int WAVES_N = BN / WN;
-  static constexpr int THREADS = (BM / WM) * (BN / WN) * 64;
-  static constexpr int IT = WM / 32, JT = WN / 32;
-  static constexpr int A_CHUNKS = BM * KCH / THREADS;  // 16-byte chunks per thread per K stage
-  static constexpr int B_CHUNKS = BN * KCH / THREADS;
-  static constexpr int OP_BYTES = 2 * (BM + BN) * LDS_STRIDE;
-};
-using CfgLarge = TileCfg<256, 128, 128, 64>;
-using CfgSmall = TileCfg<128, 128, 64, 64>;
-
-typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
-struct alignas(16) Chunk16 {
-  uint32_t w[4];
-};
-
-// One 16-byte chunk of row r, K offset k (zero outside the matrix / K range).
-__device__ __forceinline__ Chunk16 load_chunk(const int8_t* base, int64_t ld, int64_t r, int64_t nrows, int64_t k,
-                                              int64_t kend, bool aligned) {
-  Chunk16 c{{0u, 0u, 0u, 0u}};
-  if (r >= nrows) return c;
-  const int8_t* p = base + r * ld + k;
-  if (aligned && k + 16 <= kend) {
-    const uint4 v = *reinterpret_cast<const uint4*>(p);
-    c.w[0] = v.x;
-    c.w[1] = v.y;
-    c.w[2] = v.z;
-    c.w[3] = v.w;
-  } else {
-#pragma unroll
-    for (int b = 0; b < 16; ++b) {
-      const uint32_t byte = (k + b < kend) ? (uint32_t)(uint8_t)p[b] : 0u;
-      c.w[b >> 2] |= byte << (8 * (b & 3));
-    }
-  }
-  return c;
-}
 
 // Per-row epilogue data of the grad_X contraction, staged in LDS.
 struct RowStage {
@@ -83,139 +34,6 @@ struct GemmLdsSize {
   static constexpr bool STAGED = (EPI == EPI_ROW || EPI == EPI_BHQ);
   static constexpr int BYTES = (STAGED && EP_BYTES > C::OP_BYTES) ? EP_BYTES : C::OP_BYTES;
 };
-
-// Bijective block -> tile map: the first 8 * floor(T / 8) blocks give each
-// XCD (block id mod 8) a contiguous run of tiles; the rest map to themselves.
-__device__ __forceinline__ int64_t xcd_tile(int64_t id, int64_t ntiles) {
-  const int64_t q = ntiles / NUM_XCD;
-  if (id < q * NUM_XCD) return (id % NUM_XCD) * q + id / NUM_XCD;
-  return id;
-}
-
-// The K loop.  FAST requires 16-byte aligned rows, a K range that is a
-// whole number of stages and 32-bit byte offsets; then each thread keeps
-// constant offsets into a wave-uniform base pointer that advances by one
-// stage per iteration (global loads in base + offset form), rows past the
-// matrix edge are clamped to the last row (their outputs are never stored),
-// and LDS addresses are constants: the loop carries almost no vector ALU
-// work besides the matrix-core instructions.
-template <class C, bool FAST>
-__device__ __forceinline__ void gemm_mainloop(const GemmParams& p, int8_t* lds, int64_t m0, int64_t n0, int64_t kbeg,
-                                              int64_t kend, v16i (&acc)[C::IT][C::JT]) {
-  int8_t* sA = lds;                          // [2][BM * LDS_STRIDE]
-  int8_t* sB = lds + 2 * C::BM * LDS_STRIDE;  // [2][BN * LDS_STRIDE]
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = tid >> 6;
-  const int wm = wave / C::WAVES_N, wn = wave % C::WAVES_N;
-  const bool alA = ((p.lda & 15) == 0) && (((uintptr_t)p.A & 15) == 0);
-  const bool alB = ((p.ldb & 15) == 0) && (((uintptr_t)p.B & 15) == 0);
-  const int64_t nk = (kend - kbeg + BK - 1) / BK;
-
-  uint32_t offA[C::A_CHUNKS], offB[C::B_CHUNKS];
-  if constexpr (FAST) {
-#pragma unroll
-    for (int i = 0; i < C::A_CHUNKS; ++i) {
-      const int c = tid + C::THREADS * i;
-      const int64_t r = (m0 + c / KCH < p.M) ? m0 + c / KCH : p.M - 1;
-      offA[i] = (uint32_t)(r * p.lda) + 16u * (uint32_t)(c % KCH);
-    }
-#pragma unroll
-    for (int i = 0; i < C::B_CHUNKS; ++i) {
-      const int c = tid + C::THREADS * i;
-      const int64_t r = (n0 + c / KCH < p.N) ? n0 + c / KCH : p.N - 1;
-      offB[i] = (uint32_t)(r * p.ldb) + 16u * (uint32_t)(c % KCH);
-    }
-  }
-  const int8_t* Ak = p.A + kbeg;
-  const int8_t* Bk = p.B + kbeg;
-
-  // Two register staging sets: the loads of stage t + 1 are issued one
-  // iteration before the stage is stored to LDS, so each global load has two
-  // iterations of matrix-core work to land.
-  struct Stage {
-    u32x4v a[C::A_CHUNKS];
-    u32x4v b[C::B_CHUNKS];
-  };
-  Stage st0, st1;
-  auto gload = [&](Stage& st, int64_t t) __attribute__((always_inline)) {
-    if constexpr (FAST) {
-      const int8_t* a = Ak + t * BK;
-      const int8_t* b = Bk + t * BK;
-#pragma unroll
-      for (int i = 0; i < C::A_CHUNKS; ++i) st.a[i] = *reinterpret_cast<const u32x4v*>(a + offA[i]);
-#pragma unroll
-      for (int i = 0; i < C::B_CHUNKS; ++i) st.b[i] = *reinterpret_cast<const u32x4v*>(b + offB[i]);
-    } else {
-      const int64_t k0 = kbeg + t * BK;
-#pragma unroll
-      for (int i = 0; i < C::A_CHUNKS; ++i) {
-        const int c = tid + C::THREADS * i;
-        const Chunk16 v = load_chunk(p.A, p.lda, m0 + c / KCH, p.M, k0 + 16 * (c % KCH), kend, alA);
-        st.a[i] = u32x4v{v.w[0], v.w[1], v.w[2], v.w[3]};
-      }
-#pragma unroll
-      for (int i = 0; i < C::B_CHUNKS; ++i) {
-        const int c = tid + C::THREADS * i;
-        const Chunk16 v = load_chunk(p.B, p.ldb, n0 + c / KCH, p.N, k0 + 16 * (c % KCH), kend, alB);
-        st.b[i] = u32x4v{v.w[0], v.w[1], v.w[2], v.w[3]};
-      }
-    }
-  };
-  auto sstore = [&](const Stage& st, int buf) __attribute__((always_inline)) {
-#pragma unroll
-    for (int i = 0; i < C::A_CHUNKS; ++i) {
-      const int c = tid + C::THREADS * i;
-      *reinterpret_cast<u32x4v*>(&sA[buf * C::BM * LDS_STRIDE + (c / KCH) * LDS_STRIDE + 16 * (c % KCH)]) = st.a[i];
-    }
-#pragma unroll
-    for (int i = 0; i < C::B_CHUNKS; ++i) {
-      const int c = tid + C::THREADS * i;
-      *reinterpret_cast<u32x4v*>(&sB[buf * C::BN * LDS_STRIDE + (c / KCH) * LDS_STRIDE + 16 * (c % KCH)]) = st.b[i];
-    }
-  };
-  const int lrow = lane & 31;
-  const int lk = 16 * (lane >> 5);
-  const int8_t* a_lane = sA + (wm * C::WM + lrow) * LDS_STRIDE + lk;
-  const int8_t* b_lane = sB + (wn * C::WN + lrow) * LDS_STRIDE + lk;
-  auto compute = [&](int buf) __attribute__((always_inline)) {
-    const int8_t* a_base = a_lane + buf * C::BM * LDS_STRIDE;
-    const int8_t* b_base = b_lane + buf * C::BN * LDS_STRIDE;
-#pragma unroll
-    for (int kk = 0; kk < BK / 32; ++kk) {
-      v4i a[C::IT], b[C::JT];
-#pragma unroll
-      for (int i = 0; i < C::IT; ++i) a[i] = *reinterpret_cast<const v4i*>(a_base + i * 32 * LDS_STRIDE + kk * 32);
-#pragma unroll
-      for (int j = 0; j < C::JT; ++j) b[j] = *reinterpret_cast<const v4i*>(b_base + j * 32 * LDS_STRIDE + kk * 32);
-#pragma unroll
-      for (int i = 0; i < C::IT; ++i)
-#pragma unroll
-        for (int j = 0; j < C::JT; ++j) acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a[i], b[j], acc[i][j], 0, 0, 0);
-    }
-  };
-  // iteration t: LDS buffer t % 2 holds stage t; the register set (t + 1) % 2
-  // holds the in-flight loads of stage t + 1; stage t + 2 is loaded into the
-  // set that stage t came from.
-  auto iter = [&](int64_t t, int buf, Stage& next, Stage& far) __attribute__((always_inline)) {
-    if (t + 2 < nk) gload(far, t + 2);
-    compute(buf);
-    if (t + 1 < nk) sstore(next, buf ^ 1);
-    __syncthreads();
-  };
-  if (nk > 0) {
-    gload(st0, 0);
-    sstore(st0, 0);
-  }
-  if (nk > 1) gload(st1, 1);
-  __syncthreads();
-  int64_t t = 0;
-  for (; t + 1 < nk; t += 2) {
-    iter(t, 0, st1, st0);
-    iter(t + 1, 1, st0, st1);
-  }
-  if (t < nk) iter(t, 0, st1, st0);
-}
 
 template <class C, int EPI, int KG, bool FAST>
 __global__ __launch_bounds__(C::THREADS) void gemm_i8_kernel(GemmParams p) {
@@ -239,7 +57,8 @@ __global__ __launch_bounds__(C::THREADS) void gemm_i8_kernel(GemmParams p) {
   for (int i = 0; i < C::IT; ++i)
 #pragma unroll
     for (int j = 0; j < C::JT; ++j) acc[i][j] = v16i{0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0};
-  gemm_mainloop<C, FAST>(p, lds, m0, n0, kbeg, kend, acc);
+  const PlainALoader aload{p.A, p.lda, p.M, kend, ((p.lda & 15) == 0) && (((uintptr_t)p.A & 15) == 0)};
+  gemm_mainloop<C, FAST>(p, aload, lds, m0, n0, kbeg, kend, acc);
 
   // ---- epilogue.  Accumulator (i, j, r) of lane l holds
   //   row = wm*WM + i*32 + 8*(r/4) + 4*(l/32) + r%4,  col = wn*WN + j*32 + l%32
