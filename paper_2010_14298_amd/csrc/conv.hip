@@ -391,50 +391,56 @@ __global__ __launch_bounds__(256) void conv_gradx_kernel(GemmParams p, ConvGeom 
     srow[rr] = q;
   }
   __syncthreads();
-  constexpr int RUNS = C::THREADS / C::BN;
-  constexpr int RUN = C::BM / RUNS;  // 64 rows: the slots of one input pixel (npad % 64 == 0)
+  // Thread t owns column t % BN and the 64-row runs t / BN, t / BN + THREADS / BN, ...
+  // A run is 64 rows: the slots of one input pixel (npad % 64 == 0), so every
+  // group (KG <= 64, aligned) lies inside one.
+  static_assert(C::BM % 64 == 0 && KG <= 64, "64-row epilogue runs");
+  constexpr int NRUN = C::BM / 64;
+  constexpr int RSTEP = C::THREADS / C::BN;
   const int c = tid % C::BN;
-  const int rbase = (tid / C::BN) * RUN;
   const int64_t col = n0 + c;
   if (col >= p.N) return;
   const double kz = (double)g.o * zW;
-  if constexpr (EPI == EPI_BHQ && KG > 1) {
-    for (int g0 = rbase; g0 < rbase + RUN; g0 += KG) {
-      const ConvRowStage& q0 = srow[g0];
-      if (q0.orow < 0 && q0.kind == 0) continue;
-      const int pix = q0.pix;
-      const double colterm = dW * (double)ct[(int64_t)pix * g.c + col] + (double)cnt[pix] * kz;
-      double S = 0.0, T0 = 0.0;
-      for (int t = 0; t < KG; ++t) {
-        const ConvRowStage& q = srow[g0 + t];
-        const double T = dW * (double)sacc[(g0 + t) * C::BN + c] + (q.rterm + q.hz * colterm);
-        if (q.kind != 0) S += T;
-        if (t == 0) T0 = T;
-      }
-      const double alpha = q0.kind == 2 ? p.L.inv_sk_p : p.L.inv_sk_k;
-      const double tau = (alpha * S - T0) / (1.0 - alpha);
-      for (int t = 0; t < KG; ++t) {
-        const ConvRowStage& q = srow[g0 + t];
-        if (q.orow < 0) continue;
-        const double a = (double)sacc[(g0 + t) * C::BN + c];
-        double v;
-        if (q.kind != 0) {
-          const double T = dW * a + (q.rterm + q.hz * colterm);
-          const double Z = (t == 0) ? T + (1.0 - alpha) * tau : T - alpha * tau;
-          v = Z * q.dq;
-        } else {
-          v = q.dq * (dW * a + q.rterm) + q.hz * colterm;
+  for (int run = tid / C::BN; run < NRUN; run += RSTEP) {
+    const int rbase = run * 64;
+    if constexpr (EPI == EPI_BHQ && KG > 1) {
+      for (int g0 = rbase; g0 < rbase + 64; g0 += KG) {
+        const ConvRowStage& q0 = srow[g0];
+        if (q0.orow < 0 && q0.kind == 0) continue;
+        const int pix = q0.pix;
+        const double colterm = dW * (double)ct[(int64_t)pix * g.c + col] + (double)cnt[pix] * kz;
+        double S = 0.0, T0 = 0.0;
+        for (int t = 0; t < KG; ++t) {
+          const ConvRowStage& q = srow[g0 + t];
+          const double T = dW * (double)sacc[(g0 + t) * C::BN + c] + (q.rterm + q.hz * colterm);
+          if (q.kind != 0) S += T;
+          if (t == 0) T0 = T;
         }
-        p.out[(int64_t)q.orow * p.ldo + col] = (float)v;
+        const double alpha = q0.kind == 2 ? p.L.inv_sk_p : p.L.inv_sk_k;
+        const double tau = (alpha * S - T0) / (1.0 - alpha);
+        for (int t = 0; t < KG; ++t) {
+          const ConvRowStage& q = srow[g0 + t];
+          if (q.orow < 0) continue;
+          const double a = (double)sacc[(g0 + t) * C::BN + c];
+          double v;
+          if (q.kind != 0) {
+            const double T = dW * a + (q.rterm + q.hz * colterm);
+            const double Z = (t == 0) ? T + (1.0 - alpha) * tau : T - alpha * tau;
+            v = Z * q.dq;
+          } else {
+            v = q.dq * (dW * a + q.rterm) + q.hz * colterm;
+          }
+          p.out[(int64_t)q.orow * p.ldo + col] = (float)v;
+        }
       }
-    }
-  } else {
-    for (int t = rbase; t < rbase + RUN; ++t) {
-      const ConvRowStage& q = srow[t];
-      if (q.orow < 0) continue;
-      const double colterm = dW * (double)ct[(int64_t)q.pix * g.c + col] + (double)cnt[q.pix] * kz;
-      const double a = (double)sacc[t * C::BN + c];
-      p.out[(int64_t)q.orow * p.ldo + col] = (float)(q.dq * (dW * a + q.rterm) + q.hz * colterm);
+    } else {
+      for (int t = rbase; t < rbase + 64; ++t) {
+        const ConvRowStage& q = srow[t];
+        if (q.orow < 0) continue;
+        const double colterm = dW * (double)ct[(int64_t)q.pix * g.c + col] + (double)cnt[q.pix] * kz;
+        const double a = (double)sacc[t * C::BN + c];
+        p.out[(int64_t)q.orow * p.ldo + col] = (float)(q.dq * (dW * a + q.rterm) + q.hz * colterm);
+      }
     }
   }
 }

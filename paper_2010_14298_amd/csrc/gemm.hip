@@ -131,48 +131,53 @@ __global__ __launch_bounds__(C::THREADS) void gemm_i8_kernel(GemmParams p) {
       srow[rr] = q;
     }
     __syncthreads();
-    constexpr int RUNS = C::THREADS / C::BN;      // row runs per column
-    constexpr int RUN = C::BM / RUNS;             // rows per run (multiple of 64)
+    // Thread t owns column t % BN and the 64-row runs t / BN, t / BN + THREADS / BN, ...
+    // A run is 64 rows, so every group (KG <= 64, aligned) lies inside one.
+    static_assert(C::BM % 64 == 0 && KG <= 64, "64-row epilogue runs");
+    constexpr int NRUN = C::BM / 64;
+    constexpr int RSTEP = C::THREADS / C::BN;
     const int c = tid % C::BN;
-    const int rbase = (tid / C::BN) * RUN;
     const int64_t col = n0 + c;
     if (col >= p.N) return;
     // sum over K of the dequantized weight column: dW * sum q_W + K zW
     const double colterm = dW * (double)p.sumB[col] + (double)p.K * zW;
-    if constexpr (EPI == EPI_BHQ && KG > 1) {
-      for (int g0 = rbase; g0 < rbase + RUN; g0 += KG) {
-        // T_p = (code_p + c_g) . W~ ; S = sum over the group's multi-row slots
-        double S = 0.0, T0 = 0.0;
-        for (int t = 0; t < KG; ++t) {
-          const RowStage& q = srow[g0 + t];
-          const double T = dW * (double)sacc[(g0 + t) * C::BN + c] + (q.rterm + q.hz * colterm);
-          if (q.kind != 0) S += T;
-          if (t == 0) T0 = T;
-        }
-        const int gkind = srow[g0].kind;
-        const double alpha = gkind == 2 ? p.L.inv_sk_p : p.L.inv_sk_k;
-        const double tau = (alpha * S - T0) / (1.0 - alpha);
-        for (int t = 0; t < KG; ++t) {
-          const RowStage& q = srow[g0 + t];
-          if (q.orow < 0) continue;
-          const double a = (double)sacc[(g0 + t) * C::BN + c];
-          double v;
-          if (q.kind != 0) {
-            const double T = dW * a + (q.rterm + q.hz * colterm);
-            const double Z = (t == 0) ? T + (1.0 - alpha) * tau : T - alpha * tau;
-            v = Z * q.dq;
-          } else {
-            v = q.dq * (dW * a + q.rterm) + q.hz * colterm;
+    for (int run = tid / C::BN; run < NRUN; run += RSTEP) {
+      const int rbase = run * 64;
+      if constexpr (EPI == EPI_BHQ && KG > 1) {
+        for (int g0 = rbase; g0 < rbase + 64; g0 += KG) {
+          // T_p = (code_p + c_g) . W~ ; S = sum over the group's multi-row slots
+          double S = 0.0, T0 = 0.0;
+          for (int t = 0; t < KG; ++t) {
+            const RowStage& q = srow[g0 + t];
+            const double T = dW * (double)sacc[(g0 + t) * C::BN + c] + (q.rterm + q.hz * colterm);
+            if (q.kind != 0) S += T;
+            if (t == 0) T0 = T;
           }
-          p.out[(int64_t)q.orow * p.ldo + col] = (float)v;
+          const int gkind = srow[g0].kind;
+          const double alpha = gkind == 2 ? p.L.inv_sk_p : p.L.inv_sk_k;
+          const double tau = (alpha * S - T0) / (1.0 - alpha);
+          for (int t = 0; t < KG; ++t) {
+            const RowStage& q = srow[g0 + t];
+            if (q.orow < 0) continue;
+            const double a = (double)sacc[(g0 + t) * C::BN + c];
+            double v;
+            if (q.kind != 0) {
+              const double T = dW * a + (q.rterm + q.hz * colterm);
+              const double Z = (t == 0) ? T + (1.0 - alpha) * tau : T - alpha * tau;
+              v = Z * q.dq;
+            } else {
+              v = q.dq * (dW * a + q.rterm) + q.hz * colterm;
+            }
+            p.out[(int64_t)q.orow * p.ldo + col] = (float)v;
+          }
         }
-      }
-    } else {
-      for (int t = rbase; t < rbase + RUN; ++t) {
-        const RowStage& q = srow[t];
-        if (q.orow < 0) continue;
-        const double a = (double)sacc[t * C::BN + c];
-        p.out[(int64_t)q.orow * p.ldo + col] = (float)(q.dq * (dW * a + q.rterm) + q.hz * colterm);
+      } else {
+        for (int t = rbase; t < rbase + 64; ++t) {
+          const RowStage& q = srow[t];
+          if (q.orow < 0) continue;
+          const double a = (double)sacc[t * C::BN + c];
+          p.out[(int64_t)q.orow * p.ldo + col] = (float)(q.dq * (dW * a + q.rterm) + q.hz * colterm);
+        }
       }
     }
   }
@@ -220,7 +225,7 @@ static hipError_t launch_gemm_t(GemmParams p, hipStream_t s) {
   const int64_t tiles = gemm_tiles<C>(p.M, p.N);
   if (tiles > 0x7FFFFFFF || p.splits > 65535) return hipErrorInvalidValue;
   // fast K loop: aligned rows, whole stages per split, 32-bit offsets
-  const bool whole = (p.kchunk % BK == 0) && (p.K % BK == 0);
+  const bool whole = (p.kchunk % C::BK == 0) && (p.K % C::BK == 0);
   const bool fast = ((p.lda & 15) == 0) && ((p.ldb & 15) == 0) && (((uintptr_t)p.A & 15) == 0) &&
                     (((uintptr_t)p.B & 15) == 0) && whole && (p.M * p.lda < ((int64_t)1 << 32)) &&
                     (p.N * p.ldb < ((int64_t)1 << 32));

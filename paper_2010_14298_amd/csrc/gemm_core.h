@@ -12,14 +12,15 @@ namespace fqt {
 typedef int v4i __attribute__((ext_vector_type(4)));
 typedef int v16i __attribute__((ext_vector_type(16)));
 
-constexpr int BK = 128;          // K bytes per pipeline stage
-constexpr int KCH = BK / 16;     // 16-byte chunks per row per stage
-constexpr int LDS_STRIDE = 144;  // bytes per tile row in LDS: 128 + 16 (conflict-free 8- and 16-lane phases)
 constexpr int NUM_XCD = 8;
 
-template <int BM_, int BN_, int WM_, int WN_>
+// Block tile BM x BN, wave tile WM x WN, BK_ K bytes per pipeline stage.
+// LDS rows are padded by 16 bytes (conflict-free 8- and 16-lane phases).
+template <int BM_, int BN_, int WM_, int WN_, int BK_ = 128>
 struct TileCfg {
-  static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_;
+  static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_, BK = BK_;
+  static constexpr int KCH = BK / 16;          // 16-byte chunks per row per stage
+  static constexpr int LDS_STRIDE = BK + 16;
   static constexpr int WAVES_N = BN / WN;
   static constexpr int THREADS = (BM / WM) * (BN / WN) * 64;
   static constexpr int IT = WM / 32, JT = WN / 32;
@@ -27,8 +28,9 @@ struct TileCfg {
   static constexpr int B_CHUNKS = BN * KCH / THREADS;
   static constexpr int OP_BYTES = 2 * (BM + BN) * LDS_STRIDE;
 };
-using CfgLarge = TileCfg<256, 128, 128, 64>;
-using CfgSmall = TileCfg<128, 128, 64, 64>;
+// Configurations measured best on MI355X for the layer shapes (8 waves each).
+using CfgLarge = TileCfg<256, 128, 64, 64, 128>;
+using CfgSmall = TileCfg<128, 128, 32, 64, 128>;
 
 typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
 struct alignas(16) Chunk16 {
@@ -87,28 +89,28 @@ struct PlainALoader {
 template <class C, bool FAST, class ALoader>
 __device__ __forceinline__ void gemm_mainloop(const GemmParams& p, const ALoader& aload, int8_t* lds, int64_t m0,
                                               int64_t n0, int64_t kbeg, int64_t kend, v16i (&acc)[C::IT][C::JT]) {
-  int8_t* sA = lds;                          // [2][BM * LDS_STRIDE]
-  int8_t* sB = lds + 2 * C::BM * LDS_STRIDE;  // [2][BN * LDS_STRIDE]
+  int8_t* sA = lds;                          // [2][BM * C::LDS_STRIDE]
+  int8_t* sB = lds + 2 * C::BM * C::LDS_STRIDE;  // [2][BN * C::LDS_STRIDE]
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
   const int wm = wave / C::WAVES_N, wn = wave % C::WAVES_N;
   const bool alB = ((p.ldb & 15) == 0) && (((uintptr_t)p.B & 15) == 0);
-  const int64_t nk = (kend - kbeg + BK - 1) / BK;
+  const int64_t nk = (kend - kbeg + C::BK - 1) / C::BK;
 
   uint32_t offA[C::A_CHUNKS], offB[C::B_CHUNKS];
   if constexpr (FAST) {
 #pragma unroll
     for (int i = 0; i < C::A_CHUNKS; ++i) {
       const int c = tid + C::THREADS * i;
-      const int64_t r = (m0 + c / KCH < p.M) ? m0 + c / KCH : p.M - 1;
-      offA[i] = (uint32_t)(r * p.lda) + 16u * (uint32_t)(c % KCH);
+      const int64_t r = (m0 + c / C::KCH < p.M) ? m0 + c / C::KCH : p.M - 1;
+      offA[i] = (uint32_t)(r * p.lda) + 16u * (uint32_t)(c % C::KCH);
     }
 #pragma unroll
     for (int i = 0; i < C::B_CHUNKS; ++i) {
       const int c = tid + C::THREADS * i;
-      const int64_t r = (n0 + c / KCH < p.N) ? n0 + c / KCH : p.N - 1;
-      offB[i] = (uint32_t)(r * p.ldb) + 16u * (uint32_t)(c % KCH);
+      const int64_t r = (n0 + c / C::KCH < p.N) ? n0 + c / C::KCH : p.N - 1;
+      offB[i] = (uint32_t)(r * p.ldb) + 16u * (uint32_t)(c % C::KCH);
     }
   }
   const int8_t* Ak = p.A + kbeg;
@@ -124,24 +126,24 @@ __device__ __forceinline__ void gemm_mainloop(const GemmParams& p, const ALoader
   Stage st0, st1;
   auto gload = [&](Stage& st, int64_t t) __attribute__((always_inline)) {
     if constexpr (FAST) {
-      const int8_t* a = Ak + t * BK;
-      const int8_t* b = Bk + t * BK;
+      const int8_t* a = Ak + t * C::BK;
+      const int8_t* b = Bk + t * C::BK;
 #pragma unroll
       for (int i = 0; i < C::A_CHUNKS; ++i) st.a[i] = *reinterpret_cast<const u32x4v*>(a + offA[i]);
 #pragma unroll
       for (int i = 0; i < C::B_CHUNKS; ++i) st.b[i] = *reinterpret_cast<const u32x4v*>(b + offB[i]);
     } else {
-      const int64_t k0 = kbeg + t * BK;
+      const int64_t k0 = kbeg + t * C::BK;
 #pragma unroll
       for (int i = 0; i < C::A_CHUNKS; ++i) {
         const int c = tid + C::THREADS * i;
-        const Chunk16 v = aload(m0 + c / KCH, k0 + 16 * (c % KCH));
+        const Chunk16 v = aload(m0 + c / C::KCH, k0 + 16 * (c % C::KCH));
         st.a[i] = u32x4v{v.w[0], v.w[1], v.w[2], v.w[3]};
       }
 #pragma unroll
       for (int i = 0; i < C::B_CHUNKS; ++i) {
         const int c = tid + C::THREADS * i;
-        const Chunk16 v = load_chunk(p.B, p.ldb, n0 + c / KCH, p.N, k0 + 16 * (c % KCH), kend, alB);
+        const Chunk16 v = load_chunk(p.B, p.ldb, n0 + c / C::KCH, p.N, k0 + 16 * (c % C::KCH), kend, alB);
         st.b[i] = u32x4v{v.w[0], v.w[1], v.w[2], v.w[3]};
       }
     }
@@ -150,28 +152,28 @@ __device__ __forceinline__ void gemm_mainloop(const GemmParams& p, const ALoader
 #pragma unroll
     for (int i = 0; i < C::A_CHUNKS; ++i) {
       const int c = tid + C::THREADS * i;
-      *reinterpret_cast<u32x4v*>(&sA[buf * C::BM * LDS_STRIDE + (c / KCH) * LDS_STRIDE + 16 * (c % KCH)]) = st.a[i];
+      *reinterpret_cast<u32x4v*>(&sA[buf * C::BM * C::LDS_STRIDE + (c / C::KCH) * C::LDS_STRIDE + 16 * (c % C::KCH)]) = st.a[i];
     }
 #pragma unroll
     for (int i = 0; i < C::B_CHUNKS; ++i) {
       const int c = tid + C::THREADS * i;
-      *reinterpret_cast<u32x4v*>(&sB[buf * C::BN * LDS_STRIDE + (c / KCH) * LDS_STRIDE + 16 * (c % KCH)]) = st.b[i];
+      *reinterpret_cast<u32x4v*>(&sB[buf * C::BN * C::LDS_STRIDE + (c / C::KCH) * C::LDS_STRIDE + 16 * (c % C::KCH)]) = st.b[i];
     }
   };
   const int lrow = lane & 31;
   const int lk = 16 * (lane >> 5);
-  const int8_t* a_lane = sA + (wm * C::WM + lrow) * LDS_STRIDE + lk;
-  const int8_t* b_lane = sB + (wn * C::WN + lrow) * LDS_STRIDE + lk;
+  const int8_t* a_lane = sA + (wm * C::WM + lrow) * C::LDS_STRIDE + lk;
+  const int8_t* b_lane = sB + (wn * C::WN + lrow) * C::LDS_STRIDE + lk;
   auto compute = [&](int buf) __attribute__((always_inline)) {
-    const int8_t* a_base = a_lane + buf * C::BM * LDS_STRIDE;
-    const int8_t* b_base = b_lane + buf * C::BN * LDS_STRIDE;
+    const int8_t* a_base = a_lane + buf * C::BM * C::LDS_STRIDE;
+    const int8_t* b_base = b_lane + buf * C::BN * C::LDS_STRIDE;
 #pragma unroll
-    for (int kk = 0; kk < BK / 32; ++kk) {
+    for (int kk = 0; kk < C::BK / 32; ++kk) {
       v4i a[C::IT], b[C::JT];
 #pragma unroll
-      for (int i = 0; i < C::IT; ++i) a[i] = *reinterpret_cast<const v4i*>(a_base + i * 32 * LDS_STRIDE + kk * 32);
+      for (int i = 0; i < C::IT; ++i) a[i] = *reinterpret_cast<const v4i*>(a_base + i * 32 * C::LDS_STRIDE + kk * 32);
 #pragma unroll
-      for (int j = 0; j < C::JT; ++j) b[j] = *reinterpret_cast<const v4i*>(b_base + j * 32 * LDS_STRIDE + kk * 32);
+      for (int j = 0; j < C::JT; ++j) b[j] = *reinterpret_cast<const v4i*>(b_base + j * 32 * C::LDS_STRIDE + kk * 32);
 #pragma unroll
       for (int i = 0; i < C::IT; ++i)
 #pragma unroll
