@@ -22,6 +22,7 @@ HIP_FLAGS = [
     "--offload-arch=" + ARCH,
     "-ffp-contract=off",
     "-mllvm", "-disable-promote-alloca-to-lds",
+    "-mllvm", "-pragma-unroll-threshold=200000",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-Wall", "-Wno-unused-function",
 ]

@@ -473,7 +473,38 @@ __device__ __forceinline__ uint32_t pack4(int a, int b, int c, int d) {
   return (uint32_t)(a & 255) | ((uint32_t)(b & 255) << 8) | ((uint32_t)(c & 255) << 16) | ((uint32_t)(d & 255) << 24);
 }
 
-template <int MODE, int K, bool HAS2>
+// Codes of four consecutive columns of one row from transformed values y:
+// stochastic rounding with the Philox block of element e0 (VEC: e0 % 4 == 0,
+// one block for all four) or round-half-even.
+template <bool VEC>
+__device__ __forceinline__ void round4(const float (&y)[4], uint64_t e0, int stoch, uint64_t seed, uint32_t stream,
+                                       int B, int (&code)[4]) {
+  if (stoch) {
+    if constexpr (VEC) {
+      const u32x4 o = philox_block(e0, seed, stream);
+      code[0] = sr_code(y[0], o.x, B);
+      code[1] = sr_code(y[1], o.y, B);
+      code[2] = sr_code(y[2], o.z, B);
+      code[3] = sr_code(y[3], o.w, B);
+    } else {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const uint64_t e = e0 + j;
+        const u32x4 o = philox_block(e, seed, stream);
+        code[j] = sr_code(y[j], philox_word(o, (int)(e & 3)), B);
+      }
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) code[j] = rne_code(y[j], B);
+  }
+}
+
+// Tile = 64 slots x 256 columns; 4 waves of 16 slots; 4 columns per lane.
+// The loaded tile stays in registers; each row is then finished in one step
+// (transform, both quantizers, packing, code sums) so its data dies early.
+// VEC: cols % 4 == 0 (float4 loads, one Philox block per lane and row).
+template <int MODE, int K, bool HAS2, bool VEC>
 __global__ __launch_bounds__(256) void quant_tile_kernel(QuantParams p) {
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
@@ -481,9 +512,9 @@ __global__ __launch_bounds__(256) void quant_tile_kernel(QuantParams p) {
   const int64_t slot0 = tile0 + wave * QT_ROWS_PER_WAVE;
   const int64_t c0 = (int64_t)blockIdx.x * QT_COLS + lane * 4;
   const int64_t rows = p.rows, cols = p.cols;
-  const bool vec = (cols & 3) == 0;
   const int B = (1 << p.bits) - 1;
   const int half = 1 << (p.bits - 1);
+  const bool lane_ok = c0 < cols;
 
   __shared__ float s_part[4][QT_COLS];   // per-wave partial group sums (BHQ, K >= 16)
   __shared__ float s_v0[4][QT_COLS];     // v of a group's first slot (BHQ, K >= 16)
@@ -499,184 +530,146 @@ __global__ __launch_bounds__(256) void quant_tile_kernel(QuantParams p) {
     const int32_t row = ok ? (p.perm ? p.perm[slot] : (int32_t)slot) : 0;
     srow[r] = row;
     const float* xr = p.x + (int64_t)row * cols;
-    if (ok && vec && c0 + 3 < cols) {
-      const float4 v = *reinterpret_cast<const float4*>(xr + c0);
-      g[r][0] = v.x;
-      g[r][1] = v.y;
-      g[r][2] = v.z;
-      g[r][3] = v.w;
+    if constexpr (VEC) {
+      if (ok && lane_ok) {
+        const float4 v = *reinterpret_cast<const float4*>(xr + c0);
+        g[r][0] = v.x;
+        g[r][1] = v.y;
+        g[r][2] = v.z;
+        g[r][3] = v.w;
+      } else {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) g[r][j] = 0.0f;
+      }
     } else {
 #pragma unroll
       for (int j = 0; j < 4; ++j) g[r][j] = (ok && c0 + j < cols) ? xr[c0 + j] : 0.0f;
     }
   }
 
-  // ---- primary transformed values y (in place in g -> y)
-  float y[QT_ROWS_PER_WAVE][4];
-  if constexpr (MODE == QM_TENSOR || MODE == QM_ROW) {
-    const float s_t = p.scale[0], z_t = p.zero[0];
-#pragma unroll
-    for (int r = 0; r < QT_ROWS_PER_WAVE; ++r) {
-      const int64_t slot = slot0 + r;
-      const bool ok = slot < rows;
-      const float s = (MODE == QM_ROW) ? (ok ? p.scale[slot] : 1.0f) : s_t;
-      const float z = (MODE == QM_ROW) ? (ok ? p.zero[slot] : 0.0f) : z_t;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) y[r][j] = s * (g[r][j] - z);
-    }
-  } else {
-    // block Householder: v = d * g; group sums; Y = v - alpha tau (first
-    // slot: v + (1 - alpha) tau); y' = Y - c_g.  One-row groups use the
-    // per-sample map s (g - z).
+  // ---- block Householder (K >= 16): the group's column sums span waves
+  float ta[4] = {0.0f, 0.0f, 0.0f, 0.0f}, tb[4] = {0.0f, 0.0f, 0.0f, 0.0f};  // alpha tau, (1 - alpha) tau
+  if constexpr (MODE == QM_BHQ && K >= 16) {
     const BhqLayout& L = p.L;
-    float v[QT_ROWS_PER_WAVE][4];
-    int kind[QT_ROWS_PER_WAVE];
+    float P[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    float v0[4] = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
     for (int r = 0; r < QT_ROWS_PER_WAVE; ++r) {
       const int64_t slot = slot0 + r;
       const bool ok = slot < rows;
-      kind[r] = ok ? bhq_slot_kind(L, slot) : 0;
+      const bool multi = ok && bhq_slot_kind(L, slot) != 0;
       const float d = ok ? p.scale[slot] : 1.0f;
 #pragma unroll
-      for (int j = 0; j < 4; ++j) v[r][j] = d * g[r][j];
+      for (int j = 0; j < 4; ++j) {
+        const float v = d * g[r][j];
+        P[j] = P[j] + (multi ? v : 0.0f);
+        if (r == 0) v0[j] = v;
+      }
     }
-    if constexpr (K >= 16) {
-      // per-wave partial sums over the wave's 16 slots, slot order
-      float P[4] = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-      for (int r = 0; r < QT_ROWS_PER_WAVE; ++r)
+    for (int j = 0; j < 4; ++j) {
+      s_part[wave][lane * 4 + j] = P[j];
+      s_v0[wave][lane * 4 + j] = v0[j];
+    }
+    __syncthreads();
+    const int nw = K / 16;                // waves per group
+    const int w0 = (wave / nw) * nw;      // first wave of this wave's group
+    const int64_t gfirst = tile0 + w0 * 16;
+    const int gkind = gfirst < rows ? bhq_slot_kind(L, gfirst) : 0;
+    const float alpha = gkind == 2 ? L.a_p : L.a_k;
+    const float oma = gkind == 2 ? L.oma_p : L.oma_k;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) P[j] = P[j] + (kind[r] != 0 ? v[r][j] : 0.0f);
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        s_part[wave][lane * 4 + j] = P[j];
-        s_v0[wave][lane * 4 + j] = v[0][j];
-      }
-      __syncthreads();
-      const int nw = K / 16;                       // waves per group
-      const int w0 = (wave / nw) * nw;             // first wave of this wave's group
-      float S[4], v0[4];
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        S[j] = s_part[w0][lane * 4 + j];
-        for (int i = 1; i < nw; ++i) S[j] = S[j] + s_part[w0 + i][lane * 4 + j];
-        v0[j] = s_v0[w0][lane * 4 + j];
-      }
-      // the group's first slot decides full / partial (one-row slots skip)
-      const int64_t gfirst = tile0 + w0 * 16;
-      const int gkind = gfirst < rows ? bhq_slot_kind(L, gfirst) : 0;
-      const float alpha = gkind == 2 ? L.a_p : L.a_k;
-      const float oma = gkind == 2 ? L.oma_p : L.oma_k;
-      float tau[4];
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const float m = alpha * S[j] - v0[j];
-        tau[j] = __fdiv_rn(m, oma);
-      }
-#pragma unroll
-      for (int r = 0; r < QT_ROWS_PER_WAVE; ++r) {
-        const int64_t slot = slot0 + r;
-        const bool ok = slot < rows;
-        const float c = ok ? p.zero[slot] : 0.0f;
-        const bool first = (slot % K) == 0;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          if (kind[r] != 0) {
-            const float Y = first ? v[r][j] + oma * tau[j] : v[r][j] - alpha * tau[j];
-            y[r][j] = Y - c;
-          } else {
-            const float s = ok ? p.scale[slot] : 1.0f;
-            y[r][j] = s * (g[r][j] - c);
-          }
-        }
-      }
-    } else {
-      // K < 16: each group lies inside this wave's 16 slots
-      static_assert(K >= 1 && K < 16, "block size");
-#pragma unroll
-      for (int gi = 0; gi < QT_ROWS_PER_WAVE / K; ++gi) {
-        const int r0 = gi * K;
-        const int64_t gfirst = slot0 + r0;
-        const int gkind = (K > 1 && gfirst < rows) ? bhq_slot_kind(L, gfirst) : 0;
-        const float alpha = gkind == 2 ? L.a_p : L.a_k;
-        const float oma = gkind == 2 ? L.oma_p : L.oma_k;
-        float tau[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-        if constexpr (K > 1) {
-          float S[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-          for (int rr = 0; rr < K; ++rr)
-#pragma unroll
-            for (int j = 0; j < 4; ++j) S[j] = S[j] + (kind[r0 + rr] != 0 ? v[r0 + rr][j] : 0.0f);
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const float m = alpha * S[j] - v[r0][j];
-            tau[j] = __fdiv_rn(m, oma);
-          }
-        }
-#pragma unroll
-        for (int rr = 0; rr < K; ++rr) {
-          const int r = r0 + rr;
-          const int64_t slot = slot0 + r;
-          const bool ok = slot < rows;
-          const float c = ok ? p.zero[slot] : 0.0f;
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            if (K > 1 && kind[r] != 0) {
-              const float Y = rr == 0 ? v[r][j] + oma * tau[j] : v[r][j] - alpha * tau[j];
-              y[r][j] = Y - c;
-            } else {
-              const float s = ok ? p.scale[slot] : 1.0f;
-              y[r][j] = s * (g[r][j] - c);
-            }
-          }
-        }
-      }
+    for (int j = 0; j < 4; ++j) {
+      float S = s_part[w0][lane * 4 + j];
+      for (int i = 1; i < nw; ++i) S = S + s_part[w0 + i][lane * 4 + j];
+      const float m = alpha * S - s_v0[w0][lane * 4 + j];
+      const float tau = __fdiv_rn(m, oma);
+      ta[j] = alpha * tau;
+      tb[j] = oma * tau;
     }
   }
 
-  // ---- rounding, stores, code sums
-  const bool full_vec = vec && c0 + 3 < cols;
-  int csum[4] = {0, 0, 0, 0};
-  uint32_t tcodes[4][4];  // transposed: [column][4 words of 16 slots]
+  // ---- finish row by row
+  int csum[4] = {0, 0, 0, 0}, csum2[4] = {0, 0, 0, 0};
+  uint32_t tq[4][4], tq2[4][4];  // transposed codes: [column][4 words of 16 slots]
 #pragma unroll
   for (int j = 0; j < 4; ++j)
 #pragma unroll
-    for (int w = 0; w < 4; ++w) tcodes[j][w] = 0u;
-
+    for (int w = 0; w < 4; ++w) {
+      tq[j][w] = 0u;
+      tq2[j][w] = 0u;
+    }
+  const float s_t = (MODE == QM_TENSOR) ? p.scale[0] : 0.0f;
+  const float z_t = (MODE == QM_TENSOR) ? p.zero[0] : 0.0f;
 #pragma unroll
   for (int r = 0; r < QT_ROWS_PER_WAVE; ++r) {
     const int64_t slot = slot0 + r;
     const bool ok = slot < rows;
-    const uint64_t ebase = (uint64_t)srow[r] * (uint64_t)cols + (uint64_t)c0;
-    int code[4];
-    if (p.stoch) {
-      if (full_vec) {
-        const u32x4 o = philox_block(ebase, p.seed, p.stream);
-        code[0] = sr_code(y[r][0], o.x, B);
-        code[1] = sr_code(y[r][1], o.y, B);
-        code[2] = sr_code(y[r][2], o.z, B);
-        code[3] = sr_code(y[r][3], o.w, B);
-      } else {
+    float y[4];
+    if constexpr (MODE == QM_TENSOR) {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const uint64_t e = ebase + j;
-          const u32x4 o = philox_block(e, p.seed, p.stream);
-          code[j] = sr_code(y[r][j], philox_word(o, (int)(e & 3)), B);
+      for (int j = 0; j < 4; ++j) y[j] = s_t * (g[r][j] - z_t);
+    } else if constexpr (MODE == QM_ROW) {
+      const float s = ok ? p.scale[slot] : 1.0f;
+      const float z = ok ? p.zero[slot] : 0.0f;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) y[j] = s * (g[r][j] - z);
+    } else {
+      const BhqLayout& L = p.L;
+      const int kind = ok ? bhq_slot_kind(L, slot) : 0;
+      const float d = ok ? p.scale[slot] : 1.0f;
+      const float c = ok ? p.zero[slot] : 0.0f;
+      if constexpr (K > 1 && K < 16) {
+        // groups of K rows inside this wave: their sums from the registers
+        if (r % K == 0) {
+          const int64_t gfirst = slot;
+          const int gkind = (gfirst < rows) ? bhq_slot_kind(L, gfirst) : 0;
+          const float alpha = gkind == 2 ? L.a_p : L.a_k;
+          const float oma = gkind == 2 ? L.oma_p : L.oma_k;
+          float S[4] = {0.0f, 0.0f, 0.0f, 0.0f}, v0[4];
+#pragma unroll
+          for (int rr = 0; rr < K; ++rr) {
+            const int64_t sl = slot + rr;
+            const bool okr = sl < rows;
+            const bool multi = okr && bhq_slot_kind(L, sl) != 0;
+            const float dr = okr ? p.scale[sl] : 1.0f;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+              const float v = dr * g[r + rr][j];
+              S[j] = S[j] + (multi ? v : 0.0f);
+              if (rr == 0) v0[j] = v;
+            }
+          }
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const float m = alpha * S[j] - v0[j];
+            const float tau = __fdiv_rn(m, oma);
+            ta[j] = alpha * tau;
+            tb[j] = oma * tau;
+          }
         }
       }
-    } else {
+      const bool first = (K > 1) && ((slot % (K > 1 ? K : 1)) == 0);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) code[j] = rne_code(y[r][j], B);
+      for (int j = 0; j < 4; ++j) {
+        if (K > 1 && kind != 0) {
+          const float v = d * g[r][j];
+          const float Y = first ? v + tb[j] : v - ta[j];
+          y[j] = Y - c;
+        } else {
+          y[j] = d * (g[r][j] - c);
+        }
+      }
     }
+    const uint64_t e0 = (uint64_t)srow[r] * (uint64_t)cols + (uint64_t)c0;
+    int code[4];
+    round4<VEC>(y, e0, p.stoch, p.seed, p.stream, B, code);
     int q[4];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const bool cok = ok && (c0 + j < cols);
-      q[j] = cok ? code[j] - half : 0;
-    }
-    if (p.q_nat && ok) {
+    for (int j = 0; j < 4; ++j) q[j] = (ok && c0 + j < cols) ? code[j] - half : 0;
+    if (p.q_nat && ok && lane_ok) {
       int8_t* dst = p.q_nat + slot * cols + c0;
-      if (full_vec) {
+      if constexpr (VEC) {
         *reinterpret_cast<uint32_t*>(dst) = pack4(q[0], q[1], q[2], q[3]);
       } else {
 #pragma unroll
@@ -691,76 +684,50 @@ __global__ __launch_bounds__(256) void quant_tile_kernel(QuantParams p) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       csum[j] += q[j];
-      tcodes[j][r >> 2] |= (uint32_t)(q[j] & 255) << (8 * (r & 3));
+      tq[j][r >> 2] |= (uint32_t)(q[j] & 255) << (8 * (r & 3));
     }
-  }
-  if (p.q_t) {
-    const bool tvec = ((rows & 15) == 0) && (slot0 + 15 < rows);
+    if constexpr (HAS2) {
+      const int B2 = (1 << p.bits2) - 1;
+      const int half2 = 1 << (p.bits2 - 1);
+      const float s2 = p.scale2[0], z2 = p.zero2[0];
+      float y2[4];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int64_t col = c0 + j;
-      if (col >= cols) continue;
-      int8_t* dst = p.q_t + col * rows + slot0;
-      if (tvec) {
-        *reinterpret_cast<uint4*>(dst) = make_uint4(tcodes[j][0], tcodes[j][1], tcodes[j][2], tcodes[j][3]);
-      } else {
+      for (int j = 0; j < 4; ++j) y2[j] = s2 * (g[r][j] - z2);
+      int code2[4];
+      round4<VEC>(y2, e0, 1, p.seed, p.stream2, B2, code2);
 #pragma unroll
-        for (int r = 0; r < QT_ROWS_PER_WAVE; ++r)
-          if (slot0 + r < rows) dst[r] = (int8_t)((tcodes[j][r >> 2] >> (8 * (r & 3))) & 255);
+      for (int j = 0; j < 4; ++j) {
+        const int q2 = (ok && c0 + j < cols) ? code2[j] - half2 : 0;
+        csum2[j] += q2;
+        tq2[j][r >> 2] |= (uint32_t)(q2 & 255) << (8 * (r & 3));
       }
     }
   }
 
-  // ---- second quantizer (per tensor, stochastic, transposed) on the same rows
-  int csum2[4] = {0, 0, 0, 0};
-  if (HAS2) {
-    const int B2 = (1 << p.bits2) - 1;
-    const int half2 = 1 << (p.bits2 - 1);
-    const float s2 = p.scale2[0], z2 = p.zero2[0];
+  // ---- transposed stores: 16 consecutive slots per column
+  const bool tvec = ((rows & 15) == 0) && (slot0 + 15 < rows);
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
-#pragma unroll
-      for (int w = 0; w < 4; ++w) tcodes[j][w] = 0u;
-#pragma unroll
-    for (int r = 0; r < QT_ROWS_PER_WAVE; ++r) {
-      const int64_t slot = slot0 + r;
-      const bool ok = slot < rows;
-      const uint64_t ebase = (uint64_t)srow[r] * (uint64_t)cols + (uint64_t)c0;
-      int code[4];
-      if (full_vec) {
-        const u32x4 o = philox_block(ebase, p.seed, p.stream2);
-        code[0] = sr_code(s2 * (g[r][0] - z2), o.x, B2);
-        code[1] = sr_code(s2 * (g[r][1] - z2), o.y, B2);
-        code[2] = sr_code(s2 * (g[r][2] - z2), o.z, B2);
-        code[3] = sr_code(s2 * (g[r][3] - z2), o.w, B2);
-      } else {
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const uint64_t e = ebase + j;
-          const u32x4 o = philox_block(e, p.seed, p.stream2);
-          code[j] = sr_code(s2 * (g[r][j] - z2), philox_word(o, (int)(e & 3)), B2);
-        }
-      }
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const bool cok = ok && (c0 + j < cols);
-        const int q = cok ? code[j] - half2 : 0;
-        csum2[j] += q;
-        tcodes[j][r >> 2] |= (uint32_t)(q & 255) << (8 * (r & 3));
-      }
-    }
-    const bool tvec = ((rows & 15) == 0) && (slot0 + 15 < rows);
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int64_t col = c0 + j;
-      if (col >= cols) continue;
-      int8_t* dst = p.q2_t + col * rows + slot0;
+  for (int j = 0; j < 4; ++j) {
+    const int64_t col = c0 + j;
+    if (col >= cols) continue;
+    if (p.q_t) {
+      int8_t* dst = p.q_t + col * rows + slot0;
       if (tvec) {
-        *reinterpret_cast<uint4*>(dst) = make_uint4(tcodes[j][0], tcodes[j][1], tcodes[j][2], tcodes[j][3]);
+        *reinterpret_cast<uint4*>(dst) = make_uint4(tq[j][0], tq[j][1], tq[j][2], tq[j][3]);
       } else {
 #pragma unroll
         for (int r = 0; r < QT_ROWS_PER_WAVE; ++r)
-          if (slot0 + r < rows) dst[r] = (int8_t)((tcodes[j][r >> 2] >> (8 * (r & 3))) & 255);
+          if (slot0 + r < rows) dst[r] = (int8_t)((tq[j][r >> 2] >> (8 * (r & 3))) & 255);
+      }
+    }
+    if constexpr (HAS2) {
+      int8_t* dst = p.q2_t + col * rows + slot0;
+      if (tvec) {
+        *reinterpret_cast<uint4*>(dst) = make_uint4(tq2[j][0], tq2[j][1], tq2[j][2], tq2[j][3]);
+      } else {
+#pragma unroll
+        for (int r = 0; r < QT_ROWS_PER_WAVE; ++r)
+          if (slot0 + r < rows) dst[r] = (int8_t)((tq2[j][r >> 2] >> (8 * (r & 3))) & 255);
       }
     }
   }
@@ -794,10 +761,18 @@ static hipError_t launch_quant_k(const QuantParams& p, hipStream_t s) {
   const int64_t rt = (p.rows + QT_SLOTS - 1) / QT_SLOTS;
   if (ct > 0x7FFFFFFF || rt > 65535) return hipErrorInvalidValue;
   const dim3 grid((unsigned)ct, (unsigned)rt);
-  if (p.q2_t)
-    hipLaunchKernelGGL((quant_tile_kernel<MODE, K, true>), grid, dim3(256), 0, s, p);
-  else
-    hipLaunchKernelGGL((quant_tile_kernel<MODE, K, false>), grid, dim3(256), 0, s, p);
+  const bool vec = (p.cols % 4 == 0) && (((uintptr_t)p.x & 15) == 0);
+  if (p.q2_t) {
+    if (vec)
+      hipLaunchKernelGGL((quant_tile_kernel<MODE, K, true, true>), grid, dim3(256), 0, s, p);
+    else
+      hipLaunchKernelGGL((quant_tile_kernel<MODE, K, true, false>), grid, dim3(256), 0, s, p);
+  } else {
+    if (vec)
+      hipLaunchKernelGGL((quant_tile_kernel<MODE, K, false, true>), grid, dim3(256), 0, s, p);
+    else
+      hipLaunchKernelGGL((quant_tile_kernel<MODE, K, false, false>), grid, dim3(256), 0, s, p);
+  }
   return hipGetLastError();
 }
 
