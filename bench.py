@@ -32,7 +32,35 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="after timing, run a plain 256 MiB elementwise pass (traffic-counter calibration)")
     return ap.parse_args()
+
+
+TRAFFIC_FILE = os.path.join(os.path.dirname(os.path.abspath(__file__)), "profiles", "traffic_linear_ffn_bhq5.txt")
+# kernel of each phase in the rocprofv3 summaries (name prefixes)
+PHASE_KERNEL = {
+    "quant_G": ("quant_tile_kernel<2, 64, true, true>",),
+    "gemm_gradX": ("gemm_i8_kernel", ", 3, 64, true>"),
+    "gemm_gradW": ("gemm_i8_kernel", ", 1, 0, true>"),
+}
+
+
+def measured_traffic(phase):
+    """HBM bytes per launch from the committed FETCH_SIZE / WRITE_SIZE summary, if it
+    was taken on the current kernel sources; else None."""
+    try:
+        from paper_2010_14298_amd import profiling
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+        if t.get("kernel_sources") != profiling.source_hash():
+            return None
+        for name, v in t["kernels"].items():
+            if all(part in name for part in PHASE_KERNEL[phase]):
+                return v["bytes"]
+    except (OSError, ValueError, KeyError):
+        return None
+    return None
 
 
 def cpu_baseline(X, W, G):
@@ -115,7 +143,7 @@ def main():
     roof = dict(per_kernel[dom])
     roof.pop("ms")
     roof["kernel"] = dom
-    roof["traffic"] = None
+    roof["traffic"] = measured_traffic(dom)
     out = {
         "metric": "FQT layer-backward int8 TOPS + quantizer HBM GB/s (BHQ 5-bit) vs roofline",
         "value": round(value, 3),
@@ -138,6 +166,13 @@ def main():
         "kernels": per_kernel,
         "roofline": roof,
     }
+    if args.copy_probe:
+        # a plain elementwise pass: reads 256 MiB, writes 256 MiB
+        src = torch.ones(64 * 1024 * 1024, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            torch.neg(src, out=dst)
+        torch.cuda.synchronize()
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(X, W, G)
     print(json.dumps(out), flush=True)
