@@ -429,9 +429,6 @@ fqt_status fqt_linear_backward(const float* X, const float* W, const float* G, i
   px.zero = w.zx;
   px.q_t = w.qx_t;
   px.sum_t = w.sum_x;
-  tr.begin(3);
-  FQT_TRY(launch_quant(px, QM_TENSOR, s));
-  tr.end(3);
   // Q_theta(W): deterministic PTQ, codes [d_in, d_out]
   QuantParams pw{};
   pw.x = W;
@@ -442,10 +439,6 @@ fqt_status fqt_linear_backward(const float* X, const float* W, const float* G, i
   pw.zero = w.zw;
   pw.q_t = w.qw_t;
   pw.sum_t = w.sum_w;
-  tr.begin(4);
-  FQT_TRY(launch_quant(pw, QM_TENSOR, s));
-  tr.end(4);
-  // Q_b2(G) [N, d_out] slot order (stream 1) and Q_b1(G) [d_out, N] (stream 0), one read of G
   QuantParams pg{};
   pg.x = G;
   pg.rows = N;
@@ -466,6 +459,14 @@ fqt_status fqt_linear_backward(const float* X, const float* W, const float* G, i
   pg.q2_t = w.qg1_t;
   pg.sum2_t = w.sum_g1;
   pg.L = L;
+  // Q_b2(G) [N, d_out] slot order (stream 1) and Q_b1(G) [d_out, N] (stream 0)
+  // from one read of G
+  tr.begin(3);
+  FQT_TRY(launch_quant(px, QM_TENSOR, s));
+  tr.end(3);
+  tr.begin(4);
+  FQT_TRY(launch_quant(pw, QM_TENSOR, s));
+  tr.end(4);
   tr.begin(5);
   FQT_TRY(launch_quant(pg, mode, s));
   tr.end(5);
