@@ -22,8 +22,9 @@ __device__ __forceinline__ u32x4 philox10(uint32_t c0, uint32_t c1, uint32_t c2,
   for (int r = 0; r < 10; ++r) {
     const uint64_t p0 = (uint64_t)0xD2511F53u * c0;
     const uint64_t p1 = (uint64_t)0xCD9E8D57u * c2;
-    const uint32_t n0 = (uint32_t)(p1 >> 32) ^ c1 ^ k0;
-    const uint32_t n2 = (uint32_t)(p0 >> 32) ^ c3 ^ k1;
+    // three-way xors in one gfx950 bitop3 each (truth table 0x96)
+    const uint32_t n0 = __builtin_amdgcn_bitop3_b32((uint32_t)(p1 >> 32), c1, k0, 0x96);
+    const uint32_t n2 = __builtin_amdgcn_bitop3_b32((uint32_t)(p0 >> 32), c3, k1, 0x96);
     c1 = (uint32_t)p1;
     c3 = (uint32_t)p0;
     c0 = n0;
@@ -67,6 +68,40 @@ __device__ __forceinline__ int rne_code(float y, int B) {
   float r = rintf(y);
   r = fminf(fmaxf(r, 0.0f), (float)B);
   return (int)r;
+}
+
+// ---------------------------------------------------------------------------
+// The same two rounding rules in 8.24 fixed point, for the bulk quantizers.
+// Both return a word whose top byte is the offset code (code - half) as int8
+// (hoff = half << 24), so that four results pack into one word with byte
+// permutes and sum with one 4-way int8 dot product.
+//
+// sr_top: with yc = clamp(y, 0, B) (clamping first leaves the clamped code
+// of sr_code unchanged), T = ceil(yc * 2^24) = floor(yc) * 2^24 + ceil(frac
+// * 2^24) (the scaling is exact and floor(yc) * 2^24 is an integer), and
+// u' = 2^24 - 1 - (word >> 8), the sum T + u' carries into bit 24 exactly
+// when (word >> 8) < ceil(frac * 2^24), i.e. when (word >> 8) < frac * 2^24:
+// the rounding-up decision of sr_code.  T + u' < 2^32 since yc <= 255 and at
+// yc = B the fraction is 0.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ int32_t sr_top(float y, uint32_t word, float Bf, uint32_t hoff) {
+  const float yc = __builtin_amdgcn_fmed3f(y, 0.0f, Bf);
+  const uint32_t t = (uint32_t)ceilf(yc * 16777216.0f);
+  return (int32_t)((t - (word >> 8)) + (0xFFFFFFu - hoff));  // T + u' - hoff
+}
+__device__ __forceinline__ int32_t rne_top(float y, float Bf, uint32_t hoff) {
+  const float r = rintf(__builtin_amdgcn_fmed3f(y, 0.0f, Bf));
+  return (int32_t)(((uint32_t)(int)r << 24) - hoff);
+}
+// Top bytes of a, b, c, d as bytes 0..3 of one word.
+__device__ __forceinline__ uint32_t pack_top4(int32_t a, int32_t b, int32_t c, int32_t d) {
+  const uint32_t lo = __builtin_amdgcn_perm((uint32_t)b, (uint32_t)a, 0x0c0c0703u);
+  const uint32_t hi = __builtin_amdgcn_perm((uint32_t)d, (uint32_t)c, 0x07030c0cu);
+  return lo | hi;
+}
+// Sum of the four signed bytes of w, added to acc.
+__device__ __forceinline__ int32_t sum4_i8(uint32_t w, int32_t acc) {
+  return __builtin_amdgcn_sdot4((int)w, 0x01010101, acc, false);
 }
 
 // ---------------------------------------------------------------------------

@@ -469,45 +469,65 @@ constexpr int QT_SLOTS = 64;
 constexpr int QT_COLS = 256;
 constexpr int QT_ROWS_PER_WAVE = 16;
 
-__device__ __forceinline__ uint32_t pack4(int a, int b, int c, int d) {
-  return (uint32_t)(a & 255) | ((uint32_t)(b & 255) << 8) | ((uint32_t)(c & 255) << 16) | ((uint32_t)(d & 255) << 24);
-}
-
-// Codes of four consecutive columns of one row from transformed values y:
-// stochastic rounding with the Philox block of element e0 (VEC: e0 % 4 == 0,
-// one block for all four) or round-half-even.
+// Offset codes of four consecutive columns of one row from transformed values
+// y, in the top-byte form of sr_top / rne_top: stochastic rounding with the
+// Philox block of element e0 (VEC: e0 % 4 == 0, one block for all four) or
+// round-half-even.
 template <bool VEC>
-__device__ __forceinline__ void round4(const float (&y)[4], uint64_t e0, int stoch, uint64_t seed, uint32_t stream,
-                                       int B, int (&code)[4]) {
-  if (stoch) {
-    if constexpr (VEC) {
-      const u32x4 o = philox_block(e0, seed, stream);
-      code[0] = sr_code(y[0], o.x, B);
-      code[1] = sr_code(y[1], o.y, B);
-      code[2] = sr_code(y[2], o.z, B);
-      code[3] = sr_code(y[3], o.w, B);
-    } else {
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const uint64_t e = e0 + j;
-        const u32x4 o = philox_block(e, seed, stream);
-        code[j] = sr_code(y[j], philox_word(o, (int)(e & 3)), B);
-      }
-    }
+__device__ __forceinline__ void sr4(const float (&y)[4], uint64_t e0, uint64_t seed, uint32_t stream, float Bf,
+                                    uint32_t hoff, int32_t (&t)[4]) {
+  if constexpr (VEC) {
+    const u32x4 o = philox_block(e0, seed, stream);
+    t[0] = sr_top(y[0], o.x, Bf, hoff);
+    t[1] = sr_top(y[1], o.y, Bf, hoff);
+    t[2] = sr_top(y[2], o.z, Bf, hoff);
+    t[3] = sr_top(y[3], o.w, Bf, hoff);
   } else {
 #pragma unroll
-    for (int j = 0; j < 4; ++j) code[j] = rne_code(y[j], B);
+    for (int j = 0; j < 4; ++j) {
+      const uint64_t e = e0 + j;
+      const u32x4 o = philox_block(e, seed, stream);
+      t[j] = sr_top(y[j], philox_word(o, (int)(e & 3)), Bf, hoff);
+    }
   }
+}
+__device__ __forceinline__ void rne4(const float (&y)[4], float Bf, uint32_t hoff, int32_t (&t)[4]) {
+#pragma unroll
+  for (int j = 0; j < 4; ++j) t[j] = rne_top(y[j], Bf, hoff);
+}
+
+// Sums over the 64 lanes of each of 16 per-lane values v[0..15], by halving
+// exchanges (lanes differing in bit 5 swap halves of the list, then bit 4,
+// ...): lane l with l % 4 == 0 returns the sum of v[l / 4].
+__device__ __forceinline__ int32_t wave_sum16(int32_t (&v)[16], int lane) {
+#pragma unroll
+  for (int half = 8, bit = 32; half >= 1; half >>= 1, bit >>= 1) {
+    // bitwise selects (one v_bfi each): a conditional between two list
+    // entries would be turned into a dynamically indexed register read
+    const int32_t m = (lane & bit) ? -1 : 0;
+#pragma unroll
+    for (int i = 0; i < half; ++i) {
+      const int32_t keep = (v[i + half] & m) | (v[i] & ~m);
+      const int32_t give = (v[i] & m) | (v[i + half] & ~m);
+      v[i] = keep + __shfl_xor(give, bit);
+    }
+  }
+  int32_t s = v[0];
+  s += __shfl_xor(s, 2);
+  s += __shfl_xor(s, 1);
+  return s;
 }
 
 // Tile = 64 slots x 256 columns; 4 waves of 16 slots; 4 columns per lane.
 // The loaded tile stays in registers; each row is then finished in one step
 // (transform, both quantizers, packing, code sums) so its data dies early.
 // VEC: cols % 4 == 0 (float4 loads, one Philox block per lane and row).
-template <int MODE, int K, bool HAS2, bool VEC>
+// TRANS: the primary codes go out transposed ([cols, rows], column sums)
+// instead of in natural order ([rows, cols], row sums).
+template <int MODE, int K, bool HAS2, bool VEC, bool TRANS>
 __global__ __launch_bounds__(256) void quant_tile_kernel(QuantParams p) {
   const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform: slot bookkeeping stays scalar
   const int64_t tile0 = (int64_t)blockIdx.y * QT_SLOTS;
   const int64_t slot0 = tile0 + wave * QT_ROWS_PER_WAVE;
   const int64_t c0 = (int64_t)blockIdx.x * QT_COLS + lane * 4;
@@ -589,18 +609,30 @@ __global__ __launch_bounds__(256) void quant_tile_kernel(QuantParams p) {
     }
   }
 
-  // ---- finish row by row
-  int csum[4] = {0, 0, 0, 0}, csum2[4] = {0, 0, 0, 0};
-  uint32_t tq[4][4], tq2[4][4];  // transposed codes: [column][4 words of 16 slots]
+  // ---- finish row by row.  Offset codes are carried in the top-byte form
+  // (sr_top / rne_top), packed four to a word with byte permutes (natural:
+  // four columns of one row; transposed: four rows of one column) and summed
+  // with int8 dot products of the packed words.
+  const float Bf = (float)B;
+  const uint32_t hoff = (uint32_t)half << 24;
+  // bytes of the packed natural word that belong to columns inside the matrix
+  uint32_t colmask = 0u;
 #pragma unroll
   for (int j = 0; j < 4; ++j)
-#pragma unroll
-    for (int w = 0; w < 4; ++w) {
-      tq[j][w] = 0u;
-      tq2[j][w] = 0u;
-    }
+    if (c0 + j < cols) colmask |= 0xFFu << (8 * j);
+  int32_t rsum[QT_ROWS_PER_WAVE];  // per-lane partial row sums of the natural codes
+  uint32_t tq[4][4], tq2[4][4];    // transposed codes: [column][4 words of 16 slots]
+  int32_t tp[4][4], tp2[4][4];     // top-byte codes of the current 4 rows: [row % 4][column]
   const float s_t = (MODE == QM_TENSOR) ? p.scale[0] : 0.0f;
   const float z_t = (MODE == QM_TENSOR) ? p.zero[0] : 0.0f;
+  float Bf2 = 0.0f, s2 = 0.0f, z2 = 0.0f;
+  uint32_t hoff2 = 0u;
+  if constexpr (HAS2) {
+    Bf2 = (float)((1 << p.bits2) - 1);
+    hoff2 = (uint32_t)(1 << (p.bits2 - 1)) << 24;
+    s2 = p.scale2[0];
+    z2 = p.zero2[0];
+  }
 #pragma unroll
   for (int r = 0; r < QT_ROWS_PER_WAVE; ++r) {
     const int64_t slot = slot0 + r;
@@ -662,45 +694,59 @@ __global__ __launch_bounds__(256) void quant_tile_kernel(QuantParams p) {
       }
     }
     const uint64_t e0 = (uint64_t)srow[r] * (uint64_t)cols + (uint64_t)c0;
-    int code[4];
-    round4<VEC>(y, e0, p.stoch, p.seed, p.stream, B, code);
-    int q[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) q[j] = (ok && c0 + j < cols) ? code[j] - half : 0;
-    if (p.q_nat && ok && lane_ok) {
-      int8_t* dst = p.q_nat + slot * cols + c0;
-      if constexpr (VEC) {
-        *reinterpret_cast<uint32_t*>(dst) = pack4(q[0], q[1], q[2], q[3]);
-      } else {
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-          if (c0 + j < cols) dst[j] = (int8_t)q[j];
-      }
-    }
-    if (p.sum_nat) {
-      const int t = wave_sum_i(q[0] + q[1] + q[2] + q[3]);
-      if (lane == 0 && ok) atomicAdd(p.sum_nat + slot, t);
-    }
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      csum[j] += q[j];
-      tq[j][r >> 2] |= (uint32_t)(q[j] & 255) << (8 * (r & 3));
-    }
+    int32_t t[4];
+    // with a second quantizer the first is stochastic too (launch_quant checks)
+    if (HAS2 || p.stoch)
+      sr4<VEC>(y, e0, p.seed, p.stream, Bf, hoff, t);
+    else
+      rne4(y, Bf, hoff, t);
     if constexpr (HAS2) {
-      const int B2 = (1 << p.bits2) - 1;
-      const int half2 = 1 << (p.bits2 - 1);
-      const float s2 = p.scale2[0], z2 = p.zero2[0];
+      // Q_b1 of the same row: always stochastic, its own Philox stream (the
+      // counter and key are shared, so the compiler shares the first two
+      // rounds' products with the call above)
       float y2[4];
 #pragma unroll
       for (int j = 0; j < 4; ++j) y2[j] = s2 * (g[r][j] - z2);
-      int code2[4];
-      round4<VEC>(y2, e0, 1, p.seed, p.stream2, B2, code2);
+      int32_t t2[4];
+      sr4<VEC>(y2, e0, p.seed, p.stream2, Bf2, hoff2, t2);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) tp2[r & 3][j] = t2[j];
+    }
+    if constexpr (!TRANS) {
+      const uint32_t w = pack_top4(t[0], t[1], t[2], t[3]);
+      if (p.q_nat && ok && lane_ok) {
+        int8_t* dst = p.q_nat + slot * cols + c0;
+        if constexpr (VEC) {
+          *reinterpret_cast<uint32_t*>(dst) = w;
+        } else {
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            if (c0 + j < cols) dst[j] = (int8_t)(t[j] >> 24);
+        }
+      }
+      rsum[r] = sum4_i8(w & colmask, 0);
+    } else {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) tp[r & 3][j] = t[j];
+    }
+    if ((r & 3) == 3) {
+      // rows past the matrix end contribute zero bytes to the column sums
+      const int64_t nval = rows - (slot0 + (r - 3));
+      const uint32_t rowmask = nval >= 4 ? 0xFFFFFFFFu : (nval <= 0 ? 0u : (0xFFFFFFFFu >> (8 * (4 - nval))));
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const int q2 = (ok && c0 + j < cols) ? code2[j] - half2 : 0;
-        csum2[j] += q2;
-        tq2[j][r >> 2] |= (uint32_t)(q2 & 255) << (8 * (r & 3));
+        if constexpr (TRANS) tq[j][r >> 2] = pack_top4(tp[0][j], tp[1][j], tp[2][j], tp[3][j]) & rowmask;
+        if constexpr (HAS2) tq2[j][r >> 2] = pack_top4(tp2[0][j], tp2[1][j], tp2[2][j], tp2[3][j]) & rowmask;
       }
+    }
+  }
+
+  // ---- row sums of the natural codes: one exchange tree for the 16 rows
+  if constexpr (!TRANS) {
+    if (p.sum_nat) {
+      const int32_t t = wave_sum16(rsum, lane);
+      const int64_t slot = slot0 + (lane >> 2);
+      if ((lane & 3) == 0 && slot < rows) atomicAdd(p.sum_nat + slot, t);
     }
   }
 
@@ -710,7 +756,7 @@ __global__ __launch_bounds__(256) void quant_tile_kernel(QuantParams p) {
   for (int j = 0; j < 4; ++j) {
     const int64_t col = c0 + j;
     if (col >= cols) continue;
-    if (p.q_t) {
+    if constexpr (TRANS) {
       int8_t* dst = p.q_t + col * rows + slot0;
       if (tvec) {
         *reinterpret_cast<uint4*>(dst) = make_uint4(tq[j][0], tq[j][1], tq[j][2], tq[j][3]);
@@ -733,17 +779,23 @@ __global__ __launch_bounds__(256) void quant_tile_kernel(QuantParams p) {
   }
 
   // ---- column sums of the transposed outputs: reduce the 4 waves in LDS
-  if (p.sum_t || (HAS2 && p.sum2_t)) {
+  if ((TRANS && p.sum_t) || (HAS2 && p.sum2_t)) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      s_csum[0][wave][lane * 4 + j] = csum[j];
-      s_csum[1][wave][lane * 4 + j] = csum2[j];
+      int32_t cs = 0, cs2 = 0;
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        if constexpr (TRANS) cs = sum4_i8(tq[j][w], cs);
+        if constexpr (HAS2) cs2 = sum4_i8(tq2[j][w], cs2);
+      }
+      s_csum[0][wave][lane * 4 + j] = cs;
+      s_csum[1][wave][lane * 4 + j] = cs2;
     }
     __syncthreads();
     const int c = threadIdx.x;  // 256 threads = 256 columns of the tile
     const int64_t col = (int64_t)blockIdx.x * QT_COLS + c;
     if (col < cols) {
-      if (p.sum_t) {
+      if (TRANS && p.sum_t) {
         const int t = s_csum[0][0][c] + s_csum[0][1][c] + s_csum[0][2][c] + s_csum[0][3][c];
         atomicAdd(p.sum_t + col, t);
       }
@@ -755,6 +807,7 @@ __global__ __launch_bounds__(256) void quant_tile_kernel(QuantParams p) {
   }
 }
 
+
 template <int MODE, int K>
 static hipError_t launch_quant_k(const QuantParams& p, hipStream_t s) {
   const int64_t ct = (p.cols + QT_COLS - 1) / QT_COLS;
@@ -762,16 +815,25 @@ static hipError_t launch_quant_k(const QuantParams& p, hipStream_t s) {
   if (ct > 0x7FFFFFFF || rt > 65535) return hipErrorInvalidValue;
   const dim3 grid((unsigned)ct, (unsigned)rt);
   const bool vec = (p.cols % 4 == 0) && (((uintptr_t)p.x & 15) == 0);
+  // one primary layout: natural (with an optional transposed Q_b1) or transposed
+  if ((p.q_nat || p.sum_nat) && (p.q_t || p.sum_t)) return hipErrorInvalidValue;
+  const bool trans = p.q_t || p.sum_t;
   if (p.q2_t) {
+    if (trans || !p.stoch) return hipErrorInvalidValue;
     if (vec)
-      hipLaunchKernelGGL((quant_tile_kernel<MODE, K, true, true>), grid, dim3(256), 0, s, p);
+      hipLaunchKernelGGL((quant_tile_kernel<MODE, K, true, true, false>), grid, dim3(256), 0, s, p);
     else
-      hipLaunchKernelGGL((quant_tile_kernel<MODE, K, true, false>), grid, dim3(256), 0, s, p);
+      hipLaunchKernelGGL((quant_tile_kernel<MODE, K, true, false, false>), grid, dim3(256), 0, s, p);
+  } else if (trans) {
+    if (vec)
+      hipLaunchKernelGGL((quant_tile_kernel<MODE, K, false, true, true>), grid, dim3(256), 0, s, p);
+    else
+      hipLaunchKernelGGL((quant_tile_kernel<MODE, K, false, false, true>), grid, dim3(256), 0, s, p);
   } else {
     if (vec)
-      hipLaunchKernelGGL((quant_tile_kernel<MODE, K, false, true>), grid, dim3(256), 0, s, p);
+      hipLaunchKernelGGL((quant_tile_kernel<MODE, K, false, true, false>), grid, dim3(256), 0, s, p);
     else
-      hipLaunchKernelGGL((quant_tile_kernel<MODE, K, false, false>), grid, dim3(256), 0, s, p);
+      hipLaunchKernelGGL((quant_tile_kernel<MODE, K, false, false, false>), grid, dim3(256), 0, s, p);
   }
   return hipGetLastError();
 }
