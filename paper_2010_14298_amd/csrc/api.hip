@@ -73,6 +73,7 @@ QuantWs carve_quant(Carver& c, fqt_kind kind, const float* x, int64_t rows, int6
   if (kind != FQT_PTQ) {
     w.rmin = c.take<float>(rows);
     w.rmax = c.take<float>(rows);
+    stats_direct_rows(w.seg, w.rmin, w.rmax);
   }
   if (kind == FQT_BHQ) w.plan = c.take<char>((int64_t)bhq_plan_workspace(rows));
   return w;
@@ -188,6 +189,7 @@ LinearWs carve_linear(Carver& c, const float* X, const float* W, const float* G,
   w.sg_seg.part = c.take<float2>(stats_partials(w.sg_seg));
   w.rmin = c.take<float>(N);
   w.rmax = c.take<float>(N);
+  stats_direct_rows(w.sg_seg, w.rmin, w.rmax);
   w.qx_t = c.take<int8_t>(d_in * N);
   w.qw_t = c.take<int8_t>(d_in * d_out);
   w.qg1_t = c.take<int8_t>(d_out * N);
@@ -280,6 +282,7 @@ ConvWs carve_conv(Carver& c, const float* X, const float* W, const float* G, con
   w.sg_seg.part = c.take<float2>(stats_partials(w.sg_seg));
   w.rmin = c.take<float>(N);
   w.rmax = c.take<float>(N);
+  stats_direct_rows(w.sg_seg, w.rmin, w.rmax);
   w.ldq = (P + 127) / 128 * 128;
   w.xq_t = c.take<int8_t>((int64_t)g.c * N * hw);
   w.wq_t = c.take<int8_t>((int64_t)g.c * taps * g.o);

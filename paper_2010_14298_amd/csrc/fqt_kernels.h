@@ -12,15 +12,28 @@ namespace fqt {
 // Statistics: each block reduces one chunk of a flat tensor (rows = 1) or
 // of one row, into part[row * chunks + chunk] = (min, max); min is NaN when
 // the chunk holds a non-finite value.
+// A per-row segment whose rows fit one block (chunks == 1) also gets the
+// row ranges written directly: rmin[row] (+inf for a non-finite row, as the
+// finalize combination of one NaN-flagged partial gives) and rmax[row].
 struct StatsSeg {
   const float* x;
   int64_t rows, cols;
   int64_t chunk;   // columns per block
   int64_t chunks;  // blocks per row
   float2* part;
+  float* rmin;     // direct per-row ranges (chunks == 1), else nullptr
+  float* rmax;
 };
 StatsSeg stats_flat_seg(const float* x, int64_t n);
 StatsSeg stats_rows_seg(const float* x, int64_t rows, int64_t cols);
+// Route the row ranges of a per-row segment straight to rmin / rmax when a
+// block covers a whole row.
+inline void stats_direct_rows(StatsSeg& g, float* rmin, float* rmax) {
+  if (g.chunks == 1) {
+    g.rmin = rmin;
+    g.rmax = rmax;
+  }
+}
 __host__ __device__ inline int64_t stats_partials(const StatsSeg& g) { return g.rows * g.chunks; }
 struct StatsPlan {
   StatsSeg seg[3];

@@ -24,13 +24,20 @@ struct RowStage {
   double rterm;  // zW * rowsum
   double hz;     // BHQ group row: half + c_g;  affine row: zeta = z + half / s
   double dq;     // 1 / s  (Delta for an affine row, 1 / d_p for a group row)
-  int kind;      // 0 affine / one-row group, 1 full group, 2 partial group
-  int orow;      // output row, -1 past M
+  int64_t obase; // output row * ldo, -1 past M
+};
+// Per 64-row run and group of the BHQ epilogue: rows of the group that take
+// part in the Householder sum (full group: KG, partial group: its size, one-row
+// groups: 0) and the float64 sum of their rterm.
+struct GroupStage {
+  double rsum;
+  int m;
+  int kind;
 };
 
 template <class C, int EPI>
 struct GemmLdsSize {
-  static constexpr int EP_BYTES = C::BM * C::BN * 4 + C::BM * (int)sizeof(RowStage);
+  static constexpr int EP_BYTES = C::BM * C::BN * 4 + C::BM * (int)sizeof(RowStage) + C::BM * (int)sizeof(GroupStage);
   static constexpr bool STAGED = (EPI == EPI_ROW || EPI == EPI_BHQ);
   static constexpr int BYTES = (STAGED && EP_BYTES > C::OP_BYTES) ? EP_BYTES : C::OP_BYTES;
 };
@@ -82,19 +89,35 @@ __global__ __launch_bounds__(C::THREADS) void gemm_i8_kernel(GemmParams p) {
     const double zB = (double)p.zeroB[0] + (double)p.halfB * dB;
     const double kzz = (double)p.K * zA * zB;
     const double dAB = dA * dB;
+    // all code sums are loaded before the first store (for the compiler the
+    // stores could alias them, which would serialize one load per row)
+    int32_t sa[C::IT][16], sb[C::JT];
+#pragma unroll
+    for (int i = 0; i < C::IT; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int64_t row = m0 + wm * C::WM + i * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
+        sa[i][r] = row < p.M ? p.sumA[row] : 0;
+      }
+#pragma unroll
+    for (int j = 0; j < C::JT; ++j) {
+      const int64_t col = n0 + wn * C::WN + j * 32 + lrow;
+      sb[j] = col < p.N ? p.sumB[col] : 0;
+    }
+    double cterm[C::JT];
+#pragma unroll
+    for (int j = 0; j < C::JT; ++j) cterm[j] = zA * dB * (double)sb[j];
 #pragma unroll
     for (int i = 0; i < C::IT; ++i)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int64_t row = m0 + wm * C::WM + i * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
         if (row >= p.M) continue;
-        const double rterm = dA * zB * (double)p.sumA[row] + kzz;
+        const double rterm = dA * zB * (double)sa[i][r] + kzz;
 #pragma unroll
         for (int j = 0; j < C::JT; ++j) {
           const int64_t col = n0 + wn * C::WN + j * 32 + lrow;
-          if (col < p.N)
-            p.out[row * p.ldo + col] =
-                (float)(dAB * (double)acc[i][j][r] + rterm + zA * dB * (double)p.sumB[col]);
+          if (col < p.N) p.out[row * p.ldo + col] = (float)(dAB * (double)acc[i][j][r] + rterm + cterm[j]);
         }
       }
   } else {
@@ -102,8 +125,9 @@ __global__ __launch_bounds__(C::THREADS) void gemm_i8_kernel(GemmParams p) {
     // Stage the accumulators and per-row data in LDS (the operand tiles are
     // dead after the loop), then thread t owns column t % BN and a run of
     // consecutive rows: group sums are sequential in one thread.
-    int32_t* sacc = reinterpret_cast<int32_t*>(lds);                               // [BM][BN]
-    RowStage* srow = reinterpret_cast<RowStage*>(lds + C::BM * C::BN * 4);        // [BM]
+    int32_t* sacc = reinterpret_cast<int32_t*>(lds);                                   // [BM][BN]
+    RowStage* srow = reinterpret_cast<RowStage*>(lds + C::BM * C::BN * 4);            // [BM]
+    GroupStage* sgrp = reinterpret_cast<GroupStage*>(srow + C::BM);                   // [BM / KG]
     const double dW = 1.0 / (double)p.scaleB[0];
     const double zW = (double)p.zeroB[0] + (double)p.halfB * dW;
 #pragma unroll
@@ -120,20 +144,36 @@ __global__ __launch_bounds__(C::THREADS) void gemm_i8_kernel(GemmParams p) {
       if (row < p.M) {
         const float s = p.rowwiseA ? p.scaleA[row] : p.scaleA[0];
         const float z = p.rowwiseA ? p.zeroA[row] : p.zeroA[0];
-        q.kind = (EPI == EPI_BHQ) ? bhq_slot_kind(p.L, row) : 0;
+        const int kind = (EPI == EPI_BHQ) ? bhq_slot_kind(p.L, row) : 0;
         q.rterm = zW * (double)p.sumA[row];
         q.dq = 1.0 / (double)s;
-        q.hz = q.kind != 0 ? (double)p.halfA + (double)z : (double)z + (double)p.halfA * q.dq;
-        q.orow = p.perm ? p.perm[row] : (int)row;
+        q.hz = kind != 0 ? (double)p.halfA + (double)z : (double)z + (double)p.halfA * q.dq;
+        q.obase = (int64_t)(p.perm ? p.perm[row] : (int)row) * p.ldo;
       } else {
-        q.orow = -1;
+        q.obase = -1;
       }
       srow[rr] = q;
+    }
+    static_assert(C::BM % 64 == 0 && KG <= 64, "64-row epilogue runs");
+    if constexpr (EPI == EPI_BHQ && KG > 1) {
+      __syncthreads();
+      // per group: Householder rows (they come first in the group) and their rterm sum
+      for (int gi = tid; gi < C::BM / KG; gi += C::THREADS) {
+        const int64_t g0 = m0 + (int64_t)gi * KG;
+        GroupStage gs{0.0, 0, 0};
+        if (g0 < p.M) {
+          gs.kind = bhq_slot_kind(p.L, g0);
+          if (gs.kind != 0) {
+            gs.m = gs.kind == 1 ? KG : p.L.part;
+            for (int t = 0; t < gs.m; ++t) gs.rsum += srow[gi * KG + t].rterm;
+          }
+        }
+        sgrp[gi] = gs;
+      }
     }
     __syncthreads();
     // Thread t owns column t % BN and the 64-row runs t / BN, t / BN + THREADS / BN, ...
     // A run is 64 rows, so every group (KG <= 64, aligned) lies inside one.
-    static_assert(C::BM % 64 == 0 && KG <= 64, "64-row epilogue runs");
     constexpr int NRUN = C::BM / 64;
     constexpr int RSTEP = C::THREADS / C::BN;
     const int c = tid % C::BN;
@@ -145,38 +185,41 @@ __global__ __launch_bounds__(C::THREADS) void gemm_i8_kernel(GemmParams p) {
       const int rbase = run * 64;
       if constexpr (EPI == EPI_BHQ && KG > 1) {
         for (int g0 = rbase; g0 < rbase + 64; g0 += KG) {
-          // T_p = (code_p + c_g) . W~ ; S = sum over the group's multi-row slots
-          double S = 0.0, T0 = 0.0;
-          for (int t = 0; t < KG; ++t) {
-            const RowStage& q = srow[g0 + t];
-            const double T = dW * (double)sacc[(g0 + t) * C::BN + c] + (q.rterm + q.hz * colterm);
-            if (q.kind != 0) S += T;
-            if (t == 0) T0 = T;
+          // Row p of a group: T_p = (code_p + c_g) . W~ = dW a_p + rterm_p + hz colterm;
+          // the Householder sum S = sum of T_p over its m rows, with the
+          // accumulators summed exactly in int64.
+          const GroupStage gs = sgrp[g0 / KG];
+          const double hz = srow[g0].hz;
+          double tau = 0.0, alpha = 0.0;
+          if (gs.m > 0) {
+            int64_t asum = 0;
+            for (int t = 0; t < gs.m; ++t) asum += sacc[(g0 + t) * C::BN + c];
+            const double S = dW * (double)asum + (gs.rsum + (double)gs.m * (hz * colterm));
+            const double T0 = dW * (double)sacc[g0 * C::BN + c] + (srow[g0].rterm + hz * colterm);
+            alpha = gs.kind == 2 ? p.L.inv_sk_p : p.L.inv_sk_k;
+            tau = (alpha * S - T0) / (1.0 - alpha);
           }
-          const int gkind = srow[g0].kind;
-          const double alpha = gkind == 2 ? p.L.inv_sk_p : p.L.inv_sk_k;
-          const double tau = (alpha * S - T0) / (1.0 - alpha);
+          const double up0 = (1.0 - alpha) * tau, dn = alpha * tau;
           for (int t = 0; t < KG; ++t) {
-            const RowStage& q = srow[g0 + t];
-            if (q.orow < 0) continue;
+            const RowStage q = srow[g0 + t];
+            if (q.obase < 0) continue;
             const double a = (double)sacc[(g0 + t) * C::BN + c];
             double v;
-            if (q.kind != 0) {
+            if (t < gs.m) {
               const double T = dW * a + (q.rterm + q.hz * colterm);
-              const double Z = (t == 0) ? T + (1.0 - alpha) * tau : T - alpha * tau;
-              v = Z * q.dq;
+              v = (t == 0 ? T + up0 : T - dn) * q.dq;
             } else {
               v = q.dq * (dW * a + q.rterm) + q.hz * colterm;
             }
-            p.out[(int64_t)q.orow * p.ldo + col] = (float)v;
+            p.out[q.obase + col] = (float)v;
           }
         }
       } else {
         for (int t = rbase; t < rbase + 64; ++t) {
-          const RowStage& q = srow[t];
-          if (q.orow < 0) continue;
+          const RowStage q = srow[t];
+          if (q.obase < 0) continue;
           const double a = (double)sacc[t * C::BN + c];
-          p.out[(int64_t)q.orow * p.ldo + col] = (float)(q.dq * (dW * a + q.rterm) + q.hz * colterm);
+          p.out[q.obase + col] = (float)(q.dq * (dW * a + q.rterm) + q.hz * colterm);
         }
       }
     }

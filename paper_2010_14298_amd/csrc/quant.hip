@@ -100,7 +100,13 @@ __global__ __launch_bounds__(256) void stats_kernel(StatsPlan sp) {
     }
   }
   const MinMax r = block_minmax<4>(mn, mx, bad);
-  if (threadIdx.x == 0) g.part[b] = make_float2(r.bad ? NAN : r.mn, r.mx);
+  if (threadIdx.x == 0) {
+    g.part[b] = make_float2(r.bad ? NAN : r.mn, r.mx);
+    if (g.rmin) {
+      g.rmin[row] = r.bad ? INFINITY : r.mn;
+      g.rmax[row] = r.mx;
+    }
+  }
 }
 
 StatsSeg stats_flat_seg(const float* x, int64_t n) {
@@ -152,7 +158,18 @@ __global__ __launch_bounds__(1024) void finalize_kernel(FinalizePlan fp) {
     const StatsSeg& g = fp.seg[si];
     float mn = INFINITY, mx = -INFINITY;
     int bad = 0;
-    if (si == fp.row_seg) {
+    if (si == fp.row_seg && g.rmin) {
+      // row ranges already stored by the stats blocks: a load-only reduction
+      // (no stores in the loop, so the loads of several rows are in flight)
+#pragma unroll 8
+      for (int64_t r = t; r < g.rows; r += blockDim.x) {
+        const float2 p = g.part[r];
+        const float rmn = fminf(INFINITY, p.x);
+        bad |= isnan(p.x) || !isfinite(p.y - rmn);
+        mn = fminf(mn, rmn);
+        mx = fmaxf(mx, p.y);
+      }
+    } else if (si == fp.row_seg) {
       for (int64_t r = t; r < g.rows; r += blockDim.x) {
         float rmn = INFINITY, rmx = -INFINITY;
         for (int64_t c = 0; c < g.chunks; ++c) {
