@@ -127,7 +127,10 @@ fqt_status quantize_common(fqt_kind kind, const float* x, int64_t rows, int64_t 
   }
   add_zero(fp, out->code_sum, transpose ? cols : rows);
   if (kind == FQT_BHQ) add_zero(fp, bhq_plan_carve(w.plan, rows).rank, rows);
-  FQT_TRY(launch_finalize(fp, s));
+  // with row ranges straight from the statistics kernel, the BHQ plan's first
+  // launch also runs the finalize step
+  const bool fin_in_plan = kind == FQT_BHQ && w.seg.rmin != nullptr;
+  if (!fin_in_plan) FQT_TRY(launch_finalize(fp, s));
 
   QuantParams p{};
   p.x = x;
@@ -151,7 +154,8 @@ fqt_status quantize_common(fqt_kind kind, const float* x, int64_t rows, int64_t 
     mode = QM_ROW;
   } else if (kind == FQT_BHQ) {
     p.L = bhq_layout(rows, block_size);
-    FQT_TRY(launch_bhq_plan(w.rmin, w.rmax, p.L, bits, w.plan, out->perm, out->scale, out->zero, out->group_off, s));
+    FQT_TRY(launch_bhq_plan(w.rmin, w.rmax, p.L, bits, w.plan, out->perm, out->scale, out->zero, out->group_off,
+                            fin_in_plan ? &fp : nullptr, s));
     p.perm = out->perm;
     mode = QM_BHQ;
   }
@@ -411,12 +415,14 @@ fqt_status fqt_linear_backward(const float* X, const float* W, const float* G, i
   add_zero(fp, w.sum_g1, d_out);
   add_zero(fp, w.sum_g2, N);
   if (bhq) add_zero(fp, bhq_plan_carve(w.plan, N).rank, N);
-  FQT_TRY(launch_finalize(fp, s));
+  const bool fin_in_plan = bhq && w.sg_seg.rmin != nullptr;
+  if (!fin_in_plan) FQT_TRY(launch_finalize(fp, s));
   BhqLayout L{};
   int mode = qx.kind == FQT_PSQ ? QM_ROW : QM_TENSOR;
   if (bhq) {
     L = bhq_layout(N, qx.block_size);
-    FQT_TRY(launch_bhq_plan(w.rmin, w.rmax, L, qx.bits, w.plan, w.perm, w.sg2, w.zg2, nullptr, s));
+    FQT_TRY(launch_bhq_plan(w.rmin, w.rmax, L, qx.bits, w.plan, w.perm, w.sg2, w.zg2, nullptr,
+                            fin_in_plan ? &fp : nullptr, s));
     mode = QM_BHQ;
   }
   tr.end(2);
@@ -464,11 +470,11 @@ fqt_status fqt_linear_backward(const float* X, const float* W, const float* G, i
   pg.L = L;
   // Q_b2(G) [N, d_out] slot order (stream 1) and Q_b1(G) [d_out, N] (stream 0)
   // from one read of G
+  // Q_f(X) and Q_theta(W) in one launch (phase 3; phase 4 stays empty)
   tr.begin(3);
-  FQT_TRY(launch_quant(px, QM_TENSOR, s));
+  FQT_TRY(launch_quant_pair(px, pw, s));
   tr.end(3);
   tr.begin(4);
-  FQT_TRY(launch_quant(pw, QM_TENSOR, s));
   tr.end(4);
   tr.begin(5);
   FQT_TRY(launch_quant(pg, mode, s));
@@ -610,12 +616,14 @@ fqt_status fqt_conv_backward_im2col(const float* X, const float* W, const float*
   if (!bhq) fp.out[fp.nout++] = ScaleOut{2, qx.bits, qx.kind == FQT_PSQ ? 1 : 0, w.sg2, w.zg2};
   add_zero(fp, w.sumB, taps * g.c);
   if (bhq) add_zero(fp, bhq_plan_carve(w.plan, N).rank, N);
-  FQT_TRY(launch_finalize(fp, s));
+  const bool fin_in_plan = bhq && w.sg_seg.rmin != nullptr;
+  if (!fin_in_plan) FQT_TRY(launch_finalize(fp, s));
   BhqLayout L{};
   int mode = qx.kind == FQT_PSQ ? QM_ROW : QM_TENSOR;
   if (bhq) {
     L = bhq_layout(N, qx.block_size);
-    FQT_TRY(launch_bhq_plan(w.rmin, w.rmax, L, qx.bits, w.plan, w.perm, w.sg2, w.zg2, nullptr, s));
+    FQT_TRY(launch_bhq_plan(w.rmin, w.rmax, L, qx.bits, w.plan, w.perm, w.sg2, w.zg2, nullptr,
+                            fin_in_plan ? &fp : nullptr, s));
     mode = QM_BHQ;
   }
   tr.end(2);

@@ -99,8 +99,12 @@ struct BhqPlanWs {
   int32_t* sigma;
 };
 BhqPlanWs bhq_plan_carve(void* plan_ws, int64_t rows);
+// fin: run this finalize step inside the first plan launch (only when the
+// row ranges rmin / rmax were stored by the statistics kernel); nullptr when
+// the finalize kernel already ran.
 hipError_t launch_bhq_plan(const float* rmin, const float* rmax, const BhqLayout& L, int bits, void* plan_ws,
-                           int32_t* perm, float* scale, float* zero, int32_t* group_off, hipStream_t s);
+                           int32_t* perm, float* scale, float* zero, int32_t* group_off, const FinalizePlan* fin,
+                           hipStream_t s);
 
 struct QuantParams {
   const float* x;
@@ -127,6 +131,8 @@ struct QuantParams {
 };
 enum QuantMode { QM_TENSOR = 0, QM_ROW = 1, QM_BHQ = 2 };
 hipError_t launch_quant(const QuantParams& p, int mode, hipStream_t s);
+// Two per-tensor quantizations with transposed outputs only, one launch.
+hipError_t launch_quant_pair(const QuantParams& p0, const QuantParams& p1, hipStream_t s);
 
 // Narrow transposing per-tensor quantizer (conv activations and Q_b1 of a
 // conv gradient): logical [rows, cols], row r of the output taken from source

@@ -148,7 +148,8 @@ hipError_t launch_stats(StatsPlan sp, hipStream_t s) {
 // scales / zeros (Sec. 4.1), clears the code-sum and rank arrays, and sets
 // the status word (non-finite input, or a range beyond float32).
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(1024) void finalize_kernel(FinalizePlan fp) {
+template <int NW>
+__device__ void finalize_block(const FinalizePlan& fp) {
   const int t = threadIdx.x;
   for (int z = 0; z < fp.nzero; ++z)
     for (int64_t i = t; i < fp.zero_n[z]; i += blockDim.x) fp.zero_i32[z][i] = 0;
@@ -192,7 +193,7 @@ __global__ __launch_bounds__(1024) void finalize_kernel(FinalizePlan fp) {
         mx = fmaxf(mx, p.y);
       }
     }
-    const MinMax r = block_minmax<16>(mn, mx, bad);
+    const MinMax r = block_minmax<NW>(mn, mx, bad);
     if (t == 0) {
       seg_mn[si] = r.mn;
       seg_mx[si] = r.mx;
@@ -220,6 +221,8 @@ __global__ __launch_bounds__(1024) void finalize_kernel(FinalizePlan fp) {
     *fp.status = bad ? STATUS_NONFINITE : 0u;
   }
 }
+
+__global__ __launch_bounds__(1024) void finalize_kernel(FinalizePlan fp) { finalize_block<16>(fp); }
 
 hipError_t launch_finalize(const FinalizePlan& fp, hipStream_t s) {
   hipLaunchKernelGGL(finalize_kernel, dim3(1), dim3(1024), 0, s, fp);
@@ -275,11 +278,10 @@ __device__ __forceinline__ uint64_t bhq_key(const float* rmin, const float* rmax
 }
 
 // Keys of one 1024-row chunk, bitonic-sorted in LDS.
-__global__ __launch_bounds__(512) void bhq_sort_chunks_kernel(const float* rmin, const float* rmax, int64_t rows,
-                                                              uint64_t* sorted) {
+__device__ void bhq_sort_chunk(const float* rmin, const float* rmax, int64_t rows, uint64_t* sorted, int64_t chunk) {
   __shared__ uint64_t sk[SORT_CH];
   const int t = threadIdx.x;
-  const int64_t base = (int64_t)blockIdx.x * SORT_CH;
+  const int64_t base = chunk * SORT_CH;
   sk[t] = bhq_key(rmin, rmax, rows, base + t);
   sk[t + 512] = bhq_key(rmin, rmax, rows, base + t + 512);
   for (int size = 2; size <= SORT_CH; size <<= 1) {
@@ -298,6 +300,16 @@ __global__ __launch_bounds__(512) void bhq_sort_chunks_kernel(const float* rmin,
   __syncthreads();
   sorted[base + t] = sk[t];
   sorted[base + t + 512] = sk[t + 512];
+}
+
+// The chunk sorts (blocks [0, nch)) and, when the row ranges come straight
+// from the statistics kernel, the finalize step (block nch) in one launch.
+__global__ __launch_bounds__(512) void bhq_sort_chunks_kernel(const float* rmin, const float* rmax, int64_t rows,
+                                                              uint64_t* sorted, int64_t nch, FinalizePlan fp) {
+  if ((int64_t)blockIdx.x < nch)
+    bhq_sort_chunk(rmin, rmax, rows, sorted, blockIdx.x);
+  else
+    finalize_block<8>(fp);
 }
 
 // rank(key) = number of keys below it, summed over every sorted chunk.
@@ -463,14 +475,18 @@ BhqPlanWs bhq_plan_carve(void* plan_ws, int64_t rows) {
 }
 
 hipError_t launch_bhq_plan(const float* rmin, const float* rmax, const BhqLayout& L, int bits, void* plan_ws,
-                           int32_t* perm, float* scale, float* zero, int32_t* group_off, hipStream_t s) {
+                           int32_t* perm, float* scale, float* zero, int32_t* group_off, const FinalizePlan* fin,
+                           hipStream_t s) {
   const int64_t rows = L.rows;
   const int64_t np = sort_pad(rows);
   const int64_t nch = np / SORT_CH;
   if (nch > 65535 || L.G > 0x7FFFFFFF) return hipErrorInvalidValue;
   const BhqPlanWs w = bhq_plan_carve(plan_ws, rows);
-  // w.rank must be zero here (the finalize kernel clears it)
-  hipLaunchKernelGGL(bhq_sort_chunks_kernel, dim3((unsigned)nch), dim3(512), 0, s, rmin, rmax, rows, w.sorted);
+  // w.rank must be zero before the rank kernel: the finalize step clears it,
+  // either before this call or (fin) in the sort launch
+  const FinalizePlan none{};
+  hipLaunchKernelGGL(bhq_sort_chunks_kernel, dim3((unsigned)(nch + (fin ? 1 : 0))), dim3(512), 0, s, rmin, rmax, rows,
+                     w.sorted, nch, fin ? *fin : none);
   hipLaunchKernelGGL(bhq_rank_kernel, dim3((unsigned)nch, (unsigned)nch), dim3(256), 0, s, w.sorted, w.rank);
   hipLaunchKernelGGL(bhq_scatter_kernel, dim3((unsigned)((rows + 255) / 256)), dim3(256), 0, s, w.rank, rows,
                      w.sigma);
@@ -541,13 +557,14 @@ __device__ __forceinline__ int32_t wave_sum16(int32_t (&v)[16], int lane) {
 // VEC: cols % 4 == 0 (float4 loads, one Philox block per lane and row).
 // TRANS: the primary codes go out transposed ([cols, rows], column sums)
 // instead of in natural order ([rows, cols], row sums).
+// One 64 x 256 tile: column tile bx, slot tile by.
 template <int MODE, int K, bool HAS2, bool VEC, bool TRANS>
-__global__ __launch_bounds__(256) void quant_tile_kernel(QuantParams p) {
+__device__ __forceinline__ void quant_tile(const QuantParams& p, int64_t bx, int64_t by) {
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform: slot bookkeeping stays scalar
-  const int64_t tile0 = (int64_t)blockIdx.y * QT_SLOTS;
+  const int64_t tile0 = by * QT_SLOTS;
   const int64_t slot0 = tile0 + wave * QT_ROWS_PER_WAVE;
-  const int64_t c0 = (int64_t)blockIdx.x * QT_COLS + lane * 4;
+  const int64_t c0 = bx * QT_COLS + lane * 4;
   const int64_t rows = p.rows, cols = p.cols;
   const int B = (1 << p.bits) - 1;
   const int half = 1 << (p.bits - 1);
@@ -810,7 +827,7 @@ __global__ __launch_bounds__(256) void quant_tile_kernel(QuantParams p) {
     }
     __syncthreads();
     const int c = threadIdx.x;  // 256 threads = 256 columns of the tile
-    const int64_t col = (int64_t)blockIdx.x * QT_COLS + c;
+    const int64_t col = bx * QT_COLS + c;
     if (col < cols) {
       if (TRANS && p.sum_t) {
         const int t = s_csum[0][0][c] + s_csum[0][1][c] + s_csum[0][2][c] + s_csum[0][3][c];
@@ -824,6 +841,24 @@ __global__ __launch_bounds__(256) void quant_tile_kernel(QuantParams p) {
   }
 }
 
+
+template <int MODE, int K, bool HAS2, bool VEC, bool TRANS>
+__global__ __launch_bounds__(256) void quant_tile_kernel(QuantParams p) {
+  quant_tile<MODE, K, HAS2, VEC, TRANS>(p, blockIdx.x, blockIdx.y);
+}
+
+// Two independent per-tensor transposed quantizations in one launch (Q_f(X)
+// and Q_theta(W)): blocks [0, nb0) tile the first, the rest the second, each
+// over a row-major grid of ct column tiles.
+template <bool VEC>
+__global__ __launch_bounds__(256) void quant_tile2_kernel(QuantParams p0, QuantParams p1, int64_t nb0, int64_t ct0,
+                                                          int64_t ct1) {
+  const int64_t b = blockIdx.x;
+  if (b < nb0)
+    quant_tile<QM_TENSOR, 0, false, VEC, true>(p0, b % ct0, b / ct0);
+  else
+    quant_tile<QM_TENSOR, 0, false, VEC, true>(p1, (b - nb0) % ct1, (b - nb0) / ct1);
+}
 
 template <int MODE, int K>
 static hipError_t launch_quant_k(const QuantParams& p, hipStream_t s) {
@@ -852,6 +887,22 @@ static hipError_t launch_quant_k(const QuantParams& p, hipStream_t s) {
     else
       hipLaunchKernelGGL((quant_tile_kernel<MODE, K, false, false, false>), grid, dim3(256), 0, s, p);
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_quant_pair(const QuantParams& p0, const QuantParams& p1, hipStream_t s) {
+  for (const QuantParams* p : {&p0, &p1})
+    if (p->q_nat || p->sum_nat || p->q2_t || !p->q_t) return hipErrorInvalidValue;
+  const int64_t ct0 = (p0.cols + QT_COLS - 1) / QT_COLS, rt0 = (p0.rows + QT_SLOTS - 1) / QT_SLOTS;
+  const int64_t ct1 = (p1.cols + QT_COLS - 1) / QT_COLS, rt1 = (p1.rows + QT_SLOTS - 1) / QT_SLOTS;
+  const int64_t nb0 = ct0 * rt0, nb = nb0 + ct1 * rt1;
+  if (nb > 0x7FFFFFFF) return hipErrorInvalidValue;
+  const bool vec = (p0.cols % 4 == 0) && (((uintptr_t)p0.x & 15) == 0) && (p1.cols % 4 == 0) &&
+                   (((uintptr_t)p1.x & 15) == 0);
+  if (vec)
+    hipLaunchKernelGGL(quant_tile2_kernel<true>, dim3((unsigned)nb), dim3(256), 0, s, p0, p1, nb0, ct0, ct1);
+  else
+    hipLaunchKernelGGL(quant_tile2_kernel<false>, dim3((unsigned)nb), dim3(256), 0, s, p0, p1, nb0, ct0, ct1);
   return hipGetLastError();
 }
 
