@@ -529,26 +529,35 @@ __device__ __forceinline__ void rne4(const float (&y)[4], float Bf, uint32_t hof
   for (int j = 0; j < 4; ++j) t[j] = rne_top(y[j], Bf, hoff);
 }
 
-// Sums over the 64 lanes of each of 16 per-lane values v[0..15], by halving
-// exchanges (lanes differing in bit 5 swap halves of the list, then bit 4,
-// ...): lane l with l % 4 == 0 returns the sum of v[l / 4].
-__device__ __forceinline__ int32_t wave_sum16(int32_t (&v)[16], int lane) {
+// Sums over the 64 lanes of each of 4 per-lane values v[0..3], by halving
+// exchanges (lanes differing in bit 5 swap halves of the list, then bit 4),
+// then a plain tree over the low 4 lane bits: lane l with l % 16 == 0
+// returns the sum of v[l / 16].
+__device__ __forceinline__ int32_t wave_sum4(int32_t (&v)[4], int lane) {
+  // bitwise selects (one v_bfi each): a conditional between two list
+  // entries would be turned into a dynamically indexed register read
+  const int32_t m32 = (lane & 32) ? -1 : 0;
 #pragma unroll
-  for (int half = 8, bit = 32; half >= 1; half >>= 1, bit >>= 1) {
-    // bitwise selects (one v_bfi each): a conditional between two list
-    // entries would be turned into a dynamically indexed register read
-    const int32_t m = (lane & bit) ? -1 : 0;
-#pragma unroll
-    for (int i = 0; i < half; ++i) {
-      const int32_t keep = (v[i + half] & m) | (v[i] & ~m);
-      const int32_t give = (v[i] & m) | (v[i + half] & ~m);
-      v[i] = keep + __shfl_xor(give, bit);
-    }
+  for (int i = 0; i < 2; ++i) {
+    const int32_t keep = (v[i + 2] & m32) | (v[i] & ~m32);
+    const int32_t give = (v[i] & m32) | (v[i + 2] & ~m32);
+    v[i] = keep + __shfl_xor(give, 32);
   }
-  int32_t s = v[0];
+  const int32_t m16 = (lane & 16) ? -1 : 0;
+  const int32_t keep = (v[1] & m16) | (v[0] & ~m16);
+  const int32_t give = (v[0] & m16) | (v[1] & ~m16);
+  int32_t s = keep + __shfl_xor(give, 16);
+  s += __shfl_xor(s, 8);
+  s += __shfl_xor(s, 4);
   s += __shfl_xor(s, 2);
   s += __shfl_xor(s, 1);
   return s;
+}
+
+// w with byte b replaced by the top byte of v (b is a constant after unrolling).
+__device__ __forceinline__ uint32_t insert_top(uint32_t w, int32_t v, int b) {
+  const uint32_t sel = b == 0 ? 0x03020107u : (b == 1 ? 0x03020700u : (b == 2 ? 0x03070100u : 0x07020100u));
+  return __builtin_amdgcn_perm((uint32_t)v, w, sel);
 }
 
 // Tile = 64 slots x 256 columns; 4 waves of 16 slots; 4 columns per lane.
@@ -654,9 +663,15 @@ __device__ __forceinline__ void quant_tile(const QuantParams& p, int64_t bx, int
 #pragma unroll
   for (int j = 0; j < 4; ++j)
     if (c0 + j < cols) colmask |= 0xFFu << (8 * j);
-  int32_t rsum[QT_ROWS_PER_WAVE];  // per-lane partial row sums of the natural codes
-  uint32_t tq[4][4], tq2[4][4];    // transposed codes: [column][4 words of 16 slots]
-  int32_t tp[4][4], tp2[4][4];     // top-byte codes of the current 4 rows: [row % 4][column]
+  int32_t rs4[4];                // per-lane partial row sums of the natural codes, 4 rows at a time
+  uint32_t tq[4][4], tq2[4][4];  // transposed codes: [column][4 words of 16 slots]; rows past the end stay 0
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      tq[j][w] = 0u;
+      tq2[j][w] = 0u;
+    }
   const float s_t = (MODE == QM_TENSOR) ? p.scale[0] : 0.0f;
   const float z_t = (MODE == QM_TENSOR) ? p.zero[0] : 0.0f;
   float Bf2 = 0.0f, s2 = 0.0f, z2 = 0.0f;
@@ -743,8 +758,10 @@ __device__ __forceinline__ void quant_tile(const QuantParams& p, int64_t bx, int
       for (int j = 0; j < 4; ++j) y2[j] = s2 * (g[r][j] - z2);
       int32_t t2[4];
       sr4<VEC>(y2, e0, p.seed, p.stream2, Bf2, hoff2, t2);
+      if (ok) {
 #pragma unroll
-      for (int j = 0; j < 4; ++j) tp2[r & 3][j] = t2[j];
+        for (int j = 0; j < 4; ++j) tq2[j][r >> 2] = insert_top(tq2[j][r >> 2], t2[j], r & 3);
+      }
     }
     if constexpr (!TRANS) {
       const uint32_t w = pack_top4(t[0], t[1], t[2], t[3]);
@@ -758,29 +775,16 @@ __device__ __forceinline__ void quant_tile(const QuantParams& p, int64_t bx, int
             if (c0 + j < cols) dst[j] = (int8_t)(t[j] >> 24);
         }
       }
-      rsum[r] = sum4_i8(w & colmask, 0);
-    } else {
-#pragma unroll
-      for (int j = 0; j < 4; ++j) tp[r & 3][j] = t[j];
-    }
-    if ((r & 3) == 3) {
-      // rows past the matrix end contribute zero bytes to the column sums
-      const int64_t nval = rows - (slot0 + (r - 3));
-      const uint32_t rowmask = nval >= 4 ? 0xFFFFFFFFu : (nval <= 0 ? 0u : (0xFFFFFFFFu >> (8 * (4 - nval))));
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        if constexpr (TRANS) tq[j][r >> 2] = pack_top4(tp[0][j], tp[1][j], tp[2][j], tp[3][j]) & rowmask;
-        if constexpr (HAS2) tq2[j][r >> 2] = pack_top4(tp2[0][j], tp2[1][j], tp2[2][j], tp2[3][j]) & rowmask;
+      rs4[r & 3] = sum4_i8(w & colmask, 0);
+      // row sums of the natural codes: one exchange tree per 4 rows
+      if ((r & 3) == 3 && p.sum_nat) {
+        const int32_t t = wave_sum4(rs4, lane);
+        const int64_t sl = slot0 + (r - 3) + (lane >> 4);
+        if ((lane & 15) == 0 && sl < rows) atomicAdd(p.sum_nat + sl, t);
       }
-    }
-  }
-
-  // ---- row sums of the natural codes: one exchange tree for the 16 rows
-  if constexpr (!TRANS) {
-    if (p.sum_nat) {
-      const int32_t t = wave_sum16(rsum, lane);
-      const int64_t slot = slot0 + (lane >> 2);
-      if ((lane & 3) == 0 && slot < rows) atomicAdd(p.sum_nat + slot, t);
+    } else if (ok) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) tq[j][r >> 2] = insert_top(tq[j][r >> 2], t[j], r & 3);
     }
   }
 
