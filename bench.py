@@ -23,6 +23,15 @@ QB_X = ("bhq", 5, 64)
 QB_W = ("ptq", 8, 0)
 HBM_PEAK_GBS = 8000.0            # MI355X HBM3E
 INT8_PEAK_TOPS = 5000.0          # MI355X dense int8 matrix cores
+# vector ALU issue: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz, one 32-bit op per lane per cycle
+VALU_PEAK_TOPS = 256 * 4 * 16 * 2.4e9 / 1e12
+# vector ops per element of the quantizer pass (quantizer roofline):
+# gradient element: two Philox4x32-10 words (10 ops each: a quarter of 10 rounds
+# of 2 wide multiplies + 2 three-way xors), Householder column sum 2, transform 3,
+# stochastic rounding 7 (x2), per-tensor transform 2, packing and code sums 2;
+# X / W element: transform 2, round-half-even 4, packing and sums 1
+OPS_PER_G = 2 * 10 + 2 + 3 + 7 + 2 + 7 + 2
+OPS_PER_XW = 2 + 4 + 1
 CPU_SAMPLE_ROWS = 256
 
 
@@ -40,7 +49,7 @@ def parse():
 TRAFFIC_FILE = os.path.join(os.path.dirname(os.path.abspath(__file__)), "profiles", "traffic_linear_ffn_bhq5.txt")
 # kernel of each phase in the rocprofv3 summaries (name prefixes)
 PHASE_KERNEL = {
-    "quant_G": ("quant_tile_kernel<2, 64, true, true>",),
+    "quant_G": ("quant_fused_kernel<2, 64>",),
     "gemm_gradX": ("gemm_i8_kernel", ", 3, 64, true>"),
     "gemm_gradW": ("gemm_i8_kernel", ", 1, 0, true>"),
 }
@@ -130,7 +139,10 @@ def main():
     gemm_ops = 2.0 * N * D_IN * D_OUT               # per contraction
     value = 2.0 * gemm_ops / (ms_step * 1e-3) / 1e12
     nd = float(N) * D_OUT
-    quant_bytes = 4 * nd + 2 * nd                   # read G, write Q_b2 and Q_b1 codes
+    nxw = float(N) * D_IN + float(D_OUT) * D_IN
+    # the quantizer launch: read G, write Q_b2 and Q_b1 codes; read X and W, write their codes
+    quant_bytes = (4 + 2) * nd + (4 + 1) * nxw
+    quant_ops = OPS_PER_G * nd + OPS_PER_XW * nxw
     t_quant_g = phases["quant_G"] * 1e-3
     t_quantizer = (phases["stats"] + phases["scales_plan"] + phases["quant_G"]) * 1e-3
     kernels = {
@@ -138,15 +150,18 @@ def main():
                        "peak": INT8_PEAK_TOPS, "scale": 1e12},
         "gemm_gradW": {"bound": "mfma", "t": phases["gemm_gradW"] * 1e-3, "work": gemm_ops, "unit": "TFLOP/s",
                        "peak": INT8_PEAK_TOPS, "scale": 1e12},
-        "quant_G": {"bound": "hbm", "t": t_quant_g, "work": quant_bytes, "unit": "GB/s", "peak": HBM_PEAK_GBS,
-                    "scale": 1e9},
+        # ALU-bound: at peak its vector ops take longer than its HBM bytes
+        "quant_G": {"bound": "alu", "t": t_quant_g, "work": quant_ops, "unit": "TOP/s", "peak": VALU_PEAK_TOPS,
+                    "scale": 1e12},
+        "quant_G_hbm": {"bound": "hbm", "t": t_quant_g, "work": quant_bytes, "unit": "GB/s", "peak": HBM_PEAK_GBS,
+                        "scale": 1e9},
     }
     per_kernel = {}
     for name, k in kernels.items():
         ach = k["work"] / k["t"] / k["scale"]
         per_kernel[name] = {"bound": k["bound"], "achieved": round(ach, 2), "peak": k["peak"], "unit": k["unit"],
                             "frac": round(ach / k["peak"], 4), "ms": round(k["t"] * 1e3, 4)}
-    dom = max(kernels, key=lambda n: kernels[n]["t"])
+    dom = max((n for n in kernels if n != "quant_G_hbm"), key=lambda n: kernels[n]["t"])
     roof = dict(per_kernel[dom])
     roof.pop("ms")
     roof["kernel"] = dom

@@ -469,15 +469,14 @@ fqt_status fqt_linear_backward(const float* X, const float* W, const float* G, i
   pg.sum2_t = w.sum_g1;
   pg.L = L;
   // Q_b2(G) [N, d_out] slot order (stream 1) and Q_b1(G) [d_out, N] (stream 0)
-  // from one read of G
-  // Q_f(X) and Q_theta(W) in one launch (phase 3; phase 4 stays empty)
+  // from one read of G, with Q_f(X) and Q_theta(W) in the same launch (phase
+  // 5; phases 3 and 4 stay empty)
   tr.begin(3);
-  FQT_TRY(launch_quant_pair(px, pw, s));
   tr.end(3);
   tr.begin(4);
   tr.end(4);
   tr.begin(5);
-  FQT_TRY(launch_quant(pg, mode, s));
+  FQT_TRY(launch_quant_fused(pg, mode, px, pw, s));
   tr.end(5);
 
   // grad_W [d_out, d_in] = Q_b1(G)^T Q_f(X): contraction over the N samples

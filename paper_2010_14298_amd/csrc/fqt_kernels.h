@@ -133,6 +133,11 @@ enum QuantMode { QM_TENSOR = 0, QM_ROW = 1, QM_BHQ = 2 };
 hipError_t launch_quant(const QuantParams& p, int mode, hipStream_t s);
 // Two per-tensor quantizations with transposed outputs only, one launch.
 hipError_t launch_quant_pair(const QuantParams& p0, const QuantParams& p1, hipStream_t s);
+// The gradient quantizer pg (with its transposed second quantizer) and the
+// per-tensor transposed quantizers px, pw in one launch when the shapes
+// allow it, else as separate launches.
+hipError_t launch_quant_fused(const QuantParams& pg, int mode, const QuantParams& px, const QuantParams& pw,
+                              hipStream_t s);
 
 // Narrow transposing per-tensor quantizer (conv activations and Q_b1 of a
 // conv gradient): logical [rows, cols], row r of the output taken from source

@@ -864,6 +864,45 @@ __global__ __launch_bounds__(256) void quant_tile2_kernel(QuantParams p0, QuantP
     quant_tile<QM_TENSOR, 0, false, VEC, true>(p1, (b - nb0) % ct1, (b - nb0) / ct1);
 }
 
+// The gradient pass (natural codes plus the transposed Q_b1) and the two
+// per-tensor transposed passes (Q_f(X), Q_theta(W)) in one grid.  Every
+// period-th block (while they last) is an X / W tile, so that those
+// memory-light tiles interleave with the arithmetic-heavy gradient tiles;
+// the other blocks take the gradient tiles in order.
+template <int MODE, int K>
+__global__ __launch_bounds__(256) void quant_fused_kernel(QuantParams pg, QuantParams px, QuantParams pw, int64_t nbx,
+                                                          int64_t nbw, int64_t period, int64_t ctg, int64_t ctx,
+                                                          int64_t ctw) {
+  const int64_t b = blockIdx.x;
+  const int64_t nxw = nbx + nbw;
+  if (b % period == period - 1 && b / period < nxw) {
+    const int64_t t = b / period;
+    if (t < nbx)
+      quant_tile<QM_TENSOR, 0, false, true, true>(px, t % ctx, t / ctx);
+    else
+      quant_tile<QM_TENSOR, 0, false, true, true>(pw, (t - nbx) % ctw, (t - nbx) / ctw);
+  } else {
+    const int64_t before = (b + 1) / period < nxw ? (b + 1) / period : nxw;
+    const int64_t t = b - before;
+    quant_tile<MODE, K, true, true, false>(pg, t % ctg, t / ctg);
+  }
+}
+
+template <int MODE, int K>
+static hipError_t launch_quant_fused_k(const QuantParams& pg, const QuantParams& px, const QuantParams& pw,
+                                       hipStream_t s) {
+  const int64_t ctg = (pg.cols + QT_COLS - 1) / QT_COLS, rtg = (pg.rows + QT_SLOTS - 1) / QT_SLOTS;
+  const int64_t ctx = (px.cols + QT_COLS - 1) / QT_COLS, rtx = (px.rows + QT_SLOTS - 1) / QT_SLOTS;
+  const int64_t ctw = (pw.cols + QT_COLS - 1) / QT_COLS, rtw = (pw.rows + QT_SLOTS - 1) / QT_SLOTS;
+  const int64_t nbg = ctg * rtg, nbx = ctx * rtx, nbw = ctw * rtw;
+  const int64_t nb = nbg + nbx + nbw;
+  if (nb > 0x7FFFFFFF) return hipErrorInvalidValue;
+  const int64_t period = nb / (nbx + nbw);
+  hipLaunchKernelGGL((quant_fused_kernel<MODE, K>), dim3((unsigned)nb), dim3(256), 0, s, pg, px, pw, nbx, nbw, period,
+                     ctg, ctx, ctw);
+  return hipGetLastError();
+}
+
 template <int MODE, int K>
 static hipError_t launch_quant_k(const QuantParams& p, hipStream_t s) {
   const int64_t ct = (p.cols + QT_COLS - 1) / QT_COLS;
@@ -908,6 +947,32 @@ hipError_t launch_quant_pair(const QuantParams& p0, const QuantParams& p1, hipSt
   else
     hipLaunchKernelGGL(quant_tile2_kernel<false>, dim3((unsigned)nb), dim3(256), 0, s, p0, p1, nb0, ct0, ct1);
   return hipGetLastError();
+}
+
+hipError_t launch_quant_fused(const QuantParams& pg, int mode, const QuantParams& px, const QuantParams& pw,
+                              hipStream_t s) {
+  // float4 rows everywhere, natural + transposed Q_b1 for the gradient,
+  // transposed only for X and W; anything else goes out as three launches
+  auto vec = [](const QuantParams& p) { return (p.cols % 4 == 0) && (((uintptr_t)p.x & 15) == 0); };
+  const bool shape = vec(pg) && vec(px) && vec(pw) && pg.q2_t && pg.stoch && !pg.q_t && !pg.sum_t && !px.q_nat &&
+                     !px.sum_nat && !px.q2_t && px.q_t && !pw.q_nat && !pw.sum_nat && !pw.q2_t && pw.q_t;
+  if (!shape) {
+    hipError_t e = launch_quant_pair(px, pw, s);
+    if (e != hipSuccess) return e;
+    return launch_quant(pg, mode, s);
+  }
+  if (mode == QM_TENSOR) return launch_quant_fused_k<QM_TENSOR, 0>(pg, px, pw, s);
+  if (mode == QM_ROW) return launch_quant_fused_k<QM_ROW, 0>(pg, px, pw, s);
+  switch (pg.L.k) {
+    case 1: return launch_quant_fused_k<QM_BHQ, 1>(pg, px, pw, s);
+    case 2: return launch_quant_fused_k<QM_BHQ, 2>(pg, px, pw, s);
+    case 4: return launch_quant_fused_k<QM_BHQ, 4>(pg, px, pw, s);
+    case 8: return launch_quant_fused_k<QM_BHQ, 8>(pg, px, pw, s);
+    case 16: return launch_quant_fused_k<QM_BHQ, 16>(pg, px, pw, s);
+    case 32: return launch_quant_fused_k<QM_BHQ, 32>(pg, px, pw, s);
+    case 64: return launch_quant_fused_k<QM_BHQ, 64>(pg, px, pw, s);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 hipError_t launch_quant(const QuantParams& p, int mode, hipStream_t s) {
