@@ -744,8 +744,10 @@ size_t fqt_conv_backward_workspace(const fqt_conv_shape* shape, const fqt_bwd_cf
 fqt_status fqt_workspace_status(const void* ws, fqt_stream_t s) {
   if (!ws) return FQT_EINVAL;
   if (hipStreamSynchronize(s) != hipSuccess) return FQT_EDEVICE;
+  uint32_t words[STATUS_WORDS] = {};
+  if (hipMemcpy(words, ws, sizeof(words), hipMemcpyDeviceToHost) != hipSuccess) return FQT_EDEVICE;
   uint32_t word = 0;
-  if (hipMemcpy(&word, ws, sizeof(word), hipMemcpyDeviceToHost) != hipSuccess) return FQT_EDEVICE;
+  for (int i = 0; i < STATUS_WORDS; ++i) word |= words[i];
   return (word & STATUS_NONFINITE) ? FQT_ENONFINITE : FQT_OK;
 }
 

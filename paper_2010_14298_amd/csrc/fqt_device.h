@@ -129,5 +129,6 @@ __device__ __forceinline__ float scale_from_range(float R, int B) {
 
 // Status word bits (first word of every workspace).
 constexpr uint32_t STATUS_NONFINITE = 1u;
+constexpr int STATUS_WORDS = 4;  // one per statistics segment; the workspace header reserves 64
 
 }  // namespace fqt

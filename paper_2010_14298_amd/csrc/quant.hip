@@ -143,89 +143,85 @@ hipError_t launch_stats(StatsPlan sp, hipStream_t s) {
 }
 
 // ---------------------------------------------------------------------------
-// finalize: one 1024-thread block.  Combines the partials into per-tensor and
-// per-row ranges, writes the PTQ scale / zero (Sec. 3.3) and PSQ per-row
-// scales / zeros (Sec. 4.1), clears the code-sum and rank arrays, and sets
-// the status word (non-finite input, or a range beyond float32).
+// finalize: one block per statistics segment.  Block si combines segment
+// si's partials into its per-tensor range (and, for the per-row segment, the
+// per-row ranges), writes the PTQ scale / zero (Sec. 3.3) and PSQ per-row
+// scales / zeros (Sec. 4.1) that derive from it, clears its share of the
+// code-sum / rank arrays, and records a non-finite input or a range beyond
+// float32 in status word si.
 // ---------------------------------------------------------------------------
 template <int NW>
-__device__ void finalize_block(const FinalizePlan& fp) {
+__device__ void finalize_block(const FinalizePlan& fp, int si) {
   const int t = threadIdx.x;
-  for (int z = 0; z < fp.nzero; ++z)
-    for (int64_t i = t; i < fp.zero_n[z]; i += blockDim.x) fp.zero_i32[z][i] = 0;
-  __shared__ float seg_mn[3], seg_mx[3];
-  __shared__ int seg_bad[3];
-  for (int si = 0; si < fp.nseg; ++si) {
-    const StatsSeg& g = fp.seg[si];
-    float mn = INFINITY, mx = -INFINITY;
-    int bad = 0;
-    if (si == fp.row_seg && g.rmin) {
-      // row ranges already stored by the stats blocks: a load-only reduction
-      // (no stores in the loop, so the loads of several rows are in flight)
+  const int nparts = fp.nseg;
+  for (int z = 0; z < fp.nzero; ++z) {
+    const int64_t n = fp.zero_n[z];
+    const int64_t lo = n * si / nparts, hi = n * (si + 1) / nparts;
+    for (int64_t i = lo + t; i < hi; i += blockDim.x) fp.zero_i32[z][i] = 0;
+  }
+  if (si == 0)
+    for (int w = fp.nseg + t; w < STATUS_WORDS; w += blockDim.x) fp.status[w] = 0u;
+  const StatsSeg& g = fp.seg[si];
+  float mn = INFINITY, mx = -INFINITY;
+  int bad = 0;
+  if (si == fp.row_seg && g.rmin) {
+    // row ranges already stored by the stats blocks: a load-only reduction
+    // (no stores in the loop, so the loads of several rows are in flight)
 #pragma unroll 8
-      for (int64_t r = t; r < g.rows; r += blockDim.x) {
-        const float2 p = g.part[r];
-        const float rmn = fminf(INFINITY, p.x);
-        bad |= isnan(p.x) || !isfinite(p.y - rmn);
-        mn = fminf(mn, rmn);
-        mx = fmaxf(mx, p.y);
-      }
-    } else if (si == fp.row_seg) {
-      for (int64_t r = t; r < g.rows; r += blockDim.x) {
-        float rmn = INFINITY, rmx = -INFINITY;
-        for (int64_t c = 0; c < g.chunks; ++c) {
-          const float2 p = g.part[r * g.chunks + c];
-          if (isnan(p.x)) bad = 1;
-          rmn = fminf(rmn, p.x);
-          rmx = fmaxf(rmx, p.y);
-        }
-        fp.rmin[r] = rmn;
-        fp.rmax[r] = rmx;
-        if (!isfinite(rmx - rmn)) bad = 1;
-        mn = fminf(mn, rmn);
-        mx = fmaxf(mx, rmx);
-      }
-    } else {
-      for (int64_t i = t; i < stats_partials(g); i += blockDim.x) {
-        const float2 p = g.part[i];
-        if (isnan(p.x)) bad = 1;
-        mn = fminf(mn, p.x);
-        mx = fmaxf(mx, p.y);
-      }
+    for (int64_t r = t; r < g.rows; r += blockDim.x) {
+      const float2 p = g.part[r];
+      const float rmn = fminf(INFINITY, p.x);
+      bad |= isnan(p.x) || !isfinite(p.y - rmn);
+      mn = fminf(mn, rmn);
+      mx = fmaxf(mx, p.y);
     }
-    const MinMax r = block_minmax<NW>(mn, mx, bad);
-    if (t == 0) {
-      seg_mn[si] = r.mn;
-      seg_mx[si] = r.mx;
-      seg_bad[si] = r.bad || !isfinite(r.mx - r.mn);
+  } else if (si == fp.row_seg) {
+    for (int64_t r = t; r < g.rows; r += blockDim.x) {
+      float rmn = INFINITY, rmx = -INFINITY;
+      for (int64_t c = 0; c < g.chunks; ++c) {
+        const float2 p = g.part[r * g.chunks + c];
+        if (isnan(p.x)) bad = 1;
+        rmn = fminf(rmn, p.x);
+        rmx = fmaxf(rmx, p.y);
+      }
+      fp.rmin[r] = rmn;
+      fp.rmax[r] = rmx;
+      if (!isfinite(rmx - rmn)) bad = 1;
+      mn = fminf(mn, rmn);
+      mx = fmaxf(mx, rmx);
+    }
+  } else {
+#pragma unroll 8
+    for (int64_t i = t; i < stats_partials(g); i += blockDim.x) {
+      const float2 p = g.part[i];
+      if (isnan(p.x)) bad = 1;
+      mn = fminf(mn, p.x);
+      mx = fmaxf(mx, p.y);
     }
   }
-  __syncthreads();
+  const MinMax r = block_minmax<NW>(mn, mx, bad);
+  if (si == fp.row_seg) __syncthreads();  // per-row ranges of this block visible to all its threads
   for (int o = 0; o < fp.nout; ++o) {
     const ScaleOut& so = fp.out[o];
+    if (so.seg != si) continue;
     const int B = (1 << so.bits) - 1;
     if (so.per_row) {
-      const int64_t rows = fp.seg[so.seg].rows;
-      for (int64_t r = t; r < rows; r += blockDim.x) {
-        so.scale[r] = scale_from_range(fp.rmax[r] - fp.rmin[r], B);
-        so.zero[r] = fp.rmin[r];
+      for (int64_t row = t; row < g.rows; row += blockDim.x) {
+        so.scale[row] = scale_from_range(fp.rmax[row] - fp.rmin[row], B);
+        so.zero[row] = fp.rmin[row];
       }
     } else if (t == 0) {
-      so.scale[0] = scale_from_range(seg_mx[so.seg] - seg_mn[so.seg], B);
-      so.zero[0] = seg_mn[so.seg];
+      so.scale[0] = scale_from_range(r.mx - r.mn, B);
+      so.zero[0] = r.mn;
     }
   }
-  if (t == 0) {
-    int bad = 0;
-    for (int si = 0; si < fp.nseg; ++si) bad |= seg_bad[si];
-    *fp.status = bad ? STATUS_NONFINITE : 0u;
-  }
+  if (t == 0) fp.status[si] = (r.bad || !isfinite(r.mx - r.mn)) ? STATUS_NONFINITE : 0u;
 }
 
-__global__ __launch_bounds__(1024) void finalize_kernel(FinalizePlan fp) { finalize_block<16>(fp); }
+__global__ __launch_bounds__(1024) void finalize_kernel(FinalizePlan fp) { finalize_block<16>(fp, blockIdx.x); }
 
 hipError_t launch_finalize(const FinalizePlan& fp, hipStream_t s) {
-  hipLaunchKernelGGL(finalize_kernel, dim3(1), dim3(1024), 0, s, fp);
+  hipLaunchKernelGGL(finalize_kernel, dim3((unsigned)fp.nseg), dim3(1024), 0, s, fp);
   return hipGetLastError();
 }
 
@@ -309,7 +305,7 @@ __global__ __launch_bounds__(512) void bhq_sort_chunks_kernel(const float* rmin,
   if ((int64_t)blockIdx.x < nch)
     bhq_sort_chunk(rmin, rmax, rows, sorted, blockIdx.x);
   else
-    finalize_block<8>(fp);
+    finalize_block<8>(fp, (int)(blockIdx.x - nch));
 }
 
 // rank(key) = number of keys below it, summed over every sorted chunk.
@@ -340,6 +336,108 @@ __global__ __launch_bounds__(256) void bhq_rank_kernel(const uint64_t* sorted, i
 __global__ void bhq_scatter_kernel(const int32_t* rank, int64_t rows, int32_t* sigma) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i < rows) sigma[rank[i]] = (int32_t)i;
+}
+
+// First slot of group g under the fixed-block layout: full groups, then the
+// partial one, then the one-row groups.
+__device__ __forceinline__ int64_t bhq_group_base(const BhqLayout& L, int64_t g) {
+  if (g < L.full) return g * L.k;
+  if (g == L.full && L.part > 0) return L.full * L.k;
+  return L.full * L.k + L.part + (g - L.full - (L.part > 0 ? 1 : 0));
+}
+
+// Slot of the row whose sorted position is r: the G largest rows lead the
+// groups (position g -> group g, slot 0); the rest fill the groups' other
+// slots k - 1 at a time, in sorted order.
+__device__ __forceinline__ int64_t bhq_slot_of_rank(const BhqLayout& L, int64_t r) {
+  if (r < L.G || L.k <= 1) return bhq_group_base(L, r);
+  const int64_t q = r - L.G;
+  const int64_t g = q / (L.k - 1);
+  return bhq_group_base(L, g) + 1 + q % (L.k - 1);
+}
+
+// Sorted position of every row by counting, for up to RANK_MAX_ROWS rows:
+// rank_i = #{j : M_j > M_i, or M_j = M_i and j < i}, the number of keys that
+// sort before row i (M = row infinity norm compared as float32 bits, which
+// orders the non-negative values exactly as bhq_key does).  The bits of all
+// M are staged in LDS once, zero padded to a multiple of 256 (a padding key
+// never counts: it exceeds no M, and equals M_i only at j > i).  Each wave
+// owns 4 consecutive rows r0 .. r0 + 3, which share the 4-key group r0 / 4;
+// its 64 lanes split the key groups, so one LDS read feeds 16 comparisons:
+// keys before that group count when >= M_i, keys after it when > M_i, and
+// the shared group takes the exact test.  The row is then stored at its slot
+// of perm.  Blocks nrank .. nrank + nseg - 1 run the finalize step.
+constexpr int RK_THREADS = 512;
+constexpr int RK_ROWS = RK_THREADS / 64 * 4;
+constexpr int64_t RANK_MAX_ROWS = 16384;  // keys staged in at most 64 KB of LDS
+
+__host__ __device__ inline int64_t rank_pad(int64_t rows) { return (rows + 255) / 256 * 256; }
+
+__global__ __launch_bounds__(RK_THREADS) void bhq_rank_perm_kernel(const float* rmin, const float* rmax, BhqLayout L,
+                                                                   int32_t* perm, int64_t nrank, FinalizePlan fp) {
+  if ((int64_t)blockIdx.x >= nrank) {
+    finalize_block<RK_THREADS / 64>(fp, (int)(blockIdx.x - nrank));
+    return;
+  }
+  extern __shared__ uint4 rk_lds[];
+  uint32_t* mk = reinterpret_cast<uint32_t*>(rk_lds);
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  const int rows = (int)L.rows;
+  const int npad = (int)rank_pad(rows);
+  // all loads of a round in flight before the LDS stores
+  constexpr int U = 16;
+  for (int base = 0; base < npad; base += RK_THREADS * U) {
+    float lo[U], hi[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int e = base + t + u * RK_THREADS;
+      lo[u] = e < rows ? rmin[e] : 0.0f;
+      hi[u] = e < rows ? rmax[e] : 0.0f;
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int e = base + t + u * RK_THREADS;
+      if (e < npad) mk[e] = e < rows ? __float_as_uint(fmaxf(fabsf(lo[u]), fabsf(hi[u]))) : 0u;
+    }
+  }
+  __syncthreads();
+  const int r0 = (int)blockIdx.x * RK_ROWS + wave * 4;
+  const int gs = r0 / 4;
+  uint32_t mu[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) mu[q] = r0 + q < rows ? mk[r0 + q] : 0xFFFFFFFFu;
+  int cnt[4] = {0, 0, 0, 0};
+  const int ng = npad / 4;
+  int gi = lane;
+#pragma unroll 2
+  for (; gi < gs; gi += 64) {
+    const uint4 v = rk_lds[gi];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) cnt[q] += (v.x >= mu[q]) + (v.y >= mu[q]) + (v.z >= mu[q]) + (v.w >= mu[q]);
+  }
+  if (gi == gs && gs < ng) {
+    // key 4 gs + e sorts before row r0 + q when its M is larger, or equal with e < q
+    const uint4 v = rk_lds[gi];
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      cnt[q] += (v.x > mu[q] || (v.x == mu[q] && 0 < q)) + (v.y > mu[q] || (v.y == mu[q] && 1 < q)) +
+                (v.z > mu[q] || (v.z == mu[q] && 2 < q)) + (v.w > mu[q] || (v.w == mu[q] && 3 < q));
+    gi += 64;
+  }
+#pragma unroll 2
+  for (; gi < ng; gi += 64) {
+    const uint4 v = rk_lds[gi];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) cnt[q] += (v.x > mu[q]) + (v.y > mu[q]) + (v.z > mu[q]) + (v.w > mu[q]);
+  }
+#pragma unroll
+  for (int q = 0; q < 4; ++q)
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) cnt[q] += __shfl_xor(cnt[q], o);
+  if (lane < 4 && r0 + lane < rows) {
+    const int c = lane == 0 ? cnt[0] : lane == 1 ? cnt[1] : lane == 2 ? cnt[2] : cnt[3];
+    perm[bhq_slot_of_rank(L, c)] = r0 + lane;
+  }
 }
 
 // Correctly rounded float32 cube root of a positive finite float: a float64
@@ -385,8 +483,9 @@ __device__ __forceinline__ float to_f32_sat(double v) {
   return (f > FLT_MAX_F) ? FLT_MAX_F : f;
 }
 
-// One wave per group: perm, per-slot scale d_p and zero (c_g, or the row min
-// for a one-row group).  Lane j handles the group's slot j + 1.
+// FROM_PERM: perm already holds the rows in slot order (bhq_rank_perm_kernel);
+// otherwise the rows come from sigma (sorted order) and perm is written here.
+template <bool FROM_PERM>
 __global__ __launch_bounds__(64) void bhq_groups_kernel(const float* rmin, const float* rmax, const int32_t* sigma,
                                                         BhqLayout L, int B, int32_t* perm, float* scale, float* zero,
                                                         int32_t* group_off) {
@@ -409,12 +508,12 @@ __global__ __launch_bounds__(64) void bhq_groups_kernel(const float* rmin, const
     group_off[g] = (int32_t)base;
     if (g == L.G - 1) group_off[L.G] = (int32_t)L.rows;
   }
-  const int32_t big = sigma[g];
+  const int32_t big = FROM_PERM ? perm[base] : sigma[g];
   const float mn0 = rmin[big];
   const float mx0 = rmax[big];
   if (kg == 1) {
     if (lane == 0) {
-      perm[base] = big;
+      if (!FROM_PERM) perm[base] = big;
       scale[base] = scale_from_range(mx0 - mn0, B);
       zero[base] = mn0;
     }
@@ -424,7 +523,7 @@ __global__ __launch_bounds__(64) void bhq_groups_kernel(const float* rmin, const
   int32_t r = -1;
   float M = 0.0f;
   if (lane < kg - 1) {
-    r = sigma[tail + lane];
+    r = FROM_PERM ? perm[base + 1 + lane] : sigma[tail + lane];
     M = fmaxf(fabsf(rmin[r]), fabsf(rmax[r]));
   }
   const float m2 = wave_max(M);
@@ -453,12 +552,12 @@ __global__ __launch_bounds__(64) void bhq_groups_kernel(const float* rmin, const
   const double t2 = ((0.5 * (double)lam2) * (double)s2) * sk;
   const float cg = (float)(t1 - t2);
   if (lane == 0) {
-    perm[base] = big;
+    if (!FROM_PERM) perm[base] = big;
     scale[base] = s1;
     zero[base] = cg;
   }
   if (lane < kg - 1) {
-    perm[base + 1 + lane] = r;
+    if (!FROM_PERM) perm[base + 1 + lane] = r;
     scale[base + 1 + lane] = s2;
     zero[base + 1 + lane] = cg;
   }
@@ -482,15 +581,25 @@ hipError_t launch_bhq_plan(const float* rmin, const float* rmax, const BhqLayout
   const int64_t nch = np / SORT_CH;
   if (nch > 65535 || L.G > 0x7FFFFFFF) return hipErrorInvalidValue;
   const BhqPlanWs w = bhq_plan_carve(plan_ws, rows);
+  const FinalizePlan none{};
+  if (rows <= RANK_MAX_ROWS) {
+    // two launches: positions by counting (plus the finalize block), then the groups
+    const int64_t nrank = (rows + RK_ROWS - 1) / RK_ROWS;
+    const size_t lds = (size_t)rank_pad(rows) * 4;
+    hipLaunchKernelGGL(bhq_rank_perm_kernel, dim3((unsigned)(nrank + (fin ? fin->nseg : 0))), dim3(RK_THREADS), lds,
+                       s, rmin, rmax, L, perm, nrank, fin ? *fin : none);
+    hipLaunchKernelGGL(bhq_groups_kernel<true>, dim3((unsigned)L.G), dim3(64), 0, s, rmin, rmax, w.sigma, L,
+                       (1 << bits) - 1, perm, scale, zero, group_off);
+    return hipGetLastError();
+  }
   // w.rank must be zero before the rank kernel: the finalize step clears it,
   // either before this call or (fin) in the sort launch
-  const FinalizePlan none{};
-  hipLaunchKernelGGL(bhq_sort_chunks_kernel, dim3((unsigned)(nch + (fin ? 1 : 0))), dim3(512), 0, s, rmin, rmax, rows,
+  hipLaunchKernelGGL(bhq_sort_chunks_kernel, dim3((unsigned)(nch + (fin ? fin->nseg : 0))), dim3(512), 0, s, rmin, rmax, rows,
                      w.sorted, nch, fin ? *fin : none);
   hipLaunchKernelGGL(bhq_rank_kernel, dim3((unsigned)nch, (unsigned)nch), dim3(256), 0, s, w.sorted, w.rank);
   hipLaunchKernelGGL(bhq_scatter_kernel, dim3((unsigned)((rows + 255) / 256)), dim3(256), 0, s, w.rank, rows,
                      w.sigma);
-  hipLaunchKernelGGL(bhq_groups_kernel, dim3((unsigned)L.G), dim3(64), 0, s, rmin, rmax, w.sigma, L,
+  hipLaunchKernelGGL(bhq_groups_kernel<false>, dim3((unsigned)L.G), dim3(64), 0, s, rmin, rmax, w.sigma, L,
                      (1 << bits) - 1, perm, scale, zero, group_off);
   return hipGetLastError();
 }
