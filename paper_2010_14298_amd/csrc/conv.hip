@@ -22,8 +22,9 @@
 namespace fqt {
 
 // ---------------------------------------------------------------------------
-// narrow transposing per-tensor quantizer: logical [rows, cols] (cols small)
-// -> codes [cols][ldt], rows in slot order; rows in [rows, ldt) get code 0
+// narrow transposing per-tensor quantizer: logical [rows, cols] -> codes
+// [cols][ldt], rows in slot order; rows in [rows, ldt) get code 0.  A block
+// covers 4 * LPR columns (grid.y walks wider rows in chunks of 256).
 // ---------------------------------------------------------------------------
 template <int LPR>
 __global__ __launch_bounds__(256) void quant_narrow_t_kernel(NarrowQParams p) {
@@ -32,7 +33,7 @@ __global__ __launch_bounds__(256) void quant_narrow_t_kernel(NarrowQParams p) {
   const int wave = threadIdx.x >> 6;
   const int q = lane / LPR, cl = lane % LPR;
   const int64_t r0 = (int64_t)blockIdx.x * (4 * RG * 16) + wave * (RG * 16) + q * 16;
-  const int64_t c0 = (int64_t)cl * 4;
+  const int64_t c0 = (int64_t)blockIdx.y * (LPR * 4) + (int64_t)cl * 4;  // column chunks of 4 * LPR
   const int B = (1 << p.bits) - 1;
   const int half = 1 << (p.bits - 1);
   const float s = p.scale[0], z = p.zero[0];
@@ -103,15 +104,16 @@ __global__ __launch_bounds__(256) void quant_narrow_t_kernel(NarrowQParams p) {
 }
 
 hipError_t launch_quant_narrow_t(const NarrowQParams& p, hipStream_t s) {
-  // lanes per row: the smallest power of two covering cols / 4 (at most 64)
+  // lanes per row: the smallest power of two covering cols / 4, at most 64
+  // (wider rows: column chunks of 256 along grid.y)
   const int64_t need = (p.cols + 3) / 4;
   int lpr = 1;
   while (lpr < need && lpr < 64) lpr <<= 1;
-  if (need > 64) return hipErrorInvalidValue;
+  const int64_t chunks = (need + 63) / 64;
   const int64_t rows_per_block = 4 * (64 / lpr) * 16;
   const int64_t blocks = (p.ldt + rows_per_block - 1) / rows_per_block;
-  if (blocks > 0x7FFFFFFF) return hipErrorInvalidValue;
-  const dim3 grid((unsigned)blocks);
+  if (blocks > 0x7FFFFFFF || chunks > 65535) return hipErrorInvalidValue;
+  const dim3 grid((unsigned)blocks, (unsigned)chunks);
   switch (lpr) {
     case 1: hipLaunchKernelGGL(quant_narrow_t_kernel<1>, grid, dim3(256), 0, s, p); break;
     case 2: hipLaunchKernelGGL(quant_narrow_t_kernel<2>, grid, dim3(256), 0, s, p); break;
