@@ -99,23 +99,39 @@ fqt_status fqt_quantize_psq(const float* x, int64_t rows, int64_t cols, int bits
                             uint32_t stream, const fqt_qtensor* out, void* ws, size_t ws_bytes,
                             fqt_stream_t s);
 
-/* Block Householder quantizer, Sec. 4.2 / App. C.4 / App. D, fixed block
- * size k = block_size (a power of two, 1..64; 0, the adaptive grouping,
- * returns FQT_EUNSUPPORTED).  Rows are sorted by infinity norm (descending,
- * ties by row index); G = ceil(rows / k) groups each take one of the G
- * largest rows plus the next k - 1 rows of the sorted tail.  Codes are in
- * slot order, natural layout.  Needs out->q, scale, zero, perm.            */
+/* Block Householder quantizer, Sec. 4.2 / App. C.4 / App. D, block size
+ * k = block_size (a power of two, 1..64), or 0 for the adaptive block size
+ * of fqt_bhq_adaptive_block (then the call waits for `stream` once, to read
+ * the choice).  Rows are sorted by infinity norm (descending, ties by row
+ * index); G = ceil(rows / k) groups each take one of the G largest rows plus
+ * the next k - 1 rows of the sorted tail.  Codes are in slot order, natural
+ * layout.  Needs out->q, scale, zero, perm.                                 */
 fqt_status fqt_quantize_bhq(const float* x, int64_t rows, int64_t cols, int bits, int block_size,
                             uint64_t seed, uint32_t stream, const fqt_qtensor* out, void* ws,
                             size_t ws_bytes, fqt_stream_t s);
 
 size_t fqt_quantize_workspace(fqt_kind kind, int64_t rows, int64_t cols, int block_size);
 
+/* Adaptive grouping of the block Householder quantizer, App. D step 2: of
+ * the block sizes 1, 2, 4, .., 64, the one whose plan (as above) has the
+ * least |S^-1|_F^2, the factor of the variance bound (D/4)|S^-1|_F^2 of Eq.
+ * (matrix-quantizer-variance); ties go to the larger block.  (App. D's own
+ * estimate, sum_i M_i^2 / ((N - G) M_i / sum_j M_j), grows with the number
+ * of groups and would always keep one group; its proportional group sizes
+ * are not offered.)  Evaluated on the device; the call waits for `stream`
+ * and stores the choice in *block_size (host memory).  rows <= 16384
+ * (FQT_EUNSUPPORTED beyond).  Returns FQT_ENONFINITE for non-finite x.     */
+fqt_status fqt_bhq_adaptive_block(const float* x, int64_t rows, int64_t cols, int bits, int* block_size,
+                                  void* ws, size_t ws_bytes, fqt_stream_t s);
+size_t fqt_bhq_adaptive_workspace(int64_t rows, int64_t cols);
+
 /* Quantizer choice for one gradient quantizer. */
 typedef struct {
   fqt_kind kind;   /* FQT_PTQ, FQT_PSQ or FQT_BHQ */
   int bits;        /* 1..8 */
-  int block_size;  /* BHQ only: power of two in 1..64 */
+  int block_size;  /* BHQ only: power of two in 1..64, or 0 for the adaptive block size
+                   * (fqt_bhq_adaptive_block; the call then waits for the stream once,
+                   * and needs N <= 16384) */
 } fqt_qspec;
 
 /* Optional per-phase timing: when fqt_bwd_cfg.trace is non-NULL, the layer

@@ -28,7 +28,10 @@ design notes of the repository):
     both zero give s1 = s2 = 1; a one-row group is a PSQ row;
   * cube roots are correctly rounded float32; the group column sum adds the
     slots in aligned chunks of min(k, 16), each chunk left to right, then the
-    chunk sums left to right.
+    chunk sums left to right;
+  * adaptive grouping (App. D): the block size among 1, 2, 4, .., 64 whose
+    plan has the least |S^-1|_F^2 (App. D's own estimate always selects one
+    group; see bhq_adaptive_block).
 
 Offset codes (what the int8 contractions consume) are code - 2^(b-1).
 """
@@ -286,7 +289,8 @@ def bhq_transform(rows, info):
 
 
 def quantize_bhq(x, bits, k, seed=0, stream=0, plan=None):
-    """Block Householder quantizer with fixed block size k (Sec. 4.2).
+    """Block Householder quantizer with fixed block size k (Sec. 4.2); k = 0
+    takes the adaptive block size of bhq_adaptive_block (App. D).
 
     Codes are returned in slot order (group by group); the SR draw of slot p,
     column j uses element index perm[p] * cols + j (its original position).
@@ -294,6 +298,8 @@ def quantize_bhq(x, bits, k, seed=0, stream=0, plan=None):
     x = np.asarray(x, dtype=np.float32)
     N, D = x.shape
     B = n_bins(bits)
+    if k == 0:
+        k = plan["k"] if plan is not None else bhq_adaptive_block(x, bits)[0]
     if plan is None:
         plan = bhq_plan(x, bits, k)
     code = np.zeros((N, D), np.int64)
@@ -313,6 +319,48 @@ def quantize_bhq(x, bits, k, seed=0, stream=0, plan=None):
         code[base: base + kg] = sr.round_stochastic(y, u, B)
     return dict(kind="bhq", code=code, scale=plan["scale"], zero=plan["zero"], perm=plan["perm"],
                 group_off=plan["group_off"], bits=int(bits), plan=plan, k=k)
+
+
+# Candidate block sizes of the adaptive grouping (groups of at most 64 rows
+# that start at multiples of their size, the layout the fixed-block plan uses).
+ADAPTIVE_BLOCKS = (1, 2, 4, 8, 16, 32, 64)
+
+
+def bhq_scale_norm(plan):
+    """|S^-1|_F^2 of a BHQ plan, the factor of the variance bound (D/4)|S^-1|_F^2
+    (Eq. matrix-quantizer-variance).  S^-1 of a group is diag(s1, s2, .., s2)^-1
+    times an orthogonal reflection, so a group adds 1/s1^2 + (k_g - 1)/s2^2 (a
+    one-row group 1/s^2).  float64; groups added in slot order, left to right.
+    """
+    total = 0.0
+    for info in plan["groups"]:
+        base, kg = info["base"], info["size"]
+        s1 = float(plan["scale"][base])
+        term = 1.0 / (s1 * s1)
+        if kg > 1:
+            s2 = float(plan["scale"][base + 1])
+            term = term + float(kg - 1) * (1.0 / (s2 * s2))
+        total = total + term
+    return total
+
+
+def bhq_adaptive_block(x, bits):
+    """Block size of the adaptive grouping (App. D, step 2).
+
+    App. D loops over the number of groups and keeps the grouping of least
+    estimated variance.  Its estimate, sum_i M_i^2 / ((N - G) M_i / sum M),
+    equals (sum of the G largest M)^2 / (N - G), which grows with G, so read
+    literally it always keeps one group.  Here the estimate is the exact bound
+    factor |S^-1|_F^2 of each candidate plan, and the candidates are the
+    fixed-block plans with k in ADAPTIVE_BLOCKS (G = ceil(N / k)).  Ties go to
+    the larger block (fewer groups).  Returns (k, {k: |S^-1|_F^2}).
+    """
+    obj = {k: bhq_scale_norm(bhq_plan(x, bits, k)) for k in ADAPTIVE_BLOCKS}
+    best = ADAPTIVE_BLOCKS[0]
+    for k in ADAPTIVE_BLOCKS[1:]:
+        if obj[k] <= obj[best]:
+            best = k
+    return best, obj
 
 
 def dequantize_bhq(q):

@@ -63,9 +63,10 @@ struct QuantWs {
   float* rmin;
   float* rmax;
   void* plan;
+  void* adaptive;
 };
 
-QuantWs carve_quant(Carver& c, fqt_kind kind, const float* x, int64_t rows, int64_t cols) {
+QuantWs carve_quant(Carver& c, fqt_kind kind, const float* x, int64_t rows, int64_t cols, int block_size = 1) {
   QuantWs w{};
   w.h = take_header(c);
   w.seg = kind == FQT_PTQ ? stats_flat_seg(x, rows * cols) : stats_rows_seg(x, rows, cols);
@@ -76,7 +77,21 @@ QuantWs carve_quant(Carver& c, fqt_kind kind, const float* x, int64_t rows, int6
     stats_direct_rows(w.seg, w.rmin, w.rmax);
   }
   if (kind == FQT_BHQ) w.plan = c.take<char>((int64_t)bhq_plan_workspace(rows));
+  if (kind == FQT_BHQ && block_size == 0) w.adaptive = c.take<char>((int64_t)bhq_adaptive_workspace(rows));
   return w;
+}
+
+// Adaptive grouping (App. D): evaluate the candidate block sizes on the
+// device from the row ranges, wait for the stream and read the choice.
+fqt_status choose_block(const float* rmin, const float* rmax, int64_t rows, int bits, void* adaptive_ws,
+                        hipStream_t s, int* block) {
+  FQT_TRY(launch_bhq_adaptive(rmin, rmax, rows, bits, adaptive_ws, s));
+  int32_t k = 0;
+  FQT_TRY(hipMemcpyAsync(&k, bhq_adaptive_carve(adaptive_ws, rows).chosen, sizeof(k), hipMemcpyDeviceToHost, s));
+  FQT_TRY(hipStreamSynchronize(s));
+  if (!valid_block(k)) return FQT_EDEVICE;
+  *block = k;
+  return FQT_OK;
 }
 
 void add_zero(FinalizePlan& fp, int32_t* p, int64_t n) {
@@ -100,15 +115,15 @@ fqt_status quantize_common(fqt_kind kind, const float* x, int64_t rows, int64_t 
   fqt_status st = check_quant_args(x, rows, cols, bits, out);
   if (st != FQT_OK) return st;
   if (kind == FQT_BHQ) {
-    if (block_size == 0) return FQT_EUNSUPPORTED;
-    if (!valid_block(block_size) || !out->perm) return FQT_EINVAL;
+    if (block_size == 0 && !bhq_adaptive_supported(rows)) return FQT_EUNSUPPORTED;
+    if ((block_size != 0 && !valid_block(block_size)) || !out->perm) return FQT_EINVAL;
   }
   if (!ws) return FQT_EWORKSPACE;
   Carver cs(nullptr);
-  carve_quant(cs, kind, x, rows, cols);
+  carve_quant(cs, kind, x, rows, cols, block_size);
   if (ws_bytes < cs.off) return FQT_EWORKSPACE;
   Carver c(ws);
-  QuantWs w = carve_quant(c, kind, x, rows, cols);
+  QuantWs w = carve_quant(c, kind, x, rows, cols, block_size);
 
   StatsPlan sp{};
   sp.seg[0] = w.seg;
@@ -131,6 +146,11 @@ fqt_status quantize_common(fqt_kind kind, const float* x, int64_t rows, int64_t 
   // launch also runs the finalize step
   const bool fin_in_plan = kind == FQT_BHQ && w.seg.rmin != nullptr;
   if (!fin_in_plan) FQT_TRY(launch_finalize(fp, s));
+  if (kind == FQT_BHQ && block_size == 0) {
+    // the row ranges are complete here (statistics kernel, or the finalize above)
+    st = choose_block(w.rmin, w.rmax, rows, bits, w.adaptive, s, &block_size);
+    if (st != FQT_OK) return st;
+  }
 
   QuantParams p{};
   p.x = x;
@@ -175,6 +195,7 @@ struct LinearWs {
   float *sx, *zx, *sw, *zw, *sg1, *zg1, *sg2, *zg2;
   int32_t* perm;
   void* plan;
+  void* adaptive;
   int32_t* part;
   int splits;
 };
@@ -213,6 +234,7 @@ LinearWs carve_linear(Carver& c, const float* X, const float* W, const float* G,
   if (cfg.qb_x.kind == FQT_BHQ) {
     w.perm = c.take<int32_t>(N);
     w.plan = c.take<char>((int64_t)bhq_plan_workspace(N));
+    if (cfg.qb_x.block_size == 0) w.adaptive = c.take<char>((int64_t)bhq_adaptive_workspace(N));
   }
   w.splits = linear_splits(N);
   if (w.splits > 1) w.part = c.take<int32_t>((int64_t)w.splits * d_out * d_in);
@@ -227,10 +249,8 @@ fqt_status check_cfg(const fqt_bwd_cfg* cfg) {
   if (cfg->qb_x.kind < FQT_PTQ || cfg->qb_x.kind > FQT_BHQ || cfg->qb_w.kind < FQT_PTQ || cfg->qb_w.kind > FQT_BHQ)
     return FQT_EINVAL;
   if (cfg->qb_w.kind != FQT_PTQ) return FQT_EUNSUPPORTED;
-  if (cfg->qb_x.kind == FQT_BHQ) {
-    if (cfg->qb_x.block_size == 0) return FQT_EUNSUPPORTED;
-    if (!valid_block(cfg->qb_x.block_size)) return FQT_EINVAL;
-  }
+  if (cfg->qb_x.kind == FQT_BHQ && cfg->qb_x.block_size != 0 && !valid_block(cfg->qb_x.block_size))
+    return FQT_EINVAL;
   return FQT_OK;
 }
 
@@ -266,6 +286,7 @@ struct ConvWs {
   float *sx, *zx, *sw, *zw, *sg1, *zg1, *sg2, *zg2;
   int32_t* perm;
   void* plan;
+  void* adaptive;
   int32_t* part;
   int64_t ldq, kchunk;
   int splits;
@@ -312,6 +333,7 @@ ConvWs carve_conv(Carver& c, const float* X, const float* W, const float* G, con
   if (cfg.qb_x.kind == FQT_BHQ) {
     w.perm = c.take<int32_t>(N);
     w.plan = c.take<char>((int64_t)bhq_plan_workspace(N));
+    if (cfg.qb_x.block_size == 0) w.adaptive = c.take<char>((int64_t)bhq_adaptive_workspace(N));
   }
   // grad_W: split the pixel contraction so that about 512 blocks run, each
   // K chunk a whole number of 128-byte stages and at most 65536
@@ -353,11 +375,43 @@ fqt_status fqt_quantize_bhq(const float* x, int64_t rows, int64_t cols, int bits
 }
 
 size_t fqt_quantize_workspace(fqt_kind kind, int64_t rows, int64_t cols, int block_size) {
-  (void)block_size;
   if (rows < 1 || cols < 1) return 0;
   Carver c(nullptr);
-  carve_quant(c, kind, nullptr, rows, cols);
+  carve_quant(c, kind, nullptr, rows, cols, block_size);
   return c.off;
+}
+
+size_t fqt_bhq_adaptive_workspace(int64_t rows, int64_t cols) {
+  if (rows < 1 || cols < 1) return 0;
+  Carver c(nullptr);
+  carve_quant(c, FQT_BHQ, nullptr, rows, cols, 0);
+  return c.off;
+}
+
+fqt_status fqt_bhq_adaptive_block(const float* x, int64_t rows, int64_t cols, int bits, int* block_size, void* ws,
+                                  size_t ws_bytes, fqt_stream_t s) {
+  if (!x || !block_size) return FQT_EINVAL;
+  if (rows < 1 || cols < 1 || !valid_bits(bits)) return FQT_EINVAL;
+  if (!bhq_adaptive_supported(rows) || cols > ((int64_t)1 << 40) / rows) return FQT_EUNSUPPORTED;
+  if (!ws) return FQT_EWORKSPACE;
+  if (ws_bytes < fqt_bhq_adaptive_workspace(rows, cols)) return FQT_EWORKSPACE;
+  Carver c(ws);
+  QuantWs w = carve_quant(c, FQT_BHQ, x, rows, cols, 0);
+  StatsPlan sp{};
+  sp.seg[0] = w.seg;
+  sp.nseg = 1;
+  FQT_TRY(launch_stats(sp, s));
+  FinalizePlan fp{};
+  fp.seg[0] = w.seg;
+  fp.nseg = 1;
+  fp.row_seg = 0;
+  fp.rmin = w.rmin;
+  fp.rmax = w.rmax;
+  fp.status = w.h.status;
+  FQT_TRY(launch_finalize(fp, s));
+  const fqt_status st = choose_block(w.rmin, w.rmax, rows, bits, w.adaptive, s, block_size);
+  if (st != FQT_OK) return st;
+  return fqt_workspace_status(ws, s);
 }
 
 size_t fqt_linear_backward_workspace(int64_t N, int64_t d_in, int64_t d_out, const fqt_bwd_cfg* cfg) {
@@ -375,6 +429,7 @@ fqt_status fqt_linear_backward(const float* X, const float* W, const float* G, i
   fqt_status st = check_cfg(cfg);
   if (st != FQT_OK) return st;
   if (N > MAX_ROWS || d_out > MAX_ROWS || d_out > MAX_K_CHUNK || N > 0x7FFFFFFF / 2) return FQT_EUNSUPPORTED;
+  if (cfg->qb_x.kind == FQT_BHQ && cfg->qb_x.block_size == 0 && !bhq_adaptive_supported(N)) return FQT_EUNSUPPORTED;
   if (!ws) return FQT_EWORKSPACE;
   if (ws_bytes < fqt_linear_backward_workspace(N, d_in, d_out, cfg)) return FQT_EWORKSPACE;
   Carver c(ws);
@@ -417,10 +472,16 @@ fqt_status fqt_linear_backward(const float* X, const float* W, const float* G, i
   if (bhq) add_zero(fp, bhq_plan_carve(w.plan, N).rank, N);
   const bool fin_in_plan = bhq && w.sg_seg.rmin != nullptr;
   if (!fin_in_plan) FQT_TRY(launch_finalize(fp, s));
+  int block = qx.block_size;
+  if (bhq && block == 0) {
+    // adaptive grouping (App. D): the row ranges of G are complete here
+    st = choose_block(w.rmin, w.rmax, N, qx.bits, w.adaptive, s, &block);
+    if (st != FQT_OK) return st;
+  }
   BhqLayout L{};
   int mode = qx.kind == FQT_PSQ ? QM_ROW : QM_TENSOR;
   if (bhq) {
-    L = bhq_layout(N, qx.block_size);
+    L = bhq_layout(N, block);
     FQT_TRY(launch_bhq_plan(w.rmin, w.rmax, L, qx.bits, w.plan, w.perm, w.sg2, w.zg2, nullptr,
                             fin_in_plan ? &fp : nullptr, s));
     mode = QM_BHQ;
@@ -576,6 +637,8 @@ fqt_status fqt_conv_backward_im2col(const float* X, const float* W, const float*
   if (st != FQT_OK) return st;
   st = check_cfg(cfg);
   if (st != FQT_OK) return st;
+  if (cfg->qb_x.kind == FQT_BHQ && cfg->qb_x.block_size == 0 && !bhq_adaptive_supported(shape->n))
+    return FQT_EUNSUPPORTED;
   if (!ws) return FQT_EWORKSPACE;
   if (ws_bytes < fqt_conv_backward_workspace(shape, cfg)) return FQT_EWORKSPACE;
   const ConvGeom g = conv_geom(*shape);
@@ -617,10 +680,16 @@ fqt_status fqt_conv_backward_im2col(const float* X, const float* W, const float*
   if (bhq) add_zero(fp, bhq_plan_carve(w.plan, N).rank, N);
   const bool fin_in_plan = bhq && w.sg_seg.rmin != nullptr;
   if (!fin_in_plan) FQT_TRY(launch_finalize(fp, s));
+  int block = qx.block_size;
+  if (bhq && block == 0) {
+    // adaptive grouping (App. D): the row ranges of G are complete here
+    st = choose_block(w.rmin, w.rmax, N, qx.bits, w.adaptive, s, &block);
+    if (st != FQT_OK) return st;
+  }
   BhqLayout L{};
   int mode = qx.kind == FQT_PSQ ? QM_ROW : QM_TENSOR;
   if (bhq) {
-    L = bhq_layout(N, qx.block_size);
+    L = bhq_layout(N, block);
     FQT_TRY(launch_bhq_plan(w.rmin, w.rmax, L, qx.bits, w.plan, w.perm, w.sg2, w.zg2, nullptr,
                             fin_in_plan ? &fp : nullptr, s));
     mode = QM_BHQ;

@@ -106,6 +106,23 @@ hipError_t launch_bhq_plan(const float* rmin, const float* rmax, const BhqLayout
                            int32_t* perm, float* scale, float* zero, int32_t* group_off, const FinalizePlan* fin,
                            hipStream_t s);
 
+// Adaptive grouping (App. D): the block size in {1, 2, 4, .., 64} whose
+// fixed-block plan has the least |S^-1|_F^2; for rows <= 16384.  Writes the
+// chosen size to bhq_adaptive_carve(ws).chosen (and the candidates'
+// objectives) on the stream.
+constexpr int ADAPTIVE_CANDIDATES = 7;
+struct AdaptiveWs {
+  int32_t* sigma;
+  double* terms;
+  double* objective;   // [ADAPTIVE_CANDIDATES]
+  int32_t* chosen;
+};
+size_t bhq_adaptive_workspace(int64_t rows);
+AdaptiveWs bhq_adaptive_carve(void* ws, int64_t rows);
+hipError_t launch_bhq_adaptive(const float* rmin, const float* rmax, int64_t rows, int bits, void* ws,
+                               hipStream_t s);
+bool bhq_adaptive_supported(int64_t rows);
+
 struct QuantParams {
   const float* x;
   int64_t rows, cols;

@@ -483,13 +483,16 @@ __device__ __forceinline__ float to_f32_sat(double v) {
   return (f > FLT_MAX_F) ? FLT_MAX_F : f;
 }
 
-// FROM_PERM: perm already holds the rows in slot order (bhq_rank_perm_kernel);
-// otherwise the rows come from sigma (sorted order) and perm is written here.
-template <bool FROM_PERM>
-__global__ __launch_bounds__(64) void bhq_groups_kernel(const float* rmin, const float* rmax, const int32_t* sigma,
-                                                        BhqLayout L, int B, int32_t* perm, float* scale, float* zero,
-                                                        int32_t* group_off) {
-  const int64_t g = blockIdx.x;
+// One group of a fixed-block plan, one wave (lane j handles the group's slot
+// j + 1): the per-slot scale d_p and zero (c_g, or the row min for a one-row
+// group).  FROM_PERM: perm already holds the rows in slot order
+// (bhq_rank_perm_kernel); otherwise the rows come from sigma (sorted order).
+// WRITE: store perm (rows from sigma only), scale, zero and group_off.
+// term (optional): the group's share of |S^-1|_F^2 (Eq.
+// matrix-quantizer-variance): 1/s1^2 + (k_g - 1)/s2^2, a one-row group 1/s^2.
+template <bool FROM_PERM, bool WRITE>
+__device__ void bhq_group(const float* rmin, const float* rmax, const int32_t* sigma, const BhqLayout& L, int B,
+                          int64_t g, int32_t* perm, float* scale, float* zero, int32_t* group_off, double* term) {
   const int lane = threadIdx.x;
   const int k = L.k;
   int kg;
@@ -504,7 +507,7 @@ __global__ __launch_bounds__(64) void bhq_groups_kernel(const float* rmin, const
     kg = 1;
     base = L.full * k + L.part + (g - L.full - (L.part > 0 ? 1 : 0));
   }
-  if (group_off && lane == 0) {
+  if (WRITE && group_off && lane == 0) {
     group_off[g] = (int32_t)base;
     if (g == L.G - 1) group_off[L.G] = (int32_t)L.rows;
   }
@@ -512,10 +515,14 @@ __global__ __launch_bounds__(64) void bhq_groups_kernel(const float* rmin, const
   const float mn0 = rmin[big];
   const float mx0 = rmax[big];
   if (kg == 1) {
+    const float s0 = scale_from_range(mx0 - mn0, B);
     if (lane == 0) {
-      if (!FROM_PERM) perm[base] = big;
-      scale[base] = scale_from_range(mx0 - mn0, B);
-      zero[base] = mn0;
+      if (WRITE) {
+        if (!FROM_PERM) perm[base] = big;
+        scale[base] = s0;
+        zero[base] = mn0;
+      }
+      if (term) *term = 1.0 / ((double)s0 * (double)s0);
     }
     return;
   }
@@ -548,6 +555,9 @@ __global__ __launch_bounds__(64) void bhq_groups_kernel(const float* rmin, const
     s1 = to_f32_sat(num / (a * t));
     s2 = to_f32_sat(num / (c * t));
   }
+  if (term && lane == 0)
+    *term = 1.0 / ((double)s1 * (double)s1) + (double)(kg - 1) * (1.0 / ((double)s2 * (double)s2));
+  if (!WRITE) return;
   const double t1 = ((double)alpha * (double)s1) * (double)mn0;
   const double t2 = ((0.5 * (double)lam2) * (double)s2) * sk;
   const float cg = (float)(t1 - t2);
@@ -561,6 +571,100 @@ __global__ __launch_bounds__(64) void bhq_groups_kernel(const float* rmin, const
     scale[base + 1 + lane] = s2;
     zero[base + 1 + lane] = cg;
   }
+}
+
+template <bool FROM_PERM>
+__global__ __launch_bounds__(64) void bhq_groups_kernel(const float* rmin, const float* rmax, const int32_t* sigma,
+                                                        BhqLayout L, int B, int32_t* perm, float* scale, float* zero,
+                                                        int32_t* group_off) {
+  bhq_group<FROM_PERM, true>(rmin, rmax, sigma, L, B, blockIdx.x, perm, scale, zero, group_off, nullptr);
+}
+
+// ---------------------------------------------------------------------------
+// Adaptive grouping (App. D): every candidate block size k in {1, 2, .., 64}
+// is evaluated by the |S^-1|_F^2 of its fixed-block plan; the least wins,
+// ties going to the larger block.  Rows are sorted once (the k = 1 layout of
+// the rank kernel is the sorted order itself); one wave per (candidate,
+// group) writes the group's term; one thread per candidate adds its terms in
+// slot order in float64.
+// ---------------------------------------------------------------------------
+struct AdaptivePlan {
+  BhqLayout L[ADAPTIVE_CANDIDATES];
+  int64_t off[ADAPTIVE_CANDIDATES + 1];  // first term of each candidate
+};
+
+__global__ __launch_bounds__(64) void bhq_terms_kernel(const float* rmin, const float* rmax, const int32_t* sigma,
+                                                       AdaptivePlan ap, int B, double* terms) {
+  const int64_t id = blockIdx.x;
+  int c = 0;
+  while (c + 1 < ADAPTIVE_CANDIDATES && id >= ap.off[c + 1]) ++c;
+  bhq_group<false, false>(rmin, rmax, sigma, ap.L[c], B, id - ap.off[c], nullptr, nullptr, nullptr, nullptr,
+                          terms + id);
+}
+
+__global__ __launch_bounds__(64) void bhq_choose_kernel(AdaptivePlan ap, const double* terms, double* objective,
+                                                        int32_t* chosen) {
+  __shared__ double obj[ADAPTIVE_CANDIDATES];
+  const int t = threadIdx.x;
+  if (t < ADAPTIVE_CANDIDATES) {
+    double sum = 0.0;
+    for (int64_t i = ap.off[t]; i < ap.off[t + 1]; ++i) sum = sum + terms[i];
+    obj[t] = sum;
+    objective[t] = sum;
+  }
+  __syncthreads();
+  if (t == 0) {
+    int best = 0;
+    for (int c = 1; c < ADAPTIVE_CANDIDATES; ++c)
+      if (obj[c] <= obj[best]) best = c;
+    *chosen = ap.L[best].k;
+  }
+}
+
+size_t bhq_adaptive_workspace(int64_t rows) {
+  int64_t nterms = 0;
+  for (int c = 0; c < ADAPTIVE_CANDIDATES; ++c) nterms += (rows + (1 << c) - 1) >> c;
+  // sigma, terms, objectives, chosen block size
+  return (size_t)rows * 4 + 256 + (size_t)nterms * 8 + 256 + ADAPTIVE_CANDIDATES * 8 + 256 + 256;
+}
+
+AdaptiveWs bhq_adaptive_carve(void* ws, int64_t rows) {
+  char* p = static_cast<char*>(ws);
+  AdaptiveWs w{};
+  w.sigma = reinterpret_cast<int32_t*>(p);
+  p += ((size_t)rows * 4 + 255) / 256 * 256;
+  w.terms = reinterpret_cast<double*>(p);
+  int64_t nterms = 0;
+  for (int c = 0; c < ADAPTIVE_CANDIDATES; ++c) nterms += (rows + (1 << c) - 1) >> c;
+  p += ((size_t)nterms * 8 + 255) / 256 * 256;
+  w.objective = reinterpret_cast<double*>(p);
+  p += 256;
+  w.chosen = reinterpret_cast<int32_t*>(p);
+  return w;
+}
+
+bool bhq_adaptive_supported(int64_t rows) { return rows >= 1 && rows <= RANK_MAX_ROWS; }
+
+hipError_t launch_bhq_adaptive(const float* rmin, const float* rmax, int64_t rows, int bits, void* ws,
+                               hipStream_t s) {
+  if (!bhq_adaptive_supported(rows)) return hipErrorInvalidValue;
+  const AdaptiveWs w = bhq_adaptive_carve(ws, rows);
+  // sorted order: the k = 1 layout stores each row at its sorted position
+  const BhqLayout L1 = bhq_layout(rows, 1);
+  const int64_t nrank = (rows + RK_ROWS - 1) / RK_ROWS;
+  const FinalizePlan none{};
+  hipLaunchKernelGGL(bhq_rank_perm_kernel, dim3((unsigned)nrank), dim3(RK_THREADS), (size_t)rank_pad(rows) * 4, s,
+                     rmin, rmax, L1, w.sigma, nrank, none);
+  AdaptivePlan ap{};
+  ap.off[0] = 0;
+  for (int c = 0; c < ADAPTIVE_CANDIDATES; ++c) {
+    ap.L[c] = bhq_layout(rows, 1 << c);
+    ap.off[c + 1] = ap.off[c] + ap.L[c].G;
+  }
+  hipLaunchKernelGGL(bhq_terms_kernel, dim3((unsigned)ap.off[ADAPTIVE_CANDIDATES]), dim3(64), 0, s, rmin, rmax,
+                     w.sigma, ap, (1 << bits) - 1, w.terms);
+  hipLaunchKernelGGL(bhq_choose_kernel, dim3(1), dim3(64), 0, s, ap, w.terms, w.objective, w.chosen);
+  return hipGetLastError();
 }
 
 BhqPlanWs bhq_plan_carve(void* plan_ws, int64_t rows) {

@@ -55,6 +55,7 @@ class ConvShape(ctypes.Structure):
 
 EXPORTS = [
     "fqt_quantize_ptq", "fqt_quantize_psq", "fqt_quantize_bhq", "fqt_quantize_workspace",
+    "fqt_bhq_adaptive_block", "fqt_bhq_adaptive_workspace",
     "fqt_linear_backward", "fqt_linear_backward_workspace",
     "fqt_conv_backward_im2col", "fqt_conv_backward_workspace",
     "fqt_gemm_s8s8_s64", "fqt_gemm_workspace",
@@ -82,6 +83,8 @@ def load(path=LIB_PATH):
         "fqt_quantize_psq": ([vp, i64, i64, i32, u64, u32, qtp, vp, sz, vp], i32),
         "fqt_quantize_bhq": ([vp, i64, i64, i32, i32, u64, u32, qtp, vp, sz, vp], i32),
         "fqt_quantize_workspace": ([i32, i64, i64, i32], sz),
+        "fqt_bhq_adaptive_block": ([vp, i64, i64, i32, ctypes.POINTER(ctypes.c_int), vp, sz, vp], i32),
+        "fqt_bhq_adaptive_workspace": ([i64, i64], sz),
         "fqt_linear_backward": ([vp, vp, vp, i64, i64, i64, cfgp, vp, vp, vp, sz, vp], i32),
         "fqt_linear_backward_workspace": ([i64, i64, i64, cfgp], sz),
         "fqt_conv_backward_im2col": ([vp, vp, vp, shp, cfgp, vp, vp, vp, sz, vp], i32),
@@ -193,6 +196,18 @@ def fqt_quantize_bhq(x, bits, block_size, seed=0, stream=0, code_sum=False, ws=N
     _check("fqt_quantize_bhq", rc)
     out["ws"] = ws
     return out
+
+
+def fqt_bhq_adaptive_block(x, bits, ws=None):
+    """Block size of the adaptive grouping (waits for the stream)."""
+    x = _f32(x, "x")
+    rows, cols = x.shape
+    if ws is None:
+        ws = _workspace(load().fqt_bhq_adaptive_workspace(rows, cols), x.device)
+    k = ctypes.c_int(0)
+    rc = load().fqt_bhq_adaptive_block(_ptr(x), rows, cols, bits, ctypes.byref(k), _ptr(ws), ws.numel(), _stream())
+    _check("fqt_bhq_adaptive_block", rc)
+    return k.value
 
 
 def fqt_linear_backward_workspace(N, d_in, d_out, cfg):

@@ -60,10 +60,17 @@ def test_workspace_queries_and_argument_errors():
     unsup = fqt.cfg_struct(qb_w=("psq", 8, 0))
     rc = lib.fqt_linear_backward(fake, fake, fake, 4, 4, 4, ctypes.byref(unsup), fake, fake, fake, 1 << 30, null)
     assert rc == 2
-    # adaptive BHQ grouping (block size 0) is not built; block sizes must be powers of two <= 64
-    rc = lib.fqt_linear_backward(fake, fake, fake, 4, 4, 4, ctypes.byref(fqt.cfg_struct(qb_x=("bhq", 5, 0))),
+    # adaptive BHQ grouping (block size 0) sorts at most 16384 rows; block sizes must be powers of two <= 64
+    rc = lib.fqt_linear_backward(fake, fake, fake, 20000, 4, 4, ctypes.byref(fqt.cfg_struct(qb_x=("bhq", 5, 0))),
                                  fake, fake, fake, 1 << 30, null)
     assert rc == 2
+    k = ctypes.c_int(-1)
+    assert lib.fqt_bhq_adaptive_block(fake, 20000, 4, 5, ctypes.byref(k), fake, 1 << 30, null) == 2
+    assert lib.fqt_bhq_adaptive_block(fake, 40, 4, 9, ctypes.byref(k), fake, 1 << 30, null) == 1
+    assert lib.fqt_bhq_adaptive_block(fake, 40, 4, 5, None, fake, 1 << 30, null) == 1
+    assert lib.fqt_bhq_adaptive_block(fake, 40, 4, 5, ctypes.byref(k), fake, 16, null) == 4
+    assert k.value == -1
+    assert lib.fqt_bhq_adaptive_workspace(40, 4) > lib.fqt_quantize_workspace(fqt.FQT_BHQ, 40, 4, 64)
     rc = lib.fqt_linear_backward(fake, fake, fake, 4, 4, 4, ctypes.byref(fqt.cfg_struct(qb_x=("bhq", 5, 48))),
                                  fake, fake, fake, 1 << 30, null)
     assert rc == 1

@@ -293,3 +293,58 @@ def test_monte_carlo_mean_and_variance(kind):
     # total variance within a few percent of the closed form
     tv = exact_el.sum()
     assert abs(var_el.sum() - tv) / tv < 0.1
+
+
+# ---------------------------------------------------------------------------
+# adaptive grouping (App. D): pins of the block-size choice
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("k", [1, 2, 8, 64])
+def test_bhq_scale_norm_is_the_explicit_bound(k):
+    # |S^-1|_F^2 from the plan's scalars equals the Frobenius norm of the
+    # explicit inverse blocks diag(d)^-1 H (theory module, Eq. matrix-quantizer-variance)
+    rng = np.random.default_rng(k)
+    x = (rng.lognormal(0, 2, (200, 1)) * rng.standard_normal((200, 48))).astype(np.float32)
+    q = Q.quantize_bhq(x, 5, k, seed=0, stream=1)
+    D = x.shape[1]
+    assert Q.bhq_scale_norm(q["plan"]) == pytest.approx(4.0 / D * theory.matrix_var_bound(q, D), rel=1e-12)
+
+
+def test_adaptive_block_keeps_per_row_scales_for_equal_rows():
+    # identical rows: lambda2 = 2 max|row| >= lambda1 = R, so a group of k rows
+    # costs at least (1 + k)^2 R^2 / B^2 > k R^2 / B^2 (App. C.4): PSQ (k = 1) wins
+    rng = np.random.default_rng(3)
+    x = np.tile(rng.standard_normal((1, 40)).astype(np.float32), (130, 1))
+    k, obj = Q.bhq_adaptive_block(x, 5)
+    assert k == 1
+    B = Q.n_bins(5)
+    R = float(x[0].max() - x[0].min())
+    assert obj[1] == pytest.approx(130 * (R / B) ** 2, rel=1e-6)
+
+
+def test_adaptive_block_spreads_a_single_outlier():
+    # one row 1e8 times larger than the rest: one group of all 64 rows, whose
+    # bound ~ lambda1^2 / (B^2 N) beats the per-row lambda1^2 / B^2 (Sec. 4.2)
+    rng = np.random.default_rng(4)
+    x = (1e-4 * rng.standard_normal((64, 32))).astype(np.float32)
+    x[9] = (1e4 * rng.standard_normal(32)).astype(np.float32)
+    k, obj = Q.bhq_adaptive_block(x, 5)
+    assert k == 64
+    assert obj[64] < obj[1] / 32
+
+
+def test_adaptive_block_ties_go_to_the_larger_block():
+    # a zero matrix: every plan has unit scales, so |S^-1|_F^2 = N for every k
+    k, obj = Q.bhq_adaptive_block(np.zeros((100, 8), np.float32), 4)
+    assert all(v == 100.0 for v in obj.values())
+    assert k == 64
+
+
+def test_adaptive_quantize_is_the_fixed_block_of_its_choice():
+    rng = np.random.default_rng(6)
+    x = (rng.lognormal(0, 2, (150, 1)) * rng.standard_normal((150, 20))).astype(np.float32)
+    k, _ = Q.bhq_adaptive_block(x, 5)
+    a = Q.quantize_bhq(x, 5, 0, seed=2, stream=1)
+    b = Q.quantize_bhq(x, 5, k, seed=2, stream=1)
+    assert a["k"] == k
+    np.testing.assert_array_equal(a["code"], b["code"])
+    np.testing.assert_array_equal(a["perm"], b["perm"])
