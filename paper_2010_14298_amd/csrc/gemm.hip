@@ -267,11 +267,10 @@ template <class C, int EPI, int KG>
 static hipError_t launch_gemm_t(GemmParams p, hipStream_t s) {
   const int64_t tiles = gemm_tiles<C>(p.M, p.N);
   if (tiles > 0x7FFFFFFF || p.splits > 65535) return hipErrorInvalidValue;
-  // fast K loop: aligned rows, whole stages per split, 32-bit offsets
+  // fast K loop: aligned rows, whole stages per split
   const bool whole = (p.kchunk % C::BK == 0) && (p.K % C::BK == 0);
   const bool fast = ((p.lda & 15) == 0) && ((p.ldb & 15) == 0) && (((uintptr_t)p.A & 15) == 0) &&
-                    (((uintptr_t)p.B & 15) == 0) && whole && (p.M * p.lda < ((int64_t)1 << 32)) &&
-                    (p.N * p.ldb < ((int64_t)1 << 32));
+                    (((uintptr_t)p.B & 15) == 0) && whole;
   const dim3 grid((unsigned)tiles, (unsigned)p.splits);
   if (fast)
     hipLaunchKernelGGL((gemm_i8_kernel<C, EPI, KG, true>), grid, dim3(C::THREADS), 0, s, p);

@@ -15,22 +15,28 @@ typedef int v16i __attribute__((ext_vector_type(16)));
 constexpr int NUM_XCD = 8;
 
 // Block tile BM x BN, wave tile WM x WN, BK_ K bytes per pipeline stage.
-// LDS rows are padded by 16 bytes (conflict-free 8- and 16-lane phases).
-template <int BM_, int BN_, int WM_, int WN_, int BK_ = 128>
+// Generic K loop: LDS rows padded by 16 bytes (conflict-free 8- and 16-lane
+// phases), two stages.  Fast K loop: NS_ stages of swizzled 128-byte rows.
+template <int BM_, int BN_, int WM_, int WN_, int BK_ = 128, int NS_ = 2>
 struct TileCfg {
-  static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_, BK = BK_;
+  static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_, BK = BK_, NS = NS_;
   static constexpr int KCH = BK / 16;          // 16-byte chunks per row per stage
   static constexpr int LDS_STRIDE = BK + 16;
   static constexpr int WAVES_N = BN / WN;
-  static constexpr int THREADS = (BM / WM) * (BN / WN) * 64;
+  static constexpr int WAVES = (BM / WM) * (BN / WN);
+  static constexpr int THREADS = WAVES * 64;
   static constexpr int IT = WM / 32, JT = WN / 32;
   static constexpr int A_CHUNKS = BM * KCH / THREADS;  // 16-byte chunks per thread per K stage
   static constexpr int B_CHUNKS = BN * KCH / THREADS;
-  static constexpr int OP_BYTES = 2 * (BM + BN) * LDS_STRIDE;
+  // fast loop: one stage holds A then B; each wave fills whole 1 KB blocks
+  static constexpr int STAGE = (BM + BN) * BK;
+  static constexpr int A_INS = BM * BK / 1024 / WAVES, B_INS = BN * BK / 1024 / WAVES;
+  static constexpr int GEN_BYTES = 2 * (BM + BN) * LDS_STRIDE;
+  static constexpr int OP_BYTES = GEN_BYTES > NS * STAGE ? GEN_BYTES : NS * STAGE;
 };
 // Configurations measured best on MI355X for the layer shapes (8 waves each).
-using CfgLarge = TileCfg<256, 128, 64, 64, 128>;
-using CfgSmall = TileCfg<128, 128, 32, 64, 128>;
+using CfgLarge = TileCfg<256, 128, 64, 64, 128, 3>;
+using CfgSmall = TileCfg<128, 128, 32, 64, 128, 4>;
 
 typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
 struct alignas(16) Chunk16 {
@@ -67,16 +73,12 @@ __device__ __forceinline__ int64_t xcd_tile(int64_t id, int64_t ntiles) {
   return id;
 }
 
-// The K loop.  FAST requires 16-byte aligned rows, a K range that is a
-// whole number of stages and 32-bit byte offsets; then each thread keeps
-// constant offsets into a wave-uniform base pointer that advances by one
-// stage per iteration (global loads in base + offset form), rows past the
-// matrix edge are clamped to the last row (their outputs are never stored),
-// and LDS addresses are constants: the loop carries almost no vector ALU
-// work besides the matrix-core instructions.
-// The generic path takes the A operand through `aload(row, k)` (a 16-byte
-// chunk, zero outside the operand), which is how the conv input-gradient
-// contraction gathers its implicit im2col rows.
+// The K loops.  The fast one (dma_mainloop below) requires 16-byte aligned
+// rows and a K range that is a whole number of 128-byte stages.  The generic
+// one (register-staged, two LDS buffers) takes the A operand through
+// `aload(row, k)` (a 16-byte chunk, zero outside the operand), which is how
+// the conv input-gradient contraction gathers its implicit im2col rows, and
+// handles ragged K and unaligned rows.
 struct PlainALoader {
   const int8_t* A;
   int64_t lda, M, kend;
@@ -86,9 +88,135 @@ struct PlainALoader {
   }
 };
 
-template <class C, bool FAST, class ALoader>
-__device__ __forceinline__ void gemm_mainloop(const GemmParams& p, const ALoader& aload, int8_t* lds, int64_t m0,
-                                              int64_t n0, int64_t kbeg, int64_t kend, v16i (&acc)[C::IT][C::JT]) {
+typedef __attribute__((address_space(1))) void gmem_void;
+typedef __attribute__((address_space(3))) void lmem_void;
+
+// 16-byte slot of (row r, chunk c) in one operand of a fast-loop stage:
+// 8-row blocks of 1 KB, row-major, chunk index XOR-swizzled by (r / 2) mod 8.
+// One load instruction of a wave fills one block with eight whole 128-byte
+// rows (consecutive lanes read consecutive chunks of one row), and the 16
+// rows one matrix-core operand read touches at a fixed chunk fall on 16
+// distinct 16-byte bank groups.
+__device__ __forceinline__ int kslot(int r, int c) { return 8 * r + (c ^ ((r >> 1) & 7)); }
+
+// One stage of the fast loop: wait for this wave's loads of stage t, then the
+// barrier (everyone's have landed, and everyone is done reading the buffer
+// that the loads of stage t + NS - 1 now fill), start those loads, and run
+// the matrix-core work on `cur`, each MFMA followed by one LDS read of the
+// next K step.  `cur` and `nxt` are never the same buffer; the caller passes
+// them as distinct restrict pointers so that the pending loads into `nxt` do
+// not hold up the reads of `cur`.
+template <class C>
+__device__ __forceinline__ void dma_stage(const int8_t* __restrict__ cur, int8_t* __restrict__ nxt,
+                                          const int8_t* const (&srcA)[C::A_INS], const int8_t* const (&srcB)[C::B_INS],
+                                          int64_t t, int64_t nk, v16i (&acc)[C::IT][C::JT]) {
+  constexpr int PER = C::A_INS + C::B_INS;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wm = wave / C::WAVES_N, wn = wave % C::WAVES_N;
+  if (t + C::NS - 2 < nk)
+    __builtin_amdgcn_s_waitcnt(0x3F70 | ((C::NS - 2) * PER));  // vmcnt: later stages may stay in flight
+  else
+    __builtin_amdgcn_s_waitcnt(0x3F70);                          // vmcnt(0)
+  __builtin_amdgcn_s_barrier();
+  if (t + C::NS - 1 < nk) {
+    const int64_t ko = (t + C::NS - 1) * C::BK;
+#pragma unroll
+    for (int i = 0; i < C::A_INS; ++i)
+      __builtin_amdgcn_global_load_lds((gmem_void*)(srcA[i] + ko), (lmem_void*)(nxt + (wave * C::A_INS + i) * 1024),
+                                       16, 0, 0);
+#pragma unroll
+    for (int i = 0; i < C::B_INS; ++i)
+      __builtin_amdgcn_global_load_lds((gmem_void*)(srcB[i] + ko),
+                                       (lmem_void*)(nxt + C::BM * C::BK + (wave * C::B_INS + i) * 1024), 16, 0, 0);
+  }
+  const int lrow = lane & 31, lh = lane >> 5;
+  const int8_t* sa = cur;
+  const int8_t* sb = cur + C::BM * C::BK;
+  v4i a[2][C::IT], b[2][C::JT];
+  auto rd = [&](int set, int kk) __attribute__((always_inline)) {
+    const int c = 2 * kk + lh;
+#pragma unroll
+    for (int i = 0; i < C::IT; ++i) a[set][i] = *reinterpret_cast<const v4i*>(sa + 16 * kslot(wm * C::WM + i * 32 + lrow, c));
+#pragma unroll
+    for (int j = 0; j < C::JT; ++j) b[set][j] = *reinterpret_cast<const v4i*>(sb + 16 * kslot(wn * C::WN + j * 32 + lrow, c));
+  };
+  rd(0, 0);
+#pragma unroll
+  for (int kk = 0; kk < C::BK / 32; ++kk) {
+    const int cs = kk & 1;
+    if (kk + 1 < C::BK / 32) rd(cs ^ 1, kk + 1);
+#pragma unroll
+    for (int i = 0; i < C::IT; ++i)
+#pragma unroll
+      for (int j = 0; j < C::JT; ++j) acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a[cs][i], b[cs][j], acc[i][j], 0, 0, 0);
+  }
+  __builtin_amdgcn_sched_group_barrier(0x100, C::IT + C::JT, 0);
+#pragma unroll
+  for (int kk = 0; kk < C::BK / 32; ++kk)
+#pragma unroll
+    for (int m = 0; m < C::IT * C::JT; ++m) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      if (kk + 1 < C::BK / 32 && m < C::IT + C::JT) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+}
+
+// The fast K loop: operands loaded straight into LDS (global_load_lds_dwordx4,
+// NS - 1 stages in flight), 128-byte K stages, rows past the matrix edge
+// clamped to its last row (their outputs are never stored).  Ends with a
+// barrier, so the caller may reuse the LDS.
+template <class C>
+__device__ __forceinline__ void dma_mainloop(const GemmParams& p, int8_t* __restrict__ b0, int8_t* __restrict__ b1,
+                                             int8_t* __restrict__ b2, int8_t* __restrict__ b3, int64_t m0, int64_t n0,
+                                             int64_t kbeg, int64_t kend, v16i (&acc)[C::IT][C::JT]) {
+  static_assert(C::BK == 128 && C::NS >= 2 && C::NS <= 4, "fast loop: 128-byte stages, 2..4 buffers");
+  static_assert(C::A_INS * 1024 * C::WAVES == C::BM * C::BK && C::B_INS * 1024 * C::WAVES == C::BN * C::BK,
+                "whole 1 KB blocks per wave");
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int8_t* srcA[C::A_INS];
+  const int8_t* srcB[C::B_INS];
+#pragma unroll
+  for (int i = 0; i < C::A_INS; ++i) {
+    const int r = 8 * (wave * C::A_INS + i) + (lane >> 3);
+    const int64_t row = (m0 + r < p.M) ? m0 + r : p.M - 1;
+    srcA[i] = p.A + row * p.lda + kbeg + 16 * ((lane & 7) ^ ((r >> 1) & 7));
+  }
+#pragma unroll
+  for (int i = 0; i < C::B_INS; ++i) {
+    const int r = 8 * (wave * C::B_INS + i) + (lane >> 3);
+    const int64_t row = (n0 + r < p.N) ? n0 + r : p.N - 1;
+    srcB[i] = p.B + row * p.ldb + kbeg + 16 * ((lane & 7) ^ ((r >> 1) & 7));
+  }
+  const int64_t nk = (kend - kbeg) / C::BK;
+  int8_t* bufs[4] = {b0, b1, b2, b3};
+#pragma unroll
+  for (int s = 0; s < C::NS - 1; ++s) {
+    if (s < nk) {
+#pragma unroll
+      for (int i = 0; i < C::A_INS; ++i)
+        __builtin_amdgcn_global_load_lds((gmem_void*)(srcA[i] + s * C::BK),
+                                         (lmem_void*)(bufs[s] + (wave * C::A_INS + i) * 1024), 16, 0, 0);
+#pragma unroll
+      for (int i = 0; i < C::B_INS; ++i)
+        __builtin_amdgcn_global_load_lds((gmem_void*)(srcB[i] + s * C::BK),
+                                         (lmem_void*)(bufs[s] + C::BM * C::BK + (wave * C::B_INS + i) * 1024), 16,
+                                         0, 0);
+    }
+  }
+  // stage t reads buffer t % NS and fills buffer (t + NS - 1) % NS
+  for (int64_t t = 0; t < nk; t += C::NS) {
+    dma_stage<C>(b0, C::NS == 2 ? b1 : (C::NS == 3 ? b2 : b3), srcA, srcB, t, nk, acc);
+    if (t + 1 < nk) dma_stage<C>(b1, b0, srcA, srcB, t + 1, nk, acc);
+    if (C::NS > 2 && t + 2 < nk) dma_stage<C>(b2, b1, srcA, srcB, t + 2, nk, acc);
+    if (C::NS > 3 && t + 3 < nk) dma_stage<C>(b3, b2, srcA, srcB, t + 3, nk, acc);
+  }
+  __syncthreads();
+}
+
+template <class C, class ALoader>
+__device__ __forceinline__ void generic_mainloop(const GemmParams& p, const ALoader& aload, int8_t* lds, int64_t m0,
+                                                 int64_t n0, int64_t kbeg, int64_t kend, v16i (&acc)[C::IT][C::JT]) {
   int8_t* sA = lds;                          // [2][BM * C::LDS_STRIDE]
   int8_t* sB = lds + 2 * C::BM * C::LDS_STRIDE;  // [2][BN * C::LDS_STRIDE]
   const int tid = threadIdx.x;
@@ -97,24 +225,6 @@ __device__ __forceinline__ void gemm_mainloop(const GemmParams& p, const ALoader
   const int wm = wave / C::WAVES_N, wn = wave % C::WAVES_N;
   const bool alB = ((p.ldb & 15) == 0) && (((uintptr_t)p.B & 15) == 0);
   const int64_t nk = (kend - kbeg + C::BK - 1) / C::BK;
-
-  uint32_t offA[C::A_CHUNKS], offB[C::B_CHUNKS];
-  if constexpr (FAST) {
-#pragma unroll
-    for (int i = 0; i < C::A_CHUNKS; ++i) {
-      const int c = tid + C::THREADS * i;
-      const int64_t r = (m0 + c / C::KCH < p.M) ? m0 + c / C::KCH : p.M - 1;
-      offA[i] = (uint32_t)(r * p.lda) + 16u * (uint32_t)(c % C::KCH);
-    }
-#pragma unroll
-    for (int i = 0; i < C::B_CHUNKS; ++i) {
-      const int c = tid + C::THREADS * i;
-      const int64_t r = (n0 + c / C::KCH < p.N) ? n0 + c / C::KCH : p.N - 1;
-      offB[i] = (uint32_t)(r * p.ldb) + 16u * (uint32_t)(c % C::KCH);
-    }
-  }
-  const int8_t* Ak = p.A + kbeg;
-  const int8_t* Bk = p.B + kbeg;
 
   // Two register staging sets: the loads of stage t + 1 are issued one
   // iteration before the stage is stored to LDS, so each global load has two
@@ -125,27 +235,18 @@ __device__ __forceinline__ void gemm_mainloop(const GemmParams& p, const ALoader
   };
   Stage st0, st1;
   auto gload = [&](Stage& st, int64_t t) __attribute__((always_inline)) {
-    if constexpr (FAST) {
-      const int8_t* a = Ak + t * C::BK;
-      const int8_t* b = Bk + t * C::BK;
+    const int64_t k0 = kbeg + t * C::BK;
 #pragma unroll
-      for (int i = 0; i < C::A_CHUNKS; ++i) st.a[i] = *reinterpret_cast<const u32x4v*>(a + offA[i]);
+    for (int i = 0; i < C::A_CHUNKS; ++i) {
+      const int c = tid + C::THREADS * i;
+      const Chunk16 v = aload(m0 + c / C::KCH, k0 + 16 * (c % C::KCH));
+      st.a[i] = u32x4v{v.w[0], v.w[1], v.w[2], v.w[3]};
+    }
 #pragma unroll
-      for (int i = 0; i < C::B_CHUNKS; ++i) st.b[i] = *reinterpret_cast<const u32x4v*>(b + offB[i]);
-    } else {
-      const int64_t k0 = kbeg + t * C::BK;
-#pragma unroll
-      for (int i = 0; i < C::A_CHUNKS; ++i) {
-        const int c = tid + C::THREADS * i;
-        const Chunk16 v = aload(m0 + c / C::KCH, k0 + 16 * (c % C::KCH));
-        st.a[i] = u32x4v{v.w[0], v.w[1], v.w[2], v.w[3]};
-      }
-#pragma unroll
-      for (int i = 0; i < C::B_CHUNKS; ++i) {
-        const int c = tid + C::THREADS * i;
-        const Chunk16 v = load_chunk(p.B, p.ldb, n0 + c / C::KCH, p.N, k0 + 16 * (c % C::KCH), kend, alB);
-        st.b[i] = u32x4v{v.w[0], v.w[1], v.w[2], v.w[3]};
-      }
+    for (int i = 0; i < C::B_CHUNKS; ++i) {
+      const int c = tid + C::THREADS * i;
+      const Chunk16 v = load_chunk(p.B, p.ldb, n0 + c / C::KCH, p.N, k0 + 16 * (c % C::KCH), kend, alB);
+      st.b[i] = u32x4v{v.w[0], v.w[1], v.w[2], v.w[3]};
     }
   };
   auto sstore = [&](const Stage& st, int buf) __attribute__((always_inline)) {
@@ -201,6 +302,18 @@ __device__ __forceinline__ void gemm_mainloop(const GemmParams& p, const ALoader
     iter(t + 1, 1, st0, st1);
   }
   if (t < nk) iter(t, 0, st1, st0);
+}
+
+template <class C, bool FAST, class ALoader>
+__device__ __forceinline__ void gemm_mainloop(const GemmParams& p, const ALoader& aload, int8_t* lds, int64_t m0,
+                                              int64_t n0, int64_t kbeg, int64_t kend, v16i (&acc)[C::IT][C::JT]) {
+  if constexpr (FAST) {
+    // distinct stage buffers of one LDS array
+    dma_mainloop<C>(p, lds, lds + C::STAGE, lds + (C::NS > 2 ? 2 : 1) * C::STAGE, lds + (C::NS > 3 ? 3 : 1) * C::STAGE,
+                    m0, n0, kbeg, kend, acc);
+  } else {
+    generic_mainloop<C>(p, aload, lds, m0, n0, kbeg, kend, acc);
+  }
 }
 
 }  // namespace fqt
