@@ -32,6 +32,17 @@ def linear_small(seed=0, n=128, d_in=256, d_out=256):
     return X, W, G
 
 
+def mlp(seed=0, n=64, widths=(24, 32, 32, 16)):
+    """ReLU MLP inputs: X ~ N(0,1) [n, widths[0]]; W_i ~ N(0, 2/widths[i]) [widths[i+1], widths[i]]
+    (He); top output gradient G with log-normal row scales [n, widths[-1]]."""
+    rng = _rng(seed)
+    X = rng.standard_normal((n, widths[0])).astype(np.float32)
+    Ws = [(rng.standard_normal((widths[i + 1], widths[i])) * np.sqrt(2.0 / widths[i])).astype(np.float32)
+          for i in range(len(widths) - 1)]
+    G = lognormal_row_gradient(rng, n, widths[-1])
+    return X, Ws, G
+
+
 def linear_outlier(seed=0, n=8192, d_in=1024, d_out=4096, frac=0.01, big=10.0, small=0.01):
     """Transformer-FFN shaped layer: X ~ N(0,1), W ~ N(0, 1/d_in), G with 1% outlier rows.
 
