@@ -152,7 +152,13 @@ typedef struct {
  * (per-row scales lie on grad_W's contraction axis; anything else returns
  * FQT_EUNSUPPORTED).  qb_x feeds grad_X.  f_bits / theta_bits are the
  * deterministic PTQ widths of X and W.  Q_b1 draws from stream 0 and Q_b2
- * from stream 1 of `seed`.                                                  */
+ * from stream 1 of `seed`.
+ * relu_input (linear layer only; the conv returns FQT_EUNSUPPORTED): X is the
+ * output of a ReLU, and grad_X is multiplied by that ReLU's derivative,
+ * 1[X > 0], so it is the gradient of the previous layer's pre-activation.
+ * The ReLU takes no gradient quantizer: its Jacobian is applied exactly to
+ * the float result, as to any elementwise layer of a multi-layer chain
+ * (Sec. 2.2, Eq. (quantized-back-prop) with the identity as its quantizer). */
 typedef struct {
   fqt_qspec qb_w;
   fqt_qspec qb_x;
@@ -160,6 +166,7 @@ typedef struct {
   int theta_bits;
   uint64_t seed;
   const fqt_trace* trace; /* optional, NULL for none */
+  int relu_input;         /* 0: plain grad_X; 1: grad_X * 1[X > 0] */
 } fqt_bwd_cfg;
 
 /* Linear layer FQT backward, Eq. (linear-sq-backprop) with bifurcation:
@@ -173,6 +180,22 @@ fqt_status fqt_linear_backward(const float* X, const float* W, const float* G, i
                                void* ws, size_t ws_bytes, fqt_stream_t s);
 
 size_t fqt_linear_backward_workspace(int64_t N, int64_t d_in, int64_t d_out, const fqt_bwd_cfg* cfg);
+
+/* Linear layer forward of quantization-aware training (Sec. 2.1, Eq.
+ * (quantized-forward-propagation)):
+ *   Y [N, d_out] = Q_f(X) Q_theta(W)^T,   optionally Y = max(Y, 0) (relu != 0)
+ * with Q_f, Q_theta the deterministic per-tensor PTQ of X [N, d_in] and
+ * W [d_out, d_in] at f_bits / theta_bits (round half to even, Sec. 3.3
+ * ranges), contracted on int8 matrix cores with exact int32 accumulators
+ * (int64 across K-splits of d_in > 65536) and dequantized in float64, rounded
+ * to float32.  The same quantizers as the backward, so a layer's forward and
+ * backward see identical Q_f(X) and Q_theta(W).  Y is overwritten; a
+ * non-finite X or W is reported through the workspace status word.
+ * N, d_in, d_out >= 1; bits in 1..8.                                        */
+fqt_status fqt_linear_forward(const float* X, const float* W, int64_t N, int64_t d_in, int64_t d_out, int f_bits,
+                              int theta_bits, int relu, float* Y, void* ws, size_t ws_bytes, fqt_stream_t s);
+
+size_t fqt_linear_forward_workspace(int64_t N, int64_t d_in, int64_t d_out);
 
 /* Conv geometry: X NHWC [n, h, w, c], W [o, kh, kw, c], G NHWC [n, ho, wo, o],
  * ho = (h + 2 pad - kh) / stride + 1 (likewise wo); zero padding.           */

@@ -241,6 +241,39 @@ LinearWs carve_linear(Carver& c, const float* X, const float* W, const float* G,
   return w;
 }
 
+// ---------------------------------------------------------------------------
+// linear forward
+// ---------------------------------------------------------------------------
+struct ForwardWs {
+  Header h;
+  StatsSeg sx_seg, sw_seg;
+  int8_t *qx, *qw;
+  int32_t *sum_x, *sum_w;
+  float *sx, *zx, *sw, *zw;
+  int32_t* part;
+  int splits;
+};
+
+ForwardWs carve_forward(Carver& c, const float* X, const float* W, int64_t N, int64_t d_in, int64_t d_out) {
+  ForwardWs w{};
+  w.h = take_header(c);
+  w.sx_seg = stats_flat_seg(X, N * d_in);
+  w.sw_seg = stats_flat_seg(W, d_out * d_in);
+  w.sx_seg.part = c.take<float2>(stats_partials(w.sx_seg));
+  w.sw_seg.part = c.take<float2>(stats_partials(w.sw_seg));
+  w.qx = c.take<int8_t>(N * d_in);
+  w.qw = c.take<int8_t>(d_out * d_in);
+  w.sum_x = c.take<int32_t>(N);
+  w.sum_w = c.take<int32_t>(d_out);
+  w.sx = c.take<float>(1);
+  w.zx = c.take<float>(1);
+  w.sw = c.take<float>(1);
+  w.zw = c.take<float>(1);
+  w.splits = (int)((d_in + MAX_K_CHUNK - 1) / MAX_K_CHUNK);
+  if (w.splits > 1) w.part = c.take<int32_t>((int64_t)w.splits * N * d_out);
+  return w;
+}
+
 fqt_status check_cfg(const fqt_bwd_cfg* cfg) {
   if (!cfg) return FQT_EINVAL;
   if (!valid_bits(cfg->f_bits) || !valid_bits(cfg->theta_bits) || !valid_bits(cfg->qb_w.bits) ||
@@ -251,6 +284,7 @@ fqt_status check_cfg(const fqt_bwd_cfg* cfg) {
   if (cfg->qb_w.kind != FQT_PTQ) return FQT_EUNSUPPORTED;
   if (cfg->qb_x.kind == FQT_BHQ && cfg->qb_x.block_size != 0 && !valid_block(cfg->qb_x.block_size))
     return FQT_EINVAL;
+  if (cfg->relu_input != 0 && cfg->relu_input != 1) return FQT_EINVAL;
   return FQT_OK;
 }
 
@@ -594,9 +628,101 @@ fqt_status fqt_linear_backward(const float* X, const float* W, const float* G, i
   gx.zeroB = w.zw;
   gx.halfB = 1 << (cfg->theta_bits - 1);
   gx.L = L;
+  gx.mask = cfg->relu_input ? X : nullptr;  // [N, d_in], the same layout as grad_X
   tr.begin(7);
   FQT_TRY(launch_gemm(gx, bhq ? EPI_BHQ : EPI_ROW, s));
   tr.end(7);
+  return FQT_OK;
+}
+
+size_t fqt_linear_forward_workspace(int64_t N, int64_t d_in, int64_t d_out) {
+  if (N < 1 || d_in < 1 || d_out < 1) return 0;
+  Carver c(nullptr);
+  carve_forward(c, nullptr, nullptr, N, d_in, d_out);
+  return c.off;
+}
+
+fqt_status fqt_linear_forward(const float* X, const float* W, int64_t N, int64_t d_in, int64_t d_out, int f_bits,
+                              int theta_bits, int relu, float* Y, void* ws, size_t ws_bytes, fqt_stream_t s) {
+  if (!X || !W || !Y) return FQT_EINVAL;
+  if (N < 1 || d_in < 1 || d_out < 1 || !valid_bits(f_bits) || !valid_bits(theta_bits)) return FQT_EINVAL;
+  if (relu != 0 && relu != 1) return FQT_EINVAL;
+  if (N > MAX_ROWS || d_out > MAX_ROWS || N > 65535LL * 128 || (d_in + MAX_K_CHUNK - 1) / MAX_K_CHUNK > 65535)
+    return FQT_EUNSUPPORTED;
+  if (!ws) return FQT_EWORKSPACE;
+  if (ws_bytes < fqt_linear_forward_workspace(N, d_in, d_out)) return FQT_EWORKSPACE;
+  Carver c(ws);
+  ForwardWs w = carve_forward(c, X, W, N, d_in, d_out);
+
+  // ranges of X and W (per tensor), one launch; then scales and zeroed code sums
+  StatsPlan sp{};
+  sp.seg[0] = w.sx_seg;
+  sp.seg[1] = w.sw_seg;
+  sp.nseg = 2;
+  FQT_TRY(launch_stats(sp, s));
+  FinalizePlan fp{};
+  fp.seg[0] = w.sx_seg;
+  fp.seg[1] = w.sw_seg;
+  fp.nseg = 2;
+  fp.row_seg = -1;
+  fp.status = w.h.status;
+  fp.out[0] = ScaleOut{0, f_bits, 0, w.sx, w.zx};
+  fp.out[1] = ScaleOut{1, theta_bits, 0, w.sw, w.zw};
+  fp.nout = 2;
+  add_zero(fp, w.sum_x, N);
+  add_zero(fp, w.sum_w, d_out);
+  FQT_TRY(launch_finalize(fp, s));
+  // Q_f(X) [N, d_in] and Q_theta(W) [d_out, d_in]: natural layout (K = d_in
+  // contiguous), with per-row code sums for the zero-point terms
+  QuantParams px{};
+  px.x = X;
+  px.rows = N;
+  px.cols = d_in;
+  px.bits = f_bits;
+  px.scale = w.sx;
+  px.zero = w.zx;
+  px.q_nat = w.qx;
+  px.sum_nat = w.sum_x;
+  FQT_TRY(launch_quant(px, QM_TENSOR, s));
+  QuantParams pw{};
+  pw.x = W;
+  pw.rows = d_out;
+  pw.cols = d_in;
+  pw.bits = theta_bits;
+  pw.scale = w.sw;
+  pw.zero = w.zw;
+  pw.q_nat = w.qw;
+  pw.sum_nat = w.sum_w;
+  FQT_TRY(launch_quant(pw, QM_TENSOR, s));
+  // Y = Q_f(X) Q_theta(W)^T: contraction over d_in, per-tensor epilogue
+  GemmParams g{};
+  g.A = w.qx;
+  g.B = w.qw;
+  g.M = N;
+  g.N = d_out;
+  g.K = d_in;
+  g.lda = d_in;
+  g.ldb = d_in;
+  g.splits = w.splits;
+  g.kchunk = w.splits > 1 ? MAX_K_CHUNK : d_in;
+  g.part = w.part;
+  g.out = Y;
+  g.ldo = d_out;
+  g.sumA = w.sum_x;
+  g.sumB = w.sum_w;
+  g.scaleA = w.sx;
+  g.zeroA = w.zx;
+  g.halfA = 1 << (f_bits - 1);
+  g.scaleB = w.sw;
+  g.zeroB = w.zw;
+  g.halfB = 1 << (theta_bits - 1);
+  g.relu = relu;
+  if (w.splits > 1) {
+    FQT_TRY(launch_gemm(g, EPI_RAW_I32, s));
+    FQT_TRY(launch_splitk_reduce(g, nullptr, EPI_TENSOR, s));
+  } else {
+    FQT_TRY(launch_gemm(g, EPI_TENSOR, s));
+  }
   return FQT_OK;
 }
 
@@ -637,6 +763,7 @@ fqt_status fqt_conv_backward_im2col(const float* X, const float* W, const float*
   if (st != FQT_OK) return st;
   st = check_cfg(cfg);
   if (st != FQT_OK) return st;
+  if (cfg->relu_input) return FQT_EUNSUPPORTED;
   if (cfg->qb_x.kind == FQT_BHQ && cfg->qb_x.block_size == 0 && !bhq_adaptive_supported(shape->n))
     return FQT_EUNSUPPORTED;
   if (!ws) return FQT_EWORKSPACE;

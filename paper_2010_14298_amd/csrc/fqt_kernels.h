@@ -205,6 +205,8 @@ struct GemmParams {
   const float* zeroB;
   int halfB;
   BhqLayout L;           // EPI_BHQ group structure
+  int relu;              // EPI_TENSOR: store max(v, 0)
+  const float* mask;     // EPI_ROW / EPI_BHQ: nullptr, or [M, ldo] in output-row order; out = 0 where mask <= 0
 };
 hipError_t launch_gemm(const GemmParams& p, int epi, hipStream_t s);
 

@@ -35,6 +35,13 @@ struct GroupStage {
   int kind;
 };
 
+// grad_X store; with a mask (the layer input X, for the ReLU that produced
+// it) entries where the mask is not positive are zero.
+__device__ __forceinline__ void store_masked(const GemmParams& p, int64_t idx, double v) {
+  const float f = (float)v;
+  p.out[idx] = (p.mask && !(p.mask[idx] > 0.0f)) ? 0.0f : f;
+}
+
 template <class C, int EPI>
 struct GemmLdsSize {
   static constexpr int EP_BYTES = C::BM * C::BN * 4 + C::BM * (int)sizeof(RowStage) + C::BM * (int)sizeof(GroupStage);
@@ -117,7 +124,10 @@ __global__ __launch_bounds__(C::THREADS) void gemm_i8_kernel(GemmParams p) {
 #pragma unroll
         for (int j = 0; j < C::JT; ++j) {
           const int64_t col = n0 + wn * C::WN + j * 32 + lrow;
-          if (col < p.N) p.out[row * p.ldo + col] = (float)(dAB * (double)acc[i][j][r] + rterm + cterm[j]);
+          if (col < p.N) {
+            const float v = (float)(dAB * (double)acc[i][j][r] + rterm + cterm[j]);
+            p.out[row * p.ldo + col] = (p.relu && !(v > 0.0f)) ? 0.0f : v;
+          }
         }
       }
   } else {
@@ -211,7 +221,7 @@ __global__ __launch_bounds__(C::THREADS) void gemm_i8_kernel(GemmParams p) {
             } else {
               v = q.dq * (dW * a + q.rterm) + q.hz * colterm;
             }
-            p.out[q.obase + col] = (float)v;
+            store_masked(p, q.obase + col, v);
           }
         }
       } else {
@@ -219,7 +229,7 @@ __global__ __launch_bounds__(C::THREADS) void gemm_i8_kernel(GemmParams p) {
           const RowStage q = srow[t];
           if (q.obase < 0) continue;
           const double a = (double)sacc[t * C::BN + c];
-          p.out[q.obase + col] = (float)(q.dq * (dW * a + q.rterm) + q.hz * colterm);
+          store_masked(p, q.obase + col, q.dq * (dW * a + q.rterm) + q.hz * colterm);
         }
       }
     }
@@ -246,7 +256,8 @@ __global__ void splitk_reduce_kernel(GemmParams p, int64_t* out64, int epi) {
   const double zB = (double)p.zeroB[0] + (double)p.halfB * dB;
   const double v = dA * dB * (double)sum + dA * zB * (double)p.sumA[row] + zA * dB * (double)p.sumB[col] +
                    (double)p.K * zA * zB;
-  p.out[row * p.ldo + col] = (float)v;
+  const float f = (float)v;
+  p.out[row * p.ldo + col] = (p.relu && !(f > 0.0f)) ? 0.0f : f;
 }
 
 hipError_t launch_splitk_reduce(const GemmParams& p, int64_t* out64, int epi, hipStream_t s) {

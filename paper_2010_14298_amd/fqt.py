@@ -46,7 +46,7 @@ class Trace(ctypes.Structure):
 
 class BwdCfg(ctypes.Structure):
     _fields_ = [("qb_w", QSpec), ("qb_x", QSpec), ("f_bits", ctypes.c_int), ("theta_bits", ctypes.c_int),
-                ("seed", ctypes.c_uint64), ("trace", ctypes.POINTER(Trace))]
+                ("seed", ctypes.c_uint64), ("trace", ctypes.POINTER(Trace)), ("relu_input", ctypes.c_int)]
 
 
 class ConvShape(ctypes.Structure):
@@ -57,6 +57,7 @@ EXPORTS = [
     "fqt_quantize_ptq", "fqt_quantize_psq", "fqt_quantize_bhq", "fqt_quantize_workspace",
     "fqt_bhq_adaptive_block", "fqt_bhq_adaptive_workspace",
     "fqt_linear_backward", "fqt_linear_backward_workspace",
+    "fqt_linear_forward", "fqt_linear_forward_workspace",
     "fqt_conv_backward_im2col", "fqt_conv_backward_workspace",
     "fqt_gemm_s8s8_s64", "fqt_gemm_workspace",
     "fqt_workspace_status", "fqt_status_str", "fqt_version",
@@ -87,6 +88,8 @@ def load(path=LIB_PATH):
         "fqt_bhq_adaptive_workspace": ([i64, i64], sz),
         "fqt_linear_backward": ([vp, vp, vp, i64, i64, i64, cfgp, vp, vp, vp, sz, vp], i32),
         "fqt_linear_backward_workspace": ([i64, i64, i64, cfgp], sz),
+        "fqt_linear_forward": ([vp, vp, i64, i64, i64, i32, i32, i32, vp, vp, sz, vp], i32),
+        "fqt_linear_forward_workspace": ([i64, i64, i64], sz),
         "fqt_conv_backward_im2col": ([vp, vp, vp, shp, cfgp, vp, vp, vp, sz, vp], i32),
         "fqt_conv_backward_workspace": ([shp, cfgp], sz),
         "fqt_gemm_s8s8_s64": ([vp, vp, i64, i64, i64, i64, i64, vp, vp, sz, vp], i32),
@@ -126,10 +129,11 @@ def _workspace(nbytes, device):
     return torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=device)
 
 
-def cfg_struct(qb_x=("psq", 8, 0), qb_w=("ptq", 8, 0), f_bits=8, theta_bits=8, seed=0, trace=None):
+def cfg_struct(qb_x=("psq", 8, 0), qb_w=("ptq", 8, 0), f_bits=8, theta_bits=8, seed=0, trace=None,
+               relu_input=False):
     return BwdCfg(QSpec(KINDS[qb_w[0]], int(qb_w[1]), int(qb_w[2])),
                   QSpec(KINDS[qb_x[0]], int(qb_x[1]), int(qb_x[2])), int(f_bits), int(theta_bits), int(seed),
-                  ctypes.pointer(trace) if trace is not None else None)
+                  ctypes.pointer(trace) if trace is not None else None, int(bool(relu_input)))
 
 
 # ----------------------------------------------------------------------------
@@ -215,13 +219,13 @@ def fqt_linear_backward_workspace(N, d_in, d_out, cfg):
 
 
 def fqt_linear_backward(X, W, G, qb_x=("psq", 8, 0), qb_w=("ptq", 8, 0), f_bits=8, theta_bits=8, seed=0,
-                        grad_W=None, grad_X=None, ws=None, trace=None):
+                        grad_W=None, grad_X=None, ws=None, trace=None, relu_input=False):
     X, W, G = _f32(X, "X"), _f32(W, "W"), _f32(G, "G")
     N, d_in = X.shape
     d_out = W.shape[0]
     if W.shape != (d_out, d_in) or G.shape != (N, d_out):
         raise ValueError("shapes: X [N, d_in], W [d_out, d_in], G [N, d_out]")
-    cfg = cfg_struct(qb_x, qb_w, f_bits, theta_bits, seed, trace)
+    cfg = cfg_struct(qb_x, qb_w, f_bits, theta_bits, seed, trace, relu_input)
     if grad_W is None:
         grad_W = torch.empty((d_out, d_in), dtype=torch.float32, device=X.device)
     if grad_X is None:
@@ -232,6 +236,27 @@ def fqt_linear_backward(X, W, G, qb_x=("psq", 8, 0), qb_w=("ptq", 8, 0), f_bits=
                                     _ptr(grad_X), _ptr(ws), ws.numel(), _stream())
     _check("fqt_linear_backward", rc)
     return grad_W, grad_X, ws
+
+
+def fqt_linear_forward_workspace(N, d_in, d_out):
+    return load().fqt_linear_forward_workspace(N, d_in, d_out)
+
+
+def fqt_linear_forward(X, W, f_bits=8, theta_bits=8, relu=False, Y=None, ws=None):
+    """Y = Q_f(X) Q_theta(W)^T (then max(., 0) when relu); returns (Y, ws)."""
+    X, W = _f32(X, "X"), _f32(W, "W")
+    N, d_in = X.shape
+    d_out = W.shape[0]
+    if W.shape != (d_out, d_in):
+        raise ValueError("shapes: X [N, d_in], W [d_out, d_in]")
+    if Y is None:
+        Y = torch.empty((N, d_out), dtype=torch.float32, device=X.device)
+    if ws is None:
+        ws = _workspace(fqt_linear_forward_workspace(N, d_in, d_out), X.device)
+    rc = load().fqt_linear_forward(_ptr(X), _ptr(W), N, d_in, d_out, int(f_bits), int(theta_bits), int(bool(relu)),
+                                   _ptr(Y), _ptr(ws), ws.numel(), _stream())
+    _check("fqt_linear_forward", rc)
+    return Y, ws
 
 
 def conv_shape(n, c, h, w, o, kh, kw, stride, pad):
@@ -341,3 +366,40 @@ def free_trace(t):
     for i in range(t.count):
         hip.hipEventDestroy(t.start[i])
         hip.hipEventDestroy(t.stop[i])
+
+
+# ----------------------------------------------------------------------------
+# multi-layer chain: a ReLU MLP, one library call per layer
+# ----------------------------------------------------------------------------
+def mlp_forward(X, Ws, f_bits=8, theta_bits=8, ws=None):
+    """Layer inputs A_0 = X, A_{i+1} = ReLU(Q_f(A_i) Q_theta(W_i)^T), and the
+    top layer's (linear) output.  Returns (acts, Z_top)."""
+    acts = [X]
+    Z = None
+    for i, W in enumerate(Ws):
+        last = i == len(Ws) - 1
+        need = fqt_linear_forward_workspace(acts[-1].shape[0], W.shape[1], W.shape[0])
+        Y, ws = fqt_linear_forward(acts[-1], W, f_bits, theta_bits, relu=not last,
+                                   ws=ws if ws is not None and ws.numel() >= need else None)
+        if last:
+            Z = Y
+        else:
+            acts.append(Y)
+    return acts, Z
+
+
+def mlp_backward(acts, Ws, G, specs, seeds, qb_w=("ptq", 8, 0), f_bits=8, theta_bits=8):
+    """FQT backward of the chain from the top output gradient G: layer i runs
+    fqt_linear_backward with quantizer specs[i] and seed seeds[i]; below the
+    top, grad_X is masked by the ReLU that produced the layer input.
+    Returns (grads_W, dZ) per layer (dZ[i] is layer i's output gradient)."""
+    L = len(Ws)
+    grads, dZs = [None] * L, [None] * L
+    dZ = G
+    for i in range(L - 1, -1, -1):
+        dZs[i] = dZ
+        gW, gX, ws = fqt_linear_backward(acts[i], Ws[i], dZ, qb_x=specs[i], qb_w=qb_w, f_bits=f_bits,
+                                         theta_bits=theta_bits, seed=seeds[i], relu_input=i > 0)
+        grads[i] = gW
+        dZ = gX
+    return grads, dZs

@@ -86,3 +86,20 @@ def test_workspace_queries_and_argument_errors():
     assert lib.fqt_quantize_bhq(fake, 4, 4, 5, 64, 0, 0, ctypes.byref(qt), fake, 1 << 30, null) == 1   # no perm
     assert lib.fqt_gemm_s8s8_s64(fake, fake, 4, 4, 8, 4, 8, fake, fake, 1 << 30, null) == 1            # lda < K
     assert lib.fqt_status_str(3) == b"non-finite input or range overflow"
+    # layer forward: bits, relu flag, workspace
+    assert lib.fqt_linear_forward_workspace(0, 4, 4) == 0
+    assert lib.fqt_linear_forward_workspace(8192, 1024, 4096) >= 8192 * 1024 + 4096 * 1024
+    assert lib.fqt_linear_forward(null, fake, 4, 8, 3, 8, 8, 0, fake, fake, 1 << 30, null) == 1
+    assert lib.fqt_linear_forward(fake, fake, 4, 8, 3, 9, 8, 0, fake, fake, 1 << 30, null) == 1
+    assert lib.fqt_linear_forward(fake, fake, 4, 8, 3, 8, 8, 2, fake, fake, 1 << 30, null) == 1
+    assert lib.fqt_linear_forward(fake, fake, 4, 8, 3, 8, 8, 1, fake, fake, 16, null) == 4
+    assert lib.fqt_linear_forward(fake, fake, 4, 8, 3, 8, 8, 1, fake, null, 1 << 30, null) == 4
+    # relu_input: 0 or 1; the conv backward has no masked epilogue
+    relu2 = fqt.cfg_struct(relu_input=True)
+    relu2.relu_input = 2
+    rc = lib.fqt_linear_backward(fake, fake, fake, 4, 4, 4, ctypes.byref(relu2), fake, fake, fake, 1 << 30, null)
+    assert rc == 1
+    sh = fqt.conv_shape(2, 4, 8, 8, 4, 3, 3, 1, 1)
+    rc = lib.fqt_conv_backward_im2col(fake, fake, fake, ctypes.byref(sh), ctypes.byref(fqt.cfg_struct(relu_input=True)),
+                                      fake, fake, fake, 1 << 30, null)
+    assert rc == 2
