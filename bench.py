@@ -41,6 +41,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=50)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-chain", action="store_true", help="skip the multi-layer chain measurement")
     ap.add_argument("--copy-probe", action="store_true",
                     help="after timing, run a plain 256 MiB elementwise pass (traffic-counter calibration)")
     return ap.parse_args()
@@ -87,6 +88,46 @@ def cpu_baseline(X, W, G):
     ops = 2.0 * 2.0 * n * D_IN * D_OUT
     return {"value": ops / dt / 1e12, "unit": "TOPS", "cores": int(threads), "kind": "oracle",
             "sample": f"first {n} of {N} samples of the same layer (full d_in, d_out), BHQ-5 k=64; {dt:.1f} s"}
+
+
+CHAIN_WIDTHS = (1024, 4096, 4096, 1024)   # FFN-like ReLU MLP: up, square, down
+
+
+def chain_bench(args, fqt, synth, torch):
+    """The multi-layer chain: forward (Q_f, Q_theta, int8 product, ReLU) and FQT
+    backward (Q_b2 = BHQ 5-bit, Q_b1 = PTQ 8-bit, ReLU masks) of a 3-layer MLP
+    on N tokens, timed with HIP events on the library's stream."""
+    import numpy as np
+    X, Ws, _ = synth.mlp(seed=0, n=N, widths=CHAIN_WIDTHS)
+    _, _, Gtop = synth.linear_outlier(seed=1, n=N, d_in=8, d_out=CHAIN_WIDTHS[-1])
+    dX, dG = torch.from_numpy(X).cuda(), torch.from_numpy(Gtop).cuda()
+    dWs = [torch.from_numpy(W).cuda() for W in Ws]
+    specs = [QB_X] * len(dWs)
+    steps = max(1, args.steps // 4)
+    for i in range(max(1, args.warmup // 4)):
+        acts, _ = fqt.mlp_forward(dX, dWs)
+        fqt.mlp_backward(acts, dWs, dG, specs, [i] * len(dWs), qb_w=QB_W)
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    fwd, bwd = [], []
+    for i in range(steps):
+        ev[0].record()
+        acts, _ = fqt.mlp_forward(dX, dWs)
+        ev[1].record()
+        fqt.mlp_backward(acts, dWs, dG, specs, [3 * i + j for j in range(len(dWs))], qb_w=QB_W)
+        ev[2].record()
+        torch.cuda.synchronize()
+        fwd.append(ev[0].elapsed_time(ev[1]))
+        bwd.append(ev[1].elapsed_time(ev[2]))
+    layer_ops = sum(2.0 * N * CHAIN_WIDTHS[i] * CHAIN_WIDTHS[i + 1] for i in range(len(dWs)))
+    f_ms, b_ms = float(np.mean(fwd)), float(np.mean(bwd))
+    return {"workload": f"ReLU MLP {'-'.join(map(str, CHAIN_WIDTHS))}, N={N}; forward + FQT backward "
+                        "(Q_b2 = BHQ 5-bit block 64, Q_b1 = PTQ 8-bit)",
+            "steps": steps, "forward_ms": round(f_ms, 4), "backward_ms": round(b_ms, 4),
+            "ms_per_step": round(f_ms + b_ms, 4),
+            "forward_TOPS": round(layer_ops / (f_ms * 1e-3) / 1e12, 2),
+            "backward_TOPS": round(2.0 * layer_ops / (b_ms * 1e-3) / 1e12, 2),
+            "TOPS": round(3.0 * layer_ops / ((f_ms + b_ms) * 1e-3) / 1e12, 2)}
 
 
 def main():
@@ -188,6 +229,8 @@ def main():
         "kernels": per_kernel,
         "roofline": roof,
     }
+    if not args.no_chain:
+        out["chain"] = chain_bench(args, fqt, synth, torch)
     if args.copy_probe:
         # a plain elementwise pass: reads 256 MiB, writes 256 MiB
         src = torch.ones(64 * 1024 * 1024, dtype=torch.float32, device="cuda")
