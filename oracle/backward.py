@@ -31,6 +31,8 @@ def quantize_gradient(G, spec, seed, stream):
         return Q.quantize_psq(G, bits, seed, stream)
     if kind == "bhq":
         return Q.quantize_bhq(G, bits, k, seed, stream)
+    if kind == "shift":
+        return Q.quantize_shift(G, bits, seed, stream)
     raise ValueError(kind)
 
 
@@ -52,7 +54,7 @@ def linear_backward(X, W, G, qb_x=("psq", 8, 0), qb_w=("ptq", 8, 0), f_bits=8, t
     G1r, G2r = Q.dequantize(qb1), Q.dequantize(qb2)
     grad_W = (G1r.T @ Xr).astype(np.float32)
     grad_X = (G2r @ Wr).astype(np.float32)
-    acc_w = Q.offset_codes(qb1).T @ Q.offset_codes(qx)
+    acc_w = (Q.shifted_codes(qb1) if qb1["kind"] == "shift" else Q.offset_codes(qb1)).T @ Q.offset_codes(qx)
     acc_x = slot_codes(qb2) @ Q.offset_codes(qw)
     return dict(qx=qx, qw=qw, qb1=qb1, qb2=qb2, grad_W=grad_W, grad_X=grad_X,
                 acc_w=acc_w, acc_x=acc_x, grad_W64=G1r.T @ Xr, grad_X64=G2r @ Wr)

@@ -125,7 +125,7 @@ def conditional_variance(J, G, q):
     nrm = (J ** 2).sum(axis=2)                               # [N, d] response norms of unit perturbations
     if q["kind"] == "ptq":
         return float((v * nrm).sum() / float(q["scale"]) ** 2)
-    if q["kind"] == "psq":
+    if q["kind"] in ("psq", "shift"):
         return float(((v / q["scale"][:, None].astype(np.float64) ** 2) * nrm).sum())
     total = 0.0
     for info, Si in theory.inverse_scale_blocks(q):

@@ -127,6 +127,49 @@ def quantize_psq(x, bits, seed=0, stream=0):
     return dict(kind="psq", code=code, scale=s, zero=mn.astype(np.float32), bits=int(bits))
 
 
+def shift_limit(bits):
+    """E = min(4, 8 - b): the largest left shift that keeps a b-bit offset code
+    (code - 2^(b-1) in [-2^(b-1), 2^(b-1) - 1]) inside int8."""
+    return min(4, 8 - int(bits))
+
+
+def quantize_shift(x, bits, seed=0, stream=0):
+    """Per-tensor range with per-sample power-of-two steps (Sec. 4.3, the
+    hardware variant of PSQ): R = max_i R_i, s = B / R; per row z_i = min_i,
+    e_i = the largest e in [0, E] with R_i 2^e <= R, s_i = s 2^e_i (float32,
+    saturating at FLT_MAX); y = s_i (x - z_i) with SR per element, as PSQ.
+
+    `shift` holds E - e_i, the left shift that brings row i's offset codes to
+    the common step 1 / (s 2^E).
+    """
+    x = np.asarray(x, dtype=np.float32)
+    rows, cols = x.shape
+    B = n_bins(bits)
+    E = shift_limit(bits)
+    mn, _, R, _ = row_stats(x)
+    Rt = np.float32(R.max()) if rows else np.float32(0)
+    st = scale_from_range(Rt, B)
+    scale = np.zeros(rows, np.float32)
+    shift = np.zeros(rows, np.int64)
+    for i in range(rows):
+        e = 0
+        # R_i 2^(e+1) <= R: both sides exact (power-of-two scaling of a float32)
+        while e < E and float(R[i]) * 2.0 ** (e + 1) <= float(Rt):
+            e += 1
+        scale[i] = to_f32_sat(float(st) * 2.0 ** e)
+        shift[i] = E - e
+    e_idx = np.arange(rows * cols, dtype=np.uint64).reshape(rows, cols)
+    code = _affine_codes(x, scale[:, None], mn[:, None], bits, True, seed, stream, e_idx)
+    return dict(kind="shift", code=code, scale=scale, zero=mn.astype(np.float32), shift=shift,
+                step_scale=st, bits=int(bits))
+
+
+def shifted_codes(q):
+    """Offset codes shifted left by each row's shift: the int8 operands of the
+    grad_W contraction for a `shift` quantizer (all rows at step 1 / (s 2^E))."""
+    return offset_codes(q) << q["shift"][:, None]
+
+
 def dequantize_affine(q):
     """Real value of each code, code / s + z, in float64 (Sec. 3.3 inverse map)."""
     s = np.asarray(q["scale"], dtype=np.float64)

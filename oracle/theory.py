@@ -71,7 +71,7 @@ def transformed_values(x, q):
     x = np.asarray(x, np.float32)
     if q["kind"] == "ptq":
         return (q["scale"] * (x - q["zero"]).astype(np.float32)).astype(np.float32)
-    if q["kind"] == "psq":
+    if q["kind"] in ("psq", "shift"):
         return (q["scale"][:, None] * (x - q["zero"][:, None]).astype(np.float32)).astype(np.float32)
     y = np.zeros_like(x)
     for info in q["plan"]["groups"]:
@@ -97,7 +97,7 @@ def exact_elementwise_variance(x, q):
     v = sr.exact_var_code(y)                     # per code element (slot order for BHQ)
     if q["kind"] == "ptq":
         return v / float(q["scale"]) ** 2
-    if q["kind"] == "psq":
+    if q["kind"] in ("psq", "shift"):
         return v / q["scale"][:, None].astype(np.float64) ** 2
     out = np.zeros(v.shape)
     for info, Si in inverse_scale_blocks(q):
