@@ -55,7 +55,10 @@ typedef enum {
   FQT_EDEVICE = 5        /* a HIP runtime call failed */
 } fqt_status;
 
-typedef enum { FQT_PTQ = 0, FQT_PSQ = 1, FQT_BHQ = 2 } fqt_kind;
+/* FQT_SHIFT: per-tensor range with per-sample power-of-two steps (Sec. 4.3,
+ * the variant for integer hardware): a grad_W quantizer (qb_w) whose
+ * per-sample scales survive the int8 contraction over samples.           */
+typedef enum { FQT_PTQ = 0, FQT_PSQ = 1, FQT_BHQ = 2, FQT_SHIFT = 3 } fqt_kind;
 
 /* One quantized matrix (Sec. 3.3 / Eq. matrix-quantizer).  Every pointer is
  * caller-owned device memory; a NULL optional pointer is skipped.
@@ -83,6 +86,7 @@ typedef struct {
   int32_t* perm;
   int32_t* group_off;
   int32_t* code_sum;
+  int8_t* shift;  /* FQT_SHIFT only: [rows] left shift of each row's offset codes */
 } fqt_qtensor;
 
 /* Per-tensor quantizer, Sec. 3.3: z = min x, s = B / (max x - min x),
@@ -109,6 +113,19 @@ fqt_status fqt_quantize_psq(const float* x, int64_t rows, int64_t cols, int bits
 fqt_status fqt_quantize_bhq(const float* x, int64_t rows, int64_t cols, int bits, int block_size,
                             uint64_t seed, uint32_t stream, const fqt_qtensor* out, void* ws,
                             size_t ws_bytes, fqt_stream_t s);
+
+/* Per-tensor range with per-sample power-of-two steps, Sec. 4.3: R = max_i
+ * R_i (the largest row range), s = B / R; row i has z_i = row min and the
+ * largest e_i in [0, E], E = min(4, 8 - bits), with R_i 2^e_i <= R, so
+ * s_i = s 2^e_i (saturating at FLT_MAX); code = SR(s_i (x - z_i)) as PSQ.
+ * q holds each row's offset code shifted left by shift[i] = E - e_i, which
+ * stays in int8: every row then counts in the common step 1 / (s 2^E), so an
+ * int8 contraction over rows is exact.  code_sum sums the shifted codes.
+ * Natural ([rows, cols]) or transposed (transpose != 0) layout.  Needs
+ * out->q, out->scale [rows] (s_i), out->zero [rows] (z_i), out->shift.     */
+fqt_status fqt_quantize_shift(const float* x, int64_t rows, int64_t cols, int bits, uint64_t seed,
+                              uint32_t stream, int transpose, const fqt_qtensor* out, void* ws,
+                              size_t ws_bytes, fqt_stream_t s);
 
 size_t fqt_quantize_workspace(fqt_kind kind, int64_t rows, int64_t cols, int block_size);
 
@@ -149,8 +166,9 @@ typedef struct {
 } fqt_trace;
 
 /* Layer backward configuration (App. E).  qb_w feeds grad_W and must be PTQ
- * (per-row scales lie on grad_W's contraction axis; anything else returns
- * FQT_EUNSUPPORTED).  qb_x feeds grad_X.  f_bits / theta_bits are the
+ * or, for the linear layer, FQT_SHIFT (per-row scales lie on grad_W's
+ * contraction axis; power-of-two ones survive it as shifted codes; PSQ / BHQ
+ * return FQT_EUNSUPPORTED).  qb_x feeds grad_X (PTQ, PSQ or BHQ).  f_bits / theta_bits are the
  * deterministic PTQ widths of X and W.  Q_b1 draws from stream 0 and Q_b2
  * from stream 1 of `seed`.
  * relu_input (linear layer only; the conv returns FQT_EUNSUPPORTED): X is the

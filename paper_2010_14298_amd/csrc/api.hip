@@ -64,6 +64,7 @@ struct QuantWs {
   float* rmax;
   void* plan;
   void* adaptive;
+  float* tscale;  // FQT_SHIFT: the per-tensor step scale s
 };
 
 QuantWs carve_quant(Carver& c, fqt_kind kind, const float* x, int64_t rows, int64_t cols, int block_size = 1) {
@@ -78,6 +79,7 @@ QuantWs carve_quant(Carver& c, fqt_kind kind, const float* x, int64_t rows, int6
   }
   if (kind == FQT_BHQ) w.plan = c.take<char>((int64_t)bhq_plan_workspace(rows));
   if (kind == FQT_BHQ && block_size == 0) w.adaptive = c.take<char>((int64_t)bhq_adaptive_workspace(rows));
+  if (kind == FQT_SHIFT) w.tscale = c.take<float>(1);
   return w;
 }
 
@@ -118,6 +120,7 @@ fqt_status quantize_common(fqt_kind kind, const float* x, int64_t rows, int64_t 
     if (block_size == 0 && !bhq_adaptive_supported(rows)) return FQT_EUNSUPPORTED;
     if ((block_size != 0 && !valid_block(block_size)) || !out->perm) return FQT_EINVAL;
   }
+  if (kind == FQT_SHIFT && !out->shift) return FQT_EINVAL;
   if (!ws) return FQT_EWORKSPACE;
   Carver cs(nullptr);
   carve_quant(cs, kind, x, rows, cols, block_size);
@@ -137,7 +140,8 @@ fqt_status quantize_common(fqt_kind kind, const float* x, int64_t rows, int64_t 
   fp.rmax = w.rmax;
   fp.status = w.h.status;
   if (kind != FQT_BHQ) {
-    fp.out[0] = ScaleOut{0, bits, kind == FQT_PSQ ? 1 : 0, out->scale, out->zero};
+    const int per_row = kind == FQT_SHIFT ? 2 : (kind == FQT_PSQ ? 1 : 0);
+    fp.out[0] = ScaleOut{0, bits, per_row, out->scale, out->zero, out->shift, w.tscale};
     fp.nout = 1;
   }
   add_zero(fp, out->code_sum, transpose ? cols : rows);
@@ -170,8 +174,9 @@ fqt_status quantize_common(fqt_kind kind, const float* x, int64_t rows, int64_t 
     p.sum_nat = out->code_sum;
   }
   int mode = QM_TENSOR;
-  if (kind == FQT_PSQ) {
+  if (kind == FQT_PSQ || kind == FQT_SHIFT) {
     mode = QM_ROW;
+    if (kind == FQT_SHIFT) p.shift = out->shift;
   } else if (kind == FQT_BHQ) {
     p.L = bhq_layout(rows, block_size);
     FQT_TRY(launch_bhq_plan(w.rmin, w.rmax, p.L, bits, w.plan, out->perm, out->scale, out->zero, out->group_off,
@@ -198,6 +203,9 @@ struct LinearWs {
   void* adaptive;
   int32_t* part;
   int splits;
+  int8_t* shift1;    // Q_b1 = FQT_SHIFT: per-row shifts, step scale, zero-point column vector
+  float* tscale1;
+  double* colvec;
 };
 
 int linear_splits(int64_t N) { return (int)((N + MAX_K_CHUNK - 1) / MAX_K_CHUNK); }
@@ -227,8 +235,14 @@ LinearWs carve_linear(Carver& c, const float* X, const float* W, const float* G,
   w.zx = c.take<float>(1);
   w.sw = c.take<float>(1);
   w.zw = c.take<float>(1);
-  w.sg1 = c.take<float>(1);
-  w.zg1 = c.take<float>(1);
+  const bool shift = cfg.qb_w.kind == FQT_SHIFT;
+  w.sg1 = c.take<float>(shift ? N : 1);
+  w.zg1 = c.take<float>(shift ? N : 1);
+  if (shift) {
+    w.shift1 = c.take<int8_t>(N);
+    w.tscale1 = c.take<float>(1);
+    w.colvec = c.take<double>(d_in);
+  }
   w.sg2 = c.take<float>(N);
   w.zg2 = c.take<float>(N);
   if (cfg.qb_x.kind == FQT_BHQ) {
@@ -279,9 +293,11 @@ fqt_status check_cfg(const fqt_bwd_cfg* cfg) {
   if (!valid_bits(cfg->f_bits) || !valid_bits(cfg->theta_bits) || !valid_bits(cfg->qb_w.bits) ||
       !valid_bits(cfg->qb_x.bits))
     return FQT_EINVAL;
-  if (cfg->qb_x.kind < FQT_PTQ || cfg->qb_x.kind > FQT_BHQ || cfg->qb_w.kind < FQT_PTQ || cfg->qb_w.kind > FQT_BHQ)
+  if (cfg->qb_x.kind < FQT_PTQ || cfg->qb_x.kind > FQT_SHIFT || cfg->qb_w.kind < FQT_PTQ ||
+      cfg->qb_w.kind > FQT_SHIFT)
     return FQT_EINVAL;
-  if (cfg->qb_w.kind != FQT_PTQ) return FQT_EUNSUPPORTED;
+  if ((cfg->qb_w.kind != FQT_PTQ && cfg->qb_w.kind != FQT_SHIFT) || cfg->qb_x.kind == FQT_SHIFT)
+    return FQT_EUNSUPPORTED;
   if (cfg->qb_x.kind == FQT_BHQ && cfg->qb_x.block_size != 0 && !valid_block(cfg->qb_x.block_size))
     return FQT_EINVAL;
   if (cfg->relu_input != 0 && cfg->relu_input != 1) return FQT_EINVAL;
@@ -398,6 +414,11 @@ fqt_status fqt_quantize_ptq(const float* x, int64_t rows, int64_t cols, int bits
                          ws, ws_bytes, s);
 }
 
+fqt_status fqt_quantize_shift(const float* x, int64_t rows, int64_t cols, int bits, uint64_t seed, uint32_t stream,
+                              int transpose, const fqt_qtensor* out, void* ws, size_t ws_bytes, fqt_stream_t s) {
+  return quantize_common(FQT_SHIFT, x, rows, cols, bits, 1, seed, stream, transpose, 1, out, ws, ws_bytes, s);
+}
+
 fqt_status fqt_quantize_psq(const float* x, int64_t rows, int64_t cols, int bits, uint64_t seed, uint32_t stream,
                             const fqt_qtensor* out, void* ws, size_t ws_bytes, fqt_stream_t s) {
   return quantize_common(FQT_PSQ, x, rows, cols, bits, 1, seed, stream, 0, 0, out, ws, ws_bytes, s);
@@ -496,7 +517,8 @@ fqt_status fqt_linear_backward(const float* X, const float* W, const float* G, i
   fp.status = w.h.status;
   fp.out[0] = ScaleOut{0, cfg->f_bits, 0, w.sx, w.zx};
   fp.out[1] = ScaleOut{1, cfg->theta_bits, 0, w.sw, w.zw};
-  fp.out[2] = ScaleOut{2, cfg->qb_w.bits, 0, w.sg1, w.zg1};
+  const bool shift1 = cfg->qb_w.kind == FQT_SHIFT;
+  fp.out[2] = ScaleOut{2, cfg->qb_w.bits, shift1 ? 2 : 0, w.sg1, w.zg1, w.shift1, w.tscale1};
   fp.nout = 3;
   if (qx.kind != FQT_BHQ) fp.out[fp.nout++] = ScaleOut{2, qx.bits, qx.kind == FQT_PSQ ? 1 : 0, w.sg2, w.zg2};
   add_zero(fp, w.sum_x, d_in);
@@ -560,6 +582,7 @@ fqt_status fqt_linear_backward(const float* X, const float* W, const float* G, i
   pg.stream2 = 0;
   pg.scale2 = w.sg1;
   pg.zero2 = w.zg1;
+  pg.shift2 = w.shift1;
   pg.q2_t = w.qg1_t;
   pg.sum2_t = w.sum_g1;
   pg.L = L;
@@ -572,6 +595,23 @@ fqt_status fqt_linear_backward(const float* X, const float* W, const float* G, i
   tr.end(4);
   tr.begin(5);
   FQT_TRY(launch_quant_fused(pg, mode, px, pw, s));
+  if (shift1) {
+    // Q_b1's per-sample zero points meet X along the contraction: their
+    // terms form one float64 vector over d_in
+    ColvecParams cv{};
+    cv.q_t = w.qx_t;
+    cv.rows = N;
+    cv.cols = d_in;
+    cv.perm = w.perm;
+    cv.scale = w.sg1;
+    cv.zero = w.zg1;
+    cv.half = 1 << (cfg->qb_w.bits - 1);
+    cv.scaleX = w.sx;
+    cv.zeroX = w.zx;
+    cv.halfX = 1 << (cfg->f_bits - 1);
+    cv.out = w.colvec;
+    FQT_TRY(launch_colvec(cv, s));
+  }
   tr.end(5);
 
   // grad_W [d_out, d_in] = Q_b1(G)^T Q_f(X): contraction over the N samples
@@ -593,6 +633,12 @@ fqt_status fqt_linear_backward(const float* X, const float* W, const float* G, i
   gw.scaleA = w.sg1;
   gw.zeroA = w.zg1;
   gw.halfA = 1 << (cfg->qb_w.bits - 1);
+  if (shift1) {
+    // shifted codes count in the common step 1 / (s 2^E), E = min(4, 8 - bits)
+    gw.scaleA = w.tscale1;
+    gw.expA = cfg->qb_w.bits <= 4 ? 4 : 8 - cfg->qb_w.bits;
+    gw.colvec = w.colvec;
+  }
   gw.scaleB = w.sx;
   gw.zeroB = w.zx;
   gw.halfB = 1 << (cfg->f_bits - 1);
@@ -763,7 +809,7 @@ fqt_status fqt_conv_backward_im2col(const float* X, const float* W, const float*
   if (st != FQT_OK) return st;
   st = check_cfg(cfg);
   if (st != FQT_OK) return st;
-  if (cfg->relu_input) return FQT_EUNSUPPORTED;
+  if (cfg->relu_input || cfg->qb_w.kind == FQT_SHIFT) return FQT_EUNSUPPORTED;
   if (cfg->qb_x.kind == FQT_BHQ && cfg->qb_x.block_size == 0 && !bhq_adaptive_supported(shape->n))
     return FQT_EUNSUPPORTED;
   if (!ws) return FQT_EWORKSPACE;

@@ -93,6 +93,11 @@ __device__ __forceinline__ int32_t rne_top(float y, float Bf, uint32_t hoff) {
   const float r = rintf(__builtin_amdgcn_fmed3f(y, 0.0f, Bf));
   return (int32_t)(((uint32_t)(int)r << 24) - hoff);
 }
+// The offset code in the top byte of t shifted left by sh (the caller keeps
+// the result inside int8); the low 24 bits are dropped.
+__device__ __forceinline__ int32_t shift_top(int32_t t, int sh) {
+  return (int32_t)(((uint32_t)t & 0xFF000000u) << sh);
+}
 // Top bytes of a, b, c, d as bytes 0..3 of one word.
 __device__ __forceinline__ uint32_t pack_top4(int32_t a, int32_t b, int32_t c, int32_t d) {
   const uint32_t lo = __builtin_amdgcn_perm((uint32_t)b, (uint32_t)a, 0x0c0c0703u);

@@ -45,12 +45,17 @@ hipError_t launch_stats(StatsPlan sp, hipStream_t s);
 // One finalize block: per-tensor PTQ scale / zero (Sec. 3.3), per-row PSQ
 // scale / zero (Sec. 4.1), per-row min / max of the row segment, cleared
 // int32 arrays and the status word.
+// per_row: 0 per tensor (PTQ), 1 per row (PSQ), 2 per-tensor range with
+// per-row power-of-two steps (Sec. 4.3): s_i = s 2^e_i, shift[row] = E - e_i,
+// E = min(4, 8 - bits), and s itself in tensor_scale[0].
 struct ScaleOut {
   int seg;
   int bits;
   int per_row;
   float* scale;
   float* zero;
+  int8_t* shift;
+  float* tensor_scale;
 };
 struct FinalizePlan {
   StatsSeg seg[3];
@@ -144,6 +149,8 @@ struct QuantParams {
   const float* zero2;
   int8_t* q2_t;
   int32_t* sum2_t;
+  const int8_t* shift;   // QM_ROW: per-row left shift of the offset codes, or nullptr
+  const int8_t* shift2;  // Q_b1 with per-row scale2 / zero2 / shift2 (source-row order), or nullptr
   BhqLayout L;
 };
 enum QuantMode { QM_TENSOR = 0, QM_ROW = 1, QM_BHQ = 2 };
@@ -206,6 +213,8 @@ struct GemmParams {
   int halfB;
   BhqLayout L;           // EPI_BHQ group structure
   int relu;              // EPI_TENSOR: store max(v, 0)
+  int expA;              // EPI_TENSOR: A's step is 1 / (scaleA[0] 2^expA)
+  const double* colvec;  // EPI_TENSOR: nullptr, or [N] replacing A's zero-point terms (per-row zeros of A)
   const float* mask;     // EPI_ROW / EPI_BHQ: nullptr, or [M, ldo] in output-row order; out = 0 where mask <= 0
 };
 hipError_t launch_gemm(const GemmParams& p, int epi, hipStream_t s);
@@ -213,6 +222,24 @@ hipError_t launch_gemm(const GemmParams& p, int epi, hipStream_t s);
 // Sum int32 split partials in int64; either store int64 (out64) or apply the
 // per-tensor epilogue (EPI_TENSOR) into p.out.
 hipError_t launch_splitk_reduce(const GemmParams& p, int64_t* out64, int epi, hipStream_t s);
+
+// Zero-point term of a contraction over samples whose A rows (samples) carry
+// their own zero points: v[c] = sum_n zeta_n Xt[n, c], zeta_n = half / s_n +
+// z_n, Xt[n, c] = dx q[c, slot(n)] + zx (q: [cols, rows] transposed codes in
+// slot order, perm slot -> row or nullptr), float64.
+struct ColvecParams {
+  const int8_t* q_t;
+  int64_t rows, cols;
+  const int32_t* perm;
+  const float* scale;  // s_n [rows], source-row order
+  const float* zero;   // z_n [rows]
+  int half;
+  const float* scaleX;  // [1]
+  const float* zeroX;   // [1]
+  int halfX;
+  double* out;          // [cols]
+};
+hipError_t launch_colvec(const ColvecParams& p, hipStream_t s);
 
 // ---- conv ----------------------------------------------------------------
 struct ConvGeom {

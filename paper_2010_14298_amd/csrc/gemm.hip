@@ -90,8 +90,10 @@ __global__ __launch_bounds__(C::THREADS) void gemm_i8_kernel(GemmParams p) {
           if (row < p.M && col < p.N) out[row * p.N + col] = acc[i][j][r];
         }
   } else if constexpr (EPI == EPI_TENSOR) {
-    const double dA = 1.0 / (double)p.scaleA[0];
-    const double zA = (double)p.zeroA[0] + (double)p.halfA * dA;
+    // with a column vector, A's rows carry their own zero points: their
+    // terms sum_k zeta_k B~[k, col] arrive precomputed per column
+    const double dA = ldexp(1.0 / (double)p.scaleA[0], -p.expA);
+    const double zA = p.colvec ? 0.0 : (double)p.zeroA[0] + (double)p.halfA * dA;
     const double dB = 1.0 / (double)p.scaleB[0];
     const double zB = (double)p.zeroB[0] + (double)p.halfB * dB;
     const double kzz = (double)p.K * zA * zB;
@@ -113,7 +115,10 @@ __global__ __launch_bounds__(C::THREADS) void gemm_i8_kernel(GemmParams p) {
     }
     double cterm[C::JT];
 #pragma unroll
-    for (int j = 0; j < C::JT; ++j) cterm[j] = zA * dB * (double)sb[j];
+    for (int j = 0; j < C::JT; ++j) {
+      const int64_t col = n0 + wn * C::WN + j * 32 + lrow;
+      cterm[j] = p.colvec ? (col < p.N ? p.colvec[col] : 0.0) : zA * dB * (double)sb[j];
+    }
 #pragma unroll
     for (int i = 0; i < C::IT; ++i)
 #pragma unroll
@@ -250,14 +255,52 @@ __global__ void splitk_reduce_kernel(GemmParams p, int64_t* out64, int epi) {
     return;
   }
   const int64_t row = idx / p.N, col = idx % p.N;
-  const double dA = 1.0 / (double)p.scaleA[0];
-  const double zA = (double)p.zeroA[0] + (double)p.halfA * dA;
+  const double dA = ldexp(1.0 / (double)p.scaleA[0], -p.expA);
+  const double zA = p.colvec ? 0.0 : (double)p.zeroA[0] + (double)p.halfA * dA;
   const double dB = 1.0 / (double)p.scaleB[0];
   const double zB = (double)p.zeroB[0] + (double)p.halfB * dB;
-  const double v = dA * dB * (double)sum + dA * zB * (double)p.sumA[row] + zA * dB * (double)p.sumB[col] +
-                   (double)p.K * zA * zB;
+  const double cterm = p.colvec ? p.colvec[col] : zA * dB * (double)p.sumB[col];
+  const double v = dA * dB * (double)sum + dA * zB * (double)p.sumA[row] + cterm + (double)p.K * zA * zB;
   const float f = (float)v;
   p.out[row * p.ldo + col] = (p.relu && !(f > 0.0f)) ? 0.0f : f;
+}
+
+// ---------------------------------------------------------------------------
+// zero-point column vector: one block per output column c, float64
+//   v[c] = sum_n zeta_n (dx q[c, n] + zx),  zeta_n = half / s_row(n) + z_row(n)
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void colvec_kernel(ColvecParams p) {
+  const int64_t c = blockIdx.x;
+  const int8_t* q = p.q_t + c * p.rows;
+  double acc = 0.0, zs = 0.0;
+  for (int64_t n = threadIdx.x; n < p.rows; n += blockDim.x) {
+    const int32_t row = p.perm ? p.perm[n] : (int32_t)n;
+    const double zeta = (double)p.half / (double)p.scale[row] + (double)p.zero[row];
+    acc += zeta * (double)q[n];
+    zs += zeta;
+  }
+  __shared__ double sacc[256], szs[256];
+  sacc[threadIdx.x] = acc;
+  szs[threadIdx.x] = zs;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if (threadIdx.x < w) {
+      sacc[threadIdx.x] += sacc[threadIdx.x + w];
+      szs[threadIdx.x] += szs[threadIdx.x + w];
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    const double dx = 1.0 / (double)p.scaleX[0];
+    const double zx = (double)p.zeroX[0] + (double)p.halfX * dx;
+    p.out[c] = dx * sacc[0] + zx * szs[0];
+  }
+}
+
+hipError_t launch_colvec(const ColvecParams& p, hipStream_t s) {
+  if (p.cols < 1 || p.cols > 0x7FFFFFFF) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(colvec_kernel, dim3((unsigned)p.cols), dim3(256), 0, s, p);
+  return hipGetLastError();
 }
 
 hipError_t launch_splitk_reduce(const GemmParams& p, int64_t* out64, int epi, hipStream_t s) {

@@ -205,7 +205,25 @@ __device__ void finalize_block(const FinalizePlan& fp, int si) {
     const ScaleOut& so = fp.out[o];
     if (so.seg != si) continue;
     const int B = (1 << so.bits) - 1;
-    if (so.per_row) {
+    if (so.per_row == 2) {
+      // per-tensor range R = max_i R_i, step s = B / R; row i takes the
+      // largest e <= E with R_i 2^e <= R (power-of-two scalings are exact)
+      float lmax = 0.0f;
+      for (int64_t row = t; row < g.rows; row += blockDim.x) lmax = fmaxf(lmax, fp.rmax[row] - fp.rmin[row]);
+      const float Rt = block_minmax<NW>(INFINITY, lmax, 0).mx;
+      const float st = scale_from_range(Rt, B);
+      const int E = min(4, 8 - so.bits);
+      if (t == 0) so.tensor_scale[0] = st;
+      for (int64_t row = t; row < g.rows; row += blockDim.x) {
+        const float Ri = fp.rmax[row] - fp.rmin[row];
+        int e = 0;
+        while (e < E && Ri * (float)(2 << e) <= Rt) ++e;
+        const float si = st * (float)(1 << e);
+        so.scale[row] = si > FLT_MAX_F ? FLT_MAX_F : si;
+        so.zero[row] = fp.rmin[row];
+        so.shift[row] = (int8_t)(E - e);
+      }
+    } else if (so.per_row) {
       for (int64_t row = t; row < g.rows; row += blockDim.x) {
         so.scale[row] = scale_from_range(fp.rmax[row] - fp.rmin[row], B);
         so.zero[row] = fp.rmin[row];
@@ -780,7 +798,9 @@ __device__ __forceinline__ uint32_t insert_top(uint32_t w, int32_t v, int b) {
 // TRANS: the primary codes go out transposed ([cols, rows], column sums)
 // instead of in natural order ([rows, cols], row sums).
 // One 64 x 256 tile: column tile bx, slot tile by.
-template <int MODE, int K, bool HAS2, bool VEC, bool TRANS>
+// H2: the second (transposed, stochastic) quantizer of the same rows, Q_b1:
+// 0 none, 1 per tensor, 2 per row with power-of-two shifted codes.
+template <int MODE, int K, int H2, bool VEC, bool TRANS>
 __device__ __forceinline__ void quant_tile(const QuantParams& p, int64_t bx, int64_t by) {
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform: slot bookkeeping stays scalar
@@ -889,9 +909,11 @@ __device__ __forceinline__ void quant_tile(const QuantParams& p, int64_t bx, int
   const float z_t = (MODE == QM_TENSOR) ? p.zero[0] : 0.0f;
   float Bf2 = 0.0f, s2 = 0.0f, z2 = 0.0f;
   uint32_t hoff2 = 0u;
-  if constexpr (HAS2) {
+  if constexpr (H2 != 0) {
     Bf2 = (float)((1 << p.bits2) - 1);
     hoff2 = (uint32_t)(1 << (p.bits2 - 1)) << 24;
+  }
+  if constexpr (H2 == 1) {
     s2 = p.scale2[0];
     z2 = p.zero2[0];
   }
@@ -958,19 +980,39 @@ __device__ __forceinline__ void quant_tile(const QuantParams& p, int64_t bx, int
     const uint64_t e0 = (uint64_t)srow[r] * (uint64_t)cols + (uint64_t)c0;
     int32_t t[4];
     // with a second quantizer the first is stochastic too (launch_quant checks)
-    if (HAS2 || p.stoch)
+    if (H2 != 0 || p.stoch)
       sr4<VEC>(y, e0, p.seed, p.stream, Bf, hoff, t);
     else
       rne4(y, Bf, hoff, t);
-    if constexpr (HAS2) {
+    if constexpr (MODE == QM_ROW) {
+      if (p.shift && ok) {
+        const int sh = p.shift[slot];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) t[j] = shift_top(t[j], sh);
+      }
+    }
+    if constexpr (H2 != 0) {
       // Q_b1 of the same row: always stochastic, its own Philox stream (the
       // counter and key are shared, so the compiler shares the first two
       // rounds' products with the call above)
+      float s2r = s2, z2r = z2;
+      int sh2 = 0;
+      if constexpr (H2 == 2) {
+        if (ok) {
+          s2r = p.scale2[srow[r]];
+          z2r = p.zero2[srow[r]];
+          sh2 = p.shift2[srow[r]];
+        }
+      }
       float y2[4];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) y2[j] = s2 * (g[r][j] - z2);
+      for (int j = 0; j < 4; ++j) y2[j] = s2r * (g[r][j] - z2r);
       int32_t t2[4];
       sr4<VEC>(y2, e0, p.seed, p.stream2, Bf2, hoff2, t2);
+      if constexpr (H2 == 2) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) t2[j] = shift_top(t2[j], sh2);
+      }
       if (ok) {
 #pragma unroll
         for (int j = 0; j < 4; ++j) tq2[j][r >> 2] = insert_top(tq2[j][r >> 2], t2[j], r & 3);
@@ -1017,7 +1059,7 @@ __device__ __forceinline__ void quant_tile(const QuantParams& p, int64_t bx, int
           if (slot0 + r < rows) dst[r] = (int8_t)((tq[j][r >> 2] >> (8 * (r & 3))) & 255);
       }
     }
-    if constexpr (HAS2) {
+    if constexpr (H2 != 0) {
       int8_t* dst = p.q2_t + col * rows + slot0;
       if (tvec) {
         *reinterpret_cast<uint4*>(dst) = make_uint4(tq2[j][0], tq2[j][1], tq2[j][2], tq2[j][3]);
@@ -1030,14 +1072,14 @@ __device__ __forceinline__ void quant_tile(const QuantParams& p, int64_t bx, int
   }
 
   // ---- column sums of the transposed outputs: reduce the 4 waves in LDS
-  if ((TRANS && p.sum_t) || (HAS2 && p.sum2_t)) {
+  if ((TRANS && p.sum_t) || (H2 != 0 && p.sum2_t)) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       int32_t cs = 0, cs2 = 0;
 #pragma unroll
       for (int w = 0; w < 4; ++w) {
         if constexpr (TRANS) cs = sum4_i8(tq[j][w], cs);
-        if constexpr (HAS2) cs2 = sum4_i8(tq2[j][w], cs2);
+        if constexpr (H2 != 0) cs2 = sum4_i8(tq2[j][w], cs2);
       }
       s_csum[0][wave][lane * 4 + j] = cs;
       s_csum[1][wave][lane * 4 + j] = cs2;
@@ -1050,7 +1092,7 @@ __device__ __forceinline__ void quant_tile(const QuantParams& p, int64_t bx, int
         const int t = s_csum[0][0][c] + s_csum[0][1][c] + s_csum[0][2][c] + s_csum[0][3][c];
         atomicAdd(p.sum_t + col, t);
       }
-      if (HAS2 && p.sum2_t) {
+      if (H2 != 0 && p.sum2_t) {
         const int t = s_csum[1][0][c] + s_csum[1][1][c] + s_csum[1][2][c] + s_csum[1][3][c];
         atomicAdd(p.sum2_t + col, t);
       }
@@ -1059,9 +1101,9 @@ __device__ __forceinline__ void quant_tile(const QuantParams& p, int64_t bx, int
 }
 
 
-template <int MODE, int K, bool HAS2, bool VEC, bool TRANS>
+template <int MODE, int K, int H2, bool VEC, bool TRANS>
 __global__ __launch_bounds__(256) void quant_tile_kernel(QuantParams p) {
-  quant_tile<MODE, K, HAS2, VEC, TRANS>(p, blockIdx.x, blockIdx.y);
+  quant_tile<MODE, K, H2, VEC, TRANS>(p, blockIdx.x, blockIdx.y);
 }
 
 // Two independent per-tensor transposed quantizations in one launch (Q_f(X)
@@ -1072,9 +1114,9 @@ __global__ __launch_bounds__(256) void quant_tile2_kernel(QuantParams p0, QuantP
                                                           int64_t ct1) {
   const int64_t b = blockIdx.x;
   if (b < nb0)
-    quant_tile<QM_TENSOR, 0, false, VEC, true>(p0, b % ct0, b / ct0);
+    quant_tile<QM_TENSOR, 0, 0, VEC, true>(p0, b % ct0, b / ct0);
   else
-    quant_tile<QM_TENSOR, 0, false, VEC, true>(p1, (b - nb0) % ct1, (b - nb0) / ct1);
+    quant_tile<QM_TENSOR, 0, 0, VEC, true>(p1, (b - nb0) % ct1, (b - nb0) / ct1);
 }
 
 // The gradient pass (natural codes plus the transposed Q_b1) and the two
@@ -1082,7 +1124,7 @@ __global__ __launch_bounds__(256) void quant_tile2_kernel(QuantParams p0, QuantP
 // period-th block (while they last) is an X / W tile, so that those
 // memory-light tiles interleave with the arithmetic-heavy gradient tiles;
 // the other blocks take the gradient tiles in order.
-template <int MODE, int K>
+template <int MODE, int K, int H2>
 __global__ __launch_bounds__(256) void quant_fused_kernel(QuantParams pg, QuantParams px, QuantParams pw, int64_t nbx,
                                                           int64_t nbw, int64_t period, int64_t ctg, int64_t ctx,
                                                           int64_t ctw) {
@@ -1091,13 +1133,13 @@ __global__ __launch_bounds__(256) void quant_fused_kernel(QuantParams pg, QuantP
   if (b % period == period - 1 && b / period < nxw) {
     const int64_t t = b / period;
     if (t < nbx)
-      quant_tile<QM_TENSOR, 0, false, true, true>(px, t % ctx, t / ctx);
+      quant_tile<QM_TENSOR, 0, 0, true, true>(px, t % ctx, t / ctx);
     else
-      quant_tile<QM_TENSOR, 0, false, true, true>(pw, (t - nbx) % ctw, (t - nbx) / ctw);
+      quant_tile<QM_TENSOR, 0, 0, true, true>(pw, (t - nbx) % ctw, (t - nbx) / ctw);
   } else {
     const int64_t before = (b + 1) / period < nxw ? (b + 1) / period : nxw;
     const int64_t t = b - before;
-    quant_tile<MODE, K, true, true, false>(pg, t % ctg, t / ctg);
+    quant_tile<MODE, K, H2, true, false>(pg, t % ctg, t / ctg);
   }
 }
 
@@ -1111,8 +1153,12 @@ static hipError_t launch_quant_fused_k(const QuantParams& pg, const QuantParams&
   const int64_t nb = nbg + nbx + nbw;
   if (nb > 0x7FFFFFFF) return hipErrorInvalidValue;
   const int64_t period = nb / (nbx + nbw);
-  hipLaunchKernelGGL((quant_fused_kernel<MODE, K>), dim3((unsigned)nb), dim3(256), 0, s, pg, px, pw, nbx, nbw, period,
-                     ctg, ctx, ctw);
+  if (pg.shift2)
+    hipLaunchKernelGGL((quant_fused_kernel<MODE, K, 2>), dim3((unsigned)nb), dim3(256), 0, s, pg, px, pw, nbx, nbw,
+                       period, ctg, ctx, ctw);
+  else
+    hipLaunchKernelGGL((quant_fused_kernel<MODE, K, 1>), dim3((unsigned)nb), dim3(256), 0, s, pg, px, pw, nbx, nbw,
+                       period, ctg, ctx, ctw);
   return hipGetLastError();
 }
 
@@ -1126,22 +1172,29 @@ static hipError_t launch_quant_k(const QuantParams& p, hipStream_t s) {
   // one primary layout: natural (with an optional transposed Q_b1) or transposed
   if ((p.q_nat || p.sum_nat) && (p.q_t || p.sum_t)) return hipErrorInvalidValue;
   const bool trans = p.q_t || p.sum_t;
+  if (p.shift && MODE != QM_ROW) return hipErrorInvalidValue;
   if (p.q2_t) {
     if (trans || !p.stoch) return hipErrorInvalidValue;
-    if (vec)
-      hipLaunchKernelGGL((quant_tile_kernel<MODE, K, true, true, false>), grid, dim3(256), 0, s, p);
-    else
-      hipLaunchKernelGGL((quant_tile_kernel<MODE, K, true, false, false>), grid, dim3(256), 0, s, p);
+    if (p.shift2) {
+      if (vec)
+        hipLaunchKernelGGL((quant_tile_kernel<MODE, K, 2, true, false>), grid, dim3(256), 0, s, p);
+      else
+        hipLaunchKernelGGL((quant_tile_kernel<MODE, K, 2, false, false>), grid, dim3(256), 0, s, p);
+    } else if (vec) {
+      hipLaunchKernelGGL((quant_tile_kernel<MODE, K, 1, true, false>), grid, dim3(256), 0, s, p);
+    } else {
+      hipLaunchKernelGGL((quant_tile_kernel<MODE, K, 1, false, false>), grid, dim3(256), 0, s, p);
+    }
   } else if (trans) {
     if (vec)
-      hipLaunchKernelGGL((quant_tile_kernel<MODE, K, false, true, true>), grid, dim3(256), 0, s, p);
+      hipLaunchKernelGGL((quant_tile_kernel<MODE, K, 0, true, true>), grid, dim3(256), 0, s, p);
     else
-      hipLaunchKernelGGL((quant_tile_kernel<MODE, K, false, false, true>), grid, dim3(256), 0, s, p);
+      hipLaunchKernelGGL((quant_tile_kernel<MODE, K, 0, false, true>), grid, dim3(256), 0, s, p);
   } else {
     if (vec)
-      hipLaunchKernelGGL((quant_tile_kernel<MODE, K, false, true, false>), grid, dim3(256), 0, s, p);
+      hipLaunchKernelGGL((quant_tile_kernel<MODE, K, 0, true, false>), grid, dim3(256), 0, s, p);
     else
-      hipLaunchKernelGGL((quant_tile_kernel<MODE, K, false, false, false>), grid, dim3(256), 0, s, p);
+      hipLaunchKernelGGL((quant_tile_kernel<MODE, K, 0, false, false>), grid, dim3(256), 0, s, p);
   }
   return hipGetLastError();
 }

@@ -14,8 +14,8 @@ import torch
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libfqt.so")
 
-FQT_PTQ, FQT_PSQ, FQT_BHQ = 0, 1, 2
-KINDS = {"ptq": FQT_PTQ, "psq": FQT_PSQ, "bhq": FQT_BHQ}
+FQT_PTQ, FQT_PSQ, FQT_BHQ, FQT_SHIFT = 0, 1, 2, 3
+KINDS = {"ptq": FQT_PTQ, "psq": FQT_PSQ, "bhq": FQT_BHQ, "shift": FQT_SHIFT}
 STATUS = {0: "FQT_OK", 1: "FQT_EINVAL", 2: "FQT_EUNSUPPORTED", 3: "FQT_ENONFINITE", 4: "FQT_EWORKSPACE",
           5: "FQT_EDEVICE"}
 
@@ -28,7 +28,8 @@ class FqtError(RuntimeError):
 
 class QTensor(ctypes.Structure):
     _fields_ = [("q", ctypes.c_void_p), ("scale", ctypes.c_void_p), ("zero", ctypes.c_void_p),
-                ("perm", ctypes.c_void_p), ("group_off", ctypes.c_void_p), ("code_sum", ctypes.c_void_p)]
+                ("perm", ctypes.c_void_p), ("group_off", ctypes.c_void_p), ("code_sum", ctypes.c_void_p),
+                ("shift", ctypes.c_void_p)]
 
 
 class QSpec(ctypes.Structure):
@@ -54,7 +55,7 @@ class ConvShape(ctypes.Structure):
 
 
 EXPORTS = [
-    "fqt_quantize_ptq", "fqt_quantize_psq", "fqt_quantize_bhq", "fqt_quantize_workspace",
+    "fqt_quantize_ptq", "fqt_quantize_psq", "fqt_quantize_bhq", "fqt_quantize_shift", "fqt_quantize_workspace",
     "fqt_bhq_adaptive_block", "fqt_bhq_adaptive_workspace",
     "fqt_linear_backward", "fqt_linear_backward_workspace",
     "fqt_linear_forward", "fqt_linear_forward_workspace",
@@ -83,6 +84,7 @@ def load(path=LIB_PATH):
         "fqt_quantize_ptq": ([vp, i64, i64, i32, i32, u64, u32, i32, qtp, vp, sz, vp], i32),
         "fqt_quantize_psq": ([vp, i64, i64, i32, u64, u32, qtp, vp, sz, vp], i32),
         "fqt_quantize_bhq": ([vp, i64, i64, i32, i32, u64, u32, qtp, vp, sz, vp], i32),
+        "fqt_quantize_shift": ([vp, i64, i64, i32, u64, u32, i32, qtp, vp, sz, vp], i32),
         "fqt_quantize_workspace": ([i32, i64, i64, i32], sz),
         "fqt_bhq_adaptive_block": ([vp, i64, i64, i32, ctypes.POINTER(ctypes.c_int), vp, sz, vp], i32),
         "fqt_bhq_adaptive_workspace": ([i64, i64], sz),
@@ -154,12 +156,15 @@ def _quant_outputs(x, rows, cols, kind, transpose, code_sum):
     if kind == "bhq":
         out["perm"] = torch.empty(rows, dtype=torch.int32, device=dev)
         out["group_off"] = torch.empty(rows + 1, dtype=torch.int32, device=dev)
+    if kind == "shift":
+        out["shift"] = torch.empty(rows, dtype=torch.int8, device=dev)
     if code_sum:
         out["code_sum"] = torch.empty(cols if transpose else rows, dtype=torch.int32, device=dev)
     qt = QTensor(out["q"].data_ptr(), out["scale"].data_ptr(), out["zero"].data_ptr(),
                  out["perm"].data_ptr() if "perm" in out else 0,
                  out["group_off"].data_ptr() if "group_off" in out else 0,
-                 out["code_sum"].data_ptr() if "code_sum" in out else 0)
+                 out["code_sum"].data_ptr() if "code_sum" in out else 0,
+                 out["shift"].data_ptr() if "shift" in out else 0)
     return out, qt
 
 
@@ -172,6 +177,19 @@ def fqt_quantize_ptq(x, bits, stochastic, seed=0, stream=0, transpose=False, cod
     rc = load().fqt_quantize_ptq(_ptr(x), rows, cols, bits, int(bool(stochastic)), seed, stream,
                                  int(bool(transpose)), ctypes.byref(qt), _ptr(ws), ws.numel(), _stream())
     _check("fqt_quantize_ptq", rc)
+    out["ws"] = ws
+    return out
+
+
+def fqt_quantize_shift(x, bits, seed=0, stream=0, transpose=False, code_sum=False, ws=None):
+    x = _f32(x, "x")
+    rows, cols = x.shape
+    out, qt = _quant_outputs(x, rows, cols, "shift", transpose, code_sum)
+    if ws is None:
+        ws = _workspace(fqt_quantize_workspace("shift", rows, cols), x.device)
+    rc = load().fqt_quantize_shift(_ptr(x), rows, cols, bits, seed, stream, int(bool(transpose)), ctypes.byref(qt),
+                                   _ptr(ws), ws.numel(), _stream())
+    _check("fqt_quantize_shift", rc)
     out["ws"] = ws
     return out
 
