@@ -50,9 +50,9 @@ def parse():
 TRAFFIC_FILE = os.path.join(os.path.dirname(os.path.abspath(__file__)), "profiles", "traffic_linear_ffn_bhq5.txt")
 # kernel of each phase in the rocprofv3 summaries (name prefixes)
 PHASE_KERNEL = {
-    "quant_G": ("quant_fused_kernel<2, 64>",),
-    "gemm_gradX": ("gemm_i8_kernel", ", 3, 64, true>"),
-    "gemm_gradW": ("gemm_i8_kernel", ", 1, 0, true>"),
+    "quant_G": ("quant_fused_kernel<2, 64, 1>",),
+    "gemm_gradX": ("gemm_i8_kernel<fqt::TileCfg<256", ", 3, 64, true>"),
+    "gemm_gradW": ("gemm_i8_kernel<fqt::TileCfg<128", ", 1, 0, true>"),
 }
 
 
@@ -128,6 +128,31 @@ def chain_bench(args, fqt, synth, torch):
             "forward_TOPS": round(layer_ops / (f_ms * 1e-3) / 1e12, 2),
             "backward_TOPS": round(2.0 * layer_ops / (b_ms * 1e-3) / 1e12, 2),
             "TOPS": round(3.0 * layer_ops / ((f_ms + b_ms) * 1e-3) / 1e12, 2)}
+
+
+def shift_bench(args, fqt, torch, dX, dW, dG):
+    """The same layer backward with a low-bit grad_W quantizer carrying
+    per-sample power-of-two scales (Q_b1 = shift 4-bit), HIP events."""
+    import numpy as np
+    qb_w = ("shift", 4, 0)
+    cfg = fqt.cfg_struct(QB_X, qb_w, 8, 8, 0)
+    ws = torch.empty(fqt.fqt_linear_backward_workspace(N, D_IN, D_OUT, cfg), dtype=torch.uint8, device="cuda")
+    gW = torch.empty((D_OUT, D_IN), dtype=torch.float32, device="cuda")
+    gX = torch.empty((N, D_IN), dtype=torch.float32, device="cuda")
+    steps = max(1, args.steps // 4)
+    for i in range(max(1, args.warmup // 4)):
+        fqt.fqt_linear_backward(dX, dW, dG, qb_x=QB_X, qb_w=qb_w, seed=i, grad_W=gW, grad_X=gX, ws=ws)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for i in range(steps):
+        fqt.fqt_linear_backward(dX, dW, dG, qb_x=QB_X, qb_w=qb_w, seed=i, grad_W=gW, grad_X=gX, ws=ws)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    return {"workload": "the same layer backward, Q_b1 = per-tensor range with per-sample power-of-two "
+                        "steps, 4-bit (shifted codes, E = 4)", "steps": steps, "ms_per_step": round(ms, 4),
+            "TOPS": round(2.0 * 2.0 * N * D_IN * D_OUT / (ms * 1e-3) / 1e12, 2)}
 
 
 def main():
@@ -231,6 +256,7 @@ def main():
     }
     if not args.no_chain:
         out["chain"] = chain_bench(args, fqt, synth, torch)
+        out["shift_gradW"] = shift_bench(args, fqt, torch, dX, dW, dG)
     if args.copy_probe:
         # a plain elementwise pass: reads 256 MiB, writes 256 MiB
         src = torch.ones(64 * 1024 * 1024, dtype=torch.float32, device="cuda")

@@ -203,9 +203,11 @@ struct LinearWs {
   void* adaptive;
   int32_t* part;
   int splits;
-  int8_t* shift1;    // Q_b1 = FQT_SHIFT: per-row shifts, step scale, zero-point column vector
+  int8_t* shift1;    // Q_b1 = FQT_SHIFT: per-row shifts, step scale, zero-point terms and column vector
   float* tscale1;
+  double* zeta1;
   double* colvec;
+  double* colvec_part;
 };
 
 int linear_splits(int64_t N) { return (int)((N + MAX_K_CHUNK - 1) / MAX_K_CHUNK); }
@@ -241,7 +243,9 @@ LinearWs carve_linear(Carver& c, const float* X, const float* W, const float* G,
   if (shift) {
     w.shift1 = c.take<int8_t>(N);
     w.tscale1 = c.take<float>(1);
+    w.zeta1 = c.take<double>(N);
     w.colvec = c.take<double>(d_in);
+    w.colvec_part = c.take<double>(colvec_splits(N) * (d_in + 1));
   }
   w.sg2 = c.take<float>(N);
   w.zg2 = c.take<float>(N);
@@ -518,7 +522,7 @@ fqt_status fqt_linear_backward(const float* X, const float* W, const float* G, i
   fp.out[0] = ScaleOut{0, cfg->f_bits, 0, w.sx, w.zx};
   fp.out[1] = ScaleOut{1, cfg->theta_bits, 0, w.sw, w.zw};
   const bool shift1 = cfg->qb_w.kind == FQT_SHIFT;
-  fp.out[2] = ScaleOut{2, cfg->qb_w.bits, shift1 ? 2 : 0, w.sg1, w.zg1, w.shift1, w.tscale1};
+  fp.out[2] = ScaleOut{2, cfg->qb_w.bits, shift1 ? 2 : 0, w.sg1, w.zg1, w.shift1, w.tscale1, w.zeta1};
   fp.nout = 3;
   if (qx.kind != FQT_BHQ) fp.out[fp.nout++] = ScaleOut{2, qx.bits, qx.kind == FQT_PSQ ? 1 : 0, w.sg2, w.zg2};
   add_zero(fp, w.sum_x, d_in);
@@ -603,12 +607,11 @@ fqt_status fqt_linear_backward(const float* X, const float* W, const float* G, i
     cv.rows = N;
     cv.cols = d_in;
     cv.perm = w.perm;
-    cv.scale = w.sg1;
-    cv.zero = w.zg1;
-    cv.half = 1 << (cfg->qb_w.bits - 1);
+    cv.zeta = w.zeta1;
     cv.scaleX = w.sx;
     cv.zeroX = w.zx;
     cv.halfX = 1 << (cfg->f_bits - 1);
+    cv.part = w.colvec_part;
     cv.out = w.colvec;
     FQT_TRY(launch_colvec(cv, s));
   }

@@ -56,6 +56,7 @@ struct ScaleOut {
   float* zero;
   int8_t* shift;
   float* tensor_scale;
+  double* zeta;  // per_row == 2, optional: [rows] half / s_i + z_i (float64), the rows' zero-point terms
 };
 struct FinalizePlan {
   StatsSeg seg[3];
@@ -224,21 +225,21 @@ hipError_t launch_gemm(const GemmParams& p, int epi, hipStream_t s);
 hipError_t launch_splitk_reduce(const GemmParams& p, int64_t* out64, int epi, hipStream_t s);
 
 // Zero-point term of a contraction over samples whose A rows (samples) carry
-// their own zero points: v[c] = sum_n zeta_n Xt[n, c], zeta_n = half / s_n +
-// z_n, Xt[n, c] = dx q[c, slot(n)] + zx (q: [cols, rows] transposed codes in
-// slot order, perm slot -> row or nullptr), float64.
+// their own zero points: v[c] = sum_n zeta_n Xt[n, c] (zeta_n = half / s_n +
+// z_n from the finalize), Xt[n, c] = dx q[c, n] + zx (q: [cols, rows]
+// transposed codes in slot order, perm slot -> row or nullptr), float64.
 struct ColvecParams {
   const int8_t* q_t;
   int64_t rows, cols;
   const int32_t* perm;
-  const float* scale;  // s_n [rows], source-row order
-  const float* zero;   // z_n [rows]
-  int half;
+  const double* zeta;   // zeta_n [rows], source-row order
   const float* scaleX;  // [1]
   const float* zeroX;   // [1]
   int halfX;
+  double* part;         // scratch [colvec_splits(rows)][cols + 1]
   double* out;          // [cols]
 };
+int64_t colvec_splits(int64_t rows);
 hipError_t launch_colvec(const ColvecParams& p, hipStream_t s);
 
 // ---- conv ----------------------------------------------------------------

@@ -266,40 +266,89 @@ __global__ void splitk_reduce_kernel(GemmParams p, int64_t* out64, int epi) {
 }
 
 // ---------------------------------------------------------------------------
-// zero-point column vector: one block per output column c, float64
-//   v[c] = sum_n zeta_n (dx q[c, n] + zx),  zeta_n = half / s_row(n) + z_row(n)
+// zero-point column vector, float64: v[c] = sum_n zeta_row(n) (dx q[c, n] + zx),
+// in two deterministic launches.  Partials: block (x, y) takes COLVEC_C
+// columns (COLVEC_C / 4 per wave) and samples [y COLVEC_N, (y + 1) COLVEC_N),
+// 16 consecutive per lane (one 16-byte load per column row); the wave sums
+// its lanes and stores part[y][c] (and the zeta sum in part[y][cols], from
+// x = 0).  The reduce adds the partials of each column in order of y.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void colvec_kernel(ColvecParams p) {
-  const int64_t c = blockIdx.x;
-  const int8_t* q = p.q_t + c * p.rows;
-  double acc = 0.0, zs = 0.0;
-  for (int64_t n = threadIdx.x; n < p.rows; n += blockDim.x) {
-    const int32_t row = p.perm ? p.perm[n] : (int32_t)n;
-    const double zeta = (double)p.half / (double)p.scale[row] + (double)p.zero[row];
-    acc += zeta * (double)q[n];
-    zs += zeta;
+constexpr int COLVEC_C = 64;
+constexpr int COLVEC_N = 1024;
+
+__device__ __forceinline__ double wave_sum_f64(double v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+__global__ __launch_bounds__(256) void colvec_partial_kernel(ColvecParams p) {
+  constexpr int CW = COLVEC_C / 4;  // columns per wave
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int64_t cw = (int64_t)blockIdx.x * COLVEC_C + wave * CW;
+  const int64_t n0 = (int64_t)blockIdx.y * COLVEC_N + 16 * lane;
+  const bool full = n0 + 16 <= p.rows && (p.rows & 15) == 0;
+  double z[16], zs = 0.0;
+#pragma unroll
+  for (int k = 0; k < 16; ++k) {
+    const int64_t n = n0 + k;
+    z[k] = n < p.rows ? p.zeta[p.perm ? p.perm[n] : (int32_t)n] : 0.0;
+    zs += z[k];
   }
-  __shared__ double sacc[256], szs[256];
-  sacc[threadIdx.x] = acc;
-  szs[threadIdx.x] = zs;
-  __syncthreads();
-  for (int w = 128; w > 0; w >>= 1) {
-    if (threadIdx.x < w) {
-      sacc[threadIdx.x] += sacc[threadIdx.x + w];
-      szs[threadIdx.x] += szs[threadIdx.x + w];
+  double* part = p.part + (int64_t)blockIdx.y * (p.cols + 1);
+  // every column's 16 codes first (independent loads in flight together)
+  uint4 v[CW];
+#pragma unroll
+  for (int c = 0; c < CW; ++c) {
+    const int64_t col = cw + c;
+    const int8_t* q = p.q_t + col * p.rows + n0;
+    if (col >= p.cols) {
+      v[c] = make_uint4(0u, 0u, 0u, 0u);
+    } else if (full) {
+      v[c] = *reinterpret_cast<const uint4*>(q);
+    } else {
+      uint32_t w[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+      for (int k = 0; k < 16; ++k)
+        if (n0 + k < p.rows) w[k >> 2] |= (uint32_t)(uint8_t)q[k] << (8 * (k & 3));
+      v[c] = make_uint4(w[0], w[1], w[2], w[3]);
     }
-    __syncthreads();
   }
-  if (threadIdx.x == 0) {
-    const double dx = 1.0 / (double)p.scaleX[0];
-    const double zx = (double)p.zeroX[0] + (double)p.halfX * dx;
-    p.out[c] = dx * sacc[0] + zx * szs[0];
+#pragma unroll
+  for (int c = 0; c < CW; ++c) {
+    const uint32_t w[4] = {v[c].x, v[c].y, v[c].z, v[c].w};
+    double acc = 0.0;
+#pragma unroll
+    for (int k = 0; k < 16; ++k) acc += z[k] * (double)(int8_t)((w[k >> 2] >> (8 * (k & 3))) & 255u);
+    acc = wave_sum_f64(acc);
+    if (lane == 0 && cw + c < p.cols) part[cw + c] = acc;
+  }
+  if (blockIdx.x == 0 && wave == 0) {
+    zs = wave_sum_f64(zs);
+    if (lane == 0) part[p.cols] = zs;
   }
 }
 
+__global__ __launch_bounds__(256) void colvec_reduce_kernel(ColvecParams p, int64_t nsplit) {
+  const int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (c >= p.cols) return;
+  double a = 0.0, zs = 0.0;
+  for (int64_t y = 0; y < nsplit; ++y) {
+    a += p.part[y * (p.cols + 1) + c];
+    zs += p.part[y * (p.cols + 1) + p.cols];
+  }
+  const double dx = 1.0 / (double)p.scaleX[0];
+  const double zx = (double)p.zeroX[0] + (double)p.halfX * dx;
+  p.out[c] = dx * a + zx * zs;
+}
+
+int64_t colvec_splits(int64_t rows) { return (rows + COLVEC_N - 1) / COLVEC_N; }
+
 hipError_t launch_colvec(const ColvecParams& p, hipStream_t s) {
-  if (p.cols < 1 || p.cols > 0x7FFFFFFF) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(colvec_kernel, dim3((unsigned)p.cols), dim3(256), 0, s, p);
+  const int64_t cb = (p.cols + COLVEC_C - 1) / COLVEC_C, ns = colvec_splits(p.rows);
+  if (p.cols < 1 || p.rows < 1 || cb > 0x7FFFFFFF || ns > 65535) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(colvec_partial_kernel, dim3((unsigned)cb, (unsigned)ns), dim3(256), 0, s, p);
+  hipLaunchKernelGGL(colvec_reduce_kernel, dim3((unsigned)((p.cols + 255) / 256)), dim3(256), 0, s, p, ns);
   return hipGetLastError();
 }
 

@@ -208,20 +208,38 @@ __device__ void finalize_block(const FinalizePlan& fp, int si) {
     if (so.per_row == 2) {
       // per-tensor range R = max_i R_i, step s = B / R; row i takes the
       // largest e <= E with R_i 2^e <= R (power-of-two scalings are exact)
+      const float* __restrict__ rmn = fp.rmin;
+      const float* __restrict__ rmx = fp.rmax;
       float lmax = 0.0f;
-      for (int64_t row = t; row < g.rows; row += blockDim.x) lmax = fmaxf(lmax, fp.rmax[row] - fp.rmin[row]);
+#pragma unroll 8
+      for (int64_t row = t; row < g.rows; row += blockDim.x) lmax = fmaxf(lmax, rmx[row] - rmn[row]);
       const float Rt = block_minmax<NW>(INFINITY, lmax, 0).mx;
       const float st = scale_from_range(Rt, B);
       const int E = min(4, 8 - so.bits);
+      const double half = (double)(1 << (so.bits - 1));
       if (t == 0) so.tensor_scale[0] = st;
-      for (int64_t row = t; row < g.rows; row += blockDim.x) {
-        const float Ri = fp.rmax[row] - fp.rmin[row];
-        int e = 0;
-        while (e < E && Ri * (float)(2 << e) <= Rt) ++e;
-        const float si = st * (float)(1 << e);
-        so.scale[row] = si > FLT_MAX_F ? FLT_MAX_F : si;
-        so.zero[row] = fp.rmin[row];
-        so.shift[row] = (int8_t)(E - e);
+      // rows in batches of 4 per thread: loads first, then the stores
+      for (int64_t r0 = t; r0 < g.rows; r0 += 4 * (int64_t)blockDim.x) {
+        float lo[4], Ri[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const int64_t row = r0 + k * (int64_t)blockDim.x;
+          lo[k] = row < g.rows ? rmn[row] : 0.0f;
+          Ri[k] = row < g.rows ? rmx[row] - lo[k] : 0.0f;
+        }
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const int64_t row = r0 + k * (int64_t)blockDim.x;
+          if (row >= g.rows) break;
+          int e = 0;
+          while (e < E && Ri[k] * (float)(2 << e) <= Rt) ++e;
+          float si = st * (float)(1 << e);
+          si = si > FLT_MAX_F ? FLT_MAX_F : si;
+          so.scale[row] = si;
+          so.zero[row] = lo[k];
+          so.shift[row] = (int8_t)(E - e);
+          if (so.zeta) so.zeta[row] = half / (double)si + (double)lo[k];
+        }
       }
     } else if (so.per_row) {
       for (int64_t row = t; row < g.rows; row += blockDim.x) {
