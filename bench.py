@@ -155,6 +155,36 @@ def shift_bench(args, fqt, torch, dX, dW, dG):
             "TOPS": round(2.0 * 2.0 * N * D_IN * D_OUT / (ms * 1e-3) / 1e12, 2)}
 
 
+def bf6_bench(args, fqt, torch):
+    """Exact contraction of 4-bit codes: 6-bit float matrix cores (e3m2
+    operands, packed in the call) against the int8 matrix cores, on the two
+    contraction shapes of the layer; each call ends in int64 accumulators."""
+    res = {}
+    gen = torch.Generator(device="cuda").manual_seed(0)
+    for name, (M, Nn, K) in {"gradX_shape": (N, D_IN, D_OUT), "gradW_shape": (D_OUT, D_IN, N)}.items():
+        A = torch.randint(-8, 8, (M, K), dtype=torch.int8, device="cuda", generator=gen)
+        B = torch.randint(-8, 8, (Nn, K), dtype=torch.int8, device="cuda", generator=gen)
+        C = torch.empty((M, Nn), dtype=torch.int64, device="cuda")
+        ws6 = torch.empty(fqt.fqt_gemm_s4s4_bf6_workspace(M, Nn, K), dtype=torch.uint8, device="cuda")
+        ws8 = torch.empty(fqt.fqt_gemm_workspace(M, Nn, K), dtype=torch.uint8, device="cuda")
+        calls = {"bf6": lambda: fqt.fqt_gemm_s4s4_bf6(A, B, ws=ws6, C=C),
+                 "int8": lambda: fqt.fqt_gemm_s8s8_s64(A, B, ws=ws8)}
+        row = {"M": M, "N": Nn, "K": K}
+        for key, fn in calls.items():
+            for _ in range(3):
+                fn()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            reps = max(2, args.steps // 10)
+            e0.record()
+            for _ in range(reps):
+                fn()
+            e1.record()
+            torch.cuda.synchronize()
+            row[key + "_call_ms"] = round(e0.elapsed_time(e1) / reps, 4)
+        res[name] = row
+    return res
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -257,6 +287,7 @@ def main():
     if not args.no_chain:
         out["chain"] = chain_bench(args, fqt, synth, torch)
         out["shift_gradW"] = shift_bench(args, fqt, torch, dX, dW, dG)
+        out["sub8bit_mfma"] = bf6_bench(args, fqt, torch)
     if args.copy_probe:
         # a plain elementwise pass: reads 256 MiB, writes 256 MiB
         src = torch.ones(64 * 1024 * 1024, dtype=torch.float32, device="cuda")

@@ -242,6 +242,18 @@ fqt_status fqt_gemm_s8s8_s64(const int8_t* A, const int8_t* B, int64_t M, int64_
 
 size_t fqt_gemm_workspace(int64_t M, int64_t N, int64_t K);
 
+/* The same exact contraction for 4-bit offset codes (A, B int8 in [-8, 7]) on
+ * the 6-bit float matrix cores: both operands are repacked as e3m2 (every
+ * integer in [-8, 8] is one) into the workspace and contracted with float32
+ * accumulation, which stays exact for K chunks of at most 131072 (|sum| <
+ * 2^24); chunks are summed in int64 into C [M, N].  A code outside [-8, 7]
+ * is a data error: the workspace status reports FQT_ENONFINITE.  Sub-8-bit
+ * matrix formats for small codes (the storage and contraction of b <= 4-bit
+ * codes; Sec. 3.3 codes are integers in [0, 2^b - 1]).                     */
+fqt_status fqt_gemm_s4s4_bf6(const int8_t* A, const int8_t* B, int64_t M, int64_t N, int64_t K, int64_t lda,
+                             int64_t ldb, int64_t* C, void* ws, size_t ws_bytes, fqt_stream_t s);
+size_t fqt_gemm_s4s4_bf6_workspace(int64_t M, int64_t N, int64_t K);
+
 /* Waits for `s`, then reports the data status recorded in `ws` by the last
  * call that used it: FQT_OK or FQT_ENONFINITE (FQT_EDEVICE if the wait or
  * copy fails).                                                              */

@@ -804,6 +804,68 @@ fqt_status fqt_gemm_s8s8_s64(const int8_t* A, const int8_t* B, int64_t M, int64_
   return FQT_OK;
 }
 
+// 4-bit codes on the 6-bit float matrix cores: packed operands, exact chunks
+constexpr int64_t BF6_K_CHUNK = 131072;  // 64 * K < 2^24 keeps float32 sums exact
+
+struct Bf6Ws {
+  Header h;
+  int8_t *a6, *b6;
+  int32_t* part;
+  int64_t Kpad, splits;
+};
+
+Bf6Ws carve_bf6(Carver& c, int64_t M, int64_t N, int64_t K) {
+  Bf6Ws w{};
+  w.h = take_header(c);
+  const int64_t rb = bf6_row_bytes(K);
+  w.Kpad = rb / 96 * 128;
+  w.splits = (w.Kpad + BF6_K_CHUNK - 1) / BF6_K_CHUNK;
+  w.a6 = c.take<int8_t>(M * rb);
+  w.b6 = c.take<int8_t>(N * rb);
+  w.part = c.take<int32_t>(w.splits * M * N);
+  return w;
+}
+
+size_t fqt_gemm_s4s4_bf6_workspace(int64_t M, int64_t N, int64_t K) {
+  if (M < 1 || N < 1 || K < 1) return 0;
+  Carver c(nullptr);
+  carve_bf6(c, M, N, K);
+  return c.off;
+}
+
+fqt_status fqt_gemm_s4s4_bf6(const int8_t* A, const int8_t* B, int64_t M, int64_t N, int64_t K, int64_t lda,
+                             int64_t ldb, int64_t* C, void* ws, size_t ws_bytes, fqt_stream_t s) {
+  if (!A || !B || !C) return FQT_EINVAL;
+  if (M < 1 || N < 1 || K < 1 || lda < K || ldb < K) return FQT_EINVAL;
+  if (M > 65535LL * 128 || (K + BF6_K_CHUNK - 1) / BF6_K_CHUNK > 65535) return FQT_EUNSUPPORTED;
+  if (!ws) return FQT_EWORKSPACE;
+  if (ws_bytes < fqt_gemm_s4s4_bf6_workspace(M, N, K)) return FQT_EWORKSPACE;
+  Carver c(ws);
+  Bf6Ws w = carve_bf6(c, M, N, K);
+  FQT_TRY(launch_status_clear(w.h.status, s));
+  FQT_TRY(launch_pack_e3m2(A, M, K, lda, w.a6, w.h.status, s));
+  FQT_TRY(launch_pack_e3m2(B, N, K, ldb, w.b6, w.h.status, s));
+  Bf6Params p{};
+  p.A = w.a6;
+  p.B = w.b6;
+  p.M = M;
+  p.N = N;
+  p.Kpad = w.Kpad;
+  p.lda = bf6_row_bytes(K);
+  p.ldb = p.lda;
+  p.kchunk = w.splits > 1 ? BF6_K_CHUNK : w.Kpad;
+  p.splits = (int)w.splits;
+  p.part = w.part;
+  FQT_TRY(launch_gemm_bf6(p, s));
+  GemmParams g{};
+  g.M = M;
+  g.N = N;
+  g.splits = (int)w.splits;
+  g.part = w.part;
+  FQT_TRY(launch_splitk_reduce(g, C, EPI_RAW_I32, s));
+  return FQT_OK;
+}
+
 fqt_status fqt_conv_backward_im2col(const float* X, const float* W, const float* G, const fqt_conv_shape* shape,
                                     const fqt_bwd_cfg* cfg, float* grad_W, float* grad_X, void* ws,
                                     size_t ws_bytes, fqt_stream_t s) {

@@ -242,6 +242,23 @@ struct ColvecParams {
 int64_t colvec_splits(int64_t rows);
 hipError_t launch_colvec(const ColvecParams& p, hipStream_t s);
 
+// ---- 4-bit codes on 6-bit float matrix cores ---------------------------
+// Packed e3m2 operands (rows of bf6_row_bytes(K) bytes, K padded to 128),
+// exact int32 partials [splits][M][N] (reduce with launch_splitk_reduce).
+struct Bf6Params {
+  const int8_t* A;  // [M] packed rows, stride lda bytes
+  const int8_t* B;  // [N] packed rows, stride ldb bytes
+  int64_t M, N, Kpad, lda, ldb;
+  int64_t kchunk;   // codes per split, multiple of 128, <= 131072
+  int splits;
+  int32_t* part;
+};
+int64_t bf6_row_bytes(int64_t K);
+hipError_t launch_pack_e3m2(const int8_t* src, int64_t rows, int64_t K, int64_t ld, int8_t* dst, uint32_t* status,
+                            hipStream_t s);
+hipError_t launch_status_clear(uint32_t* status, hipStream_t s);
+hipError_t launch_gemm_bf6(const Bf6Params& p, hipStream_t s);
+
 // ---- conv ----------------------------------------------------------------
 struct ConvGeom {
   int n, c, h, w, o, kh, kw, stride, pad, ho, wo;

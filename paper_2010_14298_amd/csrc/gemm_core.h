@@ -65,6 +65,11 @@ __device__ __forceinline__ Chunk16 load_chunk(const int8_t* base, int64_t ld, in
   return c;
 }
 
+template <class C>
+inline int64_t gemm_tiles_of(int64_t M, int64_t N) {
+  return ((M + C::BM - 1) / C::BM) * ((N + C::BN - 1) / C::BN);
+}
+
 // Bijective block -> tile map: the first 8 * floor(T / 8) blocks give each
 // XCD (block id mod 8) a contiguous run of tiles; the rest map to themselves.
 __device__ __forceinline__ int64_t xcd_tile(int64_t id, int64_t ntiles) {

@@ -60,7 +60,7 @@ EXPORTS = [
     "fqt_linear_backward", "fqt_linear_backward_workspace",
     "fqt_linear_forward", "fqt_linear_forward_workspace",
     "fqt_conv_backward_im2col", "fqt_conv_backward_workspace",
-    "fqt_gemm_s8s8_s64", "fqt_gemm_workspace",
+    "fqt_gemm_s8s8_s64", "fqt_gemm_workspace", "fqt_gemm_s4s4_bf6", "fqt_gemm_s4s4_bf6_workspace",
     "fqt_workspace_status", "fqt_status_str", "fqt_version",
 ]
 
@@ -96,6 +96,8 @@ def load(path=LIB_PATH):
         "fqt_conv_backward_workspace": ([shp, cfgp], sz),
         "fqt_gemm_s8s8_s64": ([vp, vp, i64, i64, i64, i64, i64, vp, vp, sz, vp], i32),
         "fqt_gemm_workspace": ([i64, i64, i64], sz),
+        "fqt_gemm_s4s4_bf6": ([vp, vp, i64, i64, i64, i64, i64, vp, vp, sz, vp], i32),
+        "fqt_gemm_s4s4_bf6_workspace": ([i64, i64, i64], sz),
         "fqt_workspace_status": ([vp, vp], i32),
         "fqt_status_str": ([i32], ctypes.c_char_p),
         "fqt_version": ([], ctypes.c_char_p),
@@ -327,6 +329,29 @@ def fqt_gemm_s8s8_s64(A, B, ws=None):
                                   ws.numel(), _stream())
     _check("fqt_gemm_s8s8_s64", rc)
     return C
+
+
+def fqt_gemm_s4s4_bf6_workspace(M, N, K):
+    return load().fqt_gemm_s4s4_bf6_workspace(M, N, K)
+
+
+def fqt_gemm_s4s4_bf6(A, B, ws=None, C=None):
+    """C [M, N] int64 = A [M, K] . B [N, K]^T for codes in [-8, 7], on the 6-bit
+    float matrix cores (exact).  Returns (C, ws); check fqt_workspace_status(ws)."""
+    if not (A.is_cuda and B.is_cuda and A.dtype == torch.int8 and B.dtype == torch.int8):
+        raise ValueError("A, B must be int8 CUDA tensors")
+    M, K = A.shape
+    N = B.shape[0]
+    if B.shape[1] != K or A.stride(1) != 1 or B.stride(1) != 1:
+        raise ValueError("A [M, K], B [N, K], K contiguous")
+    if C is None:
+        C = torch.empty((M, N), dtype=torch.int64, device=A.device)
+    if ws is None:
+        ws = _workspace(fqt_gemm_s4s4_bf6_workspace(M, N, K), A.device)
+    rc = load().fqt_gemm_s4s4_bf6(_ptr(A), _ptr(B), M, N, K, A.stride(0), B.stride(0), _ptr(C), _ptr(ws),
+                                  ws.numel(), _stream())
+    _check("fqt_gemm_s4s4_bf6", rc)
+    return C, ws
 
 
 def fqt_workspace_status(ws):

@@ -85,6 +85,11 @@ def test_workspace_queries_and_argument_errors():
     assert lib.fqt_quantize_psq(fake, 4, 4, 0, 0, 0, ctypes.byref(qt), fake, 1 << 30, null) == 1
     assert lib.fqt_quantize_bhq(fake, 4, 4, 5, 64, 0, 0, ctypes.byref(qt), fake, 1 << 30, null) == 1   # no perm
     assert lib.fqt_gemm_s8s8_s64(fake, fake, 4, 4, 8, 4, 8, fake, fake, 1 << 30, null) == 1            # lda < K
+    assert lib.fqt_gemm_s4s4_bf6(fake, fake, 4, 4, 8, 4, 8, fake, fake, 1 << 30, null) == 1            # lda < K
+    assert lib.fqt_gemm_s4s4_bf6(fake, fake, 4, 4, 8, 8, 8, fake, fake, 16, null) == 4
+    assert lib.fqt_gemm_s4s4_bf6_workspace(0, 4, 4) == 0
+    # packed rows: 96 bytes per 128 codes
+    assert lib.fqt_gemm_s4s4_bf6_workspace(128, 128, 4096) >= 2 * 128 * 3072 + 128 * 128 * 4
     assert lib.fqt_status_str(3) == b"non-finite input or range overflow"
     # layer forward: bits, relu flag, workspace
     assert lib.fqt_linear_forward_workspace(0, 4, 4) == 0
