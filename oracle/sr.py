@@ -2,7 +2,7 @@
 
 Sec. 3.3 defines SR(x) = ceil(x) with probability x - floor(x), floor(x)
 otherwise.  A machine draw has finitely many bits, so the contract fixes a
-24-bit uniform u = (32-bit Philox word) >> 8 and rounds up iff
+24-bit uniform u = (32-bit Philox word) & 0xFFFFFF (its low 24 bits) and rounds up iff
 
     float(u) < frac * 2^24,   frac = y - floor(y)   (float32, exact for y >= 0)
 
@@ -21,7 +21,7 @@ TWO24 = np.float32(16777216.0)
 
 def uniform24(elem_index, seed, stream):
     """The 24-bit integer uniforms u in [0, 2^24) for the given element indices."""
-    return (philox.draws(elem_index, seed, stream) >> np.uint64(8)).astype(np.int64)
+    return (philox.draws(elem_index, seed, stream) & np.uint64(0xFFFFFF)).astype(np.int64)
 
 
 def round_stochastic(y, u, B):

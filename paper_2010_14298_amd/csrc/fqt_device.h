@@ -47,8 +47,9 @@ __device__ __forceinline__ uint32_t philox_word(const u32x4& o, int i) {
 }
 
 // ---------------------------------------------------------------------------
-// Stochastic rounding with a 24-bit uniform (Sec. 3.3):
-//   fl = floor(y); frac = y - fl; round up iff float(word >> 8) < frac * 2^24;
+// Stochastic rounding with a 24-bit uniform (Sec. 3.3), the low 24 bits of
+// the Philox word:
+//   fl = floor(y); frac = y - fl; round up iff float(word & 0xFFFFFF) < frac * 2^24;
 //   code clamped to [0, B].
 // fl is clamped to [-1, B] first, which leaves the clamped code unchanged and
 // keeps the integer conversion in range.
@@ -57,7 +58,7 @@ __device__ __forceinline__ int sr_code(float y, uint32_t word, int B) {
   float fl = floorf(y);
   const float frac = y - fl;
   const float thr = frac * 16777216.0f;
-  const float u = (float)(word >> 8);
+  const float u = (float)(word & 0xFFFFFFu);
   fl = fminf(fmaxf(fl, -1.0f), (float)B);
   int c = (int)fl + (u < thr ? 1 : 0);
   return min(max(c, 0), B);
@@ -78,16 +79,18 @@ __device__ __forceinline__ int rne_code(float y, int B) {
 //
 // sr_top: with yc = clamp(y, 0, B) (clamping first leaves the clamped code
 // of sr_code unchanged), T = ceil(yc * 2^24) = floor(yc) * 2^24 + ceil(frac
-// * 2^24) (the scaling is exact and floor(yc) * 2^24 is an integer), and
-// u' = 2^24 - 1 - (word >> 8), the sum T + u' carries into bit 24 exactly
-// when (word >> 8) < ceil(frac * 2^24), i.e. when (word >> 8) < frac * 2^24:
-// the rounding-up decision of sr_code.  T + u' < 2^32 since yc <= 255 and at
-// yc = B the fraction is 0.
+// * 2^24) (the scaling is exact and floor(yc) * 2^24 is an integer), u =
+// word & 0xFFFFFF and u' = 2^24 - 1 - u = ~word & 0xFFFFFF, the sum T + u'
+// carries into bit 24 exactly when u < ceil(frac * 2^24), i.e. when u <
+// frac * 2^24: the rounding-up decision of sr_code.  T + u' < 2^32 since
+// yc <= 255 and at yc = B the fraction is 0.  -hoff only has top-byte bits
+// and u' only low ones, so u' - hoff is one three-input logic operation.
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ int32_t sr_top(float y, uint32_t word, float Bf, uint32_t hoff) {
   const float yc = __builtin_amdgcn_fmed3f(y, 0.0f, Bf);
   const uint32_t t = (uint32_t)ceilf(yc * 16777216.0f);
-  return (int32_t)((t - (word >> 8)) + (0xFFFFFFu - hoff));  // T + u' - hoff
+  // (~word & 0xFFFFFF) | -hoff in one bitop3 (table 0xAE: ~S0 & S1 | S2)
+  return (int32_t)(t + __builtin_amdgcn_bitop3_b32(word, 0xFFFFFFu, 0u - hoff, 0xAE));  // T + u' - hoff
 }
 __device__ __forceinline__ int32_t rne_top(float y, float Bf, uint32_t hoff) {
   const float r = rintf(__builtin_amdgcn_fmed3f(y, 0.0f, Bf));

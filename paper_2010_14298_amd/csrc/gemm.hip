@@ -208,13 +208,22 @@ __global__ __launch_bounds__(C::THREADS) void gemm_i8_kernel(GemmParams p) {
           double tau = 0.0, alpha = 0.0;
           if (gs.m > 0) {
             int64_t asum = 0;
-            for (int t = 0; t < gs.m; ++t) asum += sacc[(g0 + t) * C::BN + c];
+            if (gs.m == KG) {
+              // four independent partial sums (integer: the order is free)
+              int64_t s4[4] = {0, 0, 0, 0};
+#pragma unroll
+              for (int t = 0; t < KG; ++t) s4[t & 3] += sacc[(g0 + t) * C::BN + c];
+              asum = (s4[0] + s4[1]) + (s4[2] + s4[3]);
+            } else {
+              for (int t = 0; t < gs.m; ++t) asum += sacc[(g0 + t) * C::BN + c];
+            }
             const double S = dW * (double)asum + (gs.rsum + (double)gs.m * (hz * colterm));
             const double T0 = dW * (double)sacc[g0 * C::BN + c] + (srow[g0].rterm + hz * colterm);
             alpha = gs.kind == 2 ? p.L.inv_sk_p : p.L.inv_sk_k;
             tau = (alpha * S - T0) / (1.0 - alpha);
           }
           const double up0 = (1.0 - alpha) * tau, dn = alpha * tau;
+#pragma unroll 8
           for (int t = 0; t < KG; ++t) {
             const RowStage q = srow[g0 + t];
             if (q.obase < 0) continue;
@@ -230,6 +239,7 @@ __global__ __launch_bounds__(C::THREADS) void gemm_i8_kernel(GemmParams p) {
           }
         }
       } else {
+#pragma unroll 8
         for (int t = rbase; t < rbase + 64; ++t) {
           const RowStage q = srow[t];
           if (q.obase < 0) continue;

@@ -22,7 +22,7 @@ def fixed_point_codes(y, words, bits):
     half = 1 << (bits - 1)
     yc = np.minimum(np.maximum(np.asarray(y, F32), F32(0)), F32(B)).astype(F32)
     t = np.ceil((yc * F32(16777216.0)).astype(F32)).astype(np.float64).astype(np.uint64)
-    u_prime = ((words >> np.uint32(8)) ^ np.uint32(0xFFFFFF)).astype(np.uint64)
+    u_prime = ((words & np.uint32(0xFFFFFF)) ^ np.uint32(0xFFFFFF)).astype(np.uint64)
     acc = (t + u_prime - np.uint64(half << 24)) & np.uint64(0xFFFFFFFF)
     return acc.astype(np.uint32).view(np.int32) >> 24
 
@@ -47,9 +47,9 @@ def test_fixed_point_equals_float_rule(bits):
         fr = np.nan_to_num((y - np.floor(y)).astype(F32) * F32(2 ** 24), nan=0.0, posinf=0.0, neginf=0.0)
     on_edge = rng.random(y.size) < 0.5
     u_edge = np.clip(np.ceil(fr[on_edge]) - rng.integers(0, 2, on_edge.sum()), 0, 2 ** 24 - 1).astype(np.uint64)
-    words[on_edge] = (u_edge << np.uint64(8)) | rng.integers(0, 256, on_edge.sum(), dtype=np.uint64)
+    words[on_edge] = u_edge | (rng.integers(0, 256, on_edge.sum(), dtype=np.uint64) << np.uint64(24))
     words = words.astype(np.uint32)
     with np.errstate(invalid="ignore"):
-        ref = sr.round_stochastic(y, (words >> np.uint32(8)).astype(np.int64), B)
+        ref = sr.round_stochastic(y, (words & np.uint32(0xFFFFFF)).astype(np.int64), B)
     got = fixed_point_codes(y, words, bits) + (1 << (bits - 1))
     assert np.array_equal(got, ref)
