@@ -161,3 +161,17 @@ def test_chain_theorems_1_and_2():
                 pred += np.mean([CH.lower_layer_variances(a_host, Ws, l, d, SPECS[l], maps=maps[l])[k]
                                  for d in keep[l]])
         assert abs(var.sum() - pred) <= 0.10 * pred, (k, var.sum(), pred)
+
+
+def test_linear_forward_split_k_with_relu():
+    """d_in beyond one int32-exact chunk (65536): int32 partials summed in int64,
+    the per-tensor epilogue and the ReLU in the reduction pass."""
+    f = fqt()
+    rng = np.random.default_rng(21)
+    X = rng.standard_normal((6, 70000)).astype(np.float32)
+    W = (rng.standard_normal((5, 70000)) / 300.0).astype(np.float32)
+    for relu in (False, True):
+        Y, ws = f.fqt_linear_forward(dev(X), dev(W), relu=relu)
+        assert f.fqt_workspace_status(ws) == 0
+        _, ref = CH.layer_forward(X, W, relu)
+        assert rownorm_err(host(Y), ref) <= REL_TOL

@@ -92,3 +92,19 @@ def test_linear_backward_shift_ffn_layer_sampled():
     cols = rng.choice(G.shape[1], 24, replace=False)
     G1r = Q.dequantize_affine(dict(q1, code=q1["code"][:, cols]))
     assert rownorm_err(gW[cols], G1r.T @ Q.dequantize(qx)) <= REL_TOL
+
+
+def test_linear_backward_shift_split_k():
+    """N beyond one int32-exact chunk (65536 samples): grad_W from int32 partials
+    summed in int64, with the shift quantizer's column vector in the reduction."""
+    f = fqt()
+    rng = np.random.default_rng(8)
+    N, d_in, d_out = 70000, 8, 6
+    X = rng.standard_normal((N, d_in)).astype(np.float32)
+    W = rng.standard_normal((d_out, d_in)).astype(np.float32)
+    G = (rng.standard_normal((N, d_out)) * np.exp(rng.uniform(-3, 1, size=(N, 1)))).astype(np.float32)
+    qb_w, qb_x = ("shift", 4, 0), ("psq", 8, 0)
+    gW, gX, ws = f.fqt_linear_backward(dev(X), dev(W), dev(G), qb_x=qb_x, qb_w=qb_w, seed=4)
+    assert f.fqt_workspace_status(ws) == 0
+    r = BW.linear_backward(X, W, G, qb_x, qb_w, 8, 8, 4)
+    assert rownorm_err(host(gW), r["grad_W64"]) <= REL_TOL
