@@ -85,6 +85,8 @@ __global__ __launch_bounds__(256) void stats_kernel(StatsPlan sp) {
   int bad = 0;
   if ((g.cols & 3) == 0 && ((uintptr_t)g.x & 15) == 0) {
     const float4* x4 = reinterpret_cast<const float4*>(xr);
+    // unrolled: a thread's loads are all in flight before the reductions
+#pragma unroll 4
     for (int64_t i = (c_begin >> 2) + threadIdx.x; i < (c_end >> 2); i += blockDim.x) {
       const float4 v = x4[i];
       mn = fminf(fminf(mn, v.x), fminf(v.y, fminf(v.z, v.w)));
