@@ -336,7 +336,7 @@ struct ConvWs {
   StatsSeg sx_seg, sw_seg, sg_seg;
   float *rmin, *rmax;
   int8_t *xq_t, *wq_t, *q2, *q1_t, *bw;
-  int32_t *swq, *sumB, *qs, *sumA_tap, *count_tap, *sg, *ct, *cnt;
+  int32_t *swq, *sumB, *xs, *qs, *sumA_tap, *count_tap, *sg, *ct, *cnt;
   float *sx, *zx, *sw, *zw, *sg1, *zg1, *sg2, *zg2;
   int32_t* perm;
   void* plan;
@@ -370,6 +370,7 @@ ConvWs carve_conv(Carver& c, const float* X, const float* W, const float* G, con
   w.bw = c.take<int8_t>(taps * g.c * w.ldq);
   w.swq = c.take<int32_t>(taps * g.c);
   w.sumB = c.take<int32_t>(taps * g.c);
+  w.xs = c.take<int32_t>((int64_t)g.c * g.h * g.w);
   w.qs = c.take<int32_t>((int64_t)g.o * howo);
   w.sumA_tap = c.take<int32_t>((int64_t)g.o * taps);
   w.count_tap = c.take<int32_t>(taps);
@@ -988,7 +989,7 @@ fqt_status fqt_conv_backward_im2col(const float* X, const float* W, const float*
 
   // grad_W [o][(r, s, c)] = Q_b1(G)^T im2col(Q_f(X)), split over output pixels
   tr.begin(6);
-  FQT_TRY(launch_conv_im2col_w(g, w.xq_t, w.bw, w.ldq, w.sumB, s));
+  FQT_TRY(launch_conv_im2col_w(g, w.xq_t, w.bw, w.ldq, w.xs, w.sumB, s));
   FQT_TRY(launch_conv_tapsums(g, w.q1_t, w.ldq, w.qs, w.sumA_tap, w.count_tap, s));
   GemmParams gw{};
   gw.A = w.q1_t;

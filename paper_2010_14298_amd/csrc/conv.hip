@@ -152,8 +152,7 @@ __global__ void conv_wq_kernel(const float* W, ConvGeom g, int bits, const float
 // im2col of the X codes for grad_W: B[(r, s, c)][p] over output pixels p in
 // slot order (zero codes on padded taps and for p >= P), plus row sums
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void conv_im2col_w_kernel(ConvGeom g, const int8_t* xq_t, int8_t* bw, int64_t ldb,
-                                                            int32_t* sumB) {
+__global__ __launch_bounds__(256) void conv_im2col_w_kernel(ConvGeom g, const int8_t* xq_t, int8_t* bw, int64_t ldb) {
   const int64_t row = blockIdx.y;
   const int tap = (int)(row / g.c), c = (int)(row % g.c);
   const int r = tap / g.kw, s = tap % g.kw;
@@ -162,48 +161,120 @@ __global__ __launch_bounds__(256) void conv_im2col_w_kernel(ConvGeom g, const in
   const int64_t p0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 16;
   const int8_t* xc = xq_t + (int64_t)c * g.n * hw;
   uint32_t w[4] = {0u, 0u, 0u, 0u};
-  int sum = 0;
   if (p0 < ldb) {
+    // (sample, y, x) of p0 once; the 16 pixels then step through x, y, sample
+    int64_t slot = p0 / howo;
+    const int pix0 = (int)(p0 - slot * howo);
+    int y = pix0 / g.wo, x = pix0 - (pix0 / g.wo) * g.wo;
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
-      const int64_t p = p0 + i;
       int v = 0;
-      if (p < P) {
-        const int64_t slot = p / howo, pix = p % howo;
-        const int y = (int)(pix / g.wo), x = (int)(pix % g.wo);
+      if (p0 + i < P) {
         const int iy = y * g.stride - g.pad + r, ix = x * g.stride - g.pad + s;
-        if (iy >= 0 && iy < g.h && ix >= 0 && ix < g.w) v = xc[slot * hw + (int64_t)iy * g.w + ix];
+        if (iy >= 0 && iy < g.h && ix >= 0 && ix < g.w) v = xc[slot * hw + iy * g.w + ix];
       }
-      sum += v;
       w[i >> 2] |= (uint32_t)(v & 255) << (8 * (i & 3));
+      if (++x == g.wo) {
+        x = 0;
+        if (++y == g.ho) {
+          y = 0;
+          ++slot;
+        }
+      }
     }
     *reinterpret_cast<uint4*>(bw + row * ldb + p0) = make_uint4(w[0], w[1], w[2], w[3]);
   }
-  // block sum -> one atomic per block
-  __shared__ int ssum[4];
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) sum += __shfl_xor(sum, o);
-  if ((threadIdx.x & 63) == 0) ssum[threadIdx.x >> 6] = sum;
-  __syncthreads();
-  if (threadIdx.x == 0) atomicAdd(sumB + row, ssum[0] + ssum[1] + ssum[2] + ssum[3]);
 }
 
 // ---------------------------------------------------------------------------
 // masked zero-point sums of Q_b1(G) per (o, tap) and the valid-pixel count of
 // each tap: Qs[o][y][x] = sum over samples, then rectangle sums per tap
 // ---------------------------------------------------------------------------
-__global__ void conv_qsum_kernel(ConvGeom g, const int8_t* q1_t, int64_t ldq, int32_t* qs) {
-  const int64_t howo = (int64_t)g.ho * g.wo;
-  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (t >= (int64_t)g.o * howo) return;
-  const int64_t o = t / howo, pix = t % howo;
-  const int8_t* row = q1_t + o * ldq + pix;
-  int sum = 0;
-  for (int n = 0; n < g.n; ++n) sum += row[(int64_t)n * howo];
-  qs[t] = sum;
+// Stride-1 im2col of the activation codes for grad_W, one thread per output
+// word: a block takes whole output row segments (sample, y) of one (tap,
+// channel) row, and its threads walk the segments' words in order, so loads
+// and stores are coalesced along the row.  Output x reads input x + s - pad
+// of row iy = y - pad + r; with w and wo multiples of 4 and 4-byte aligned
+// rows each output word is a byte funnel shift of two input words, and
+// input words outside the row read as zero, which is exactly the padding.
+__host__ __device__ inline bool conv_im2col_rows_ok(const ConvGeom& g, const int8_t* xq_t, const int8_t* bw,
+                                                    int64_t ldb) {
+  return g.stride == 1 && (g.w & 3) == 0 && (g.wo & 3) == 0 && (ldb & 3) == 0 && (((uintptr_t)xq_t) & 3) == 0 &&
+         (((uintptr_t)bw) & 3) == 0 && g.wo <= 1024;
 }
 
-// valid output rows / columns of tap offset r: y with 0 <= y*stride - pad + r < h
+constexpr int IM2COL_WPT = 8;  // output words per thread (loads in flight together)
+
+__global__ __launch_bounds__(256) void conv_im2col_rows_kernel(ConvGeom g, const int8_t* xq_t, int8_t* bw,
+                                                               int64_t ldb, int segs_per_block) {
+  const int64_t row = blockIdx.y;
+  const int tap = (int)(row / g.c), c = (int)(row % g.c);
+  const int r = tap / g.kw, s = tap % g.kw;
+  const int64_t hw = (int64_t)g.h * g.w;
+  const int nw = g.wo >> 2, iw = g.w >> 2;
+  const int64_t nseg = (int64_t)g.n * g.ho;
+  const int d = s - g.pad;                              // output x reads input x + d
+  const int wq = d >= 0 ? d >> 2 : -((-d + 3) >> 2);   // floor(d / 4)
+  const int sh = d - 4 * wq;                            // 0..3
+  const int8_t* xc = xq_t + (int64_t)c * g.n * hw;
+  int8_t* dst = bw + row * ldb;
+  uint32_t lo[IM2COL_WPT], hi[IM2COL_WPT];
+  int64_t at[IM2COL_WPT];
+  // thread t takes words t, t + 256, ...: a step of 256 words is `sa` whole
+  // segments and `sb` words, so (segment, word) and (slot, y) advance
+  // without divisions (32-bit: n * ho < 2^31 is checked at launch)
+  const int sa = (int)blockDim.x / nw, sb = (int)blockDim.x - sa * nw;
+  int ls = threadIdx.x / nw, j = threadIdx.x - ls * nw;
+  int seg = (int)blockIdx.x * segs_per_block + ls;
+  int slot = seg / g.ho, y = seg - slot * g.ho;
+#pragma unroll
+  for (int q = 0; q < IM2COL_WPT; ++q) {
+    lo[q] = hi[q] = 0u;
+    at[q] = -1;
+    if (ls < segs_per_block && seg < (int)nseg) {
+      const int iy = y - g.pad + r;
+      at[q] = (int64_t)seg * g.wo + 4 * j;
+      if (iy >= 0 && iy < g.h) {
+        const uint32_t* src = reinterpret_cast<const uint32_t*>(xc + (int64_t)slot * hw + (int64_t)iy * g.w);
+        const int k0 = j + wq;
+        if (k0 >= 0 && k0 < iw) lo[q] = src[k0];
+        if (k0 + 1 >= 0 && k0 + 1 < iw) hi[q] = src[k0 + 1];
+      }
+    }
+    // advance by blockDim.x words
+    int step = sa;
+    j += sb;
+    if (j >= nw) {
+      j -= nw;
+      ++step;
+    }
+    ls += step;
+    seg += step;
+    y += step;
+    while (y >= g.ho) {
+      y -= g.ho;
+      ++slot;
+    }
+  }
+#pragma unroll
+  for (int q = 0; q < IM2COL_WPT; ++q)
+    if (at[q] >= 0)
+      *reinterpret_cast<uint32_t*>(dst + at[q]) =
+          sh == 0 ? lo[q] : (uint32_t)((((uint64_t)hi[q] << 32) | lo[q]) >> (8 * sh));
+  // the zero tail [P, ldb) of the row: the last block's threads
+  if (blockIdx.x == gridDim.x - 1) {
+    const int64_t P = nseg * g.wo;
+    for (int64_t t = P + 4 * (int64_t)threadIdx.x; t < ldb; t += 4 * (int64_t)blockDim.x)
+      *reinterpret_cast<uint32_t*>(dst + t) = 0u;
+  }
+}
+
+__device__ __forceinline__ int wave_sum4_i(int v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
 __device__ __forceinline__ void tap_range(int r, int stride, int pad, int h, int ho, int& lo, int& hi) {
   lo = 0;
   while (lo < ho && lo * stride - pad + r < 0) ++lo;
@@ -211,21 +282,83 @@ __device__ __forceinline__ void tap_range(int r, int stride, int pad, int h, int
   while (hi > lo && (hi - 1) * stride - pad + r >= h) --hi;
 }
 
-__global__ void conv_tapsum_kernel(ConvGeom g, const int32_t* qs, int32_t* sumA_tap, int32_t* count_tap) {
-  const int taps = g.kh * g.kw;
+// One block per (o, tap): the code sums qs[o] over the tap's valid output
+// pixels (a rectangle), spread over the block's threads.
+// Code sums of the im2col rows without touching them: xs[c][pix] sums the
+// activation codes over samples, and row (tap, c) of the im2col matrix sums
+// xs[c] over the input pixels its valid output pixels read (a strided
+// rectangle), one block per row.
+__global__ void conv_xsum_kernel(ConvGeom g, const int8_t* xq_t, int32_t* xs) {
+  const int64_t hw = (int64_t)g.h * g.w;
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (t >= (int64_t)g.o * taps) return;
+  if (t >= (int64_t)g.c * hw) return;
+  const int64_t c = t / hw, pix = t % hw;
+  const int8_t* col = xq_t + c * g.n * hw + pix;
+  int s4[4] = {0, 0, 0, 0};
+#pragma unroll 16
+  for (int n = 0; n < g.n; ++n) s4[n & 3] += col[(int64_t)n * hw];
+  xs[t] = (s4[0] + s4[1]) + (s4[2] + s4[3]);
+}
+
+__global__ __launch_bounds__(256) void conv_xtapsum_kernel(ConvGeom g, const int32_t* xs, int32_t* sumB) {
+  const int64_t row = blockIdx.x;  // (tap, c)
+  const int tap = (int)(row / g.c), c = (int)(row % g.c);
+  const int r = tap / g.kw, s = tap % g.kw;
+  int ylo, yhi, xlo, xhi;
+  tap_range(r, g.stride, g.pad, g.h, g.ho, ylo, yhi);
+  tap_range(s, g.stride, g.pad, g.w, g.wo, xlo, xhi);
+  const int32_t* x = xs + (int64_t)c * g.h * g.w;
+  const int wx = xhi - xlo, cnt = (yhi - ylo) * wx;
+  int sum = 0;
+  for (int i = threadIdx.x; i < cnt; i += blockDim.x) {
+    const int dy = i / wx;
+    const int iy = (ylo + dy) * g.stride - g.pad + r, ix = (xlo + i - dy * wx) * g.stride - g.pad + s;
+    sum += x[(int64_t)iy * g.w + ix];
+  }
+  __shared__ int ssum[4];
+  sum = wave_sum4_i(sum);
+  if ((threadIdx.x & 63) == 0) ssum[threadIdx.x >> 6] = sum;
+  __syncthreads();
+  if (threadIdx.x == 0) sumB[row] = ssum[0] + ssum[1] + ssum[2] + ssum[3];
+}
+
+__global__ void conv_qsum_kernel(ConvGeom g, const int8_t* q1_t, int64_t ldq, int32_t* qs) {
+  const int64_t howo = (int64_t)g.ho * g.wo;
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= (int64_t)g.o * howo) return;
+  const int64_t o = t / howo, pix = t % howo;
+  const int8_t* row = q1_t + o * ldq + pix;
+  int s4[4] = {0, 0, 0, 0};
+#pragma unroll 16
+  for (int n = 0; n < g.n; ++n) s4[n & 3] += row[(int64_t)n * howo];
+  qs[t] = (s4[0] + s4[1]) + (s4[2] + s4[3]);
+}
+
+// valid output rows / columns of tap offset r: y with 0 <= y*stride - pad + r < h
+__global__ __launch_bounds__(256) void conv_tapsum_kernel(ConvGeom g, const int32_t* qs, int32_t* sumA_tap,
+                                                          int32_t* count_tap) {
+  const int taps = g.kh * g.kw;
+  const int64_t t = blockIdx.x;
   const int o = (int)(t / taps), tap = (int)(t % taps);
   const int r = tap / g.kw, s = tap % g.kw;
   int ylo, yhi, xlo, xhi;
   tap_range(r, g.stride, g.pad, g.h, g.ho, ylo, yhi);
   tap_range(s, g.stride, g.pad, g.w, g.wo, xlo, xhi);
   const int32_t* q = qs + (int64_t)o * g.ho * g.wo;
+  const int wx = xhi - xlo, cnt = (yhi - ylo) * wx;
   int sum = 0;
-  for (int y = ylo; y < yhi; ++y)
-    for (int x = xlo; x < xhi; ++x) sum += q[(int64_t)y * g.wo + x];
-  sumA_tap[t] = sum;
-  if (o == 0) count_tap[tap] = g.n * (yhi - ylo) * (xhi - xlo);
+  for (int i = threadIdx.x; i < cnt; i += blockDim.x) {
+    const int dy = i / wx;
+    sum += q[(int64_t)(ylo + dy) * g.wo + xlo + (i - dy * wx)];
+  }
+  __shared__ int ssum[4];
+  sum = wave_sum4_i(sum);
+  if ((threadIdx.x & 63) == 0) ssum[threadIdx.x >> 6] = sum;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    sumA_tap[t] = ssum[0] + ssum[1] + ssum[2] + ssum[3];
+    if (o == 0) count_tap[tap] = g.n * cnt;
+  }
 }
 
 // split-K reduction of grad_W with the per-tap masked zero-point expansion:
@@ -258,7 +391,14 @@ __global__ void conv_sg_kernel(ConvGeom g, const int8_t* q2, int32_t* sg) {
   if (t >= (int64_t)g.n * howo) return;
   const int8_t* src = q2 + t * g.o;  // slot-major [slot][(pix, o)] is contiguous in t * o
   int sum = 0;
-  for (int o = 0; o < g.o; ++o) sum += src[o];
+  if ((g.o & 15) == 0 && ((uintptr_t)q2 & 15) == 0) {
+    for (int o = 0; o < g.o; o += 16) {
+      const uint4 v = *reinterpret_cast<const uint4*>(src + o);
+      sum = sum4_i8(v.x, sum4_i8(v.y, sum4_i8(v.z, sum4_i8(v.w, sum))));
+    }
+  } else {
+    for (int o = 0; o < g.o; ++o) sum += src[o];
+  }
   sg[t] = sum;
 }
 
@@ -297,17 +437,38 @@ struct ConvXLoader {
   const int8_t* q2;
   ConvGeom g;
   int64_t M, K, D;
-  __device__ __forceinline__ Chunk16 operator()(int64_t m, int64_t k) const {
-    Chunk16 c{{0u, 0u, 0u, 0u}};
-    if (m >= M || k >= K) return c;
+  struct Row {
+    const int8_t* base;  // this slot's gradient codes
+    int iy, ix;          // input pixel
+    bool ok;
+  };
+  __device__ __forceinline__ Row row(int64_t m) const {
+    Row rw{q2, 0, 0, false};
+    if (m >= M) return rw;
     const int64_t slot = m % g.npad, pix = m / g.npad;
-    if (slot >= g.n) return c;
-    const int tap = (int)(k / g.o), o0 = (int)(k % g.o);
-    const int r = tap / g.kw, s = tap % g.kw;
-    const int iy = (int)(pix / g.w), ix = (int)(pix % g.w);
+    if (slot >= g.n) return rw;
+    rw.base = q2 + slot * D;
+    rw.iy = (int)(pix / g.w);
+    rw.ix = (int)(pix - (int64_t)rw.iy * g.w);
+    rw.ok = true;
+    return rw;
+  }
+  __device__ __forceinline__ Chunk16 load(const Row& rw, int64_t k) const {
+    Chunk16 c{{0u, 0u, 0u, 0u}};
+    if (!rw.ok || k >= K) return c;
+    const int kk = (int)k;
+    const int tap = kk / g.o, o0 = kk - tap * g.o;
+    const int r = tap / g.kw, s = tap - r * g.kw;
     int y, x;
-    if (!tap_hits(g, iy, ix, r, s, y, x)) return c;
-    const uint4 v = *reinterpret_cast<const uint4*>(q2 + slot * D + ((int64_t)y * g.wo + x) * g.o + o0);
+    if (g.stride == 1) {
+      // output pixel (iy + pad - r, ix + pad - s): no divisions
+      y = rw.iy + g.pad - r;
+      x = rw.ix + g.pad - s;
+      if (y < 0 || x < 0 || y >= g.ho || x >= g.wo) return c;
+    } else if (!tap_hits(g, rw.iy, rw.ix, r, s, y, x)) {
+      return c;
+    }
+    const uint4 v = *reinterpret_cast<const uint4*>(rw.base + ((int64_t)y * g.wo + x) * g.o + o0);
     c.w[0] = v.x;
     c.w[1] = v.y;
     c.w[2] = v.z;
@@ -325,7 +486,7 @@ struct ConvRowStage {
   int pix;       // input pixel
 };
 
-using CfgConvX = TileCfg<256, 64, 64, 64>;
+using CfgConvX = TileCfg<128, 64, 64, 64, 64>;  // 64-code K stages, 38 KB of LDS: four blocks per CU
 
 template <int EPI, int KG>
 __global__ __launch_bounds__(256) void conv_gradx_kernel(GemmParams p, ConvGeom g, const int8_t* q2, const int32_t* sg,
@@ -458,13 +619,25 @@ hipError_t launch_conv_wq(const float* W, const ConvGeom& g, int bits, const flo
   return hipGetLastError();
 }
 
-hipError_t launch_conv_im2col_w(const ConvGeom& g, const int8_t* xq_t, int8_t* bw, int64_t ldb, int32_t* sumB,
-                                hipStream_t s) {
+hipError_t launch_conv_im2col_w(const ConvGeom& g, const int8_t* xq_t, int8_t* bw, int64_t ldb, int32_t* xs,
+                                int32_t* sumB, hipStream_t s) {
   const int64_t rows = (int64_t)g.kh * g.kw * g.c;
-  const int64_t chunks = (ldb + 16 * 256 - 1) / (16 * 256);
-  if (rows > 65535 || chunks > 0x7FFFFFFF) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(conv_im2col_w_kernel, dim3((unsigned)chunks, (unsigned)rows), dim3(256), 0, s, g, xq_t, bw, ldb,
-                     sumB);
+  if (rows > 65535) return hipErrorInvalidValue;
+  if (conv_im2col_rows_ok(g, xq_t, bw, ldb)) {
+    // stride 1, rows of 4-byte words: one thread per output word
+    const int spb = 256 * IM2COL_WPT / (g.wo / 4);
+    const int64_t blocks = ((int64_t)g.n * g.ho + spb - 1) / spb;
+    if (blocks > 0x7FFFFFFF || (int64_t)g.n * g.ho + 256 * IM2COL_WPT > 0x7FFFFFFF) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(conv_im2col_rows_kernel, dim3((unsigned)blocks, (unsigned)rows), dim3(256), 0, s, g, xq_t, bw,
+                       ldb, spb);
+  } else {
+    const int64_t chunks = (ldb + 16 * 256 - 1) / (16 * 256);
+    if (chunks > 0x7FFFFFFF) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(conv_im2col_w_kernel, dim3((unsigned)chunks, (unsigned)rows), dim3(256), 0, s, g, xq_t, bw, ldb);
+  }
+  const int64_t nx = (int64_t)g.c * g.h * g.w;
+  hipLaunchKernelGGL(conv_xsum_kernel, dim3((unsigned)((nx + 255) / 256)), dim3(256), 0, s, g, xq_t, xs);
+  hipLaunchKernelGGL(conv_xtapsum_kernel, dim3((unsigned)rows), dim3(256), 0, s, g, xs, sumB);
   return hipGetLastError();
 }
 
@@ -473,8 +646,7 @@ hipError_t launch_conv_tapsums(const ConvGeom& g, const int8_t* q1_t, int64_t ld
   const int64_t n1 = (int64_t)g.o * g.ho * g.wo;
   hipLaunchKernelGGL(conv_qsum_kernel, dim3((unsigned)((n1 + 255) / 256)), dim3(256), 0, s, g, q1_t, ldq, qs);
   const int64_t n2 = (int64_t)g.o * g.kh * g.kw;
-  hipLaunchKernelGGL(conv_tapsum_kernel, dim3((unsigned)((n2 + 255) / 256)), dim3(256), 0, s, g, qs, sumA_tap,
-                     count_tap);
+  hipLaunchKernelGGL(conv_tapsum_kernel, dim3((unsigned)n2), dim3(256), 0, s, g, qs, sumA_tap, count_tap);
   return hipGetLastError();
 }
 

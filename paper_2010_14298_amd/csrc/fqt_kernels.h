@@ -266,8 +266,8 @@ struct ConvGeom {
 };
 hipError_t launch_conv_wq(const float* W, const ConvGeom& g, int bits, const float* scale, const float* zero,
                           int8_t* wq_t, int32_t* swq, hipStream_t s);
-hipError_t launch_conv_im2col_w(const ConvGeom& g, const int8_t* xq_t, int8_t* bw, int64_t ldb, int32_t* sumB,
-                                hipStream_t s);
+hipError_t launch_conv_im2col_w(const ConvGeom& g, const int8_t* xq_t, int8_t* bw, int64_t ldb, int32_t* xs,
+                                int32_t* sumB, hipStream_t s);
 hipError_t launch_conv_tapsums(const ConvGeom& g, const int8_t* q1_t, int64_t ldq, int32_t* qs, int32_t* sumA_tap,
                                int32_t* count_tap, hipStream_t s);
 hipError_t launch_conv_gradw_reduce(const GemmParams& p, const ConvGeom& g, const int32_t* sumA_tap,

@@ -83,13 +83,19 @@ __device__ __forceinline__ int64_t xcd_tile(int64_t id, int64_t ntiles) {
 // one (register-staged, two LDS buffers) takes the A operand through
 // `aload(row, k)` (a 16-byte chunk, zero outside the operand), which is how
 // the conv input-gradient contraction gathers its implicit im2col rows, and
-// handles ragged K and unaligned rows.
+// handles ragged K and unaligned rows.  A loader maps a row once to a
+// per-row state (`row`), then loads 16-byte chunks of it (`load`) stage by
+// stage, so per-row index arithmetic stays out of the K loop.
 struct PlainALoader {
   const int8_t* A;
   int64_t lda, M, kend;
   bool aligned;
-  __device__ __forceinline__ Chunk16 operator()(int64_t r, int64_t k) const {
-    return load_chunk(A, lda, r, M, k, kend, aligned);
+  struct Row {
+    int64_t r;
+  };
+  __device__ __forceinline__ Row row(int64_t r) const { return Row{r}; }
+  __device__ __forceinline__ Chunk16 load(const Row& rw, int64_t k) const {
+    return load_chunk(A, lda, rw.r, M, k, kend, aligned);
   }
 };
 
@@ -239,12 +245,16 @@ __device__ __forceinline__ void generic_mainloop(const GemmParams& p, const ALoa
     u32x4v b[C::B_CHUNKS];
   };
   Stage st0, st1;
+  typename ALoader::Row arow[C::A_CHUNKS];
+#pragma unroll
+  for (int i = 0; i < C::A_CHUNKS; ++i) arow[i] = aload.row(m0 + (tid + C::THREADS * i) / C::KCH);
+  static_assert(C::THREADS % C::KCH == 0, "a thread keeps one chunk column");
+  const int kch = 16 * (tid % C::KCH);  // the K offset of every A chunk this thread loads
   auto gload = [&](Stage& st, int64_t t) __attribute__((always_inline)) {
     const int64_t k0 = kbeg + t * C::BK;
 #pragma unroll
     for (int i = 0; i < C::A_CHUNKS; ++i) {
-      const int c = tid + C::THREADS * i;
-      const Chunk16 v = aload(m0 + c / C::KCH, k0 + 16 * (c % C::KCH));
+      const Chunk16 v = aload.load(arow[i], k0 + kch);
       st.a[i] = u32x4v{v.w[0], v.w[1], v.w[2], v.w[3]};
     }
 #pragma unroll
