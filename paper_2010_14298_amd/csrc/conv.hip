@@ -21,6 +21,13 @@
 
 namespace fqt {
 
+__device__ __forceinline__ int wave_sum4_i(int v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
+
 // ---------------------------------------------------------------------------
 // narrow transposing per-tensor quantizer: logical [rows, cols] -> codes
 // [cols][ldt], rows in slot order; rows in [rows, ldt) get code 0.  A block
@@ -43,11 +50,18 @@ __global__ __launch_bounds__(256) void quant_narrow_t_kernel(NarrowQParams p) {
   for (int j = 0; j < 4; ++j)
 #pragma unroll
     for (int w = 0; w < 4; ++w) tcodes[j][w] = 0u;
+  // rows r0 .. r0 + 15: block index and offset of r0 once, then stepped
+  int64_t bq = p.perm ? r0 / p.blk : 0;
+  int64_t br = p.perm ? r0 - bq * p.blk : 0;
 #pragma unroll
   for (int r = 0; r < 16; ++r) {
     const int64_t row = r0 + r;
     const bool ok = row < p.rows;
-    const int64_t src = ok ? (p.perm ? (int64_t)p.perm[row / p.blk] * p.blk + row % p.blk : row) : 0;
+    const int64_t src = ok ? (p.perm ? (int64_t)p.perm[bq] * p.blk + br : row) : 0;
+    if (p.perm && ++br == p.blk) {
+      br = 0;
+      ++bq;
+    }
     const float* xr = p.x + src * p.cols;
     float g[4];
     if (ok && vec && c0 + 3 < p.cols) {
@@ -129,23 +143,26 @@ hipError_t launch_quant_narrow_t(const NarrowQParams& p, hipStream_t s) {
 // ---------------------------------------------------------------------------
 // W codes [c][(r, s, o)] (deterministic PTQ) and their sums over o per (tap, c)
 // ---------------------------------------------------------------------------
-__global__ void conv_wq_kernel(const float* W, ConvGeom g, int bits, const float* scale, const float* zero,
-                               int8_t* wq_t, int32_t* swq) {
-  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+// One wave per (tap, channel): lanes over the output channels o.
+__global__ __launch_bounds__(256) void conv_wq_kernel(const float* W, ConvGeom g, int bits, const float* scale,
+                                                      const float* zero, int8_t* wq_t, int32_t* swq) {
+  const int lane = threadIdx.x & 63;
+  const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   const int taps = g.kh * g.kw;
-  if (t >= (int64_t)taps * g.c) return;
+  if (t >= (int64_t)taps * g.c) return;  // whole waves
   const int tap = (int)(t / g.c), c = (int)(t % g.c);
   const int B = (1 << bits) - 1, half = 1 << (bits - 1);
   const float s = scale[0], z = zero[0];
   const int64_t K = (int64_t)taps * g.o;
   int sum = 0;
-  for (int o = 0; o < g.o; ++o) {
+  for (int o = lane; o < g.o; o += 64) {
     const float v = W[((int64_t)o * taps + tap) * g.c + c];
     const int q = rne_code(s * (v - z), B) - half;
     wq_t[(int64_t)c * K + (int64_t)tap * g.o + o] = (int8_t)q;
     sum += q;
   }
-  swq[(int64_t)tap * g.c + c] = sum;
+  sum = wave_sum4_i(sum);
+  if (lane == 0) swq[(int64_t)tap * g.c + c] = sum;
 }
 
 // ---------------------------------------------------------------------------
@@ -269,12 +286,6 @@ __global__ __launch_bounds__(256) void conv_im2col_rows_kernel(ConvGeom g, const
   }
 }
 
-__device__ __forceinline__ int wave_sum4_i(int v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
-  return v;
-}
-
 __device__ __forceinline__ void tap_range(int r, int stride, int pad, int h, int ho, int& lo, int& hi) {
   lo = 0;
   while (lo < ho && lo * stride - pad + r < 0) ++lo;
@@ -367,8 +378,14 @@ __global__ void conv_gradw_reduce_kernel(GemmParams p, ConvGeom g, const int32_t
   const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int64_t MN = p.M * p.N;
   if (idx >= MN) return;
-  int64_t sum = 0;
-  for (int s = 0; s < p.splits; ++s) sum += (int64_t)p.part[(int64_t)s * MN + idx];
+  // eight independent partial sums keep the split loads in flight (integers: any order)
+  int64_t s8[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  int sp = 0;
+  for (; sp + 8 <= p.splits; sp += 8)
+#pragma unroll
+    for (int u = 0; u < 8; ++u) s8[u] += (int64_t)p.part[(int64_t)(sp + u) * MN + idx];
+  for (; sp < p.splits; ++sp) s8[0] += (int64_t)p.part[(int64_t)sp * MN + idx];
+  const int64_t sum = ((s8[0] + s8[1]) + (s8[2] + s8[3])) + ((s8[4] + s8[5]) + (s8[6] + s8[7]));
   const int64_t row = idx / p.N, col = idx % p.N;
   const int taps = g.kh * g.kw;
   const int tap = (int)(col / g.c);
@@ -614,7 +631,7 @@ __global__ __launch_bounds__(256) void conv_gradx_kernel(GemmParams p, ConvGeom 
 hipError_t launch_conv_wq(const float* W, const ConvGeom& g, int bits, const float* scale, const float* zero,
                           int8_t* wq_t, int32_t* swq, hipStream_t s) {
   const int64_t n = (int64_t)g.kh * g.kw * g.c;
-  hipLaunchKernelGGL(conv_wq_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, W, g, bits, scale, zero, wq_t,
+  hipLaunchKernelGGL(conv_wq_kernel, dim3((unsigned)((n + 3) / 4)), dim3(256), 0, s, W, g, bits, scale, zero, wq_t,
                      swq);
   return hipGetLastError();
 }

@@ -414,6 +414,7 @@ static hipError_t launch_gemm_c(const GemmParams& p, int epi, hipStream_t s) {
 }
 
 hipError_t launch_gemm(const GemmParams& p, int epi, hipStream_t s) {
+  if (p.M <= 64 && epi == EPI_RAW_I32) return launch_gemm_t<CfgNarrow, EPI_RAW_I32, 0>(p, s);
   return gemm_use_large(p.M, p.N) ? launch_gemm_c<CfgLarge>(p, epi, s) : launch_gemm_c<CfgSmall>(p, epi, s);
 }
 
