@@ -470,22 +470,32 @@ struct ConvXLoader {
     rw.ok = true;
     return rw;
   }
-  __device__ __forceinline__ Chunk16 load(const Row& rw, int64_t k) const {
-    Chunk16 c{{0u, 0u, 0u, 0u}};
-    if (!rw.ok || k >= K) return c;
+  struct KState {
+    int o0, r, s;  // channel offset and tap of the chunk column
+    bool ok;
+  };
+  __device__ __forceinline__ KState kstate(int64_t k) const {
+    KState ks{0, 0, 0, k < K};
     const int kk = (int)k;
-    const int tap = kk / g.o, o0 = kk - tap * g.o;
-    const int r = tap / g.kw, s = tap - r * g.kw;
+    const int tap = kk / g.o;
+    ks.o0 = kk - tap * g.o;
+    ks.r = tap / g.kw;
+    ks.s = tap - ks.r * g.kw;
+    return ks;
+  }
+  __device__ __forceinline__ Chunk16 load(const Row& rw, const KState& ks) const {
+    Chunk16 c{{0u, 0u, 0u, 0u}};
+    if (!rw.ok || !ks.ok) return c;
     int y, x;
     if (g.stride == 1) {
       // output pixel (iy + pad - r, ix + pad - s): no divisions
-      y = rw.iy + g.pad - r;
-      x = rw.ix + g.pad - s;
+      y = rw.iy + g.pad - ks.r;
+      x = rw.ix + g.pad - ks.s;
       if (y < 0 || x < 0 || y >= g.ho || x >= g.wo) return c;
-    } else if (!tap_hits(g, rw.iy, rw.ix, r, s, y, x)) {
+    } else if (!tap_hits(g, rw.iy, rw.ix, ks.r, ks.s, y, x)) {
       return c;
     }
-    const uint4 v = *reinterpret_cast<const uint4*>(rw.base + ((int64_t)y * g.wo + x) * g.o + o0);
+    const uint4 v = *reinterpret_cast<const uint4*>(rw.base + ((int64_t)y * g.wo + x) * g.o + ks.o0);
     c.w[0] = v.x;
     c.w[1] = v.y;
     c.w[2] = v.z;

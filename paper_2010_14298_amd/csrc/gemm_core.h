@@ -88,7 +88,8 @@ __device__ __forceinline__ int64_t xcd_tile(int64_t id, int64_t ntiles) {
 // the conv input-gradient contraction gathers its implicit im2col rows, and
 // handles ragged K and unaligned rows.  A loader maps a row once to a
 // per-row state (`row`), then loads 16-byte chunks of it (`load`) stage by
-// stage, so per-row index arithmetic stays out of the K loop.
+// stage, so per-row index arithmetic stays out of the K loop; a thread's
+// chunks of one stage share their K offset, decoded once (`kstate`).
 struct PlainALoader {
   const int8_t* A;
   int64_t lda, M, kend;
@@ -96,8 +97,10 @@ struct PlainALoader {
   struct Row {
     int64_t r;
   };
+  typedef int64_t KState;
   __device__ __forceinline__ Row row(int64_t r) const { return Row{r}; }
-  __device__ __forceinline__ Chunk16 load(const Row& rw, int64_t k) const {
+  __device__ __forceinline__ KState kstate(int64_t k) const { return k; }
+  __device__ __forceinline__ Chunk16 load(const Row& rw, const KState& k) const {
     return load_chunk(A, lda, rw.r, M, k, kend, aligned);
   }
 };
@@ -255,9 +258,10 @@ __device__ __forceinline__ void generic_mainloop(const GemmParams& p, const ALoa
   const int kch = 16 * (tid % C::KCH);  // the K offset of every A chunk this thread loads
   auto gload = [&](Stage& st, int64_t t) __attribute__((always_inline)) {
     const int64_t k0 = kbeg + t * C::BK;
+    const typename ALoader::KState ks = aload.kstate(k0 + kch);  // once per stage: shared by the thread's rows
 #pragma unroll
     for (int i = 0; i < C::A_CHUNKS; ++i) {
-      const Chunk16 v = aload.load(arow[i], k0 + kch);
+      const Chunk16 v = aload.load(arow[i], ks);
       st.a[i] = u32x4v{v.w[0], v.w[1], v.w[2], v.w[3]};
     }
 #pragma unroll
