@@ -93,6 +93,30 @@ def cpu_baseline(X, W, G):
 CHAIN_WIDTHS = (1024, 4096, 4096, 1024)   # FFN-like ReLU MLP: up, square, down
 
 
+def measured_peaks(fqt, torch):
+    """The machine's own ceilings: the library's register-only int8 matrix-core
+    loop and its streaming copy, timed with HIP events."""
+    sink = torch.zeros(1, dtype=torch.int32, device="cuda")
+    fqt.fqt_probe_mfma_i8(100, sink)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    ops = fqt.fqt_probe_mfma_i8(10000, sink)
+    e1.record()
+    torch.cuda.synchronize()
+    mfma = ops / (e0.elapsed_time(e1) * 1e-3) / 1e12
+    src = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    fqt.fqt_probe_copy(src, dst)
+    e0.record()
+    moved = sum(fqt.fqt_probe_copy(src, dst) for _ in range(5))
+    e1.record()
+    torch.cuda.synchronize()
+    copy = moved / (e0.elapsed_time(e1) * 1e-3) / 1e9
+    del src, dst
+    return {"mfma_i8_TOPS": round(mfma, 1), "copy_GBps": round(copy, 1),
+            "mfma_frac_of_spec": round(mfma / INT8_PEAK_TOPS, 4), "copy_frac_of_spec": round(copy / HBM_PEAK_GBS, 4)}
+
+
 def chain_bench(args, fqt, synth, torch):
     """The multi-layer chain: forward (Q_f, Q_theta, int8 product, ReLU) and FQT
     backward (Q_b2 = BHQ 5-bit, Q_b1 = PTQ 8-bit, ReLU masks) of a 3-layer MLP
@@ -280,11 +304,16 @@ def main():
         "quant_G_hbm": {"bound": "hbm", "t": t_quant_g, "work": quant_bytes, "unit": "GB/s", "peak": HBM_PEAK_GBS,
                         "scale": 1e9},
     }
+    measured = measured_peaks(fqt, torch)
     per_kernel = {}
     for name, k in kernels.items():
         ach = k["work"] / k["t"] / k["scale"]
         per_kernel[name] = {"bound": k["bound"], "achieved": round(ach, 2), "peak": k["peak"], "unit": k["unit"],
                             "frac": round(ach / k["peak"], 4), "ms": round(k["t"] * 1e3, 4)}
+        mp = {"mfma": measured["mfma_i8_TOPS"], "hbm": measured["copy_GBps"]}.get(k["bound"])
+        if mp:
+            per_kernel[name]["measured_peak"] = mp
+            per_kernel[name]["frac_measured"] = round(ach / mp, 4)
     dom = max((n for n in kernels if n != "quant_G_hbm"), key=lambda n: kernels[n]["t"])
     roof = dict(per_kernel[dom])
     roof.pop("ms")
@@ -309,6 +338,7 @@ def main():
         "quantizer_GBps": round(quant_bytes / t_quantizer / 1e9, 2),
         "quant_G_pass_GBps": round(quant_bytes / t_quant_g / 1e9, 2),
         "phases_ms": phases,
+        "measured_peaks": measured,
         "kernels": per_kernel,
         "roofline": roof,
     }

@@ -259,6 +259,16 @@ size_t fqt_gemm_s4s4_bf6_workspace(int64_t M, int64_t N, int64_t K);
  * copy fails).                                                              */
 fqt_status fqt_workspace_status(const void* ws, fqt_stream_t s);
 
+/* Machine probes for measured peaks (the roofline's second reference).
+ * fqt_probe_mfma_i8: iters back-to-back v_mfma_i32_32x32x32_i8 on four
+ * independent register accumulators in every wave of 2048 blocks x 4 waves;
+ * *ops (host) receives the int8 operation count, to be divided by the time
+ * the caller measures on `s`.  sink: one device int32 (written only by an
+ * improbable checksum).  fqt_probe_copy: a streaming 16-byte copy of `bytes`
+ * (a multiple of 16, 16-byte aligned device buffers); moved bytes = 2 bytes. */
+fqt_status fqt_probe_mfma_i8(int64_t iters, int32_t* sink, double* ops, fqt_stream_t s);
+fqt_status fqt_probe_copy(const void* src, void* dst, size_t bytes, fqt_stream_t s);
+
 const char* fqt_status_str(fqt_status st);
 
 /* Library version string. */

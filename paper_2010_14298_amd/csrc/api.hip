@@ -1049,6 +1049,20 @@ size_t fqt_conv_backward_workspace(const fqt_conv_shape* shape, const fqt_bwd_cf
   return c.off;
 }
 
+constexpr int64_t PROBE_BLOCKS = 2048;  // 8 blocks of 4 waves per CU
+
+fqt_status fqt_probe_mfma_i8(int64_t iters, int32_t* sink, double* ops, fqt_stream_t s) {
+  if (iters < 1 || !sink || !ops) return FQT_EINVAL;
+  *ops = (double)PROBE_BLOCKS * 4.0 * 4.0 * (double)iters * (2.0 * 32 * 32 * 32);
+  return launch_mfma_probe(PROBE_BLOCKS, iters, sink, s) == hipSuccess ? FQT_OK : FQT_EDEVICE;
+}
+
+fqt_status fqt_probe_copy(const void* src, void* dst, size_t bytes, fqt_stream_t s) {
+  if (!src || !dst || bytes == 0 || bytes % 16 != 0 || ((uintptr_t)src & 15) || ((uintptr_t)dst & 15))
+    return FQT_EINVAL;
+  return launch_copy_probe(PROBE_BLOCKS * 4, src, dst, (int64_t)(bytes / 16), s) == hipSuccess ? FQT_OK : FQT_EDEVICE;
+}
+
 fqt_status fqt_workspace_status(const void* ws, fqt_stream_t s) {
   if (!ws) return FQT_EINVAL;
   if (hipStreamSynchronize(s) != hipSuccess) return FQT_EDEVICE;

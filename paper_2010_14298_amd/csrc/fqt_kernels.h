@@ -242,6 +242,10 @@ struct ColvecParams {
 int64_t colvec_splits(int64_t rows);
 hipError_t launch_colvec(const ColvecParams& p, hipStream_t s);
 
+// ---- machine probes -------------------------------------------------------
+hipError_t launch_mfma_probe(int64_t blocks, int64_t iters, int32_t* sink, hipStream_t s);
+hipError_t launch_copy_probe(int64_t blocks, const void* src, void* dst, int64_t n16, hipStream_t s);
+
 // ---- 4-bit codes on 6-bit float matrix cores ---------------------------
 // Packed e3m2 operands (rows of bf6_row_bytes(K) bytes, K padded to 128),
 // exact int32 partials [splits][M][N] (reduce with launch_splitk_reduce).

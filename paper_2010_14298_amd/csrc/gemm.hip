@@ -419,3 +419,49 @@ hipError_t launch_gemm(const GemmParams& p, int epi, hipStream_t s) {
 }
 
 }  // namespace fqt
+
+namespace fqt {
+
+// ---------------------------------------------------------------------------
+// machine probes for the measured peaks: a register-only int8 matrix-core
+// loop (four independent accumulators per wave, so the instructions issue
+// back to back) and a streaming 16-byte copy
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void mfma_probe_kernel(int64_t iters, int32_t* sink) {
+  const int lane = threadIdx.x & 63;
+  v4i a = {lane, lane + 1, lane + 2, lane + 3};
+  v4i b = {lane ^ 5, lane ^ 6, lane ^ 7, lane ^ 9};
+  v16i acc[4];
+#pragma unroll
+  for (int u = 0; u < 4; ++u)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[u][r] = 0;
+  for (int64_t it = 0; it < iters; ++it) {
+#pragma unroll
+    for (int u = 0; u < 4; ++u) acc[u] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a, b, acc[u], 0, 0, 0);
+  }
+  int32_t x = 0;
+#pragma unroll
+  for (int u = 0; u < 4; ++u)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) x ^= acc[u][r];
+  if (x == 0x7FFFFFFF) sink[0] = x;  // keeps the loop; practically never stores
+}
+
+__global__ __launch_bounds__(256) void copy_probe_kernel(const uint4* src, uint4* dst, int64_t n) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+    dst[i] = src[i];
+}
+
+hipError_t launch_mfma_probe(int64_t blocks, int64_t iters, int32_t* sink, hipStream_t s) {
+  hipLaunchKernelGGL(mfma_probe_kernel, dim3((unsigned)blocks), dim3(256), 0, s, iters, sink);
+  return hipGetLastError();
+}
+
+hipError_t launch_copy_probe(int64_t blocks, const void* src, void* dst, int64_t n16, hipStream_t s) {
+  hipLaunchKernelGGL(copy_probe_kernel, dim3((unsigned)blocks), dim3(256), 0, s, static_cast<const uint4*>(src),
+                     static_cast<uint4*>(dst), n16);
+  return hipGetLastError();
+}
+
+}  // namespace fqt

@@ -61,6 +61,7 @@ EXPORTS = [
     "fqt_linear_forward", "fqt_linear_forward_workspace",
     "fqt_conv_backward_im2col", "fqt_conv_backward_workspace",
     "fqt_gemm_s8s8_s64", "fqt_gemm_workspace", "fqt_gemm_s4s4_bf6", "fqt_gemm_s4s4_bf6_workspace",
+    "fqt_probe_mfma_i8", "fqt_probe_copy",
     "fqt_workspace_status", "fqt_status_str", "fqt_version",
 ]
 
@@ -98,6 +99,8 @@ def load(path=LIB_PATH):
         "fqt_gemm_workspace": ([i64, i64, i64], sz),
         "fqt_gemm_s4s4_bf6": ([vp, vp, i64, i64, i64, i64, i64, vp, vp, sz, vp], i32),
         "fqt_gemm_s4s4_bf6_workspace": ([i64, i64, i64], sz),
+        "fqt_probe_mfma_i8": ([i64, vp, ctypes.POINTER(ctypes.c_double), vp], i32),
+        "fqt_probe_copy": ([vp, vp, sz, vp], i32),
         "fqt_workspace_status": ([vp, vp], i32),
         "fqt_status_str": ([i32], ctypes.c_char_p),
         "fqt_version": ([], ctypes.c_char_p),
@@ -446,3 +449,20 @@ def mlp_backward(acts, Ws, G, specs, seeds, qb_w=("ptq", 8, 0), f_bits=8, theta_
         grads[i] = gW
         dZ = gX
     return grads, dZs
+
+
+# ----------------------------------------------------------------------------
+# machine probes (measured peaks)
+# ----------------------------------------------------------------------------
+def fqt_probe_mfma_i8(iters, sink):
+    """Enqueue the int8 matrix-core loop; returns its operation count."""
+    ops = ctypes.c_double(0.0)
+    _check("fqt_probe_mfma_i8", load().fqt_probe_mfma_i8(int(iters), _ptr(sink), ctypes.byref(ops), _stream()))
+    return ops.value
+
+
+def fqt_probe_copy(src, dst):
+    """Enqueue a streaming copy of src into dst (same byte size); returns bytes moved."""
+    nbytes = src.numel() * src.element_size()
+    _check("fqt_probe_copy", load().fqt_probe_copy(_ptr(src), _ptr(dst), nbytes, _stream()))
+    return 2 * nbytes

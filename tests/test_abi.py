@@ -88,6 +88,9 @@ def test_workspace_queries_and_argument_errors():
     assert lib.fqt_gemm_s4s4_bf6(fake, fake, 4, 4, 8, 4, 8, fake, fake, 1 << 30, null) == 1            # lda < K
     assert lib.fqt_gemm_s4s4_bf6(fake, fake, 4, 4, 8, 8, 8, fake, fake, 16, null) == 4
     assert lib.fqt_gemm_s4s4_bf6_workspace(0, 4, 4) == 0
+    ops = ctypes.c_double(0)
+    assert lib.fqt_probe_mfma_i8(0, fake, ctypes.byref(ops), null) == 1
+    assert lib.fqt_probe_copy(fake, fake, 24, null) == 1
     # packed rows: 96 bytes per 128 codes
     assert lib.fqt_gemm_s4s4_bf6_workspace(128, 128, 4096) >= 2 * 128 * 3072 + 128 * 128 * 4
     assert lib.fqt_status_str(3) == b"non-finite input or range overflow"
