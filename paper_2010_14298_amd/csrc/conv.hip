@@ -399,14 +399,17 @@ __global__ void conv_gradw_reduce_kernel(GemmParams p, ConvGeom g, const int32_t
 }
 
 // ---------------------------------------------------------------------------
-// grad_X helpers: S_G[slot][pix] = sum_o Q_b2 codes; CT[pix_in][c] = sum of W
+// grad_X helpers: S_G[pix][slot] = sum_o Q_b2 codes (pixel-major, so that the
+// slots of one output pixel are consecutive words); CT[pix_in][c] = sum of W
 // codes over the valid taps of an input pixel, cnt[pix_in] = their number
 // ---------------------------------------------------------------------------
 __global__ void conv_sg_kernel(ConvGeom g, const int8_t* q2, int32_t* sg) {
-  const int64_t howo = (int64_t)g.ho * g.wo;
-  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (t >= (int64_t)g.n * howo) return;
-  const int8_t* src = q2 + t * g.o;  // slot-major [slot][(pix, o)] is contiguous in t * o
+  // n * ho * wo < 2^31 (checked by the launcher): thread t = pix * n + slot
+  const uint32_t howo = (uint32_t)g.ho * (uint32_t)g.wo;
+  const uint32_t t = blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= (uint32_t)g.n * howo) return;
+  const uint32_t pix = t / (uint32_t)g.n, slot = t - pix * (uint32_t)g.n;
+  const int8_t* src = q2 + ((int64_t)slot * howo + pix) * g.o;  // Q_b2 rows are slot-major [slot][pix][o]
   int sum = 0;
   if ((g.o & 15) == 0 && ((uintptr_t)q2 & 15) == 0) {
     for (int o = 0; o < g.o; o += 16) {
@@ -510,7 +513,6 @@ struct ConvRowStage {
   double dq;     // 1 / s
   int kind;      // BHQ slot kind (0 affine)
   int orow;      // output pixel row (sample * h * w + pixel), -1 if none
-  int pix;       // input pixel
 };
 
 using CfgConvX = TileCfg<128, 64, 64, 64, 64>;  // 64-code K stages, 38 KB of LDS: four blocks per CU
@@ -555,82 +557,133 @@ __global__ __launch_bounds__(256) void conv_gradx_kernel(GemmParams p, ConvGeom 
       for (int r = 0; r < 16; ++r)
         sacc[(wm * C::WM + i * 32 + 8 * (r >> 2) + 4 * h + (r & 3)) * C::BN + wn * C::WN + j * 32 + lrow] =
             acc[i][j][r];
-  const int64_t hw = (int64_t)g.h * g.w, howo = (int64_t)g.ho * g.wo;
-  for (int rr = tid; rr < C::BM; rr += C::THREADS) {
-    const int64_t m = m0 + rr;
+  // Row terms, one thread per tile row.  M < 2^31 (checked by the launcher),
+  // so the row splits into (input pixel, slot) in 32-bit arithmetic; S_G is
+  // pixel-major, so the slots of one tap read consecutive words.
+  if (tid < C::BM) {
+    const int64_t m = m0 + tid;
     ConvRowStage q{};
     q.orow = -1;
-    const int64_t slot = m % g.npad, pix = m / g.npad;
-    if (m < p.M && slot < g.n) {
+    const uint32_t npad = (uint32_t)g.npad;
+    const uint32_t pix = (uint32_t)m / npad, slot = (uint32_t)m - pix * npad;
+    if (m < p.M && slot < (uint32_t)g.n) {
       const float s = p.rowwiseA ? p.scaleA[slot] : p.scaleA[0];
       const float z = p.rowwiseA ? p.zeroA[slot] : p.zeroA[0];
       q.kind = (EPI == EPI_BHQ) ? bhq_slot_kind(p.L, slot) : 0;
-      const int iy = (int)(pix / g.w), ix = (int)(pix % g.w);
+      const int iy = (int)(pix / (uint32_t)g.w), ix = (int)pix - iy * g.w;
       int rs = 0;
       for (int r = 0; r < g.kh; ++r)
         for (int s2 = 0; s2 < g.kw; ++s2) {
           int y, x;
-          if (tap_hits(g, iy, ix, r, s2, y, x)) rs += sg[slot * howo + (int64_t)y * g.wo + x];
+          if (tap_hits(g, iy, ix, r, s2, y, x)) rs += sg[((int64_t)y * g.wo + x) * g.n + slot];
         }
       q.rterm = zW * (double)rs;
       q.dq = 1.0 / (double)s;
       q.hz = q.kind != 0 ? (double)p.halfA + (double)z : (double)z + (double)p.halfA * q.dq;
-      q.orow = (int)((p.perm ? (int64_t)p.perm[slot] : slot) * hw + pix);
-      q.pix = (int)pix;
+      q.orow = (int)((p.perm ? (int64_t)p.perm[slot] : (int64_t)slot) * ((int64_t)g.h * g.w) + pix);
     }
-    srow[rr] = q;
+    srow[tid] = q;
   }
   __syncthreads();
-  // Thread t owns column t % BN and the 64-row runs t / BN, t / BN + THREADS / BN, ...
-  // A run is 64 rows: the slots of one input pixel (npad % 64 == 0), so every
-  // group (KG <= 64, aligned) lies inside one.
-  static_assert(C::BM % 64 == 0 && KG <= 64, "64-row epilogue runs");
-  constexpr int NRUN = C::BM / 64;
-  constexpr int RSTEP = C::THREADS / C::BN;
-  const int c = tid % C::BN;
-  const int64_t col = n0 + c;
-  if (col >= p.N) return;
-  const double kz = (double)g.o * zW;
-  for (int run = tid / C::BN; run < NRUN; run += RSTEP) {
-    const int rbase = run * 64;
-    if constexpr (EPI == EPI_BHQ && KG > 1) {
-      for (int g0 = rbase; g0 < rbase + 64; g0 += KG) {
-        const ConvRowStage& q0 = srow[g0];
-        if (q0.orow < 0 && q0.kind == 0) continue;
-        const int pix = q0.pix;
-        const double colterm = dW * (double)ct[(int64_t)pix * g.c + col] + (double)cnt[pix] * kz;
-        double S = 0.0, T0 = 0.0;
-        for (int t = 0; t < KG; ++t) {
-          const ConvRowStage& q = srow[g0 + t];
-          const double T = dW * (double)sacc[(g0 + t) * C::BN + c] + (q.rterm + q.hz * colterm);
-          if (q.kind != 0) S += T;
-          if (t == 0) T0 = T;
-        }
-        const double alpha = q0.kind == 2 ? p.L.inv_sk_p : p.L.inv_sk_k;
-        const double tau = (alpha * S - T0) / (1.0 - alpha);
-        for (int t = 0; t < KG; ++t) {
-          const ConvRowStage& q = srow[g0 + t];
-          if (q.orow < 0) continue;
-          const double a = (double)sacc[(g0 + t) * C::BN + c];
-          double v;
-          if (q.kind != 0) {
-            const double T = dW * a + (q.rterm + q.hz * colterm);
-            const double Z = (t == 0) ? T + (1.0 - alpha) * tau : T - alpha * tau;
-            v = Z * q.dq;
-          } else {
-            v = q.dq * (dW * a + q.rterm) + q.hz * colterm;
-          }
-          p.out[(int64_t)q.orow * p.ldo + col] = (float)v;
-        }
-      }
+  // Wave w owns the 64 tile rows [64 w, 64 w + 64): one run, the slots of one
+  // input pixel (npad % 64 == 0), so the column terms are loaded once.  Lane
+  // l holds the four columns n0 + 4 (l % 16) .. +3 of row 4 i + l / 16 in
+  // step i, so one step covers four rows and stores 16-byte words.  A BHQ
+  // group of KG rows (KG <= 64, aligned) lies inside the run; its column sums
+  // meet across the four row lanes by xor shuffles, which give every lane of
+  // the group the same sum.
+  constexpr int WROWS = C::BM / C::WAVES;
+  static_assert(C::BN == 64 && WROWS == 64 && KG <= 64, "epilogue wave layout");
+  const int r0 = wave * WROWS;
+  const int cq = lane & 15, rsub = lane >> 4;
+  const int64_t col = n0 + 4 * cq;
+  if (col >= p.N || m0 + r0 >= p.M) return;
+  const bool vec = col + 3 < p.N && (p.ldo & 3) == 0 && ((uintptr_t)p.out & 15) == 0;
+  const int64_t pix = (int64_t)((uint32_t)(m0 + r0) / (uint32_t)g.npad);
+  const double kz = (double)cnt[pix] * ((double)g.o * zW);
+  double colterm[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e)
+    colterm[e] = col + e < p.N ? dW * (double)ct[pix * g.c + col + e] + kz : 0.0;
+  auto row_acc = [&](int row, double (&a)[4]) {
+    const int4 v = *reinterpret_cast<const int4*>(&sacc[row * C::BN + 4 * cq]);
+    a[0] = (double)v.x;
+    a[1] = (double)v.y;
+    a[2] = (double)v.z;
+    a[3] = (double)v.w;
+  };
+  auto store = [&](int orow, const double (&v)[4]) {
+    float* dst = p.out + (int64_t)orow * p.ldo + col;
+    if (vec) {
+      *reinterpret_cast<float4*>(dst) = make_float4((float)v[0], (float)v[1], (float)v[2], (float)v[3]);
     } else {
-      for (int t = rbase; t < rbase + 64; ++t) {
-        const ConvRowStage& q = srow[t];
-        if (q.orow < 0) continue;
-        const double colterm = dW * (double)ct[(int64_t)q.pix * g.c + col] + (double)cnt[q.pix] * kz;
-        const double a = (double)sacc[t * C::BN + c];
-        p.out[(int64_t)q.orow * p.ldo + col] = (float)(q.dq * (dW * a + q.rterm) + q.hz * colterm);
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        if (col + e < p.N) dst[e] = (float)v[e];
+    }
+  };
+  if constexpr (EPI == EPI_BHQ && KG > 1) {
+    constexpr int RB = KG > 4 ? KG : 4;  // rows per block of steps
+    for (int blk = r0; blk < r0 + WROWS; blk += RB) {
+      double S[4] = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll 4
+      for (int i = 0; i < RB / 4; ++i) {
+        const int row = blk + 4 * i + rsub;
+        const ConvRowStage& q = srow[row];
+        double a[4];
+        row_acc(row, a);
+        if (q.kind != 0) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) S[e] += dW * a[e] + (q.rterm + q.hz * colterm[e]);
+        }
       }
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        S[e] += __shfl_xor(S[e], 16);
+        if constexpr (KG >= 4) S[e] += __shfl_xor(S[e], 32);
+      }
+      const int g0 = (blk + rsub) & ~(KG - 1);  // first row of this lane's group
+      const ConvRowStage& q0 = srow[g0];
+      if (q0.orow < 0 && q0.kind == 0) continue;
+      double a0[4], tau[4];
+      row_acc(g0, a0);
+      const double alpha = q0.kind == 2 ? p.L.inv_sk_p : p.L.inv_sk_k;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const double T0 = dW * a0[e] + (q0.rterm + q0.hz * colterm[e]);
+        tau[e] = (alpha * S[e] - T0) / (1.0 - alpha);
+      }
+#pragma unroll 4
+      for (int i = 0; i < RB / 4; ++i) {
+        const int row = blk + 4 * i + rsub;
+        const ConvRowStage& q = srow[row];
+        if (q.orow < 0) continue;
+        double a[4], v[4];
+        row_acc(row, a);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          if (q.kind != 0) {
+            const double T = dW * a[e] + (q.rterm + q.hz * colterm[e]);
+            const double Z = (row == g0) ? T + (1.0 - alpha) * tau[e] : T - alpha * tau[e];
+            v[e] = Z * q.dq;
+          } else {
+            v[e] = q.dq * (dW * a[e] + q.rterm) + q.hz * colterm[e];
+          }
+        }
+        store(q.orow, v);
+      }
+    }
+  } else {
+#pragma unroll 4
+    for (int i = 0; i < WROWS / 4; ++i) {
+      const int row = r0 + 4 * i + rsub;
+      const ConvRowStage& q = srow[row];
+      if (q.orow < 0) continue;
+      double a[4], v[4];
+      row_acc(row, a);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[e] = q.dq * (dW * a[e] + q.rterm) + q.hz * colterm[e];
+      store(q.orow, v);
     }
   }
 }
@@ -688,6 +741,7 @@ hipError_t launch_conv_gradw_reduce(const GemmParams& p, const ConvGeom& g, cons
 hipError_t launch_conv_gradx_prep(const ConvGeom& g, const int8_t* q2, const int32_t* swq, int32_t* sg, int32_t* ct,
                                   int32_t* cnt, hipStream_t s) {
   const int64_t n1 = (int64_t)g.n * g.ho * g.wo;
+  if (n1 > 0x7FFFFFFF) return hipErrorInvalidValue;
   hipLaunchKernelGGL(conv_sg_kernel, dim3((unsigned)((n1 + 255) / 256)), dim3(256), 0, s, g, q2, sg);
   const int64_t n2 = (int64_t)g.h * g.w * g.c;
   hipLaunchKernelGGL(conv_ct_kernel, dim3((unsigned)((n2 + 255) / 256)), dim3(256), 0, s, g, swq, ct, cnt);
@@ -698,7 +752,7 @@ template <int EPI, int KG>
 static hipError_t launch_conv_gradx_t(const GemmParams& p, const ConvGeom& g, const int8_t* q2, const int32_t* sg,
                                       const int32_t* ct, const int32_t* cnt, hipStream_t s) {
   const int64_t tiles = ((p.M + CfgConvX::BM - 1) / CfgConvX::BM) * ((p.N + CfgConvX::BN - 1) / CfgConvX::BN);
-  if (tiles > 0x7FFFFFFF) return hipErrorInvalidValue;
+  if (tiles > 0x7FFFFFFF || p.M > 0x7FFFFFFF || g.npad % 64 != 0) return hipErrorInvalidValue;
   hipLaunchKernelGGL((conv_gradx_kernel<EPI, KG>), dim3((unsigned)tiles), dim3(CfgConvX::THREADS), 0, s, p, g, q2, sg,
                      ct, cnt);
   return hipGetLastError();
