@@ -462,14 +462,16 @@ struct ConvXLoader {
     int iy, ix;          // input pixel
     bool ok;
   };
+  // M < 2^31 (checked at launch): the row splits in 32-bit arithmetic
   __device__ __forceinline__ Row row(int64_t m) const {
     Row rw{q2, 0, 0, false};
     if (m >= M) return rw;
-    const int64_t slot = m % g.npad, pix = m / g.npad;
-    if (slot >= g.n) return rw;
-    rw.base = q2 + slot * D;
-    rw.iy = (int)(pix / g.w);
-    rw.ix = (int)(pix - (int64_t)rw.iy * g.w);
+    const uint32_t npad = (uint32_t)g.npad;
+    const uint32_t pix = (uint32_t)m / npad, slot = (uint32_t)m - pix * npad;
+    if (slot >= (uint32_t)g.n) return rw;
+    rw.base = q2 + (int64_t)slot * D;
+    rw.iy = (int)(pix / (uint32_t)g.w);
+    rw.ix = (int)pix - rw.iy * g.w;
     rw.ok = true;
     return rw;
   }
@@ -507,6 +509,77 @@ struct ConvXLoader {
   }
 };
 
+// Stride-1 grad_X loader with at most 32 taps.  A row maps once to the code
+// offset of output pixel (iy + pad, ix + pad) of its slot and a bit mask of
+// the taps (r, s) whose output pixel (iy + pad - r, ix + pad - s) exists; a
+// stage maps its K offset to a tap and the offset of that tap's channels
+// relative to the row's pixel.  A chunk is then a bit test and an add; a
+// lane whose tap misses reads a 16-byte block of zeros instead, so no lane
+// is masked off around the load.
+__device__ __attribute__((aligned(16))) int8_t conv_zero16[16];
+
+struct ConvXLoader1 {
+  const int8_t* q2;
+  ConvGeom g;
+  int64_t M, K, D;
+  struct Row {
+    int64_t off;    // codes of output pixel (iy + pad, ix + pad) of this slot
+    uint32_t mask;  // bit r * kw + s: that tap reaches an output pixel
+  };
+  __device__ __forceinline__ Row row(int64_t m) const {
+    Row rw{0, 0u};
+    if (m >= M) return rw;
+    const uint32_t npad = (uint32_t)g.npad;
+    const uint32_t pix = (uint32_t)m / npad, slot = (uint32_t)m - pix * npad;
+    if (slot >= (uint32_t)g.n) return rw;
+    const int iy = (int)(pix / (uint32_t)g.w), ix = (int)pix - iy * g.w;
+    const int yc = iy + g.pad, xc = ix + g.pad;
+    uint32_t mask = 0u;
+    for (int r = 0; r < g.kh; ++r)
+      for (int s = 0; s < g.kw; ++s)
+        if (yc - r >= 0 && yc - r < g.ho && xc - s >= 0 && xc - s < g.wo) mask |= 1u << (r * g.kw + s);
+    rw.off = (int64_t)slot * D + ((int64_t)yc * g.wo + xc) * g.o;
+    rw.mask = mask;
+    return rw;
+  }
+  struct KState {
+    int64_t off;  // channel offset of the tap minus its pixel displacement
+    int tap;      // 32 (no tap) past the end of K
+  };
+  __device__ __forceinline__ KState kstate(int64_t k) const {
+    KState ks{0, 32};
+    if (k >= K) return ks;
+    const int kk = (int)k;
+    const int tap = kk / g.o;
+    const int o0 = kk - tap * g.o;
+    const int r = tap / g.kw, s = tap - r * g.kw;
+    ks.off = (int64_t)o0 - ((int64_t)r * g.wo + s) * g.o;
+    ks.tap = tap;
+    return ks;
+  }
+  __device__ __forceinline__ Chunk16 load(const Row& rw, const KState& ks) const {
+    const bool hit = ks.tap < 32 && ((rw.mask >> ks.tap) & 1u);
+    const int8_t* src = hit ? q2 + (rw.off + ks.off) : conv_zero16;
+    const uint4 v = *reinterpret_cast<const uint4*>(src);
+    return Chunk16{{v.x, v.y, v.z, v.w}};
+  }
+};
+
+// B operand of the grad_X contraction: the W codes [c][(r, s, o)] (16-byte
+// aligned rows, K a multiple of 16).  Rows past N are clamped to the last
+// one (their columns are never stored) and chunks past K come from the zero
+// block, so the K loop has no branches around its loads.
+struct ConvWLoader {
+  const int8_t* B;
+  int64_t ldb, N, K;
+  __device__ __forceinline__ Chunk16 load(int64_t r, int64_t k) const {
+    const int64_t rr = r < N ? r : N - 1;
+    const int8_t* src = k < K ? B + rr * ldb + k : conv_zero16;
+    const uint4 v = *reinterpret_cast<const uint4*>(src);
+    return Chunk16{{v.x, v.y, v.z, v.w}};
+  }
+};
+
 struct ConvRowStage {
   double rterm;  // zW * (codes summed over the valid taps of the row)
   double hz;     // BHQ group row: half + c_g;  affine row: z + half / s
@@ -517,7 +590,7 @@ struct ConvRowStage {
 
 using CfgConvX = TileCfg<128, 64, 64, 64, 64>;  // 64-code K stages, 38 KB of LDS: four blocks per CU
 
-template <int EPI, int KG>
+template <int EPI, int KG, class XLoader>
 __global__ __launch_bounds__(256) void conv_gradx_kernel(GemmParams p, ConvGeom g, const int8_t* q2, const int32_t* sg,
                                                           const int32_t* ct, const int32_t* cnt) {
   using C = CfgConvX;
@@ -542,8 +615,8 @@ __global__ __launch_bounds__(256) void conv_gradx_kernel(GemmParams p, ConvGeom 
   for (int i = 0; i < C::IT; ++i)
 #pragma unroll
     for (int j = 0; j < C::JT; ++j) acc[i][j] = v16i{0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0};
-  const ConvXLoader aload{q2, g, p.M, p.K, D};
-  gemm_mainloop<C, false>(p, aload, lds, m0, n0, 0, p.K, acc);
+  const XLoader aload{q2, g, p.M, p.K, D};
+  generic_mainloop<C>(p, aload, ConvWLoader{p.B, p.ldb, p.N, p.K}, lds, m0, n0, 0, p.K, acc);
 
   int32_t* sacc = reinterpret_cast<int32_t*>(lds);
   ConvRowStage* srow = reinterpret_cast<ConvRowStage*>(lds + C::BM * C::BN * 4);
@@ -753,8 +826,13 @@ static hipError_t launch_conv_gradx_t(const GemmParams& p, const ConvGeom& g, co
                                       const int32_t* ct, const int32_t* cnt, hipStream_t s) {
   const int64_t tiles = ((p.M + CfgConvX::BM - 1) / CfgConvX::BM) * ((p.N + CfgConvX::BN - 1) / CfgConvX::BN);
   if (tiles > 0x7FFFFFFF || p.M > 0x7FFFFFFF || g.npad % 64 != 0) return hipErrorInvalidValue;
-  hipLaunchKernelGGL((conv_gradx_kernel<EPI, KG>), dim3((unsigned)tiles), dim3(CfgConvX::THREADS), 0, s, p, g, q2, sg,
-                     ct, cnt);
+  // q2 is a workspace carve (16-byte aligned); o % 16 == 0 keeps every chunk aligned
+  if (g.stride == 1 && g.kh * g.kw <= 32)
+    hipLaunchKernelGGL((conv_gradx_kernel<EPI, KG, ConvXLoader1>), dim3((unsigned)tiles), dim3(CfgConvX::THREADS), 0,
+                       s, p, g, q2, sg, ct, cnt);
+  else
+    hipLaunchKernelGGL((conv_gradx_kernel<EPI, KG, ConvXLoader>), dim3((unsigned)tiles), dim3(CfgConvX::THREADS), 0,
+                       s, p, g, q2, sg, ct, cnt);
   return hipGetLastError();
 }
 

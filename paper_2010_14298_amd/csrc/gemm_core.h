@@ -105,6 +105,17 @@ struct PlainALoader {
   }
 };
 
+// The B operand of the generic loop: 16-byte chunks of K-contiguous rows,
+// zero outside the matrix / K range (`load_chunk`).
+struct PlainBLoader {
+  const int8_t* B;
+  int64_t ldb, N, kend;
+  bool aligned;
+  __device__ __forceinline__ Chunk16 load(int64_t r, int64_t k) const {
+    return load_chunk(B, ldb, r, N, k, kend, aligned);
+  }
+};
+
 typedef __attribute__((address_space(1))) void gmem_void;
 typedef __attribute__((address_space(3))) void lmem_void;
 
@@ -231,16 +242,16 @@ __device__ __forceinline__ void dma_mainloop(const GemmParams& p, int8_t* __rest
   __syncthreads();
 }
 
-template <class C, class ALoader>
-__device__ __forceinline__ void generic_mainloop(const GemmParams& p, const ALoader& aload, int8_t* lds, int64_t m0,
-                                                 int64_t n0, int64_t kbeg, int64_t kend, v16i (&acc)[C::IT][C::JT]) {
+template <class C, class ALoader, class BLoader>
+__device__ __forceinline__ void generic_mainloop(const GemmParams& p, const ALoader& aload, const BLoader& bload,
+                                                 int8_t* lds, int64_t m0, int64_t n0, int64_t kbeg, int64_t kend,
+                                                 v16i (&acc)[C::IT][C::JT]) {
   int8_t* sA = lds;                          // [2][BM * C::LDS_STRIDE]
   int8_t* sB = lds + 2 * C::BM * C::LDS_STRIDE;  // [2][BN * C::LDS_STRIDE]
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
   const int wm = wave / C::WAVES_N, wn = wave % C::WAVES_N;
-  const bool alB = ((p.ldb & 15) == 0) && (((uintptr_t)p.B & 15) == 0);
   const int64_t nk = (kend - kbeg + C::BK - 1) / C::BK;
 
   // Two register staging sets: the loads of stage t + 1 are issued one
@@ -267,7 +278,7 @@ __device__ __forceinline__ void generic_mainloop(const GemmParams& p, const ALoa
 #pragma unroll
     for (int i = 0; i < C::B_CHUNKS; ++i) {
       const int c = tid + C::THREADS * i;
-      const Chunk16 v = load_chunk(p.B, p.ldb, n0 + c / C::KCH, p.N, k0 + 16 * (c % C::KCH), kend, alB);
+      const Chunk16 v = bload.load(n0 + c / C::KCH, k0 + 16 * (c % C::KCH));
       st.b[i] = u32x4v{v.w[0], v.w[1], v.w[2], v.w[3]};
     }
   };
@@ -305,18 +316,21 @@ __device__ __forceinline__ void generic_mainloop(const GemmParams& p, const ALoa
   };
   // iteration t: LDS buffer t % 2 holds stage t; the register set (t + 1) % 2
   // holds the in-flight loads of stage t + 1; stage t + 2 is loaded into the
-  // set that stage t came from.
+  // set that stage t came from.  Loads and stores are unconditional (stages
+  // past the end of K load zero chunks into a buffer nobody reads), so the
+  // loop body has no branches and the compiler's count of loads in flight
+  // stays exact across iterations: the stores of stage t + 1 wait for its
+  // own loads only, while those of stage t + 2 stay in flight.
   auto iter = [&](int64_t t, int buf, Stage& next, Stage& far) __attribute__((always_inline)) {
-    if (t + 2 < nk) gload(far, t + 2);
+    gload(far, t + 2);
     compute(buf);
-    if (t + 1 < nk) sstore(next, buf ^ 1);
+    sstore(next, buf ^ 1);
     __syncthreads();
   };
-  if (nk > 0) {
-    gload(st0, 0);
-    sstore(st0, 0);
-  }
-  if (nk > 1) gload(st1, 1);
+  if (nk <= 0) return;
+  gload(st0, 0);
+  sstore(st0, 0);
+  gload(st1, 1);
   __syncthreads();
   int64_t t = 0;
   for (; t + 1 < nk; t += 2) {
@@ -334,7 +348,8 @@ __device__ __forceinline__ void gemm_mainloop(const GemmParams& p, const ALoader
     dma_mainloop<C>(p, lds, lds + C::STAGE, lds + (C::NS > 2 ? 2 : 1) * C::STAGE, lds + (C::NS > 3 ? 3 : 1) * C::STAGE,
                     m0, n0, kbeg, kend, acc);
   } else {
-    generic_mainloop<C>(p, aload, lds, m0, n0, kbeg, kend, acc);
+    const bool alB = ((p.ldb & 15) == 0) && (((uintptr_t)p.B & 15) == 0);
+    generic_mainloop<C>(p, aload, PlainBLoader{p.B, p.ldb, p.N, kend, alB}, lds, m0, n0, kbeg, kend, acc);
   }
 }
 
