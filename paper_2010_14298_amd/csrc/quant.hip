@@ -836,43 +836,15 @@ __device__ __forceinline__ void quant_tile(const QuantParams& p, int64_t bx, int
   __shared__ float s_v0[4][QT_COLS];     // v of a group's first slot (BHQ, K >= 16)
   __shared__ int s_csum[2][4][QT_COLS];  // per-wave column code sums (transposed outputs)
 
-  // ---- load 16 rows x 4 columns, and every per-row parameter the rows
-  // need, before any store: the code stores below may alias the parameter
-  // arrays as far as the compiler knows, so loads left inside the row loop
-  // would each wait for the previous rows' stores and complete one by one
+  // ---- load 16 rows x 4 columns
   float g[QT_ROWS_PER_WAVE][4];
   int32_t srow[QT_ROWS_PER_WAVE];
-  float rsc[QT_ROWS_PER_WAVE], rze[QT_ROWS_PER_WAVE];    // per-row / per-slot scale, zero (MODE != QM_TENSOR)
-  float rsc2[QT_ROWS_PER_WAVE], rze2[QT_ROWS_PER_WAVE];  // per-row Q_b1 scale, zero (H2 == 2)
-  int rsh[QT_ROWS_PER_WAVE], rsh2[QT_ROWS_PER_WAVE];     // per-row shifts (QM_ROW with shift; H2 == 2)
 #pragma unroll
   for (int r = 0; r < QT_ROWS_PER_WAVE; ++r) {
     const int64_t slot = slot0 + r;
     const bool ok = slot < rows;
     const int32_t row = ok ? (p.perm ? p.perm[slot] : (int32_t)slot) : 0;
     srow[r] = row;
-    rsc[r] = 1.0f;
-    rze[r] = 0.0f;
-    rsh[r] = 0;
-    if constexpr (MODE != QM_TENSOR) {
-      if (ok) {
-        rsc[r] = p.scale[slot];
-        rze[r] = p.zero[slot];
-      }
-    }
-    if constexpr (MODE == QM_ROW) {
-      if (ok && p.shift) rsh[r] = p.shift[slot];
-    }
-    rsc2[r] = 0.0f;
-    rze2[r] = 0.0f;
-    rsh2[r] = 0;
-    if constexpr (H2 == 2) {
-      if (ok) {
-        rsc2[r] = p.scale2[row];
-        rze2[r] = p.zero2[row];
-        rsh2[r] = p.shift2[row];
-      }
-    }
     const float* xr = p.x + (int64_t)row * cols;
     if constexpr (VEC) {
       if (ok && lane_ok) {
@@ -902,7 +874,7 @@ __device__ __forceinline__ void quant_tile(const QuantParams& p, int64_t bx, int
       const int64_t slot = slot0 + r;
       const bool ok = slot < rows;
       const bool multi = ok && bhq_slot_kind(L, slot) != 0;
-      const float d = rsc[r];
+      const float d = ok ? p.scale[slot] : 1.0f;
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const float v = d * g[r][j];
@@ -974,15 +946,15 @@ __device__ __forceinline__ void quant_tile(const QuantParams& p, int64_t bx, int
 #pragma unroll
       for (int j = 0; j < 4; ++j) y[j] = s_t * (g[r][j] - z_t);
     } else if constexpr (MODE == QM_ROW) {
-      const float s = rsc[r];
-      const float z = rze[r];
+      const float s = ok ? p.scale[slot] : 1.0f;
+      const float z = ok ? p.zero[slot] : 0.0f;
 #pragma unroll
       for (int j = 0; j < 4; ++j) y[j] = s * (g[r][j] - z);
     } else {
       const BhqLayout& L = p.L;
       const int kind = ok ? bhq_slot_kind(L, slot) : 0;
-      const float d = rsc[r];
-      const float c = rze[r];
+      const float d = ok ? p.scale[slot] : 1.0f;
+      const float c = ok ? p.zero[slot] : 0.0f;
       if constexpr (K > 1 && K < 16) {
         // groups of K rows inside this wave: their sums from the registers
         if (r % K == 0) {
@@ -996,7 +968,7 @@ __device__ __forceinline__ void quant_tile(const QuantParams& p, int64_t bx, int
             const int64_t sl = slot + rr;
             const bool okr = sl < rows;
             const bool multi = okr && bhq_slot_kind(L, sl) != 0;
-            const float dr = rsc[r + rr];
+            const float dr = okr ? p.scale[sl] : 1.0f;
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
               const float v = dr * g[r + rr][j];
@@ -1034,7 +1006,7 @@ __device__ __forceinline__ void quant_tile(const QuantParams& p, int64_t bx, int
       rne4(y, Bf, hoff, t);
     if constexpr (MODE == QM_ROW) {
       if (p.shift && ok) {
-        const int sh = rsh[r];
+        const int sh = p.shift[slot];
 #pragma unroll
         for (int j = 0; j < 4; ++j) t[j] = shift_top(t[j], sh);
       }
@@ -1047,9 +1019,9 @@ __device__ __forceinline__ void quant_tile(const QuantParams& p, int64_t bx, int
       int sh2 = 0;
       if constexpr (H2 == 2) {
         if (ok) {
-          s2r = rsc2[r];
-          z2r = rze2[r];
-          sh2 = rsh2[r];
+          s2r = p.scale2[srow[r]];
+          z2r = p.zero2[srow[r]];
+          sh2 = p.shift2[srow[r]];
         }
       }
       float y2[4];
