@@ -1,9 +1,11 @@
 """GPU parity of fqt_conv_backward_im2col against the oracle's explicit im2col.
 
 Small shapes cover every element (stride 1 / 2, 1x1, 3x3, 7x7, ragged
-sample counts, all three gradient quantizers); the 3x3 64 -> 64 layer at
-56 x 56 with a batch of 128 (the launch configuration of the conv
-benchmark) is checked on sampled outputs computed one by one in float64.
+sample counts, all three gradient quantizers; rectangular images and
+kernels, 25- and 36-tap kernels, part K stages and column tiles); the 3x3
+64 -> 64 layer at 56 x 56 with a batch of 128 (the launch configuration of
+the conv benchmark) is checked on sampled outputs computed one by one in
+float64.
 """
 import numpy as np
 import pytest
@@ -75,6 +77,41 @@ def test_conv_ragged_batch_groups(qb_x):
     X, W, G = synth.conv_layer(seed=7, n=130, c=16, h=5, w=5, o=16, k=3, stride=1, pad=1)
     r = BW.conv_backward(X, W, G, 1, 1, qb_x=qb_x, seed=1)
     gW, gX = run(X, W, G, 1, 1, qb_x, seed=1)
+    assert rownorm_err(gW, r["grad_W64"]) <= REL_TOL
+    assert rownorm_err(gX, r["grad_X64"]) <= REL_TOL
+
+
+def conv_inputs(seed, n, c, h, w, o, kh, kw, stride, pad):
+    """Rectangular images and kernels (the synthetic generator makes square
+    ones): X half-normal NHWC, W He-init [o, kh, kw, c], G per-sample
+    log-normal scales."""
+    rng = np.random.default_rng(seed)
+    X = np.maximum(rng.standard_normal((n, h, w, c)), 0.0).astype(np.float32)
+    W = (rng.standard_normal((o, kh, kw, c)) * np.sqrt(2.0 / (kh * kw * c))).astype(np.float32)
+    ho = (h + 2 * pad - kh) // stride + 1
+    wo = (w + 2 * pad - kw) // stride + 1
+    G = synth.lognormal_row_gradient(rng, n, ho * wo * o).reshape(n, ho, wo, o)
+    return X, W, G
+
+
+GEOMETRIES = [
+    # n, c, h, w, o, kh, kw, stride, pad
+    (3, 8, 9, 7, 16, 5, 5, 1, 2),    # 25 taps, rectangular image
+    (4, 8, 6, 5, 16, 1, 3, 1, 1),    # 1 x 3 kernel
+    (4, 8, 5, 7, 16, 3, 1, 1, 0),    # 3 x 1 kernel, no padding
+    (3, 8, 7, 7, 16, 3, 3, 1, 0),    # valid 3 x 3
+    (3, 24, 6, 6, 48, 3, 3, 1, 1),   # K = 432: a part K stage; 24 input channels: a part column tile
+    (2, 8, 8, 8, 16, 6, 6, 1, 2),    # 36 taps: the general grad_X gather at stride 1
+]
+
+
+@pytest.mark.parametrize("geo", GEOMETRIES)
+@pytest.mark.parametrize("qb_x", [("bhq", 5, 2), ("psq", 6, 0)])
+def test_conv_geometries(geo, qb_x):
+    n, c, h, w, o, kh, kw, st, pad = geo
+    X, W, G = conv_inputs(sum(geo), n, c, h, w, o, kh, kw, st, pad)
+    r = BW.conv_backward(X, W, G, st, pad, qb_x=qb_x, seed=5)
+    gW, gX = run(X, W, G, st, pad, qb_x, seed=5)
     assert rownorm_err(gW, r["grad_W64"]) <= REL_TOL
     assert rownorm_err(gX, r["grad_X64"]) <= REL_TOL
 
