@@ -422,15 +422,19 @@ __global__ __launch_bounds__(RK_THREADS) void bhq_rank_perm_kernel(const float* 
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
   const int rows = (int)L.rows;
   const int npad = (int)rank_pad(rows);
-  // all loads of a round in flight before the LDS stores
+  // all loads of a round in flight before the LDS stores: the loads are
+  // unconditional (indices past the end are clamped to the last row and
+  // their keys replaced below), since a load under a branch makes the
+  // compiler wait for each one before issuing the next
   constexpr int U = 16;
   for (int base = 0; base < npad; base += RK_THREADS * U) {
     float lo[U], hi[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int e = base + t + u * RK_THREADS;
-      lo[u] = e < rows ? rmin[e] : 0.0f;
-      hi[u] = e < rows ? rmax[e] : 0.0f;
+      const int ec = e < rows ? e : rows - 1;
+      lo[u] = rmin[ec];
+      hi[u] = rmax[ec];
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
