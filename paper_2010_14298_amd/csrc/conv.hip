@@ -321,10 +321,20 @@ __global__ __launch_bounds__(256) void conv_xtapsum_kernel(ConvGeom g, const int
   const int32_t* x = xs + (int64_t)c * g.h * g.w;
   const int wx = xhi - xlo, cnt = (yhi - ylo) * wx;
   int sum = 0;
-  for (int i = threadIdx.x; i < cnt; i += blockDim.x) {
-    const int dy = i / wx;
-    const int iy = (ylo + dy) * g.stride - g.pad + r, ix = (xlo + i - dy * wx) * g.stride - g.pad + s;
-    sum += x[(int64_t)iy * g.w + ix];
+  // eight loads in flight per round: indices past cnt are clamped (their
+  // values dropped), so no load sits under a branch
+  for (int i0 = threadIdx.x; i0 < cnt; i0 += 8 * blockDim.x) {
+    int v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int i = min(i0 + u * (int)blockDim.x, cnt - 1);
+      const int dy = i / wx;
+      const int iy = (ylo + dy) * g.stride - g.pad + r, ix = (xlo + i - dy * wx) * g.stride - g.pad + s;
+      v[u] = x[(int64_t)iy * g.w + ix];
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      if (i0 + u * (int)blockDim.x < cnt) sum += v[u];
   }
   __shared__ int ssum[4];
   sum = wave_sum4_i(sum);
@@ -358,9 +368,18 @@ __global__ __launch_bounds__(256) void conv_tapsum_kernel(ConvGeom g, const int3
   const int32_t* q = qs + (int64_t)o * g.ho * g.wo;
   const int wx = xhi - xlo, cnt = (yhi - ylo) * wx;
   int sum = 0;
-  for (int i = threadIdx.x; i < cnt; i += blockDim.x) {
-    const int dy = i / wx;
-    sum += q[(int64_t)(ylo + dy) * g.wo + xlo + (i - dy * wx)];
+  // eight loads in flight per round (clamped indices, values past cnt dropped)
+  for (int i0 = threadIdx.x; i0 < cnt; i0 += 8 * blockDim.x) {
+    int v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int i = min(i0 + u * (int)blockDim.x, cnt - 1);
+      const int dy = i / wx;
+      v[u] = q[(int64_t)(ylo + dy) * g.wo + xlo + (i - dy * wx)];
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      if (i0 + u * (int)blockDim.x < cnt) sum += v[u];
   }
   __shared__ int ssum[4];
   sum = wave_sum4_i(sum);
@@ -412,7 +431,16 @@ __global__ void conv_sg_kernel(ConvGeom g, const int8_t* q2, int32_t* sg) {
   const int8_t* src = q2 + ((int64_t)slot * howo + pix) * g.o;  // Q_b2 rows are slot-major [slot][pix][o]
   int sum = 0;
   if ((g.o & 15) == 0 && ((uintptr_t)q2 & 15) == 0) {
-    for (int o = 0; o < g.o; o += 16) {
+    // 64 channels (four loads in flight) per step, then 16 at a time
+    int o = 0;
+    for (; o + 64 <= g.o; o += 64) {
+      uint4 v[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) v[u] = *reinterpret_cast<const uint4*>(src + o + 16 * u);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) sum = sum4_i8(v[u].x, sum4_i8(v[u].y, sum4_i8(v[u].z, sum4_i8(v[u].w, sum))));
+    }
+    for (; o < g.o; o += 16) {
       const uint4 v = *reinterpret_cast<const uint4*>(src + o);
       sum = sum4_i8(v.x, sum4_i8(v.y, sum4_i8(v.z, sum4_i8(v.w, sum))));
     }
