@@ -393,18 +393,27 @@ __global__ __launch_bounds__(256) void conv_tapsum_kernel(ConvGeom g, const int3
 
 // split-K reduction of grad_W with the per-tap masked zero-point expansion:
 // out[o][(tap, c)] = dA dB acc + dA zB sumA_tap[o][tap] + zA dB sumB[(tap, c)] + count[tap] zA zB
-__global__ void conv_gradw_reduce_kernel(GemmParams p, ConvGeom g, const int32_t* sumA_tap, const int32_t* count_tap) {
-  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+// A block takes 64 outputs; its wave w sums splits w, w + 4, ... with eight
+// loads in flight, and the four wave sums meet in LDS (integers: any order
+// gives the same sum).  Lanes past the end load a clamped index and store
+// nothing, so the loads sit under no branch.
+__global__ __launch_bounds__(256) void conv_gradw_reduce_kernel(GemmParams p, ConvGeom g, const int32_t* sumA_tap,
+                                                                const int32_t* count_tap) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int64_t idx = (int64_t)blockIdx.x * 64 + lane;
   const int64_t MN = p.M * p.N;
-  if (idx >= MN) return;
-  // eight independent partial sums keep the split loads in flight (integers: any order)
+  const int64_t ic = idx < MN ? idx : MN - 1;
   int64_t s8[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-  int sp = 0;
-  for (; sp + 8 <= p.splits; sp += 8)
+  int sp = wave;
+  for (; sp + 28 < p.splits; sp += 32)
 #pragma unroll
-    for (int u = 0; u < 8; ++u) s8[u] += (int64_t)p.part[(int64_t)(sp + u) * MN + idx];
-  for (; sp < p.splits; ++sp) s8[0] += (int64_t)p.part[(int64_t)sp * MN + idx];
-  const int64_t sum = ((s8[0] + s8[1]) + (s8[2] + s8[3])) + ((s8[4] + s8[5]) + (s8[6] + s8[7]));
+    for (int u = 0; u < 8; ++u) s8[u] += (int64_t)p.part[(int64_t)(sp + 4 * u) * MN + ic];
+  for (; sp < p.splits; sp += 4) s8[0] += (int64_t)p.part[(int64_t)sp * MN + ic];
+  __shared__ int64_t swave[4][64];
+  swave[wave][lane] = ((s8[0] + s8[1]) + (s8[2] + s8[3])) + ((s8[4] + s8[5]) + (s8[6] + s8[7]));
+  __syncthreads();
+  if (wave != 0 || idx >= MN) return;
+  const int64_t sum = (swave[0][lane] + swave[1][lane]) + (swave[2][lane] + swave[3][lane]);
   const int64_t row = idx / p.N, col = idx % p.N;
   const int taps = g.kh * g.kw;
   const int tap = (int)(col / g.c);
@@ -834,7 +843,8 @@ hipError_t launch_conv_tapsums(const ConvGeom& g, const int8_t* q1_t, int64_t ld
 hipError_t launch_conv_gradw_reduce(const GemmParams& p, const ConvGeom& g, const int32_t* sumA_tap,
                                     const int32_t* count_tap, hipStream_t s) {
   const int64_t MN = p.M * p.N;
-  hipLaunchKernelGGL(conv_gradw_reduce_kernel, dim3((unsigned)((MN + 255) / 256)), dim3(256), 0, s, p, g, sumA_tap,
+  if (MN < 1 || (MN + 63) / 64 > 0x7FFFFFFF) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(conv_gradw_reduce_kernel, dim3((unsigned)((MN + 63) / 64)), dim3(256), 0, s, p, g, sumA_tap,
                      count_tap);
   return hipGetLastError();
 }
