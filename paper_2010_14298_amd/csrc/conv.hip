@@ -625,7 +625,7 @@ struct ConvRowStage {
   int orow;      // output pixel row (sample * h * w + pixel), -1 if none
 };
 
-using CfgConvX = TileCfg<128, 64, 64, 64, 64>;  // 64-code K stages, 38 KB of LDS: four blocks per CU
+using CfgConvX = TileCfg<128, 64, 64, 64, 64>;  // 64-code K stages, 36 KB of LDS: four blocks per CU
 
 template <int EPI, int KG, class XLoader>
 __global__ __launch_bounds__(256) void conv_gradx_kernel(GemmParams p, ConvGeom g, const int8_t* q2, const int32_t* sg,

@@ -83,13 +83,14 @@ __device__ __forceinline__ int64_t xcd_tile(int64_t id, int64_t ntiles) {
 
 // The K loops.  The fast one (dma_mainloop below) requires 16-byte aligned
 // rows and a K range that is a whole number of 128-byte stages.  The generic
-// one (register-staged, two LDS buffers) takes the A operand through
-// `aload(row, k)` (a 16-byte chunk, zero outside the operand), which is how
-// the conv input-gradient contraction gathers its implicit im2col rows, and
-// handles ragged K and unaligned rows.  A loader maps a row once to a
-// per-row state (`row`), then loads 16-byte chunks of it (`load`) stage by
-// stage, so per-row index arithmetic stays out of the K loop; a thread's
-// chunks of one stage share their K offset, decoded once (`kstate`).
+// one (register-staged, two LDS buffers) takes both operands through loaders
+// (16-byte chunks, zero outside the operand and past the end of K, where the
+// loop also loads), which is how the conv input-gradient contraction gathers
+// its implicit im2col rows, and handles ragged K and unaligned rows.  An A
+// loader maps a row once to a per-row state (`row`), then loads 16-byte
+// chunks of it (`load`) stage by stage, so per-row index arithmetic stays out
+// of the K loop; a thread's chunks of one stage share their K offset, decoded
+// once (`kstate`).
 struct PlainALoader {
   const int8_t* A;
   int64_t lda, M, kend;
