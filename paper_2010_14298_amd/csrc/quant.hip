@@ -1148,12 +1148,10 @@ __global__ __launch_bounds__(256) void quant_tile2_kernel(QuantParams p0, QuantP
 // period-th block (while they last) is an X / W tile, so that those
 // memory-light tiles interleave with the arithmetic-heavy gradient tiles;
 // the other blocks take the gradient tiles in order.
-// Five waves per SIMD (96 registers, four of them spilled): measured faster
-// than four waves without spills.
 template <int MODE, int K, int H2>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5))) void quant_fused_kernel(
-    QuantParams pg, QuantParams px, QuantParams pw, int64_t nbx, int64_t nbw, int64_t period, int64_t ctg, int64_t ctx,
-    int64_t ctw) {
+__global__ __launch_bounds__(256) void quant_fused_kernel(QuantParams pg, QuantParams px, QuantParams pw, int64_t nbx,
+                                                          int64_t nbw, int64_t period, int64_t ctg, int64_t ctx,
+                                                          int64_t ctw) {
   const int64_t b = blockIdx.x;
   const int64_t nxw = nbx + nbw;
   if (b % period == period - 1 && b / period < nxw) {
