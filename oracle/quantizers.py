@@ -21,17 +21,18 @@ design notes of the repository):
   * PSQ zero point is the row minimum (by analogy with PTQ);
   * BHQ with a fixed block size k: G = ceil(N/k) groups; group g takes the
     g-th largest row plus the next k-1 rows of the sorted tail, in order;
+  * BHQ with adaptive groups (App. D, step 2): every number of groups G from
+    1 to N is tried; group i takes the i-th largest row plus n_i small rows,
+    n_i proportional to M_i with cumulative rounding (appd_small_counts),
+    small rows in sorted order; each candidate is scored by the exact
+    |S^-1|_F^2 of the plan it builds and the least wins (ties: fewer groups);
   * BHQ zero point: one offset c_g per group in the transformed domain,
     c_g = alpha s1 min(large row) - lambda2 s2 sqrt(k) / 2, which App. C.4's
     range bound places at the bottom of the transformed values;
   * lambda1 = 0 takes lambda2; lambda2 = 0 gives s2 = s1 = B sqrt(k)/lambda1;
     both zero give s1 = s2 = 1; a one-row group is a PSQ row;
   * cube roots are correctly rounded float32; the group column sum adds the
-    slots in aligned chunks of min(k, 16), each chunk left to right, then the
-    chunk sums left to right;
-  * adaptive grouping (App. D): the block size among 1, 2, 4, .., 64 whose
-    plan has the least |S^-1|_F^2 (App. D's own estimate always selects one
-    group; see bhq_adaptive_block).
+    group's slots one at a time in slot order (float32).
 
 Offset codes (what the int8 contractions consume) are code - 2^(b-1).
 """
@@ -43,7 +44,6 @@ import numpy as np
 from . import sr
 
 FLT_MAX = float(np.finfo(np.float32).max)
-CHUNK = 16          # slots per partial column sum in the BHQ group sum
 
 
 def n_bins(bits):
@@ -227,57 +227,90 @@ def bhq_groups(N, k):
     return G, sizes
 
 
-def bhq_plan(x, bits, k):
-    """Sort, grouping and per-group scalars of the block Householder quantizer.
+_cbrt_cache = {}
 
-    Sec. 4.2 / App. D: sort the row infinity norms M_i in descending order
-    (ties: lower row index first); the first G rows are the large rows.
-    App. C.4: s1 = B k^(1/6) lambda1^(-1/3) / (lambda1^(2/3) k^(-1/3) +
-    lambda2^(2/3) k^(2/3)) and likewise s2 with lambda2^(-1/3); multiplying
-    through by k^(1/3) gives the form evaluated here, s1 = B sqrt(k) /
-    (a (a^2 + c^2 k)), s2 = B sqrt(k) / (c (a^2 + c^2 k)), a = lambda1^(1/3),
-    c = lambda2^(1/3).
+
+def _cbrt(v):
+    """cbrt_rn, remembered per float32 value (the App. D search reuses them)."""
+    key = float(v)
+    r = _cbrt_cache.get(key)
+    if r is None:
+        r = _cbrt_cache[key] = float(cbrt_rn(np.float32(v)))
+    return r
+
+
+def group_scales(lam1, lam2, kg, B):
+    """s1, s2 of a group of kg >= 2 rows (App. C.4), float32.
+
+    s1 = B sqrt(k) / (a (a^2 + c^2 k)), s2 = B sqrt(k) / (c (a^2 + c^2 k)) with
+    a = lambda1^(1/3), c = lambda2^(1/3): the closed form of App. C.4
+    multiplied through by k^(1/3).  lambda1 = 0 takes lambda2; lambda2 = 0
+    gives s1 = s2 = B sqrt(k) / lambda1; both zero give 1.  Returns
+    (lambda1 as used, s1, s2, sqrt(k)).
     """
+    lam1, lam2 = np.float32(lam1), np.float32(lam2)
+    if lam1 == 0:
+        lam1 = lam2
+    sk = math.sqrt(float(kg))
+    if lam1 == 0 and lam2 == 0:
+        s1 = s2 = np.float32(1.0)
+    elif lam2 == 0:
+        s1 = s2 = to_f32_sat((float(B) * sk) / float(lam1))
+    else:
+        a = _cbrt(lam1)
+        c = _cbrt(lam2)
+        t = a * a + (c * c) * float(kg)
+        num = float(B) * sk
+        s1 = to_f32_sat(num / (a * t))
+        s2 = to_f32_sat(num / (c * t))
+    return lam1, s1, s2, sk
+
+
+def group_term(s1, s2, kg):
+    """A group's share of |S^-1|_F^2 (Eq. matrix-quantizer-variance): S^-1 of
+    the group is diag(s1, s2, .., s2)^-1 times an orthogonal reflection, so
+    1/s1^2 + (k_g - 1)/s2^2 (a one-row group: 1/s^2), in float64."""
+    s1 = float(s1)
+    term = 1.0 / (s1 * s1)
+    if kg > 1:
+        s2 = float(s2)
+        term = term + float(kg - 1) * (1.0 / (s2 * s2))
+    return term
+
+
+def _sorted_rows(x):
+    """Row statistics and the order of Sec. 4.2 / App. D: M descending, ties by
+    row index ascending."""
+    mn, mx, R, M = row_stats(x)
+    order = np.lexsort((np.arange(len(M)), -M))
+    return mn, R, M, order
+
+
+def _build_plan(x, bits, order, members_list):
+    """Per-slot scales and zero points of a BHQ plan whose groups (each a list of
+    original rows, large row first) are given in slot order."""
     x = np.asarray(x, dtype=np.float32)
     N, D = x.shape
     B = n_bins(bits)
     mn, mx, R, M = row_stats(x)
-    order = np.lexsort((np.arange(N), -M))          # M descending, index ascending
-    G, sizes = bhq_groups(N, k)
     perm, group_off = [], [0]
     scale = np.zeros(N, np.float32)
     zero = np.zeros(N, np.float32)
     groups = []
-    for g in range(G):
-        small = order[G + g * (k - 1): G + g * (k - 1) + sizes[g] - 1]
-        members = [int(order[g])] + [int(i) for i in small]
+    for members in members_list:
         base = len(perm)
         perm.extend(members)
         group_off.append(len(perm))
         kg = len(members)
-        info = dict(members=members, base=base, size=kg)
+        info = dict(members=list(members), base=base, size=kg)
         if kg == 1:
             i = members[0]
             scale[base] = scale_from_range(R[i], B)
             zero[base] = mn[i]
         else:
             big = members[0]
-            lam1 = np.float32(R[big])
             lam2 = np.float32(np.float32(2.0) * np.float32(M[members[1:]].max()))
-            if lam1 == 0:
-                lam1 = lam2
-            sk = math.sqrt(float(kg))
-            if lam1 == 0 and lam2 == 0:
-                s1 = s2 = np.float32(1.0)
-            elif lam2 == 0:
-                s1 = s2 = to_f32_sat((float(B) * sk) / float(lam1))
-            else:
-                a = float(cbrt_rn(lam1))
-                c = float(cbrt_rn(lam2))
-                t = a * a + (c * c) * float(kg)
-                num = float(B) * sk
-                s1 = to_f32_sat(num / (a * t))
-                s2 = to_f32_sat(num / (c * t))
+            lam1, s1, s2, sk = group_scales(R[big], lam2, kg, B)
             alpha = np.float32(1.0 / sk)
             oma = np.float32(np.float32(1.0) - alpha)
             cg = np.float32(((float(alpha) * float(s1)) * float(mn[big]))
@@ -288,23 +321,160 @@ def bhq_plan(x, bits, k):
             info.update(lam1=lam1, lam2=lam2, s1=s1, s2=s2, alpha=alpha, oma=oma, cg=cg, sk=sk)
         groups.append(info)
     return dict(perm=np.array(perm, np.int64), group_off=np.array(group_off, np.int64),
-                scale=scale, zero=zero, groups=groups, G=G, k=k, bits=int(bits), sorted=order)
+                scale=scale, zero=zero, groups=groups, G=len(members_list), bits=int(bits), sorted=order)
 
 
-def group_column_sum(v, k):
-    """Column sums of a group's scaled rows v [k_g, D] (float32).
+def bhq_plan(x, bits, k):
+    """Sort, grouping and per-group scalars of the block Householder quantizer
+    with a fixed block size k >= 1.
 
-    Slots are added in aligned chunks of min(k, 16): each chunk left to right,
-    then the chunk sums left to right.  Slots past k_g count as zero.
+    Sec. 4.2 / App. D: sort the row infinity norms M_i in descending order
+    (ties: lower row index first); the first G = ceil(N/k) rows are the large
+    rows; group g takes the g-th large row and the next k-1 rows of the sorted
+    tail.  Scalars per group: group_scales.
     """
-    ch = min(k, CHUNK)
-    kg, D = v.shape
-    S = None
-    for c0 in range(0, max(kg, 1), ch):
-        P = np.zeros(D, np.float32)
-        for p in range(c0, min(kg, c0 + ch)):
-            P = (P + v[p]).astype(np.float32)
-        S = P if S is None else (S + P).astype(np.float32)
+    x = np.asarray(x, dtype=np.float32)
+    N = x.shape[0]
+    order = _sorted_rows(x)[3]
+    G, sizes = bhq_groups(N, k)
+    members_list, t = [], G
+    for g in range(G):
+        members_list.append([int(order[g])] + [int(i) for i in order[t: t + sizes[g] - 1]])
+        t += sizes[g] - 1
+    plan = _build_plan(x, bits, order, members_list)
+    plan["k"] = int(k)
+    return plan
+
+
+# ----------------------------------------------------------------------------
+# App. D: adaptive grouping
+# ----------------------------------------------------------------------------
+
+def appd_prefix(M_sorted):
+    """P_i = M_(1) + .. + M_(i) of the sorted infinity norms, float64, added one
+    at a time in sorted order; P_0 = 0."""
+    P = [0.0]
+    for m in M_sorted:
+        P.append(P[-1] + float(m))
+    return P
+
+
+def appd_small_counts(P, N, G):
+    """Number of small rows n_1..n_G of each group for G groups (App. D, step 2).
+
+    App. D sizes the i-th group's share of the N - G small rows in proportion
+    to M_i: (N - G) M_i / sum_{j<=G} M_j, which is fractional.  Rounded
+    cumulatively: with q_i = (N - G) P_i / P_G (float64: product, then
+    quotient), the first i groups take c_i = floor(q_i + 1/2) small rows
+    (c_G = N - G), so n_i = c_i - c_(i-1) >= 0 and the counts add up to N - G.
+    If the G largest norms are all zero, P_i is replaced by i.
+    """
+    small = N - G
+    S = P[G]
+    counts, prev = [], 0
+    for i in range(1, G + 1):
+        if i == G:
+            c = small
+        else:
+            q = (float(small) * P[i]) / S if S > 0 else float(small * i) / float(G)
+            c = min(int(math.floor(q + 0.5)), small)
+        counts.append(c - prev)
+        prev = c
+    return counts
+
+
+def appd_members(order, G, counts):
+    """Groups for G: group i is the i-th largest row, then its n_i small rows
+    taken from the sorted tail in order."""
+    members_list, t = [], G
+    for i in range(G):
+        members_list.append([int(order[i])] + [int(r) for r in order[t: t + counts[i]]])
+        t += counts[i]
+    return members_list
+
+
+def appd_objective(R, M, order, P, bits, G):
+    """|S^-1|_F^2 of the App. D plan with G groups: the sum over groups of
+    group_term, float64, added in group order.  A group's lambda1 is its large
+    row's range and lambda2 twice the largest infinity norm of its small rows
+    (the first of them: they come in sorted order)."""
+    N = len(order)
+    B = n_bins(bits)
+    counts = appd_small_counts(P, N, G)
+    total, t = 0.0, G
+    for i in range(G):
+        big = order[i]
+        n = counts[i]
+        if n == 0:
+            s = scale_from_range(R[big], B)
+            term = group_term(s, s, 1)
+        else:
+            lam2 = np.float32(np.float32(2.0) * M[order[t]])
+            _, s1, s2, _ = group_scales(R[big], lam2, n + 1, B)
+            term = group_term(s1, s2, n + 1)
+        total = total + term
+        t += n
+    return total
+
+
+def bhq_appd(x, bits):
+    """App. D, step 2: loop over the number of groups G = 1..N and keep the G
+    whose plan has the least |S^-1|_F^2 (ties: the smaller G).
+
+    App. D's own estimate of the objective, sum_i M_i^2 / ((N - G) M_i / sum M),
+    equals (sum of the G largest M)^2 / (N - G), which grows with G, so read
+    literally it always keeps one group; here every candidate is scored by the
+    exact factor |S^-1|_F^2 of the variance bound (D/4)|S^-1|_F^2 (Eq.
+    matrix-quantizer-variance) of the plan App. D's sizes build.
+    Returns (G, [objective for G = 1..N]).
+    """
+    x = np.asarray(x, dtype=np.float32)
+    N = x.shape[0]
+    _, R, M, order = _sorted_rows(x)
+    P = appd_prefix(M[order])
+    obj = [appd_objective(R, M, order, P, bits, G) for G in range(1, N + 1)]
+    best = 1
+    for G in range(2, N + 1):
+        if obj[G - 1] < obj[best - 1]:
+            best = G
+    return best, obj
+
+
+def bhq_appd_plan(x, bits, G=None):
+    """The App. D plan: G groups (bhq_appd's choice when G is None)."""
+    x = np.asarray(x, dtype=np.float32)
+    N = x.shape[0]
+    if G is None:
+        G = bhq_appd(x, bits)[0]
+    _, R, M, order = _sorted_rows(x)
+    counts = appd_small_counts(appd_prefix(M[order]), N, G)
+    plan = _build_plan(x, bits, order, appd_members(order, G, counts))
+    plan["k"] = 0
+    return plan
+
+
+def bhq_scale_norm(plan):
+    """|S^-1|_F^2 of a BHQ plan, the factor of the variance bound (D/4)|S^-1|_F^2
+    (Eq. matrix-quantizer-variance): group_term summed over groups in slot
+    order, float64."""
+    total = 0.0
+    for info in plan["groups"]:
+        base, kg = info["base"], info["size"]
+        s2 = plan["scale"][base + 1] if kg > 1 else plan["scale"][base]
+        total = total + group_term(plan["scale"][base], s2, kg)
+    return total
+
+
+# ----------------------------------------------------------------------------
+# BHQ transform and quantizer
+# ----------------------------------------------------------------------------
+
+def group_column_sum(v):
+    """Column sums of a group's scaled rows v [k_g, D], float32, adding the
+    slots one at a time in slot order."""
+    S = np.zeros(v.shape[1], np.float32)
+    for p in range(v.shape[0]):
+        S = (S + v[p]).astype(np.float32)
     return S
 
 
@@ -319,7 +489,7 @@ def bhq_transform(rows, info):
     kg = info["size"]
     d = np.array([info["s1"]] + [info["s2"]] * (kg - 1), np.float32)
     v = (d[:, None] * rows).astype(np.float32)
-    S = group_column_sum(v, info["k"])
+    S = group_column_sum(v)
     alpha, oma = np.float32(info["alpha"]), np.float32(info["oma"])
     m = (alpha * S).astype(np.float32)
     m = (m - v[0]).astype(np.float32)
@@ -332,8 +502,8 @@ def bhq_transform(rows, info):
 
 
 def quantize_bhq(x, bits, k, seed=0, stream=0, plan=None):
-    """Block Householder quantizer with fixed block size k (Sec. 4.2); k = 0
-    takes the adaptive block size of bhq_adaptive_block (App. D).
+    """Block Householder quantizer (Sec. 4.2) with a fixed block size k >= 1, or
+    with App. D's adaptive groups for k = 0.
 
     Codes are returned in slot order (group by group); the SR draw of slot p,
     column j uses element index perm[p] * cols + j (its original position).
@@ -341,14 +511,11 @@ def quantize_bhq(x, bits, k, seed=0, stream=0, plan=None):
     x = np.asarray(x, dtype=np.float32)
     N, D = x.shape
     B = n_bins(bits)
-    if k == 0:
-        k = plan["k"] if plan is not None else bhq_adaptive_block(x, bits)[0]
     if plan is None:
-        plan = bhq_plan(x, bits, k)
+        plan = bhq_appd_plan(x, bits) if k == 0 else bhq_plan(x, bits, k)
     code = np.zeros((N, D), np.int64)
     cols = np.arange(D, dtype=np.uint64)
     for info in plan["groups"]:
-        info = dict(info, k=k)
         mem = info["members"]
         base, kg = info["base"], info["size"]
         rows = x[mem]
@@ -361,49 +528,7 @@ def quantize_bhq(x, bits, k, seed=0, stream=0, plan=None):
         u = sr.uniform24(e, seed, stream)
         code[base: base + kg] = sr.round_stochastic(y, u, B)
     return dict(kind="bhq", code=code, scale=plan["scale"], zero=plan["zero"], perm=plan["perm"],
-                group_off=plan["group_off"], bits=int(bits), plan=plan, k=k)
-
-
-# Candidate block sizes of the adaptive grouping (groups of at most 64 rows
-# that start at multiples of their size, the layout the fixed-block plan uses).
-ADAPTIVE_BLOCKS = (1, 2, 4, 8, 16, 32, 64)
-
-
-def bhq_scale_norm(plan):
-    """|S^-1|_F^2 of a BHQ plan, the factor of the variance bound (D/4)|S^-1|_F^2
-    (Eq. matrix-quantizer-variance).  S^-1 of a group is diag(s1, s2, .., s2)^-1
-    times an orthogonal reflection, so a group adds 1/s1^2 + (k_g - 1)/s2^2 (a
-    one-row group 1/s^2).  float64; groups added in slot order, left to right.
-    """
-    total = 0.0
-    for info in plan["groups"]:
-        base, kg = info["base"], info["size"]
-        s1 = float(plan["scale"][base])
-        term = 1.0 / (s1 * s1)
-        if kg > 1:
-            s2 = float(plan["scale"][base + 1])
-            term = term + float(kg - 1) * (1.0 / (s2 * s2))
-        total = total + term
-    return total
-
-
-def bhq_adaptive_block(x, bits):
-    """Block size of the adaptive grouping (App. D, step 2).
-
-    App. D loops over the number of groups and keeps the grouping of least
-    estimated variance.  Its estimate, sum_i M_i^2 / ((N - G) M_i / sum M),
-    equals (sum of the G largest M)^2 / (N - G), which grows with G, so read
-    literally it always keeps one group.  Here the estimate is the exact bound
-    factor |S^-1|_F^2 of each candidate plan, and the candidates are the
-    fixed-block plans with k in ADAPTIVE_BLOCKS (G = ceil(N / k)).  Ties go to
-    the larger block (fewer groups).  Returns (k, {k: |S^-1|_F^2}).
-    """
-    obj = {k: bhq_scale_norm(bhq_plan(x, bits, k)) for k in ADAPTIVE_BLOCKS}
-    best = ADAPTIVE_BLOCKS[0]
-    for k in ADAPTIVE_BLOCKS[1:]:
-        if obj[k] <= obj[best]:
-            best = k
-    return best, obj
+                group_off=plan["group_off"], bits=int(bits), plan=plan, k=plan["k"], G=plan["G"])
 
 
 def dequantize_bhq(q):

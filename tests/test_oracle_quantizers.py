@@ -14,6 +14,7 @@
 import decimal
 import itertools
 import math
+from fractions import Fraction
 
 import numpy as np
 import pytest
@@ -296,7 +297,24 @@ def test_monte_carlo_mean_and_variance(kind):
 
 
 # ---------------------------------------------------------------------------
-# adaptive grouping (App. D): pins of the block-size choice
+# group column sum: one slot at a time, in slot order
+# ---------------------------------------------------------------------------
+def test_group_column_sum_is_sequential_in_slot_order():
+    # float32 values whose sum depends on the order of addition (the spacing
+    # of float32 at 1e8 is 8): ((1e8 + 1) - 1e8) + 1 = (1e8 - 1e8) + 1 = 1,
+    # whereas pairs (1e8 + 1) + (-1e8 + 1) = 1e8 - 1e8 = 0, and the reverse
+    # order ((1 - 1e8) + 1) + 1e8 = 0
+    v = np.float32([[1e8], [1.0], [-1e8], [1.0]])
+    assert Q.group_column_sum(v)[0] == np.float32(1.0)
+    assert Q.group_column_sum(v[::-1])[0] == np.float32(0.0)
+    # 20 slots (more than one 16-slot chunk): a chunked sum would give 0 here
+    w = np.zeros((20, 1), np.float32)
+    w[0], w[1], w[16], w[17] = 1e8, 1.0, -1e8, 1.0
+    assert Q.group_column_sum(w)[0] == np.float32(1.0)
+
+
+# ---------------------------------------------------------------------------
+# App. D grouping: pins against explicit matrices and brute force
 # ---------------------------------------------------------------------------
 @pytest.mark.parametrize("k", [1, 2, 8, 64])
 def test_bhq_scale_norm_is_the_explicit_bound(k):
@@ -309,42 +327,188 @@ def test_bhq_scale_norm_is_the_explicit_bound(k):
     assert Q.bhq_scale_norm(q["plan"]) == pytest.approx(4.0 / D * theory.matrix_var_bound(q, D), rel=1e-12)
 
 
-def test_adaptive_block_keeps_per_row_scales_for_equal_rows():
-    # identical rows: lambda2 = 2 max|row| >= lambda1 = R, so a group of k rows
-    # costs at least (1 + k)^2 R^2 / B^2 > k R^2 / B^2 (App. C.4): PSQ (k = 1) wins
+def explicit_inverse_norm(plan):
+    """|S^-1|_F^2 by inverting the explicit N x N block-diagonal scale matrix
+    S = blockdiag(H_g diag(d_g)) of a plan (numpy's LU inverse)."""
+    N = len(plan["perm"])
+    S = np.zeros((N, N))
+    for info in plan["groups"]:
+        b, kg = info["base"], info["size"]
+        d = plan["scale"][b: b + kg].astype(np.float64)
+        Hk = theory.householder_matrix(kg) if kg > 1 else np.eye(1)
+        S[b: b + kg, b: b + kg] = Hk @ np.diag(d)
+    return float((np.linalg.inv(S) ** 2).sum())
+
+
+def tiny_cases():
+    rng = np.random.default_rng(21)
+    cases = []
+    for n in range(1, 9):
+        for t in range(3):
+            x = (rng.lognormal(0, 2, (n, 1)) * rng.standard_normal((n, 5))).astype(np.float32)
+            cases.append(x)
+    x = (0.01 * rng.standard_normal((8, 5))).astype(np.float32)
+    x[3] = 50 * rng.standard_normal(5)                 # one outlier
+    cases.append(x)
+    x = rng.standard_normal((7, 4)).astype(np.float32)
+    x[[1, 4]] = x[0]                                   # tied norms
+    cases.append(x)
+    return cases
+
+
+def exact_counts(M_sorted, G):
+    """App. D's cumulative rounding in exact rational arithmetic: the first i
+    groups take round((N - G) P_i / P_G) small rows (None near a half-integer)."""
+    N = len(M_sorted)
+    P = [Fraction(0)]
+    for m in M_sorted:
+        P.append(P[-1] + Fraction(float(m)))
+    out, prev = [], 0
+    for i in range(1, G + 1):
+        q = Fraction(N - G) * P[i] / P[G] if P[G] > 0 else Fraction((N - G) * i, G)
+        frac = q - math.floor(q)
+        if abs(frac - Fraction(1, 2)) < Fraction(1, 10 ** 9):
+            return None
+        c = math.floor(q + Fraction(1, 2))
+        out.append(c - prev)
+        prev = c
+    return out
+
+
+def test_appd_counts_are_the_proportional_cumulative_rounding():
+    for x in tiny_cases() + [heavy_rows(22, 60, 3)]:
+        N = x.shape[0]
+        M = np.abs(x).max(axis=1)
+        Ms = np.sort(M)[::-1]
+        P = Q.appd_prefix(Ms)
+        for G in range(1, N + 1):
+            n = Q.appd_small_counts(P, N, G)
+            assert len(n) == G and min(n) >= 0 and sum(n) == N - G
+            ref = exact_counts(Ms, G)
+            if ref is not None:
+                assert n == ref, (N, G, n, ref)
+
+
+def test_appd_objective_is_the_explicit_inverse_norm():
+    # for every G, the objective App. D scores equals |S^-1|_F^2 of the plan
+    # it builds, with S assembled explicitly and inverted
+    for x in tiny_cases():
+        N = x.shape[0]
+        _, obj = Q.bhq_appd(x, 4)
+        for G in range(1, N + 1):
+            plan = Q.bhq_appd_plan(x, 4, G)
+            assert plan["G"] == G
+            assert obj[G - 1] == pytest.approx(explicit_inverse_norm(plan), rel=1e-11)
+
+
+def compositions(total, parts):
+    if parts == 1:
+        yield (total,)
+        return
+    for first in range(total + 1):
+        for rest in compositions(total - first, parts - 1):
+            yield (first,) + rest
+
+
+def test_appd_choice_brute_force_over_contiguous_groupings():
+    # every contiguous grouping (G large rows, then n_1..n_G small rows in
+    # sorted order) of N <= 7 rows, scored by the explicit inverse: App. D's
+    # candidate for each G is one of them, and its choice is the best of its
+    # candidates; PSQ (G = N) and one group (G = 1) are candidates, so the
+    # choice never loses to either
+    for x in [c for c in tiny_cases() if c.shape[0] <= 7]:
+        N = x.shape[0]
+        _, _, M, order = Q._sorted_rows(x)
+        G_best, obj = Q.bhq_appd(x, 4)
+        brute = {}
+        for G in range(1, N + 1):
+            for n in compositions(N - G, G):
+                plan = Q._build_plan(x, 4, order, Q.appd_members(order, G, list(n)))
+                brute[(G, n)] = explicit_inverse_norm(plan)
+        cands = {}
+        for G in range(1, N + 1):
+            n = tuple(Q.appd_small_counts(Q.appd_prefix(M[order]), N, G))
+            cands[G] = brute[(G, n)]
+            assert obj[G - 1] == pytest.approx(cands[G], rel=1e-11)
+        best = min(cands.values())
+        assert cands[G_best] == pytest.approx(best, rel=1e-11)
+        assert all(cands[G] > best * (1 + 1e-9) for G in range(1, G_best))   # ties go to fewer groups
+        assert cands[G_best] <= cands[N] * (1 + 1e-12) and cands[G_best] <= cands[1] * (1 + 1e-12)
+        assert min(brute.values()) <= cands[G_best] * (1 + 1e-12)
+
+
+def test_appd_equal_norms_give_the_fixed_block_plan():
+    # every row with the same infinity norm: App. D's proportional sizes are
+    # equal, so for N = G k its plan for G is the fixed-block plan of size k
+    rng = np.random.default_rng(23)
+    for N, k in ((12, 3), (64, 8), (40, 5)):
+        x = rng.uniform(-1, 1, (N, 9)).astype(np.float32)
+        x[:, 0] = 2.0                                   # M = 2 for every row
+        G = N // k
+        a = Q.bhq_appd_plan(x, 5, G)
+        b = Q.bhq_plan(x, 5, k)
+        np.testing.assert_array_equal(a["perm"], b["perm"])
+        np.testing.assert_array_equal(a["group_off"], b["group_off"])
+        np.testing.assert_array_equal(a["scale"], b["scale"])
+        np.testing.assert_array_equal(a["zero"], b["zero"])
+
+
+def test_appd_literal_estimate_always_picks_one_group():
+    # App. D's approximation sum_i M_i^2 / ((N - G) M_i / S_G) = S_G^2 / (N - G)
+    # grows with G: read literally the search always ends at G = 1
+    rng = np.random.default_rng(24)
+    M = np.sort(rng.lognormal(0, 2, 50))[::-1]
+    est = []
+    for G in range(1, 50):
+        S = M[:G].sum()
+        lit = sum(m * m / ((50 - G) * m / S) for m in M[:G])
+        assert lit == pytest.approx(S * S / (50 - G), rel=1e-12)
+        est.append(lit)
+    assert all(b > a for a, b in zip(est, est[1:]))
+
+
+def test_appd_equal_rows_keep_per_row_scales():
+    # identical rows: lambda2 = 2 max|row| >= lambda1 = R, so any group costs
+    # more than its rows do alone (App. C.4): every row is its own group (PSQ)
     rng = np.random.default_rng(3)
     x = np.tile(rng.standard_normal((1, 40)).astype(np.float32), (130, 1))
-    k, obj = Q.bhq_adaptive_block(x, 5)
-    assert k == 1
+    G, obj = Q.bhq_appd(x, 5)
+    assert G == 130
     B = Q.n_bins(5)
     R = float(x[0].max() - x[0].min())
-    assert obj[1] == pytest.approx(130 * (R / B) ** 2, rel=1e-6)
+    assert obj[-1] == pytest.approx(130 * (R / B) ** 2, rel=1e-6)
 
 
-def test_adaptive_block_spreads_a_single_outlier():
-    # one row 1e8 times larger than the rest: one group of all 64 rows, whose
+def test_appd_spreads_a_single_outlier():
+    # one row 1e8 times larger than the rest: one group of all the rows, whose
     # bound ~ lambda1^2 / (B^2 N) beats the per-row lambda1^2 / B^2 (Sec. 4.2)
     rng = np.random.default_rng(4)
     x = (1e-4 * rng.standard_normal((64, 32))).astype(np.float32)
     x[9] = (1e4 * rng.standard_normal(32)).astype(np.float32)
-    k, obj = Q.bhq_adaptive_block(x, 5)
-    assert k == 64
-    assert obj[64] < obj[1] / 32
+    G, obj = Q.bhq_appd(x, 5)
+    assert G == 1
+    assert obj[0] < obj[-1] / 32
 
 
-def test_adaptive_block_ties_go_to_the_larger_block():
-    # a zero matrix: every plan has unit scales, so |S^-1|_F^2 = N for every k
-    k, obj = Q.bhq_adaptive_block(np.zeros((100, 8), np.float32), 4)
-    assert all(v == 100.0 for v in obj.values())
-    assert k == 64
+def test_appd_zero_matrix_ties_to_one_group():
+    # unit scales everywhere: |S^-1|_F^2 = N for every G, and ties go to fewer groups
+    G, obj = Q.bhq_appd(np.zeros((30, 8), np.float32), 4)
+    assert all(v == 30.0 for v in obj)
+    assert G == 1
 
 
-def test_adaptive_quantize_is_the_fixed_block_of_its_choice():
-    rng = np.random.default_rng(6)
-    x = (rng.lognormal(0, 2, (150, 1)) * rng.standard_normal((150, 20))).astype(np.float32)
-    k, _ = Q.bhq_adaptive_block(x, 5)
-    a = Q.quantize_bhq(x, 5, 0, seed=2, stream=1)
-    b = Q.quantize_bhq(x, 5, k, seed=2, stream=1)
-    assert a["k"] == k
-    np.testing.assert_array_equal(a["code"], b["code"])
-    np.testing.assert_array_equal(a["perm"], b["perm"])
+def test_appd_quantizer_is_unbiased_within_its_bound():
+    x = heavy_rows(25, 150, 20)
+    q = Q.quantize_bhq(x, 5, 0, seed=2, stream=1)
+    assert q["k"] == 0 and q["G"] == Q.bhq_appd(x, 5)[0]
+    np.testing.assert_array_equal(q["code"], Q.quantize_bhq(x, 5, 0, seed=2, stream=1, plan=q["plan"])["code"])
+    m = theory.exact_mean(x, q)
+    for g in q["plan"]["groups"]:
+        mem = g["members"]
+        assert np.abs(m[mem] - x[mem]).max() <= 2.0 ** -18 * np.abs(x[mem]).max()
+    v = theory.exact_quantizer_variance(x, q)
+    assert v <= x.shape[1] / 4.0 * Q.bhq_scale_norm(q["plan"]) * (1 + 1e-9)
+    assert v < theory.exact_quantizer_variance(x, Q.quantize_psq(x, 5))
+    y = theory.transformed_values(x, q)
+    B = Q.n_bins(5)
+    assert y.min() >= -1e-4 * B and y.max() <= B * (1 + 1e-4)
