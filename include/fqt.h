@@ -73,9 +73,10 @@ typedef enum { FQT_PTQ = 0, FQT_PSQ = 1, FQT_BHQ = 2, FQT_SHIFT = 3 } fqt_kind;
  *             row min, as PSQ).
  *   perm      BHQ only: [rows] slot -> original row.
  *   group_off BHQ only, optional: [rows + 1]; the first G + 1 entries are
- *             the group boundaries in slot order (G = ceil(rows / k)).
+ *             the group boundaries in slot order.
  *   code_sum  optional int32 sums of q along the contiguous axis of the
  *             stored layout: [rows] for natural, [cols] for transposed.
+ *   num_groups BHQ only, optional: one int32, the number of groups G.
  * Dequantized value: PTQ/PSQ code / s + z.  BHQ group of k_g > 1 slots:
  * diag(d)^-1 H (code + c_g), H the k_g x k_g Householder reflection with
  * normal 1/sqrt(k_g) - e_1 (Sec. 4.2).                                      */
@@ -87,6 +88,7 @@ typedef struct {
   int32_t* group_off;
   int32_t* code_sum;
   int8_t* shift;  /* FQT_SHIFT only: [rows] left shift of each row's offset codes */
+  int32_t* num_groups;
 } fqt_qtensor;
 
 /* Per-tensor quantizer, Sec. 3.3: z = min x, s = B / (max x - min x),
@@ -103,13 +105,17 @@ fqt_status fqt_quantize_psq(const float* x, int64_t rows, int64_t cols, int bits
                             uint32_t stream, const fqt_qtensor* out, void* ws, size_t ws_bytes,
                             fqt_stream_t s);
 
-/* Block Householder quantizer, Sec. 4.2 / App. C.4 / App. D, block size
- * k = block_size (a power of two, 1..64), or 0 for the adaptive block size
- * of fqt_bhq_adaptive_block (then the call waits for `stream` once, to read
- * the choice).  Rows are sorted by infinity norm (descending, ties by row
- * index); G = ceil(rows / k) groups each take one of the G largest rows plus
- * the next k - 1 rows of the sorted tail.  Codes are in slot order, natural
- * layout.  Needs out->q, scale, zero, perm.                                 */
+/* Block Householder quantizer, Sec. 4.2 / App. C.4 / App. D.  Rows are
+ * sorted by infinity norm M (descending, ties by row index); each group
+ * holds one of the G largest rows and a run of the sorted tail.
+ *   block_size = k >= 1: G = ceil(rows / k) groups, group g takes the g-th
+ *     largest row and the next k - 1 rows of the tail (the last groups may
+ *     be shorter, see group_off).
+ *   block_size = 0: App. D's adaptive groups (fqt_bhq_adaptive_groups), all
+ *     on the device, nothing waits; rows <= 65536 (FQT_EUNSUPPORTED beyond).
+ * The transform Q diag(d) G_g of each group sums its column over the group's
+ * slots one at a time in slot order (float32).  Codes are in slot order,
+ * natural layout.  Needs out->q, scale, zero, perm.                         */
 fqt_status fqt_quantize_bhq(const float* x, int64_t rows, int64_t cols, int bits, int block_size,
                             uint64_t seed, uint32_t stream, const fqt_qtensor* out, void* ws,
                             size_t ws_bytes, fqt_stream_t s);
@@ -129,26 +135,30 @@ fqt_status fqt_quantize_shift(const float* x, int64_t rows, int64_t cols, int bi
 
 size_t fqt_quantize_workspace(fqt_kind kind, int64_t rows, int64_t cols, int block_size);
 
-/* Adaptive grouping of the block Householder quantizer, App. D step 2: of
- * the block sizes 1, 2, 4, .., 64, the one whose plan (as above) has the
- * least |S^-1|_F^2, the factor of the variance bound (D/4)|S^-1|_F^2 of Eq.
- * (matrix-quantizer-variance); ties go to the larger block.  (App. D's own
- * estimate, sum_i M_i^2 / ((N - G) M_i / sum_j M_j), grows with the number
- * of groups and would always keep one group; its proportional group sizes
- * are not offered.)  Evaluated on the device; the call waits for `stream`
- * and stores the choice in *block_size (host memory).  rows <= 16384
- * (FQT_EUNSUPPORTED beyond).  Returns FQT_ENONFINITE for non-finite x.     */
-fqt_status fqt_bhq_adaptive_block(const float* x, int64_t rows, int64_t cols, int bits, int* block_size,
-                                  void* ws, size_t ws_bytes, fqt_stream_t s);
+/* Adaptive grouping of the block Householder quantizer, App. D step 2: for
+ * every number of groups G = 1..rows, the G largest rows lead the groups
+ * and the rows - G others are shared out in sorted order in proportion to
+ * the leaders' norms: the first i groups take floor((rows - G) P_i / P_G +
+ * 1/2) of them, P_i = M_(1) + .. + M_(i) summed in float64 one at a time.
+ * Each G is scored by the exact |S^-1|_F^2 of its plan (the factor of the
+ * variance bound (D/4)|S^-1|_F^2, Eq. matrix-quantizer-variance), groups
+ * added in order in float64; the least wins, ties to the smaller G.  (App.
+ * D's own estimate, sum_i M_i^2 / ((N - G) M_i / sum_j M_j), grows with G
+ * and would always keep one group.)  Asynchronous on `stream`: writes the
+ * chosen G to num_groups (one device int32) and, if objective is not NULL,
+ * the score of every G to objective[G - 1] (device, [rows] float64).
+ * O(rows^2) work; rows <= 65536 (FQT_EUNSUPPORTED beyond).  A non-finite x
+ * is reported by fqt_workspace_status (the plan then treats its norms as 0). */
+fqt_status fqt_bhq_adaptive_groups(const float* x, int64_t rows, int64_t cols, int bits, int32_t* num_groups,
+                                   double* objective, void* ws, size_t ws_bytes, fqt_stream_t s);
 size_t fqt_bhq_adaptive_workspace(int64_t rows, int64_t cols);
 
 /* Quantizer choice for one gradient quantizer. */
 typedef struct {
   fqt_kind kind;   /* FQT_PTQ, FQT_PSQ or FQT_BHQ */
   int bits;        /* 1..8 */
-  int block_size;  /* BHQ only: power of two in 1..64, or 0 for the adaptive block size
-                   * (fqt_bhq_adaptive_block; the call then waits for the stream once,
-                   * and needs N <= 16384) */
+  int block_size;  /* BHQ only: block size k >= 1, or 0 for App. D's adaptive groups
+                   * (fqt_bhq_adaptive_groups; needs N <= 65536) */
 } fqt_qspec;
 
 /* Optional per-phase timing: when fqt_bwd_cfg.trace is non-NULL, the layer

@@ -46,7 +46,11 @@ struct Tracer {
     if (t && i < t->count && t->stop[i]) (void)hipEventRecord(static_cast<hipEvent_t>(t->stop[i]), s);
   }
 };
-bool valid_block(int k) { return k >= 1 && k <= 64 && (k & (k - 1)) == 0; }
+// Block sizes the aligned fast path takes (groups inside 64-row tiles); any
+// other size, and 0 (App. D), go through the general plan.
+bool aligned_block(int k) { return k >= 1 && k <= 64 && (k & (k - 1)) == 0; }
+// App. D scores every number of groups, O(rows^2) terms.
+constexpr int64_t APPD_MAX_ROWS = 65536;
 
 #define FQT_TRY(expr)                              \
   do {                                             \
@@ -57,13 +61,89 @@ bool valid_block(int k) { return k >= 1 && k <= 64 && (k & (k - 1)) == 0; }
 // ---------------------------------------------------------------------------
 // standalone quantizers
 // ---------------------------------------------------------------------------
+// Workspace pieces of a block Householder plan: the sort, and for the
+// general plan (App. D, or a block size the aligned path does not take) the
+// sorted-position scalars, slot records and the forward transform's
+// per-group column term.  group_off / num_groups stand in when the caller
+// gives none.
+struct BhqWs {
+  void* plan;
+  bool general;
+  AppdWs appd;
+  SlotInfo* slot;
+  float* tau;
+  int32_t* group_off;
+  int32_t* num_groups;
+};
+
+BhqWs carve_bhq(Carver& c, int64_t rows, int64_t cols, int block_size) {
+  BhqWs b{};
+  b.plan = c.take<char>((int64_t)bhq_plan_workspace(rows));
+  b.general = !aligned_block(block_size);
+  b.group_off = c.take<int32_t>(rows + 1);
+  b.num_groups = c.take<int32_t>(1);
+  if (b.general) {
+    void* ap = c.take<char>((int64_t)appd_workspace(rows));
+    if (ap) b.appd = appd_carve(ap, rows);
+    b.slot = c.take<SlotInfo>(rows);
+    b.tau = c.take<float>((rows + 1) / 2 * cols);
+  }
+  return b;
+}
+
+// The plan of a BHQ quantization, asynchronous: perm, per-slot scale / zero,
+// group offsets and the number of groups (and the slot records for the
+// general plan).  fin: the finalize step to run inside the first launch.
+fqt_status plan_bhq(const BhqWs& b, const float* rmin, const float* rmax, int64_t rows, int bits, int block_size,
+                    int32_t* perm, float* scale, float* zero, int32_t* group_off, int32_t* num_groups,
+                    const FinalizePlan* fin, hipStream_t s) {
+  int32_t* goff = group_off ? group_off : b.group_off;
+  int32_t* ng = num_groups ? num_groups : b.num_groups;
+  if (!b.general) {
+    const BhqLayout L = bhq_layout(rows, block_size);
+    FQT_TRY(launch_bhq_plan(rmin, rmax, L, bits, b.plan, perm, scale, zero, goff, fin, s));
+    FQT_TRY(launch_store_i32(ng, (int32_t)L.G, s));
+    return FQT_OK;
+  }
+  FQT_TRY(launch_bhq_sort(rmin, rmax, rows, b.plan, b.appd.sigma, fin, s));
+  FQT_TRY(launch_general_plan(rmin, rmax, rows, bits, block_size, b.appd, nullptr, perm, scale, zero, goff, b.slot,
+                              ng, s));
+  return FQT_OK;
+}
+
+// Quantizer parameters of a planned BHQ: the aligned layout, or the general
+// plan with its per-group column term computed here (after the plan).
+fqt_status bhq_params(const BhqWs& b, const float* x, int64_t rows, int64_t cols, int block_size,
+                      const int32_t* perm, const float* scale, QuantParams& p, hipStream_t s) {
+  if (!b.general) {
+    p.L = bhq_layout(rows, block_size);
+    return FQT_OK;
+  }
+  FQT_TRY(launch_bhq_tau(x, rows, cols, perm, scale, b.slot, b.tau, s));
+  p.L = BhqLayout{};
+  p.L.rows = rows;
+  p.L.k = 0;
+  p.slot = b.slot;
+  p.tau = b.tau;
+  return FQT_OK;
+}
+
+// Whether a BHQ block size is valid (>= 0) and, for App. D (0), within its rows limit.
+fqt_status check_block(int block_size, int64_t rows) {
+  if (block_size < 0) return FQT_EINVAL;
+  if (block_size == 0 && rows > APPD_MAX_ROWS) return FQT_EUNSUPPORTED;
+  return FQT_OK;
+}
+
+// ---------------------------------------------------------------------------
+// standalone quantizers
+// ---------------------------------------------------------------------------
 struct QuantWs {
   Header h;
   StatsSeg seg;
   float* rmin;
   float* rmax;
-  void* plan;
-  void* adaptive;
+  BhqWs bhq;
   float* tscale;  // FQT_SHIFT: the per-tensor step scale s
 };
 
@@ -77,23 +157,9 @@ QuantWs carve_quant(Carver& c, fqt_kind kind, const float* x, int64_t rows, int6
     w.rmax = c.take<float>(rows);
     stats_direct_rows(w.seg, w.rmin, w.rmax);
   }
-  if (kind == FQT_BHQ) w.plan = c.take<char>((int64_t)bhq_plan_workspace(rows));
-  if (kind == FQT_BHQ && block_size == 0) w.adaptive = c.take<char>((int64_t)bhq_adaptive_workspace(rows));
+  if (kind == FQT_BHQ) w.bhq = carve_bhq(c, rows, cols, block_size);
   if (kind == FQT_SHIFT) w.tscale = c.take<float>(1);
   return w;
-}
-
-// Adaptive grouping (App. D): evaluate the candidate block sizes on the
-// device from the row ranges, wait for the stream and read the choice.
-fqt_status choose_block(const float* rmin, const float* rmax, int64_t rows, int bits, void* adaptive_ws,
-                        hipStream_t s, int* block) {
-  FQT_TRY(launch_bhq_adaptive(rmin, rmax, rows, bits, adaptive_ws, s));
-  int32_t k = 0;
-  FQT_TRY(hipMemcpyAsync(&k, bhq_adaptive_carve(adaptive_ws, rows).chosen, sizeof(k), hipMemcpyDeviceToHost, s));
-  FQT_TRY(hipStreamSynchronize(s));
-  if (!valid_block(k)) return FQT_EDEVICE;
-  *block = k;
-  return FQT_OK;
 }
 
 void add_zero(FinalizePlan& fp, int32_t* p, int64_t n) {
@@ -117,8 +183,9 @@ fqt_status quantize_common(fqt_kind kind, const float* x, int64_t rows, int64_t 
   fqt_status st = check_quant_args(x, rows, cols, bits, out);
   if (st != FQT_OK) return st;
   if (kind == FQT_BHQ) {
-    if (block_size == 0 && !bhq_adaptive_supported(rows)) return FQT_EUNSUPPORTED;
-    if ((block_size != 0 && !valid_block(block_size)) || !out->perm) return FQT_EINVAL;
+    if (!out->perm) return FQT_EINVAL;
+    st = check_block(block_size, rows);
+    if (st != FQT_OK) return st;
   }
   if (kind == FQT_SHIFT && !out->shift) return FQT_EINVAL;
   if (!ws) return FQT_EWORKSPACE;
@@ -145,16 +212,11 @@ fqt_status quantize_common(fqt_kind kind, const float* x, int64_t rows, int64_t 
     fp.nout = 1;
   }
   add_zero(fp, out->code_sum, transpose ? cols : rows);
-  if (kind == FQT_BHQ) add_zero(fp, bhq_plan_carve(w.plan, rows).rank, rows);
+  if (kind == FQT_BHQ) add_zero(fp, bhq_plan_carve(w.bhq.plan, rows).rank, rows);
   // with row ranges straight from the statistics kernel, the BHQ plan's first
   // launch also runs the finalize step
   const bool fin_in_plan = kind == FQT_BHQ && w.seg.rmin != nullptr;
   if (!fin_in_plan) FQT_TRY(launch_finalize(fp, s));
-  if (kind == FQT_BHQ && block_size == 0) {
-    // the row ranges are complete here (statistics kernel, or the finalize above)
-    st = choose_block(w.rmin, w.rmax, rows, bits, w.adaptive, s, &block_size);
-    if (st != FQT_OK) return st;
-  }
 
   QuantParams p{};
   p.x = x;
@@ -178,9 +240,11 @@ fqt_status quantize_common(fqt_kind kind, const float* x, int64_t rows, int64_t 
     mode = QM_ROW;
     if (kind == FQT_SHIFT) p.shift = out->shift;
   } else if (kind == FQT_BHQ) {
-    p.L = bhq_layout(rows, block_size);
-    FQT_TRY(launch_bhq_plan(w.rmin, w.rmax, p.L, bits, w.plan, out->perm, out->scale, out->zero, out->group_off,
-                            fin_in_plan ? &fp : nullptr, s));
+    st = plan_bhq(w.bhq, w.rmin, w.rmax, rows, bits, block_size, out->perm, out->scale, out->zero, out->group_off,
+                  out->num_groups, fin_in_plan ? &fp : nullptr, s);
+    if (st != FQT_OK) return st;
+    st = bhq_params(w.bhq, x, rows, cols, block_size, out->perm, out->scale, p, s);
+    if (st != FQT_OK) return st;
     p.perm = out->perm;
     mode = QM_BHQ;
   }
@@ -199,8 +263,8 @@ struct LinearWs {
   int32_t *sum_x, *sum_w, *sum_g1, *sum_g2;
   float *sx, *zx, *sw, *zw, *sg1, *zg1, *sg2, *zg2;
   int32_t* perm;
-  void* plan;
-  void* adaptive;
+  BhqWs bhq;
+  double* tbuf;      // general BHQ plan: T rows of multi-row groups [N, d_in]
   int32_t* part;
   int splits;
   int8_t* shift1;    // Q_b1 = FQT_SHIFT: per-row shifts, step scale, zero-point terms and column vector
@@ -251,8 +315,8 @@ LinearWs carve_linear(Carver& c, const float* X, const float* W, const float* G,
   w.zg2 = c.take<float>(N);
   if (cfg.qb_x.kind == FQT_BHQ) {
     w.perm = c.take<int32_t>(N);
-    w.plan = c.take<char>((int64_t)bhq_plan_workspace(N));
-    if (cfg.qb_x.block_size == 0) w.adaptive = c.take<char>((int64_t)bhq_adaptive_workspace(N));
+    w.bhq = carve_bhq(c, N, d_out, cfg.qb_x.block_size);
+    if (w.bhq.general) w.tbuf = c.take<double>(N * d_in);
   }
   w.splits = linear_splits(N);
   if (w.splits > 1) w.part = c.take<int32_t>((int64_t)w.splits * d_out * d_in);
@@ -302,8 +366,7 @@ fqt_status check_cfg(const fqt_bwd_cfg* cfg) {
     return FQT_EINVAL;
   if ((cfg->qb_w.kind != FQT_PTQ && cfg->qb_w.kind != FQT_SHIFT) || cfg->qb_x.kind == FQT_SHIFT)
     return FQT_EUNSUPPORTED;
-  if (cfg->qb_x.kind == FQT_BHQ && cfg->qb_x.block_size != 0 && !valid_block(cfg->qb_x.block_size))
-    return FQT_EINVAL;
+  if (cfg->qb_x.kind == FQT_BHQ && cfg->qb_x.block_size < 0) return FQT_EINVAL;
   if (cfg->relu_input != 0 && cfg->relu_input != 1) return FQT_EINVAL;
   return FQT_OK;
 }
@@ -339,8 +402,8 @@ struct ConvWs {
   int32_t *swq, *sumB, *xs, *qs, *sumA_tap, *count_tap, *sg, *ct, *cnt;
   float *sx, *zx, *sw, *zw, *sg1, *zg1, *sg2, *zg2;
   int32_t* perm;
-  void* plan;
-  void* adaptive;
+  BhqWs bhq;
+  double* tbuf;      // general BHQ plan: T rows (input pixel, slot) of multi-row groups [h w npad, c]
   int32_t* part;
   int64_t ldq, kchunk;
   int splits;
@@ -387,8 +450,8 @@ ConvWs carve_conv(Carver& c, const float* X, const float* W, const float* G, con
   w.zg2 = c.take<float>(N);
   if (cfg.qb_x.kind == FQT_BHQ) {
     w.perm = c.take<int32_t>(N);
-    w.plan = c.take<char>((int64_t)bhq_plan_workspace(N));
-    if (cfg.qb_x.block_size == 0) w.adaptive = c.take<char>((int64_t)bhq_adaptive_workspace(N));
+    w.bhq = carve_bhq(c, N, howo * g.o, cfg.qb_x.block_size);
+    if (w.bhq.general) w.tbuf = c.take<double>(hw * g.npad * g.c);
   }
   // grad_W: split the pixel contraction so that about 512 blocks run, each
   // K chunk a whole number of 128-byte stages and at most 65536
@@ -448,11 +511,11 @@ size_t fqt_bhq_adaptive_workspace(int64_t rows, int64_t cols) {
   return c.off;
 }
 
-fqt_status fqt_bhq_adaptive_block(const float* x, int64_t rows, int64_t cols, int bits, int* block_size, void* ws,
-                                  size_t ws_bytes, fqt_stream_t s) {
-  if (!x || !block_size) return FQT_EINVAL;
+fqt_status fqt_bhq_adaptive_groups(const float* x, int64_t rows, int64_t cols, int bits, int32_t* num_groups,
+                                   double* objective, void* ws, size_t ws_bytes, fqt_stream_t s) {
+  if (!x || !num_groups) return FQT_EINVAL;
   if (rows < 1 || cols < 1 || !valid_bits(bits)) return FQT_EINVAL;
-  if (!bhq_adaptive_supported(rows) || cols > ((int64_t)1 << 40) / rows) return FQT_EUNSUPPORTED;
+  if (rows > APPD_MAX_ROWS || cols > ((int64_t)1 << 40) / rows) return FQT_EUNSUPPORTED;
   if (!ws) return FQT_EWORKSPACE;
   if (ws_bytes < fqt_bhq_adaptive_workspace(rows, cols)) return FQT_EWORKSPACE;
   Carver c(ws);
@@ -468,10 +531,11 @@ fqt_status fqt_bhq_adaptive_block(const float* x, int64_t rows, int64_t cols, in
   fp.rmin = w.rmin;
   fp.rmax = w.rmax;
   fp.status = w.h.status;
+  add_zero(fp, bhq_plan_carve(w.bhq.plan, rows).rank, rows);
   FQT_TRY(launch_finalize(fp, s));
-  const fqt_status st = choose_block(w.rmin, w.rmax, rows, bits, w.adaptive, s, block_size);
-  if (st != FQT_OK) return st;
-  return fqt_workspace_status(ws, s);
+  FQT_TRY(launch_bhq_sort(w.rmin, w.rmax, rows, w.bhq.plan, w.bhq.appd.sigma, nullptr, s));
+  FQT_TRY(launch_appd_search(w.rmin, w.rmax, rows, bits, w.bhq.appd, objective, num_groups, s));
+  return FQT_OK;
 }
 
 size_t fqt_linear_backward_workspace(int64_t N, int64_t d_in, int64_t d_out, const fqt_bwd_cfg* cfg) {
@@ -489,7 +553,10 @@ fqt_status fqt_linear_backward(const float* X, const float* W, const float* G, i
   fqt_status st = check_cfg(cfg);
   if (st != FQT_OK) return st;
   if (N > MAX_ROWS || d_out > MAX_ROWS || d_out > MAX_K_CHUNK || N > 0x7FFFFFFF / 2) return FQT_EUNSUPPORTED;
-  if (cfg->qb_x.kind == FQT_BHQ && cfg->qb_x.block_size == 0 && !bhq_adaptive_supported(N)) return FQT_EUNSUPPORTED;
+  if (cfg->qb_x.kind == FQT_BHQ) {
+    st = check_block(cfg->qb_x.block_size, N);
+    if (st != FQT_OK) return st;
+  }
   if (!ws) return FQT_EWORKSPACE;
   if (ws_bytes < fqt_linear_backward_workspace(N, d_in, d_out, cfg)) return FQT_EWORKSPACE;
   Carver c(ws);
@@ -530,21 +597,14 @@ fqt_status fqt_linear_backward(const float* X, const float* W, const float* G, i
   add_zero(fp, w.sum_w, d_in);
   add_zero(fp, w.sum_g1, d_out);
   add_zero(fp, w.sum_g2, N);
-  if (bhq) add_zero(fp, bhq_plan_carve(w.plan, N).rank, N);
+  if (bhq) add_zero(fp, bhq_plan_carve(w.bhq.plan, N).rank, N);
   const bool fin_in_plan = bhq && w.sg_seg.rmin != nullptr;
   if (!fin_in_plan) FQT_TRY(launch_finalize(fp, s));
-  int block = qx.block_size;
-  if (bhq && block == 0) {
-    // adaptive grouping (App. D): the row ranges of G are complete here
-    st = choose_block(w.rmin, w.rmax, N, qx.bits, w.adaptive, s, &block);
-    if (st != FQT_OK) return st;
-  }
-  BhqLayout L{};
   int mode = qx.kind == FQT_PSQ ? QM_ROW : QM_TENSOR;
   if (bhq) {
-    L = bhq_layout(N, block);
-    FQT_TRY(launch_bhq_plan(w.rmin, w.rmax, L, qx.bits, w.plan, w.perm, w.sg2, w.zg2, nullptr,
-                            fin_in_plan ? &fp : nullptr, s));
+    st = plan_bhq(w.bhq, w.rmin, w.rmax, N, qx.bits, qx.block_size, w.perm, w.sg2, w.zg2, nullptr, nullptr,
+                  fin_in_plan ? &fp : nullptr, s);
+    if (st != FQT_OK) return st;
     mode = QM_BHQ;
   }
   tr.end(2);
@@ -590,7 +650,10 @@ fqt_status fqt_linear_backward(const float* X, const float* W, const float* G, i
   pg.shift2 = w.shift1;
   pg.q2_t = w.qg1_t;
   pg.sum2_t = w.sum_g1;
-  pg.L = L;
+  if (bhq) {
+    st = bhq_params(w.bhq, G, N, d_out, qx.block_size, w.perm, w.sg2, pg, s);
+    if (st != FQT_OK) return st;
+  }
   // Q_b2(G) [N, d_out] slot order (stream 1) and Q_b1(G) [d_out, N] (stream 0)
   // from one read of G, with Q_f(X) and Q_theta(W) in the same launch (phase
   // 5; phases 3 and 4 stay empty)
@@ -677,10 +740,35 @@ fqt_status fqt_linear_backward(const float* X, const float* W, const float* G, i
   gx.scaleB = w.sw;
   gx.zeroB = w.zw;
   gx.halfB = 1 << (cfg->theta_bits - 1);
-  gx.L = L;
+  gx.L = pg.L;
   gx.mask = cfg->relu_input ? X : nullptr;  // [N, d_in], the same layout as grad_X
   tr.begin(7);
-  FQT_TRY(launch_gemm(gx, bhq ? EPI_BHQ : EPI_ROW, s));
+  if (bhq && w.bhq.general) {
+    // general plan: one-row groups finished in the epilogue, the other rows'
+    // T through the inverse pass
+    gx.slot = w.bhq.slot;
+    gx.tbuf = w.tbuf;
+    gx.ldt = d_in;
+    FQT_TRY(launch_gemm(gx, EPI_BHQT, s));
+    InverseParams ip{};
+    ip.T = w.tbuf;
+    ip.ldt = d_in;
+    ip.tstride = 0;
+    ip.nblk = 1;
+    ip.rows = N;
+    ip.cols = d_in;
+    ip.slot = w.bhq.slot;
+    ip.perm = w.perm;
+    ip.scale = w.sg2;
+    ip.out = grad_X;
+    ip.ldo = d_in;
+    ip.ostride = 1;
+    ip.obstride = 0;
+    ip.mask = gx.mask;
+    FQT_TRY(launch_bhq_inverse(ip, s));
+  } else {
+    FQT_TRY(launch_gemm(gx, bhq ? EPI_BHQ : EPI_ROW, s));
+  }
   tr.end(7);
   return FQT_OK;
 }
@@ -876,8 +964,10 @@ fqt_status fqt_conv_backward_im2col(const float* X, const float* W, const float*
   st = check_cfg(cfg);
   if (st != FQT_OK) return st;
   if (cfg->relu_input || cfg->qb_w.kind == FQT_SHIFT) return FQT_EUNSUPPORTED;
-  if (cfg->qb_x.kind == FQT_BHQ && cfg->qb_x.block_size == 0 && !bhq_adaptive_supported(shape->n))
-    return FQT_EUNSUPPORTED;
+  if (cfg->qb_x.kind == FQT_BHQ) {
+    st = check_block(cfg->qb_x.block_size, shape->n);
+    if (st != FQT_OK) return st;
+  }
   if (!ws) return FQT_EWORKSPACE;
   if (ws_bytes < fqt_conv_backward_workspace(shape, cfg)) return FQT_EWORKSPACE;
   const ConvGeom g = conv_geom(*shape);
@@ -916,21 +1006,14 @@ fqt_status fqt_conv_backward_im2col(const float* X, const float* W, const float*
   fp.nout = 3;
   if (!bhq) fp.out[fp.nout++] = ScaleOut{2, qx.bits, qx.kind == FQT_PSQ ? 1 : 0, w.sg2, w.zg2};
   add_zero(fp, w.sumB, taps * g.c);
-  if (bhq) add_zero(fp, bhq_plan_carve(w.plan, N).rank, N);
+  if (bhq) add_zero(fp, bhq_plan_carve(w.bhq.plan, N).rank, N);
   const bool fin_in_plan = bhq && w.sg_seg.rmin != nullptr;
   if (!fin_in_plan) FQT_TRY(launch_finalize(fp, s));
-  int block = qx.block_size;
-  if (bhq && block == 0) {
-    // adaptive grouping (App. D): the row ranges of G are complete here
-    st = choose_block(w.rmin, w.rmax, N, qx.bits, w.adaptive, s, &block);
-    if (st != FQT_OK) return st;
-  }
-  BhqLayout L{};
   int mode = qx.kind == FQT_PSQ ? QM_ROW : QM_TENSOR;
   if (bhq) {
-    L = bhq_layout(N, block);
-    FQT_TRY(launch_bhq_plan(w.rmin, w.rmax, L, qx.bits, w.plan, w.perm, w.sg2, w.zg2, nullptr,
-                            fin_in_plan ? &fp : nullptr, s));
+    st = plan_bhq(w.bhq, w.rmin, w.rmax, N, qx.bits, qx.block_size, w.perm, w.sg2, w.zg2, nullptr, nullptr,
+                  fin_in_plan ? &fp : nullptr, s);
+    if (st != FQT_OK) return st;
     mode = QM_BHQ;
   }
   tr.end(2);
@@ -968,7 +1051,10 @@ fqt_status fqt_conv_backward_im2col(const float* X, const float* W, const float*
   pg.scale = w.sg2;
   pg.zero = w.zg2;
   pg.q_nat = w.q2;
-  pg.L = L;
+  if (bhq) {
+    st = bhq_params(w.bhq, G, N, D, qx.block_size, w.perm, w.sg2, pg, s);
+    if (st != FQT_OK) return st;
+  }
   FQT_TRY(launch_quant(pg, mode, s));
   NarrowQParams n1{};
   n1.x = G;
@@ -1036,8 +1122,30 @@ fqt_status fqt_conv_backward_im2col(const float* X, const float* W, const float*
   gx.scaleB = w.sw;
   gx.zeroB = w.zw;
   gx.halfB = 1 << (cfg->theta_bits - 1);
-  gx.L = L;
-  FQT_TRY(launch_conv_gradx(gx, bhq ? EPI_BHQ : EPI_ROW, g, w.q2, w.sg, w.ct, w.cnt, s));
+  gx.L = pg.L;
+  if (bhq && w.bhq.general) {
+    gx.slot = w.bhq.slot;
+    gx.tbuf = w.tbuf;
+    gx.ldt = g.c;
+    FQT_TRY(launch_conv_gradx(gx, EPI_BHQT, g, w.q2, w.sg, w.ct, w.cnt, s));
+    InverseParams ip{};
+    ip.T = w.tbuf;
+    ip.ldt = g.c;
+    ip.tstride = g.npad;
+    ip.nblk = hw;
+    ip.rows = N;
+    ip.cols = g.c;
+    ip.slot = w.bhq.slot;
+    ip.perm = w.perm;
+    ip.scale = w.sg2;
+    ip.out = grad_X;
+    ip.ldo = g.c;
+    ip.ostride = hw;
+    ip.obstride = 1;
+    FQT_TRY(launch_bhq_inverse(ip, s));
+  } else {
+    FQT_TRY(launch_conv_gradx(gx, bhq ? EPI_BHQ : EPI_ROW, g, w.q2, w.sg, w.ct, w.cnt, s));
+  }
   tr.end(7);
   return FQT_OK;
 }

@@ -679,7 +679,7 @@ __global__ __launch_bounds__(256) void conv_gradx_kernel(GemmParams p, ConvGeom 
     if (m < p.M && slot < (uint32_t)g.n) {
       const float s = p.rowwiseA ? p.scaleA[slot] : p.scaleA[0];
       const float z = p.rowwiseA ? p.zeroA[slot] : p.zeroA[0];
-      q.kind = (EPI == EPI_BHQ) ? bhq_slot_kind(p.L, slot) : 0;
+      q.kind = (EPI == EPI_BHQ) ? bhq_slot_kind(p.L, slot) : (EPI == EPI_BHQT ? (p.slot[slot].size > 1) : 0);
       const int iy = (int)(pix / (uint32_t)g.w), ix = (int)pix - iy * g.w;
       int rs = 0;
       for (int r = 0; r < g.kh; ++r)
@@ -791,6 +791,14 @@ __global__ __launch_bounds__(256) void conv_gradx_kernel(GemmParams p, ConvGeom 
       if (q.orow < 0) continue;
       double a[4], v[4];
       row_acc(row, a);
+      if (EPI == EPI_BHQT && q.kind != 0) {
+        // a row of a multi-row group of the general plan: its T for the inverse pass
+        double* dst = p.tbuf + (m0 + row) * p.ldt + col;
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (col + e < p.N) dst[e] = dW * a[e] + (q.rterm + q.hz * colterm[e]);
+        continue;
+      }
 #pragma unroll
       for (int e = 0; e < 4; ++e) v[e] = q.dq * (dW * a[e] + q.rterm) + q.hz * colterm[e];
       store(q.orow, v);
@@ -877,6 +885,8 @@ static hipError_t launch_conv_gradx_t(const GemmParams& p, const ConvGeom& g, co
 hipError_t launch_conv_gradx(const GemmParams& p, int epi, const ConvGeom& g, const int8_t* q2, const int32_t* sg,
                              const int32_t* ct, const int32_t* cnt, hipStream_t s) {
   if (epi == EPI_ROW) return launch_conv_gradx_t<EPI_ROW, 0>(p, g, q2, sg, ct, cnt, s);
+  if (epi == EPI_BHQT)
+    return p.slot && p.tbuf ? launch_conv_gradx_t<EPI_BHQT, 0>(p, g, q2, sg, ct, cnt, s) : hipErrorInvalidValue;
   switch (p.L.k) {
     case 1: return launch_conv_gradx_t<EPI_BHQ, 1>(p, g, q2, sg, ct, cnt, s);
     case 2: return launch_conv_gradx_t<EPI_BHQ, 2>(p, g, q2, sg, ct, cnt, s);

@@ -1,5 +1,5 @@
 // Device helpers shared by the FQT kernels: Philox4x32-10, stochastic
-// rounding, order-preserving float encodings for atomic min / max.
+// rounding, the scalars of a block Householder group.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -112,19 +112,6 @@ __device__ __forceinline__ int32_t sum4_i8(uint32_t w, int32_t acc) {
   return __builtin_amdgcn_sdot4((int)w, 0x01010101, acc, false);
 }
 
-// ---------------------------------------------------------------------------
-// Order-preserving uint32 encoding of float32 (for unsigned atomic min/max).
-// ---------------------------------------------------------------------------
-__host__ __device__ __forceinline__ uint32_t f2ord(float f) {
-  uint32_t u = __float_as_uint(f);
-  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
-}
-__host__ __device__ __forceinline__ float ord2f(uint32_t u) {
-  return __uint_as_float((u & 0x80000000u) ? (u & 0x7FFFFFFFu) : ~u);
-}
-constexpr uint32_t ORD_POS_INF = 0xFF800000u;  // f2ord(+inf): identity of min
-constexpr uint32_t ORD_NEG_INF = 0x007FFFFFu;  // f2ord(-inf): identity of max
-
 constexpr float FLT_MAX_F = 3.402823466e+38f;
 
 // s = B / R (one correctly rounded float32 division); R = 0 gives 1;
@@ -133,6 +120,88 @@ __device__ __forceinline__ float scale_from_range(float R, int B) {
   if (!(R > 0.0f)) return 1.0f;
   float s = __fdiv_rn((float)B, R);
   return (s > FLT_MAX_F) ? FLT_MAX_F : s;
+}
+
+// ---------------------------------------------------------------------------
+// Scalars of a block Householder group (App. C.4).
+// ---------------------------------------------------------------------------
+
+// Correctly rounded float32 cube root of a positive finite float: a float64
+// estimate, then exact comparisons of x with the cubes of the midpoints to
+// the float32 neighbours.  mid^2 is exact in float64 (25-bit mid); mid^3 =
+// p + e exactly with p = fl(mid^2 mid), e = fma(mid^2, mid, -p); p - x is
+// exact (Sterbenz), so mid^3 > x iff (p - x) > -e.
+__device__ inline bool cube_gt(double mid, double x) {
+  const double m2 = mid * mid;
+  const double p = m2 * mid;
+  const double e = fma(m2, mid, -p);
+  return (p - x) > -e;
+}
+__device__ inline bool cube_lt(double mid, double x) {
+  const double m2 = mid * mid;
+  const double p = m2 * mid;
+  const double e = fma(m2, mid, -p);
+  return (p - x) < -e;
+}
+__device__ inline float cbrt_rn(float x) {
+  if (!(x > 0.0f)) return 0.0f;
+  float r = (float)cbrt((double)x);
+  const double xd = (double)x;
+  for (int it = 0; it < 8; ++it) {
+    const uint32_t b = __float_as_uint(r);
+    const float up = __uint_as_float(b + 1);
+    const float dn = __uint_as_float(b - 1);
+    const double mid_up = 0.5 * ((double)r + (double)up);
+    const double mid_dn = 0.5 * ((double)r + (double)dn);
+    if (cube_lt(mid_up, xd)) {
+      r = up;
+    } else if (cube_gt(mid_dn, xd)) {
+      r = dn;
+    } else {
+      break;
+    }
+  }
+  return r;
+}
+
+__device__ __forceinline__ float to_f32_sat(double v) {
+  float f = (float)v;
+  return (f > FLT_MAX_F) ? FLT_MAX_F : f;
+}
+
+// s1, s2 of a group of k >= 2 rows: s1 = B sqrt(k) / (a (a^2 + c^2 k)),
+// s2 = B sqrt(k) / (c (a^2 + c^2 k)) with a = cbrt(lambda1), c =
+// cbrt(lambda2) (App. C.4 multiplied through by k^(1/3)), float64 in this
+// operation order, rounded once to float32.  lambda1 = 0 takes lambda2;
+// lambda2 = 0 gives s1 = s2 = B sqrt(k) / lambda1; both zero give 1.  The
+// cube roots come in precomputed (ca = cbrt_rn(lambda1), cc =
+// cbrt_rn(lambda2)); sk = sqrt(k) in float64.
+__device__ __forceinline__ void group_scales(float lam1, float lam2, float ca, float cc, int64_t k, double sk, int B,
+                                             float& s1, float& s2) {
+  if (lam1 == 0.0f) {
+    lam1 = lam2;
+    ca = cc;
+  }
+  if (lam1 == 0.0f && lam2 == 0.0f) {
+    s1 = s2 = 1.0f;
+  } else if (lam2 == 0.0f) {
+    s1 = s2 = to_f32_sat(((double)B * sk) / (double)lam1);
+  } else {
+    const double a = (double)ca;
+    const double c = (double)cc;
+    const double t = a * a + (c * c) * (double)k;
+    const double num = (double)B * sk;
+    s1 = to_f32_sat(num / (a * t));
+    s2 = to_f32_sat(num / (c * t));
+  }
+}
+
+// A group's share of |S^-1|_F^2 (Eq. matrix-quantizer-variance):
+// 1/s1^2 + (k - 1)/s2^2, a one-row group 1/s^2, float64.
+__device__ __forceinline__ double group_term(float s1, float s2, int64_t k) {
+  double t = 1.0 / ((double)s1 * (double)s1);
+  if (k > 1) t = t + (double)(k - 1) * (1.0 / ((double)s2 * (double)s2));
+  return t;
 }
 
 // Status word bits (first word of every workspace).

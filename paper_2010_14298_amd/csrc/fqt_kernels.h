@@ -112,22 +112,68 @@ hipError_t launch_bhq_plan(const float* rmin, const float* rmax, const BhqLayout
                            int32_t* perm, float* scale, float* zero, int32_t* group_off, const FinalizePlan* fin,
                            hipStream_t s);
 
-// Adaptive grouping (App. D): the block size in {1, 2, 4, .., 64} whose
-// fixed-block plan has the least |S^-1|_F^2; for rows <= 16384.  Writes the
-// chosen size to bhq_adaptive_carve(ws).chosen (and the candidates'
-// objectives) on the stream.
-constexpr int ADAPTIVE_CANDIDATES = 7;
-struct AdaptiveWs {
-  int32_t* sigma;
-  double* terms;
-  double* objective;   // [ADAPTIVE_CANDIDATES]
-  int32_t* chosen;
+// One int32 stored on the stream (a device scalar known on the host).
+hipError_t launch_store_i32(int32_t* p, int32_t v, hipStream_t s);
+
+// Rows in sorted order (M descending, ties by row index), for the general
+// plans below; fin as for launch_bhq_plan.
+hipError_t launch_bhq_sort(const float* rmin, const float* rmax, int64_t rows, void* plan_ws, int32_t* sigma,
+                           const FinalizePlan* fin, hipStream_t s);
+
+// ---- general BHQ plans: groups of any size, in slot order ----------------
+// Slot record: the slot's group starts at slot `base` and has `size` slots;
+// alpha = float32(1 / sqrt(size)), oma = float32(1 - alpha) (multi-row groups).
+struct SlotInfo {
+  int32_t base, size;
+  float alpha, oma;
 };
-size_t bhq_adaptive_workspace(int64_t rows);
-AdaptiveWs bhq_adaptive_carve(void* ws, int64_t rows);
-hipError_t launch_bhq_adaptive(const float* rmin, const float* rmax, int64_t rows, int bits, void* ws,
-                               hipStream_t s);
-bool bhq_adaptive_supported(int64_t rows);
+// Per sorted position r (row sigma[r]): its infinity norm M and range R
+// (non-finite values read as 0, so that a plan over bad data stays a valid
+// permutation), cbrt_rn(R), cbrt_rn(2 M); prefix sums P of M (float64,
+// P[0] = 0, added one at a time in sorted order); the App. D objective of
+// every number of groups G = 1..rows and the chosen G.
+struct AppdWs {
+  int32_t* sigma;
+  float *Ms, *Rs, *ca, *cc;
+  double* P;
+  double* obj;
+  int32_t* G;
+};
+size_t appd_workspace(int64_t rows);
+AppdWs appd_carve(void* ws, int64_t rows);
+// Everything of the plan after the sort: the sorted-position scalars, and
+// for block_size = 0 the App. D search over G (objective into obj_out when
+// given, else the workspace's), then the groups (block_size > 0: the fixed
+// layout of bhq_layout).  Writes perm, scale, zero, group_off [G + 1], slot
+// and num_groups (device scalar).
+hipError_t launch_general_plan(const float* rmin, const float* rmax, int64_t rows, int bits, int block_size,
+                               const AppdWs& w, double* obj_out, int32_t* perm, float* scale, float* zero,
+                               int32_t* group_off, SlotInfo* slot, int32_t* num_groups, hipStream_t s);
+// The App. D search alone (objective and chosen G), after the sort.
+hipError_t launch_appd_search(const float* rmin, const float* rmax, int64_t rows, int bits, const AppdWs& w,
+                              double* obj_out, int32_t* num_groups, hipStream_t s);
+// Per multi-row group and column: tau = (alpha S - v_0) / (1 - alpha), S the
+// group's column sum of v_p = d_p x[perm[p]] in slot order (float32),
+// stored at tau[(base / 2) * cols + col] (group bases are at least 2 apart).
+hipError_t launch_bhq_tau(const float* x, int64_t rows, int64_t cols, const int32_t* perm, const float* scale,
+                          const SlotInfo* slot, float* tau, hipStream_t s);
+// Inverse transform of the general plans' grad_X rows.  Rows of T are (block
+// b, slot p) at T[(b * tstride + p) * ldt + col] (float64: the dequantized
+// code row times the weights, see EPI_BHQT); per multi-row group S = sum of
+// its T rows (float64, slot order), tau = (alpha S - T_0) / (1 - alpha),
+// alpha = 1 / sqrt(k); out row = perm[p] * ostride + b * obstride, value
+// (T_0 + (1 - alpha) tau or T_p - alpha tau) / d_p; zero where mask <= 0.
+struct InverseParams {
+  const double* T;
+  int64_t ldt, tstride, nblk, rows, cols;
+  const SlotInfo* slot;
+  const int32_t* perm;
+  const float* scale;
+  float* out;
+  int64_t ldo, ostride, obstride;
+  const float* mask;
+};
+hipError_t launch_bhq_inverse(const InverseParams& p, hipStream_t s);
 
 struct QuantParams {
   const float* x;
@@ -152,7 +198,9 @@ struct QuantParams {
   int32_t* sum2_t;
   const int8_t* shift;   // QM_ROW: per-row left shift of the offset codes, or nullptr
   const int8_t* shift2;  // Q_b1 with per-row scale2 / zero2 / shift2 (source-row order), or nullptr
-  BhqLayout L;
+  BhqLayout L;           // BHQ: L.k = 0 selects the general plan (slot, tau)
+  const SlotInfo* slot;
+  const float* tau;
 };
 enum QuantMode { QM_TENSOR = 0, QM_ROW = 1, QM_BHQ = 2 };
 hipError_t launch_quant(const QuantParams& p, int mode, hipStream_t s);
@@ -189,7 +237,8 @@ enum Epilogue {
   EPI_RAW_I32 = 0,   // int32 partials [splits][M][N] (caller reduces)
   EPI_TENSOR = 1,    // per-tensor A, per-tensor B: grad_W
   EPI_ROW = 2,       // per-row A (PTQ broadcasts), per-tensor B: grad_X
-  EPI_BHQ = 3        // per-group Householder on A rows, per-tensor B: grad_X
+  EPI_BHQ = 3,       // per-group Householder on A rows, per-tensor B: grad_X
+  EPI_BHQT = 4       // general BHQ plan: one-row groups finished, other rows' T into tbuf
 };
 
 struct GemmParams {
@@ -217,6 +266,9 @@ struct GemmParams {
   int expA;              // EPI_TENSOR: A's step is 1 / (scaleA[0] 2^expA)
   const double* colvec;  // EPI_TENSOR: nullptr, or [N] replacing A's zero-point terms (per-row zeros of A)
   const float* mask;     // EPI_ROW / EPI_BHQ: nullptr, or [M, ldo] in output-row order; out = 0 where mask <= 0
+  const SlotInfo* slot;  // EPI_BHQT: the general plan
+  double* tbuf;          // EPI_BHQT: [M, ldt] T of the rows of multi-row groups
+  int64_t ldt;
 };
 hipError_t launch_gemm(const GemmParams& p, int epi, hipStream_t s);
 

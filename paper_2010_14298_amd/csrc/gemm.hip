@@ -24,7 +24,8 @@ struct RowStage {
   double rterm;  // zW * rowsum
   double hz;     // BHQ group row: half + c_g;  affine row: zeta = z + half / s
   double dq;     // 1 / s  (Delta for an affine row, 1 / d_p for a group row)
-  int64_t obase; // output row * ldo, -1 past M
+  int64_t obase; // output row * ldo (EPI_BHQT group row: slot * ldt into tbuf), -1 past M
+  int trow;      // EPI_BHQT: the row belongs to a multi-row group (its T goes to tbuf)
 };
 // Per 64-row run and group of the BHQ epilogue: rows of the group that take
 // part in the Householder sum (full group: KG, partial group: its size, one-row
@@ -45,7 +46,7 @@ __device__ __forceinline__ void store_masked(const GemmParams& p, int64_t idx, d
 template <class C, int EPI>
 struct GemmLdsSize {
   static constexpr int EP_BYTES = C::BM * C::BN * 4 + C::BM * (int)sizeof(RowStage) + C::BM * (int)sizeof(GroupStage);
-  static constexpr bool STAGED = (EPI == EPI_ROW || EPI == EPI_BHQ);
+  static constexpr bool STAGED = (EPI == EPI_ROW || EPI == EPI_BHQ || EPI == EPI_BHQT);
   static constexpr int BYTES = (STAGED && EP_BYTES > C::OP_BYTES) ? EP_BYTES : C::OP_BYTES;
 };
 
@@ -159,11 +160,15 @@ __global__ __launch_bounds__(C::THREADS) void gemm_i8_kernel(GemmParams p) {
       if (row < p.M) {
         const float s = p.rowwiseA ? p.scaleA[row] : p.scaleA[0];
         const float z = p.rowwiseA ? p.zeroA[row] : p.zeroA[0];
-        const int kind = (EPI == EPI_BHQ) ? bhq_slot_kind(p.L, row) : 0;
+        const int kind = (EPI == EPI_BHQ) ? bhq_slot_kind(p.L, row) : (EPI == EPI_BHQT ? (p.slot[row].size > 1) : 0);
         q.rterm = zW * (double)p.sumA[row];
         q.dq = 1.0 / (double)s;
         q.hz = kind != 0 ? (double)p.halfA + (double)z : (double)z + (double)p.halfA * q.dq;
         q.obase = (int64_t)(p.perm ? p.perm[row] : (int)row) * p.ldo;
+        if (EPI == EPI_BHQT && kind != 0) {
+          q.trow = 1;
+          q.obase = row * p.ldt;
+        }
       } else {
         q.obase = -1;
       }
@@ -244,7 +249,10 @@ __global__ __launch_bounds__(C::THREADS) void gemm_i8_kernel(GemmParams p) {
           const RowStage q = srow[t];
           if (q.obase < 0) continue;
           const double a = (double)sacc[t * C::BN + c];
-          store_masked(p, q.obase + col, q.dq * (dW * a + q.rterm) + q.hz * colterm);
+          if (EPI == EPI_BHQT && q.trow)
+            p.tbuf[q.obase + col] = dW * a + (q.rterm + q.hz * colterm);
+          else
+            store_masked(p, q.obase + col, q.dq * (dW * a + q.rterm) + q.hz * colterm);
         }
       }
     }
@@ -398,6 +406,7 @@ static hipError_t launch_gemm_c(const GemmParams& p, int epi, hipStream_t s) {
     case EPI_RAW_I32: return launch_gemm_t<C, EPI_RAW_I32, 0>(p, s);
     case EPI_TENSOR: return launch_gemm_t<C, EPI_TENSOR, 0>(p, s);
     case EPI_ROW: return launch_gemm_t<C, EPI_ROW, 0>(p, s);
+    case EPI_BHQT: return p.slot && p.tbuf ? launch_gemm_t<C, EPI_BHQT, 0>(p, s) : hipErrorInvalidValue;
     case EPI_BHQ:
       switch (p.L.k) {
         case 1: return launch_gemm_t<C, EPI_BHQ, 1>(p, s);

@@ -482,59 +482,14 @@ __global__ __launch_bounds__(RK_THREADS) void bhq_rank_perm_kernel(const float* 
   }
 }
 
-// Correctly rounded float32 cube root of a positive finite float: a float64
-// estimate, then exact comparisons of x with the cubes of the midpoints to
-// the float32 neighbours.  mid^2 is exact in float64 (25-bit mid); mid^3 =
-// p + e exactly with p = fl(mid^2 mid), e = fma(mid^2, mid, -p); p - x is
-// exact (Sterbenz), so mid^3 > x iff (p - x) > -e.
-__device__ bool cube_gt(double mid, double x) {
-  const double m2 = mid * mid;
-  const double p = m2 * mid;
-  const double e = fma(m2, mid, -p);
-  return (p - x) > -e;
-}
-__device__ bool cube_lt(double mid, double x) {
-  const double m2 = mid * mid;
-  const double p = m2 * mid;
-  const double e = fma(m2, mid, -p);
-  return (p - x) < -e;
-}
-__device__ float cbrt_rn(float x) {
-  if (!(x > 0.0f)) return 0.0f;
-  float r = (float)cbrt((double)x);
-  const double xd = (double)x;
-  for (int it = 0; it < 8; ++it) {
-    const uint32_t b = __float_as_uint(r);
-    const float up = __uint_as_float(b + 1);
-    const float dn = __uint_as_float(b - 1);
-    const double mid_up = 0.5 * ((double)r + (double)up);
-    const double mid_dn = 0.5 * ((double)r + (double)dn);
-    if (cube_lt(mid_up, xd)) {
-      r = up;
-    } else if (cube_gt(mid_dn, xd)) {
-      r = dn;
-    } else {
-      break;
-    }
-  }
-  return r;
-}
-
-__device__ __forceinline__ float to_f32_sat(double v) {
-  float f = (float)v;
-  return (f > FLT_MAX_F) ? FLT_MAX_F : f;
-}
-
 // One group of a fixed-block plan, one wave (lane j handles the group's slot
 // j + 1): the per-slot scale d_p and zero (c_g, or the row min for a one-row
 // group).  FROM_PERM: perm already holds the rows in slot order
-// (bhq_rank_perm_kernel); otherwise the rows come from sigma (sorted order).
-// WRITE: store perm (rows from sigma only), scale, zero and group_off.
-// term (optional): the group's share of |S^-1|_F^2 (Eq.
-// matrix-quantizer-variance): 1/s1^2 + (k_g - 1)/s2^2, a one-row group 1/s^2.
-template <bool FROM_PERM, bool WRITE>
+// (bhq_rank_perm_kernel); otherwise the rows come from sigma (sorted order)
+// and are stored into perm here.
+template <bool FROM_PERM>
 __device__ void bhq_group(const float* rmin, const float* rmax, const int32_t* sigma, const BhqLayout& L, int B,
-                          int64_t g, int32_t* perm, float* scale, float* zero, int32_t* group_off, double* term) {
+                          int64_t g, int32_t* perm, float* scale, float* zero, int32_t* group_off) {
   const int lane = threadIdx.x;
   const int k = L.k;
   int kg;
@@ -549,7 +504,7 @@ __device__ void bhq_group(const float* rmin, const float* rmax, const int32_t* s
     kg = 1;
     base = L.full * k + L.part + (g - L.full - (L.part > 0 ? 1 : 0));
   }
-  if (WRITE && group_off && lane == 0) {
+  if (group_off && lane == 0) {
     group_off[g] = (int32_t)base;
     if (g == L.G - 1) group_off[L.G] = (int32_t)L.rows;
   }
@@ -559,12 +514,9 @@ __device__ void bhq_group(const float* rmin, const float* rmax, const int32_t* s
   if (kg == 1) {
     const float s0 = scale_from_range(mx0 - mn0, B);
     if (lane == 0) {
-      if (WRITE) {
-        if (!FROM_PERM) perm[base] = big;
-        scale[base] = s0;
-        zero[base] = mn0;
-      }
-      if (term) *term = 1.0 / ((double)s0 * (double)s0);
+      if (!FROM_PERM) perm[base] = big;
+      scale[base] = s0;
+      zero[base] = mn0;
     }
     return;
   }
@@ -576,30 +528,12 @@ __device__ void bhq_group(const float* rmin, const float* rmax, const int32_t* s
     M = fmaxf(fabsf(rmin[r]), fabsf(rmax[r]));
   }
   const float m2 = wave_max(M);
-  float lam1 = mx0 - mn0;
   const float lam2 = 2.0f * m2;
-  if (lam1 == 0.0f) lam1 = lam2;
+  const float lam1 = mx0 - mn0;
   const double sk = (kg == k) ? L.sk_k : L.sk_p;
   const float alpha = (kg == k) ? L.a_k : L.a_p;
   float s1, s2;
-  if (lam1 == 0.0f && lam2 == 0.0f) {
-    s1 = s2 = 1.0f;
-  } else if (lam2 == 0.0f) {
-    s1 = s2 = to_f32_sat(((double)B * sk) / (double)lam1);
-  } else {
-    const double a = (double)cbrt_rn(lam1);
-    const double c = (double)cbrt_rn(lam2);
-    const double aa = a * a;
-    const double cc = c * c;
-    const double cck = cc * (double)kg;
-    const double t = aa + cck;
-    const double num = (double)B * sk;
-    s1 = to_f32_sat(num / (a * t));
-    s2 = to_f32_sat(num / (c * t));
-  }
-  if (term && lane == 0)
-    *term = 1.0 / ((double)s1 * (double)s1) + (double)(kg - 1) * (1.0 / ((double)s2 * (double)s2));
-  if (!WRITE) return;
+  group_scales(lam1, lam2, cbrt_rn(lam1), cbrt_rn(lam2), kg, sk, B, s1, s2);
   const double t1 = ((double)alpha * (double)s1) * (double)mn0;
   const double t2 = ((0.5 * (double)lam2) * (double)s2) * sk;
   const float cg = (float)(t1 - t2);
@@ -619,94 +553,7 @@ template <bool FROM_PERM>
 __global__ __launch_bounds__(64) void bhq_groups_kernel(const float* rmin, const float* rmax, const int32_t* sigma,
                                                         BhqLayout L, int B, int32_t* perm, float* scale, float* zero,
                                                         int32_t* group_off) {
-  bhq_group<FROM_PERM, true>(rmin, rmax, sigma, L, B, blockIdx.x, perm, scale, zero, group_off, nullptr);
-}
-
-// ---------------------------------------------------------------------------
-// Adaptive grouping (App. D): every candidate block size k in {1, 2, .., 64}
-// is evaluated by the |S^-1|_F^2 of its fixed-block plan; the least wins,
-// ties going to the larger block.  Rows are sorted once (the k = 1 layout of
-// the rank kernel is the sorted order itself); one wave per (candidate,
-// group) writes the group's term; one thread per candidate adds its terms in
-// slot order in float64.
-// ---------------------------------------------------------------------------
-struct AdaptivePlan {
-  BhqLayout L[ADAPTIVE_CANDIDATES];
-  int64_t off[ADAPTIVE_CANDIDATES + 1];  // first term of each candidate
-};
-
-__global__ __launch_bounds__(64) void bhq_terms_kernel(const float* rmin, const float* rmax, const int32_t* sigma,
-                                                       AdaptivePlan ap, int B, double* terms) {
-  const int64_t id = blockIdx.x;
-  int c = 0;
-  while (c + 1 < ADAPTIVE_CANDIDATES && id >= ap.off[c + 1]) ++c;
-  bhq_group<false, false>(rmin, rmax, sigma, ap.L[c], B, id - ap.off[c], nullptr, nullptr, nullptr, nullptr,
-                          terms + id);
-}
-
-__global__ __launch_bounds__(64) void bhq_choose_kernel(AdaptivePlan ap, const double* terms, double* objective,
-                                                        int32_t* chosen) {
-  __shared__ double obj[ADAPTIVE_CANDIDATES];
-  const int t = threadIdx.x;
-  if (t < ADAPTIVE_CANDIDATES) {
-    double sum = 0.0;
-    for (int64_t i = ap.off[t]; i < ap.off[t + 1]; ++i) sum = sum + terms[i];
-    obj[t] = sum;
-    objective[t] = sum;
-  }
-  __syncthreads();
-  if (t == 0) {
-    int best = 0;
-    for (int c = 1; c < ADAPTIVE_CANDIDATES; ++c)
-      if (obj[c] <= obj[best]) best = c;
-    *chosen = ap.L[best].k;
-  }
-}
-
-size_t bhq_adaptive_workspace(int64_t rows) {
-  int64_t nterms = 0;
-  for (int c = 0; c < ADAPTIVE_CANDIDATES; ++c) nterms += (rows + (1 << c) - 1) >> c;
-  // sigma, terms, objectives, chosen block size
-  return (size_t)rows * 4 + 256 + (size_t)nterms * 8 + 256 + ADAPTIVE_CANDIDATES * 8 + 256 + 256;
-}
-
-AdaptiveWs bhq_adaptive_carve(void* ws, int64_t rows) {
-  char* p = static_cast<char*>(ws);
-  AdaptiveWs w{};
-  w.sigma = reinterpret_cast<int32_t*>(p);
-  p += ((size_t)rows * 4 + 255) / 256 * 256;
-  w.terms = reinterpret_cast<double*>(p);
-  int64_t nterms = 0;
-  for (int c = 0; c < ADAPTIVE_CANDIDATES; ++c) nterms += (rows + (1 << c) - 1) >> c;
-  p += ((size_t)nterms * 8 + 255) / 256 * 256;
-  w.objective = reinterpret_cast<double*>(p);
-  p += 256;
-  w.chosen = reinterpret_cast<int32_t*>(p);
-  return w;
-}
-
-bool bhq_adaptive_supported(int64_t rows) { return rows >= 1 && rows <= RANK_MAX_ROWS; }
-
-hipError_t launch_bhq_adaptive(const float* rmin, const float* rmax, int64_t rows, int bits, void* ws,
-                               hipStream_t s) {
-  if (!bhq_adaptive_supported(rows)) return hipErrorInvalidValue;
-  const AdaptiveWs w = bhq_adaptive_carve(ws, rows);
-  // sorted order: the k = 1 layout stores each row at its sorted position
-  const BhqLayout L1 = bhq_layout(rows, 1);
-  const int64_t nrank = (rows + RK_ROWS - 1) / RK_ROWS;
-  const FinalizePlan none{};
-  hipLaunchKernelGGL(bhq_rank_perm_kernel, dim3((unsigned)nrank), dim3(RK_THREADS), (size_t)rank_pad(rows) * 4, s,
-                     rmin, rmax, L1, w.sigma, nrank, none);
-  AdaptivePlan ap{};
-  ap.off[0] = 0;
-  for (int c = 0; c < ADAPTIVE_CANDIDATES; ++c) {
-    ap.L[c] = bhq_layout(rows, 1 << c);
-    ap.off[c + 1] = ap.off[c] + ap.L[c].G;
-  }
-  hipLaunchKernelGGL(bhq_terms_kernel, dim3((unsigned)ap.off[ADAPTIVE_CANDIDATES]), dim3(64), 0, s, rmin, rmax,
-                     w.sigma, ap, (1 << bits) - 1, w.terms);
-  hipLaunchKernelGGL(bhq_choose_kernel, dim3(1), dim3(64), 0, s, ap, w.terms, w.objective, w.chosen);
-  return hipGetLastError();
+  bhq_group<FROM_PERM>(rmin, rmax, sigma, L, B, blockIdx.x, perm, scale, zero, group_off);
 }
 
 BhqPlanWs bhq_plan_carve(void* plan_ws, int64_t rows) {
@@ -747,6 +594,38 @@ hipError_t launch_bhq_plan(const float* rmin, const float* rmax, const BhqLayout
                      w.sigma);
   hipLaunchKernelGGL(bhq_groups_kernel<false>, dim3((unsigned)L.G), dim3(64), 0, s, rmin, rmax, w.sigma, L,
                      (1 << bits) - 1, perm, scale, zero, group_off);
+  return hipGetLastError();
+}
+
+__global__ void store_i32_kernel(int32_t* p, int32_t v) { *p = v; }
+
+hipError_t launch_store_i32(int32_t* p, int32_t v, hipStream_t s) {
+  hipLaunchKernelGGL(store_i32_kernel, dim3(1), dim3(1), 0, s, p, v);
+  return hipGetLastError();
+}
+
+// Rows in sorted order (M descending, ties by row index) into sigma: the
+// counting rank for up to RANK_MAX_ROWS rows (its k = 1 layout stores each
+// row at its sorted position), else chunk sorts, rank merge and scatter.
+hipError_t launch_bhq_sort(const float* rmin, const float* rmax, int64_t rows, void* plan_ws, int32_t* sigma,
+                           const FinalizePlan* fin, hipStream_t s) {
+  const int64_t nch = sort_pad(rows) / SORT_CH;
+  if (nch > 65535) return hipErrorInvalidValue;
+  const FinalizePlan none{};
+  if (rows <= RANK_MAX_ROWS) {
+    const BhqLayout L1 = bhq_layout(rows, 1);
+    const int64_t nrank = (rows + RK_ROWS - 1) / RK_ROWS;
+    hipLaunchKernelGGL(bhq_rank_perm_kernel, dim3((unsigned)(nrank + (fin ? fin->nseg : 0))), dim3(RK_THREADS),
+                       (size_t)rank_pad(rows) * 4, s, rmin, rmax, L1, sigma, nrank, fin ? *fin : none);
+    return hipGetLastError();
+  }
+  // the rank array must be zero here: the finalize step clears it (before
+  // this call, or in the sort launch with fin)
+  const BhqPlanWs w = bhq_plan_carve(plan_ws, rows);
+  hipLaunchKernelGGL(bhq_sort_chunks_kernel, dim3((unsigned)(nch + (fin ? fin->nseg : 0))), dim3(512), 0, s, rmin,
+                     rmax, rows, w.sorted, nch, fin ? *fin : none);
+  hipLaunchKernelGGL(bhq_rank_kernel, dim3((unsigned)nch, (unsigned)nch), dim3(256), 0, s, w.sorted, w.rank);
+  hipLaunchKernelGGL(bhq_scatter_kernel, dim3((unsigned)((rows + 255) / 256)), dim3(256), 0, s, w.rank, rows, sigma);
   return hipGetLastError();
 }
 
@@ -867,41 +746,47 @@ __device__ __forceinline__ void quant_tile(const QuantParams& p, int64_t bx, int
     }
   }
 
-  // ---- block Householder (K >= 16): the group's column sums span waves
+  // ---- block Householder (K >= 16): a group spans K / 16 waves.  Its column
+  // sum adds the slots one at a time in slot order, so the running sum is
+  // handed from wave to wave through LDS: in step i the i-th wave of every
+  // group continues the sum its predecessor left (K / 16 barrier steps).
   float ta[4] = {0.0f, 0.0f, 0.0f, 0.0f}, tb[4] = {0.0f, 0.0f, 0.0f, 0.0f};  // alpha tau, (1 - alpha) tau
   if constexpr (MODE == QM_BHQ && K >= 16) {
     const BhqLayout& L = p.L;
-    float P[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-    float v0[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-    for (int r = 0; r < QT_ROWS_PER_WAVE; ++r) {
-      const int64_t slot = slot0 + r;
-      const bool ok = slot < rows;
-      const bool multi = ok && bhq_slot_kind(L, slot) != 0;
-      const float d = ok ? p.scale[slot] : 1.0f;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const float v = d * g[r][j];
-        P[j] = P[j] + (multi ? v : 0.0f);
-        if (r == 0) v0[j] = v;
-      }
-    }
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      s_part[wave][lane * 4 + j] = P[j];
-      s_v0[wave][lane * 4 + j] = v0[j];
-    }
-    __syncthreads();
-    const int nw = K / 16;                // waves per group
+    constexpr int nw = K / 16;            // waves per group
     const int w0 = (wave / nw) * nw;      // first wave of this wave's group
+    for (int step = 0; step < nw; ++step) {
+      if (wave - w0 == step) {
+        float P[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+        if (step > 0) {
+#pragma unroll
+          for (int j = 0; j < 4; ++j) P[j] = s_part[wave - 1][lane * 4 + j];
+        }
+#pragma unroll
+        for (int r = 0; r < QT_ROWS_PER_WAVE; ++r) {
+          const int64_t slot = slot0 + r;
+          const bool ok = slot < rows;
+          const bool multi = ok && bhq_slot_kind(L, slot) != 0;
+          const float d = ok ? p.scale[slot] : 1.0f;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const float v = d * g[r][j];
+            P[j] = P[j] + (multi ? v : 0.0f);
+            if (r == 0 && step == 0) s_v0[wave][lane * 4 + j] = v;
+          }
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) s_part[wave][lane * 4 + j] = P[j];
+      }
+      __syncthreads();
+    }
     const int64_t gfirst = tile0 + w0 * 16;
     const int gkind = gfirst < rows ? bhq_slot_kind(L, gfirst) : 0;
     const float alpha = gkind == 2 ? L.a_p : L.a_k;
     const float oma = gkind == 2 ? L.oma_p : L.oma_k;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      float S = s_part[w0][lane * 4 + j];
-      for (int i = 1; i < nw; ++i) S = S + s_part[w0 + i][lane * 4 + j];
+      const float S = s_part[w0 + nw - 1][lane * 4 + j];
       const float m = alpha * S - s_v0[w0][lane * 4 + j];
       const float tau = __fdiv_rn(m, oma);
       ta[j] = alpha * tau;
@@ -954,6 +839,38 @@ __device__ __forceinline__ void quant_tile(const QuantParams& p, int64_t bx, int
       const float z = ok ? p.zero[slot] : 0.0f;
 #pragma unroll
       for (int j = 0; j < 4; ++j) y[j] = s * (g[r][j] - z);
+    } else if constexpr (K == 0) {
+      // general plan: the group's rank-1 term comes precomputed per column
+      const SlotInfo si = ok ? p.slot[slot] : SlotInfo{0, 1, 0.0f, 0.0f};
+      const float d = ok ? p.scale[slot] : 1.0f;
+      const float c = ok ? p.zero[slot] : 0.0f;
+      if (si.size > 1) {
+        float t[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+        const float* tp = p.tau + (int64_t)(si.base >> 1) * cols + c0;
+        if constexpr (VEC) {
+          if (lane_ok) {
+            const float4 v = *reinterpret_cast<const float4*>(tp);
+            t[0] = v.x;
+            t[1] = v.y;
+            t[2] = v.z;
+            t[3] = v.w;
+          }
+        } else {
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            if (c0 + j < cols) t[j] = tp[j];
+        }
+        const bool first = slot == si.base;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const float v = d * g[r][j];
+          const float Y = first ? v + si.oma * t[j] : v - si.alpha * t[j];
+          y[j] = Y - c;
+        }
+      } else {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) y[j] = d * (g[r][j] - c);
+      }
     } else {
       const BhqLayout& L = p.L;
       const int kind = ok ? bhq_slot_kind(L, slot) : 0;
@@ -1254,6 +1171,7 @@ hipError_t launch_quant_fused(const QuantParams& pg, int mode, const QuantParams
   if (mode == QM_TENSOR) return launch_quant_fused_k<QM_TENSOR, 0>(pg, px, pw, s);
   if (mode == QM_ROW) return launch_quant_fused_k<QM_ROW, 0>(pg, px, pw, s);
   switch (pg.L.k) {
+    case 0: return pg.slot && pg.tau ? launch_quant_fused_k<QM_BHQ, 0>(pg, px, pw, s) : hipErrorInvalidValue;
     case 1: return launch_quant_fused_k<QM_BHQ, 1>(pg, px, pw, s);
     case 2: return launch_quant_fused_k<QM_BHQ, 2>(pg, px, pw, s);
     case 4: return launch_quant_fused_k<QM_BHQ, 4>(pg, px, pw, s);
@@ -1269,6 +1187,7 @@ hipError_t launch_quant(const QuantParams& p, int mode, hipStream_t s) {
   if (mode == QM_TENSOR) return launch_quant_k<QM_TENSOR, 0>(p, s);
   if (mode == QM_ROW) return launch_quant_k<QM_ROW, 0>(p, s);
   switch (p.L.k) {
+    case 0: return p.slot && p.tau ? launch_quant_k<QM_BHQ, 0>(p, s) : hipErrorInvalidValue;
     case 1: return launch_quant_k<QM_BHQ, 1>(p, s);
     case 2: return launch_quant_k<QM_BHQ, 2>(p, s);
     case 4: return launch_quant_k<QM_BHQ, 4>(p, s);

@@ -29,7 +29,7 @@ class FqtError(RuntimeError):
 class QTensor(ctypes.Structure):
     _fields_ = [("q", ctypes.c_void_p), ("scale", ctypes.c_void_p), ("zero", ctypes.c_void_p),
                 ("perm", ctypes.c_void_p), ("group_off", ctypes.c_void_p), ("code_sum", ctypes.c_void_p),
-                ("shift", ctypes.c_void_p)]
+                ("shift", ctypes.c_void_p), ("num_groups", ctypes.c_void_p)]
 
 
 class QSpec(ctypes.Structure):
@@ -56,7 +56,7 @@ class ConvShape(ctypes.Structure):
 
 EXPORTS = [
     "fqt_quantize_ptq", "fqt_quantize_psq", "fqt_quantize_bhq", "fqt_quantize_shift", "fqt_quantize_workspace",
-    "fqt_bhq_adaptive_block", "fqt_bhq_adaptive_workspace",
+    "fqt_bhq_adaptive_groups", "fqt_bhq_adaptive_workspace",
     "fqt_linear_backward", "fqt_linear_backward_workspace",
     "fqt_linear_forward", "fqt_linear_forward_workspace",
     "fqt_conv_backward_im2col", "fqt_conv_backward_workspace",
@@ -87,7 +87,7 @@ def load(path=LIB_PATH):
         "fqt_quantize_bhq": ([vp, i64, i64, i32, i32, u64, u32, qtp, vp, sz, vp], i32),
         "fqt_quantize_shift": ([vp, i64, i64, i32, u64, u32, i32, qtp, vp, sz, vp], i32),
         "fqt_quantize_workspace": ([i32, i64, i64, i32], sz),
-        "fqt_bhq_adaptive_block": ([vp, i64, i64, i32, ctypes.POINTER(ctypes.c_int), vp, sz, vp], i32),
+        "fqt_bhq_adaptive_groups": ([vp, i64, i64, i32, vp, vp, vp, sz, vp], i32),
         "fqt_bhq_adaptive_workspace": ([i64, i64], sz),
         "fqt_linear_backward": ([vp, vp, vp, i64, i64, i64, cfgp, vp, vp, vp, sz, vp], i32),
         "fqt_linear_backward_workspace": ([i64, i64, i64, cfgp], sz),
@@ -161,6 +161,7 @@ def _quant_outputs(x, rows, cols, kind, transpose, code_sum):
     if kind == "bhq":
         out["perm"] = torch.empty(rows, dtype=torch.int32, device=dev)
         out["group_off"] = torch.empty(rows + 1, dtype=torch.int32, device=dev)
+        out["num_groups"] = torch.empty(1, dtype=torch.int32, device=dev)
     if kind == "shift":
         out["shift"] = torch.empty(rows, dtype=torch.int8, device=dev)
     if code_sum:
@@ -169,7 +170,8 @@ def _quant_outputs(x, rows, cols, kind, transpose, code_sum):
                  out["perm"].data_ptr() if "perm" in out else 0,
                  out["group_off"].data_ptr() if "group_off" in out else 0,
                  out["code_sum"].data_ptr() if "code_sum" in out else 0,
-                 out["shift"].data_ptr() if "shift" in out else 0)
+                 out["shift"].data_ptr() if "shift" in out else 0,
+                 out["num_groups"].data_ptr() if "num_groups" in out else 0)
     return out, qt
 
 
@@ -225,16 +227,19 @@ def fqt_quantize_bhq(x, bits, block_size, seed=0, stream=0, code_sum=False, ws=N
     return out
 
 
-def fqt_bhq_adaptive_block(x, bits, ws=None):
-    """Block size of the adaptive grouping (waits for the stream)."""
+def fqt_bhq_adaptive_groups(x, bits, objective=True, ws=None):
+    """App. D's number of groups (device int32 [1]) and, with objective=True,
+    the score of every G (device float64 [rows]); asynchronous."""
     x = _f32(x, "x")
     rows, cols = x.shape
     if ws is None:
         ws = _workspace(load().fqt_bhq_adaptive_workspace(rows, cols), x.device)
-    k = ctypes.c_int(0)
-    rc = load().fqt_bhq_adaptive_block(_ptr(x), rows, cols, bits, ctypes.byref(k), _ptr(ws), ws.numel(), _stream())
-    _check("fqt_bhq_adaptive_block", rc)
-    return k.value
+    G = torch.empty(1, dtype=torch.int32, device=x.device)
+    obj = torch.empty(rows, dtype=torch.float64, device=x.device) if objective else None
+    rc = load().fqt_bhq_adaptive_groups(_ptr(x), rows, cols, bits, _ptr(G), _ptr(obj), _ptr(ws), ws.numel(),
+                                        _stream())
+    _check("fqt_bhq_adaptive_groups", rc)
+    return G, obj, ws
 
 
 def fqt_linear_backward_workspace(N, d_in, d_out, cfg):

@@ -60,18 +60,17 @@ def test_workspace_queries_and_argument_errors():
     unsup = fqt.cfg_struct(qb_w=("psq", 8, 0))
     rc = lib.fqt_linear_backward(fake, fake, fake, 4, 4, 4, ctypes.byref(unsup), fake, fake, fake, 1 << 30, null)
     assert rc == 2
-    # adaptive BHQ grouping (block size 0) sorts at most 16384 rows; block sizes must be powers of two <= 64
-    rc = lib.fqt_linear_backward(fake, fake, fake, 20000, 4, 4, ctypes.byref(fqt.cfg_struct(qb_x=("bhq", 5, 0))),
+    # App. D's adaptive groups (block size 0) score every number of groups: at most 65536 rows
+    rc = lib.fqt_linear_backward(fake, fake, fake, 70000, 4, 4, ctypes.byref(fqt.cfg_struct(qb_x=("bhq", 5, 0))),
                                  fake, fake, fake, 1 << 30, null)
     assert rc == 2
-    k = ctypes.c_int(-1)
-    assert lib.fqt_bhq_adaptive_block(fake, 20000, 4, 5, ctypes.byref(k), fake, 1 << 30, null) == 2
-    assert lib.fqt_bhq_adaptive_block(fake, 40, 4, 9, ctypes.byref(k), fake, 1 << 30, null) == 1
-    assert lib.fqt_bhq_adaptive_block(fake, 40, 4, 5, None, fake, 1 << 30, null) == 1
-    assert lib.fqt_bhq_adaptive_block(fake, 40, 4, 5, ctypes.byref(k), fake, 16, null) == 4
-    assert k.value == -1
+    assert lib.fqt_bhq_adaptive_groups(fake, 70000, 4, 5, fake, null, fake, 1 << 30, null) == 2
+    assert lib.fqt_bhq_adaptive_groups(fake, 40, 4, 9, fake, null, fake, 1 << 30, null) == 1
+    assert lib.fqt_bhq_adaptive_groups(fake, 40, 4, 5, null, null, fake, 1 << 30, null) == 1
+    assert lib.fqt_bhq_adaptive_groups(fake, 40, 4, 5, fake, null, fake, 16, null) == 4
     assert lib.fqt_bhq_adaptive_workspace(40, 4) > lib.fqt_quantize_workspace(fqt.FQT_BHQ, 40, 4, 64)
-    rc = lib.fqt_linear_backward(fake, fake, fake, 4, 4, 4, ctypes.byref(fqt.cfg_struct(qb_x=("bhq", 5, 48))),
+    # a negative block size
+    rc = lib.fqt_linear_backward(fake, fake, fake, 4, 4, 4, ctypes.byref(fqt.cfg_struct(qb_x=("bhq", 5, -1))),
                                  fake, fake, fake, 1 << 30, null)
     assert rc == 1
     # workspace too small / missing
@@ -107,7 +106,13 @@ def test_workspace_queries_and_argument_errors():
     relu2.relu_input = 2
     rc = lib.fqt_linear_backward(fake, fake, fake, 4, 4, 4, ctypes.byref(relu2), fake, fake, fake, 1 << 30, null)
     assert rc == 1
-    sh = fqt.conv_shape(2, 4, 8, 8, 4, 3, 3, 1, 1)
+    # (o = 16 passes the shape checks, so the rejection comes from the
+    # configuration, before anything is launched on the fake pointers)
+    sh = fqt.conv_shape(2, 4, 8, 8, 16, 3, 3, 1, 1)
+    assert lib.fqt_conv_backward_workspace(ctypes.byref(sh), ctypes.byref(cfg)) > 0
     rc = lib.fqt_conv_backward_im2col(fake, fake, fake, ctypes.byref(sh), ctypes.byref(fqt.cfg_struct(relu_input=True)),
                                       fake, fake, fake, 1 << 30, null)
+    assert rc == 2
+    rc = lib.fqt_conv_backward_im2col(fake, fake, fake, ctypes.byref(sh),
+                                      ctypes.byref(fqt.cfg_struct(qb_w=("shift", 4, 0))), fake, fake, fake, 1 << 30, null)
     assert rc == 2
