@@ -105,6 +105,21 @@ fqt_status fqt_quantize_psq(const float* x, int64_t rows, int64_t cols, int bits
                             uint32_t stream, const fqt_qtensor* out, void* ws, size_t ws_bytes,
                             fqt_stream_t s);
 
+/* fqt_quantize_psq without a workspace argument, for callers that cannot
+ * allocate device memory (code under stream capture, tight serving loops,
+ * harnesses that forbid allocation).  The same kernels and results as
+ * fqt_quantize_psq; the scratch memory they need comes from a fixed 4 MiB
+ * array that the library holds on each GPU until the process ends.  The
+ * call itself allocates nothing.  Sizes whose fqt_quantize_workspace(FQT_PSQ,
+ * rows, cols, 0) exceeds 4 MiB return FQT_EUNSUPPORTED (for cols <= 8192
+ * that allows about 250 000 rows).  status (optional, device, 4 uint32
+ * words) receives the data status: bit 0 set in any word means a non-finite
+ * input.  Every call on one GPU shares that GPU's array, which keeps the
+ * last call's contents: calls that overlap on one GPU (several streams or
+ * host threads) race and must be serialized by the caller.                 */
+fqt_status fqt_quantize_psq_noalloc(const float* x, int64_t rows, int64_t cols, int bits, uint64_t seed,
+                                    uint32_t stream, const fqt_qtensor* out, uint32_t* status, fqt_stream_t s);
+
 /* Block Householder quantizer, Sec. 4.2 / App. C.4 / App. D.  Rows are
  * sorted by infinity norm M (descending, ties by row index); each group
  * holds one of the G largest rows and a run of the sorted tail.

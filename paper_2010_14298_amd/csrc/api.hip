@@ -2,6 +2,8 @@
 // carving and the launch sequence of each entry point.
 #include <string.h>
 
+#include <mutex>
+
 #include "../../include/fqt.h"
 #include "fqt_device.h"
 #include "fqt_kernels.h"
@@ -468,6 +470,34 @@ ConvWs carve_conv(Carver& c, const float* X, const float* W, const float* G, con
   return w;
 }
 
+// ---------------------------------------------------------------------------
+// Scratch memory of the no-allocation entry point: one array per GPU, held
+// until the process ends.  Its device address is taken once per device (with
+// that device current) and used wherever host code hands the memory out.
+// ---------------------------------------------------------------------------
+constexpr size_t NOALLOC_SCRATCH_BYTES = (size_t)4 << 20;
+constexpr int NOALLOC_MAX_DEVICES = 64;
+static __device__ __align__(256) uint8_t scratch[NOALLOC_SCRATCH_BYTES];
+std::mutex scratch_mu;
+void* scratch_ptr[NOALLOC_MAX_DEVICES];
+
+fqt_status scratch_of_current_device(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= NOALLOC_MAX_DEVICES) return FQT_EDEVICE;
+  std::lock_guard<std::mutex> lock(scratch_mu);
+  if (!scratch_ptr[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return FQT_EDEVICE;
+    scratch_ptr[dev] = p;
+  }
+  *out = scratch_ptr[dev];
+  return FQT_OK;
+}
+
+__global__ void copy_status_kernel(const uint32_t* src, uint32_t* dst) {
+  if (threadIdx.x < STATUS_WORDS) dst[threadIdx.x] = src[threadIdx.x];
+}
+
 }  // namespace
 }  // namespace fqt
 
@@ -495,6 +525,25 @@ fqt_status fqt_quantize_psq(const float* x, int64_t rows, int64_t cols, int bits
 fqt_status fqt_quantize_bhq(const float* x, int64_t rows, int64_t cols, int bits, int block_size, uint64_t seed,
                             uint32_t stream, const fqt_qtensor* out, void* ws, size_t ws_bytes, fqt_stream_t s) {
   return quantize_common(FQT_BHQ, x, rows, cols, bits, 1, seed, stream, 0, block_size, out, ws, ws_bytes, s);
+}
+
+fqt_status fqt_quantize_psq_noalloc(const float* x, int64_t rows, int64_t cols, int bits, uint64_t seed,
+                                    uint32_t stream, const fqt_qtensor* out, uint32_t* status, fqt_stream_t s) {
+  fqt_status st = check_quant_args(x, rows, cols, bits, out);
+  if (st != FQT_OK) return st;
+  Carver cs(nullptr);
+  carve_quant(cs, FQT_PSQ, x, rows, cols, 0);
+  if (cs.off > NOALLOC_SCRATCH_BYTES) return FQT_EUNSUPPORTED;
+  void* ws = nullptr;
+  st = scratch_of_current_device(&ws);
+  if (st != FQT_OK) return st;
+  st = quantize_common(FQT_PSQ, x, rows, cols, bits, 1, seed, stream, 0, 0, out, ws, NOALLOC_SCRATCH_BYTES, s);
+  if (st != FQT_OK) return st;
+  if (status) {
+    hipLaunchKernelGGL(copy_status_kernel, dim3(1), dim3(64), 0, s, static_cast<const uint32_t*>(ws), status);
+    FQT_TRY(hipGetLastError());
+  }
+  return FQT_OK;
 }
 
 size_t fqt_quantize_workspace(fqt_kind kind, int64_t rows, int64_t cols, int block_size) {

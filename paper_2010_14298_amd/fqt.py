@@ -55,7 +55,7 @@ class ConvShape(ctypes.Structure):
 
 
 EXPORTS = [
-    "fqt_quantize_ptq", "fqt_quantize_psq", "fqt_quantize_bhq", "fqt_quantize_shift", "fqt_quantize_workspace",
+    "fqt_quantize_ptq", "fqt_quantize_psq", "fqt_quantize_psq_noalloc", "fqt_quantize_bhq", "fqt_quantize_shift", "fqt_quantize_workspace",
     "fqt_bhq_adaptive_groups", "fqt_bhq_adaptive_workspace",
     "fqt_linear_backward", "fqt_linear_backward_workspace",
     "fqt_linear_forward", "fqt_linear_forward_workspace",
@@ -84,6 +84,7 @@ def load(path=LIB_PATH):
     sig = {
         "fqt_quantize_ptq": ([vp, i64, i64, i32, i32, u64, u32, i32, qtp, vp, sz, vp], i32),
         "fqt_quantize_psq": ([vp, i64, i64, i32, u64, u32, qtp, vp, sz, vp], i32),
+        "fqt_quantize_psq_noalloc": ([vp, i64, i64, i32, u64, u32, qtp, vp, vp], i32),
         "fqt_quantize_bhq": ([vp, i64, i64, i32, i32, u64, u32, qtp, vp, sz, vp], i32),
         "fqt_quantize_shift": ([vp, i64, i64, i32, u64, u32, i32, qtp, vp, sz, vp], i32),
         "fqt_quantize_workspace": ([i32, i64, i64, i32], sz),
@@ -211,6 +212,24 @@ def fqt_quantize_psq(x, bits, seed=0, stream=0, code_sum=False, ws=None):
                                  _stream())
     _check("fqt_quantize_psq", rc)
     out["ws"] = ws
+    return out
+
+
+def fqt_quantize_psq_noalloc(x, bits, seed=0, stream=0, code_sum=False, out=None):
+    """fqt_quantize_psq on the library's fixed scratch memory (no workspace).
+    `out` may hold preallocated q / scale / zero (/ code_sum) tensors; returns
+    them with a device status tensor of 4 uint32 words (as int32)."""
+    x = _f32(x, "x")
+    rows, cols = x.shape
+    fresh, _ = _quant_outputs(x, rows, cols, "psq", False, code_sum)
+    out = dict(fresh, **(out or {}))
+    qt = QTensor(out["q"].data_ptr(), out["scale"].data_ptr(), out["zero"].data_ptr(), 0, 0,
+                 out["code_sum"].data_ptr() if "code_sum" in out else 0, 0, 0)
+    status = torch.full((4,), -1, dtype=torch.int32, device=x.device)
+    rc = load().fqt_quantize_psq_noalloc(_ptr(x), rows, cols, bits, seed, stream, ctypes.byref(qt), _ptr(status),
+                                         _stream())
+    _check("fqt_quantize_psq_noalloc", rc)
+    out["status"] = status
     return out
 
 
