@@ -210,6 +210,16 @@ typedef struct {
   uint64_t seed;
   const fqt_trace* trace; /* optional, NULL for none */
   int relu_input;         /* 0: plain grad_X; 1: grad_X * 1[X > 0] */
+  /* Optional caller buffers (device; linear layer only, the conv ignores
+   * them) that receive the gradient codes the contractions read, in place of
+   * the workspace copies:
+   *   qb2_codes [N, d_out]  Q_b2(G) offset codes, rows in slot order
+   *   qb1_codes [d_out, N]  Q_b1(G) offset codes, transposed, slot order
+   *   perm      [N]         BHQ: slot -> row (not written for PTQ / PSQ,
+   *                         whose slot order is the row order)             */
+  int8_t* qb2_codes;
+  int8_t* qb1_codes;
+  int32_t* perm;
 } fqt_bwd_cfg;
 
 /* Linear layer FQT backward, Eq. (linear-sq-backprop) with bifurcation:

@@ -610,6 +610,10 @@ fqt_status fqt_linear_backward(const float* X, const float* W, const float* G, i
   if (ws_bytes < fqt_linear_backward_workspace(N, d_in, d_out, cfg)) return FQT_EWORKSPACE;
   Carver c(ws);
   LinearWs w = carve_linear(c, X, W, G, N, d_in, d_out, *cfg);
+  // caller buffers for the gradient codes (and the BHQ permutation)
+  if (cfg->qb2_codes) w.qg2 = cfg->qb2_codes;
+  if (cfg->qb1_codes) w.qg1_t = cfg->qb1_codes;
+  if (cfg->perm && w.perm) w.perm = cfg->perm;
   const fqt_qspec qx = cfg->qb_x;
   const bool bhq = qx.kind == FQT_BHQ;
   const Tracer tr{cfg->trace, s};

@@ -47,7 +47,8 @@ class Trace(ctypes.Structure):
 
 class BwdCfg(ctypes.Structure):
     _fields_ = [("qb_w", QSpec), ("qb_x", QSpec), ("f_bits", ctypes.c_int), ("theta_bits", ctypes.c_int),
-                ("seed", ctypes.c_uint64), ("trace", ctypes.POINTER(Trace)), ("relu_input", ctypes.c_int)]
+                ("seed", ctypes.c_uint64), ("trace", ctypes.POINTER(Trace)), ("relu_input", ctypes.c_int),
+                ("qb2_codes", ctypes.c_void_p), ("qb1_codes", ctypes.c_void_p), ("perm", ctypes.c_void_p)]
 
 
 class ConvShape(ctypes.Structure):
@@ -266,13 +267,24 @@ def fqt_linear_backward_workspace(N, d_in, d_out, cfg):
 
 
 def fqt_linear_backward(X, W, G, qb_x=("psq", 8, 0), qb_w=("ptq", 8, 0), f_bits=8, theta_bits=8, seed=0,
-                        grad_W=None, grad_X=None, ws=None, trace=None, relu_input=False):
+                        grad_W=None, grad_X=None, ws=None, trace=None, relu_input=False, codes=None):
+    """codes: optional dict to receive the gradient codes the contractions read:
+    it is filled with qb2 [N, d_out], qb1_t [d_out, N] (int8, slot order) and,
+    for BHQ, perm [N]."""
     X, W, G = _f32(X, "X"), _f32(W, "W"), _f32(G, "G")
     N, d_in = X.shape
     d_out = W.shape[0]
     if W.shape != (d_out, d_in) or G.shape != (N, d_out):
         raise ValueError("shapes: X [N, d_in], W [d_out, d_in], G [N, d_out]")
     cfg = cfg_struct(qb_x, qb_w, f_bits, theta_bits, seed, trace, relu_input)
+    if codes is not None:
+        codes["qb2"] = torch.empty((N, d_out), dtype=torch.int8, device=X.device)
+        codes["qb1_t"] = torch.empty((d_out, N), dtype=torch.int8, device=X.device)
+        cfg.qb2_codes = codes["qb2"].data_ptr()
+        cfg.qb1_codes = codes["qb1_t"].data_ptr()
+        if KINDS.get(qb_x[0], qb_x[0]) == FQT_BHQ:
+            codes["perm"] = torch.empty(N, dtype=torch.int32, device=X.device)
+            cfg.perm = codes["perm"].data_ptr()
     if grad_W is None:
         grad_W = torch.empty((d_out, d_in), dtype=torch.float32, device=X.device)
     if grad_X is None:

@@ -111,26 +111,63 @@ def test_linear_outlier_layer_mid_size():
         assert rownorm_err(gX, r["grad_X64"]) <= REL_TOL
 
 
-@pytest.mark.parametrize("qb_x", [("bhq", 5, 64), ("psq", 8, 0), ("ptq", 4, 0)])
-def test_linear_ffn_full_size_sampled(qb_x):
-    """N=8192, d_in=1024, d_out=4096 through the same entry point the benchmark times.
+@pytest.mark.parametrize("M,N,K", [(8192, 1024, 4096), (4096, 1024, 8192)])
+def test_gemm_accumulators_full_size_sampled(M, N, K):
+    # the two contraction shapes of the FFN layer: the 256 x 128 tiles
+    # (grad_X, 256 tiles) and the 128 x 128 tiles (grad_W) of the fast loop;
+    # 64 sampled rows against an exact float64 product (|sum| < 2^53)
+    f = fqt()
+    rng = np.random.default_rng(M + K)
+    A = rng.integers(-128, 128, (M, K), dtype=np.int8)
+    B = rng.integers(-128, 128, (N, K), dtype=np.int8)
+    C = host(f.fqt_gemm_s8s8_s64(dev(A), dev(B)))
+    rows = np.union1d(rng.choice(M, 62, replace=False), [0, M - 1])
+    ref = A[rows].astype(np.float64) @ B.astype(np.float64).T
+    np.testing.assert_array_equal(C[rows], ref.astype(np.int64))
 
-    The oracle quantizes G in full (codes are elementwise cheap); grad_X rows
-    and grad_W entries are then sampled and computed one by one in float64.
-    """
+
+@pytest.fixture(scope="module")
+def ffn_layer():
+    """The FFN layer's inputs and the oracle's parts that do not depend on Q_b2."""
     X, W, G = synth.linear_outlier(seed=0)
-    gW, gX = run_linear(X, W, G, qb_x, seed=0)
     qx = Q.quantize_ptq(X, 8, False)
     qw = Q.quantize_ptq(W, 8, False)
     qb1 = Q.quantize_ptq(G, 8, True, seed=0, stream=0)
+    return dict(X=X, W=W, G=G, Xr=Q.dequantize(qx), Wr=Q.dequantize(qw), qb1=qb1)
+
+
+FULL_CASES = [(k, b, 64 if k == "bhq" else 0) for k in ("ptq", "psq", "bhq") for b in (4, 5, 8)]
+
+
+@pytest.mark.parametrize("qb_x", FULL_CASES, ids=lambda s: f"{s[0]}{s[1]}")
+def test_linear_ffn_full_size(ffn_layer, qb_x):
+    """N=8192, d_in=1024, d_out=4096 through the entry point the benchmark times.
+
+    The codes of the fused quantizer launch (Q_b2 in slot order, the
+    transposed Q_b1, the BHQ permutation) are compared in full, bit for bit;
+    grad_X rows and grad_W rows are sampled and computed one by one in
+    float64 from the oracle's codes.
+    """
+    L = ffn_layer
+    X, W, G = L["X"], L["W"], L["G"]
+    f = fqt()
+    codes = {}
+    gW, gX, ws = f.fqt_linear_backward(dev(X), dev(W), dev(G), qb_x=qb_x, seed=0, codes=codes)
+    assert f.fqt_workspace_status(ws) == 0
+    gW, gX = host(gW), host(gX)
     qb2 = BW.quantize_gradient(G, qb_x, 0, 1)
-    Xr, Wr = Q.dequantize(qx), Q.dequantize(qw)
+    perm = qb2["perm"] if qb_x[0] == "bhq" else np.arange(G.shape[0])
+    if qb_x[0] == "bhq":
+        np.testing.assert_array_equal(host(codes["perm"]), perm)
+    np.testing.assert_array_equal(host(codes["qb2"]), (qb2["code"] - Q.offset(qb_x[1])).astype(np.int8))
+    qb1 = L["qb1"]
+    np.testing.assert_array_equal(host(codes["qb1_t"]), (qb1["code"][perm].T - 128).astype(np.int8))
     G2r = Q.dequantize(qb2)
     rng = np.random.default_rng(0)
     rows = rng.choice(G.shape[0], 64, replace=False)
-    ref_x = G2r[rows] @ Wr
-    assert rownorm_err(gX[rows], ref_x) <= REL_TOL
+    big = np.argsort(-np.abs(G).max(axis=1))[:4]
+    rows = np.union1d(rows, big)
+    assert rownorm_err(gX[rows], G2r[rows] @ L["Wr"]) <= REL_TOL
     cols_o = rng.choice(G.shape[1], 48, replace=False)
     G1r = Q.dequantize_affine(dict(qb1, code=qb1["code"][:, cols_o]))
-    ref_w = G1r.T @ Xr
-    assert rownorm_err(gW[cols_o], ref_w) <= REL_TOL
+    assert rownorm_err(gW[cols_o], G1r.T @ L["Xr"]) <= REL_TOL

@@ -167,3 +167,73 @@ def test_conv_unsupported_channels():
     with pytest.raises(f.FqtError) as e:
         f.fqt_conv_backward_im2col(dev(X), dev(W), dev(G), 1, 1, qb_x=("psq", 8, 0))
     assert e.value.code == 2
+
+
+# ---------------------------------------------------------------------------
+# Exact accumulators of the conv contractions.  Inputs on the integer grid
+# 0..255 (each tensor, and each gradient sample, holding both 0 and 255) make
+# every quantizer exact: Q_f, Q_theta and the per-sample Q_b2 have step 1 and
+# zero 0, and the stochastic Q_b1 never rounds (fraction 0).  The float64
+# epilogues then evaluate exact integers, so grad_W and grad_X must equal the
+# float32 rounding of the exact integer contractions, which sparse inputs
+# keep below 2^24: any accumulator off by one (or a zero-point term at a
+# padded tap) changes an output.
+# ---------------------------------------------------------------------------
+def grid_conv_inputs(seed, n, c, h, o, k, stride, pad, dx=0.01, dw=0.1, dg=0.01):
+    rng = np.random.default_rng(seed)
+    ho = (h + 2 * pad - k) // stride + 1
+
+    def sparse(shape, d):
+        v = rng.integers(1, 256, shape)
+        return np.where(rng.random(shape) < d, v, 0).astype(np.float32)
+
+    X = sparse((n, h, h, c), dx)
+    X.flat[rng.integers(X.size)] = 255.0
+    X.flat[rng.integers(X.size)] = 0.0
+    W = sparse((o, k, k, c), dw)
+    W.flat[rng.integers(W.size)] = 255.0
+    W.flat[rng.integers(W.size)] = 0.0
+    G = sparse((n, ho, ho, o), dg)
+    Gf = G.reshape(n, -1)
+    Gf[np.arange(n), rng.integers(0, Gf.shape[1], n)] = 255.0
+    Gf[np.arange(n), rng.integers(0, Gf.shape[1], n)] = 0.0
+    return X, W, G
+
+
+def exact_conv_grads(X, W, G, stride, pad):
+    """grad_W and grad_X of the conv as float64 tap-by-tap products (exact:
+    integer sums below 2^53)."""
+    n, h, w, c = X.shape
+    o, kh, kw, _ = W.shape
+    ho, wo = G.shape[1:3]
+    Xp = np.zeros((n, h + 2 * pad, w + 2 * pad, c))
+    Xp[:, pad: pad + h, pad: pad + w] = X
+    Gf = G.reshape(-1, o).astype(np.float64)
+    gW = np.zeros((o, kh, kw, c))
+    gXp = np.zeros_like(Xp)
+    for r in range(kh):
+        for s in range(kw):
+            sl = (slice(None), slice(r, r + stride * (ho - 1) + 1, stride), slice(s, s + stride * (wo - 1) + 1, stride))
+            gW[:, r, s, :] = Gf.T @ Xp[sl].reshape(-1, c)
+            gXp[sl] += (Gf @ W[:, r, s, :].astype(np.float64)).reshape(n, ho, wo, c)
+    return gW, gXp[:, pad: pad + h, pad: pad + w]
+
+
+@pytest.mark.parametrize("geom", [
+    (128, 64, 56, 64, 3, 1, 1),     # the 56 x 56 layer at full size
+    (150, 16, 9, 32, 3, 2, 1),      # more slots per input pixel than one tile
+    (40, 3, 32, 64, 7, 2, 3),       # stem-like: 7 x 7, stride 2, three channels
+    (24, 32, 14, 48, 1, 2, 0),      # 1 x 1, stride 2
+    (8, 16, 11, 16, 5, 1, 2),       # 5 x 5
+], ids=lambda g: "n{}_c{}_h{}_o{}_k{}_s{}_p{}".format(*g))
+def test_conv_contractions_exact_on_the_grid(geom):
+    n, c, h, o, k, stride, pad = geom
+    X, W, G = grid_conv_inputs(n + c + o, n, c, h, o, k, stride, pad)
+    refW, refX = exact_conv_grads(X, W, G, stride, pad)
+    assert np.abs(refW).max() < 2 ** 24 and np.abs(refX).max() < 2 ** 24
+    f = fqt()
+    gW, gX, ws = f.fqt_conv_backward_im2col(dev(X), dev(W), dev(G), stride, pad, qb_x=("psq", 8, 0),
+                                           qb_w=("ptq", 8, 0), seed=1)
+    assert f.fqt_workspace_status(ws) == 0
+    np.testing.assert_array_equal(host(gW), refW.astype(np.float32))
+    np.testing.assert_array_equal(host(gX), refX.astype(np.float32))

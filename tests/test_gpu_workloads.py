@@ -222,3 +222,89 @@ def test_seed_sweep_unbiased_and_exact_variance():
         assert abs(emp_total - ex_total) <= 0.10 * ex_total, (kind, emp_total, ex_total)
         totals[kind] = ex_total
     assert totals["bhq"] < totals["psq"] < totals["ptq"]
+
+
+# ---------------------------------------------------------------------------
+# ResNet-50 shapes at batch 256 for every gradient quantizer: the oracle
+# quantizes only the rows a sampled output needs (with their own element
+# indices), so the full-batch check stays cheap on the host
+# ---------------------------------------------------------------------------
+def oracle_rows(Gf, spec, seed, stream, rows):
+    """Dequantized rows `rows` (original order) of the quantization of Gf."""
+    kind, bits, k = spec
+    D = Gf.shape[1]
+    cols = np.arange(D, dtype=np.uint64)
+    out = np.zeros((len(rows), D))
+    if kind in ("ptq", "psq"):
+        if kind == "ptq":
+            z = np.float32(Gf.min())
+            s = Q.scale_from_range(np.float32(np.float32(Gf.max()) - z), Q.n_bins(bits))
+            zs, ss = np.full(len(rows), z, np.float32), np.full(len(rows), s, np.float32)
+        else:
+            mn, _, R, _ = Q.row_stats(Gf[rows])
+            zs = mn.astype(np.float32)
+            ss = np.array([Q.scale_from_range(r, Q.n_bins(bits)) for r in R], np.float32)
+        e = np.asarray(rows, np.uint64)[:, None] * np.uint64(D) + cols[None, :]
+        code = Q._affine_codes(Gf[rows], ss[:, None], zs[:, None], bits, True, seed, stream, e)
+        return code / ss[:, None].astype(np.float64) + zs[:, None].astype(np.float64)
+    plan = Q.bhq_plan(Gf, bits, k)
+    for info in plan["groups"]:
+        mem = info["members"]
+        hit = [i for i, r in enumerate(rows) if r in mem]
+        if not hit:
+            continue
+        sub = dict(plan, groups=[info])
+        base, kg = info["base"], info["size"]
+        q = Q.quantize_bhq(Gf, bits, k, seed=seed, stream=stream, plan=sub)
+        part = dict(q, code=q["code"], plan=sub)
+        deq = Q.dequantize_bhq(part)
+        for i in hit:
+            out[i] = deq[rows[i]]
+    return out
+
+
+@pytest.mark.parametrize("shape,spec", [
+    ((64, 64, 3, 1, 56, 3), ("bhq", 5, 64)),
+    ((128, 128, 3, 1, 28, 3), ("bhq", 5, 64)),
+    ((256, 256, 3, 1, 14, 5), ("bhq", 5, 64)),
+    ((64, 256, 1, 1, 56, 4), ("ptq", 8, 0)),
+    ((256, 256, 3, 2, 28, 1), ("ptq", 8, 0)),
+    ((1024, 2048, 1, 2, 14, 1), ("ptq", 8, 0)),
+    ((64, 256, 1, 1, 56, 4), ("psq", 8, 0)),
+    ((256, 256, 3, 2, 28, 1), ("psq", 8, 0)),
+    ((1024, 2048, 1, 2, 14, 1), ("psq", 8, 0)),
+], ids=lambda v: resnet_shape_id(v) if len(v) == 6 else f"{v[0]}{v[1]}")
+def test_resnet50_batch256_quantizers(shape, spec):
+    c, o, k, stride, h, _ = shape
+    pad = k // 2
+    n = 256
+    X, W, G = synth.conv_layer(seed=13, n=n, c=c, h=h, w=h, o=o, k=k, stride=stride, pad=pad)
+    gW, gX = conv_run(X, W, G, stride, pad, spec, seed=21)
+    ho = G.shape[1]
+    Gf = G.reshape(n, -1)
+    Xr = Q.dequantize(Q.quantize_ptq(X.reshape(n, -1), 8, False)).reshape(n, h, h, c)
+    Wr = Q.dequantize(Q.quantize_ptq(W.reshape(o, -1), 8, False)).reshape(o, k, k, c)
+    rng = np.random.default_rng(3)
+    if spec[0] == "bhq":
+        # two rows of one group (one of them its large row) and one other
+        plan = Q.bhq_plan(Gf, spec[1], spec[2])
+        g0 = plan["groups"][int(rng.integers(len(plan["groups"])))]
+        rows = [g0["members"][0], g0["members"][1 + int(rng.integers(g0["size"] - 1))]]
+    else:
+        rows = [int(r) for r in rng.choice(n, 2, replace=False)]
+    rows.append(int(np.argmax(np.abs(Gf).max(axis=1))))
+    G2r = oracle_rows(Gf, spec, 21, 1, rows)
+    for i, r in enumerate(rows):
+        ref = conv_reference_sample(G2r[i].reshape(ho, ho, o), Wr, h, h, stride, pad)
+        assert rownorm_err(gX[r].reshape(1, -1), ref.reshape(1, -1)) <= REL_TOL, r
+    # grad_W rows: Q_b1 (PTQ-8, stream 0) of one output channel, every sample
+    oo = int(rng.integers(o))
+    z = np.float32(Gf.min())
+    s = Q.scale_from_range(np.float32(np.float32(Gf.max()) - z), 255)
+    idx = np.arange(ho * ho, dtype=np.uint64) * np.uint64(o) + np.uint64(oo)
+    e = np.arange(n, dtype=np.uint64)[:, None] * np.uint64(Gf.shape[1]) + idx[None, :]
+    gch = G[..., oo].reshape(n, -1)
+    code = Q._affine_codes(gch, s, z, 8, True, 21, 0, e)
+    G1r = (code / np.float64(s) + np.float64(z)).reshape(n, ho, ho)
+    ref = conv_reference_wrow(G1r, Xr, k, k, stride, pad)
+    assert rownorm_err(gW[oo].reshape(1, -1), ref.reshape(1, -1)) <= REL_TOL
