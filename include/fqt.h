@@ -150,6 +150,22 @@ fqt_status fqt_quantize_shift(const float* x, int64_t rows, int64_t cols, int bi
 
 size_t fqt_quantize_workspace(fqt_kind kind, int64_t rows, int64_t cols, int block_size);
 
+/* Seed batch of one stochastic quantizer (Sec. 3.3 SR; the unbiasedness of
+ * Sec. 2.2 and the variance of App. C measured over seeds): the quantizer
+ * kind (FQT_PTQ, FQT_PSQ or FQT_BHQ with block_size as for
+ * fqt_quantize_bhq) plans once and rounds the same transformed values under
+ * the keys seed, seed + 1, .., seed + nseeds - 1 (1 <= nseeds <= 32768),
+ * each exactly as the single-seed quantizer with that seed would.  Instead
+ * of codes it writes, per element of the natural layout (BHQ: slot order),
+ * sum_code = sum over seeds of the code in [0, B] and sum_code2 = the sum of
+ * its squares (int32, [rows, cols], 16-byte aligned).  plan receives scale,
+ * zero (and perm, group_off, num_groups for BHQ) as for the single
+ * quantizers; plan->q is not used.  cols % 4 == 0 and x 16-byte aligned
+ * (FQT_EUNSUPPORTED otherwise).  Workspace: fqt_quantize_workspace(kind, ..). */
+fqt_status fqt_quantize_seeds(const float* x, int64_t rows, int64_t cols, fqt_kind kind, int bits, int block_size,
+                              uint64_t seed, int32_t nseeds, uint32_t stream, const fqt_qtensor* plan,
+                              int32_t* sum_code, int32_t* sum_code2, void* ws, size_t ws_bytes, fqt_stream_t s);
+
 /* Adaptive grouping of the block Householder quantizer, App. D step 2: for
  * every number of groups G = 1..rows, the G largest rows lead the groups
  * and the rows - G others are shared out in sorted order in proportion to

@@ -172,17 +172,21 @@ void add_zero(FinalizePlan& fp, int32_t* p, int64_t n) {
   }
 }
 
-fqt_status check_quant_args(const float* x, int64_t rows, int64_t cols, int bits, const fqt_qtensor* out) {
-  if (!x || !out || !out->q || !out->scale || !out->zero) return FQT_EINVAL;
+fqt_status check_quant_args(const float* x, int64_t rows, int64_t cols, int bits, const fqt_qtensor* out,
+                            bool need_q = true) {
+  if (!x || !out || (need_q && !out->q) || !out->scale || !out->zero) return FQT_EINVAL;
   if (rows < 1 || cols < 1 || !valid_bits(bits)) return FQT_EINVAL;
   if (rows > MAX_ROWS || cols > ((int64_t)1 << 40) / rows) return FQT_EUNSUPPORTED;
   return FQT_OK;
 }
 
+// nseeds > 0: the seed batch (sums of the codes and of their squares over the
+// keys seed .. seed + nseeds - 1 into sum_c / sum_c2) instead of the codes.
 fqt_status quantize_common(fqt_kind kind, const float* x, int64_t rows, int64_t cols, int bits, int stochastic,
                            uint64_t seed, uint32_t stream, int transpose, int block_size, const fqt_qtensor* out,
-                           void* ws, size_t ws_bytes, hipStream_t s) {
-  fqt_status st = check_quant_args(x, rows, cols, bits, out);
+                           void* ws, size_t ws_bytes, hipStream_t s, int nseeds = 0, int32_t* sum_c = nullptr,
+                           int32_t* sum_c2 = nullptr) {
+  fqt_status st = check_quant_args(x, rows, cols, bits, out, nseeds == 0);
   if (st != FQT_OK) return st;
   if (kind == FQT_BHQ) {
     if (!out->perm) return FQT_EINVAL;
@@ -249,6 +253,15 @@ fqt_status quantize_common(fqt_kind kind, const float* x, int64_t rows, int64_t 
     if (st != FQT_OK) return st;
     p.perm = out->perm;
     mode = QM_BHQ;
+  }
+  if (nseeds > 0) {
+    p.q_nat = nullptr;
+    p.sum_nat = nullptr;
+    p.nseeds = nseeds;
+    p.sum_c = sum_c;
+    p.sum_c2 = sum_c2;
+    FQT_TRY(launch_quant_seeds(p, mode, s));
+    return FQT_OK;
   }
   FQT_TRY(launch_quant(p, mode, s));
   return FQT_OK;
@@ -544,6 +557,18 @@ fqt_status fqt_quantize_psq_noalloc(const float* x, int64_t rows, int64_t cols, 
     FQT_TRY(hipGetLastError());
   }
   return FQT_OK;
+}
+
+fqt_status fqt_quantize_seeds(const float* x, int64_t rows, int64_t cols, fqt_kind kind, int bits, int block_size,
+                              uint64_t seed, int32_t nseeds, uint32_t stream, const fqt_qtensor* plan,
+                              int32_t* sum_code, int32_t* sum_code2, void* ws, size_t ws_bytes, fqt_stream_t s) {
+  if (!sum_code || !sum_code2 || !plan) return FQT_EINVAL;
+  if (kind != FQT_PTQ && kind != FQT_PSQ && kind != FQT_BHQ) return FQT_EINVAL;
+  if (nseeds < 1 || nseeds > 32768) return FQT_EINVAL;
+  if (cols % 4 != 0 || ((uintptr_t)x & 15) || ((uintptr_t)sum_code & 15) || ((uintptr_t)sum_code2 & 15))
+    return FQT_EUNSUPPORTED;
+  return quantize_common(kind, x, rows, cols, bits, 1, seed, stream, 0, kind == FQT_BHQ ? block_size : 0, plan, ws,
+                         ws_bytes, s, nseeds, sum_code, sum_code2);
 }
 
 size_t fqt_quantize_workspace(fqt_kind kind, int64_t rows, int64_t cols, int block_size) {

@@ -201,9 +201,16 @@ struct QuantParams {
   BhqLayout L;           // BHQ: L.k = 0 selects the general plan (slot, tau)
   const SlotInfo* slot;
   const float* tau;
+  // seed batch (launch_quant_seeds): nseeds roundings under keys seed + b,
+  // per element [rows, cols] (slot order) the sum of the codes and of their squares
+  int nseeds;
+  int32_t* sum_c;
+  int32_t* sum_c2;
 };
 enum QuantMode { QM_TENSOR = 0, QM_ROW = 1, QM_BHQ = 2 };
 hipError_t launch_quant(const QuantParams& p, int mode, hipStream_t s);
+// The seed batch of one quantizer (natural layout, cols % 4 == 0).
+hipError_t launch_quant_seeds(const QuantParams& p, int mode, hipStream_t s);
 // Two per-tensor quantizations with transposed outputs only, one launch.
 hipError_t launch_quant_pair(const QuantParams& p0, const QuantParams& p1, hipStream_t s);
 // The gradient quantizer pg (with its transposed second quantizer) and the

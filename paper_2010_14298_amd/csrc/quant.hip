@@ -703,7 +703,7 @@ __device__ __forceinline__ uint32_t insert_top(uint32_t w, int32_t v, int b) {
 // One 64 x 256 tile: column tile bx, slot tile by.
 // H2: the second (transposed, stochastic) quantizer of the same rows, Q_b1:
 // 0 none, 1 per tensor, 2 per row with power-of-two shifted codes.
-template <int MODE, int K, int H2, bool VEC, bool TRANS>
+template <int MODE, int K, int H2, bool VEC, bool TRANS, bool SD = false>
 __device__ __forceinline__ void quant_tile(const QuantParams& p, int64_t bx, int64_t by) {
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform: slot bookkeeping stays scalar
@@ -919,6 +919,27 @@ __device__ __forceinline__ void quant_tile(const QuantParams& p, int64_t bx, int
       }
     }
     const uint64_t e0 = (uint64_t)srow[r] * (uint64_t)cols + (uint64_t)c0;
+    if constexpr (SD) {
+      // seed batch: the same transformed values rounded under keys seed + b,
+      // b < nseeds; per element the sum of the codes and of their squares
+      if (ok && lane_ok) {
+        int32_t c1[4] = {0, 0, 0, 0}, c2[4] = {0, 0, 0, 0};
+        for (int b = 0; b < p.nseeds; ++b) {
+          int32_t tb[4];
+          sr4<VEC>(y, e0, p.seed + (uint64_t)b, p.stream, Bf, hoff, tb);
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const int32_t c = (tb[j] >> 24) + half;
+            c1[j] += c;
+            c2[j] += c * c;
+          }
+        }
+        const int64_t o = slot * cols + c0;
+        *reinterpret_cast<int4*>(p.sum_c + o) = make_int4(c1[0], c1[1], c1[2], c1[3]);
+        *reinterpret_cast<int4*>(p.sum_c2 + o) = make_int4(c2[0], c2[1], c2[2], c2[3]);
+      }
+      continue;
+    }
     int32_t t[4];
     // with a second quantizer the first is stochastic too (launch_quant checks)
     if (H2 != 0 || p.stoch)
@@ -1179,6 +1200,40 @@ hipError_t launch_quant_fused(const QuantParams& pg, int mode, const QuantParams
     case 16: return launch_quant_fused_k<QM_BHQ, 16>(pg, px, pw, s);
     case 32: return launch_quant_fused_k<QM_BHQ, 32>(pg, px, pw, s);
     case 64: return launch_quant_fused_k<QM_BHQ, 64>(pg, px, pw, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+// Seed batch (natural layout, float4 rows): one block per 64 x 256 tile.
+template <int MODE, int K>
+__global__ __launch_bounds__(256) void quant_seeds_kernel(QuantParams p) {
+  quant_tile<MODE, K, 0, true, false, true>(p, blockIdx.x, blockIdx.y);
+}
+
+template <int MODE, int K>
+static hipError_t launch_seeds_k(const QuantParams& p, hipStream_t s) {
+  const int64_t ct = (p.cols + QT_COLS - 1) / QT_COLS;
+  const int64_t rt = (p.rows + QT_SLOTS - 1) / QT_SLOTS;
+  if (ct > 0x7FFFFFFF || rt > 65535) return hipErrorInvalidValue;
+  hipLaunchKernelGGL((quant_seeds_kernel<MODE, K>), dim3((unsigned)ct, (unsigned)rt), dim3(256), 0, s, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_quant_seeds(const QuantParams& p, int mode, hipStream_t s) {
+  if (p.nseeds < 1 || !p.sum_c || !p.sum_c2 || p.cols % 4 != 0 || ((uintptr_t)p.x & 15) ||
+      ((uintptr_t)p.sum_c & 15) || ((uintptr_t)p.sum_c2 & 15))
+    return hipErrorInvalidValue;
+  if (mode == QM_TENSOR) return launch_seeds_k<QM_TENSOR, 0>(p, s);
+  if (mode == QM_ROW) return launch_seeds_k<QM_ROW, 0>(p, s);
+  switch (p.L.k) {
+    case 0: return p.slot && p.tau ? launch_seeds_k<QM_BHQ, 0>(p, s) : hipErrorInvalidValue;
+    case 1: return launch_seeds_k<QM_BHQ, 1>(p, s);
+    case 2: return launch_seeds_k<QM_BHQ, 2>(p, s);
+    case 4: return launch_seeds_k<QM_BHQ, 4>(p, s);
+    case 8: return launch_seeds_k<QM_BHQ, 8>(p, s);
+    case 16: return launch_seeds_k<QM_BHQ, 16>(p, s);
+    case 32: return launch_seeds_k<QM_BHQ, 32>(p, s);
+    case 64: return launch_seeds_k<QM_BHQ, 64>(p, s);
     default: return hipErrorInvalidValue;
   }
 }

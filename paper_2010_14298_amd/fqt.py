@@ -57,6 +57,7 @@ class ConvShape(ctypes.Structure):
 
 EXPORTS = [
     "fqt_quantize_ptq", "fqt_quantize_psq", "fqt_quantize_psq_noalloc", "fqt_quantize_bhq", "fqt_quantize_shift", "fqt_quantize_workspace",
+    "fqt_quantize_seeds",
     "fqt_bhq_adaptive_groups", "fqt_bhq_adaptive_workspace",
     "fqt_linear_backward", "fqt_linear_backward_workspace",
     "fqt_linear_forward", "fqt_linear_forward_workspace",
@@ -89,6 +90,7 @@ def load(path=LIB_PATH):
         "fqt_quantize_bhq": ([vp, i64, i64, i32, i32, u64, u32, qtp, vp, sz, vp], i32),
         "fqt_quantize_shift": ([vp, i64, i64, i32, u64, u32, i32, qtp, vp, sz, vp], i32),
         "fqt_quantize_workspace": ([i32, i64, i64, i32], sz),
+        "fqt_quantize_seeds": ([vp, i64, i64, i32, i32, i32, u64, i32, u32, qtp, vp, vp, vp, sz, vp], i32),
         "fqt_bhq_adaptive_groups": ([vp, i64, i64, i32, vp, vp, vp, sz, vp], i32),
         "fqt_bhq_adaptive_workspace": ([i64, i64], sz),
         "fqt_linear_backward": ([vp, vp, vp, i64, i64, i64, cfgp, vp, vp, vp, sz, vp], i32),
@@ -212,6 +214,26 @@ def fqt_quantize_psq(x, bits, seed=0, stream=0, code_sum=False, ws=None):
     rc = load().fqt_quantize_psq(_ptr(x), rows, cols, bits, seed, stream, ctypes.byref(qt), _ptr(ws), ws.numel(),
                                  _stream())
     _check("fqt_quantize_psq", rc)
+    out["ws"] = ws
+    return out
+
+
+def fqt_quantize_seeds(x, kind, bits, nseeds, block_size=0, seed=0, stream=0, ws=None):
+    """Seed batch: per element the sum over keys seed .. seed + nseeds - 1 of
+    the code and of its square (int32 tensors sum_c, sum_c2), plus the plan."""
+    x = _f32(x, "x")
+    rows, cols = x.shape
+    out, qt = _quant_outputs(x, rows, cols, kind, False, False)
+    out.pop("q")
+    qt.q = 0
+    out["sum_c"] = torch.empty((rows, cols), dtype=torch.int32, device=x.device)
+    out["sum_c2"] = torch.empty((rows, cols), dtype=torch.int32, device=x.device)
+    if ws is None:
+        ws = _workspace(fqt_quantize_workspace(kind, rows, cols, block_size), x.device)
+    rc = load().fqt_quantize_seeds(_ptr(x), rows, cols, KINDS[kind], bits, block_size, seed, nseeds, stream,
+                                   ctypes.byref(qt), _ptr(out["sum_c"]), _ptr(out["sum_c2"]), _ptr(ws), ws.numel(),
+                                   _stream())
+    _check("fqt_quantize_seeds", rc)
     out["ws"] = ws
     return out
 
