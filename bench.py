@@ -9,8 +9,13 @@ contractions and their dequantizing epilogues) on inputs resident in HBM.
 
 Prints one JSON line: the int8 throughput of the whole layer backward
 (2 * 2 N d_in d_out ops per step / step time), per-phase times from HIP
-events recorded inside the timed steps, the roofline of the dominant kernel
-and the CPU oracle timed on a bounded sample of the same layer.
+events recorded in a second run of the same steps, the roofline of the
+dominant kernel (the fused quantizer launch, against HBM, with its measured
+vector-ALU busy share beside it) and the CPU oracle timed on a bounded
+sample of the same layer, single-threaded and on all host cores.  Extra legs:
+the multi-layer chain, the low-bit grad_W quantizer, sub-8-bit contractions,
+the paper's conv layer, every ResNet-50 conv shape at batch 256 for three
+gradient quantizers, and the seed-batched quantizer over 1000 seeds.
 """
 import argparse
 import json
@@ -23,16 +28,7 @@ QB_X = ("bhq", 5, 64)
 QB_W = ("ptq", 8, 0)
 HBM_PEAK_GBS = 8000.0            # MI355X HBM3E
 INT8_PEAK_TOPS = 5000.0          # MI355X dense int8 matrix cores
-# vector ALU issue: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz, one 32-bit op per lane per cycle
-VALU_PEAK_TOPS = 256 * 4 * 16 * 2.4e9 / 1e12
-# vector ops per element of the quantizer pass (quantizer roofline):
-# gradient element: two Philox4x32-10 words (10 ops each: a quarter of 10 rounds
-# of 2 wide multiplies + 2 three-way xors), Householder column sum 2, transform 3,
-# stochastic rounding 7 (x2), per-tensor transform 2, packing and code sums 2;
-# X / W element: transform 2, round-half-even 4, packing and sums 1
-OPS_PER_G = 2 * 10 + 2 + 3 + 7 + 2 + 7 + 2
-OPS_PER_XW = 2 + 4 + 1
-CPU_SAMPLE_ROWS = 256
+CPU_SAMPLE_ROWS = N          # the whole layer: about 15 s of oracle work per thread setting
 
 
 def parse():
@@ -48,6 +44,7 @@ def parse():
 
 
 TRAFFIC_FILE = os.path.join(os.path.dirname(os.path.abspath(__file__)), "profiles", "traffic_linear_ffn_bhq5.txt")
+COUNTER_FILE = os.path.join(os.path.dirname(os.path.abspath(__file__)), "profiles", "counters_linear_ffn_bhq5.json")
 # kernel of each phase in the rocprofv3 summaries (name prefixes)
 PHASE_KERNEL = {
     "quant_G": ("quant_fused_kernel<2, 64, 1>",),
@@ -73,21 +70,66 @@ def measured_traffic(phase):
     return None
 
 
-def cpu_baseline(X, W, G):
-    """The oracle, as is, on the first CPU_SAMPLE_ROWS samples of the same layer."""
-    from oracle import backward as BW
+def measured_counters(phase):
+    """Counter summary of one kernel from the committed rocprofv3 passes, if they
+    were taken on the current kernel sources; else None."""
     try:
-        from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-    except Exception:
-        threads = 1
+        from paper_2010_14298_amd import profiling
+        with open(COUNTER_FILE) as f:
+            t = json.load(f)
+        if t.get("kernel_sources") != profiling.source_hash():
+            return None
+        for name, v in t["kernels"].items():
+            if all(part in name for part in PHASE_KERNEL[phase]):
+                return v
+    except (OSError, ValueError, KeyError):
+        return None
+    return None
+
+
+def cpu_baseline(X, W, G):
+    """The oracle, as is, on the first CPU_SAMPLE_ROWS samples (all of them) of the same layer:
+    its quantizers (Q_f, Q_theta, Q_b1, Q_b2) and its contractions (float64
+    products of the dequantized operands) timed apart, with one thread and
+    with every host core (numpy's BLAS threads)."""
+    import numpy as np
+    from threadpoolctl import threadpool_info, threadpool_limits
+    from oracle import backward as BW
+    from oracle import quantizers as Q
     n = CPU_SAMPLE_ROWS
-    t0 = time.perf_counter()
-    BW.linear_backward(X[:n], W, G[:n], qb_x=QB_X, qb_w=QB_W, seed=0)
-    dt = time.perf_counter() - t0
+    Xs, Gs = X[:n], G[:n]
+
+    def step():
+        t0 = time.perf_counter()
+        qx = Q.quantize_ptq(Xs, 8, False)
+        qw = Q.quantize_ptq(W, 8, False)
+        qb1 = BW.quantize_gradient(Gs, QB_W, 0, 0)
+        qb2 = BW.quantize_gradient(Gs, QB_X, 0, 1)
+        t1 = time.perf_counter()
+        Xr, Wr, G1r, G2r = (Q.dequantize(q) for q in (qx, qw, qb1, qb2))
+        gW = (G1r.T @ Xr).astype(np.float32)
+        gX = (G2r @ Wr).astype(np.float32)
+        t2 = time.perf_counter()
+        return t1 - t0, t2 - t1
+
     ops = 2.0 * 2.0 * n * D_IN * D_OUT
-    return {"value": ops / dt / 1e12, "unit": "TOPS", "cores": int(threads), "kind": "oracle",
-            "sample": f"first {n} of {N} samples of the same layer (full d_in, d_out), BHQ-5 k=64; {dt:.1f} s"}
+    res = {}
+    for label, limit in (("one_core", 1), ("all_cores", None)):
+        if limit is None:
+            tq, tc = step()
+            threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+        else:
+            with threadpool_limits(limits=limit):
+                tq, tc = step()
+            threads = 1
+        res[label] = {"quantizers_s": round(tq, 3), "contractions_s": round(tc, 3),
+                      "TOPS": ops / (tq + tc) / 1e12, "threads": int(threads)}
+    a = res["all_cores"]
+    return {"value": a["TOPS"], "unit": "TOPS", "cores": a["threads"], "kind": "oracle",
+            "sample": (f"the whole layer ({N} samples)" if n == N else f"first {n} of {N} samples of the layer")
+                      + f", full d_in and d_out, BHQ-5 k=64; {a['quantizers_s'] + a['contractions_s']:.1f} s "
+                      "on all cores",
+            "per_step": res}
 
 
 CHAIN_WIDTHS = (1024, 4096, 4096, 1024)   # FFN-like ReLU MLP: up, square, down
@@ -207,6 +249,86 @@ def conv_bench(args, fqt, synth, torch):
             "ms_per_step": round(ms, 4), "TOPS": round(ops / (ms * 1e-3) / 1e12, 2)}
 
 
+def resnet_sweep(args, fqt, synth, torch):
+    """Every ResNet-50 v1.5 conv shape (stem to stage 4) at batch 256: the whole
+    FQT conv backward per layer for three gradient quantizers (Q_b2 = BHQ
+    5-bit block 64, PSQ 8-bit, PTQ 8-bit; Q_b1 = PTQ 8-bit), HIP events.
+    Inputs drawn on the device with the recipe of synth.conv_layer:
+    post-ReLU half-normal X (N(0,1) at the stem), He-init W, per-sample
+    LogNormal(0, 2) gradient scales."""
+    import math
+    n = 256
+    specs = (("bhq5", ("bhq", 5, 64)), ("psq8", ("psq", 8, 0)), ("ptq8", ("ptq", 8, 0)))
+    gen = torch.Generator(device="cuda").manual_seed(0)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    reps = max(2, args.steps // 40)
+    layers, net = [], {name: [0.0, 0.0] for name, _ in specs}
+    for (c, o, k, stride, h, count) in synth.RESNET50_CONVS:
+        pad = k // 2
+        ho = (h + 2 * pad - k) // stride + 1
+        X = torch.randn((n, h, h, c), generator=gen, device="cuda")
+        if c != 3:
+            X.clamp_(min=0.0)
+        W = torch.randn((o, k, k, c), generator=gen, device="cuda") * math.sqrt(2.0 / (k * k * c))
+        G = torch.exp(2.0 * torch.randn((n, 1, 1, 1), generator=gen, device="cuda")) * \
+            torch.randn((n, ho, ho, o), generator=gen, device="cuda")
+        ops = 2.0 * 2.0 * n * ho * ho * o * k * k * c
+        row = {"shape": f"{c}->{o} k{k} s{stride} {h}->{ho}", "count": count, "GOP": round(ops / 1e9, 2)}
+        gW, gX = torch.empty_like(W), torch.empty_like(X)
+        for name, spec in specs:
+            ws = None
+            for i in range(2):
+                _, _, ws = fqt.fqt_conv_backward_im2col(X, W, G, stride, pad, qb_x=spec, qb_w=QB_W, seed=i,
+                                                         grad_W=gW, grad_X=gX, ws=ws)
+            torch.cuda.synchronize()
+            e0.record()
+            for i in range(reps):
+                fqt.fqt_conv_backward_im2col(X, W, G, stride, pad, qb_x=spec, qb_w=QB_W, seed=i, grad_W=gW,
+                                             grad_X=gX, ws=ws)
+            e1.record()
+            torch.cuda.synchronize()
+            ms = e0.elapsed_time(e1) / reps
+            row[name] = {"ms": round(ms, 4), "TOPS": round(ops / (ms * 1e-3) / 1e12, 2)}
+            net[name][0] += count * ms
+            net[name][1] += count * ops
+            del ws
+        layers.append(row)
+        del X, W, G, gW, gX
+    torch.cuda.empty_cache()
+    return {"workload": "ResNet-50 v1.5 conv layers at batch 256 (224 x 224), every unique shape; whole FQT conv "
+                        "backward per layer", "steps_per_layer": reps, "layers": layers,
+            "network": {name: {"ms": round(v[0], 3), "TOPS": round(v[1] / (v[0] * 1e-3) / 1e12, 2)}
+                        for name, v in net.items()}}
+
+
+def seeds_bench(args, fqt, synth, torch):
+    """The seed-batched quantizer on the 4096 x 4096 single-outlier gradient:
+    1000 seeds per quantizer and width in one launch each (G read once, every
+    seed's codes drawn and summed per element), HIP events; draws per second."""
+    _, _, G = synth.linear_single_outlier(seed=0)
+    dG = torch.from_numpy(G).cuda()
+    S = 1000
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    res = {}
+    for kind, k in (("ptq", 0), ("psq", 0), ("bhq", 64)):
+        for bits in (4, 5, 6, 8):
+            out = fqt.fqt_quantize_seeds(dG, kind, bits, 4, block_size=k)
+            torch.cuda.synchronize()
+            e0.record()
+            out = fqt.fqt_quantize_seeds(dG, kind, bits, S, block_size=k, seed=0, stream=1, ws=out["ws"])
+            e1.record()
+            torch.cuda.synchronize()
+            ms = e0.elapsed_time(e1)
+            r = {"ms": round(ms, 3), "draws_per_s": round(S * G.size / (ms * 1e-3), 1)}
+            if bits == 5:
+                s1 = out["sum_c"].double()
+                var = (out["sum_c2"].double() - s1 * s1 / S) / (S - 1)
+                r["sum_code_variance"] = round(float(var.sum()), 1)
+            res[f"{kind}{bits}"] = r
+    return {"workload": "4096 x 4096 gradient, N(0,1) with one row x 1000; 1000 seeds (keys 0..999) per "
+                        "quantizer; PTQ / PSQ / BHQ block 64 at 4, 5, 6, 8 bits", "seeds": S, "runs": res}
+
+
 def bf6_bench(args, fqt, torch):
     """Exact contraction of 4-bit codes: 6-bit float matrix cores (e3m2
     operands, packed in the call) against the int8 matrix cores, on the two
@@ -290,19 +412,18 @@ def main():
     nxw = float(N) * D_IN + float(D_OUT) * D_IN
     # the quantizer launch: read G, write Q_b2 and Q_b1 codes; read X and W, write their codes
     quant_bytes = (4 + 2) * nd + (4 + 1) * nxw
-    quant_ops = OPS_PER_G * nd + OPS_PER_XW * nxw
     t_quant_g = phases["quant_G"] * 1e-3
     t_quantizer = (phases["stats"] + phases["scales_plan"] + phases["quant_G"]) * 1e-3
     kernels = {
-        "gemm_gradX": {"bound": "mfma", "t": phases["gemm_gradX"] * 1e-3, "work": gemm_ops, "unit": "TFLOP/s",
+        "gemm_gradX": {"bound": "mfma", "t": phases["gemm_gradX"] * 1e-3, "work": gemm_ops, "unit": "TOP/s",
                        "peak": INT8_PEAK_TOPS, "scale": 1e12},
-        "gemm_gradW": {"bound": "mfma", "t": phases["gemm_gradW"] * 1e-3, "work": gemm_ops, "unit": "TFLOP/s",
+        "gemm_gradW": {"bound": "mfma", "t": phases["gemm_gradW"] * 1e-3, "work": gemm_ops, "unit": "TOP/s",
                        "peak": INT8_PEAK_TOPS, "scale": 1e12},
-        # ALU-bound: at peak its vector ops take longer than its HBM bytes
-        "quant_G": {"bound": "alu", "t": t_quant_g, "work": quant_ops, "unit": "TOP/s", "peak": VALU_PEAK_TOPS,
-                    "scale": 1e12},
-        "quant_G_hbm": {"bound": "hbm", "t": t_quant_g, "work": quant_bytes, "unit": "GB/s", "peak": HBM_PEAK_GBS,
-                        "scale": 1e9},
+        # the fused quantizer launch against HBM: algorithmic bytes (each input
+        # read once, each code written once); its vector-ALU busy share, from
+        # the committed counters, goes beside it
+        "quant_G": {"bound": "hbm", "t": t_quant_g, "work": quant_bytes, "unit": "GB/s", "peak": HBM_PEAK_GBS,
+                    "scale": 1e9},
     }
     measured = measured_peaks(fqt, torch)
     per_kernel = {}
@@ -314,11 +435,19 @@ def main():
         if mp:
             per_kernel[name]["measured_peak"] = mp
             per_kernel[name]["frac_measured"] = round(ach / mp, 4)
-    dom = max((n for n in kernels if n != "quant_G_hbm"), key=lambda n: kernels[n]["t"])
+    for name in kernels:
+        cnt = measured_counters(name)
+        if cnt:
+            per_kernel[name]["counters"] = cnt
+    dom = max(kernels, key=lambda n: kernels[n]["t"])
     roof = dict(per_kernel[dom])
     roof.pop("ms")
+    roof.pop("counters", None)
     roof["kernel"] = dom
     roof["traffic"] = measured_traffic(dom)
+    cnt = measured_counters(dom)
+    if cnt and "VALUBusy" in cnt:
+        roof["valu_busy_pct"] = cnt["VALUBusy"]
     out = {
         "metric": "FQT layer-backward int8 TOPS + quantizer HBM GB/s (BHQ 5-bit) vs roofline",
         "value": round(value, 3),
@@ -347,6 +476,8 @@ def main():
         out["shift_gradW"] = shift_bench(args, fqt, torch, dX, dW, dG)
         out["sub8bit_mfma"] = bf6_bench(args, fqt, torch)
         out["conv_layer"] = conv_bench(args, fqt, synth, torch)
+        out["resnet50_batch256"] = resnet_sweep(args, fqt, synth, torch)
+        out["seed_batch"] = seeds_bench(args, fqt, synth, torch)
     if args.copy_probe:
         # a plain elementwise pass: reads 256 MiB, writes 256 MiB
         src = torch.ones(64 * 1024 * 1024, dtype=torch.float32, device="cuda")

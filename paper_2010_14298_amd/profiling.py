@@ -2,10 +2,13 @@
 
     python -m paper_2010_14298_amd.profiling trace  <trace_dir> <out.md> "<command>"
     python -m paper_2010_14298_amd.profiling traffic <fetch_dir> <write_dir> <out.txt> "<commands>"
+    python -m paper_2010_14298_amd.profiling counters <out.json> "<commands>" <pmc_dir> [<pmc_dir> ...]
 
 `trace` reads the kernel-trace CSV of `rocprofv3 --kernel-trace --stats
 --output-format csv` and writes per-kernel call counts and average / total
-durations.  `traffic` reads two `rocprofv3 --pmc FETCH_SIZE` / `--pmc
+durations.  `counters` averages every counter of the given `rocprofv3 --pmc` passes per
+kernel (and the derived VALUBusy / MfmaUtil when a pass collected them),
+with the hash of the kernel sources.  `traffic` reads two `rocprofv3 --pmc FETCH_SIZE` / `--pmc
 WRITE_SIZE` runs (KiB per dispatch), calibrates each counter on the plain
 elementwise pass that `bench.py --copy-probe` launches (known bytes read and
 written), and writes the scaled HBM bytes per dispatch of every kernel, with
@@ -95,8 +98,26 @@ def traffic(fetch_dir, write_dir, out, command):
     print(json.dumps(res, indent=1))
 
 
+def counters(out, command, dirs):
+    kernels = defaultdict(dict)
+    for d in dirs:
+        rows = list(csv.DictReader(open(_find(d, "counter_collection.csv"))))
+        agg = defaultdict(lambda: defaultdict(list))
+        for r in rows:
+            agg[_short(r["Kernel_Name"])][r["Counter_Name"]].append(float(r["Counter_Value"]))
+        for k, cs in agg.items():
+            for c, v in cs.items():
+                kernels[k][c] = round(sum(v) / len(v), 4)
+    res = {"command": command, "kernel_sources": source_hash(), "passes": len(dirs), "kernels": kernels}
+    with open(out, "w") as f:
+        json.dump(res, f, indent=1)
+    print(json.dumps(res, indent=1))
+
+
 if __name__ == "__main__":
-    if sys.argv[1] == "trace":
+    if sys.argv[1] == "counters":
+        counters(sys.argv[2], sys.argv[3], sys.argv[4:])
+    elif sys.argv[1] == "trace":
         trace(sys.argv[2], sys.argv[3], sys.argv[4])
     elif sys.argv[1] == "traffic":
         traffic(sys.argv[2], sys.argv[3], sys.argv[4], sys.argv[5])
