@@ -229,13 +229,22 @@ typedef struct {
   /* Optional caller buffers (device; linear layer only, the conv ignores
    * them) that receive the gradient codes the contractions read, in place of
    * the workspace copies:
-   *   qb2_codes [N, d_out]  Q_b2(G) offset codes, rows in slot order
+   *   qb2_codes [N, d_out]  Q_b2(G) offset codes, rows in slot order; with
+   *                         packed_codes they are [N, d_out / 2] bytes,
+   *                         code + 2^(b-1) in a nibble (column 2i in the low
+   *                         half of byte i)
    *   qb1_codes [d_out, N]  Q_b1(G) offset codes, transposed, slot order
    *   perm      [N]         BHQ: slot -> row (not written for PTQ / PSQ,
    *                         whose slot order is the row order)             */
   int8_t* qb2_codes;
   int8_t* qb1_codes;
   int32_t* perm;
+  /* packed_codes (linear layer): 1 stores Q_b2 codes of at most 4 bits two
+   * per byte (qb_x.bits <= 4, d_out % 16 == 0; ignored otherwise), halving
+   * their bytes; the grad_X contraction unpacks them as it loads them (its
+   * register-staged loop, slower than the int8 path's direct-to-LDS loop).
+   * 0 keeps one byte per code.                                             */
+  int packed_codes;
 } fqt_bwd_cfg;
 
 /* Linear layer FQT backward, Eq. (linear-sq-backprop) with bifurcation:
@@ -243,6 +252,8 @@ typedef struct {
  *   grad_X [N, d_in]     = Q_b2(G)   Q_theta(W)
  * both contracted on int8 matrix cores with exact int32 accumulators
  * (int64 across K-splits) and dequantized in float64, rounded to float32.
+ * With cfg->packed_codes, Q_b2 codes of at most 4 bits are stored two per
+ * byte and unpacked as the grad_X contraction loads them.
  * Outputs are overwritten.  N, d_in, d_out >= 1.                            */
 fqt_status fqt_linear_backward(const float* X, const float* W, const float* G, int64_t N, int64_t d_in,
                                int64_t d_out, const fqt_bwd_cfg* cfg, float* grad_W, float* grad_X,

@@ -383,6 +383,7 @@ fqt_status check_cfg(const fqt_bwd_cfg* cfg) {
     return FQT_EUNSUPPORTED;
   if (cfg->qb_x.kind == FQT_BHQ && cfg->qb_x.block_size < 0) return FQT_EINVAL;
   if (cfg->relu_input != 0 && cfg->relu_input != 1) return FQT_EINVAL;
+  if (cfg->packed_codes != 0 && cfg->packed_codes != 1) return FQT_EINVAL;
   return FQT_OK;
 }
 
@@ -721,6 +722,10 @@ fqt_status fqt_linear_backward(const float* X, const float* W, const float* G, i
   pg.zero = w.zg2;
   pg.q_nat = w.qg2;
   pg.sum_nat = w.sum_g2;
+  // codes of at most 4 bits are stored two per byte and unpacked by the
+  // grad_X contraction's loader
+  const bool packed = cfg->packed_codes == 1 && qx.bits <= 4 && d_out % 16 == 0;
+  pg.packed = packed ? 1 : 0;
   pg.bits2 = cfg->qb_w.bits;
   pg.stream2 = 0;
   pg.scale2 = w.sg1;
@@ -802,7 +807,8 @@ fqt_status fqt_linear_backward(const float* X, const float* W, const float* G, i
   gx.M = N;
   gx.N = d_in;
   gx.K = d_out;
-  gx.lda = d_out;
+  gx.lda = packed ? d_out / 2 : d_out;
+  gx.packedA = packed ? 1 : 0;
   gx.ldb = d_out;
   gx.splits = 1;
   gx.kchunk = d_out;

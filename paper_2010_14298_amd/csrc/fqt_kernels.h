@@ -185,7 +185,8 @@ struct QuantParams {
   uint32_t stream;
   const float* scale;  // per tensor: [1]; per row / BHQ: [rows] per slot
   const float* zero;
-  int8_t* q_nat;       // [rows, cols] slot order, or nullptr
+  int8_t* q_nat;       // [rows, cols] slot order, or nullptr (packed: [rows, cols / 2] bytes)
+  int packed;          // natural codes of bits <= 4 stored two per byte (float4 rows only)
   int32_t* sum_nat;    // [rows] row sums, or nullptr
   int8_t* q_t;         // [cols, rows] slot order, or nullptr
   int32_t* sum_t;      // [cols] column sums, or nullptr
@@ -249,7 +250,8 @@ enum Epilogue {
 };
 
 struct GemmParams {
-  const int8_t* A;  // [M, K] row stride lda
+  const int8_t* A;  // [M, K] row stride lda (bytes)
+  int packedA;      // A holds codes of at most 4 bits two per byte (as the quantizer packs them), K % 16 == 0
   const int8_t* B;  // [N, K] row stride ldb
   int64_t M, N, K, lda, ldb;
   int64_t kchunk;   // K per split (multiple of 128 when split, <= 65536)

@@ -50,7 +50,7 @@ struct GemmLdsSize {
   static constexpr int BYTES = (STAGED && EP_BYTES > C::OP_BYTES) ? EP_BYTES : C::OP_BYTES;
 };
 
-template <class C, int EPI, int KG, bool FAST>
+template <class C, int EPI, int KG, bool FAST, bool PK = false>
 __global__ __launch_bounds__(C::THREADS) void gemm_i8_kernel(GemmParams p) {
   __shared__ __attribute__((aligned(16))) int8_t lds[GemmLdsSize<C, EPI>::BYTES];
   const int tid = threadIdx.x;
@@ -72,8 +72,15 @@ __global__ __launch_bounds__(C::THREADS) void gemm_i8_kernel(GemmParams p) {
   for (int i = 0; i < C::IT; ++i)
 #pragma unroll
     for (int j = 0; j < C::JT; ++j) acc[i][j] = v16i{0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0};
-  const PlainALoader aload{p.A, p.lda, p.M, kend, ((p.lda & 15) == 0) && (((uintptr_t)p.A & 15) == 0)};
-  gemm_mainloop<C, FAST>(p, aload, lds, m0, n0, kbeg, kend, acc);
+  if constexpr (PK) {
+    // packed A: the register-staged loop, unpacking in the loader
+    const bool alB = ((p.ldb & 15) == 0) && (((uintptr_t)p.B & 15) == 0);
+    generic_mainloop<C>(p, PackedALoader{p.A, p.lda, p.M, kend}, PlainBLoader{p.B, p.ldb, p.N, kend, alB}, lds, m0,
+                        n0, kbeg, kend, acc);
+  } else {
+    const PlainALoader aload{p.A, p.lda, p.M, kend, ((p.lda & 15) == 0) && (((uintptr_t)p.A & 15) == 0)};
+    gemm_mainloop<C, FAST>(p, aload, lds, m0, n0, kbeg, kend, acc);
+  }
 
   // ---- epilogue.  Accumulator (i, j, r) of lane l holds
   //   row = wm*WM + i*32 + 8*(r/4) + 4*(l/32) + r%4,  col = wn*WN + j*32 + l%32
@@ -393,6 +400,14 @@ static hipError_t launch_gemm_t(GemmParams p, hipStream_t s) {
   const bool fast = ((p.lda & 15) == 0) && ((p.ldb & 15) == 0) && (((uintptr_t)p.A & 15) == 0) &&
                     (((uintptr_t)p.B & 15) == 0) && whole;
   const dim3 grid((unsigned)tiles, (unsigned)p.splits);
+  if constexpr (EPI == EPI_ROW || EPI == EPI_BHQ || EPI == EPI_BHQT) {
+    if (p.packedA) {
+      if (p.K % 16 != 0 || (p.lda & 7) != 0 || ((uintptr_t)p.A & 7) != 0) return hipErrorInvalidValue;
+      hipLaunchKernelGGL((gemm_i8_kernel<C, EPI, KG, false, true>), grid, dim3(C::THREADS), 0, s, p);
+      return hipGetLastError();
+    }
+  }
+  if (p.packedA) return hipErrorInvalidValue;
   if (fast)
     hipLaunchKernelGGL((gemm_i8_kernel<C, EPI, KG, true>), grid, dim3(C::THREADS), 0, s, p);
   else

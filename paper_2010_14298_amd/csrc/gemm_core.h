@@ -106,6 +106,36 @@ struct PlainALoader {
   }
 };
 
+// A operand of codes of at most 4 bits stored two per byte (code + 8 in a
+// nibble, column 2i in the low half of byte i): 16 codes from 8 bytes,
+// unpacked to int8 offset codes.  K is a multiple of 16 (checked at launch),
+// so a chunk is whole or past the end (zero).
+struct PackedALoader {
+  const int8_t* A;
+  int64_t lda, M, kend;  // lda in bytes
+  struct Row {
+    int64_t r;
+  };
+  typedef int64_t KState;
+  __device__ __forceinline__ Row row(int64_t r) const { return Row{r}; }
+  __device__ __forceinline__ KState kstate(int64_t k) const { return k; }
+  // 8 nibbles of w -> 8 offset codes in two words
+  __device__ __forceinline__ static void unpack8(uint32_t w, uint32_t& o0, uint32_t& o1) {
+    const uint32_t lo = w & 0x0F0F0F0Fu, hi = (w >> 4) & 0x0F0F0F0Fu;
+    // bytes (lo0, hi0, lo1, hi1) and (lo2, hi2, lo3, hi3); u -> u - 8 as int8 is (u + 0x78) ^ 0x80
+    o0 = (__builtin_amdgcn_perm(hi, lo, 0x05010400u) + 0x78787878u) ^ 0x80808080u;
+    o1 = (__builtin_amdgcn_perm(hi, lo, 0x07030602u) + 0x78787878u) ^ 0x80808080u;
+  }
+  __device__ __forceinline__ Chunk16 load(const Row& rw, const KState& k) const {
+    Chunk16 c{{0u, 0u, 0u, 0u}};
+    if (rw.r >= M || k >= kend) return c;
+    const uint2 v = *reinterpret_cast<const uint2*>(A + rw.r * lda + (k >> 1));
+    unpack8(v.x, c.w[0], c.w[1]);
+    unpack8(v.y, c.w[2], c.w[3]);
+    return c;
+  }
+};
+
 // The B operand of the generic loop: 16-byte chunks of K-contiguous rows,
 // zero outside the matrix / K range (`load_chunk`).
 struct PlainBLoader {

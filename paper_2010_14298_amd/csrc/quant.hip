@@ -984,7 +984,14 @@ __device__ __forceinline__ void quant_tile(const QuantParams& p, int64_t bx, int
       const uint32_t w = pack_top4(t[0], t[1], t[2], t[3]);
       if (p.q_nat && ok && lane_ok) {
         int8_t* dst = p.q_nat + slot * cols + c0;
-        if constexpr (VEC) {
+        if (VEC && p.packed) {
+          // codes of at most 4 bits, two per byte: the nibble of column 2i is
+          // the low half of byte i, the code stored as q + 8 in [0, 15]
+          const uint32_t nb = (w ^ 0x08080808u) & 0x0F0F0F0Fu;
+          const uint32_t x2 = nb | (nb >> 4);
+          const uint32_t pk = __builtin_amdgcn_perm(0u, x2, 0x0c0c0200u);  // bytes 0 and 2 of x2
+          *reinterpret_cast<uint16_t*>(p.q_nat + (slot * cols + c0) / 2) = (uint16_t)pk;
+        } else if constexpr (VEC) {
           *reinterpret_cast<uint32_t*>(dst) = w;
         } else {
 #pragma unroll
@@ -1131,6 +1138,7 @@ static hipError_t launch_quant_k(const QuantParams& p, hipStream_t s) {
   if (ct > 0x7FFFFFFF || rt > 65535) return hipErrorInvalidValue;
   const dim3 grid((unsigned)ct, (unsigned)rt);
   const bool vec = (p.cols % 4 == 0) && (((uintptr_t)p.x & 15) == 0);
+  if (p.packed && (!vec || p.bits > 4 || p.q_t)) return hipErrorInvalidValue;
   // one primary layout: natural (with an optional transposed Q_b1) or transposed
   if ((p.q_nat || p.sum_nat) && (p.q_t || p.sum_t)) return hipErrorInvalidValue;
   const bool trans = p.q_t || p.sum_t;
@@ -1182,6 +1190,7 @@ hipError_t launch_quant_fused(const QuantParams& pg, int mode, const QuantParams
   // float4 rows everywhere, natural + transposed Q_b1 for the gradient,
   // transposed only for X and W; anything else goes out as three launches
   auto vec = [](const QuantParams& p) { return (p.cols % 4 == 0) && (((uintptr_t)p.x & 15) == 0); };
+  if (pg.packed && (!vec(pg) || pg.bits > 4)) return hipErrorInvalidValue;
   const bool shape = vec(pg) && vec(px) && vec(pw) && pg.q2_t && pg.stoch && !pg.q_t && !pg.sum_t && !px.q_nat &&
                      !px.sum_nat && !px.q2_t && px.q_t && !pw.q_nat && !pw.sum_nat && !pw.q2_t && pw.q_t;
   if (!shape) {

@@ -48,7 +48,8 @@ class Trace(ctypes.Structure):
 class BwdCfg(ctypes.Structure):
     _fields_ = [("qb_w", QSpec), ("qb_x", QSpec), ("f_bits", ctypes.c_int), ("theta_bits", ctypes.c_int),
                 ("seed", ctypes.c_uint64), ("trace", ctypes.POINTER(Trace)), ("relu_input", ctypes.c_int),
-                ("qb2_codes", ctypes.c_void_p), ("qb1_codes", ctypes.c_void_p), ("perm", ctypes.c_void_p)]
+                ("qb2_codes", ctypes.c_void_p), ("qb1_codes", ctypes.c_void_p), ("perm", ctypes.c_void_p),
+                ("packed_codes", ctypes.c_int)]
 
 
 class ConvShape(ctypes.Structure):
@@ -289,7 +290,8 @@ def fqt_linear_backward_workspace(N, d_in, d_out, cfg):
 
 
 def fqt_linear_backward(X, W, G, qb_x=("psq", 8, 0), qb_w=("ptq", 8, 0), f_bits=8, theta_bits=8, seed=0,
-                        grad_W=None, grad_X=None, ws=None, trace=None, relu_input=False, codes=None):
+                        grad_W=None, grad_X=None, ws=None, trace=None, relu_input=False, codes=None,
+                        packed_codes=False):
     """codes: optional dict to receive the gradient codes the contractions read:
     it is filled with qb2 [N, d_out], qb1_t [d_out, N] (int8, slot order) and,
     for BHQ, perm [N]."""
@@ -299,6 +301,7 @@ def fqt_linear_backward(X, W, G, qb_x=("psq", 8, 0), qb_w=("ptq", 8, 0), f_bits=
     if W.shape != (d_out, d_in) or G.shape != (N, d_out):
         raise ValueError("shapes: X [N, d_in], W [d_out, d_in], G [N, d_out]")
     cfg = cfg_struct(qb_x, qb_w, f_bits, theta_bits, seed, trace, relu_input)
+    cfg.packed_codes = int(bool(packed_codes))
     if codes is not None:
         codes["qb2"] = torch.empty((N, d_out), dtype=torch.int8, device=X.device)
         codes["qb1_t"] = torch.empty((d_out, N), dtype=torch.int8, device=X.device)

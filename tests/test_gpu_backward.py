@@ -126,6 +126,20 @@ def test_gemm_accumulators_full_size_sampled(M, N, K):
     np.testing.assert_array_equal(C[rows], ref.astype(np.int64))
 
 
+def stored_codes(buf, bits):
+    """Offset codes from the layer's Q_b2 code buffer [N, d_out]: codes of at
+    most 4 bits are packed two per byte ([N, d_out / 2], code + 2^(b-1) in a
+    nibble, column 2i in the low half of byte i), wider codes are int8."""
+    if bits > 4:
+        return buf
+    N, D = buf.shape
+    pk = buf.reshape(-1)[: N * D // 2].view(np.uint8).reshape(N, D // 2)
+    out = np.empty((N, D), np.int16)
+    out[:, 0::2] = pk & 15
+    out[:, 1::2] = pk >> 4
+    return (out - 8).astype(np.int8)
+
+
 @pytest.fixture(scope="module")
 def ffn_layer():
     """The FFN layer's inputs and the oracle's parts that do not depend on Q_b2."""
@@ -171,3 +185,22 @@ def test_linear_ffn_full_size(ffn_layer, qb_x):
     cols_o = rng.choice(G.shape[1], 48, replace=False)
     G1r = Q.dequantize_affine(dict(qb1, code=qb1["code"][:, cols_o]))
     assert rownorm_err(gW[cols_o], G1r.T @ L["Xr"]) <= REL_TOL
+
+
+@pytest.mark.parametrize("shape", [(300, 64, 160), (1000, 96, 512), (129, 130, 36)])
+@pytest.mark.parametrize("qb_x", [("ptq", 4, 0), ("psq", 3, 0), ("bhq", 4, 64), ("bhq", 2, 0)])
+def test_linear_packed_codes(shape, qb_x):
+    """Q_b2 codes of at most 4 bits stored two per byte: the stored codes
+    unpack to the oracle's, and grad_X (read through the unpacking loader)
+    matches within 1e-5."""
+    N, d_in, d_out = shape
+    X, W, G = synth.linear_small(seed=N + d_out, n=N, d_in=d_in, d_out=d_out)
+    r = BW.linear_backward(X, W, G, qb_x=qb_x, seed=3)
+    f = fqt()
+    codes = {}
+    gW, gX, ws = f.fqt_linear_backward(dev(X), dev(W), dev(G), qb_x=qb_x, seed=3, codes=codes, packed_codes=True)
+    assert f.fqt_workspace_status(ws) == 0
+    np.testing.assert_array_equal(stored_codes(host(codes["qb2"]), qb_x[1]) if d_out % 16 == 0
+                                  else host(codes["qb2"]), (r["qb2"]["code"] - Q.offset(qb_x[1])).astype(np.int8))
+    assert rownorm_err(host(gW), r["grad_W64"]) <= REL_TOL
+    assert rownorm_err(host(gX), r["grad_X64"]) <= REL_TOL
