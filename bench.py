@@ -221,10 +221,12 @@ def shift_bench(args, fqt, torch, dX, dW, dG):
             "TOPS": round(2.0 * 2.0 * N * D_IN * D_OUT / (ms * 1e-3) / 1e12, 2)}
 
 
-def conv_bench(args, fqt, synth, torch):
+def conv_bench(args, fqt, synth, torch, qb_w=None):
     """The conv layer of the paper's overhead example (N = 128, C = 64, 56 x 56;
     a 3 x 3, 64 -> 64, stride-1 conv): the whole FQT backward with Q_b2 = BHQ
-    5-bit across samples (block 64), Q_b1 = PTQ 8-bit, HIP events."""
+    5-bit across samples (block 64), Q_b1 = PTQ 8-bit (or per sample: grad_W
+    in one K block per sample), HIP events."""
+    qb_w = qb_w or QB_W
     n, c, h, o, k = 128, 64, 56, 64, 3
     X, W, G = synth.conv_layer(seed=0, n=n, c=c, h=h, w=h, o=o, k=k, stride=1, pad=1)
     dX, dW, dG = (torch.from_numpy(a).cuda() for a in (X, W, G))
@@ -232,20 +234,21 @@ def conv_bench(args, fqt, synth, torch):
     gX = torch.empty(X.shape, dtype=torch.float32, device="cuda")
     ws = None
     for i in range(3):
-        _, _, ws = fqt.fqt_conv_backward_im2col(dX, dW, dG, 1, 1, qb_x=QB_X, qb_w=QB_W, seed=i, grad_W=gW,
+        _, _, ws = fqt.fqt_conv_backward_im2col(dX, dW, dG, 1, 1, qb_x=QB_X, qb_w=qb_w, seed=i, grad_W=gW,
                                                  grad_X=gX, ws=ws)
     torch.cuda.synchronize()
     steps = max(2, args.steps // 10)
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record()
     for i in range(steps):
-        fqt.fqt_conv_backward_im2col(dX, dW, dG, 1, 1, qb_x=QB_X, qb_w=QB_W, seed=i, grad_W=gW, grad_X=gX, ws=ws)
+        fqt.fqt_conv_backward_im2col(dX, dW, dG, 1, 1, qb_x=QB_X, qb_w=qb_w, seed=i, grad_W=gW, grad_X=gX, ws=ws)
     e1.record()
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / steps
     ops = 2.0 * 2.0 * n * h * h * (c * k * k) * o
     return {"workload": "conv 3x3 64->64, 56x56, batch 128, stride 1 (the paper's overhead-example layer); "
-                        "Q_b2 = BHQ 5-bit across samples (block 64), Q_b1 = PTQ 8-bit", "steps": steps,
+                        "Q_b2 = BHQ 5-bit across samples (block 64), Q_b1 = %s %d-bit" % (qb_w[0].upper(), qb_w[1]),
+            "steps": steps,
             "ms_per_step": round(ms, 4), "TOPS": round(ops / (ms * 1e-3) / 1e12, 2)}
 
 
@@ -476,6 +479,7 @@ def main():
         out["shift_gradW"] = shift_bench(args, fqt, torch, dX, dW, dG)
         out["sub8bit_mfma"] = bf6_bench(args, fqt, torch)
         out["conv_layer"] = conv_bench(args, fqt, synth, torch)
+        out["conv_layer_per_sample_b1"] = conv_bench(args, fqt, synth, torch, qb_w=("psq", 8, 0))
         out["resnet50_batch256"] = resnet_sweep(args, fqt, synth, torch)
         out["seed_batch"] = seeds_bench(args, fqt, synth, torch)
     if args.copy_probe:

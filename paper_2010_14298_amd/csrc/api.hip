@@ -379,8 +379,7 @@ fqt_status check_cfg(const fqt_bwd_cfg* cfg) {
   if (cfg->qb_x.kind < FQT_PTQ || cfg->qb_x.kind > FQT_SHIFT || cfg->qb_w.kind < FQT_PTQ ||
       cfg->qb_w.kind > FQT_SHIFT)
     return FQT_EINVAL;
-  if ((cfg->qb_w.kind != FQT_PTQ && cfg->qb_w.kind != FQT_SHIFT) || cfg->qb_x.kind == FQT_SHIFT)
-    return FQT_EUNSUPPORTED;
+  if (cfg->qb_w.kind == FQT_BHQ || cfg->qb_x.kind == FQT_SHIFT) return FQT_EUNSUPPORTED;
   if (cfg->qb_x.kind == FQT_BHQ && cfg->qb_x.block_size < 0) return FQT_EINVAL;
   if (cfg->relu_input != 0 && cfg->relu_input != 1) return FQT_EINVAL;
   if (cfg->packed_codes != 0 && cfg->packed_codes != 1) return FQT_EINVAL;
@@ -405,8 +404,16 @@ fqt_status check_conv_shape(const fqt_conv_shape& sh) {
 }
 
 ConvGeom conv_geom(const fqt_conv_shape& sh) {
-  ConvGeom g{sh.n, sh.c, sh.h, sh.w, sh.o, sh.kh, sh.kw, sh.stride, sh.pad, sh.ho, sh.wo, 0};
+  ConvGeom g{sh.n, sh.c, sh.h, sh.w, sh.o, sh.kh, sh.kw, sh.stride, sh.pad, sh.ho, sh.wo, 0, 0};
   g.npad = ((int64_t)sh.n + 63) / 64 * 64;
+  g.psp = (int64_t)sh.ho * sh.wo;
+  return g;
+}
+
+// per-sample Q_b1: each slot's output pixels start a 128-byte K stage
+ConvGeom conv_geom(const fqt_conv_shape& sh, const fqt_bwd_cfg& cfg) {
+  ConvGeom g = conv_geom(sh);
+  if (cfg.qb_w.kind == FQT_PSQ) g.psp = (g.psp + 127) / 128 * 128;
   return g;
 }
 
@@ -420,6 +427,7 @@ struct ConvWs {
   int32_t* perm;
   BhqWs bhq;
   double* tbuf;      // general BHQ plan: T rows (input pixel, slot) of multi-row groups [h w npad, c]
+  ConvPsqSums ps;    // per-sample Q_b1
   int32_t* part;
   int64_t ldq, kchunk;
   int splits;
@@ -441,7 +449,8 @@ ConvWs carve_conv(Carver& c, const float* X, const float* W, const float* G, con
   w.rmin = c.take<float>(N);
   w.rmax = c.take<float>(N);
   stats_direct_rows(w.sg_seg, w.rmin, w.rmax);
-  w.ldq = (P + 127) / 128 * 128;
+  const bool psq1 = cfg.qb_w.kind == FQT_PSQ;
+  w.ldq = psq1 ? N * g.psp : (P + 127) / 128 * 128;
   w.xq_t = c.take<int8_t>((int64_t)g.c * N * hw);
   w.wq_t = c.take<int8_t>((int64_t)g.c * taps * g.o);
   w.q2 = c.take<int8_t>(N * howo * g.o);
@@ -460,14 +469,28 @@ ConvWs carve_conv(Carver& c, const float* X, const float* W, const float* G, con
   w.zx = c.take<float>(1);
   w.sw = c.take<float>(1);
   w.zw = c.take<float>(1);
-  w.sg1 = c.take<float>(1);
-  w.zg1 = c.take<float>(1);
+  w.sg1 = c.take<float>(psq1 ? N : 1);
+  w.zg1 = c.take<float>(psq1 ? N : 1);
   w.sg2 = c.take<float>(N);
   w.zg2 = c.take<float>(N);
   if (cfg.qb_x.kind == FQT_BHQ) {
     w.perm = c.take<int32_t>(N);
     w.bhq = carve_bhq(c, N, howo * g.o, cfg.qb_x.block_size);
     if (w.bhq.general) w.tbuf = c.take<double>(hw * g.npad * g.c);
+  }
+  if (psq1) {
+    // one K block per slot: exact int32 partials, weighted in float64
+    w.ps.dA = c.take<double>(N);
+    w.ps.zA = c.take<double>(N);
+    w.ps.zsum = c.take<double>(1);
+    w.ps.qw = c.take<double>((int64_t)g.o * howo);
+    w.ps.xw = c.take<double>((int64_t)g.c * hw);
+    w.ps.WA = c.take<double>((int64_t)g.o * taps);
+    w.ps.WB = c.take<double>(taps * g.c);
+    w.kchunk = g.psp;
+    w.splits = (int)N;
+    w.part = c.take<int32_t>(N * g.o * taps * g.c);
+    return w;
   }
   // grad_W: split the pixel contraction so that about 512 blocks run, each
   // K chunk a whole number of 128-byte stages and at most 65536
@@ -614,7 +637,7 @@ fqt_status fqt_bhq_adaptive_groups(const float* x, int64_t rows, int64_t cols, i
 }
 
 size_t fqt_linear_backward_workspace(int64_t N, int64_t d_in, int64_t d_out, const fqt_bwd_cfg* cfg) {
-  if (!cfg || N < 1 || d_in < 1 || d_out < 1) return 0;
+  if (!cfg || N < 1 || d_in < 1 || d_out < 1 || cfg->qb_w.kind == FQT_PSQ) return 0;
   Carver c(nullptr);
   carve_linear(c, nullptr, nullptr, nullptr, N, d_in, d_out, *cfg);
   return c.off;
@@ -627,6 +650,8 @@ fqt_status fqt_linear_backward(const float* X, const float* W, const float* G, i
   if (N < 1 || d_in < 1 || d_out < 1) return FQT_EINVAL;
   fqt_status st = check_cfg(cfg);
   if (st != FQT_OK) return st;
+  // a per-sample Q_b1 takes the shift form (Sec. 4.3) on a linear layer
+  if (cfg->qb_w.kind == FQT_PSQ) return FQT_EUNSUPPORTED;
   if (N > MAX_ROWS || d_out > MAX_ROWS || d_out > MAX_K_CHUNK || N > 0x7FFFFFFF / 2) return FQT_EUNSUPPORTED;
   if (cfg->qb_x.kind == FQT_BHQ) {
     st = check_block(cfg->qb_x.block_size, N);
@@ -1048,13 +1073,17 @@ fqt_status fqt_conv_backward_im2col(const float* X, const float* W, const float*
   st = check_cfg(cfg);
   if (st != FQT_OK) return st;
   if (cfg->relu_input || cfg->qb_w.kind == FQT_SHIFT) return FQT_EUNSUPPORTED;
+  // per-sample Q_b1: one int32-exact K block per sample, one split per sample
+  if (cfg->qb_w.kind == FQT_PSQ && ((int64_t)shape->ho * shape->wo > MAX_K_CHUNK || shape->n > 65535))
+    return FQT_EUNSUPPORTED;
   if (cfg->qb_x.kind == FQT_BHQ) {
     st = check_block(cfg->qb_x.block_size, shape->n);
     if (st != FQT_OK) return st;
   }
   if (!ws) return FQT_EWORKSPACE;
   if (ws_bytes < fqt_conv_backward_workspace(shape, cfg)) return FQT_EWORKSPACE;
-  const ConvGeom g = conv_geom(*shape);
+  const ConvGeom g = conv_geom(*shape, *cfg);
+  const bool psq1 = cfg->qb_w.kind == FQT_PSQ;
   Carver c(ws);
   ConvWs w = carve_conv(c, X, W, G, g, *cfg);
   const fqt_qspec qx = cfg->qb_x;
@@ -1086,10 +1115,10 @@ fqt_status fqt_conv_backward_im2col(const float* X, const float* W, const float*
   fp.status = w.h.status;
   fp.out[0] = ScaleOut{0, cfg->f_bits, 0, w.sx, w.zx};
   fp.out[1] = ScaleOut{1, cfg->theta_bits, 0, w.sw, w.zw};
-  fp.out[2] = ScaleOut{2, cfg->qb_w.bits, 0, w.sg1, w.zg1};
+  fp.out[2] = ScaleOut{2, cfg->qb_w.bits, psq1 ? 1 : 0, w.sg1, w.zg1};
   fp.nout = 3;
   if (!bhq) fp.out[fp.nout++] = ScaleOut{2, qx.bits, qx.kind == FQT_PSQ ? 1 : 0, w.sg2, w.zg2};
-  add_zero(fp, w.sumB, taps * g.c);
+  if (!psq1) add_zero(fp, w.sumB, taps * g.c);
   if (bhq) add_zero(fp, bhq_plan_carve(w.bhq.plan, N).rank, N);
   const bool fin_in_plan = bhq && w.sg_seg.rmin != nullptr;
   if (!fin_in_plan) FQT_TRY(launch_finalize(fp, s));
@@ -1142,10 +1171,12 @@ fqt_status fqt_conv_backward_im2col(const float* X, const float* W, const float*
   FQT_TRY(launch_quant(pg, mode, s));
   NarrowQParams n1{};
   n1.x = G;
-  n1.rows = N * howo;
+  n1.rows = N * g.psp;
   n1.cols = g.o;
   n1.perm = w.perm;
-  n1.blk = howo;
+  n1.blk = g.psp;
+  n1.vblk = howo;
+  n1.rowscale = psq1 ? 1 : 0;
   n1.bits = cfg->qb_w.bits;
   n1.stoch = 1;
   n1.seed = cfg->seed;
@@ -1159,8 +1190,12 @@ fqt_status fqt_conv_backward_im2col(const float* X, const float* W, const float*
 
   // grad_W [o][(r, s, c)] = Q_b1(G)^T im2col(Q_f(X)), split over output pixels
   tr.begin(6);
-  FQT_TRY(launch_conv_im2col_w(g, w.xq_t, w.bw, w.ldq, w.xs, w.sumB, s));
-  FQT_TRY(launch_conv_tapsums(g, w.q1_t, w.ldq, w.qs, w.sumA_tap, w.count_tap, s));
+  FQT_TRY(launch_conv_im2col_w(g, w.xq_t, w.bw, w.ldq, psq1 ? nullptr : w.xs, w.sumB, s));
+  if (psq1)
+    FQT_TRY(launch_conv_psq_sums(g, w.sg1, w.zg1, w.perm, 1 << (cfg->qb_w.bits - 1), w.q1_t, w.ldq, w.xq_t, w.ps,
+                                 w.count_tap, s));
+  else
+    FQT_TRY(launch_conv_tapsums(g, w.q1_t, w.ldq, w.qs, w.sumA_tap, w.count_tap, s));
   GemmParams gw{};
   gw.A = w.q1_t;
   gw.B = w.bw;
@@ -1182,7 +1217,10 @@ fqt_status fqt_conv_backward_im2col(const float* X, const float* W, const float*
   gw.zeroB = w.zx;
   gw.halfB = 1 << (cfg->f_bits - 1);
   FQT_TRY(launch_gemm(gw, EPI_RAW_I32, s));
-  FQT_TRY(launch_conv_gradw_reduce(gw, g, w.sumA_tap, w.count_tap, s));
+  if (psq1)
+    FQT_TRY(launch_conv_gradw_psq_reduce(gw, g, w.ps, w.count_tap, s));
+  else
+    FQT_TRY(launch_conv_gradw_reduce(gw, g, w.sumA_tap, w.count_tap, s));
   tr.end(6);
 
   // grad_X [n][h][w][c] = col2im(Q_b2(G) Q_theta(W)), implicit im2col rows
@@ -1237,7 +1275,7 @@ fqt_status fqt_conv_backward_im2col(const float* X, const float* W, const float*
 size_t fqt_conv_backward_workspace(const fqt_conv_shape* shape, const fqt_bwd_cfg* cfg) {
   if (!shape || !cfg || check_conv_shape(*shape) != FQT_OK) return 0;
   Carver c(nullptr);
-  carve_conv(c, nullptr, nullptr, nullptr, conv_geom(*shape), *cfg);
+  carve_conv(c, nullptr, nullptr, nullptr, conv_geom(*shape, *cfg), *cfg);
   return c.off;
 }
 

@@ -21,17 +21,22 @@
 
 namespace fqt {
 
-__device__ __forceinline__ int wave_sum4_i(int v) {
+template <typename T>
+__device__ __forceinline__ T wave_sum_t(T v) {
 #pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
   return v;
 }
+__device__ __forceinline__ int wave_sum4_i(int v) { return wave_sum_t<int>(v); }
 
 
 // ---------------------------------------------------------------------------
-// narrow transposing per-tensor quantizer: logical [rows, cols] -> codes
-// [cols][ldt], rows in slot order; rows in [rows, ldt) get code 0.  A block
-// covers 4 * LPR columns (grid.y walks wider rows in chunks of 256).
+// narrow transposing quantizer: logical [rows, cols] -> codes [cols][ldt].
+// Rows come in blocks of blk (a sample's pixels); block b takes source block
+// perm[b] (slot order) of vblk rows, and its rows past vblk, like rows in
+// [rows, ldt), get code 0.  Scale and zero are per tensor, or per source
+// block (a per-sample quantizer).  A block covers 4 * LPR columns (grid.y
+// walks wider rows in chunks of 256).
 // ---------------------------------------------------------------------------
 template <int LPR>
 __global__ __launch_bounds__(256) void quant_narrow_t_kernel(NarrowQParams p) {
@@ -43,22 +48,27 @@ __global__ __launch_bounds__(256) void quant_narrow_t_kernel(NarrowQParams p) {
   const int64_t c0 = (int64_t)blockIdx.y * (LPR * 4) + (int64_t)cl * 4;  // column chunks of 4 * LPR
   const int B = (1 << p.bits) - 1;
   const int half = 1 << (p.bits - 1);
-  const float s = p.scale[0], z = p.zero[0];
+  const float s0 = p.scale[0], z0 = p.zero[0];
+  const int64_t vblk = p.vblk > 0 ? p.vblk : p.blk;
   const bool vec = (p.cols & 3) == 0;
   uint32_t tcodes[4][4];
 #pragma unroll
   for (int j = 0; j < 4; ++j)
 #pragma unroll
     for (int w = 0; w < 4; ++w) tcodes[j][w] = 0u;
-  // rows r0 .. r0 + 15: block index and offset of r0 once, then stepped
-  int64_t bq = p.perm ? r0 / p.blk : 0;
-  int64_t br = p.perm ? r0 - bq * p.blk : 0;
+  // rows r0 .. r0 + 15: block index and offset of r0 once, then stepped.
+  // Row (bq, br) reads row br of source block perm[bq] (or bq) of vblk rows.
+  int64_t bq = r0 / p.blk;
+  int64_t br = r0 - bq * p.blk;
 #pragma unroll
   for (int r = 0; r < 16; ++r) {
     const int64_t row = r0 + r;
-    const bool ok = row < p.rows;
-    const int64_t src = ok ? (p.perm ? (int64_t)p.perm[bq] * p.blk + br : row) : 0;
-    if (p.perm && ++br == p.blk) {
+    const bool ok = row < p.rows && br < vblk;
+    const int64_t sb = ok ? (p.perm ? (int64_t)p.perm[bq] : bq) : 0;
+    const int64_t src = sb * vblk + br;
+    const float s = (p.rowscale && ok) ? p.scale[sb] : s0;
+    const float z = (p.rowscale && ok) ? p.zero[sb] : z0;
+    if (++br == p.blk) {
       br = 0;
       ++bq;
     }
@@ -118,6 +128,7 @@ __global__ __launch_bounds__(256) void quant_narrow_t_kernel(NarrowQParams p) {
 }
 
 hipError_t launch_quant_narrow_t(const NarrowQParams& p, hipStream_t s) {
+  if (p.blk < 1 || p.vblk < 0 || p.vblk > p.blk) return hipErrorInvalidValue;
   // lanes per row: the smallest power of two covering cols / 4, at most 64
   // (wider rows: column chunks of 256 along grid.y)
   const int64_t need = (p.cols + 3) / 4;
@@ -174,29 +185,31 @@ __global__ __launch_bounds__(256) void conv_im2col_w_kernel(ConvGeom g, const in
   const int tap = (int)(row / g.c), c = (int)(row % g.c);
   const int r = tap / g.kw, s = tap % g.kw;
   const int64_t hw = (int64_t)g.h * g.w, howo = (int64_t)g.ho * g.wo;
-  const int64_t P = (int64_t)g.n * howo;
   const int64_t p0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 16;
   const int8_t* xc = xq_t + (int64_t)c * g.n * hw;
   uint32_t w[4] = {0u, 0u, 0u, 0u};
   if (p0 < ldb) {
-    // (sample, y, x) of p0 once; the 16 pixels then step through x, y, sample
-    int64_t slot = p0 / howo;
-    const int pix0 = (int)(p0 - slot * howo);
-    int y = pix0 / g.wo, x = pix0 - (pix0 / g.wo) * g.wo;
+    // (sample, pixel, y, x) of p0 once; the 16 columns then step through x,
+    // y and the sample's pitch (columns past ho wo in a pitch are zero)
+    int64_t slot = p0 / g.psp;
+    int pix = (int)(p0 - slot * g.psp);
+    int y = pix / g.wo, x = pix - (pix / g.wo) * g.wo;
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
       int v = 0;
-      if (p0 + i < P) {
+      if (slot < g.n && pix < howo) {
         const int iy = y * g.stride - g.pad + r, ix = x * g.stride - g.pad + s;
         if (iy >= 0 && iy < g.h && ix >= 0 && ix < g.w) v = xc[slot * hw + iy * g.w + ix];
       }
       w[i >> 2] |= (uint32_t)(v & 255) << (8 * (i & 3));
+      ++pix;
       if (++x == g.wo) {
         x = 0;
-        if (++y == g.ho) {
-          y = 0;
-          ++slot;
-        }
+        ++y;
+      }
+      if (pix == g.psp) {
+        pix = x = y = 0;
+        ++slot;
       }
     }
     *reinterpret_cast<uint4*>(bw + row * ldb + p0) = make_uint4(w[0], w[1], w[2], w[3]);
@@ -250,7 +263,7 @@ __global__ __launch_bounds__(256) void conv_im2col_rows_kernel(ConvGeom g, const
     at[q] = -1;
     if (ls < segs_per_block && seg < (int)nseg) {
       const int iy = y - g.pad + r;
-      at[q] = (int64_t)seg * g.wo + 4 * j;
+      at[q] = (int64_t)slot * g.psp + (int64_t)y * g.wo + 4 * j;
       if (iy >= 0 && iy < g.h) {
         const uint32_t* src = reinterpret_cast<const uint32_t*>(xc + (int64_t)slot * hw + (int64_t)iy * g.w);
         const int k0 = j + wq;
@@ -278,8 +291,9 @@ __global__ __launch_bounds__(256) void conv_im2col_rows_kernel(ConvGeom g, const
     if (at[q] >= 0)
       *reinterpret_cast<uint32_t*>(dst + at[q]) =
           sh == 0 ? lo[q] : (uint32_t)((((uint64_t)hi[q] << 32) | lo[q]) >> (8 * sh));
-  // the zero tail [P, ldb) of the row: the last block's threads
-  if (blockIdx.x == gridDim.x - 1) {
+  // the zero tail [P, ldb) of the row: the last block's threads (a pitch
+  // longer than ho wo gets its zeros from conv_pitch_zero_kernel)
+  if (blockIdx.x == gridDim.x - 1 && g.psp == (int64_t)g.ho * g.wo) {
     const int64_t P = nseg * g.wo;
     for (int64_t t = P + 4 * (int64_t)threadIdx.x; t < ldb; t += 4 * (int64_t)blockDim.x)
       *reinterpret_cast<uint32_t*>(dst + t) = 0u;
@@ -311,20 +325,21 @@ __global__ void conv_xsum_kernel(ConvGeom g, const int8_t* xq_t, int32_t* xs) {
   xs[t] = (s4[0] + s4[1]) + (s4[2] + s4[3]);
 }
 
-__global__ __launch_bounds__(256) void conv_xtapsum_kernel(ConvGeom g, const int32_t* xs, int32_t* sumB) {
+template <typename T>
+__global__ __launch_bounds__(256) void conv_xtapsum_kernel(ConvGeom g, const T* xs, T* sumB) {
   const int64_t row = blockIdx.x;  // (tap, c)
   const int tap = (int)(row / g.c), c = (int)(row % g.c);
   const int r = tap / g.kw, s = tap % g.kw;
   int ylo, yhi, xlo, xhi;
   tap_range(r, g.stride, g.pad, g.h, g.ho, ylo, yhi);
   tap_range(s, g.stride, g.pad, g.w, g.wo, xlo, xhi);
-  const int32_t* x = xs + (int64_t)c * g.h * g.w;
+  const T* x = xs + (int64_t)c * g.h * g.w;
   const int wx = xhi - xlo, cnt = (yhi - ylo) * wx;
-  int sum = 0;
+  T sum = 0;
   // eight loads in flight per round: indices past cnt are clamped (their
   // values dropped), so no load sits under a branch
   for (int i0 = threadIdx.x; i0 < cnt; i0 += 8 * blockDim.x) {
-    int v[8];
+    T v[8];
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
       const int i = min(i0 + u * (int)blockDim.x, cnt - 1);
@@ -336,8 +351,8 @@ __global__ __launch_bounds__(256) void conv_xtapsum_kernel(ConvGeom g, const int
     for (int u = 0; u < 8; ++u)
       if (i0 + u * (int)blockDim.x < cnt) sum += v[u];
   }
-  __shared__ int ssum[4];
-  sum = wave_sum4_i(sum);
+  __shared__ T ssum[4];
+  sum = wave_sum_t<T>(sum);
   if ((threadIdx.x & 63) == 0) ssum[threadIdx.x >> 6] = sum;
   __syncthreads();
   if (threadIdx.x == 0) sumB[row] = ssum[0] + ssum[1] + ssum[2] + ssum[3];
@@ -356,8 +371,8 @@ __global__ void conv_qsum_kernel(ConvGeom g, const int8_t* q1_t, int64_t ldq, in
 }
 
 // valid output rows / columns of tap offset r: y with 0 <= y*stride - pad + r < h
-__global__ __launch_bounds__(256) void conv_tapsum_kernel(ConvGeom g, const int32_t* qs, int32_t* sumA_tap,
-                                                          int32_t* count_tap) {
+template <typename T>
+__global__ __launch_bounds__(256) void conv_tapsum_kernel(ConvGeom g, const T* qs, T* sumA_tap, int32_t* count_tap) {
   const int taps = g.kh * g.kw;
   const int64_t t = blockIdx.x;
   const int o = (int)(t / taps), tap = (int)(t % taps);
@@ -365,12 +380,12 @@ __global__ __launch_bounds__(256) void conv_tapsum_kernel(ConvGeom g, const int3
   int ylo, yhi, xlo, xhi;
   tap_range(r, g.stride, g.pad, g.h, g.ho, ylo, yhi);
   tap_range(s, g.stride, g.pad, g.w, g.wo, xlo, xhi);
-  const int32_t* q = qs + (int64_t)o * g.ho * g.wo;
+  const T* q = qs + (int64_t)o * g.ho * g.wo;
   const int wx = xhi - xlo, cnt = (yhi - ylo) * wx;
-  int sum = 0;
+  T sum = 0;
   // eight loads in flight per round (clamped indices, values past cnt dropped)
   for (int i0 = threadIdx.x; i0 < cnt; i0 += 8 * blockDim.x) {
-    int v[8];
+    T v[8];
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
       const int i = min(i0 + u * (int)blockDim.x, cnt - 1);
@@ -381,8 +396,8 @@ __global__ __launch_bounds__(256) void conv_tapsum_kernel(ConvGeom g, const int3
     for (int u = 0; u < 8; ++u)
       if (i0 + u * (int)blockDim.x < cnt) sum += v[u];
   }
-  __shared__ int ssum[4];
-  sum = wave_sum4_i(sum);
+  __shared__ T ssum[4];
+  sum = wave_sum_t<T>(sum);
   if ((threadIdx.x & 63) == 0) ssum[threadIdx.x >> 6] = sum;
   __syncthreads();
   if (threadIdx.x == 0) {
@@ -423,6 +438,88 @@ __global__ __launch_bounds__(256) void conv_gradw_reduce_kernel(GemmParams p, Co
   const double zB = (double)p.zeroB[0] + (double)p.halfB * dB;
   const double v = dA * dB * (double)sum + dA * zB * (double)sumA_tap[row * taps + tap] +
                    zA * dB * (double)p.sumB[col] + (double)count_tap[tap] * zA * zB;
+  p.out[row * p.ldo + col] = (float)v;
+}
+
+// ---------------------------------------------------------------------------
+// K-blocked grad_W for a per-sample Q_b1 (Sec. 4.1's per-sample scales on the
+// weight-gradient product).  A sample's pixels form one K block, so the
+// contraction gives an exact int32 sum per (slot, o, (tap, c)); each is
+// scaled by its slot's 1 / s in float64.  With x1 = q dA_n + zA_n for the
+// gradient codes of slot n and x2 = q dB + zB on valid taps:
+//   grad_W[o][(tap, c)] = dB sum_n dA_n acc_n + zB sum_n dA_n SA_n[o][tap]
+//                       + dB sum_n zA_n SB_n[(tap, c)] + zB cnt[tap] sum_n zA_n
+// with SA_n, SB_n the code sums of slot n over the tap's valid pixels and
+// cnt[tap] their number per sample.
+// ---------------------------------------------------------------------------
+// zero codes in the pitch tails [n psp + ho wo, (n + 1) psp) of each row
+__global__ __launch_bounds__(256) void conv_pitch_zero_kernel(ConvGeom g, int8_t* bw, int64_t ldb) {
+  const int64_t howo = (int64_t)g.ho * g.wo, tail = g.psp - howo;
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= (int64_t)g.n * tail) return;
+  const int64_t slot = t / tail;
+  bw[(int64_t)blockIdx.y * ldb + slot * g.psp + howo + (t - slot * tail)] = 0;
+}
+
+// slot weights dA = 1 / s, zA = z + half / s (slot n holds sample perm[n])
+// and sum_n zA_n, one block
+__global__ __launch_bounds__(256) void conv_psq_weights_kernel(const float* scale, const float* zero,
+                                                               const int32_t* perm, int n, int half, ConvPsqSums ps) {
+  double zs = 0.0;
+  for (int i = threadIdx.x; i < n; i += blockDim.x) {
+    const int smp = perm ? perm[i] : i;
+    const double d = 1.0 / (double)scale[smp];
+    const double za = (double)zero[smp] + (double)half * d;
+    ps.dA[i] = d;
+    ps.zA[i] = za;
+    zs += za;
+  }
+  __shared__ double sw[4];
+  zs = wave_sum_t<double>(zs);
+  if ((threadIdx.x & 63) == 0) sw[threadIdx.x >> 6] = zs;
+  __syncthreads();
+  if (threadIdx.x == 0) ps.zsum[0] = (sw[0] + sw[1]) + (sw[2] + sw[3]);
+}
+
+// out[ch][pix] = sum over slots i of wt[i] codes[ch ld + i pitch + pix] (float64)
+__global__ void conv_wsum_kernel(const int8_t* codes, int64_t ld, int64_t pitch, int64_t npix, int64_t nch, int n,
+                                 const double* wt, double* out) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= nch * npix) return;
+  const int64_t ch = t / npix, pix = t - (t / npix) * npix;
+  const int8_t* col = codes + ch * ld + pix;
+  double s4[4] = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll 4
+  for (int i = 0; i < n; ++i) s4[i & 3] += wt[i] * (double)col[(int64_t)i * pitch];
+  out[t] = (s4[0] + s4[1]) + (s4[2] + s4[3]);
+}
+
+// the reduction over slots (split i = slot i), weighted by dA, plus the
+// zero-point terms; layout of the work as in conv_gradw_reduce_kernel
+__global__ __launch_bounds__(256) void conv_gradw_psq_reduce_kernel(GemmParams p, ConvGeom g, ConvPsqSums ps,
+                                                                    const int32_t* count_tap) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int64_t idx = (int64_t)blockIdx.x * 64 + lane;
+  const int64_t MN = p.M * p.N;
+  const int64_t ic = idx < MN ? idx : MN - 1;
+  double s8[8] = {0.0, 0.0, 0.0, 0.0, 0.0, 0.0, 0.0, 0.0};
+  int sp = wave;
+  for (; sp + 28 < p.splits; sp += 32)
+#pragma unroll
+    for (int u = 0; u < 8; ++u) s8[u] += ps.dA[sp + 4 * u] * (double)p.part[(int64_t)(sp + 4 * u) * MN + ic];
+  for (; sp < p.splits; sp += 4) s8[0] += ps.dA[sp] * (double)p.part[(int64_t)sp * MN + ic];
+  __shared__ double swave[4][64];
+  swave[wave][lane] = ((s8[0] + s8[1]) + (s8[2] + s8[3])) + ((s8[4] + s8[5]) + (s8[6] + s8[7]));
+  __syncthreads();
+  if (wave != 0 || idx >= MN) return;
+  const double sum = (swave[0][lane] + swave[1][lane]) + (swave[2][lane] + swave[3][lane]);
+  const int64_t row = idx / p.N, col = idx % p.N;
+  const int taps = g.kh * g.kw;
+  const int tap = (int)(col / g.c);
+  const double dB = 1.0 / (double)p.scaleB[0];
+  const double zB = (double)p.zeroB[0] + (double)p.halfB * dB;
+  const double cnt1 = (double)(count_tap[tap] / g.n);
+  const double v = dB * sum + zB * ps.WA[row * taps + tap] + dB * ps.WB[col] + zB * cnt1 * ps.zsum[0];
   p.out[row * p.ldo + col] = (float)v;
 }
 
@@ -820,7 +917,8 @@ hipError_t launch_conv_wq(const float* W, const ConvGeom& g, int bits, const flo
 hipError_t launch_conv_im2col_w(const ConvGeom& g, const int8_t* xq_t, int8_t* bw, int64_t ldb, int32_t* xs,
                                 int32_t* sumB, hipStream_t s) {
   const int64_t rows = (int64_t)g.kh * g.kw * g.c;
-  if (rows > 65535) return hipErrorInvalidValue;
+  if (rows > 65535 || g.psp < (int64_t)g.ho * g.wo || ldb < (int64_t)g.n * g.psp || (ldb & 15) != 0)
+    return hipErrorInvalidValue;
   if (conv_im2col_rows_ok(g, xq_t, bw, ldb)) {
     // stride 1, rows of 4-byte words: one thread per output word
     const int spb = 256 * IM2COL_WPT / (g.wo / 4);
@@ -828,14 +926,21 @@ hipError_t launch_conv_im2col_w(const ConvGeom& g, const int8_t* xq_t, int8_t* b
     if (blocks > 0x7FFFFFFF || (int64_t)g.n * g.ho + 256 * IM2COL_WPT > 0x7FFFFFFF) return hipErrorInvalidValue;
     hipLaunchKernelGGL(conv_im2col_rows_kernel, dim3((unsigned)blocks, (unsigned)rows), dim3(256), 0, s, g, xq_t, bw,
                        ldb, spb);
+    if (g.psp > (int64_t)g.ho * g.wo) {
+      const int64_t nt = (int64_t)g.n * (g.psp - (int64_t)g.ho * g.wo);
+      if ((nt + 255) / 256 > 0x7FFFFFFF) return hipErrorInvalidValue;
+      hipLaunchKernelGGL(conv_pitch_zero_kernel, dim3((unsigned)((nt + 255) / 256), (unsigned)rows), dim3(256), 0, s,
+                         g, bw, ldb);
+    }
   } else {
     const int64_t chunks = (ldb + 16 * 256 - 1) / (16 * 256);
     if (chunks > 0x7FFFFFFF) return hipErrorInvalidValue;
     hipLaunchKernelGGL(conv_im2col_w_kernel, dim3((unsigned)chunks, (unsigned)rows), dim3(256), 0, s, g, xq_t, bw, ldb);
   }
+  if (!xs) return hipGetLastError();  // per-sample Q_b1 forms its own sums
   const int64_t nx = (int64_t)g.c * g.h * g.w;
   hipLaunchKernelGGL(conv_xsum_kernel, dim3((unsigned)((nx + 255) / 256)), dim3(256), 0, s, g, xq_t, xs);
-  hipLaunchKernelGGL(conv_xtapsum_kernel, dim3((unsigned)rows), dim3(256), 0, s, g, xs, sumB);
+  hipLaunchKernelGGL(conv_xtapsum_kernel<int32_t>, dim3((unsigned)rows), dim3(256), 0, s, g, xs, sumB);
   return hipGetLastError();
 }
 
@@ -844,7 +949,7 @@ hipError_t launch_conv_tapsums(const ConvGeom& g, const int8_t* q1_t, int64_t ld
   const int64_t n1 = (int64_t)g.o * g.ho * g.wo;
   hipLaunchKernelGGL(conv_qsum_kernel, dim3((unsigned)((n1 + 255) / 256)), dim3(256), 0, s, g, q1_t, ldq, qs);
   const int64_t n2 = (int64_t)g.o * g.kh * g.kw;
-  hipLaunchKernelGGL(conv_tapsum_kernel, dim3((unsigned)n2), dim3(256), 0, s, g, qs, sumA_tap, count_tap);
+  hipLaunchKernelGGL(conv_tapsum_kernel<int32_t>, dim3((unsigned)n2), dim3(256), 0, s, g, qs, sumA_tap, count_tap);
   return hipGetLastError();
 }
 
@@ -853,6 +958,36 @@ hipError_t launch_conv_gradw_reduce(const GemmParams& p, const ConvGeom& g, cons
   const int64_t MN = p.M * p.N;
   if (MN < 1 || (MN + 63) / 64 > 0x7FFFFFFF) return hipErrorInvalidValue;
   hipLaunchKernelGGL(conv_gradw_reduce_kernel, dim3((unsigned)((MN + 63) / 64)), dim3(256), 0, s, p, g, sumA_tap,
+                     count_tap);
+  return hipGetLastError();
+}
+
+hipError_t launch_conv_psq_sums(const ConvGeom& g, const float* scale, const float* zero, const int32_t* perm,
+                                int half, const int8_t* q1_t, int64_t ldq, const int8_t* xq_t, const ConvPsqSums& ps,
+                                int32_t* count_tap, hipStream_t s) {
+  const int64_t howo = (int64_t)g.ho * g.wo, hw = (int64_t)g.h * g.w;
+  const int64_t taps = (int64_t)g.kh * g.kw;
+  const int64_t n1 = (int64_t)g.o * howo, n2 = (int64_t)g.c * hw;
+  if ((n1 + 255) / 256 > 0x7FFFFFFF || (n2 + 255) / 256 > 0x7FFFFFFF || g.o * taps > 0x7FFFFFFF ||
+      taps * g.c > 65535)
+    return hipErrorInvalidValue;
+  hipLaunchKernelGGL(conv_psq_weights_kernel, dim3(1), dim3(256), 0, s, scale, zero, perm, g.n, half, ps);
+  hipLaunchKernelGGL(conv_wsum_kernel, dim3((unsigned)((n1 + 255) / 256)), dim3(256), 0, s, q1_t, ldq, g.psp, howo,
+                     (int64_t)g.o, g.n, (const double*)ps.dA, ps.qw);
+  hipLaunchKernelGGL(conv_wsum_kernel, dim3((unsigned)((n2 + 255) / 256)), dim3(256), 0, s, xq_t, g.n * hw, hw, hw,
+                     (int64_t)g.c, g.n, (const double*)ps.zA, ps.xw);
+  hipLaunchKernelGGL(conv_tapsum_kernel<double>, dim3((unsigned)(g.o * taps)), dim3(256), 0, s, g,
+                     (const double*)ps.qw, ps.WA, count_tap);
+  hipLaunchKernelGGL(conv_xtapsum_kernel<double>, dim3((unsigned)(taps * g.c)), dim3(256), 0, s, g,
+                     (const double*)ps.xw, ps.WB);
+  return hipGetLastError();
+}
+
+hipError_t launch_conv_gradw_psq_reduce(const GemmParams& p, const ConvGeom& g, const ConvPsqSums& ps,
+                                        const int32_t* count_tap, hipStream_t s) {
+  const int64_t MN = p.M * p.N;
+  if (MN < 1 || (MN + 63) / 64 > 0x7FFFFFFF || p.splits != g.n) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(conv_gradw_psq_reduce_kernel, dim3((unsigned)((MN + 63) / 64)), dim3(256), 0, s, p, g, ps,
                      count_tap);
   return hipGetLastError();
 }

@@ -236,6 +236,8 @@ struct NarrowQParams {
   const float* zero;
   int8_t* q_t;
   int64_t ldt;
+  int64_t vblk;  // rows of each block of blk that exist in x (the rest are zero codes); 0: blk
+  int rowscale;  // scale / zero per block (indexed by the block's source block), else per tensor
 };
 hipError_t launch_quant_narrow_t(const NarrowQParams& p, hipStream_t s);
 
@@ -328,6 +330,8 @@ hipError_t launch_gemm_bf6(const Bf6Params& p, hipStream_t s);
 struct ConvGeom {
   int n, c, h, w, o, kh, kw, stride, pad, ho, wo;
   int64_t npad;  // slots per input pixel in the grad_X rows (multiple of 64)
+  int64_t psp;   // K pitch of a slot's output pixels in the grad_W operands (ho wo, or
+                 // ho wo rounded up to 128 with zero codes after them when Q_b1 is per sample)
 };
 hipError_t launch_conv_wq(const float* W, const ConvGeom& g, int bits, const float* scale, const float* zero,
                           int8_t* wq_t, int32_t* swq, hipStream_t s);
@@ -337,6 +341,19 @@ hipError_t launch_conv_tapsums(const ConvGeom& g, const int8_t* q1_t, int64_t ld
                                int32_t* count_tap, hipStream_t s);
 hipError_t launch_conv_gradw_reduce(const GemmParams& p, const ConvGeom& g, const int32_t* sumA_tap,
                                     const int32_t* count_tap, hipStream_t s);
+// per-sample Q_b1 (K-blocked grad_W): slot weights dA = 1 / s, zA = z + half / s
+// and their sum; float64 weighted code sums over slots and their tap
+// rectangles; the weighted reduction of the per-slot int32 contractions
+struct ConvPsqSums {
+  double *dA, *zA, *zsum;  // [n], [n], [1]
+  double *qw, *xw;         // [o][ho wo], [c][h w]
+  double *WA, *WB;         // [o][taps], [(tap, c)]
+};
+hipError_t launch_conv_psq_sums(const ConvGeom& g, const float* scale, const float* zero, const int32_t* perm,
+                                int half, const int8_t* q1_t, int64_t ldq, const int8_t* xq_t, const ConvPsqSums& ps,
+                                int32_t* count_tap, hipStream_t s);
+hipError_t launch_conv_gradw_psq_reduce(const GemmParams& p, const ConvGeom& g, const ConvPsqSums& ps,
+                                        const int32_t* count_tap, hipStream_t s);
 hipError_t launch_conv_gradx_prep(const ConvGeom& g, const int8_t* q2, const int32_t* swq, int32_t* sg, int32_t* ct,
                                   int32_t* cnt, hipStream_t s);
 hipError_t launch_conv_gradx(const GemmParams& p, int epi, const ConvGeom& g, const int8_t* q2, const int32_t* sg,

@@ -56,9 +56,14 @@ def test_workspace_queries_and_argument_errors():
     bad = fqt.cfg_struct(qb_x=("psq", 9, 0))
     rc = lib.fqt_linear_backward(fake, fake, fake, 4, 4, 4, ctypes.byref(bad), fake, fake, fake, 1 << 30, null)
     assert rc == 1
-    # grad_W quantizer other than PTQ is unsupported (per-row scales lie on its contraction axis)
+    # a per-sample grad_W quantizer on a linear layer: its per-row scales lie on
+    # the contraction axis, one sample per K step, so the layer takes the shift form
     unsup = fqt.cfg_struct(qb_w=("psq", 8, 0))
     rc = lib.fqt_linear_backward(fake, fake, fake, 4, 4, 4, ctypes.byref(unsup), fake, fake, fake, 1 << 30, null)
+    assert rc == 2
+    assert lib.fqt_linear_backward_workspace(4, 4, 4, ctypes.byref(unsup)) == 0
+    rc = lib.fqt_linear_backward(fake, fake, fake, 4, 4, 4, ctypes.byref(fqt.cfg_struct(qb_w=("bhq", 8, 4))),
+                                 fake, fake, fake, 1 << 30, null)
     assert rc == 2
     # App. D's adaptive groups (block size 0) score every number of groups: at most 65536 rows
     rc = lib.fqt_linear_backward(fake, fake, fake, 70000, 4, 4, ctypes.byref(fqt.cfg_struct(qb_x=("bhq", 5, 0))),
@@ -115,4 +120,14 @@ def test_workspace_queries_and_argument_errors():
     assert rc == 2
     rc = lib.fqt_conv_backward_im2col(fake, fake, fake, ctypes.byref(sh),
                                       ctypes.byref(fqt.cfg_struct(qb_w=("shift", 4, 0))), fake, fake, fake, 1 << 30, null)
+    assert rc == 2
+    # a per-sample grad_W quantizer on a conv: one K block of 128-byte stages
+    # per sample (8 x 8 outputs pad to 128), an int32 partial per sample
+    psq1 = fqt.cfg_struct(qb_w=("psq", 8, 0))
+    ws_psq = lib.fqt_conv_backward_workspace(ctypes.byref(sh), ctypes.byref(psq1))
+    assert ws_psq >= 2 * 16 * 9 * 4 * 4 + 16 * 2 * 128 + 9 * 4 * 2 * 128
+    # more output pixels than one int32-exact K block holds
+    big = fqt.conv_shape(1, 16, 260, 260, 16, 1, 1, 1, 0)
+    rc = lib.fqt_conv_backward_im2col(fake, fake, fake, ctypes.byref(big), ctypes.byref(psq1), fake, fake, fake,
+                                      1 << 40, null)
     assert rc == 2

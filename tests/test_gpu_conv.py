@@ -237,3 +237,93 @@ def test_conv_contractions_exact_on_the_grid(geom):
     assert f.fqt_workspace_status(ws) == 0
     np.testing.assert_array_equal(host(gW), refW.astype(np.float32))
     np.testing.assert_array_equal(host(gX), refX.astype(np.float32))
+
+
+def test_conv_contractions_exact_per_sample_scales():
+    # per-sample Q_b1 and Q_b2 on the grid with sample i scaled by 2^(i mod 3):
+    # each sample's step is 2^(i mod 3), so both quantizers stay exact while a
+    # per-tensor one would not, and every sample's int32 block and its scale
+    # must be right for grad_W to equal the exact sum
+    for geom in [(128, 64, 56, 64, 3, 1, 1), (150, 16, 9, 32, 3, 2, 1), (40, 3, 32, 64, 7, 2, 3),
+                 (24, 32, 14, 48, 1, 2, 0), (8, 16, 11, 16, 5, 1, 2)]:
+        n, c, h, o, k, stride, pad = geom
+        X, W, G = grid_conv_inputs(n + c + o, n, c, h, o, k, stride, pad)
+        G = G * (2.0 ** (np.arange(n) % 3)).reshape(n, 1, 1, 1).astype(np.float32)
+        refW, refX = exact_conv_grads(X, W, G, stride, pad)
+        assert np.abs(refW).max() < 2 ** 24 and np.abs(refX).max() < 2 ** 24
+        f = fqt()
+        gW, gX, ws = f.fqt_conv_backward_im2col(dev(X), dev(W), dev(G), stride, pad, qb_x=("psq", 8, 0),
+                                               qb_w=("psq", 8, 0), seed=2)
+        assert f.fqt_workspace_status(ws) == 0
+        np.testing.assert_array_equal(host(gW), refW.astype(np.float32), err_msg=str(geom))
+        np.testing.assert_array_equal(host(gX), refX.astype(np.float32), err_msg=str(geom))
+        # BHQ across samples puts the grad_W operands in slot order: the
+        # per-sample scales must follow the permutation
+        gW, _, ws = f.fqt_conv_backward_im2col(dev(X), dev(W), dev(G), stride, pad, qb_x=("bhq", 5, 4),
+                                              qb_w=("psq", 8, 0), seed=2)
+        assert f.fqt_workspace_status(ws) == 0
+        np.testing.assert_array_equal(host(gW), refW.astype(np.float32), err_msg=str(geom))
+
+
+# ---------------------------------------------------------------------------
+# Per-sample Q_b1: the weight-gradient contraction in one K block per sample
+# (the sample's output pixels, padded to whole 128-byte stages), an exact
+# int32 sum per block, then the sample's scale in float64.
+# ---------------------------------------------------------------------------
+def run_w(X, W, G, stride, pad, qb_x, qb_w, seed=0):
+    f = fqt()
+    gW, gX, ws = f.fqt_conv_backward_im2col(dev(X), dev(W), dev(G), stride, pad, qb_x=qb_x, qb_w=qb_w, seed=seed)
+    assert f.fqt_workspace_status(ws) == 0
+    return host(gW), host(gX)
+
+
+@pytest.mark.parametrize("shape", SHAPES)
+@pytest.mark.parametrize("qbs", [(("ptq", 8, 0), ("psq", 8, 0)), (("bhq", 5, 2), ("psq", 8, 0)),
+                                 (("psq", 5, 0), ("psq", 4, 0))], ids=["ptq8-psq8", "bhq5-psq8", "psq5-psq4"])
+def test_conv_per_sample_grad_w(shape, qbs):
+    n, c, h, o, k, st, pad = shape
+    qb_x, qb_w = qbs
+    X, W, G = synth.conv_layer(seed=sum(shape), n=n, c=c, h=h, w=h, o=o, k=k, stride=st, pad=pad, stem=(c == 3))
+    r = BW.conv_backward(X, W, G, st, pad, qb_x=qb_x, qb_w=qb_w, seed=4)
+    gW, gX = run_w(X, W, G, st, pad, qb_x, qb_w, seed=4)
+    assert rownorm_err(gW, r["grad_W64"]) <= REL_TOL
+    assert rownorm_err(gX, r["grad_X64"]) <= REL_TOL
+
+
+@pytest.mark.parametrize("geo", GEOMETRIES[:3])
+def test_conv_per_sample_grad_w_geometries(geo):
+    n, c, h, w, o, kh, kw, st, pad = geo
+    X, W, G = conv_inputs(sum(geo) + 1, n, c, h, w, o, kh, kw, st, pad)
+    r = BW.conv_backward(X, W, G, st, pad, qb_x=("bhq", 5, 2), qb_w=("psq", 8, 0), seed=6)
+    gW, gX = run_w(X, W, G, st, pad, ("bhq", 5, 2), ("psq", 8, 0), seed=6)
+    assert rownorm_err(gW, r["grad_W64"]) <= REL_TOL
+    assert rownorm_err(gX, r["grad_X64"]) <= REL_TOL
+
+
+def test_conv_per_sample_grad_w_ragged_groups():
+    # 130 samples in BHQ groups 64 + 64 + 2: 130 K blocks in slot order
+    X, W, G = synth.conv_layer(seed=8, n=130, c=16, h=5, w=5, o=16, k=3, stride=1, pad=1)
+    r = BW.conv_backward(X, W, G, 1, 1, qb_x=("bhq", 5, 64), qb_w=("psq", 8, 0), seed=1)
+    gW, gX = run_w(X, W, G, 1, 1, ("bhq", 5, 64), ("psq", 8, 0), seed=1)
+    assert rownorm_err(gW, r["grad_W64"]) <= REL_TOL
+    assert rownorm_err(gX, r["grad_X64"]) <= REL_TOL
+
+
+def test_conv_per_sample_grad_w_full_size_sampled():
+    """Batch 128, 64 -> 64, 3x3, 56 x 56 (3136 output pixels: 25 stages per
+    sample), BHQ-5 Q_b2 and per-sample 8-bit Q_b1: sampled grad_W rows."""
+    X, W, G = synth.conv_layer(seed=0, n=128, c=64, h=56, w=56, o=64, k=3, stride=1, pad=1)
+    gW, _ = run_w(X, W, G, 1, 1, ("bhq", 5, 64), ("psq", 8, 0), seed=0)
+    n, h, w, c = X.shape
+    o = W.shape[0]
+    Xr = Q.dequantize(Q.quantize_ptq(X.reshape(n, -1), 8, False)).reshape(n, h, w, c)
+    G1r = Q.dequantize(Q.quantize_psq(G.reshape(n, -1), 8, seed=0, stream=0)).reshape(n, h, w, o)
+    xpad = np.zeros((n, h + 2, w + 2, c))
+    xpad[:, 1:-1, 1:-1] = Xr
+    rng = np.random.default_rng(1)
+    for oo in rng.choice(o, 4, replace=False):
+        ref = np.zeros((3, 3, c))
+        for rr in range(3):
+            for ss in range(3):
+                ref[rr, ss] = np.einsum("nyx,nyxc->c", G1r[..., oo], xpad[:, rr: rr + h, ss: ss + w])
+        assert rownorm_err(gW[oo].reshape(1, -1), ref.reshape(1, -1)) <= REL_TOL

@@ -195,3 +195,24 @@ def test_conv_backward_unbiased_and_accumulators():
     e = BW.col2im(EG2 @ Wr, n, h, w, c, 3, 3, 1, 1, h, w)
     qat = BW.col2im(G.reshape(-1, o).astype(np.float64) @ Wr, n, h, w, c, 3, 3, 1, 1, h, w)
     assert np.abs(e - qat).max() <= 1e-5 * np.abs(qat).max()
+
+
+def test_conv_backward_per_sample_grad_w_unbiased():
+    # per-sample Q_b1 on the conv (one scale per sample, Sec. 4.1): Theorem 1
+    # through grad_W, whose expectation is the QAT weight gradient G^T im2col(X~)
+    rng = np.random.default_rng(6)
+    n, h, w, c, o = 5, 6, 6, 3, 2
+    X = np.maximum(rng.standard_normal((n, h, w, c)), 0).astype(np.float32)
+    W = rng.standard_normal((o, 3, 3, c)).astype(np.float32)
+    G = (rng.lognormal(0, 2, (n, 1, 1, 1)) * rng.standard_normal((n, 3, 3, o))).astype(np.float32)
+    r = BW.conv_backward(X, W, G, 2, 1, qb_x=("ptq", 8, 0), qb_w=("psq", 8, 0))
+    assert r["qb1"]["scale"].shape == (n,)
+    cols = BW.im2col(Q.dequantize(r["qx"]).reshape(n, h, w, c), 3, 3, 2, 1, 3, 3)
+    EG1 = theory.exact_mean(G.reshape(n, -1), r["qb1"]).reshape(-1, o)
+    qat = G.reshape(-1, o).astype(np.float64).T @ cols
+    assert np.abs(EG1.T @ cols - qat).max() <= 1e-5 * np.abs(qat).max()
+    # each sample's rows dequantize on their own grid: step 1 / s_i from its range
+    G1r = Q.dequantize(r["qb1"]).reshape(n, -1)
+    for i in range(n):
+        R = float(G[i].max()) - float(G[i].min())
+        assert np.abs(G1r[i] - G[i].reshape(-1)).max() <= R / 255 * (1 + 1e-6)
