@@ -719,15 +719,22 @@ __device__ __forceinline__ void quant_tile(const QuantParams& p, int64_t bx, int
   __shared__ float s_v0[4][QT_COLS];     // v of a group's first slot (BHQ, K >= 16)
   __shared__ int s_csum[2][4][QT_COLS];  // per-wave column code sums (transposed outputs)
 
+  // source row of each of the wave's 16 slots, lane l holding slot l: one
+  // load, so that the 16 row loads below issue back to back
+  int32_t lrow = 0;
+  {
+    const int64_t sl = slot0 + (lane & 15);
+    if (sl < rows) lrow = p.perm ? p.perm[sl] : (int32_t)sl;
+  }
+  auto src_row = [&](int r) { return __builtin_amdgcn_readlane(lrow, r); };
+
   // ---- load 16 rows x 4 columns
   float g[QT_ROWS_PER_WAVE][4];
-  int32_t srow[QT_ROWS_PER_WAVE];
 #pragma unroll
   for (int r = 0; r < QT_ROWS_PER_WAVE; ++r) {
     const int64_t slot = slot0 + r;
     const bool ok = slot < rows;
-    const int32_t row = ok ? (p.perm ? p.perm[slot] : (int32_t)slot) : 0;
-    srow[r] = row;
+    const int32_t row = src_row(r);
     const float* xr = p.x + (int64_t)row * cols;
     if constexpr (VEC) {
       if (ok && lane_ok) {
@@ -746,6 +753,19 @@ __device__ __forceinline__ void quant_tile(const QuantParams& p, int64_t bx, int
     }
   }
 
+  // per-slot scale and zero of the wave's 16 rows, lane l holding row l:
+  // loaded with the tile, so that the row loop reads them from registers
+  // instead of loads that would queue behind its code stores
+  float lscale = 1.0f, lzero = 0.0f;
+  if constexpr (MODE == QM_ROW || (MODE == QM_BHQ && K != 0)) {
+    const int64_t sl = slot0 + (lane & 15);
+    if (sl < rows) {
+      lscale = p.scale[sl];
+      lzero = p.zero[sl];
+    }
+  }
+  auto row_scale = [&](int r) { return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, lscale), r)); };
+  auto row_zero = [&](int r) { return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, lzero), r)); };
   // ---- block Householder (K >= 16): a group spans K / 16 waves.  Its column
   // sum adds the slots one at a time in slot order, so the running sum is
   // handed from wave to wave through LDS: in step i the i-th wave of every
@@ -767,7 +787,7 @@ __device__ __forceinline__ void quant_tile(const QuantParams& p, int64_t bx, int
           const int64_t slot = slot0 + r;
           const bool ok = slot < rows;
           const bool multi = ok && bhq_slot_kind(L, slot) != 0;
-          const float d = ok ? p.scale[slot] : 1.0f;
+          const float d = row_scale(r);
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
             const float v = d * g[r][j];
@@ -835,8 +855,8 @@ __device__ __forceinline__ void quant_tile(const QuantParams& p, int64_t bx, int
 #pragma unroll
       for (int j = 0; j < 4; ++j) y[j] = s_t * (g[r][j] - z_t);
     } else if constexpr (MODE == QM_ROW) {
-      const float s = ok ? p.scale[slot] : 1.0f;
-      const float z = ok ? p.zero[slot] : 0.0f;
+      const float s = row_scale(r);
+      const float z = row_zero(r);
 #pragma unroll
       for (int j = 0; j < 4; ++j) y[j] = s * (g[r][j] - z);
     } else if constexpr (K == 0) {
@@ -874,8 +894,8 @@ __device__ __forceinline__ void quant_tile(const QuantParams& p, int64_t bx, int
     } else {
       const BhqLayout& L = p.L;
       const int kind = ok ? bhq_slot_kind(L, slot) : 0;
-      const float d = ok ? p.scale[slot] : 1.0f;
-      const float c = ok ? p.zero[slot] : 0.0f;
+      const float d = row_scale(r);
+      const float c = row_zero(r);
       if constexpr (K > 1 && K < 16) {
         // groups of K rows inside this wave: their sums from the registers
         if (r % K == 0) {
@@ -889,7 +909,7 @@ __device__ __forceinline__ void quant_tile(const QuantParams& p, int64_t bx, int
             const int64_t sl = slot + rr;
             const bool okr = sl < rows;
             const bool multi = okr && bhq_slot_kind(L, sl) != 0;
-            const float dr = okr ? p.scale[sl] : 1.0f;
+            const float dr = row_scale(r + rr);
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
               const float v = dr * g[r + rr][j];
@@ -918,7 +938,7 @@ __device__ __forceinline__ void quant_tile(const QuantParams& p, int64_t bx, int
         }
       }
     }
-    const uint64_t e0 = (uint64_t)srow[r] * (uint64_t)cols + (uint64_t)c0;
+    const uint64_t e0 = (uint64_t)(uint32_t)src_row(r) * (uint64_t)cols + (uint64_t)c0;
     if constexpr (SD) {
       // seed batch: the same transformed values rounded under keys seed + b,
       // b < nseeds; per element the sum of the codes and of their squares
@@ -961,9 +981,10 @@ __device__ __forceinline__ void quant_tile(const QuantParams& p, int64_t bx, int
       int sh2 = 0;
       if constexpr (H2 == 2) {
         if (ok) {
-          s2r = p.scale2[srow[r]];
-          z2r = p.zero2[srow[r]];
-          sh2 = p.shift2[srow[r]];
+          const int32_t sr = src_row(r);
+          s2r = p.scale2[sr];
+          z2r = p.zero2[sr];
+          sh2 = p.shift2[sr];
         }
       }
       float y2[4];
