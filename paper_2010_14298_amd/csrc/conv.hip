@@ -38,7 +38,7 @@ __device__ __forceinline__ int wave_sum4_i(int v) { return wave_sum_t<int>(v); }
 // block (a per-sample quantizer).  A block covers 4 * LPR columns (grid.y
 // walks wider rows in chunks of 256).
 // ---------------------------------------------------------------------------
-template <int LPR>
+template <int LPR, bool TWO, bool VEC>
 __global__ __launch_bounds__(256) void quant_narrow_t_kernel(NarrowQParams p) {
   constexpr int RG = 64 / LPR;  // row groups of 16 per wave
   const int lane = threadIdx.x & 63;
@@ -50,60 +50,115 @@ __global__ __launch_bounds__(256) void quant_narrow_t_kernel(NarrowQParams p) {
   const int half = 1 << (p.bits - 1);
   const float s0 = p.scale[0], z0 = p.zero[0];
   const int64_t vblk = p.vblk > 0 ? p.vblk : p.blk;
-  const bool vec = (p.cols & 3) == 0;
+  // VEC: cols % 4 == 0, so a lane's four columns are all inside or all past the end
+  const bool full = VEC && c0 < p.cols;
+  // Rows r0 .. r0 + 15: row (bq, br) reads row br of source block perm[bq]
+  // (or bq) of vblk rows.  TWO (blk >= 16): the 16 rows lie in blocks bq0
+  // and bq0 + 1, whose source blocks and scales are read once up front.
+  const int64_t bq0 = r0 / p.blk, br0 = r0 - bq0 * p.blk;
+  int64_t sbA = 0, sbB = 0;
+  float sA = s0, zA = z0, sB = s0, zB = z0;
+  if constexpr (TWO) {
+    const int64_t nblk = (p.rows + p.blk - 1) / p.blk;
+    const int64_t qa = bq0 < nblk ? bq0 : nblk - 1, qb = bq0 + 1 < nblk ? bq0 + 1 : nblk - 1;
+    sbA = p.perm ? (int64_t)p.perm[qa] : qa;
+    sbB = p.perm ? (int64_t)p.perm[qb] : qb;
+    if (p.rowscale) {
+      sA = p.scale[sbA];
+      zA = p.zero[sbA];
+      sB = p.scale[sbB];
+      zB = p.zero[sbB];
+    }
+  }
+  // source row, scale and zero of row r (row r of the 16 has offset br0 + r)
+  auto locate = [&](int r, int64_t& src, float& s, float& z) -> bool {
+    int64_t bq = bq0, br = br0 + r;
+    if (br >= p.blk) {  // at most one block boundary for TWO; stepped for small blocks
+      const int64_t d = br / p.blk;
+      bq += d;
+      br -= d * p.blk;
+    }
+    const bool ok = r0 + r < p.rows && br < vblk;
+    int64_t sb;
+    if constexpr (TWO) {
+      const bool inb = bq != bq0;
+      sb = inb ? sbB : sbA;
+      s = inb ? sB : sA;
+      z = inb ? zB : zA;
+    } else {
+      sb = ok ? (p.perm ? (int64_t)p.perm[bq] : bq) : 0;
+      s = (p.rowscale && ok) ? p.scale[sb] : s0;
+      z = (p.rowscale && ok) ? p.zero[sb] : z0;
+    }
+    src = sb * vblk + br;
+    return ok;
+  };
+  // ---- phase 1: the 16 rows' loads, issued together (clamped addresses and
+  // selects instead of branches around the loads).  Kept for phase 2: the
+  // source row (32 bits; -1 past the end) and, for TWO, a bit per row in
+  // block bq0 + 1.
+  float g[16][4];
+  int32_t src32[16];
+  uint32_t inb_mask = 0u;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    int64_t src;
+    float s, z;
+    const bool ok = locate(r, src, s, z);
+    src32[r] = ok ? (int32_t)src : -1;
+    if (TWO && br0 + r >= p.blk) inb_mask |= 1u << r;
+    if constexpr (VEC) {
+      const bool in = ok && full;
+      const float4 v = *reinterpret_cast<const float4*>(p.x + (in ? src * p.cols + c0 : 0));
+      g[r][0] = in ? v.x : 0.0f;
+      g[r][1] = in ? v.y : 0.0f;
+      g[r][2] = in ? v.z : 0.0f;
+      g[r][3] = in ? v.w : 0.0f;
+    } else {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) g[r][j] = (ok && c0 + j < p.cols) ? p.x[src * p.cols + c0 + j] : 0.0f;
+    }
+  }
+  // ---- phase 2: codes, transposed into words of four rows
   uint32_t tcodes[4][4];
 #pragma unroll
   for (int j = 0; j < 4; ++j)
 #pragma unroll
     for (int w = 0; w < 4; ++w) tcodes[j][w] = 0u;
-  // rows r0 .. r0 + 15: block index and offset of r0 once, then stepped.
-  // Row (bq, br) reads row br of source block perm[bq] (or bq) of vblk rows.
-  int64_t bq = r0 / p.blk;
-  int64_t br = r0 - bq * p.blk;
 #pragma unroll
   for (int r = 0; r < 16; ++r) {
-    const int64_t row = r0 + r;
-    const bool ok = row < p.rows && br < vblk;
-    const int64_t sb = ok ? (p.perm ? (int64_t)p.perm[bq] : bq) : 0;
-    const int64_t src = sb * vblk + br;
-    const float s = (p.rowscale && ok) ? p.scale[sb] : s0;
-    const float z = (p.rowscale && ok) ? p.zero[sb] : z0;
-    if (++br == p.blk) {
-      br = 0;
-      ++bq;
-    }
-    const float* xr = p.x + src * p.cols;
-    float g[4];
-    if (ok && vec && c0 + 3 < p.cols) {
-      const float4 v = *reinterpret_cast<const float4*>(xr + c0);
-      g[0] = v.x;
-      g[1] = v.y;
-      g[2] = v.z;
-      g[3] = v.w;
+    int64_t src;
+    float s, z;
+    bool ok;
+    if constexpr (TWO) {
+      ok = src32[r] >= 0;
+      src = ok ? src32[r] : 0;
+      const bool inb = (inb_mask >> r) & 1u;
+      s = inb ? sB : sA;
+      z = inb ? zB : zA;
     } else {
-#pragma unroll
-      for (int j = 0; j < 4; ++j) g[j] = (ok && c0 + j < p.cols) ? xr[c0 + j] : 0.0f;
+      ok = locate(r, src, s, z);
     }
     int code[4];
     const uint64_t ebase = (uint64_t)src * (uint64_t)p.cols + (uint64_t)c0;
     if (p.stoch) {
-      if (vec) {
+      if constexpr (VEC) {
         const u32x4 o = philox_block(ebase, p.seed, p.stream);
-        code[0] = sr_code(s * (g[0] - z), o.x, B);
-        code[1] = sr_code(s * (g[1] - z), o.y, B);
-        code[2] = sr_code(s * (g[2] - z), o.z, B);
-        code[3] = sr_code(s * (g[3] - z), o.w, B);
+        code[0] = sr_code(s * (g[r][0] - z), o.x, B);
+        code[1] = sr_code(s * (g[r][1] - z), o.y, B);
+        code[2] = sr_code(s * (g[r][2] - z), o.z, B);
+        code[3] = sr_code(s * (g[r][3] - z), o.w, B);
       } else {
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           const uint64_t e = ebase + j;
           const u32x4 o = philox_block(e, p.seed, p.stream);
-          code[j] = sr_code(s * (g[j] - z), philox_word(o, (int)(e & 3)), B);
+          code[j] = sr_code(s * (g[r][j] - z), philox_word(o, (int)(e & 3)), B);
         }
       }
     } else {
 #pragma unroll
-      for (int j = 0; j < 4; ++j) code[j] = rne_code(s * (g[j] - z), B);
+      for (int j = 0; j < 4; ++j) code[j] = rne_code(s * (g[r][j] - z), B);
     }
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
@@ -127,6 +182,20 @@ __global__ __launch_bounds__(256) void quant_narrow_t_kernel(NarrowQParams p) {
   }
 }
 
+template <bool TWO, bool VEC>
+static hipError_t launch_narrow_lpr(const NarrowQParams& p, int lpr, dim3 grid, hipStream_t s) {
+  switch (lpr) {
+    case 1: hipLaunchKernelGGL((quant_narrow_t_kernel<1, TWO, VEC>), grid, dim3(256), 0, s, p); break;
+    case 2: hipLaunchKernelGGL((quant_narrow_t_kernel<2, TWO, VEC>), grid, dim3(256), 0, s, p); break;
+    case 4: hipLaunchKernelGGL((quant_narrow_t_kernel<4, TWO, VEC>), grid, dim3(256), 0, s, p); break;
+    case 8: hipLaunchKernelGGL((quant_narrow_t_kernel<8, TWO, VEC>), grid, dim3(256), 0, s, p); break;
+    case 16: hipLaunchKernelGGL((quant_narrow_t_kernel<16, TWO, VEC>), grid, dim3(256), 0, s, p); break;
+    case 32: hipLaunchKernelGGL((quant_narrow_t_kernel<32, TWO, VEC>), grid, dim3(256), 0, s, p); break;
+    default: hipLaunchKernelGGL((quant_narrow_t_kernel<64, TWO, VEC>), grid, dim3(256), 0, s, p); break;
+  }
+  return hipGetLastError();
+}
+
 hipError_t launch_quant_narrow_t(const NarrowQParams& p, hipStream_t s) {
   if (p.blk < 1 || p.vblk < 0 || p.vblk > p.blk) return hipErrorInvalidValue;
   // lanes per row: the smallest power of two covering cols / 4, at most 64
@@ -139,16 +208,9 @@ hipError_t launch_quant_narrow_t(const NarrowQParams& p, hipStream_t s) {
   const int64_t blocks = (p.ldt + rows_per_block - 1) / rows_per_block;
   if (blocks > 0x7FFFFFFF || chunks > 65535) return hipErrorInvalidValue;
   const dim3 grid((unsigned)blocks, (unsigned)chunks);
-  switch (lpr) {
-    case 1: hipLaunchKernelGGL(quant_narrow_t_kernel<1>, grid, dim3(256), 0, s, p); break;
-    case 2: hipLaunchKernelGGL(quant_narrow_t_kernel<2>, grid, dim3(256), 0, s, p); break;
-    case 4: hipLaunchKernelGGL(quant_narrow_t_kernel<4>, grid, dim3(256), 0, s, p); break;
-    case 8: hipLaunchKernelGGL(quant_narrow_t_kernel<8>, grid, dim3(256), 0, s, p); break;
-    case 16: hipLaunchKernelGGL(quant_narrow_t_kernel<16>, grid, dim3(256), 0, s, p); break;
-    case 32: hipLaunchKernelGGL(quant_narrow_t_kernel<32>, grid, dim3(256), 0, s, p); break;
-    default: hipLaunchKernelGGL(quant_narrow_t_kernel<64>, grid, dim3(256), 0, s, p); break;
-  }
-  return hipGetLastError();
+  const bool two = p.blk >= 16, vec = (p.cols & 3) == 0;
+  if (vec) return two ? launch_narrow_lpr<true, true>(p, lpr, grid, s) : launch_narrow_lpr<false, true>(p, lpr, grid, s);
+  return two ? launch_narrow_lpr<true, false>(p, lpr, grid, s) : launch_narrow_lpr<false, false>(p, lpr, grid, s);
 }
 
 // ---------------------------------------------------------------------------
