@@ -404,16 +404,35 @@ fqt_status check_conv_shape(const fqt_conv_shape& sh) {
 }
 
 ConvGeom conv_geom(const fqt_conv_shape& sh) {
-  ConvGeom g{sh.n, sh.c, sh.h, sh.w, sh.o, sh.kh, sh.kw, sh.stride, sh.pad, sh.ho, sh.wo, 0, 0};
+  ConvGeom g{sh.n, sh.c, sh.h, sh.w, sh.o, sh.kh, sh.kw, sh.stride, sh.pad, sh.ho, sh.wo, 0, 0, 0, 0, 0};
   g.npad = ((int64_t)sh.n + 63) / 64 * 64;
   g.psp = (int64_t)sh.ho * sh.wo;
   return g;
 }
 
-// per-sample Q_b1: each slot's output pixels start a 128-byte K stage
+// The grad_W layout.  Stride 1: the implicit form on the zero-halo grid
+// (rows of gwp = w + 2 pad rounded up to 16 bytes) when a slot's grid pitch
+// is at most 1.5 times its output pixels (rounded up to 128 for a per-sample
+// Q_b1), else the explicit im2col.  Per-sample Q_b1: each slot's pixels start
+// a 128-byte K stage.
 ConvGeom conv_geom(const fqt_conv_shape& sh, const fqt_bwd_cfg& cfg) {
   ConvGeom g = conv_geom(sh);
-  if (cfg.qb_w.kind == FQT_PSQ) g.psp = (g.psp + 127) / 128 * 128;
+  const bool psq1 = cfg.qb_w.kind == FQT_PSQ;
+  const int64_t howo = g.psp;
+  const int64_t compact = psq1 ? (howo + 127) / 128 * 128 : howo;
+  if (sh.stride == 1) {
+    const int64_t gwp = ((int64_t)sh.w + 2 * sh.pad + 15) / 16 * 16, ghp = (int64_t)sh.h + 2 * sh.pad;
+    const int64_t gsp = (ghp * gwp + 127) / 128 * 128;
+    if (2 * gsp <= 3 * compact && gwp <= 4096 && (!psq1 || gsp <= MAX_K_CHUNK)) {
+      g.gwp = gwp;
+      g.ghp = ghp;
+      g.psp = gsp;
+      // copies reach r gwp <= (kh - 1) gwp past the last slot's K range
+      g.ldx = ((int64_t)sh.n * gsp + (sh.kh - 1) * gwp + 127) / 128 * 128;
+      return g;
+    }
+  }
+  g.psp = compact;
   return g;
 }
 
@@ -450,12 +469,13 @@ ConvWs carve_conv(Carver& c, const float* X, const float* W, const float* G, con
   w.rmax = c.take<float>(N);
   stats_direct_rows(w.sg_seg, w.rmin, w.rmax);
   const bool psq1 = cfg.qb_w.kind == FQT_PSQ;
-  w.ldq = psq1 ? N * g.psp : (P + 127) / 128 * 128;
+  w.ldq = (psq1 || g.gwp > 0) ? N * g.psp : (P + 127) / 128 * 128;
   w.xq_t = c.take<int8_t>((int64_t)g.c * N * hw);
   w.wq_t = c.take<int8_t>((int64_t)g.c * taps * g.o);
   w.q2 = c.take<int8_t>(N * howo * g.o);
   w.q1_t = c.take<int8_t>((int64_t)g.o * w.ldq);
-  w.bw = c.take<int8_t>(taps * g.c * w.ldq);
+  // explicit im2col [(tap, c)][ldq], or the kw shifted activation grids [s][c][ldx]
+  w.bw = c.take<int8_t>(g.gwp > 0 ? (int64_t)g.kw * g.c * g.ldx : taps * g.c * w.ldq);
   w.swq = c.take<int32_t>(taps * g.c);
   w.sumB = c.take<int32_t>(taps * g.c);
   w.xs = c.take<int32_t>((int64_t)g.c * g.h * g.w);
@@ -492,17 +512,27 @@ ConvWs carve_conv(Carver& c, const float* X, const float* W, const float* G, con
     w.part = c.take<int32_t>(N * g.o * taps * g.c);
     return w;
   }
-  // grad_W: split the pixel contraction so that about 512 blocks run, each
-  // K chunk a whole number of 128-byte stages and at most 65536
-  const int64_t tiles = ((g.o + 127) / 128) * ((taps * g.c + 127) / 128);
-  int64_t want = (512 + tiles - 1) / tiles;
+  // grad_W: split the pixel contraction so that at most 512 blocks run (two
+  // full rounds of one block per CU), in a multiple of the XCD count of
+  // splits when there are that many, each K chunk a whole number of 128-byte
+  // stages and at most 65536
+  const int64_t tiles = (g.o <= 64 ? 1 : (g.o + 127) / 128) * ((taps * g.c + 127) / 128);
+  int64_t want = 512 / tiles;
+  if (want >= NUM_XCD) want = want / NUM_XCD * NUM_XCD;
   const int64_t stages = w.ldq / 128;
   if (want > stages) want = stages;
   if (want < 1) want = 1;
   int64_t kchunk = (stages + want - 1) / want * 128;
   if (kchunk > 65536) kchunk = 65536;
+  int64_t splits = (w.ldq + kchunk - 1) / kchunk;
+  if (splits >= NUM_XCD && splits % NUM_XCD != 0) {
+    // a multiple of the XCD count, so that the contraction keeps each
+    // split's tiles on one XCD (trailing splits may be empty: zero partials)
+    splits = (splits + NUM_XCD - 1) / NUM_XCD * NUM_XCD;
+    kchunk = (stages + splits - 1) / splits * 128;
+  }
   w.kchunk = kchunk;
-  w.splits = (int)((w.ldq + kchunk - 1) / kchunk);
+  w.splits = (int)splits;
   w.part = c.take<int32_t>((int64_t)w.splits * g.o * taps * g.c);
   return w;
 }
@@ -1177,6 +1207,11 @@ fqt_status fqt_conv_backward_im2col(const float* X, const float* W, const float*
   n1.blk = g.psp;
   n1.vblk = howo;
   n1.rowscale = psq1 ? 1 : 0;
+  if (g.gwp > 0) {  // output pixel (y, x) at y gwp + x of its slot's grid
+    n1.gw = g.gwp;
+    n1.gwo = g.wo;
+    n1.gho = g.ho;
+  }
   n1.bits = cfg->qb_w.bits;
   n1.stoch = 1;
   n1.seed = cfg->seed;
@@ -1190,7 +1225,7 @@ fqt_status fqt_conv_backward_im2col(const float* X, const float* W, const float*
 
   // grad_W [o][(r, s, c)] = Q_b1(G)^T im2col(Q_f(X)), split over output pixels
   tr.begin(6);
-  FQT_TRY(launch_conv_im2col_w(g, w.xq_t, w.bw, w.ldq, psq1 ? nullptr : w.xs, w.sumB, s));
+  FQT_TRY(launch_conv_im2col_w(g, w.xq_t, w.bw, g.gwp > 0 ? g.ldx : w.ldq, psq1 ? nullptr : w.xs, w.sumB, s));
   if (psq1)
     FQT_TRY(launch_conv_psq_sums(g, w.sg1, w.zg1, w.perm, 1 << (cfg->qb_w.bits - 1), w.q1_t, w.ldq, w.xq_t, w.ps,
                                  w.count_tap, s));
@@ -1204,6 +1239,12 @@ fqt_status fqt_conv_backward_im2col(const float* X, const float* W, const float*
   gw.K = w.ldq;
   gw.lda = w.ldq;
   gw.ldb = w.ldq;
+  if (g.gwp > 0) {  // tap (r, s), channel c: copy s at K offset r gwp
+    gw.ldb = g.ldx;
+    gw.bmap_c = g.c;
+    gw.bmap_kw = g.kw;
+    gw.bmap_wp = g.gwp;
+  }
   gw.splits = w.splits;
   gw.kchunk = w.kchunk;
   gw.part = w.part;

@@ -70,15 +70,35 @@ __global__ __launch_bounds__(256) void quant_narrow_t_kernel(NarrowQParams p) {
       zB = p.zero[sbB];
     }
   }
+  // 2-D blocks: (y, x) of offset br0 once; the 16 rows then step x (gw >= 16
+  // and blocks of at least 128 rows: at most one row wrap, at most one block
+  // boundary, after which (y, x) = (0, br))
+  const int64_t gy0 = p.gw > 0 ? br0 / p.gw : 0, gx0 = p.gw > 0 ? br0 - gy0 * p.gw : 0;
+  const int64_t vb = p.gw > 0 ? p.gho * p.gwo : vblk;  // source rows per block
   // source row, scale and zero of row r (row r of the 16 has offset br0 + r)
   auto locate = [&](int r, int64_t& src, float& s, float& z) -> bool {
     int64_t bq = bq0, br = br0 + r;
-    if (br >= p.blk) {  // at most one block boundary for TWO; stepped for small blocks
+    const bool wrapped = br >= p.blk;
+    if (wrapped) {  // at most one block boundary for TWO; stepped for small blocks
       const int64_t d = br / p.blk;
       bq += d;
       br -= d * p.blk;
     }
-    const bool ok = r0 + r < p.rows && br < vblk;
+    bool inside;
+    int64_t srow;
+    if (p.gw > 0) {
+      int64_t y = wrapped ? 0 : gy0, x = wrapped ? br : gx0 + r;
+      if (x >= p.gw) {
+        x -= p.gw;
+        ++y;
+      }
+      inside = y < p.gho && x < p.gwo;
+      srow = y * p.gwo + x;
+    } else {
+      inside = br < vblk;
+      srow = br;
+    }
+    const bool ok = r0 + r < p.rows && inside;
     int64_t sb;
     if constexpr (TWO) {
       const bool inb = bq != bq0;
@@ -90,7 +110,7 @@ __global__ __launch_bounds__(256) void quant_narrow_t_kernel(NarrowQParams p) {
       s = (p.rowscale && ok) ? p.scale[sb] : s0;
       z = (p.rowscale && ok) ? p.zero[sb] : z0;
     }
-    src = sb * vblk + br;
+    src = sb * vb + srow;
     return ok;
   };
   // ---- phase 1: the 16 rows' loads, issued together (clamped addresses and
@@ -198,6 +218,7 @@ static hipError_t launch_narrow_lpr(const NarrowQParams& p, int lpr, dim3 grid, 
 
 hipError_t launch_quant_narrow_t(const NarrowQParams& p, hipStream_t s) {
   if (p.blk < 1 || p.vblk < 0 || p.vblk > p.blk) return hipErrorInvalidValue;
+  if (p.gw > 0 && (p.gw < 16 || p.blk < 128 || p.gwo > p.gw || p.gho * p.gw > p.blk)) return hipErrorInvalidValue;
   // lanes per row: the smallest power of two covering cols / 4, at most 64
   // (wider rows: column chunks of 256 along grid.y)
   const int64_t need = (p.cols + 3) / 4;
@@ -362,6 +383,62 @@ __global__ __launch_bounds__(256) void conv_im2col_rows_kernel(ConvGeom g, const
   }
 }
 
+// The kw shifted copies of the zero-halo activation grid (the implicit
+// grad_W form), one thread per 16-byte chunk j of grid row y' of one
+// (channel, slot): byte x' of copy s holds input pixel (y' - pad, x' + s -
+// pad), zero outside the image.  The thread loads the input words under
+// the chunk plus the kw - 1 bytes after it once (word-aligned rows: w % 4
+// == 0) and stores each copy's chunk as a byte funnel shift of them.
+constexpr int XGRID_MAXKW = 8;
+__global__ __launch_bounds__(256) void conv_xgrid_kernel(ConvGeom g, const int8_t* xq_t, int8_t* grid) {
+  constexpr int NWD = (16 + XGRID_MAXKW - 1 + 3) / 4 + 1;  // input words a chunk can need
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int cpr = (int)(g.gwp >> 4);  // chunks per grid row
+  const int64_t rows_per_c = (int64_t)g.n * g.ghp;
+  if (t >= (int64_t)g.c * rows_per_c * cpr) return;
+  const int j = (int)(t % cpr);
+  const int64_t rr = t / cpr;  // (c, slot, y')
+  const int yp = (int)(rr % g.ghp);
+  const int64_t cs = rr / g.ghp;
+  const int slot = (int)(cs % g.n);
+  const int c = (int)(cs / g.n);
+  const int iy = yp - g.pad;
+  const int iw = g.w >> 2;
+  // input bytes from x0 = 16 j - pad on: words w0 .. w0 + NWD - 1 with w0 = floor(x0 / 4)
+  const int x0 = 16 * j - g.pad;
+  const int w0 = x0 >= 0 ? x0 >> 2 : -((-x0 + 3) >> 2);
+  const int sh0 = x0 - 4 * w0;  // 0..3
+  uint32_t wd[NWD];
+  const bool rowin = iy >= 0 && iy < g.h;
+  const uint32_t* src = reinterpret_cast<const uint32_t*>(xq_t + ((int64_t)c * g.n + slot) * g.h * g.w +
+                                                          (int64_t)(rowin ? iy : 0) * g.w);
+#pragma unroll
+  for (int k = 0; k < NWD; ++k) {
+    const int wi = w0 + k;
+    wd[k] = (rowin && wi >= 0 && wi < iw) ? src[wi] : 0u;
+  }
+  int8_t* dst0 = grid + (int64_t)c * g.ldx + (int64_t)slot * g.psp + (int64_t)yp * g.gwp + 16 * j;
+#pragma unroll
+  for (int s = 0; s < XGRID_MAXKW; ++s) {
+    if (s >= g.kw) break;
+    // bytes x0 + s .. x0 + s + 15: word offset (sh0 + s) / 4, byte shift (sh0 + s) % 4
+    const int b = sh0 + s, q = b >> 2, sh = b & 3;
+    uint32_t o[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      uint32_t lo = 0u, hi = 0u;
+#pragma unroll
+      for (int k = 0; k + 1 < NWD; ++k)
+        if (k == q + u) {
+          lo = wd[k];
+          hi = wd[k + 1];
+        }
+      o[u] = sh == 0 ? lo : (uint32_t)((((uint64_t)hi << 32) | lo) >> (8 * sh));
+    }
+    *reinterpret_cast<uint4*>(dst0 + (int64_t)s * g.c * g.ldx) = make_uint4(o[0], o[1], o[2], o[3]);
+  }
+}
+
 __device__ __forceinline__ void tap_range(int r, int stride, int pad, int h, int ho, int& lo, int& hi) {
   lo = 0;
   while (lo < ho && lo * stride - pad + r < 0) ++lo;
@@ -425,10 +502,12 @@ __global__ void conv_qsum_kernel(ConvGeom g, const int8_t* q1_t, int64_t ldq, in
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (t >= (int64_t)g.o * howo) return;
   const int64_t o = t / howo, pix = t % howo;
-  const int8_t* row = q1_t + o * ldq + pix;
+  // slot n's codes start at n psp; grid rows of gwp in the implicit form
+  const int64_t off = g.gwp > 0 ? (pix / g.wo) * g.gwp + pix % g.wo : pix;
+  const int8_t* row = q1_t + o * ldq + off;
   int s4[4] = {0, 0, 0, 0};
 #pragma unroll 16
-  for (int n = 0; n < g.n; ++n) s4[n & 3] += row[(int64_t)n * howo];
+  for (int n = 0; n < g.n; ++n) s4[n & 3] += row[(int64_t)n * g.psp];
   qs[t] = (s4[0] + s4[1]) + (s4[2] + s4[3]);
 }
 
@@ -544,12 +623,14 @@ __global__ __launch_bounds__(256) void conv_psq_weights_kernel(const float* scal
 }
 
 // out[ch][pix] = sum over slots i of wt[i] codes[ch ld + i pitch + pix] (float64)
+// (rows of rw pixels stored rp apart when rp > 0)
 __global__ void conv_wsum_kernel(const int8_t* codes, int64_t ld, int64_t pitch, int64_t npix, int64_t nch, int n,
-                                 const double* wt, double* out) {
+                                 int64_t rw, int64_t rp, const double* wt, double* out) {
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (t >= nch * npix) return;
   const int64_t ch = t / npix, pix = t - (t / npix) * npix;
-  const int8_t* col = codes + ch * ld + pix;
+  const int64_t off = rp > 0 ? (pix / rw) * rp + pix % rw : pix;
+  const int8_t* col = codes + ch * ld + off;
   double s4[4] = {0.0, 0.0, 0.0, 0.0};
 #pragma unroll 4
   for (int i = 0; i < n; ++i) s4[i & 3] += wt[i] * (double)col[(int64_t)i * pitch];
@@ -976,33 +1057,66 @@ hipError_t launch_conv_wq(const float* W, const ConvGeom& g, int bits, const flo
   return hipGetLastError();
 }
 
+hipError_t launch_conv_im2col_w_t(const ConvGeom& gi, const int8_t* xq_t, int8_t* bw, int64_t ldb, int32_t* xs,
+                                  int32_t* sumB, const ConvGeom& g, hipStream_t s);
+
 hipError_t launch_conv_im2col_w(const ConvGeom& g, const int8_t* xq_t, int8_t* bw, int64_t ldb, int32_t* xs,
                                 int32_t* sumB, hipStream_t s) {
-  const int64_t rows = (int64_t)g.kh * g.kw * g.c;
-  if (rows > 65535 || g.psp < (int64_t)g.ho * g.wo || ldb < (int64_t)g.n * g.psp || (ldb & 15) != 0)
+  if (g.gwp > 0) {
+    // the kw shifted copies of the zero-halo grid: the im2col kernels on a
+    // one-row kernel whose output rows are the ghp grid rows of gwp bytes
+    ConvGeom gg = g;
+    gg.kh = 1;
+    gg.ho = (int)g.ghp;
+    gg.wo = (int)g.gwp;
+    if (g.stride != 1 || g.ghp != g.h + 2 * g.pad || g.gwp < g.w + 2 * g.pad || (g.gwp & 15) != 0 ||
+        g.psp < g.ghp * g.gwp || ldb != g.ldx || g.kw > g.gwp)
+      return hipErrorInvalidValue;
+    if ((g.w & 3) == 0 && g.kw <= XGRID_MAXKW && (((uintptr_t)xq_t) & 3) == 0 && (((uintptr_t)bw) & 15) == 0) {
+      const int64_t nt = (int64_t)g.c * g.n * g.ghp * (g.gwp >> 4);
+      if ((nt + 255) / 256 > 0x7FFFFFFF) return hipErrorInvalidValue;
+      hipLaunchKernelGGL(conv_xgrid_kernel, dim3((unsigned)((nt + 255) / 256)), dim3(256), 0, s, g, xq_t, bw);
+      return launch_conv_im2col_w_t(gg, xq_t, nullptr, ldb, xs, sumB, g, s);
+    }
+    return launch_conv_im2col_w_t(gg, xq_t, bw, ldb, xs, sumB, g, s);
+  }
+  return launch_conv_im2col_w_t(g, xq_t, bw, ldb, xs, sumB, g, s);
+}
+
+// gi: the geometry the codes are laid out for (im2col, or the grid copies);
+// g: the conv's own (for the zero-point sums)
+hipError_t launch_conv_im2col_w_t(const ConvGeom& gi, const int8_t* xq_t, int8_t* bw, int64_t ldb, int32_t* xs,
+                                  int32_t* sumB, const ConvGeom& g, hipStream_t s) {
+  const int64_t rows = (int64_t)gi.kh * gi.kw * gi.c;
+  if (rows > 65535 || gi.psp < (int64_t)gi.ho * gi.wo || ldb < (int64_t)gi.n * gi.psp || (ldb & 15) != 0)
     return hipErrorInvalidValue;
-  if (conv_im2col_rows_ok(g, xq_t, bw, ldb)) {
+  if (!bw) {
+    // the codes are laid out already: only the zero-point sums
+  } else if (conv_im2col_rows_ok(gi, xq_t, bw, ldb)) {
     // stride 1, rows of 4-byte words: one thread per output word
-    const int spb = 256 * IM2COL_WPT / (g.wo / 4);
-    const int64_t blocks = ((int64_t)g.n * g.ho + spb - 1) / spb;
-    if (blocks > 0x7FFFFFFF || (int64_t)g.n * g.ho + 256 * IM2COL_WPT > 0x7FFFFFFF) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(conv_im2col_rows_kernel, dim3((unsigned)blocks, (unsigned)rows), dim3(256), 0, s, g, xq_t, bw,
+    const int spb = 256 * IM2COL_WPT / (gi.wo / 4);
+    const int64_t blocks = ((int64_t)gi.n * gi.ho + spb - 1) / spb;
+    if (spb < 1 || blocks > 0x7FFFFFFF || (int64_t)gi.n * gi.ho + 256 * IM2COL_WPT > 0x7FFFFFFF)
+      return hipErrorInvalidValue;
+    hipLaunchKernelGGL(conv_im2col_rows_kernel, dim3((unsigned)blocks, (unsigned)rows), dim3(256), 0, s, gi, xq_t, bw,
                        ldb, spb);
-    if (g.psp > (int64_t)g.ho * g.wo) {
-      const int64_t nt = (int64_t)g.n * (g.psp - (int64_t)g.ho * g.wo);
+    if (gi.psp > (int64_t)gi.ho * gi.wo) {
+      const int64_t nt = (int64_t)gi.n * (gi.psp - (int64_t)gi.ho * gi.wo);
       if ((nt + 255) / 256 > 0x7FFFFFFF) return hipErrorInvalidValue;
       hipLaunchKernelGGL(conv_pitch_zero_kernel, dim3((unsigned)((nt + 255) / 256), (unsigned)rows), dim3(256), 0, s,
-                         g, bw, ldb);
+                         gi, bw, ldb);
     }
   } else {
     const int64_t chunks = (ldb + 16 * 256 - 1) / (16 * 256);
     if (chunks > 0x7FFFFFFF) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(conv_im2col_w_kernel, dim3((unsigned)chunks, (unsigned)rows), dim3(256), 0, s, g, xq_t, bw, ldb);
+    hipLaunchKernelGGL(conv_im2col_w_kernel, dim3((unsigned)chunks, (unsigned)rows), dim3(256), 0, s, gi, xq_t, bw,
+                       ldb);
   }
   if (!xs) return hipGetLastError();  // per-sample Q_b1 forms its own sums
   const int64_t nx = (int64_t)g.c * g.h * g.w;
   hipLaunchKernelGGL(conv_xsum_kernel, dim3((unsigned)((nx + 255) / 256)), dim3(256), 0, s, g, xq_t, xs);
-  hipLaunchKernelGGL(conv_xtapsum_kernel<int32_t>, dim3((unsigned)rows), dim3(256), 0, s, g, xs, sumB);
+  hipLaunchKernelGGL(conv_xtapsum_kernel<int32_t>, dim3((unsigned)((int64_t)g.kh * g.kw * g.c)), dim3(256), 0, s, g,
+                     xs, sumB);
   return hipGetLastError();
 }
 
@@ -1035,9 +1149,9 @@ hipError_t launch_conv_psq_sums(const ConvGeom& g, const float* scale, const flo
     return hipErrorInvalidValue;
   hipLaunchKernelGGL(conv_psq_weights_kernel, dim3(1), dim3(256), 0, s, scale, zero, perm, g.n, half, ps);
   hipLaunchKernelGGL(conv_wsum_kernel, dim3((unsigned)((n1 + 255) / 256)), dim3(256), 0, s, q1_t, ldq, g.psp, howo,
-                     (int64_t)g.o, g.n, (const double*)ps.dA, ps.qw);
+                     (int64_t)g.o, g.n, (int64_t)g.wo, g.gwp, (const double*)ps.dA, ps.qw);
   hipLaunchKernelGGL(conv_wsum_kernel, dim3((unsigned)((n2 + 255) / 256)), dim3(256), 0, s, xq_t, g.n * hw, hw, hw,
-                     (int64_t)g.c, g.n, (const double*)ps.zA, ps.xw);
+                     (int64_t)g.c, g.n, (int64_t)0, (int64_t)0, (const double*)ps.zA, ps.xw);
   hipLaunchKernelGGL(conv_tapsum_kernel<double>, dim3((unsigned)(g.o * taps)), dim3(256), 0, s, g,
                      (const double*)ps.qw, ps.WA, count_tap);
   hipLaunchKernelGGL(conv_xtapsum_kernel<double>, dim3((unsigned)(taps * g.c)), dim3(256), 0, s, g,

@@ -238,6 +238,10 @@ struct NarrowQParams {
   int64_t ldt;
   int64_t vblk;  // rows of each block of blk that exist in x (the rest are zero codes); 0: blk
   int rowscale;  // scale / zero per block (indexed by the block's source block), else per tensor
+  // 2-D blocks (gw > 0, replaces vblk): row br of a block is (y, x) = (br / gw,
+  // br % gw) of a grid with rows of gw; it exists iff y < gho and x < gwo and
+  // reads source row y gwo + x of its block
+  int64_t gw, gwo, gho;
 };
 hipError_t launch_quant_narrow_t(const NarrowQParams& p, hipStream_t s);
 
@@ -256,6 +260,10 @@ struct GemmParams {
   int packedA;      // A holds codes of at most 4 bits two per byte (as the quantizer packs them), K % 16 == 0
   const int8_t* B;  // [N, K] row stride ldb
   int64_t M, N, K, lda, ldb;
+  // conv B row map (bmap_c > 0, fast K loop only): row j = (tap, c) with
+  // tap = (r, s) of a bmap_kw-wide kernel starts at B + (s bmap_c + c) ldb +
+  // r bmap_wp (shifted activation-code grids, see ConvGeom)
+  int64_t bmap_c, bmap_kw, bmap_wp;
   int64_t kchunk;   // K per split (multiple of 128 when split, <= 65536)
   int splits;
   int32_t* part;    // EPI_RAW_I32 output [splits][M][N]
@@ -326,12 +334,22 @@ hipError_t launch_pack_e3m2(const int8_t* src, int64_t rows, int64_t K, int64_t 
 hipError_t launch_status_clear(uint32_t* status, hipStream_t s);
 hipError_t launch_gemm_bf6(const Bf6Params& p, hipStream_t s);
 
+constexpr int NUM_XCD = 8;  // accelerator dies of the GPU, each with its own L2; blocks go to them round robin
+
 // ---- conv ----------------------------------------------------------------
 struct ConvGeom {
   int n, c, h, w, o, kh, kw, stride, pad, ho, wo;
   int64_t npad;  // slots per input pixel in the grad_X rows (multiple of 64)
   int64_t psp;   // K pitch of a slot's output pixels in the grad_W operands (ho wo, or
-                 // ho wo rounded up to 128 with zero codes after them when Q_b1 is per sample)
+                 // ho wo rounded up to 128 with zero codes after them when Q_b1 is per sample;
+                 // the grid's ghp gwp rounded up to 128 for the implicit form)
+  // implicit grad_W (gwp > 0, stride 1): output pixel (y, x) of slot n is K
+  // index n psp + y gwp + x of Q_b1 (zero codes elsewhere); the activation
+  // codes sit on a zero-halo grid of ghp = h + 2 pad rows of gwp bytes (input
+  // pixel (iy, ix) at (iy + pad, ix + pad)), stored kw times [s][c][ldx], copy
+  // s shifted left by s bytes, so that tap (r, s) reads copy s at K offset
+  // r gwp: no im2col matrix
+  int64_t gwp, ghp, ldx;
 };
 hipError_t launch_conv_wq(const float* W, const ConvGeom& g, int bits, const float* scale, const float* zero,
                           int8_t* wq_t, int32_t* swq, hipStream_t s);

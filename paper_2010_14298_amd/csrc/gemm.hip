@@ -59,10 +59,23 @@ __global__ __launch_bounds__(C::THREADS) void gemm_i8_kernel(GemmParams p) {
   const int wm = wave / C::WAVES_N, wn = wave % C::WAVES_N;
   const int64_t tiles_n = (p.N + C::BN - 1) / C::BN;
   const int64_t tiles_m = (p.M + C::BM - 1) / C::BM;
-  const int64_t tile = xcd_tile(blockIdx.x, tiles_m * tiles_n);
+  int64_t tile;
+  int split;
+  if (p.splits > 1 && p.splits % NUM_XCD == 0) {
+    // split-K: blocks go to the XCDs round robin in launch order; give one
+    // XCD every tile of its splits, so that the tiles sharing a split's A
+    // panel (and, for the conv taps, overlapping B rows) meet in its L2
+    const int64_t T = tiles_m * tiles_n;
+    const int64_t L = (int64_t)blockIdx.x + (int64_t)gridDim.x * blockIdx.y;
+    const int64_t j = L / NUM_XCD;
+    tile = j % T;
+    split = (int)(L % NUM_XCD + NUM_XCD * (j / T));
+  } else {
+    tile = xcd_tile(blockIdx.x, tiles_m * tiles_n);
+    split = blockIdx.y;
+  }
   const int64_t m0 = (tile / tiles_n) * C::BM;
   const int64_t n0 = (tile % tiles_n) * C::BN;
-  const int split = blockIdx.y;
   const int64_t kbeg = (int64_t)split * p.kchunk;
   const int64_t kend = (kbeg + p.kchunk < p.K) ? kbeg + p.kchunk : p.K;
   const int lrow = lane & 31;
@@ -408,6 +421,7 @@ static hipError_t launch_gemm_t(GemmParams p, hipStream_t s) {
     }
   }
   if (p.packedA) return hipErrorInvalidValue;
+  if (p.bmap_c > 0 && (!fast || (p.bmap_wp & 15) != 0)) return hipErrorInvalidValue;  // mapped rows: fast loop only
   if (fast)
     hipLaunchKernelGGL((gemm_i8_kernel<C, EPI, KG, true>), grid, dim3(C::THREADS), 0, s, p);
   else

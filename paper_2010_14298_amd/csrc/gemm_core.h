@@ -12,7 +12,6 @@ namespace fqt {
 typedef int v4i __attribute__((ext_vector_type(4)));
 typedef int v16i __attribute__((ext_vector_type(16)));
 
-constexpr int NUM_XCD = 8;
 
 // Block tile BM x BN, wave tile WM x WN, BK_ K bytes per pipeline stage.
 // Generic K loop: LDS rows padded by 16 bytes (conflict-free 8- and 16-lane
@@ -245,7 +244,13 @@ __device__ __forceinline__ void dma_mainloop(const GemmParams& p, int8_t* __rest
   for (int i = 0; i < C::B_INS; ++i) {
     const int r = 8 * (wave * C::B_INS + i) + (lane >> 3);
     const int64_t row = (n0 + r < p.N) ? n0 + r : p.N - 1;
-    srcB[i] = p.B + row * p.ldb + kbeg + 16 * ((lane & 7) ^ ((r >> 1) & 7));
+    int64_t off = row * p.ldb;
+    if (p.bmap_c > 0) {  // conv tap (kr, ks), channel ch: copy ks, K offset kr gwp
+      const int64_t tap = row / p.bmap_c, ch = row - tap * p.bmap_c;
+      const int64_t kr = tap / p.bmap_kw, ks = tap - kr * p.bmap_kw;
+      off = (ks * p.bmap_c + ch) * p.ldb + kr * p.bmap_wp;
+    }
+    srcB[i] = p.B + off + kbeg + 16 * ((lane & 7) ^ ((r >> 1) & 7));
   }
   const int64_t nk = (kend - kbeg) / C::BK;
   int8_t* bufs[4] = {b0, b1, b2, b3};

@@ -126,6 +126,12 @@ def test_workspace_queries_and_argument_errors():
     psq1 = fqt.cfg_struct(qb_w=("psq", 8, 0))
     ws_psq = lib.fqt_conv_backward_workspace(ctypes.byref(sh), ctypes.byref(psq1))
     assert ws_psq >= 2 * 16 * 9 * 4 * 4 + 16 * 2 * 128 + 9 * 4 * 2 * 128
+    # stride-1 layers with dense enough grids contract over shifted copies of
+    # the activation codes, not an im2col matrix: the 56 x 56 batch-128
+    # layer's whole workspace is below its im2col matrix alone
+    l56 = fqt.conv_shape(128, 64, 56, 56, 64, 3, 3, 1, 1)
+    for q in (cfg, psq1):
+        assert lib.fqt_conv_backward_workspace(ctypes.byref(l56), ctypes.byref(q)) < 9 * 64 * 128 * 56 * 56
     # more output pixels than one int32-exact K block holds
     big = fqt.conv_shape(1, 16, 260, 260, 16, 1, 1, 1, 0)
     rc = lib.fqt_conv_backward_im2col(fake, fake, fake, ctypes.byref(big), ctypes.byref(psq1), fake, fake, fake,

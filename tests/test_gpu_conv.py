@@ -105,7 +105,16 @@ GEOMETRIES = [
 ]
 
 
-@pytest.mark.parametrize("geo", GEOMETRIES)
+IMPLICIT_GEOMETRIES = [
+    # stride 1 with enough output pixels per grid row: grad_W on the zero-halo grid
+    (3, 8, 24, 28, 16, 1, 3, 1, 1),   # 1 x 3 kernel, rectangular image
+    (3, 8, 28, 30, 16, 3, 1, 1, 1),   # 3 x 1 kernel
+    (2, 24, 14, 14, 48, 3, 3, 1, 1),  # part K stage, part column tile, byte-wise grid copies
+    (2, 8, 30, 30, 16, 2, 2, 1, 0),   # even kernel, no padding
+]
+
+
+@pytest.mark.parametrize("geo", GEOMETRIES + IMPLICIT_GEOMETRIES)
 @pytest.mark.parametrize("qb_x", [("bhq", 5, 2), ("psq", 6, 0)])
 def test_conv_geometries(geo, qb_x):
     n, c, h, w, o, kh, kw, st, pad = geo
@@ -219,13 +228,21 @@ def exact_conv_grads(X, W, G, stride, pad):
     return gW, gXp[:, pad: pad + h, pad: pad + w]
 
 
-@pytest.mark.parametrize("geom", [
-    (128, 64, 56, 64, 3, 1, 1),     # the 56 x 56 layer at full size
+GRID_GEOMS = [
+    (128, 64, 56, 64, 3, 1, 1),     # the 56 x 56 layer at full size (implicit grad_W, word-aligned rows)
     (150, 16, 9, 32, 3, 2, 1),      # more slots per input pixel than one tile
     (40, 3, 32, 64, 7, 2, 3),       # stem-like: 7 x 7, stride 2, three channels
     (24, 32, 14, 48, 1, 2, 0),      # 1 x 1, stride 2
-    (8, 16, 11, 16, 5, 1, 2),       # 5 x 5
-], ids=lambda g: "n{}_c{}_h{}_o{}_k{}_s{}_p{}".format(*g))
+    (8, 16, 11, 16, 5, 1, 2),       # 5 x 5 (explicit im2col: the grid would be too sparse)
+    (6, 8, 14, 16, 3, 1, 1),        # implicit grad_W, 14-byte rows (byte-wise grid copies)
+    (4, 16, 28, 32, 3, 1, 1),       # implicit, 28 x 28
+    (3, 8, 16, 16, 1, 1, 0),        # implicit 1 x 1: one grid copy
+    (2, 8, 44, 16, 5, 1, 2),        # implicit 5 x 5: five copies, K offsets up to 4 grid rows
+    (3, 8, 16, 16, 3, 1, 0),        # implicit valid 3 x 3
+]
+
+
+@pytest.mark.parametrize("geom", GRID_GEOMS, ids=lambda g: "n{}_c{}_h{}_o{}_k{}_s{}_p{}".format(*g))
 def test_conv_contractions_exact_on_the_grid(geom):
     n, c, h, o, k, stride, pad = geom
     X, W, G = grid_conv_inputs(n + c + o, n, c, h, o, k, stride, pad)
@@ -244,8 +261,7 @@ def test_conv_contractions_exact_per_sample_scales():
     # each sample's step is 2^(i mod 3), so both quantizers stay exact while a
     # per-tensor one would not, and every sample's int32 block and its scale
     # must be right for grad_W to equal the exact sum
-    for geom in [(128, 64, 56, 64, 3, 1, 1), (150, 16, 9, 32, 3, 2, 1), (40, 3, 32, 64, 7, 2, 3),
-                 (24, 32, 14, 48, 1, 2, 0), (8, 16, 11, 16, 5, 1, 2)]:
+    for geom in GRID_GEOMS:
         n, c, h, o, k, stride, pad = geom
         X, W, G = grid_conv_inputs(n + c + o, n, c, h, o, k, stride, pad)
         G = G * (2.0 ** (np.arange(n) % 3)).reshape(n, 1, 1, 1).astype(np.float32)
@@ -290,7 +306,7 @@ def test_conv_per_sample_grad_w(shape, qbs):
     assert rownorm_err(gX, r["grad_X64"]) <= REL_TOL
 
 
-@pytest.mark.parametrize("geo", GEOMETRIES[:3])
+@pytest.mark.parametrize("geo", GEOMETRIES[:3] + IMPLICIT_GEOMETRIES)
 def test_conv_per_sample_grad_w_geometries(geo):
     n, c, h, w, o, kh, kw, st, pad = geo
     X, W, G = conv_inputs(sum(geo) + 1, n, c, h, w, o, kh, kw, st, pad)
