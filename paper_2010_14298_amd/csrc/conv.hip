@@ -867,6 +867,18 @@ struct ConvRowStage {
 
 using CfgConvX = TileCfg<128, 64, 64, 64, 64>;  // 64-code K stages, 36 KB of LDS: four blocks per CU
 
+// The K stages of a grad_X tile: only the taps that reach one of the tile's
+// input pixels (a tile's 128 rows hold the slots of at most two pixels).
+// With stride 2 about a quarter of the taps reach a pixel, and pixels with
+// none (odd ones of a 1 x 1 stride-2 conv) run no K loop at all.  Stage t
+// at K offset 64 st[t]; past the list, K (the loaders load zeros).
+constexpr int CONVX_MAXST = 512;
+struct KStageList {
+  const uint16_t* st;
+  int64_t n, K;
+  __device__ __forceinline__ int64_t k(int64_t t) const { return t < n ? 64 * (int64_t)st[t] : K; }
+};
+
 template <int EPI, int KG, class XLoader>
 __global__ __launch_bounds__(256) void conv_gradx_kernel(GemmParams p, ConvGeom g, const int8_t* q2, const int32_t* sg,
                                                           const int32_t* ct, const int32_t* cnt) {
@@ -893,7 +905,39 @@ __global__ __launch_bounds__(256) void conv_gradx_kernel(GemmParams p, ConvGeom 
 #pragma unroll
     for (int j = 0; j < C::JT; ++j) acc[i][j] = v16i{0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0};
   const XLoader aload{q2, g, p.M, p.K, D};
-  generic_mainloop<C>(p, aload, ConvWLoader{p.B, p.ldb, p.N, p.K}, lds, m0, n0, 0, p.K, acc);
+  const int taps = g.kh * g.kw;
+  const int spt = g.o / 64;  // K stages per tap
+  if (taps <= 64 && g.o % 64 == 0 && taps * spt <= CONVX_MAXST) {
+    __shared__ uint16_t s_st[CONVX_MAXST];
+    __shared__ int s_nst;
+    if (wave == 0) {
+      // lane i: does tap i reach an input pixel of this tile?
+      const uint32_t npad = (uint32_t)g.npad, hw = (uint32_t)(g.h * g.w);
+      const uint32_t pa = (uint32_t)m0 / npad;
+      const uint32_t last = (uint32_t)((m0 + C::BM - 1 < p.M ? m0 + C::BM - 1 : p.M - 1));
+      const uint32_t pb = last / npad;
+      bool hit = false;
+      if (lane < taps) {
+        const int r = lane / g.kw, s2 = lane - (lane / g.kw) * g.kw;
+        int y, x;
+        for (uint32_t pix = pa; pix <= pb && pix < hw; ++pix) {
+          const int iy = (int)(pix / (uint32_t)g.w), ix = (int)pix - iy * g.w;
+          if (tap_hits(g, iy, ix, r, s2, y, x)) hit = true;
+        }
+      }
+      const uint64_t mask = __ballot(hit);
+      if (hit) {
+        const int before = __popcll(mask & ((1ull << lane) - 1ull));
+        for (int j = 0; j < spt; ++j) s_st[before * spt + j] = (uint16_t)(lane * spt + j);
+      }
+      if (lane == 0) s_nst = __popcll(mask) * spt;
+    }
+    __syncthreads();
+    generic_mainloop_km<C>(p, aload, ConvWLoader{p.B, p.ldb, p.N, p.K}, lds, m0, n0, KStageList{s_st, s_nst, p.K},
+                           acc);
+  } else {
+    generic_mainloop<C>(p, aload, ConvWLoader{p.B, p.ldb, p.N, p.K}, lds, m0, n0, 0, p.K, acc);
+  }
 
   int32_t* sacc = reinterpret_cast<int32_t*>(lds);
   ConvRowStage* srow = reinterpret_cast<ConvRowStage*>(lds + C::BM * C::BN * 4);

@@ -278,17 +278,27 @@ __device__ __forceinline__ void dma_mainloop(const GemmParams& p, int8_t* __rest
   __syncthreads();
 }
 
-template <class C, class ALoader, class BLoader>
-__device__ __forceinline__ void generic_mainloop(const GemmParams& p, const ALoader& aload, const BLoader& bload,
-                                                 int8_t* lds, int64_t m0, int64_t n0, int64_t kbeg, int64_t kend,
-                                                 v16i (&acc)[C::IT][C::JT]) {
+// K offsets of the stages a K loop runs: stage t starts at kbeg + t bk, n
+// stages (offsets past the end load zero chunks)
+struct KRange {
+  int64_t kbeg, bk, n;
+  __device__ __forceinline__ int64_t k(int64_t t) const { return kbeg + t * bk; }
+};
+
+// The register-staged K loop over the stages of a stage map KM (km.n stages,
+// stage t at K offset km.k(t); for t >= km.n, km.k(t) must lie past the
+// loaders' K range so that they load zeros).
+template <class C, class ALoader, class BLoader, class KM>
+__device__ __forceinline__ void generic_mainloop_km(const GemmParams& p, const ALoader& aload, const BLoader& bload,
+                                                    int8_t* lds, int64_t m0, int64_t n0, const KM& km,
+                                                    v16i (&acc)[C::IT][C::JT]) {
   int8_t* sA = lds;                          // [2][BM * C::LDS_STRIDE]
   int8_t* sB = lds + 2 * C::BM * C::LDS_STRIDE;  // [2][BN * C::LDS_STRIDE]
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
   const int wm = wave / C::WAVES_N, wn = wave % C::WAVES_N;
-  const int64_t nk = (kend - kbeg + C::BK - 1) / C::BK;
+  const int64_t nk = km.n;
 
   // Two register staging sets: the loads of stage t + 1 are issued one
   // iteration before the stage is stored to LDS, so each global load has two
@@ -304,7 +314,7 @@ __device__ __forceinline__ void generic_mainloop(const GemmParams& p, const ALoa
   static_assert(C::THREADS % C::KCH == 0, "a thread keeps one chunk column");
   const int kch = 16 * (tid % C::KCH);  // the K offset of every A chunk this thread loads
   auto gload = [&](Stage& st, int64_t t) __attribute__((always_inline)) {
-    const int64_t k0 = kbeg + t * C::BK;
+    const int64_t k0 = km.k(t);
     const typename ALoader::KState ks = aload.kstate(k0 + kch);  // once per stage: shared by the thread's rows
 #pragma unroll
     for (int i = 0; i < C::A_CHUNKS; ++i) {
@@ -374,6 +384,13 @@ __device__ __forceinline__ void generic_mainloop(const GemmParams& p, const ALoa
     iter(t + 1, 1, st0, st1);
   }
   if (t < nk) iter(t, 0, st1, st0);
+}
+
+template <class C, class ALoader, class BLoader>
+__device__ __forceinline__ void generic_mainloop(const GemmParams& p, const ALoader& aload, const BLoader& bload,
+                                                 int8_t* lds, int64_t m0, int64_t n0, int64_t kbeg, int64_t kend,
+                                                 v16i (&acc)[C::IT][C::JT]) {
+  generic_mainloop_km<C>(p, aload, bload, lds, m0, n0, KRange{kbeg, C::BK, (kend - kbeg + C::BK - 1) / C::BK}, acc);
 }
 
 template <class C, bool FAST, class ALoader>
