@@ -258,7 +258,9 @@ def resnet_sweep(args, fqt, synth, torch):
     5-bit block 64, PSQ 8-bit, PTQ 8-bit; Q_b1 = PTQ 8-bit), HIP events.
     Inputs drawn on the device with the recipe of synth.conv_layer:
     post-ReLU half-normal X (N(0,1) at the stem), He-init W, per-sample
-    LogNormal(0, 2) gradient scales."""
+    LogNormal(0, 2) gradient scales.  The stem's input is the image, which
+    takes no gradient in training: its row and the network total run it
+    without grad_X (NULL), and its full backward is reported beside them."""
     import math
     n = 256
     specs = (("bhq5", ("bhq", 5, 64)), ("psq8", ("psq", 8, 0)), ("ptq8", ("ptq", 8, 0)))
@@ -278,28 +280,39 @@ def resnet_sweep(args, fqt, synth, torch):
         ops = 2.0 * 2.0 * n * ho * ho * o * k * k * c
         row = {"shape": f"{c}->{o} k{k} s{stride} {h}->{ho}", "count": count, "GOP": round(ops / 1e9, 2)}
         gW, gX = torch.empty_like(W), torch.empty_like(X)
-        for name, spec in specs:
+        stem = c == 3
+        if stem:
+            row["input_grad"] = False
+            row["GOP"] = round(ops / 2 / 1e9, 2)  # the grad_W contraction only
+
+        def timed(spec, input_grad):
             ws = None
             for i in range(2):
                 _, _, ws = fqt.fqt_conv_backward_im2col(X, W, G, stride, pad, qb_x=spec, qb_w=QB_W, seed=i,
-                                                         grad_W=gW, grad_X=gX, ws=ws)
+                                                         grad_W=gW, grad_X=gX, ws=ws, input_grad=input_grad)
             torch.cuda.synchronize()
             e0.record()
             for i in range(reps):
                 fqt.fqt_conv_backward_im2col(X, W, G, stride, pad, qb_x=spec, qb_w=QB_W, seed=i, grad_W=gW,
-                                             grad_X=gX, ws=ws)
+                                             grad_X=gX, ws=ws, input_grad=input_grad)
             e1.record()
             torch.cuda.synchronize()
-            ms = e0.elapsed_time(e1) / reps
-            row[name] = {"ms": round(ms, 4), "TOPS": round(ops / (ms * 1e-3) / 1e12, 2)}
+            return e0.elapsed_time(e1) / reps
+
+        for name, spec in specs:
+            lops = ops / 2 if stem else ops  # grad_W only
+            ms = timed(spec, not stem)
+            row[name] = {"ms": round(ms, 4), "TOPS": round(lops / (ms * 1e-3) / 1e12, 2)}
+            if stem:
+                row[name]["ms_with_input_grad"] = round(timed(spec, True), 4)
             net[name][0] += count * ms
-            net[name][1] += count * ops
-            del ws
+            net[name][1] += count * lops
         layers.append(row)
         del X, W, G, gW, gX
     torch.cuda.empty_cache()
     return {"workload": "ResNet-50 v1.5 conv layers at batch 256 (224 x 224), every unique shape; whole FQT conv "
-                        "backward per layer", "steps_per_layer": reps, "layers": layers,
+                        "backward per layer (the stem without its input gradient)", "steps_per_layer": reps,
+            "layers": layers,
             "network": {name: {"ms": round(v[0], 3), "TOPS": round(v[1] / (v[0] * 1e-3) / 1e12, 2)}
                         for name, v in net.items()}}
 

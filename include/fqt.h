@@ -283,12 +283,22 @@ typedef struct {
   int n, c, h, w, o, kh, kw, stride, pad, ho, wo;
 } fqt_conv_shape;
 
-/* Conv layer FQT backward as implicit-im2col contractions: the conv is the
- * linear layer Y = im2col(X) W^T, so grad_W = Q_b1(G)^T im2col(Q_f(X)) and
+/* Conv layer FQT backward (Sec. 2.2 applied to the conv as the linear layer
+ * Y = im2col(X) W^T): grad_W = Q_b1(G)^T im2col(Q_f(X)) and
  * grad_X = col2im(Q_b2(G) Q_theta(W)).  Quantizer rows are samples
  * (Sec. 4.1): X and W per tensor, G [n, ho*wo*o] per sample / group.
- * Padding taps contribute exactly zero.  Outputs grad_W [o, kh, kw, c] and
- * grad_X [n, h, w, c] are overwritten.                                      */
+ * Padding taps contribute exactly zero.
+ *   cfg->qb_x: Q_b2, PTQ / PSQ / BHQ (any block size, 0 = App. D groups).
+ *   cfg->qb_w: Q_b1, PTQ, or PSQ (Sec. 4.1's per-sample scales on grad_W:
+ *              each sample's output pixels are one int32-exact K block of
+ *              the contraction, scaled by the sample's 1 / s in float64;
+ *              ho * wo <= 65536 and n <= 65535, else FQT_EUNSUPPORTED).
+ *              The shift form is linear-only (FQT_EUNSUPPORTED here).
+ *   cfg->relu_input must be 0 (FQT_EUNSUPPORTED).
+ * Outputs grad_W [o, kh, kw, c] and grad_X [n, h, w, c] are overwritten.
+ * grad_X may be NULL: the input gradient is then not formed (no Q_b2, no
+ * Q_theta(W), no grad_X contraction), as for a first layer whose input
+ * takes no gradient; grad_W is the same as with it.  o % 16 == 0.          */
 fqt_status fqt_conv_backward_im2col(const float* X, const float* W, const float* G,
                                     const fqt_conv_shape* shape, const fqt_bwd_cfg* cfg, float* grad_W,
                                     float* grad_X, void* ws, size_t ws_bytes, fqt_stream_t s);

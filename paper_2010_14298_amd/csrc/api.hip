@@ -1097,7 +1097,8 @@ fqt_status fqt_gemm_s4s4_bf6(const int8_t* A, const int8_t* B, int64_t M, int64_
 fqt_status fqt_conv_backward_im2col(const float* X, const float* W, const float* G, const fqt_conv_shape* shape,
                                     const fqt_bwd_cfg* cfg, float* grad_W, float* grad_X, void* ws,
                                     size_t ws_bytes, fqt_stream_t s) {
-  if (!X || !W || !G || !grad_W || !grad_X || !shape) return FQT_EINVAL;
+  if (!X || !W || !G || !grad_W || !shape) return FQT_EINVAL;
+  const bool want_x = grad_X != nullptr;  // NULL: no input gradient
   fqt_status st = check_conv_shape(*shape);
   if (st != FQT_OK) return st;
   st = check_cfg(cfg);
@@ -1117,7 +1118,9 @@ fqt_status fqt_conv_backward_im2col(const float* X, const float* W, const float*
   Carver c(ws);
   ConvWs w = carve_conv(c, X, W, G, g, *cfg);
   const fqt_qspec qx = cfg->qb_x;
-  const bool bhq = qx.kind == FQT_BHQ;
+  // without an input gradient there is no Q_b2, so no BHQ plan: samples stay in order
+  const bool bhq = qx.kind == FQT_BHQ && want_x;
+  int32_t* const perm = bhq ? w.perm : nullptr;
   const Tracer tr{cfg->trace, s};
   const int64_t N = g.n, D = (int64_t)g.ho * g.wo * g.o;
   const int64_t hw = (int64_t)g.h * g.w, howo = (int64_t)g.ho * g.wo;
@@ -1147,7 +1150,7 @@ fqt_status fqt_conv_backward_im2col(const float* X, const float* W, const float*
   fp.out[1] = ScaleOut{1, cfg->theta_bits, 0, w.sw, w.zw};
   fp.out[2] = ScaleOut{2, cfg->qb_w.bits, psq1 ? 1 : 0, w.sg1, w.zg1};
   fp.nout = 3;
-  if (!bhq) fp.out[fp.nout++] = ScaleOut{2, qx.bits, qx.kind == FQT_PSQ ? 1 : 0, w.sg2, w.zg2};
+  if (!bhq && want_x) fp.out[fp.nout++] = ScaleOut{2, qx.bits, qx.kind == FQT_PSQ ? 1 : 0, w.sg2, w.zg2};
   if (!psq1) add_zero(fp, w.sumB, taps * g.c);
   if (bhq) add_zero(fp, bhq_plan_carve(w.bhq.plan, N).rank, N);
   const bool fin_in_plan = bhq && w.sg_seg.rmin != nullptr;
@@ -1167,7 +1170,7 @@ fqt_status fqt_conv_backward_im2col(const float* X, const float* W, const float*
   nx.x = X;
   nx.rows = N * hw;
   nx.cols = g.c;
-  nx.perm = w.perm;
+  nx.perm = perm;
   nx.blk = hw;
   nx.bits = cfg->f_bits;
   nx.scale = w.sx;
@@ -1178,7 +1181,7 @@ fqt_status fqt_conv_backward_im2col(const float* X, const float* W, const float*
   tr.end(3);
   // Q_theta(W): codes [c][(r, s, o)] and their sums over o
   tr.begin(4);
-  FQT_TRY(launch_conv_wq(W, g, cfg->theta_bits, w.sw, w.zw, w.wq_t, w.swq, s));
+  if (want_x) FQT_TRY(launch_conv_wq(W, g, cfg->theta_bits, w.sw, w.zw, w.wq_t, w.swq, s));
   tr.end(4);
   // Q_b2(G) [slot][(y, x, o)] (stream 1); Q_b1(G) [o][pixels] (stream 0)
   tr.begin(5);
@@ -1198,12 +1201,12 @@ fqt_status fqt_conv_backward_im2col(const float* X, const float* W, const float*
     st = bhq_params(w.bhq, G, N, D, qx.block_size, w.perm, w.sg2, pg, s);
     if (st != FQT_OK) return st;
   }
-  FQT_TRY(launch_quant(pg, mode, s));
+  if (want_x) FQT_TRY(launch_quant(pg, mode, s));
   NarrowQParams n1{};
   n1.x = G;
   n1.rows = N * g.psp;
   n1.cols = g.o;
-  n1.perm = w.perm;
+  n1.perm = perm;
   n1.blk = g.psp;
   n1.vblk = howo;
   n1.rowscale = psq1 ? 1 : 0;
@@ -1227,7 +1230,7 @@ fqt_status fqt_conv_backward_im2col(const float* X, const float* W, const float*
   tr.begin(6);
   FQT_TRY(launch_conv_im2col_w(g, w.xq_t, w.bw, g.gwp > 0 ? g.ldx : w.ldq, psq1 ? nullptr : w.xs, w.sumB, s));
   if (psq1)
-    FQT_TRY(launch_conv_psq_sums(g, w.sg1, w.zg1, w.perm, 1 << (cfg->qb_w.bits - 1), w.q1_t, w.ldq, w.xq_t, w.ps,
+    FQT_TRY(launch_conv_psq_sums(g, w.sg1, w.zg1, perm, 1 << (cfg->qb_w.bits - 1), w.q1_t, w.ldq, w.xq_t, w.ps,
                                  w.count_tap, s));
   else
     FQT_TRY(launch_conv_tapsums(g, w.q1_t, w.ldq, w.qs, w.sumA_tap, w.count_tap, s));
@@ -1265,6 +1268,11 @@ fqt_status fqt_conv_backward_im2col(const float* X, const float* W, const float*
   tr.end(6);
 
   // grad_X [n][h][w][c] = col2im(Q_b2(G) Q_theta(W)), implicit im2col rows
+  if (!want_x) {
+    tr.begin(7);
+    tr.end(7);
+    return FQT_OK;
+  }
   tr.begin(7);
   FQT_TRY(launch_conv_gradx_prep(g, w.q2, w.swq, w.sg, w.ct, w.cnt, s));
   GemmParams gx{};

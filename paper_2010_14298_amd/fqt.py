@@ -354,7 +354,8 @@ def fqt_conv_backward_workspace(shape, cfg):
 
 
 def fqt_conv_backward_im2col(X, W, G, stride, pad, qb_x=("bhq", 5, 64), qb_w=("ptq", 8, 0), f_bits=8,
-                             theta_bits=8, seed=0, grad_W=None, grad_X=None, ws=None, trace=None):
+                             theta_bits=8, seed=0, grad_W=None, grad_X=None, ws=None, trace=None, input_grad=True):
+    """input_grad=False passes a NULL grad_X (no input gradient); grad_X is then returned as None."""
     X, W, G = _f32(X, "X"), _f32(W, "W"), _f32(G, "G")
     n, h, w, c = X.shape
     o, kh, kw, _ = W.shape
@@ -364,7 +365,9 @@ def fqt_conv_backward_im2col(X, W, G, stride, pad, qb_x=("bhq", 5, 64), qb_w=("p
     cfg = cfg_struct(qb_x, qb_w, f_bits, theta_bits, seed, trace)
     if grad_W is None:
         grad_W = torch.empty(W.shape, dtype=torch.float32, device=X.device)
-    if grad_X is None:
+    if not input_grad:
+        grad_X = None
+    elif grad_X is None:
         grad_X = torch.empty(X.shape, dtype=torch.float32, device=X.device)
     if ws is None:
         ws = _workspace(fqt_conv_backward_workspace(sh, cfg), X.device)

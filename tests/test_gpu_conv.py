@@ -343,3 +343,25 @@ def test_conv_per_sample_grad_w_full_size_sampled():
             for ss in range(3):
                 ref[rr, ss] = np.einsum("nyx,nyxc->c", G1r[..., oo], xpad[:, rr: rr + h, ss: ss + w])
         assert rownorm_err(gW[oo].reshape(1, -1), ref.reshape(1, -1)) <= REL_TOL
+
+
+@pytest.mark.parametrize("qbs", [(("bhq", 5, 4), ("ptq", 8, 0)), (("psq", 8, 0), ("psq", 8, 0))])
+@pytest.mark.parametrize("geom", [(6, 8, 14, 16, 3, 1, 1), (40, 3, 32, 64, 7, 2, 3)])
+def test_conv_without_input_gradient(geom, qbs):
+    # a NULL grad_X skips Q_b2, Q_theta and the input-gradient contraction;
+    # grad_W is unchanged: bit for bit with a per-tensor Q_b1 (exact integer
+    # sums), within the float64 order of its per-sample sums otherwise
+    n, c, h, o, k, stride, pad = geom
+    qb_x, qb_w = qbs
+    X, W, G = synth.conv_layer(seed=n + k, n=n, c=c, h=h, w=h, o=o, k=k, stride=stride, pad=pad, stem=(c == 3))
+    f = fqt()
+    gW, gX, _ = f.fqt_conv_backward_im2col(dev(X), dev(W), dev(G), stride, pad, qb_x=qb_x, qb_w=qb_w, seed=3)
+    gW1, gX1, ws = f.fqt_conv_backward_im2col(dev(X), dev(W), dev(G), stride, pad, qb_x=qb_x, qb_w=qb_w, seed=3,
+                                              input_grad=False)
+    assert gX1 is None and f.fqt_workspace_status(ws) == 0
+    if qb_w[0] == "ptq":
+        np.testing.assert_array_equal(host(gW1), host(gW))
+    else:
+        assert rownorm_err(host(gW1), host(gW)) <= 1e-6
+    r = BW.conv_backward(X, W, G, stride, pad, qb_x=qb_x, qb_w=qb_w, seed=3)
+    assert rownorm_err(host(gW1), r["grad_W64"]) <= REL_TOL
