@@ -1197,6 +1197,7 @@ fqt_status fqt_conv_backward_im2col(const float* X, const float* W, const float*
   pg.scale = w.sg2;
   pg.zero = w.zg2;
   pg.q_nat = w.q2;
+  pg.pm_o = g.o;  // [output pixel][slot][o]: a grad_X tile's slots of one tap read one contiguous run
   if (bhq) {
     st = bhq_params(w.bhq, G, N, D, qx.block_size, w.perm, w.sg2, pg, s);
     if (st != FQT_OK) return st;

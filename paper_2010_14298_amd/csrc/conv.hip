@@ -5,13 +5,18 @@
 // grad_X = col2im(Q_b2(G) Q_theta(W)) (Sec. 2.2).  Layouts:
 //
 //   X codes    [c][pixels]           per-tensor PTQ, samples in slot order
-//   Q_b1(G)    [o][pixels (padded)]  per-tensor stochastic PTQ, slot order
+//   Q_b1(G)    [o][pixels (padded)]  stochastic PTQ or PSQ, slot order; on
+//                                    the zero-halo grid for the implicit form
 //   im2col     [(r, s, c)][pixels]   X codes per tap, zero codes on padding
+//   X grids    [s][c][grid]          implicit form (stride 1): kw shifted
+//                                    copies of the zero-halo activation grid
 //   W codes    [c][(r, s, o)]        per-tensor PTQ
-//   Q_b2(G)    [slot][(y, x, o)]     PTQ / PSQ / BHQ, natural layout
+//   Q_b2(G)    [(y, x)][slot][o]     PTQ / PSQ / BHQ, pixel-major
 //
-// grad_W is a split-K int8 contraction over output pixels with per-tap
-// masked zero-point sums in its epilogue.  grad_X is an implicit-im2col
+// grad_W is a split-K int8 contraction over output pixels (over im2col rows,
+// or over tap rows of the shifted grids) with per-tap masked zero-point sums
+// in its reduction; a per-sample Q_b1 takes one K block per sample.  grad_X
+// is an implicit-im2col
 // contraction: its A rows (input pixel, slot) are gathered 16 output
 // channels at a time from Q_b2(G); padded taps load zero codes and the
 // epilogue subtracts nothing for them (their zero-point sums are built from
@@ -676,8 +681,8 @@ __global__ void conv_sg_kernel(ConvGeom g, const int8_t* q2, int32_t* sg) {
   const uint32_t howo = (uint32_t)g.ho * (uint32_t)g.wo;
   const uint32_t t = blockIdx.x * blockDim.x + threadIdx.x;
   if (t >= (uint32_t)g.n * howo) return;
-  const uint32_t pix = t / (uint32_t)g.n, slot = t - pix * (uint32_t)g.n;
-  const int8_t* src = q2 + ((int64_t)slot * howo + pix) * g.o;  // Q_b2 rows are slot-major [slot][pix][o]
+  // Q_b2 codes are pixel-major [pix][slot][o]: thread t reads the t-th run of o codes
+  const int8_t* src = q2 + (int64_t)t * g.o;
   int sum = 0;
   if ((g.o & 15) == 0 && ((uintptr_t)q2 & 15) == 0) {
     // 64 channels (four loads in flight) per step, then 16 at a time
@@ -746,7 +751,7 @@ struct ConvXLoader {
     const uint32_t npad = (uint32_t)g.npad;
     const uint32_t pix = (uint32_t)m / npad, slot = (uint32_t)m - pix * npad;
     if (slot >= (uint32_t)g.n) return rw;
-    rw.base = q2 + (int64_t)slot * D;
+    rw.base = q2 + (int64_t)slot * g.o;  // pixel-major codes: slot offset inside each pixel
     rw.iy = (int)(pix / (uint32_t)g.w);
     rw.ix = (int)pix - rw.iy * g.w;
     rw.ok = true;
@@ -777,7 +782,7 @@ struct ConvXLoader {
     } else if (!tap_hits(g, rw.iy, rw.ix, ks.r, ks.s, y, x)) {
       return c;
     }
-    const uint4 v = *reinterpret_cast<const uint4*>(rw.base + ((int64_t)y * g.wo + x) * g.o + ks.o0);
+    const uint4 v = *reinterpret_cast<const uint4*>(rw.base + ((int64_t)y * g.wo + x) * g.n * g.o + ks.o0);
     c.w[0] = v.x;
     c.w[1] = v.y;
     c.w[2] = v.z;
@@ -815,7 +820,7 @@ struct ConvXLoader1 {
     for (int r = 0; r < g.kh; ++r)
       for (int s = 0; s < g.kw; ++s)
         if (yc - r >= 0 && yc - r < g.ho && xc - s >= 0 && xc - s < g.wo) mask |= 1u << (r * g.kw + s);
-    rw.off = (int64_t)slot * D + ((int64_t)yc * g.wo + xc) * g.o;
+    rw.off = (((int64_t)yc * g.wo + xc) * g.n + slot) * g.o;  // pixel-major codes
     rw.mask = mask;
     return rw;
   }
@@ -830,7 +835,7 @@ struct ConvXLoader1 {
     const int tap = kk / g.o;
     const int o0 = kk - tap * g.o;
     const int r = tap / g.kw, s = tap - r * g.kw;
-    ks.off = (int64_t)o0 - ((int64_t)r * g.wo + s) * g.o;
+    ks.off = (int64_t)o0 - ((int64_t)r * g.wo + s) * g.n * g.o;
     ks.tap = tap;
     return ks;
   }

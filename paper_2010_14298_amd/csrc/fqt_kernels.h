@@ -187,6 +187,8 @@ struct QuantParams {
   const float* zero;
   int8_t* q_nat;       // [rows, cols] slot order, or nullptr (packed: [rows, cols / 2] bytes)
   int packed;          // natural codes of bits <= 4 stored two per byte (float4 rows only)
+  int64_t pm_o;        // > 0: natural codes pixel-major, column j of row (slot) i at
+                       // ((j / pm_o) rows + i) pm_o + j % pm_o (cols % pm_o == 0, pm_o % 4 == 0)
   int32_t* sum_nat;    // [rows] row sums, or nullptr
   int8_t* q_t;         // [cols, rows] slot order, or nullptr
   int32_t* sum_t;      // [cols] column sums, or nullptr

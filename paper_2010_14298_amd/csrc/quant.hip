@@ -825,6 +825,8 @@ __device__ __forceinline__ void quant_tile(const QuantParams& p, int64_t bx, int
 #pragma unroll
   for (int j = 0; j < 4; ++j)
     if (c0 + j < cols) colmask |= 0xFFu << (8 * j);
+  // pixel-major natural codes: this lane's four columns lie in one pixel of pm_o channels
+  const int64_t pm_lane = p.pm_o > 0 ? (c0 / p.pm_o) * rows * p.pm_o + c0 % p.pm_o : 0;
   int32_t rs4[4];                // per-lane partial row sums of the natural codes, 4 rows at a time
   uint32_t tq[4][4], tq2[4][4];  // transposed codes: [column][4 words of 16 slots]; rows past the end stay 0
 #pragma unroll
@@ -1004,7 +1006,7 @@ __device__ __forceinline__ void quant_tile(const QuantParams& p, int64_t bx, int
     if constexpr (!TRANS) {
       const uint32_t w = pack_top4(t[0], t[1], t[2], t[3]);
       if (p.q_nat && ok && lane_ok) {
-        int8_t* dst = p.q_nat + slot * cols + c0;
+        int8_t* dst = p.q_nat + (p.pm_o > 0 ? pm_lane + slot * p.pm_o : slot * cols + c0);
         if (VEC && p.packed) {
           // codes of at most 4 bits, two per byte: the nibble of column 2i is
           // the low half of byte i, the code stored as q + 8 in [0, 15]
@@ -1162,6 +1164,8 @@ static hipError_t launch_quant_k(const QuantParams& p, hipStream_t s) {
   if (p.packed && (!vec || p.bits > 4 || p.q_t)) return hipErrorInvalidValue;
   // one primary layout: natural (with an optional transposed Q_b1) or transposed
   if ((p.q_nat || p.sum_nat) && (p.q_t || p.sum_t)) return hipErrorInvalidValue;
+  if (p.pm_o < 0 || (p.pm_o > 0 && ((p.pm_o & 3) != 0 || p.cols % p.pm_o != 0 || p.packed || (p.cols & 3) != 0)))
+    return hipErrorInvalidValue;
   const bool trans = p.q_t || p.sum_t;
   if (p.shift && MODE != QM_ROW) return hipErrorInvalidValue;
   if (p.q2_t) {
