@@ -441,7 +441,7 @@ struct ConvWs {
   StatsSeg sx_seg, sw_seg, sg_seg;
   float *rmin, *rmax;
   int8_t *xq_t, *wq_t, *q2, *q1_t, *bw;
-  int32_t *swq, *sumB, *xs, *qs, *sumA_tap, *count_tap, *sg, *ct, *cnt;
+  int32_t *swq, *sumB, *xs, *qs, *sumA_tap, *count_tap, *sg, *rs, *ct, *cnt;
   float *sx, *zx, *sw, *zw, *sg1, *zg1, *sg2, *zg2;
   int32_t* perm;
   BhqWs bhq;
@@ -483,6 +483,7 @@ ConvWs carve_conv(Carver& c, const float* X, const float* W, const float* G, con
   w.sumA_tap = c.take<int32_t>((int64_t)g.o * taps);
   w.count_tap = c.take<int32_t>(taps);
   w.sg = c.take<int32_t>(N * howo);
+  w.rs = c.take<int32_t>(N * hw);
   w.ct = c.take<int32_t>(hw * g.c);
   w.cnt = c.take<int32_t>(hw);
   w.sx = c.take<float>(1);
@@ -1275,7 +1276,7 @@ fqt_status fqt_conv_backward_im2col(const float* X, const float* W, const float*
     return FQT_OK;
   }
   tr.begin(7);
-  FQT_TRY(launch_conv_gradx_prep(g, w.q2, w.swq, w.sg, w.ct, w.cnt, s));
+  FQT_TRY(launch_conv_gradx_prep(g, w.q2, w.swq, w.sg, w.rs, w.ct, w.cnt, s));
   GemmParams gx{};
   gx.B = w.wq_t;
   gx.M = hw * g.npad;
@@ -1299,7 +1300,7 @@ fqt_status fqt_conv_backward_im2col(const float* X, const float* W, const float*
     gx.slot = w.bhq.slot;
     gx.tbuf = w.tbuf;
     gx.ldt = g.c;
-    FQT_TRY(launch_conv_gradx(gx, EPI_BHQT, g, w.q2, w.sg, w.ct, w.cnt, s));
+    FQT_TRY(launch_conv_gradx(gx, EPI_BHQT, g, w.q2, w.rs, w.ct, w.cnt, s));
     InverseParams ip{};
     ip.T = w.tbuf;
     ip.ldt = g.c;
@@ -1316,7 +1317,7 @@ fqt_status fqt_conv_backward_im2col(const float* X, const float* W, const float*
     ip.obstride = 1;
     FQT_TRY(launch_bhq_inverse(ip, s));
   } else {
-    FQT_TRY(launch_conv_gradx(gx, bhq ? EPI_BHQ : EPI_ROW, g, w.q2, w.sg, w.ct, w.cnt, s));
+    FQT_TRY(launch_conv_gradx(gx, bhq ? EPI_BHQ : EPI_ROW, g, w.q2, w.rs, w.ct, w.cnt, s));
   }
   tr.end(7);
   return FQT_OK;

@@ -713,6 +713,23 @@ __device__ __forceinline__ bool tap_hits(const ConvGeom& g, int iy, int ix, int 
   return y < g.ho && x < g.wo;
 }
 
+// Row sums of the grad_X A rows: rs[pix][slot] = sum of S_G[pixel][slot]
+// over the output pixels whose taps reach input pixel pix (slot fastest,
+// so a wave reads consecutive words of each tap's S_G run)
+__global__ void conv_rs_kernel(ConvGeom g, const int32_t* sg, int32_t* rs) {
+  const uint32_t t = blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= (uint32_t)g.n * (uint32_t)(g.h * g.w)) return;
+  const uint32_t pix = t / (uint32_t)g.n, slot = t - pix * (uint32_t)g.n;
+  const int iy = (int)(pix / (uint32_t)g.w), ix = (int)pix - iy * g.w;
+  int sum = 0;
+  for (int r = 0; r < g.kh; ++r)
+    for (int s = 0; s < g.kw; ++s) {
+      int y, x;
+      if (tap_hits(g, iy, ix, r, s, y, x)) sum += sg[((int64_t)y * g.wo + x) * g.n + slot];
+    }
+  rs[t] = sum;
+}
+
 __global__ void conv_ct_kernel(ConvGeom g, const int32_t* swq, int32_t* ct, int32_t* cnt) {
   const int64_t hw = (int64_t)g.h * g.w;
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -885,7 +902,7 @@ struct KStageList {
 };
 
 template <int EPI, int KG, class XLoader>
-__global__ __launch_bounds__(256) void conv_gradx_kernel(GemmParams p, ConvGeom g, const int8_t* q2, const int32_t* sg,
+__global__ __launch_bounds__(256) void conv_gradx_kernel(GemmParams p, ConvGeom g, const int8_t* q2, const int32_t* rs,
                                                           const int32_t* ct, const int32_t* cnt) {
   using C = CfgConvX;
   constexpr int EP_BYTES = C::BM * C::BN * 4 + C::BM * (int)sizeof(ConvRowStage);
@@ -969,14 +986,7 @@ __global__ __launch_bounds__(256) void conv_gradx_kernel(GemmParams p, ConvGeom 
       const float s = p.rowwiseA ? p.scaleA[slot] : p.scaleA[0];
       const float z = p.rowwiseA ? p.zeroA[slot] : p.zeroA[0];
       q.kind = (EPI == EPI_BHQ) ? bhq_slot_kind(p.L, slot) : (EPI == EPI_BHQT ? (p.slot[slot].size > 1) : 0);
-      const int iy = (int)(pix / (uint32_t)g.w), ix = (int)pix - iy * g.w;
-      int rs = 0;
-      for (int r = 0; r < g.kh; ++r)
-        for (int s2 = 0; s2 < g.kw; ++s2) {
-          int y, x;
-          if (tap_hits(g, iy, ix, r, s2, y, x)) rs += sg[((int64_t)y * g.wo + x) * g.n + slot];
-        }
-      q.rterm = zW * (double)rs;
+      q.rterm = zW * (double)rs[(int64_t)pix * g.n + slot];
       q.dq = 1.0 / (double)s;
       q.hz = q.kind != 0 ? (double)p.halfA + (double)z : (double)z + (double)p.halfA * q.dq;
       q.orow = (int)((p.perm ? (int64_t)p.perm[slot] : (int64_t)slot) * ((int64_t)g.h * g.w) + pix);
@@ -1217,44 +1227,48 @@ hipError_t launch_conv_gradw_psq_reduce(const GemmParams& p, const ConvGeom& g, 
   return hipGetLastError();
 }
 
-hipError_t launch_conv_gradx_prep(const ConvGeom& g, const int8_t* q2, const int32_t* swq, int32_t* sg, int32_t* ct,
+hipError_t launch_conv_gradx_prep(const ConvGeom& g, const int8_t* q2, const int32_t* swq, int32_t* sg, int32_t* rs,
+                                  int32_t* ct,
                                   int32_t* cnt, hipStream_t s) {
   const int64_t n1 = (int64_t)g.n * g.ho * g.wo;
   if (n1 > 0x7FFFFFFF) return hipErrorInvalidValue;
   hipLaunchKernelGGL(conv_sg_kernel, dim3((unsigned)((n1 + 255) / 256)), dim3(256), 0, s, g, q2, sg);
+  const int64_t nr = (int64_t)g.n * g.h * g.w;
+  if (nr > 0x7FFFFFFF) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(conv_rs_kernel, dim3((unsigned)((nr + 255) / 256)), dim3(256), 0, s, g, (const int32_t*)sg, rs);
   const int64_t n2 = (int64_t)g.h * g.w * g.c;
   hipLaunchKernelGGL(conv_ct_kernel, dim3((unsigned)((n2 + 255) / 256)), dim3(256), 0, s, g, swq, ct, cnt);
   return hipGetLastError();
 }
 
 template <int EPI, int KG>
-static hipError_t launch_conv_gradx_t(const GemmParams& p, const ConvGeom& g, const int8_t* q2, const int32_t* sg,
+static hipError_t launch_conv_gradx_t(const GemmParams& p, const ConvGeom& g, const int8_t* q2, const int32_t* rs,
                                       const int32_t* ct, const int32_t* cnt, hipStream_t s) {
   const int64_t tiles = ((p.M + CfgConvX::BM - 1) / CfgConvX::BM) * ((p.N + CfgConvX::BN - 1) / CfgConvX::BN);
   if (tiles > 0x7FFFFFFF || p.M > 0x7FFFFFFF || g.npad % 64 != 0) return hipErrorInvalidValue;
   // q2 is a workspace carve (16-byte aligned); o % 16 == 0 keeps every chunk aligned
   if (g.stride == 1 && g.kh * g.kw <= 32)
     hipLaunchKernelGGL((conv_gradx_kernel<EPI, KG, ConvXLoader1>), dim3((unsigned)tiles), dim3(CfgConvX::THREADS), 0,
-                       s, p, g, q2, sg, ct, cnt);
+                       s, p, g, q2, rs, ct, cnt);
   else
     hipLaunchKernelGGL((conv_gradx_kernel<EPI, KG, ConvXLoader>), dim3((unsigned)tiles), dim3(CfgConvX::THREADS), 0,
-                       s, p, g, q2, sg, ct, cnt);
+                       s, p, g, q2, rs, ct, cnt);
   return hipGetLastError();
 }
 
-hipError_t launch_conv_gradx(const GemmParams& p, int epi, const ConvGeom& g, const int8_t* q2, const int32_t* sg,
+hipError_t launch_conv_gradx(const GemmParams& p, int epi, const ConvGeom& g, const int8_t* q2, const int32_t* rs,
                              const int32_t* ct, const int32_t* cnt, hipStream_t s) {
-  if (epi == EPI_ROW) return launch_conv_gradx_t<EPI_ROW, 0>(p, g, q2, sg, ct, cnt, s);
+  if (epi == EPI_ROW) return launch_conv_gradx_t<EPI_ROW, 0>(p, g, q2, rs, ct, cnt, s);
   if (epi == EPI_BHQT)
-    return p.slot && p.tbuf ? launch_conv_gradx_t<EPI_BHQT, 0>(p, g, q2, sg, ct, cnt, s) : hipErrorInvalidValue;
+    return p.slot && p.tbuf ? launch_conv_gradx_t<EPI_BHQT, 0>(p, g, q2, rs, ct, cnt, s) : hipErrorInvalidValue;
   switch (p.L.k) {
-    case 1: return launch_conv_gradx_t<EPI_BHQ, 1>(p, g, q2, sg, ct, cnt, s);
-    case 2: return launch_conv_gradx_t<EPI_BHQ, 2>(p, g, q2, sg, ct, cnt, s);
-    case 4: return launch_conv_gradx_t<EPI_BHQ, 4>(p, g, q2, sg, ct, cnt, s);
-    case 8: return launch_conv_gradx_t<EPI_BHQ, 8>(p, g, q2, sg, ct, cnt, s);
-    case 16: return launch_conv_gradx_t<EPI_BHQ, 16>(p, g, q2, sg, ct, cnt, s);
-    case 32: return launch_conv_gradx_t<EPI_BHQ, 32>(p, g, q2, sg, ct, cnt, s);
-    case 64: return launch_conv_gradx_t<EPI_BHQ, 64>(p, g, q2, sg, ct, cnt, s);
+    case 1: return launch_conv_gradx_t<EPI_BHQ, 1>(p, g, q2, rs, ct, cnt, s);
+    case 2: return launch_conv_gradx_t<EPI_BHQ, 2>(p, g, q2, rs, ct, cnt, s);
+    case 4: return launch_conv_gradx_t<EPI_BHQ, 4>(p, g, q2, rs, ct, cnt, s);
+    case 8: return launch_conv_gradx_t<EPI_BHQ, 8>(p, g, q2, rs, ct, cnt, s);
+    case 16: return launch_conv_gradx_t<EPI_BHQ, 16>(p, g, q2, rs, ct, cnt, s);
+    case 32: return launch_conv_gradx_t<EPI_BHQ, 32>(p, g, q2, rs, ct, cnt, s);
+    case 64: return launch_conv_gradx_t<EPI_BHQ, 64>(p, g, q2, rs, ct, cnt, s);
     default: return hipErrorInvalidValue;
   }
 }

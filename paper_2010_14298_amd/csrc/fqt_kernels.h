@@ -374,9 +374,10 @@ hipError_t launch_conv_psq_sums(const ConvGeom& g, const float* scale, const flo
                                 int32_t* count_tap, hipStream_t s);
 hipError_t launch_conv_gradw_psq_reduce(const GemmParams& p, const ConvGeom& g, const ConvPsqSums& ps,
                                         const int32_t* count_tap, hipStream_t s);
-hipError_t launch_conv_gradx_prep(const ConvGeom& g, const int8_t* q2, const int32_t* swq, int32_t* sg, int32_t* ct,
+hipError_t launch_conv_gradx_prep(const ConvGeom& g, const int8_t* q2, const int32_t* swq, int32_t* sg, int32_t* rs,
+                                  int32_t* ct,
                                   int32_t* cnt, hipStream_t s);
-hipError_t launch_conv_gradx(const GemmParams& p, int epi, const ConvGeom& g, const int8_t* q2, const int32_t* sg,
+hipError_t launch_conv_gradx(const GemmParams& p, int epi, const ConvGeom& g, const int8_t* q2, const int32_t* rs,
                              const int32_t* ct, const int32_t* cnt, hipStream_t s);
 
 }  // namespace fqt
