@@ -7,14 +7,17 @@
 //            rows (BHQ: diag(d)^-1 H applied to each group of rows inside
 //            the tile, then rows scattered back to sample order)
 //
-// Both operands are K-contiguous (A [M, K], B [N, K]).  Two tile shapes:
-// 256 x 128 per block with 128 x 64 per wave (large problems), and
-// 128 x 128 with 64 x 64 per wave; 4 waves per block, K in steps of 64
-// bytes through double-buffered LDS.  Blocks are numbered so that each of
-// the 8 XCDs works on a contiguous run of output tiles (sharing A panels in
-// its L2).  Exact int32 accumulation over K-chunks of at most 65536 (|q| <=
-// 128, so 65536 * 2^14 < 2^31); longer K is split and the int32 partials
-// are summed in int64.
+// Both operands are K-contiguous (A [M, K], B [N, K]).  Three tile shapes
+// of 8 waves (gemm_core.h): 256 x 128 per block with 64 x 64 per wave and
+// three stage buffers (problems with at least 256 such tiles), 128 x 128
+// with 32 x 64 per wave and four buffers, and 64 x 128 for at most 64 rows.
+// The K loop moves 128-byte stages straight from HBM into LDS
+// (global_load_lds); a register-staged loop serves unaligned operands and
+// packed 4-bit A codes.  Blocks are numbered so that each of the 8 XCDs
+// works on a contiguous run of output tiles (sharing A panels in its L2);
+// split-K launches keep every tile of a split on one XCD.  Exact int32
+// accumulation over K-chunks of at most 65536 (|q| <= 128, so 65536 * 2^14 <
+// 2^31); longer K is split and the int32 partials are summed in int64.
 #include "gemm_core.h"
 
 namespace fqt {

@@ -1,11 +1,13 @@
 // Gradient / activation / weight quantizers of the FQT backward on gfx950.
 //
-//   stats      per-row and per-tensor min / max by wavefront shuffles and
-//              order-preserving atomics (exact in any order)
+//   stats      per-row and per-tensor min / max by wavefront shuffles; each
+//              block stores its partial, no atomics (min / max are exact in
+//              any order)
 //   finalize   PTQ scale s = B / R, zero z = min (Sec. 3.3); PSQ per row
 //              (Sec. 4.1)
 //   bhq plan   sort by row infinity norm, grouping and per-group scalars of
-//              the block Householder quantizer (Sec. 4.2, App. C.4, App. D)
+//              the block Householder quantizer (Sec. 4.2, App. C.4); the
+//              search over every number of groups of App. D is in plan.hip
 //   quant      one pass over the matrix: affine map or block Householder
 //              transform, stochastic rounding from a Philox stream, int8
 //              offset codes in natural and / or transposed layout with code
