@@ -13,14 +13,14 @@ stated order, which numpy evaluates without contraction.
 
 Determinism contract (shared by definition, not by code, with the GPU path):
 
-* stochastic rounding draws come from Philox4x32-10 (``philox.py``), keyed by
+* stochastic rounding draws come from Philox4x32-7 (``philox.py``), keyed by
   the seed, with the element's logical row-major index as counter;
 * per-tensor / per-sample / block-Householder scales and zero points are
   computed by the formulas in ``quantizers.py``;
 * integer accumulators are exact (int64 here).
 
 Modules:
-  philox      -- Philox4x32-10 counter-based generator (Salmon et al., SC'11)
+  philox      -- Philox4x32 counter-based generator (Salmon et al., SC'11), 7 rounds
   sr          -- stochastic rounding SR(.) of Sec. 3.3 and its exact moments
   quantizers  -- PTQ (Sec. 3.3), PSQ (Sec. 4.1), BHQ (Sec. 4.2, App. C.4, App. D)
   backward    -- linear / conv layer backward of Sec. 2.2 (Eq. linear-sq-backprop)

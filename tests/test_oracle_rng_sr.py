@@ -1,7 +1,9 @@
 """Pins for the oracle's random stream and stochastic rounding.
 
-* Philox4x32-10 against rocRAND's independent implementation (a different
-  code base built here from its installed header);
+* Philox4x32 against rocRAND's independent implementation (a different
+  code base built here from its installed header): its ten-round generator,
+  and seven of its rounds composed from its own round and key-bump functions
+  (the FQT stream's count);
 * statistical sanity of the 24-bit uniforms;
 * SR: exact round-up probability (Sec. 3.3), variance p(1-p) (App. C), and
   brute-force enumeration of every outcome on tiny inputs.
@@ -20,14 +22,23 @@ ROCRAND_HDR = "/opt/rocm/include/rocrand/rocrand_philox4x32_10.h"
 
 ROCRAND_PROBE = r"""
 #include <cstdio>
+// the round and key-bump helpers are private members; open them for this probe
+#define private public
 #include <rocrand/rocrand_philox4x32_10.h>
+#undef private
 struct Eng : rocrand_device::philox4x32_10_engine {
   uint4 run(uint4 c, uint2 k) { return ten_rounds(c, k); }
+  uint4 run7(uint4 c, uint2 k) {
+    for (int r = 0; r < 6; ++r) { c = single_round(c, k); k = bumpkey(k); }
+    return single_round(c, k);
+  }
 };
-int main() {
+int main(int argc, char**) {
   Eng eng; unsigned c[4], k[2];
   while (scanf("%u %u %u %u %u %u", &c[0], &c[1], &c[2], &c[3], &k[0], &k[1]) == 6) {
-    uint4 r = eng.run(uint4{c[0], c[1], c[2], c[3]}, uint2{k[0], k[1]});
+    const uint4 ci{c[0], c[1], c[2], c[3]};
+    const uint2 ki{k[0], k[1]};
+    uint4 r = argc > 1 ? eng.run7(ci, ki) : eng.run(ci, ki);
     printf("%u %u %u %u\n", r.x, r.y, r.z, r.w);
   }
 }
@@ -47,11 +58,13 @@ def test_philox_matches_rocrand(tmp_path):
     cases[0] = 0
     cases[1] = 2 ** 32 - 1
     inp = "\n".join(" ".join(str(int(v)) for v in row) for row in cases) + "\n"
-    out = subprocess.run([str(exe)], input=inp, capture_output=True, text=True, check=True).stdout
-    ref = np.array([[int(t) for t in line.split()] for line in out.strip().splitlines()], dtype=np.uint64)
-    got = np.stack(philox.philox4x32(cases[:, 0], cases[:, 1], cases[:, 2], cases[:, 3],
-                                      cases[:, 4], cases[:, 5]), axis=1)
-    np.testing.assert_array_equal(got, ref)
+    for rounds, args in ((10, []), (7, ["7"])):
+        out = subprocess.run([str(exe)] + args, input=inp, capture_output=True, text=True, check=True).stdout
+        ref = np.array([[int(t) for t in line.split()] for line in out.strip().splitlines()], dtype=np.uint64)
+        got = np.stack(philox.philox4x32(cases[:, 0], cases[:, 1], cases[:, 2], cases[:, 3],
+                                          cases[:, 4], cases[:, 5], rounds=rounds), axis=1)
+        np.testing.assert_array_equal(got, ref)
+    assert philox.ROUNDS == 7
 
 
 def test_draw_counter_mapping():
