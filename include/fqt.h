@@ -28,8 +28,9 @@
  *     overflows float32) are recorded in the workspace and returned by
  *     fqt_workspace_status(); outputs are then unspecified.
  *   - Stochastic rounding draw for logical element e (row-major index in the
- *     quantized matrix) = Philox4x32-10 with key = seed, counter =
- *     (e >> 2, stream, 0), word e & 3; its low 24 bits are the uniform.
+ *     quantized matrix) = Philox4x32-7 (Salmon et al., SC'11, seven rounds)
+ *     with key = seed, counter = (e >> 2, stream, 0), word e & 3; its low
+ *     24 bits are the uniform.
  *     Results are a deterministic function of (inputs, seed, stream).
  *   - Codes are stored as int8 offset codes q = code - 2^(bits-1), where code
  *     in [0, 2^bits - 1] is the quantization bin of Sec. 3.3.

@@ -1,4 +1,4 @@
-// Device helpers shared by the FQT kernels: Philox4x32-10, stochastic
+// Device helpers shared by the FQT kernels: Philox4x32-7, stochastic
 // rounding, the scalars of a block Householder group.
 #pragma once
 
@@ -8,18 +8,22 @@
 namespace fqt {
 
 // ---------------------------------------------------------------------------
-// Philox4x32-10 (Salmon et al., SC'11): four 32-bit words from a 128-bit
-// counter under a 64-bit key.  Ten rounds; the key is advanced by the two
-// Weyl increments between rounds.
+// Philox4x32 (Salmon et al., SC'11): four 32-bit words from a 128-bit
+// counter under a 64-bit key; the key is advanced by the two Weyl increments
+// between rounds.  The stochastic-rounding stream takes seven rounds (the
+// family's count from which its authors' test batteries pass; ten is their
+// safety margin).
 // ---------------------------------------------------------------------------
 struct u32x4 {
   uint32_t x, y, z, w;
 };
 
-__device__ __forceinline__ u32x4 philox10(uint32_t c0, uint32_t c1, uint32_t c2, uint32_t c3, uint32_t k0,
-                                          uint32_t k1) {
+constexpr int PHILOX_ROUNDS = 7;
+
+__device__ __forceinline__ u32x4 philox_rounds(uint32_t c0, uint32_t c1, uint32_t c2, uint32_t c3, uint32_t k0,
+                                               uint32_t k1) {
 #pragma unroll
-  for (int r = 0; r < 10; ++r) {
+  for (int r = 0; r < PHILOX_ROUNDS; ++r) {
     const uint64_t p0 = (uint64_t)0xD2511F53u * c0;
     const uint64_t p1 = (uint64_t)0xCD9E8D57u * c2;
     // three-way xors in one gfx950 bitop3 each (truth table 0x96)
@@ -39,7 +43,7 @@ __device__ __forceinline__ u32x4 philox10(uint32_t c0, uint32_t c1, uint32_t c2,
 // e..e+3 in order).
 __device__ __forceinline__ u32x4 philox_block(uint64_t e, uint64_t seed, uint32_t stream) {
   const uint64_t blk = e >> 2;
-  return philox10((uint32_t)blk, (uint32_t)(blk >> 32), stream, 0u, (uint32_t)seed, (uint32_t)(seed >> 32));
+  return philox_rounds((uint32_t)blk, (uint32_t)(blk >> 32), stream, 0u, (uint32_t)seed, (uint32_t)(seed >> 32));
 }
 
 __device__ __forceinline__ uint32_t philox_word(const u32x4& o, int i) {
