@@ -102,9 +102,9 @@ fqt_status plan_bhq(const BhqWs& b, const float* rmin, const float* rmax, int64_
   int32_t* goff = group_off ? group_off : b.group_off;
   int32_t* ng = num_groups ? num_groups : b.num_groups;
   if (!b.general) {
+    // the aligned layout's group count is known here: stored only when asked for
     const BhqLayout L = bhq_layout(rows, block_size);
-    FQT_TRY(launch_bhq_plan(rmin, rmax, L, bits, b.plan, perm, scale, zero, goff, fin, s));
-    FQT_TRY(launch_store_i32(ng, (int32_t)L.G, s));
+    FQT_TRY(launch_bhq_plan(rmin, rmax, L, bits, b.plan, perm, scale, zero, goff, num_groups, fin, s));
     return FQT_OK;
   }
   FQT_TRY(launch_bhq_sort(rmin, rmax, rows, b.plan, b.appd.sigma, fin, s));

@@ -109,11 +109,9 @@ BhqPlanWs bhq_plan_carve(void* plan_ws, int64_t rows);
 // row ranges rmin / rmax were stored by the statistics kernel); nullptr when
 // the finalize kernel already ran.
 hipError_t launch_bhq_plan(const float* rmin, const float* rmax, const BhqLayout& L, int bits, void* plan_ws,
-                           int32_t* perm, float* scale, float* zero, int32_t* group_off, const FinalizePlan* fin,
+                           int32_t* perm, float* scale, float* zero, int32_t* group_off, int32_t* num_groups, const FinalizePlan* fin,
                            hipStream_t s);
 
-// One int32 stored on the stream (a device scalar known on the host).
-hipError_t launch_store_i32(int32_t* p, int32_t v, hipStream_t s);
 
 // Rows in sorted order (M descending, ties by row index), for the general
 // plans below; fin as for launch_bhq_plan.

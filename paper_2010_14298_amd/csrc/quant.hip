@@ -554,8 +554,9 @@ __device__ void bhq_group(const float* rmin, const float* rmax, const int32_t* s
 template <bool FROM_PERM>
 __global__ __launch_bounds__(64) void bhq_groups_kernel(const float* rmin, const float* rmax, const int32_t* sigma,
                                                         BhqLayout L, int B, int32_t* perm, float* scale, float* zero,
-                                                        int32_t* group_off) {
+                                                        int32_t* group_off, int32_t* num_groups) {
   bhq_group<FROM_PERM>(rmin, rmax, sigma, L, B, blockIdx.x, perm, scale, zero, group_off);
+  if (num_groups && blockIdx.x == 0 && threadIdx.x == 0) *num_groups = (int32_t)L.G;
 }
 
 BhqPlanWs bhq_plan_carve(void* plan_ws, int64_t rows) {
@@ -569,8 +570,8 @@ BhqPlanWs bhq_plan_carve(void* plan_ws, int64_t rows) {
 }
 
 hipError_t launch_bhq_plan(const float* rmin, const float* rmax, const BhqLayout& L, int bits, void* plan_ws,
-                           int32_t* perm, float* scale, float* zero, int32_t* group_off, const FinalizePlan* fin,
-                           hipStream_t s) {
+                           int32_t* perm, float* scale, float* zero, int32_t* group_off, int32_t* num_groups,
+                           const FinalizePlan* fin, hipStream_t s) {
   const int64_t rows = L.rows;
   const int64_t np = sort_pad(rows);
   const int64_t nch = np / SORT_CH;
@@ -584,7 +585,7 @@ hipError_t launch_bhq_plan(const float* rmin, const float* rmax, const BhqLayout
     hipLaunchKernelGGL(bhq_rank_perm_kernel, dim3((unsigned)(nrank + (fin ? fin->nseg : 0))), dim3(RK_THREADS), lds,
                        s, rmin, rmax, L, perm, nrank, fin ? *fin : none);
     hipLaunchKernelGGL(bhq_groups_kernel<true>, dim3((unsigned)L.G), dim3(64), 0, s, rmin, rmax, w.sigma, L,
-                       (1 << bits) - 1, perm, scale, zero, group_off);
+                       (1 << bits) - 1, perm, scale, zero, group_off, num_groups);
     return hipGetLastError();
   }
   // w.rank must be zero before the rank kernel: the finalize step clears it,
@@ -595,14 +596,7 @@ hipError_t launch_bhq_plan(const float* rmin, const float* rmax, const BhqLayout
   hipLaunchKernelGGL(bhq_scatter_kernel, dim3((unsigned)((rows + 255) / 256)), dim3(256), 0, s, w.rank, rows,
                      w.sigma);
   hipLaunchKernelGGL(bhq_groups_kernel<false>, dim3((unsigned)L.G), dim3(64), 0, s, rmin, rmax, w.sigma, L,
-                     (1 << bits) - 1, perm, scale, zero, group_off);
-  return hipGetLastError();
-}
-
-__global__ void store_i32_kernel(int32_t* p, int32_t v) { *p = v; }
-
-hipError_t launch_store_i32(int32_t* p, int32_t v, hipStream_t s) {
-  hipLaunchKernelGGL(store_i32_kernel, dim3(1), dim3(1), 0, s, p, v);
+                     (1 << bits) - 1, perm, scale, zero, group_off, num_groups);
   return hipGetLastError();
 }
 
