@@ -37,7 +37,9 @@ def parse():
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=50)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--no-chain", action="store_true", help="skip the multi-layer chain measurement")
+    ap.add_argument("--no-chain", action="store_true", help="skip every leg beyond the layer backward")
+    ap.add_argument("--legs", default="chain,shift,bf6,conv,resnet,seeds",
+                    help="comma list of the legs beyond the layer backward (chain, shift, bf6, conv, resnet, seeds)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="after timing, run a plain 256 MiB elementwise pass (traffic-counter calibration)")
     return ap.parse_args()
@@ -487,13 +489,19 @@ def main():
         "kernels": per_kernel,
         "roofline": roof,
     }
-    if not args.no_chain:
+    legs = set() if args.no_chain else set(args.legs.split(","))
+    if "chain" in legs:
         out["chain"] = chain_bench(args, fqt, synth, torch)
+    if "shift" in legs:
         out["shift_gradW"] = shift_bench(args, fqt, torch, dX, dW, dG)
+    if "bf6" in legs:
         out["sub8bit_mfma"] = bf6_bench(args, fqt, torch)
+    if "conv" in legs:
         out["conv_layer"] = conv_bench(args, fqt, synth, torch)
         out["conv_layer_per_sample_b1"] = conv_bench(args, fqt, synth, torch, qb_w=("psq", 8, 0))
+    if "resnet" in legs:
         out["resnet50_batch256"] = resnet_sweep(args, fqt, synth, torch)
+    if "seeds" in legs:
         out["seed_batch"] = seeds_bench(args, fqt, synth, torch)
     if args.copy_probe:
         # a plain elementwise pass: reads 256 MiB, writes 256 MiB
