@@ -47,6 +47,7 @@ def parse():
 
 TRAFFIC_FILE = os.path.join(os.path.dirname(os.path.abspath(__file__)), "profiles", "traffic_linear_ffn_bhq5.txt")
 COUNTER_FILE = os.path.join(os.path.dirname(os.path.abspath(__file__)), "profiles", "counters_linear_ffn_bhq5.json")
+SEEDS_COUNTER_FILE = os.path.join(os.path.dirname(os.path.abspath(__file__)), "profiles", "counters_seed_batch.json")
 # kernel of each phase in the rocprofv3 summaries (name prefixes)
 PHASE_KERNEL = {
     "quant_G": ("quant_fused_kernel<2, 64, 1>",),
@@ -72,17 +73,18 @@ def measured_traffic(phase):
     return None
 
 
-def measured_counters(phase):
-    """Counter summary of one kernel from the committed rocprofv3 passes, if they
-    were taken on the current kernel sources; else None."""
+def measured_counters(phase, path=COUNTER_FILE, parts=None):
+    """Counter summary of one kernel (a phase's, or the kernel whose name holds
+    every string of `parts`) from committed rocprofv3 passes, if they were taken
+    on the current kernel sources; else None."""
     try:
         from paper_2010_14298_amd import profiling
-        with open(COUNTER_FILE) as f:
+        with open(path) as f:
             t = json.load(f)
         if t.get("kernel_sources") != profiling.source_hash():
             return None
         for name, v in t["kernels"].items():
-            if all(part in name for part in PHASE_KERNEL[phase]):
+            if all(part in name for part in (parts or PHASE_KERNEL[phase])):
                 return v
     except (OSError, ValueError, KeyError):
         return None
@@ -322,7 +324,9 @@ def resnet_sweep(args, fqt, synth, torch):
 def seeds_bench(args, fqt, synth, torch):
     """The seed-batched quantizer on the 4096 x 4096 single-outlier gradient:
     1000 seeds per quantizer and width in one launch each (G read once, every
-    seed's codes drawn and summed per element), HIP events; draws per second."""
+    seed's codes drawn and summed per element), HIP events; draws per second,
+    and the vector-ALU busy share of each quantizer's launches from the
+    committed counter summary (all widths together)."""
     _, _, G = synth.linear_single_outlier(seed=0)
     dG = torch.from_numpy(G).cuda()
     S = 1000
@@ -343,6 +347,10 @@ def seeds_bench(args, fqt, synth, torch):
                 var = (out["sum_c2"].double() - s1 * s1 / S) / (S - 1)
                 r["sum_code_variance"] = round(float(var.sum()), 1)
             res[f"{kind}{bits}"] = r
+        mode = {"ptq": 0, "psq": 1, "bhq": 2}[kind]
+        cnt = measured_counters(None, SEEDS_COUNTER_FILE, (f"quant_seeds_kernel<{mode}, {k}>",))
+        if cnt and "VALUBusy" in cnt:
+            res[f"{kind}_valu_busy_pct"] = cnt["VALUBusy"]
     return {"workload": "4096 x 4096 gradient, N(0,1) with one row x 1000; 1000 seeds (keys 0..999) per "
                         "quantizer; PTQ / PSQ / BHQ block 64 at 4, 5, 6, 8 bits", "seeds": S, "runs": res}
 
