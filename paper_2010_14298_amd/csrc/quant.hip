@@ -710,6 +710,21 @@ __device__ __forceinline__ void quant_tile(const QuantParams& p, int64_t bx, int
   const int B = (1 << p.bits) - 1;
   const int half = 1 << (p.bits - 1);
   const bool lane_ok = c0 < cols;
+  // per-row tests as 32-bit counts from slot0, worked out once per wave: row
+  // r of the wave lies inside the matrix iff r < nok, in a full block
+  // Householder group iff r < nk1, in the partial group iff nk1 <= r < nk2
+  // (64-bit comparisons per row would go through vector compares and lane
+  // masks)
+  auto clamp16 = [](int64_t v) { return (int)(v < 0 ? 0 : (v > QT_ROWS_PER_WAVE ? QT_ROWS_PER_WAVE : v)); };
+  const int nok = clamp16(rows - slot0);
+  int nk1 = 0, nk2 = 0;
+  if constexpr (MODE == QM_BHQ && K != 0) {
+    const int64_t end1 = p.L.full * (int64_t)p.L.k;
+    nk1 = clamp16(end1 - slot0);
+    nk2 = clamp16(end1 + (p.L.part > 0 ? p.L.part : 0) - slot0);
+  }
+  // bhq_slot_kind of row r of the wave
+  auto kind_of = [&](int r) { return r < nk1 ? 1 : (r < nk2 ? 2 : 0); };
 
   __shared__ float s_part[4][QT_COLS];   // per-wave partial group sums (BHQ, K >= 16)
   __shared__ float s_v0[4][QT_COLS];     // v of a group's first slot (BHQ, K >= 16)
@@ -728,8 +743,7 @@ __device__ __forceinline__ void quant_tile(const QuantParams& p, int64_t bx, int
   float g[QT_ROWS_PER_WAVE][4];
 #pragma unroll
   for (int r = 0; r < QT_ROWS_PER_WAVE; ++r) {
-    const int64_t slot = slot0 + r;
-    const bool ok = slot < rows;
+    const bool ok = r < nok;
     const int32_t row = src_row(r);
     const float* xr = p.x + (int64_t)row * cols;
     if constexpr (VEC) {
@@ -780,9 +794,7 @@ __device__ __forceinline__ void quant_tile(const QuantParams& p, int64_t bx, int
         }
 #pragma unroll
         for (int r = 0; r < QT_ROWS_PER_WAVE; ++r) {
-          const int64_t slot = slot0 + r;
-          const bool ok = slot < rows;
-          const bool multi = ok && bhq_slot_kind(L, slot) != 0;
+          const bool multi = kind_of(r) != 0;
           const float d = row_scale(r);
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
@@ -822,7 +834,10 @@ __device__ __forceinline__ void quant_tile(const QuantParams& p, int64_t bx, int
   for (int j = 0; j < 4; ++j)
     if (c0 + j < cols) colmask |= 0xFFu << (8 * j);
   // pixel-major natural codes: this lane's four columns lie in one pixel of pm_o channels
-  const int64_t pm_lane = p.pm_o > 0 ? (c0 / p.pm_o) * rows * p.pm_o + c0 % p.pm_o : 0;
+  // natural codes of row r go to nat0 + r * nat_step (bytes; with packed
+  // codes to nat0 / 2 + r * nat_step / 2, cols % 4 == 0)
+  const int64_t nat0 = p.pm_o > 0 ? (c0 / p.pm_o) * rows * p.pm_o + c0 % p.pm_o + slot0 * p.pm_o : slot0 * cols + c0;
+  const int64_t nat_step = p.pm_o > 0 ? p.pm_o : cols;
   int32_t rs4[4];                // per-lane partial row sums of the natural codes, 4 rows at a time
   uint32_t tq[4][4], tq2[4][4];  // transposed codes: [column][4 words of 16 slots]; rows past the end stay 0
 #pragma unroll
@@ -847,7 +862,7 @@ __device__ __forceinline__ void quant_tile(const QuantParams& p, int64_t bx, int
 #pragma unroll
   for (int r = 0; r < QT_ROWS_PER_WAVE; ++r) {
     const int64_t slot = slot0 + r;
-    const bool ok = slot < rows;
+    const bool ok = r < nok;
     float y[4];
     if constexpr (MODE == QM_TENSOR) {
 #pragma unroll
@@ -891,22 +906,19 @@ __device__ __forceinline__ void quant_tile(const QuantParams& p, int64_t bx, int
       }
     } else {
       const BhqLayout& L = p.L;
-      const int kind = ok ? bhq_slot_kind(L, slot) : 0;
+      const int kind = kind_of(r);
       const float d = row_scale(r);
       const float c = row_zero(r);
       if constexpr (K > 1 && K < 16) {
         // groups of K rows inside this wave: their sums from the registers
         if (r % K == 0) {
-          const int64_t gfirst = slot;
-          const int gkind = (gfirst < rows) ? bhq_slot_kind(L, gfirst) : 0;
+          const int gkind = kind_of(r);
           const float alpha = gkind == 2 ? L.a_p : L.a_k;
           const float oma = gkind == 2 ? L.oma_p : L.oma_k;
           float S[4] = {0.0f, 0.0f, 0.0f, 0.0f}, v0[4];
 #pragma unroll
           for (int rr = 0; rr < K; ++rr) {
-            const int64_t sl = slot + rr;
-            const bool okr = sl < rows;
-            const bool multi = okr && bhq_slot_kind(L, sl) != 0;
+            const bool multi = kind_of(r + rr) != 0;
             const float dr = row_scale(r + rr);
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
@@ -924,16 +936,22 @@ __device__ __forceinline__ void quant_tile(const QuantParams& p, int64_t bx, int
           }
         }
       }
-      const bool first = (K > 1) && ((slot % (K > 1 ? K : 1)) == 0);
+      // one branch per row (the test is the same for the four columns)
+      if (K > 1 && kind != 0) {
+        // slot0 is a multiple of 16, so a group of K >= 16 starts at row 0
+        // of a wave
+        const bool first = K >= 16 ? (r == 0 && (wave * QT_ROWS_PER_WAVE) % (K > 1 ? K : 1) == 0)
+                                   : (r % (K > 1 ? K : 1) == 0);
+        if (first) {
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        if (K > 1 && kind != 0) {
-          const float v = d * g[r][j];
-          const float Y = first ? v + tb[j] : v - ta[j];
-          y[j] = Y - c;
+          for (int j = 0; j < 4; ++j) y[j] = (d * g[r][j] + tb[j]) - c;
         } else {
-          y[j] = d * (g[r][j] - c);
+#pragma unroll
+          for (int j = 0; j < 4; ++j) y[j] = (d * g[r][j] - ta[j]) - c;
         }
+      } else {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) y[j] = d * (g[r][j] - c);
       }
     }
     const uint64_t e0 = (uint64_t)(uint32_t)src_row(r) * (uint64_t)cols + (uint64_t)c0;
@@ -1002,14 +1020,14 @@ __device__ __forceinline__ void quant_tile(const QuantParams& p, int64_t bx, int
     if constexpr (!TRANS) {
       const uint32_t w = pack_top4(t[0], t[1], t[2], t[3]);
       if (p.q_nat && ok && lane_ok) {
-        int8_t* dst = p.q_nat + (p.pm_o > 0 ? pm_lane + slot * p.pm_o : slot * cols + c0);
+        int8_t* dst = p.q_nat + nat0 + r * nat_step;
         if (VEC && p.packed) {
           // codes of at most 4 bits, two per byte: the nibble of column 2i is
           // the low half of byte i, the code stored as q + 8 in [0, 15]
           const uint32_t nb = (w ^ 0x08080808u) & 0x0F0F0F0Fu;
           const uint32_t x2 = nb | (nb >> 4);
           const uint32_t pk = __builtin_amdgcn_perm(0u, x2, 0x0c0c0200u);  // bytes 0 and 2 of x2
-          *reinterpret_cast<uint16_t*>(p.q_nat + (slot * cols + c0) / 2) = (uint16_t)pk;
+          *reinterpret_cast<uint16_t*>(p.q_nat + nat0 / 2 + r * (nat_step / 2)) = (uint16_t)pk;
         } else if constexpr (VEC) {
           *reinterpret_cast<uint32_t*>(dst) = w;
         } else {
@@ -1022,8 +1040,8 @@ __device__ __forceinline__ void quant_tile(const QuantParams& p, int64_t bx, int
       // row sums of the natural codes: one exchange tree per 4 rows
       if ((r & 3) == 3 && p.sum_nat) {
         const int32_t t = wave_sum4(rs4, lane);
-        const int64_t sl = slot0 + (r - 3) + (lane >> 4);
-        if ((lane & 15) == 0 && sl < rows) atomicAdd(p.sum_nat + sl, t);
+        const int rl = (r - 3) + (lane >> 4);
+        if ((lane & 15) == 0 && rl < nok) atomicAdd(p.sum_nat + slot0 + rl, t);
       }
     } else if (ok) {
 #pragma unroll
@@ -1032,7 +1050,7 @@ __device__ __forceinline__ void quant_tile(const QuantParams& p, int64_t bx, int
   }
 
   // ---- transposed stores: 16 consecutive slots per column
-  const bool tvec = ((rows & 15) == 0) && (slot0 + 15 < rows);
+  const bool tvec = ((rows & 15) == 0) && nok == QT_ROWS_PER_WAVE;
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const int64_t col = c0 + j;
@@ -1044,7 +1062,7 @@ __device__ __forceinline__ void quant_tile(const QuantParams& p, int64_t bx, int
       } else {
 #pragma unroll
         for (int r = 0; r < QT_ROWS_PER_WAVE; ++r)
-          if (slot0 + r < rows) dst[r] = (int8_t)((tq[j][r >> 2] >> (8 * (r & 3))) & 255);
+          if (r < nok) dst[r] = (int8_t)((tq[j][r >> 2] >> (8 * (r & 3))) & 255);
       }
     }
     if constexpr (H2 != 0) {
@@ -1054,7 +1072,7 @@ __device__ __forceinline__ void quant_tile(const QuantParams& p, int64_t bx, int
       } else {
 #pragma unroll
         for (int r = 0; r < QT_ROWS_PER_WAVE; ++r)
-          if (slot0 + r < rows) dst[r] = (int8_t)((tq2[j][r >> 2] >> (8 * (r & 3))) & 255);
+          if (r < nok) dst[r] = (int8_t)((tq2[j][r >> 2] >> (8 * (r & 3))) & 255);
       }
     }
   }
