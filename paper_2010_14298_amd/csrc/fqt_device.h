@@ -41,9 +41,11 @@ __device__ __forceinline__ u32x4 philox_rounds(uint32_t c0, uint32_t c1, uint32_
 
 // Philox block holding logical element e (e multiple of 4 gives words for
 // e..e+3 in order).
-__device__ __forceinline__ u32x4 philox_block(uint64_t e, uint64_t seed, uint32_t stream) {
-  const uint64_t blk = e >> 2;
+__device__ __forceinline__ u32x4 philox_of_block(uint64_t blk, uint64_t seed, uint32_t stream) {
   return philox_rounds((uint32_t)blk, (uint32_t)(blk >> 32), stream, 0u, (uint32_t)seed, (uint32_t)(seed >> 32));
+}
+__device__ __forceinline__ u32x4 philox_block(uint64_t e, uint64_t seed, uint32_t stream) {
+  return philox_of_block(e >> 2, seed, stream);
 }
 
 __device__ __forceinline__ uint32_t philox_word(const u32x4& o, int i) {

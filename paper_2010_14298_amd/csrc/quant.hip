@@ -634,13 +634,13 @@ constexpr int QT_ROWS_PER_WAVE = 16;
 
 // Offset codes of four consecutive columns of one row from transformed values
 // y, in the top-byte form of sr_top / rne_top: stochastic rounding with the
-// Philox block of element e0 (VEC: e0 % 4 == 0, one block for all four) or
-// round-half-even.
+// Philox blocks of elements e0 .. e0 + 3 (VEC: the argument is the block
+// index e0 / 4 of the one block that holds all four) or round-half-even.
 template <bool VEC>
 __device__ __forceinline__ void sr4(const float (&y)[4], uint64_t e0, uint64_t seed, uint32_t stream, float Bf,
                                     uint32_t hoff, int32_t (&t)[4]) {
   if constexpr (VEC) {
-    const u32x4 o = philox_block(e0, seed, stream);
+    const u32x4 o = philox_of_block(e0, seed, stream);
     t[0] = sr_top(y[0], o.x, Bf, hoff);
     t[1] = sr_top(y[1], o.y, Bf, hoff);
     t[2] = sr_top(y[2], o.z, Bf, hoff);
@@ -659,28 +659,25 @@ __device__ __forceinline__ void rne4(const float (&y)[4], float Bf, uint32_t hof
   for (int j = 0; j < 4; ++j) t[j] = rne_top(y[j], Bf, hoff);
 }
 
-// Sums over the 64 lanes of each of 4 per-lane values v[0..3], by halving
-// exchanges (lanes differing in bit 5 swap halves of the list, then bit 4),
-// then a plain tree over the low 4 lane bits: lane l with l % 16 == 0
-// returns the sum of v[l / 16].
-__device__ __forceinline__ int32_t wave_sum4(int32_t (&v)[4], int lane) {
-  // bitwise selects (one v_bfi each): a conditional between two list
-  // entries would be turned into a dynamically indexed register read
-  const int32_t m32 = (lane & 32) ? -1 : 0;
+// Sums over the 64 lanes of each of 4 per-lane values v[0..3], all in
+// vector registers: lanes 32 apart add up with one half-wave swap per pair
+// (v[i] keeps the low half, v[i + 2] the high one), rows of 16 lanes with
+// one row swap, then each row adds up by shifted adds within the row.  Lane
+// l with l % 16 == 15 returns the sum of v[l / 16].
+__device__ __forceinline__ int32_t wave_sum4(int32_t (&v)[4]) {
+  int32_t h[2];
 #pragma unroll
   for (int i = 0; i < 2; ++i) {
-    const int32_t keep = (v[i + 2] & m32) | (v[i] & ~m32);
-    const int32_t give = (v[i] & m32) | (v[i + 2] & ~m32);
-    v[i] = keep + __shfl_xor(give, 32);
+    const auto sw = __builtin_amdgcn_permlane32_swap(v[i], v[i + 2], false, false);
+    h[i] = (int32_t)sw[0] + (int32_t)sw[1];
   }
-  const int32_t m16 = (lane & 16) ? -1 : 0;
-  const int32_t keep = (v[1] & m16) | (v[0] & ~m16);
-  const int32_t give = (v[0] & m16) | (v[1] & ~m16);
-  int32_t s = keep + __shfl_xor(give, 16);
-  s += __shfl_xor(s, 8);
-  s += __shfl_xor(s, 4);
-  s += __shfl_xor(s, 2);
-  s += __shfl_xor(s, 1);
+  const auto sw = __builtin_amdgcn_permlane16_swap(h[0], h[1], false, false);
+  int32_t s = (int32_t)sw[0] + (int32_t)sw[1];
+  // row_shr:n (source lane l - n of the same row; 0 where that leaves the row)
+  s += __builtin_amdgcn_update_dpp(0, s, 0x111, 0xf, 0xf, false);
+  s += __builtin_amdgcn_update_dpp(0, s, 0x112, 0xf, 0xf, false);
+  s += __builtin_amdgcn_update_dpp(0, s, 0x114, 0xf, 0xf, false);
+  s += __builtin_amdgcn_update_dpp(0, s, 0x118, 0xf, 0xf, false);
   return s;
 }
 
@@ -954,7 +951,10 @@ __device__ __forceinline__ void quant_tile(const QuantParams& p, int64_t bx, int
         for (int j = 0; j < 4; ++j) y[j] = d * (g[r][j] - c);
       }
     }
-    const uint64_t e0 = (uint64_t)(uint32_t)src_row(r) * (uint64_t)cols + (uint64_t)c0;
+    // logical element index of the row's first column (VEC: its Philox
+    // block index, row * cols / 4 + c0 / 4 with cols % 4 == c0 % 4 == 0)
+    const uint64_t e0 = VEC ? (uint64_t)(uint32_t)src_row(r) * (uint64_t)(cols >> 2) + (uint64_t)(c0 >> 2)
+                            : (uint64_t)(uint32_t)src_row(r) * (uint64_t)cols + (uint64_t)c0;
     if constexpr (SD) {
       // seed batch: the same transformed values rounded under keys seed + b,
       // b < nseeds; per element the sum of the codes and of their squares
@@ -1039,9 +1039,9 @@ __device__ __forceinline__ void quant_tile(const QuantParams& p, int64_t bx, int
       rs4[r & 3] = sum4_i8(w & colmask, 0);
       // row sums of the natural codes: one exchange tree per 4 rows
       if ((r & 3) == 3 && p.sum_nat) {
-        const int32_t t = wave_sum4(rs4, lane);
+        const int32_t t = wave_sum4(rs4);
         const int rl = (r - 3) + (lane >> 4);
-        if ((lane & 15) == 0 && rl < nok) atomicAdd(p.sum_nat + slot0 + rl, t);
+        if ((lane & 15) == 15 && rl < nok) atomicAdd(p.sum_nat + slot0 + rl, t);
       }
     } else if (ok) {
 #pragma unroll
