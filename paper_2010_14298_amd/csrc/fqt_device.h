@@ -19,13 +19,16 @@ struct u32x4 {
 };
 
 constexpr int PHILOX_ROUNDS = 7;
+constexpr uint32_t PHILOX_M0 = 0xD2511F53u, PHILOX_M1 = 0xCD9E8D57u;  // round multipliers
+constexpr uint32_t PHILOX_W0 = 0x9E3779B9u, PHILOX_W1 = 0xBB67AE85u;  // key increments
 
+// n rounds from counter (c0, c1, c2, c3) under key (k0, k1).
 __device__ __forceinline__ u32x4 philox_rounds(uint32_t c0, uint32_t c1, uint32_t c2, uint32_t c3, uint32_t k0,
-                                               uint32_t k1) {
+                                               uint32_t k1, int n) {
 #pragma unroll
-  for (int r = 0; r < PHILOX_ROUNDS; ++r) {
-    const uint64_t p0 = (uint64_t)0xD2511F53u * c0;
-    const uint64_t p1 = (uint64_t)0xCD9E8D57u * c2;
+  for (int r = 0; r < n; ++r) {
+    const uint64_t p0 = (uint64_t)PHILOX_M0 * c0;
+    const uint64_t p1 = (uint64_t)PHILOX_M1 * c2;
     // three-way xors in one gfx950 bitop3 each (truth table 0x96)
     const uint32_t n0 = __builtin_amdgcn_bitop3_b32((uint32_t)(p1 >> 32), c1, k0, 0x96);
     const uint32_t n2 = __builtin_amdgcn_bitop3_b32((uint32_t)(p0 >> 32), c3, k1, 0x96);
@@ -33,16 +36,36 @@ __device__ __forceinline__ u32x4 philox_rounds(uint32_t c0, uint32_t c1, uint32_
     c3 = (uint32_t)p0;
     c0 = n0;
     c2 = n2;
-    k0 += 0x9E3779B9u;
-    k1 += 0xBB67AE85u;
+    k0 += PHILOX_W0;
+    k1 += PHILOX_W1;
   }
   return u32x4{c0, c1, c2, c3};
 }
 
-// Philox block holding logical element e (e multiple of 4 gives words for
-// e..e+3 in order).
+// The block with counter (blk low word, blk high word, stream, 0) under key
+// seed.  The first two rounds are written out: the stream and zero counter
+// words make round one's second product, and round two's second counter
+// word, the same in every lane, so those xors combine the uniform operands
+// first (one scalar op) and leave one vector op per word.
 __device__ __forceinline__ u32x4 philox_of_block(uint64_t blk, uint64_t seed, uint32_t stream) {
-  return philox_rounds((uint32_t)blk, (uint32_t)(blk >> 32), stream, 0u, (uint32_t)seed, (uint32_t)(seed >> 32));
+  uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
+  const uint64_t p0 = (uint64_t)PHILOX_M0 * (uint32_t)blk;
+  const uint64_t p1 = (uint64_t)PHILOX_M1 * stream;
+  uint32_t c0 = (uint32_t)(blk >> 32) ^ ((uint32_t)(p1 >> 32) ^ k0);
+  uint32_t c1 = (uint32_t)p1;
+  uint32_t c2 = (uint32_t)(p0 >> 32) ^ k1;  // counter word 3 is zero
+  uint32_t c3 = (uint32_t)p0;
+  k0 += PHILOX_W0;
+  k1 += PHILOX_W1;
+  const uint64_t q0 = (uint64_t)PHILOX_M0 * c0;
+  const uint64_t q1 = (uint64_t)PHILOX_M1 * c2;
+  const uint32_t n0 = (uint32_t)(q1 >> 32) ^ (c1 ^ k0);
+  const uint32_t n2 = __builtin_amdgcn_bitop3_b32((uint32_t)(q0 >> 32), c3, k1, 0x96);
+  c1 = (uint32_t)q1;
+  c3 = (uint32_t)q0;
+  k0 += PHILOX_W0;
+  k1 += PHILOX_W1;
+  return philox_rounds(n0, c1, n2, c3, k0, k1, PHILOX_ROUNDS - 2);
 }
 __device__ __forceinline__ u32x4 philox_block(uint64_t e, uint64_t seed, uint32_t stream) {
   return philox_of_block(e >> 2, seed, stream);

@@ -953,8 +953,16 @@ __device__ __forceinline__ void quant_tile(const QuantParams& p, int64_t bx, int
     }
     // logical element index of the row's first column (VEC: its Philox
     // block index, row * cols / 4 + c0 / 4 with cols % 4 == c0 % 4 == 0)
-    const uint64_t e0 = VEC ? (uint64_t)(uint32_t)src_row(r) * (uint64_t)(cols >> 2) + (uint64_t)(c0 >> 2)
-                            : (uint64_t)(uint32_t)src_row(r) * (uint64_t)cols + (uint64_t)c0;
+    uint64_t e0;
+    if constexpr (VEC) {
+      // the row's product stays on the scalar unit; one 64-bit vector add
+      const uint64_t rb = (uint64_t)(uint32_t)src_row(r) * (uint64_t)(cols >> 2);
+      const uint32_t rlo = __builtin_amdgcn_readfirstlane((uint32_t)rb);
+      const uint32_t rhi = __builtin_amdgcn_readfirstlane((uint32_t)(rb >> 32));
+      e0 = (((uint64_t)rhi << 32) | rlo) + (uint64_t)(c0 >> 2);
+    } else {
+      e0 = (uint64_t)(uint32_t)src_row(r) * (uint64_t)cols + (uint64_t)c0;
+    }
     if constexpr (SD) {
       // seed batch: the same transformed values rounded under keys seed + b,
       // b < nseeds; per element the sum of the codes and of their squares
