@@ -49,25 +49,28 @@ __global__ __launch_bounds__(256) void quant_narrow_t_kernel(NarrowQParams p) {
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int q = lane / LPR, cl = lane % LPR;
-  const int64_t r0 = (int64_t)blockIdx.x * (4 * RG * 16) + wave * (RG * 16) + q * 16;
+  // row indices in 32 bits: the launch checks that ldt, rows + blk (which
+  // bounds every source row) and cols stay below 2^31
+  const int blk = (int)p.blk;
+  const int r0 = (int)blockIdx.x * (4 * RG * 16) + wave * (RG * 16) + q * 16;
   const int64_t c0 = (int64_t)blockIdx.y * (LPR * 4) + (int64_t)cl * 4;  // column chunks of 4 * LPR
   const int B = (1 << p.bits) - 1;
   const int half = 1 << (p.bits - 1);
   const float s0 = p.scale[0], z0 = p.zero[0];
-  const int64_t vblk = p.vblk > 0 ? p.vblk : p.blk;
+  const int vblk = p.vblk > 0 ? (int)p.vblk : blk;
   // VEC: cols % 4 == 0, so a lane's four columns are all inside or all past the end
   const bool full = VEC && c0 < p.cols;
   // Rows r0 .. r0 + 15: row (bq, br) reads row br of source block perm[bq]
   // (or bq) of vblk rows.  TWO (blk >= 16): the 16 rows lie in blocks bq0
   // and bq0 + 1, whose source blocks and scales are read once up front.
-  const int64_t bq0 = r0 / p.blk, br0 = r0 - bq0 * p.blk;
-  int64_t sbA = 0, sbB = 0;
+  const int bq0 = r0 / blk, br0 = r0 - bq0 * blk;
+  int sbA = 0, sbB = 0;
   float sA = s0, zA = z0, sB = s0, zB = z0;
   if constexpr (TWO) {
-    const int64_t nblk = (p.rows + p.blk - 1) / p.blk;
-    const int64_t qa = bq0 < nblk ? bq0 : nblk - 1, qb = bq0 + 1 < nblk ? bq0 + 1 : nblk - 1;
-    sbA = p.perm ? (int64_t)p.perm[qa] : qa;
-    sbB = p.perm ? (int64_t)p.perm[qb] : qb;
+    const int nblk = (int)((p.rows + p.blk - 1) / p.blk);
+    const int qa = bq0 < nblk ? bq0 : nblk - 1, qb = bq0 + 1 < nblk ? bq0 + 1 : nblk - 1;
+    sbA = p.perm ? p.perm[qa] : qa;
+    sbB = p.perm ? p.perm[qb] : qb;
     if (p.rowscale) {
       sA = p.scale[sbA];
       zA = p.zero[sbA];
@@ -78,40 +81,47 @@ __global__ __launch_bounds__(256) void quant_narrow_t_kernel(NarrowQParams p) {
   // 2-D blocks: (y, x) of offset br0 once; the 16 rows then step x (gw >= 16
   // and blocks of at least 128 rows: at most one row wrap, at most one block
   // boundary, after which (y, x) = (0, br))
-  const int64_t gy0 = p.gw > 0 ? br0 / p.gw : 0, gx0 = p.gw > 0 ? br0 - gy0 * p.gw : 0;
-  const int64_t vb = p.gw > 0 ? p.gho * p.gwo : vblk;  // source rows per block
+  const int gw = (int)p.gw, gwo = (int)p.gwo, gho = (int)p.gho;
+  const int gy0 = gw > 0 ? br0 / gw : 0, gx0 = gw > 0 ? br0 - gy0 * gw : 0;
+  const int vb = gw > 0 ? gho * gwo : vblk;  // source rows per block
+  const int rows = (int)p.rows;
   // source row, scale and zero of row r (row r of the 16 has offset br0 + r)
-  auto locate = [&](int r, int64_t& src, float& s, float& z) -> bool {
-    int64_t bq = bq0, br = br0 + r;
-    const bool wrapped = br >= p.blk;
-    if (wrapped) {  // at most one block boundary for TWO; stepped for small blocks
-      const int64_t d = br / p.blk;
-      bq += d;
-      br -= d * p.blk;
+  auto locate = [&](int r, int& src, float& s, float& z) -> bool {
+    int bq = bq0, br = br0 + r;
+    const bool wrapped = br >= blk;
+    if (wrapped) {
+      if constexpr (TWO) {  // blk >= 16: at most one block boundary
+        bq += 1;
+        br -= blk;
+      } else {  // small blocks: stepped
+        const int d = br / blk;
+        bq += d;
+        br -= d * blk;
+      }
     }
     bool inside;
-    int64_t srow;
-    if (p.gw > 0) {
-      int64_t y = wrapped ? 0 : gy0, x = wrapped ? br : gx0 + r;
-      if (x >= p.gw) {
-        x -= p.gw;
+    int srow;
+    if (gw > 0) {
+      int y = wrapped ? 0 : gy0, x = wrapped ? br : gx0 + r;
+      if (x >= gw) {
+        x -= gw;
         ++y;
       }
-      inside = y < p.gho && x < p.gwo;
-      srow = y * p.gwo + x;
+      inside = y < gho && x < gwo;
+      srow = y * gwo + x;
     } else {
       inside = br < vblk;
       srow = br;
     }
-    const bool ok = r0 + r < p.rows && inside;
-    int64_t sb;
+    const bool ok = r0 + r < rows && inside;
+    int sb;
     if constexpr (TWO) {
       const bool inb = bq != bq0;
       sb = inb ? sbB : sbA;
       s = inb ? sB : sA;
       z = inb ? zB : zA;
     } else {
-      sb = ok ? (p.perm ? (int64_t)p.perm[bq] : bq) : 0;
+      sb = ok ? (p.perm ? p.perm[bq] : bq) : 0;
       s = (p.rowscale && ok) ? p.scale[sb] : s0;
       z = (p.rowscale && ok) ? p.zero[sb] : z0;
     }
@@ -120,39 +130,44 @@ __global__ __launch_bounds__(256) void quant_narrow_t_kernel(NarrowQParams p) {
   };
   // ---- phase 1: the 16 rows' loads, issued together (clamped addresses and
   // selects instead of branches around the loads).  Kept for phase 2: the
-  // source row (32 bits; -1 past the end) and, for TWO, a bit per row in
-  // block bq0 + 1.
+  // source row (-1 past the end) and, for TWO, a bit per row in block
+  // bq0 + 1.
   float g[16][4];
   int32_t src32[16];
   uint32_t inb_mask = 0u;
 #pragma unroll
   for (int r = 0; r < 16; ++r) {
-    int64_t src;
+    int src;
     float s, z;
     const bool ok = locate(r, src, s, z);
-    src32[r] = ok ? (int32_t)src : -1;
-    if (TWO && br0 + r >= p.blk) inb_mask |= 1u << r;
+    src32[r] = ok ? src : -1;
+    if (TWO && br0 + r >= blk) inb_mask |= 1u << r;
     if constexpr (VEC) {
       const bool in = ok && full;
-      const float4 v = *reinterpret_cast<const float4*>(p.x + (in ? src * p.cols + c0 : 0));
+      const float4 v = *reinterpret_cast<const float4*>(p.x + (in ? (uint64_t)(uint32_t)src * (uint64_t)p.cols + c0 : 0));
       g[r][0] = in ? v.x : 0.0f;
       g[r][1] = in ? v.y : 0.0f;
       g[r][2] = in ? v.z : 0.0f;
       g[r][3] = in ? v.w : 0.0f;
     } else {
 #pragma unroll
-      for (int j = 0; j < 4; ++j) g[r][j] = (ok && c0 + j < p.cols) ? p.x[src * p.cols + c0 + j] : 0.0f;
+      for (int j = 0; j < 4; ++j)
+        g[r][j] = (ok && c0 + j < p.cols) ? p.x[(int64_t)src * p.cols + c0 + j] : 0.0f;
     }
   }
-  // ---- phase 2: codes, transposed into words of four rows
+  // ---- phase 2: codes, transposed into words of four rows.  The float4
+  // path works in the top-byte form of sr_top / rne_top (offset codes packed
+  // by byte permutes); the other path rounds element by element.
   uint32_t tcodes[4][4];
 #pragma unroll
   for (int j = 0; j < 4; ++j)
 #pragma unroll
     for (int w = 0; w < 4; ++w) tcodes[j][w] = 0u;
+  const float Bf = (float)B;
+  const uint32_t hoff = (uint32_t)half << 24;
 #pragma unroll
   for (int r = 0; r < 16; ++r) {
-    int64_t src;
+    int src;
     float s, z;
     bool ok;
     if constexpr (TWO) {
@@ -164,31 +179,45 @@ __global__ __launch_bounds__(256) void quant_narrow_t_kernel(NarrowQParams p) {
     } else {
       ok = locate(r, src, s, z);
     }
-    int code[4];
-    const uint64_t ebase = (uint64_t)src * (uint64_t)p.cols + (uint64_t)c0;
-    if (p.stoch) {
-      if constexpr (VEC) {
-        const u32x4 o = philox_block(ebase, p.seed, p.stream);
-        code[0] = sr_code(s * (g[r][0] - z), o.x, B);
-        code[1] = sr_code(s * (g[r][1] - z), o.y, B);
-        code[2] = sr_code(s * (g[r][2] - z), o.z, B);
-        code[3] = sr_code(s * (g[r][3] - z), o.w, B);
+    if constexpr (VEC) {
+      float y[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) y[j] = s * (g[r][j] - z);
+      int32_t t[4];
+      if (p.stoch) {
+        // Philox block index src * cols / 4 + c0 / 4 (cols % 4 == c0 % 4 == 0)
+        const uint64_t pb = (uint64_t)(uint32_t)src * (uint64_t)(p.cols >> 2) + (uint64_t)(c0 >> 2);
+        const u32x4 o = philox_of_block(pb, p.seed, p.stream);
+        t[0] = sr_top(y[0], o.x, Bf, hoff);
+        t[1] = sr_top(y[1], o.y, Bf, hoff);
+        t[2] = sr_top(y[2], o.z, Bf, hoff);
+        t[3] = sr_top(y[3], o.w, Bf, hoff);
       } else {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) t[j] = rne_top(y[j], Bf, hoff);
+      }
+      const bool in = ok && full;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) tcodes[j][r >> 2] = insert_top(tcodes[j][r >> 2], in ? t[j] : 0, r & 3);
+    } else {
+      int code[4];
+      const uint64_t ebase = (uint64_t)(uint32_t)src * (uint64_t)p.cols + (uint64_t)c0;
+      if (p.stoch) {
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           const uint64_t e = ebase + j;
           const u32x4 o = philox_block(e, p.seed, p.stream);
           code[j] = sr_code(s * (g[r][j] - z), philox_word(o, (int)(e & 3)), B);
         }
+      } else {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) code[j] = rne_code(s * (g[r][j] - z), B);
       }
-    } else {
 #pragma unroll
-      for (int j = 0; j < 4; ++j) code[j] = rne_code(s * (g[r][j] - z), B);
-    }
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int qv = (ok && c0 + j < p.cols) ? code[j] - half : 0;
-      tcodes[j][r >> 2] |= (uint32_t)(qv & 255) << (8 * (r & 3));
+      for (int j = 0; j < 4; ++j) {
+        const int qv = (ok && c0 + j < p.cols) ? code[j] - half : 0;
+        tcodes[j][r >> 2] |= (uint32_t)(qv & 255) << (8 * (r & 3));
+      }
     }
   }
   const bool tvec = ((p.ldt & 15) == 0) && (r0 + 15 < p.ldt);
@@ -223,6 +252,9 @@ static hipError_t launch_narrow_lpr(const NarrowQParams& p, int lpr, dim3 grid, 
 
 hipError_t launch_quant_narrow_t(const NarrowQParams& p, hipStream_t s) {
   if (p.blk < 1 || p.vblk < 0 || p.vblk > p.blk) return hipErrorInvalidValue;
+  // the kernel keeps row indices in 32 bits
+  if (p.ldt + 4096 >= (1ll << 31) || p.rows + p.blk >= (1ll << 31) || p.cols >= (1ll << 31) || p.ldt < p.rows)
+    return hipErrorInvalidValue;
   if (p.gw > 0 && (p.gw < 16 || p.blk < 128 || p.gwo > p.gw || p.gho * p.gw > p.blk)) return hipErrorInvalidValue;
   // lanes per row: the smallest power of two covering cols / 4, at most 64
   // (wider rows: column chunks of 256 along grid.y)

@@ -136,6 +136,11 @@ __device__ __forceinline__ uint32_t pack_top4(int32_t a, int32_t b, int32_t c, i
   const uint32_t hi = __builtin_amdgcn_perm((uint32_t)d, (uint32_t)c, 0x07030c0cu);
   return lo | hi;
 }
+// w with byte b replaced by the top byte of v (b is a constant after unrolling).
+__device__ __forceinline__ uint32_t insert_top(uint32_t w, int32_t v, int b) {
+  const uint32_t sel = b == 0 ? 0x03020107u : (b == 1 ? 0x03020700u : (b == 2 ? 0x03070100u : 0x07020100u));
+  return __builtin_amdgcn_perm((uint32_t)v, w, sel);
+}
 // Sum of the four signed bytes of w, added to acc.
 __device__ __forceinline__ int32_t sum4_i8(uint32_t w, int32_t acc) {
   return __builtin_amdgcn_sdot4((int)w, 0x01010101, acc, false);

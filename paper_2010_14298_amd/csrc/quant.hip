@@ -681,11 +681,6 @@ __device__ __forceinline__ int32_t wave_sum4(int32_t (&v)[4]) {
   return s;
 }
 
-// w with byte b replaced by the top byte of v (b is a constant after unrolling).
-__device__ __forceinline__ uint32_t insert_top(uint32_t w, int32_t v, int b) {
-  const uint32_t sel = b == 0 ? 0x03020107u : (b == 1 ? 0x03020700u : (b == 2 ? 0x03070100u : 0x07020100u));
-  return __builtin_amdgcn_perm((uint32_t)v, w, sel);
-}
 
 // Tile = 64 slots x 256 columns; 4 waves of 16 slots; 4 columns per lane.
 // The loaded tile stays in registers; each row is then finished in one step
