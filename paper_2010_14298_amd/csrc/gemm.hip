@@ -215,67 +215,127 @@ __global__ __launch_bounds__(C::THREADS) void gemm_i8_kernel(GemmParams p) {
       }
     }
     __syncthreads();
-    // Thread t owns column t % BN and the 64-row runs t / BN, t / BN + THREADS / BN, ...
-    // A run is 64 rows, so every group (KG <= 64, aligned) lies inside one.
-    constexpr int NRUN = C::BM / 64;
-    constexpr int RSTEP = C::THREADS / C::BN;
-    const int c = tid % C::BN;
-    const int64_t col = n0 + c;
-    if (col >= p.N) return;
-    // sum over K of the dequantized weight column: dW * sum q_W + K zW
-    const double colterm = dW * (double)p.sumB[col] + (double)p.K * zW;
-    for (int run = tid / C::BN; run < NRUN; run += RSTEP) {
-      const int rbase = run * 64;
-      if constexpr (EPI == EPI_BHQ && KG > 1) {
-        for (int g0 = rbase; g0 < rbase + 64; g0 += KG) {
-          // Row p of a group: T_p = (code_p + c_g) . W~ = dW a_p + rterm_p + hz colterm;
-          // the Householder sum S = sum of T_p over its m rows, with the
-          // accumulators summed exactly in int64.
-          const GroupStage gs = sgrp[g0 / KG];
-          const double hz = srow[g0].hz;
-          double tau = 0.0, alpha = 0.0;
-          if (gs.m > 0) {
-            int64_t asum = 0;
-            if (gs.m == KG) {
-              // four independent partial sums (integer: the order is free)
-              int64_t s4[4] = {0, 0, 0, 0};
+    // Wave w takes the (64-row run, 64-column half) units w, w + WAVES, ...;
+    // lane l holds the four columns 4 (l % 16) .. +3 of the half and rows
+    // 4 i + l / 16 of the run, so one step covers four rows with 16-byte
+    // loads and stores.  A BHQ group of KG rows (KG <= 64, aligned) lies
+    // inside its run; its accumulator column sums meet across the row lanes
+    // (the lanes that share the columns) by xor shuffles.
+    constexpr int NRUN = C::BM / 64, NHALF = C::BN / 64;
+    const int cq = lane & 15, rsub = lane >> 4;
+    const bool al = (p.ldo & 3) == 0 && (((uintptr_t)p.out | (uintptr_t)p.mask) & 15) == 0;
+    for (int u = wave; u < NRUN * NHALF; u += C::WAVES) {
+      const int rbase = (u / NHALF) * 64;
+      const int cb = (u % NHALF) * 64 + 4 * cq;  // tile column of this lane's first column
+      const int64_t col = n0 + cb;
+      if (col >= p.N) continue;  // the shuffle partners share the columns
+      const bool vec = al && col + 3 < p.N;
+      // sum over K of the dequantized weight column: dW * sum q_W + K zW
+      double colterm[4];
 #pragma unroll
-              for (int t = 0; t < KG; ++t) s4[t & 3] += sacc[(g0 + t) * C::BN + c];
-              asum = (s4[0] + s4[1]) + (s4[2] + s4[3]);
-            } else {
-              for (int t = 0; t < gs.m; ++t) asum += sacc[(g0 + t) * C::BN + c];
-            }
-            const double S = dW * (double)asum + (gs.rsum + (double)gs.m * (hz * colterm));
-            const double T0 = dW * (double)sacc[g0 * C::BN + c] + (srow[g0].rterm + hz * colterm);
-            alpha = gs.kind == 2 ? p.L.inv_sk_p : p.L.inv_sk_k;
-            tau = (alpha * S - T0) / (1.0 - alpha);
+      for (int e = 0; e < 4; ++e) colterm[e] = col + e < p.N ? dW * (double)p.sumB[col + e] + (double)p.K * zW : 0.0;
+      auto row_acc = [&](int row, double (&a)[4]) {
+        const int4 v = *reinterpret_cast<const int4*>(&sacc[row * C::BN + cb]);
+        a[0] = (double)v.x;
+        a[1] = (double)v.y;
+        a[2] = (double)v.z;
+        a[3] = (double)v.w;
+      };
+      auto put = [&](int64_t obase, const double (&v)[4]) {
+        const int64_t idx = obase + col;
+        if (vec) {
+          float4 f = make_float4((float)v[0], (float)v[1], (float)v[2], (float)v[3]);
+          if (p.mask) {
+            const float4 m = *reinterpret_cast<const float4*>(p.mask + idx);
+            f.x = m.x > 0.0f ? f.x : 0.0f;
+            f.y = m.y > 0.0f ? f.y : 0.0f;
+            f.z = m.z > 0.0f ? f.z : 0.0f;
+            f.w = m.w > 0.0f ? f.w : 0.0f;
           }
-          const double up0 = (1.0 - alpha) * tau, dn = alpha * tau;
-#pragma unroll 8
-          for (int t = 0; t < KG; ++t) {
-            const RowStage q = srow[g0 + t];
-            if (q.obase < 0) continue;
-            const double a = (double)sacc[(g0 + t) * C::BN + c];
-            double v;
-            if (t < gs.m) {
-              const double T = dW * a + (q.rterm + q.hz * colterm);
-              v = (t == 0 ? T + up0 : T - dn) * q.dq;
-            } else {
-              v = q.dq * (dW * a + q.rterm) + q.hz * colterm;
+          *reinterpret_cast<float4*>(p.out + idx) = f;
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            if (col + e < p.N) store_masked(p, idx + e, v[e]);
+        }
+      };
+      if constexpr (EPI == EPI_BHQ && KG > 1) {
+        constexpr int RB = KG > 4 ? KG : 4;  // rows per block of steps: one group, or 4 / KG groups
+        for (int blk = rbase; blk < rbase + 64; blk += RB) {
+          const int g0 = (blk + rsub) & ~(KG - 1);  // first row of this lane's group
+          const GroupStage gs = sgrp[g0 / KG];
+          // Row t of a group: T_t = (code_t + c_g) . W~ = dW a_t + rterm_t + hz colterm;
+          // the Householder sum S = sum of T_t over its m rows, with the
+          // accumulators summed exactly (integers below 2^53 in float64)
+          double asum[4] = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll
+          for (int i = 0; i < RB / 4; ++i) {
+            const int row = blk + 4 * i + rsub;
+            if (row - g0 < gs.m) {
+              double a[4];
+              row_acc(row, a);
+#pragma unroll
+              for (int e = 0; e < 4; ++e) asum[e] += a[e];
             }
-            store_masked(p, q.obase + col, v);
+          }
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            asum[e] += __shfl_xor(asum[e], 16);
+            if constexpr (KG >= 4) asum[e] += __shfl_xor(asum[e], 32);
+          }
+          const double hz = srow[g0].hz;
+          double up0[4] = {0.0, 0.0, 0.0, 0.0}, dn[4] = {0.0, 0.0, 0.0, 0.0};
+          if (gs.m > 0) {
+            double a0[4];
+            row_acc(g0, a0);
+            const double alpha = gs.kind == 2 ? p.L.inv_sk_p : p.L.inv_sk_k;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const double S = dW * asum[e] + (gs.rsum + (double)gs.m * (hz * colterm[e]));
+              const double T0 = dW * a0[e] + (srow[g0].rterm + hz * colterm[e]);
+              const double tau = (alpha * S - T0) / (1.0 - alpha);
+              up0[e] = (1.0 - alpha) * tau;
+              dn[e] = alpha * tau;
+            }
+          }
+#pragma unroll
+          for (int i = 0; i < RB / 4; ++i) {
+            const int row = blk + 4 * i + rsub;
+            const RowStage q = srow[row];
+            if (q.obase < 0) continue;
+            const int t = row - g0;
+            double a[4], v[4];
+            row_acc(row, a);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              if (t < gs.m) {
+                const double T = dW * a[e] + (q.rterm + q.hz * colterm[e]);
+                v[e] = (t == 0 ? T + up0[e] : T - dn[e]) * q.dq;
+              } else {
+                v[e] = q.dq * (dW * a[e] + q.rterm) + q.hz * colterm[e];
+              }
+            }
+            put(q.obase, v);
           }
         }
       } else {
-#pragma unroll 8
-        for (int t = rbase; t < rbase + 64; ++t) {
-          const RowStage q = srow[t];
+#pragma unroll 4
+        for (int i = 0; i < 16; ++i) {
+          const int row = rbase + 4 * i + rsub;
+          const RowStage q = srow[row];
           if (q.obase < 0) continue;
-          const double a = (double)sacc[t * C::BN + c];
-          if (EPI == EPI_BHQT && q.trow)
-            p.tbuf[q.obase + col] = dW * a + (q.rterm + q.hz * colterm);
-          else
-            store_masked(p, q.obase + col, q.dq * (dW * a + q.rterm) + q.hz * colterm);
+          double a[4], v[4];
+          row_acc(row, a);
+          if (EPI == EPI_BHQT && q.trow) {
+            double* dst = p.tbuf + q.obase + col;
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              if (col + e < p.N) dst[e] = dW * a[e] + (q.rterm + q.hz * colterm[e]);
+            continue;
+          }
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] = q.dq * (dW * a[e] + q.rterm) + q.hz * colterm[e];
+          put(q.obase, v);
         }
       }
     }
