@@ -182,8 +182,22 @@ __device__ void finalize_block(const FinalizePlan& fp, int si) {
   } else if (si == fp.row_seg) {
     for (int64_t r = t; r < g.rows; r += blockDim.x) {
       float rmn = INFINITY, rmx = -INFINITY;
-      for (int64_t c = 0; c < g.chunks; ++c) {
-        const float2 p = g.part[r * g.chunks + c];
+      const float2* pr = g.part + r * g.chunks;
+      // the row's partials eight at a time, all eight loads in flight
+      int64_t c = 0;
+      for (; c + 8 <= g.chunks; c += 8) {
+        float2 q[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) q[u] = pr[c + u];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          if (isnan(q[u].x)) bad = 1;
+          rmn = fminf(rmn, q[u].x);
+          rmx = fmaxf(rmx, q[u].y);
+        }
+      }
+      for (; c < g.chunks; ++c) {
+        const float2 p = pr[c];
         if (isnan(p.x)) bad = 1;
         rmn = fminf(rmn, p.x);
         rmx = fmaxf(rmx, p.y);
