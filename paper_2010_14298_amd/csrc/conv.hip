@@ -747,21 +747,43 @@ __device__ __forceinline__ bool tap_hits(const ConvGeom& g, int iy, int ix, int 
 
 // Row sums of the grad_X A rows: rs[pix][slot] = sum of S_G[pixel][slot]
 // over the output pixels whose taps reach input pixel pix (slot fastest,
-// so a wave reads consecutive words of each tap's S_G run)
+// so a wave reads consecutive words of each tap's S_G run).  Stride 1: the
+// taps' loads go out together (missing taps read entry 0 and add nothing).
+template <bool S1>
 __global__ void conv_rs_kernel(ConvGeom g, const int32_t* sg, int32_t* rs) {
   const uint32_t t = blockIdx.x * blockDim.x + threadIdx.x;
   if (t >= (uint32_t)g.n * (uint32_t)(g.h * g.w)) return;
   const uint32_t pix = t / (uint32_t)g.n, slot = t - pix * (uint32_t)g.n;
   const int iy = (int)(pix / (uint32_t)g.w), ix = (int)pix - iy * g.w;
   int sum = 0;
-  for (int r = 0; r < g.kh; ++r)
-    for (int s = 0; s < g.kw; ++s) {
-      int y, x;
-      if (tap_hits(g, iy, ix, r, s, y, x)) sum += sg[((int64_t)y * g.wo + x) * g.n + slot];
+  if constexpr (S1) {
+    constexpr int U = 8;  // taps per round of loads
+    const int taps = g.kh * g.kw;
+    for (int t0 = 0; t0 < taps; t0 += U) {
+      int v[U];
+      bool ok[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int tap = t0 + u;
+        const int r = tap / g.kw, s = tap - r * g.kw;
+        const int y = iy + g.pad - r, x = ix + g.pad - s;
+        ok[u] = tap < taps && y >= 0 && y < g.ho && x >= 0 && x < g.wo;
+        v[u] = sg[ok[u] ? ((int64_t)y * g.wo + x) * g.n + slot : 0];
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) sum += ok[u] ? v[u] : 0;
     }
+  } else {
+    for (int r = 0; r < g.kh; ++r)
+      for (int s = 0; s < g.kw; ++s) {
+        int y, x;
+        if (tap_hits(g, iy, ix, r, s, y, x)) sum += sg[((int64_t)y * g.wo + x) * g.n + slot];
+      }
+  }
   rs[t] = sum;
 }
 
+template <bool S1>
 __global__ void conv_ct_kernel(ConvGeom g, const int32_t* swq, int32_t* ct, int32_t* cnt) {
   const int64_t hw = (int64_t)g.h * g.w;
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -770,14 +792,36 @@ __global__ void conv_ct_kernel(ConvGeom g, const int32_t* swq, int32_t* ct, int3
   const int c = (int)(t % g.c);
   const int iy = (int)(pix / g.w), ix = (int)(pix % g.w);
   int sum = 0, n = 0;
-  for (int r = 0; r < g.kh; ++r)
-    for (int s = 0; s < g.kw; ++s) {
-      int y, x;
-      if (tap_hits(g, iy, ix, r, s, y, x)) {
-        sum += swq[(int64_t)(r * g.kw + s) * g.c + c];
-        ++n;
+  if constexpr (S1) {
+    constexpr int U = 8;
+    const int taps = g.kh * g.kw;
+    for (int t0 = 0; t0 < taps; t0 += U) {
+      int v[U];
+      bool ok[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int tap = t0 + u;
+        const int r = tap / g.kw, s = tap - r * g.kw;
+        const int y = iy + g.pad - r, x = ix + g.pad - s;
+        ok[u] = tap < taps && y >= 0 && y < g.ho && x >= 0 && x < g.wo;
+        v[u] = swq[ok[u] ? (int64_t)tap * g.c + c : 0];
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        sum += ok[u] ? v[u] : 0;
+        n += ok[u] ? 1 : 0;
       }
     }
+  } else {
+    for (int r = 0; r < g.kh; ++r)
+      for (int s = 0; s < g.kw; ++s) {
+        int y, x;
+        if (tap_hits(g, iy, ix, r, s, y, x)) {
+          sum += swq[(int64_t)(r * g.kw + s) * g.c + c];
+          ++n;
+        }
+      }
+  }
   ct[t] = sum;
   if (c == 0) cnt[pix] = n;
 }
@@ -1267,9 +1311,17 @@ hipError_t launch_conv_gradx_prep(const ConvGeom& g, const int8_t* q2, const int
   hipLaunchKernelGGL(conv_sg_kernel, dim3((unsigned)((n1 + 255) / 256)), dim3(256), 0, s, g, q2, sg);
   const int64_t nr = (int64_t)g.n * g.h * g.w;
   if (nr > 0x7FFFFFFF) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(conv_rs_kernel, dim3((unsigned)((nr + 255) / 256)), dim3(256), 0, s, g, (const int32_t*)sg, rs);
+  if (g.stride == 1)
+    hipLaunchKernelGGL(conv_rs_kernel<true>, dim3((unsigned)((nr + 255) / 256)), dim3(256), 0, s, g, (const int32_t*)sg,
+                       rs);
+  else
+    hipLaunchKernelGGL(conv_rs_kernel<false>, dim3((unsigned)((nr + 255) / 256)), dim3(256), 0, s, g, (const int32_t*)sg,
+                       rs);
   const int64_t n2 = (int64_t)g.h * g.w * g.c;
-  hipLaunchKernelGGL(conv_ct_kernel, dim3((unsigned)((n2 + 255) / 256)), dim3(256), 0, s, g, swq, ct, cnt);
+  if (g.stride == 1)
+    hipLaunchKernelGGL(conv_ct_kernel<true>, dim3((unsigned)((n2 + 255) / 256)), dim3(256), 0, s, g, swq, ct, cnt);
+  else
+    hipLaunchKernelGGL(conv_ct_kernel<false>, dim3((unsigned)((n2 + 255) / 256)), dim3(256), 0, s, g, swq, ct, cnt);
   return hipGetLastError();
 }
 
