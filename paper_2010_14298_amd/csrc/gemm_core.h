@@ -159,16 +159,21 @@ __device__ __forceinline__ int kslot(int r, int c) { return 8 * r + (c ^ ((r >> 
 
 // One stage of the fast loop: wait for this wave's loads of stage t, then the
 // barrier (everyone's have landed, and everyone is done reading the buffer
-// that the loads of stage t + NS - 1 now fill), start those loads, and run
-// the matrix-core work on `cur`, each MFMA followed by one LDS read of the
-// next K step.  `cur` and `nxt` are never the same buffer; the caller passes
-// them as distinct restrict pointers so that the pending loads into `nxt` do
-// not hold up the reads of `cur`.
+// that the loads of stage t + NS - 1 now fill), then the matrix-core work on
+// `cur`, each MFMA followed by one LDS read of the next K step, with this
+// wave's loads of stage t + NS - 1 spread over the MFMAs (one after every
+// second MFMA where there are enough): issued back to back they queue up in
+// the address unit and hold up the MFMA issue behind them.  `cur` and `nxt` are never the same
+// buffer; the caller passes them as distinct restrict pointers so that the
+// pending loads into `nxt` do not hold up the reads of `cur`.
 template <class C>
 __device__ __forceinline__ void dma_stage(const int8_t* __restrict__ cur, int8_t* __restrict__ nxt,
                                           const int8_t* const (&srcA)[C::A_INS], const int8_t* const (&srcB)[C::B_INS],
                                           int64_t t, int64_t nk, v16i (&acc)[C::IT][C::JT]) {
   constexpr int PER = C::A_INS + C::B_INS;
+  constexpr int NMF = C::IT * C::JT * (C::BK / 32);  // MFMAs per stage
+  constexpr int SPREAD = 2 * PER <= NMF ? 2 : 1;  // MFMAs per load slot
+  static_assert(PER <= (NMF + SPREAD - 1) / SPREAD, "every load of a stage gets an MFMA slot");
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int wm = wave / C::WAVES_N, wn = wave % C::WAVES_N;
@@ -177,17 +182,18 @@ __device__ __forceinline__ void dma_stage(const int8_t* __restrict__ cur, int8_t
   else
     __builtin_amdgcn_s_waitcnt(0x3F70);                          // vmcnt(0)
   __builtin_amdgcn_s_barrier();
-  if (t + C::NS - 1 < nk) {
-    const int64_t ko = (t + C::NS - 1) * C::BK;
-#pragma unroll
-    for (int i = 0; i < C::A_INS; ++i)
-      __builtin_amdgcn_global_load_lds((gmem_void*)(srcA[i] + ko), (lmem_void*)(nxt + (wave * C::A_INS + i) * 1024),
-                                       16, 0, 0);
-#pragma unroll
-    for (int i = 0; i < C::B_INS; ++i)
-      __builtin_amdgcn_global_load_lds((gmem_void*)(srcB[i] + ko),
-                                       (lmem_void*)(nxt + C::BM * C::BK + (wave * C::B_INS + i) * 1024), 16, 0, 0);
-  }
+  const bool more = t + C::NS - 1 < nk;
+  const int64_t ko = (t + C::NS - 1) * C::BK;
+  // load q of the next stage (q < A_INS: A, else B), in its MFMA slot
+  auto load = [&](int q) __attribute__((always_inline)) {
+    if (q < C::A_INS)
+      __builtin_amdgcn_global_load_lds((gmem_void*)(srcA[q] + ko), (lmem_void*)(nxt + (wave * C::A_INS + q) * 1024), 16,
+                                       0, 0);
+    else
+      __builtin_amdgcn_global_load_lds((gmem_void*)(srcB[q - C::A_INS] + ko),
+                                       (lmem_void*)(nxt + C::BM * C::BK + (wave * C::B_INS + q - C::A_INS) * 1024), 16,
+                                       0, 0);
+  };
   const int lrow = lane & 31, lh = lane >> 5;
   const int8_t* sa = cur;
   const int8_t* sb = cur + C::BM * C::BK;
@@ -207,16 +213,12 @@ __device__ __forceinline__ void dma_stage(const int8_t* __restrict__ cur, int8_t
 #pragma unroll
     for (int i = 0; i < C::IT; ++i)
 #pragma unroll
-      for (int j = 0; j < C::JT; ++j) acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a[cs][i], b[cs][j], acc[i][j], 0, 0, 0);
+      for (int j = 0; j < C::JT; ++j) {
+        acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a[cs][i], b[cs][j], acc[i][j], 0, 0, 0);
+        const int m = (kk * C::IT + i) * C::JT + j;
+        if (m % SPREAD == 0 && m / SPREAD < PER && more) load(m / SPREAD);
+      }
   }
-  __builtin_amdgcn_sched_group_barrier(0x100, C::IT + C::JT, 0);
-#pragma unroll
-  for (int kk = 0; kk < C::BK / 32; ++kk)
-#pragma unroll
-    for (int m = 0; m < C::IT * C::JT; ++m) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      if (kk + 1 < C::BK / 32 && m < C::IT + C::JT) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-    }
 }
 
 // The fast K loop: operands loaded straight into LDS (global_load_lds_dwordx4,
