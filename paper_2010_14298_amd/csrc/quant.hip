@@ -39,6 +39,28 @@ __device__ __forceinline__ int wave_sum_i(int v) {
   return v;
 }
 
+// Sums over the 64 lanes of each of 4 per-lane values v[0..3], all in
+// vector registers: lanes 32 apart add up with one half-wave swap per pair
+// (v[i] keeps the low half, v[i + 2] the high one), rows of 16 lanes with
+// one row swap, then each row adds up by shifted adds within the row.  Lane
+// l with l % 16 == 15 returns the sum of v[l / 16].
+__device__ __forceinline__ int32_t wave_sum4(int32_t (&v)[4]) {
+  int32_t h[2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const auto sw = __builtin_amdgcn_permlane32_swap(v[i], v[i + 2], false, false);
+    h[i] = (int32_t)sw[0] + (int32_t)sw[1];
+  }
+  const auto sw = __builtin_amdgcn_permlane16_swap(h[0], h[1], false, false);
+  int32_t s = (int32_t)sw[0] + (int32_t)sw[1];
+  // row_shr:n (source lane l - n of the same row; 0 where that leaves the row)
+  s += __builtin_amdgcn_update_dpp(0, s, 0x111, 0xf, 0xf, false);
+  s += __builtin_amdgcn_update_dpp(0, s, 0x112, 0xf, 0xf, false);
+  s += __builtin_amdgcn_update_dpp(0, s, 0x114, 0xf, 0xf, false);
+  s += __builtin_amdgcn_update_dpp(0, s, 0x118, 0xf, 0xf, false);
+  return s;
+}
+
 // Block-wide (min, max, any-bad); every thread gets the result.
 struct MinMax {
   float mn, mx;
@@ -488,14 +510,10 @@ __global__ __launch_bounds__(RK_THREADS) void bhq_rank_perm_kernel(const float* 
 #pragma unroll
     for (int q = 0; q < 4; ++q) cnt[q] += (v.x > mu[q]) + (v.y > mu[q]) + (v.z > mu[q]) + (v.w > mu[q]);
   }
-#pragma unroll
-  for (int q = 0; q < 4; ++q)
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) cnt[q] += __shfl_xor(cnt[q], o);
-  if (lane < 4 && r0 + lane < rows) {
-    const int c = lane == 0 ? cnt[0] : lane == 1 ? cnt[1] : lane == 2 ? cnt[2] : cnt[3];
-    perm[bhq_slot_of_rank(L, c)] = r0 + lane;
-  }
+  // lane 16 q + 15 gets the count of row r0 + q
+  const int c = wave_sum4(cnt);
+  const int q = lane >> 4;
+  if ((lane & 15) == 15 && r0 + q < rows) perm[bhq_slot_of_rank(L, c)] = r0 + q;
 }
 
 // One group of a fixed-block plan, one wave (lane j handles the group's slot
@@ -672,29 +690,6 @@ __device__ __forceinline__ void rne4(const float (&y)[4], float Bf, uint32_t hof
 #pragma unroll
   for (int j = 0; j < 4; ++j) t[j] = rne_top(y[j], Bf, hoff);
 }
-
-// Sums over the 64 lanes of each of 4 per-lane values v[0..3], all in
-// vector registers: lanes 32 apart add up with one half-wave swap per pair
-// (v[i] keeps the low half, v[i + 2] the high one), rows of 16 lanes with
-// one row swap, then each row adds up by shifted adds within the row.  Lane
-// l with l % 16 == 15 returns the sum of v[l / 16].
-__device__ __forceinline__ int32_t wave_sum4(int32_t (&v)[4]) {
-  int32_t h[2];
-#pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const auto sw = __builtin_amdgcn_permlane32_swap(v[i], v[i + 2], false, false);
-    h[i] = (int32_t)sw[0] + (int32_t)sw[1];
-  }
-  const auto sw = __builtin_amdgcn_permlane16_swap(h[0], h[1], false, false);
-  int32_t s = (int32_t)sw[0] + (int32_t)sw[1];
-  // row_shr:n (source lane l - n of the same row; 0 where that leaves the row)
-  s += __builtin_amdgcn_update_dpp(0, s, 0x111, 0xf, 0xf, false);
-  s += __builtin_amdgcn_update_dpp(0, s, 0x112, 0xf, 0xf, false);
-  s += __builtin_amdgcn_update_dpp(0, s, 0x114, 0xf, 0xf, false);
-  s += __builtin_amdgcn_update_dpp(0, s, 0x118, 0xf, 0xf, false);
-  return s;
-}
-
 
 // Tile = 64 slots x 256 columns; 4 waves of 16 slots; 4 columns per lane.
 // The loaded tile stays in registers; each row is then finished in one step
