@@ -38,7 +38,7 @@ using CfgLarge = TileCfg<256, 128, 64, 64, 128, 3>;
 using CfgSmall = TileCfg<128, 128, 32, 64, 128, 4>;
 // at most 64 rows (the conv grad_W contraction over output channels): no
 // half-empty 128-row tiles
-using CfgNarrow = TileCfg<64, 128, 32, 64, 128, 4>;
+using CfgNarrow = TileCfg<64, 128, 32, 64, 128, 3>;
 
 typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
 struct alignas(16) Chunk16 {
