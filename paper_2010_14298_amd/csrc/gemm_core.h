@@ -369,9 +369,49 @@ __device__ __forceinline__ void generic_mainloop_km(const GemmParams& p, const A
   // loop body has no branches and the compiler's count of loads in flight
   // stays exact across iterations: the stores of stage t + 1 wait for its
   // own loads only, while those of stage t + 2 stay in flight.
+  // The loads of stage t + 2 go out between the MFMAs of stage t (one after
+  // each MFMA, or after every second when there are twice as many MFMAs):
+  // issued as one burst they queue in the address unit and hold up the
+  // MFMAs behind them.
+  constexpr int NLD = C::A_CHUNKS + C::B_CHUNKS;
+  constexpr int NMF = C::IT * C::JT * (C::BK / 32);
+  constexpr int SPREAD = 2 * NLD <= NMF ? 2 : 1;
   auto iter = [&](int64_t t, int buf, Stage& next, Stage& far) __attribute__((always_inline)) {
-    gload(far, t + 2);
-    compute(buf);
+    if constexpr (NLD <= (NMF + SPREAD - 1) / SPREAD) {
+      const int64_t k0 = km.k(t + 2);
+      const typename ALoader::KState ks = aload.kstate(k0 + kch);
+      auto load = [&](int q) __attribute__((always_inline)) {
+        if (q < C::A_CHUNKS) {
+          const Chunk16 v = aload.load(arow[q], ks);
+          far.a[q] = u32x4v{v.w[0], v.w[1], v.w[2], v.w[3]};
+        } else {
+          const int c = tid + C::THREADS * (q - C::A_CHUNKS);
+          const Chunk16 v = bload.load(n0 + c / C::KCH, k0 + 16 * (c % C::KCH));
+          far.b[q - C::A_CHUNKS] = u32x4v{v.w[0], v.w[1], v.w[2], v.w[3]};
+        }
+      };
+      const int8_t* a_base = a_lane + buf * C::BM * C::LDS_STRIDE;
+      const int8_t* b_base = b_lane + buf * C::BN * C::LDS_STRIDE;
+#pragma unroll
+      for (int kk = 0; kk < C::BK / 32; ++kk) {
+        v4i a[C::IT], b[C::JT];
+#pragma unroll
+        for (int i = 0; i < C::IT; ++i) a[i] = *reinterpret_cast<const v4i*>(a_base + i * 32 * C::LDS_STRIDE + kk * 32);
+#pragma unroll
+        for (int j = 0; j < C::JT; ++j) b[j] = *reinterpret_cast<const v4i*>(b_base + j * 32 * C::LDS_STRIDE + kk * 32);
+#pragma unroll
+        for (int i = 0; i < C::IT; ++i)
+#pragma unroll
+          for (int j = 0; j < C::JT; ++j) {
+            acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a[i], b[j], acc[i][j], 0, 0, 0);
+            const int m = (kk * C::IT + i) * C::JT + j;
+            if (m % SPREAD == 0 && m / SPREAD < NLD) load(m / SPREAD);
+          }
+      }
+    } else {
+      gload(far, t + 2);
+      compute(buf);
+    }
     sstore(next, buf ^ 1);
     __syncthreads();
   };
